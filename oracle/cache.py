@@ -1,0 +1,89 @@
+"""Whole-layer quantization into the packed cache buffers, and decode over them.
+
+Builds exactly the byte contents the GPU library writes for a layer
+([B][Hkv] sequences of keys and values, a modality map, per-sequence lengths),
+from the FMT codecs of ``keys`` and ``values`` and the pack maps of ``layout``.
+Slots beyond a sequence's length are zero. Appending a sequence in chunks must
+give the same bytes as this one-shot quantization of the concatenation
+(reading of the cache reuse of Sec. 2.1 and the streaming protocol of Sec. 3.1).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+from .attention import decode_bruteforce, decode_dense, decode_rotated
+from .keys import quantize_keys_fmt
+from .layout import WINDOW, pack_keys, pack_values, unpack_keys, unpack_values
+from .values import quantize_values_fmt
+
+
+def quantize_layer(k, v, modality, lens, signs, rot, capacity=None):
+    """Dict of packed buffers (numpy) for k, v [B][H][N][d] fp16, modality [B][N], lens [B]."""
+    B, H, N, D = k.shape
+    cap = int(capacity or -(-N // WINDOW) * WINDOW)
+    nw = cap // WINDOW
+    out = dict(
+        k_codes=np.zeros((B, H, cap, D // 4), np.uint8),
+        v_codes=np.zeros((B, H, nw, 1024), np.uint8),
+        k_norm=np.zeros((B, H, cap), np.float16),
+        v_norm=np.zeros((B, H, cap), np.float16),
+        k_min=np.zeros((B, H, nw, D), np.float16),
+        k_step=np.zeros((B, H, nw, D), np.float16),
+        modality=np.zeros((B, cap), np.uint8),
+    )
+    for b in range(B):
+        L = int(lens[b])
+        out["modality"][b, :L] = modality[b, :L]
+        for h in range(H):
+            kq = quantize_keys_fmt(k[b, h], L, signs)
+            npad = kq["codes"].shape[0]
+            out["k_codes"][b, h, :npad] = pack_keys(kq["codes"])
+            out["k_norm"][b, h, :npad] = kq["n16"]
+            out["k_min"][b, h, :npad // WINDOW] = kq["m16"]
+            out["k_step"][b, h, :npad // WINDOW] = kq["step16"]
+            vq = quantize_values_fmt(v[b, h], modality[b], rot, L)
+            vcodes = np.zeros((npad, D), np.uint8)
+            vcodes[:L] = vq["codes"]
+            out["v_codes"][b, h, :npad // WINDOW] = pack_values(vcodes)
+            out["v_norm"][b, h, :L] = vq["n16"]
+    return out
+
+
+def unpacked_fields(cache, b, h):
+    """(kc, m16, st16, nk, vc, nv, modality) for one sequence and KV head of a packed cache."""
+    return (unpack_keys(cache["k_codes"][b, h]), cache["k_min"][b, h], cache["k_step"][b, h],
+            cache["k_norm"][b, h], unpack_values(cache["v_codes"][b, h]), cache["v_norm"][b, h],
+            cache["modality"][b])
+
+
+def decode_layer(cache, q16, lens, signs, rot, sm_scale, rotated=True, heads=None):
+    """fp64 outputs [B][Hq][d] of one decode step over a packed cache.
+
+    ``heads`` optionally restricts the work to a list of (b, kv head) pairs; other rows are NaN.
+    """
+    B, Hq, D = q16.shape
+    H = cache["k_codes"].shape[1]
+    G = Hq // H
+    out = np.full((B, Hq, D), np.nan)
+    fn = decode_rotated if rotated else decode_bruteforce
+    for b in range(B):
+        for h in range(H):
+            if heads is not None and (b, h) not in heads:
+                continue
+            kc, m16, st16, nk, vc, nv, mod = unpacked_fields(cache, b, h)
+            out[b, h * G:(h + 1) * G] = fn(q16[b, h * G:(h + 1) * G], kc, m16, st16, nk, vc, nv, mod,
+                                           lens[b], signs, rot, sm_scale, G)
+    return out
+
+
+def decode_layer_dense(k16, v16, q16, lens, sm_scale):
+    B, Hq, D = q16.shape
+    H = k16.shape[1]
+    G = Hq // H
+    out = np.zeros((B, Hq, D))
+    for b in range(B):
+        for h in range(H):
+            out[b, h * G:(h + 1) * G] = decode_dense(q16[b, h * G:(h + 1) * G], k16[b, h], v16[b, h],
+                                                     lens[b], sm_scale, G)
+    return out
