@@ -1,0 +1,177 @@
+/*
+ * okvq.h -- C ABI of the OmniKVQuant 2-bit KV-cache hot path for AMD Instinct MI355X (gfx950).
+ *
+ * The method (arXiv 2609.11582, "OmniKVQuant: KV Cache Quantization for Omni-LLMs"):
+ *   keys   -- per-token norm split and randomized Hadamard rotation (Sec. 2.1, Eq. 2), then
+ *             min / step per group of 32 consecutive tokens and channel (Sec. 2.3, Eq. 4),
+ *             2-bit codes;
+ *   values -- per-token norm split, rotation by a per-modality orthogonal matrix R_m
+ *             (audio / video / text; Sec. 2.3, Eq. 6), 2-bit codes of the fixed Gaussian
+ *             codebook (Eq. 3);
+ *   decode -- softmax attention of one query per head over the packed cache (Eq. 1), scoring
+ *             in the rotated key space after rotating the query once per head, and applying
+ *             the inverse value rotation once per modality after aggregation (Sec. 2.3).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - head_dim must be 128 and window 32; 1 <= num_q_heads / num_kv_heads <= 8 with
+ *   num_q_heads a multiple of num_kv_heads (query head j reads KV head j / G).
+ * - Every array argument named "device" is device memory of the current HIP device, caller
+ *   owned and 16-byte aligned. fp16 data is passed as uint16_t bit patterns (IEEE binary16).
+ * - The library allocates no memory, keeps no state between calls, never synchronizes and
+ *   never copies between host and device: each call validates its arguments on the host and
+ *   then enqueues kernels on `stream` (a hipStream_t; NULL is the default stream).
+ * - Argument errors are detected before anything is enqueued: the call returns a negative
+ *   status and writes nothing. A failed kernel launch returns OKVQ_ERR_HIP.
+ * - Device data contract: inputs are finite and modality ids are 0, 1 or 2. Violations give
+ *   unspecified (but memory-safe) results; there is no device-side error channel.
+ * - Host "lens" arrays plan the launches; the kernels read lengths on the device where noted.
+ *   Callers keep the two equal.
+ *
+ * Cache layout (per layer; B = batch, H = num_kv_heads, cap = capacity, a multiple of 32)
+ * ------------------------------------------------------------------------------------------
+ *   k_codes  u8  [B][H][cap][32]      token i, channel c -> byte 32i + c/4, bits 2(c%4)..+1
+ *   v_codes  u8  [B][H][cap/32][1024] window token t, channel c -> byte
+ *                                      16*((c%16) + 16*((t/4)%4)) + 8*(t/16) + c/16,
+ *                                      bits 2(t%4)..+1 (one channel of 4 consecutive tokens)
+ *   k_norm   f16 [B][H][cap]          fp16 ||k||
+ *   v_norm   f16 [B][H][cap]          fp16 ||v||
+ *   k_min    f16 [B][H][cap/32][128]  per (window, channel) minimum of the rotated key direction
+ *   k_step   f16 [B][H][cap/32][128]  per (window, channel) step = (max - min) / 3
+ *   modality u8  [B][cap]             0 audio, 1 video, 2 text
+ *   k_stage  f16 [B][H][32][128]      raw keys of the open (partial) window, used by append
+ *   seq_lens i32 [B]                  current lengths (device copy)
+ * Slots of the last window beyond a sequence's length hold code 0 and norm 0.
+ * Storage is 84 bytes per token per KV head: 2.625 bits per element, the "FP16 meta." row of
+ * the paper's Tab. 3.
+ */
+#ifndef OKVQ_H
+#define OKVQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t okvq_status;
+enum {
+  OKVQ_OK = 0,
+  OKVQ_ERR_INVALID_ARGUMENT = -1, /* null / misaligned pointer, bad size or length           */
+  OKVQ_ERR_UNSUPPORTED = -2,      /* head_dim != 128, window != 32, group size outside 1..8  */
+  OKVQ_ERR_CAPACITY = -3,         /* a length (or length + appended tokens) exceeds capacity */
+  OKVQ_ERR_WORKSPACE = -4,        /* decode workspace missing or too small                   */
+  OKVQ_ERR_HIP = -5               /* a HIP launch failed                                     */
+};
+
+enum { OKVQ_MOD_AUDIO = 0, OKVQ_MOD_VIDEO = 1, OKVQ_MOD_TEXT = 2, OKVQ_NUM_MODALITIES = 3 };
+
+/* flags */
+enum {
+  OKVQ_VALUE_EXACT = 1u << 0 /* value rotation as a sequential fp32 dot product (bit-exact codes) */
+};
+
+/* which_buffer for okvq_buffer_bytes */
+enum {
+  OKVQ_BUF_K_CODES = 0, OKVQ_BUF_V_CODES, OKVQ_BUF_K_NORM, OKVQ_BUF_V_NORM, OKVQ_BUF_K_MIN,
+  OKVQ_BUF_K_STEP, OKVQ_BUF_MODALITY, OKVQ_BUF_K_STAGE, OKVQ_BUF_SEQ_LENS, OKVQ_NUM_BUFFERS
+};
+
+typedef struct {
+  int32_t batch;        /* B                                        */
+  int32_t num_kv_heads; /* H                                        */
+  int32_t num_q_heads;  /* Hq, a multiple of H, Hq / H <= 8         */
+  int32_t head_dim;     /* must be 128                              */
+  int32_t window;       /* key group size, must be 32 (Sec. 3.1)    */
+  int32_t capacity;     /* token slots per sequence, multiple of 32 */
+} okvq_dims;
+
+typedef struct {               /* all pointers are device memory, laid out as above */
+  okvq_dims dims;
+  uint8_t* k_codes;
+  uint8_t* v_codes;
+  uint16_t* k_norm;
+  uint16_t* v_norm;
+  uint16_t* k_min;
+  uint16_t* k_step;
+  uint8_t* modality;
+  uint16_t* k_stage;
+  int32_t* seq_lens;
+  const int8_t* key_signs;     /* [128] +1 / -1: H = Had diag(s) / sqrt(128) (Eq. 2)        */
+  const float* v_rot;          /* [3][128][128] fp32 row-major R_m, z = R_m u (Eq. 6)       */
+} okvq_cache;
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+int32_t okvq_version(void);
+
+/* Human-readable name of a status code (static string). */
+const char* okvq_status_string(okvq_status status);
+
+/* Bytes of one cache buffer for `dims` (0 for an unknown buffer or invalid dims). */
+size_t okvq_buffer_bytes(const okvq_dims* dims, int32_t which_buffer);
+
+/* Fixed Gaussian codebook of Eq. 3 as used by the kernels: the 4 levels and 3 decision
+ * thresholds of the Lloyd-Max quantizer of N(0, 1/128), computed by the library on the host.
+ * levels: host float[4]; thresholds: host float[3]. */
+okvq_status okvq_codebook(float* levels, float* thresholds);
+
+/* Quantize keys (Eq. 2 then Eq. 4) of a dense block into cache-layout buffers.
+ *   k          device f16 [B][H][n_tokens][128]; token i of sequence b is valid if i < lens_host[b]
+ *   lens_host  host i32 [B], 0 <= lens_host[b] <= min(n_tokens, capacity)
+ *   key_signs  device i8 [128]
+ *   outputs    device k_codes, k_min, k_step, k_norm in the cache layout of dims->capacity;
+ *              windows are aligned to token 0; a partial last window takes its min/step over
+ *              its valid tokens; its padded slots get code 0 and norm 0. Nothing beyond the
+ *              last window of each sequence is written.
+ * Bit-exact contract: norms, min, step and codes equal the documented fp32 operation order. */
+okvq_status okvq_quantize_keys(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens,
+                               const int32_t* lens_host, const int8_t* key_signs, uint8_t* k_codes,
+                               uint16_t* k_min, uint16_t* k_step, uint16_t* k_norm, void* stream);
+
+/* Quantize values (Eq. 6 with the codebook of Eq. 3) of a dense block into cache-layout buffers.
+ *   v          device f16 [B][H][n_tokens][128]
+ *   modality   device u8 [B][n_tokens] (0 audio, 1 video, 2 text)
+ *   v_rot      device f32 [3][128][128], R_m row-major
+ *   flags      OKVQ_VALUE_EXACT: y = R_m v as a sequential fp32 dot product (codes bit-exact with
+ *              the documented order); otherwise MFMA with an fp16 hi/lo split of R_m and fp32
+ *              accumulation (codes may differ from the exact order only where y lies within a
+ *              small band around a decision threshold).
+ *   outputs    device v_codes, v_norm in the cache layout (whole 32-token windows are written;
+ *              slots beyond a length get code 0 and norm 0). */
+okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const uint8_t* modality,
+                                 int32_t n_tokens, const int32_t* lens_host, const float* v_rot,
+                                 uint32_t flags, uint8_t* v_codes, uint16_t* v_norm, void* stream);
+
+/* Append n_new[b] tokens to every sequence of a cache (prefill is an append to an empty cache).
+ *   lens_host  host i32 [B] current lengths (equal to cache->seq_lens on the device)
+ *   k_new,v_new device f16 [B][H][n_max][128]; mod_new device u8 [B][n_max]
+ *   n_new_host host i32 [B], n_new_dev the same values in device memory, 0 <= n_new <= n_max
+ * The open key window is re-quantized from the staged raw keys plus the new ones, so any
+ * chunking of a sequence yields the same cache bytes as one quantization of the whole sequence.
+ * cache->seq_lens[b] is advanced by n_new[b] on the device. Fails with OKVQ_ERR_CAPACITY if
+ * lens_host[b] + n_new_host[b] > capacity. */
+okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
+                        const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
+                        const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream);
+
+/* Device workspace bytes needed by okvq_decode_attention for sequences up to max_seq_len. */
+size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len);
+
+/* One decode step: attention of one query per head over the packed cache (Eq. 1).
+ *   lens_host  host i32 [B] (plans the split-K launch; the kernels read cache->seq_lens)
+ *   q          device f16 [B][Hq][128]
+ *   sm_scale   softmax scale, normally 1/sqrt(128)
+ *   out        device f32 [B][Hq][128]
+ *   workspace  device, at least okvq_decode_workspace_bytes(dims, max(lens_host)) bytes
+ * A sequence of length 0 yields zeros. fp32 accumulation; the result matches float64 attention
+ * over the dequantized cache within 2e-3 of the output norm. */
+okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,
+                                  float sm_scale, uint32_t flags, float* out, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OKVQ_H */

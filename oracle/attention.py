@@ -15,6 +15,7 @@ Two formulations are given, which agree in exact arithmetic:
   o = sum_m R_m^T acc_m / sum_i p_i.
 
 GQA reading (R11): query head j reads KV head j // G with G = Hq / Hkv.
+An empty cache (length 0) has no softmax; its output is defined as zeros.
 """
 
 from __future__ import annotations
@@ -37,6 +38,8 @@ def softmax_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, sm_scale: flo
 def decode_bruteforce(q16, kc, m16, st16, nk, vc, nv, modality, length, signs, rot, sm_scale, group):
     """o [G][d] for the G query heads q16 [G][d] sharing one KV head (unpacked cache fields)."""
     L = int(length)
+    if L == 0:
+        return np.zeros((group, q16.shape[-1]))
     khat = dequantize_keys(kc[:L], m16, st16, nk[:L], signs)
     vhat = dequantize_values(vc[:L], nv[:L], modality[:L], rot)
     return np.stack([softmax_attention(q16[j], khat, vhat, sm_scale) for j in range(group)])
@@ -45,6 +48,8 @@ def decode_bruteforce(q16, kc, m16, st16, nk, vc, nv, modality, length, signs, r
 def decode_rotated(q16, kc, m16, st16, nk, vc, nv, modality, length, signs, rot, sm_scale, group):
     """Same as ``decode_bruteforce`` in the rotated-space order of the fused kernel."""
     L = int(length)
+    if L == 0:
+        return np.zeros((group, q16.shape[-1]))
     hm = randomized_hadamard(signs)
     cb, _ = codebook(kc.shape[1])
     zhat = dequantize_directions(kc[:L], m16, st16)
@@ -70,4 +75,6 @@ def decode_rotated(q16, kc, m16, st16, nk, vc, nv, modality, length, signs, rot,
 def decode_dense(q16, k16, v16, length, sm_scale, group):
     """Unquantized fp16 cache: o [G][d] (the dense baseline's reference)."""
     L = int(length)
+    if L == 0:
+        return np.zeros((group, q16.shape[-1]))
     return np.stack([softmax_attention(q16[j], k16[:L], v16[:L], sm_scale) for j in range(group)])

@@ -1,0 +1,10 @@
+"""OmniKVQuant 2-bit KV-cache hot path for AMD MI355X (gfx950).
+
+The computation lives in libokvq.so (hand-written HIP kernels behind the C ABI of
+include/okvq.h); ``okvq`` is its ctypes binding.
+"""
+
+from . import okvq  # noqa: F401
+from .okvq import (KVCache, OkvqError, make_dims, okvq_append, okvq_buffer_bytes, okvq_codebook,  # noqa: F401
+                   okvq_decode_attention, okvq_decode_workspace_bytes, okvq_quantize_keys, okvq_quantize_values,
+                   okvq_version, status_string)

@@ -1,0 +1,291 @@
+// C ABI of the okvq library: argument validation, launch planning and the fixed codebook.
+// Declarations and contracts: include/okvq.h.
+#include <cmath>
+#include <cstring>
+
+#include "okvq.h"
+#include "launch.hpp"
+
+using namespace okvq;
+
+namespace {
+
+constexpr int32_t kVersion = 100;  // 0.1.0
+
+// ---- fixed Gaussian codebook (Sec. 2.1, Eq. 3): Lloyd-Max quantizer of N(0, 1), 4 levels ----
+double phi(double x) { return std::isinf(x) ? 0.0 : std::exp(-0.5 * x * x) / std::sqrt(2.0 * M_PI); }
+double cdf(double x) {
+  if (std::isinf(x)) return x < 0 ? 0.0 : 1.0;
+  return 0.5 * std::erfc(-x / std::sqrt(2.0));
+}
+
+struct Codebook {
+  float level[4];      // levels of N(0, 1/128), fp32
+  float thr[3];        // decision thresholds (midpoints), fp32
+  uint16_t level16[4]; // fp16 levels used by the decode kernel
+};
+
+Codebook make_codebook() {
+  // Lloyd iteration: thresholds are midpoints of neighbouring levels, levels are the centroids
+  // of their cells (closed form for a Gaussian density).
+  double c[4] = {-1.5, -0.5, 0.5, 1.5};
+  for (int it = 0; it < 100000; ++it) {
+    const double t[3] = {(c[0] + c[1]) / 2, (c[1] + c[2]) / 2, (c[2] + c[3]) / 2};
+    const double e[5] = {-INFINITY, t[0], t[1], t[2], INFINITY};
+    double delta = 0.0;
+    for (int i = 0; i < 4; ++i) {
+      const double n = (phi(e[i]) - phi(e[i + 1])) / (cdf(e[i + 1]) - cdf(e[i]));
+      delta = std::fmax(delta, std::fabs(n - c[i]));
+      c[i] = n;
+    }
+    if (delta < 1e-15) break;
+  }
+  double s[4];
+  for (int i = 0; i < 4; ++i) s[i] = (c[i] - c[3 - i]) / 2;  // exact symmetry of the density
+  const double sc = 1.0 / std::sqrt(128.0);
+  Codebook cb;
+  for (int i = 0; i < 4; ++i) {
+    cb.level[i] = (float)(s[i] * sc);
+    cb.level16[i] = __builtin_bit_cast(uint16_t, (_Float16)(s[i] * sc));
+  }
+  for (int i = 0; i < 3; ++i) cb.thr[i] = (float)(((s[i] + s[i + 1]) / 2) * sc);
+  return cb;
+}
+
+const Codebook& codebook() {
+  static const Codebook cb = make_codebook();
+  return cb;
+}
+
+Thresholds thresholds() {
+  const Codebook& cb = codebook();
+  return Thresholds{cb.thr[0], cb.thr[1], cb.thr[2]};
+}
+
+bool aligned16(const void* p) { return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+okvq_status check_dims(const okvq_dims* d) {
+  if (!d) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (d->head_dim != 128 || d->window != 32) return OKVQ_ERR_UNSUPPORTED;
+  if (d->batch < 1 || d->num_kv_heads < 1 || d->num_q_heads < 1) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (d->num_q_heads % d->num_kv_heads != 0) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (d->num_q_heads / d->num_kv_heads > 8) return OKVQ_ERR_UNSUPPORTED;
+  if (d->capacity < 32 || d->capacity % 32 != 0) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (d->batch > 65535 || d->num_kv_heads > 65535) return OKVQ_ERR_UNSUPPORTED;
+  return OKVQ_OK;
+}
+
+okvq_status check_cache(const okvq_cache* c) {
+  if (!c) return OKVQ_ERR_INVALID_ARGUMENT;
+  okvq_status st = check_dims(&c->dims);
+  if (st != OKVQ_OK) return st;
+  const void* ptrs[] = {c->k_codes, c->v_codes, c->k_norm, c->v_norm, c->k_min, c->k_step,
+                        c->modality, c->k_stage, c->seq_lens, c->key_signs, c->v_rot};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return OKVQ_ERR_INVALID_ARGUMENT;
+  return OKVQ_OK;
+}
+
+CacheView view(const okvq_cache* c) {
+  CacheView v;
+  v.B = c->dims.batch;
+  v.H = c->dims.num_kv_heads;
+  v.Hq = c->dims.num_q_heads;
+  v.cap = c->dims.capacity;
+  v.k_codes = c->k_codes;
+  v.v_codes = c->v_codes;
+  v.k_norm = c->k_norm;
+  v.v_norm = c->v_norm;
+  v.k_min = c->k_min;
+  v.k_step = c->k_step;
+  v.modality = c->modality;
+  v.k_stage = c->k_stage;
+  v.seq_lens = c->seq_lens;
+  v.signs = c->key_signs;
+  v.rot = c->v_rot;
+  return v;
+}
+
+okvq_status hip_status(hipError_t e) { return e == hipSuccess ? OKVQ_OK : OKVQ_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t okvq_version(void) { return kVersion; }
+
+const char* okvq_status_string(okvq_status s) {
+  switch (s) {
+    case OKVQ_OK: return "ok";
+    case OKVQ_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case OKVQ_ERR_UNSUPPORTED: return "unsupported configuration";
+    case OKVQ_ERR_CAPACITY: return "capacity exceeded";
+    case OKVQ_ERR_WORKSPACE: return "workspace missing or too small";
+    case OKVQ_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
+  if (check_dims(d) != OKVQ_OK) return 0;
+  const size_t B = d->batch, H = d->num_kv_heads, cap = d->capacity, D = d->head_dim, W = d->window;
+  switch (which) {
+    case OKVQ_BUF_K_CODES: return B * H * cap * (D / 4);
+    case OKVQ_BUF_V_CODES: return B * H * cap * (D / 4);
+    case OKVQ_BUF_K_NORM: return B * H * cap * 2;
+    case OKVQ_BUF_V_NORM: return B * H * cap * 2;
+    case OKVQ_BUF_K_MIN: return B * H * (cap / W) * D * 2;
+    case OKVQ_BUF_K_STEP: return B * H * (cap / W) * D * 2;
+    case OKVQ_BUF_MODALITY: return B * cap;
+    case OKVQ_BUF_K_STAGE: return B * H * W * D * 2;
+    case OKVQ_BUF_SEQ_LENS: return B * 4;
+    default: return 0;
+  }
+}
+
+okvq_status okvq_codebook(float* levels, float* thresholds_out) {
+  if (!levels || !thresholds_out) return OKVQ_ERR_INVALID_ARGUMENT;
+  const Codebook& cb = codebook();
+  std::memcpy(levels, cb.level, sizeof(cb.level));
+  std::memcpy(thresholds_out, cb.thr, sizeof(cb.thr));
+  return OKVQ_OK;
+}
+
+okvq_status okvq_quantize_keys(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens, const int32_t* lens_host,
+                               const int8_t* key_signs, uint8_t* k_codes, uint16_t* k_min, uint16_t* k_step,
+                               uint16_t* k_norm, void* stream) {
+  okvq_status st = check_dims(dims);
+  if (st != OKVQ_OK) return st;
+  if (n_tokens < 0 || !lens_host) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(k) || !aligned16(key_signs) || !aligned16(k_codes) || !aligned16(k_min) || !aligned16(k_step) ||
+      !aligned16(k_norm))
+    return OKVQ_ERR_INVALID_ARGUMENT;
+  for (int b = 0; b < dims->batch; ++b) {
+    if (lens_host[b] < 0 || lens_host[b] > n_tokens) return OKVQ_ERR_INVALID_ARGUMENT;
+    if (lens_host[b] > dims->capacity) return OKVQ_ERR_CAPACITY;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
+    const int nb = std::min(kMaxLenArgs, dims->batch - b0);
+    CodecJob j{};
+    j.src = k;
+    j.n_rows = n_tokens;
+    j.b0 = b0;
+    j.H = dims->num_kv_heads;
+    j.cap = dims->capacity;
+    int max_len = 0;
+    for (int i = 0; i < nb; ++i) {
+      j.lens.lens[i] = lens_host[b0 + i];
+      max_len = std::max(max_len, lens_host[b0 + i]);
+    }
+    st = hip_status(launch_quantize_keys(j, nb, max_len, key_signs, k_codes, k_min, k_step, k_norm, s));
+    if (st != OKVQ_OK) return st;
+  }
+  return OKVQ_OK;
+}
+
+okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const uint8_t* modality, int32_t n_tokens,
+                                 const int32_t* lens_host, const float* v_rot, uint32_t flags, uint8_t* v_codes,
+                                 uint16_t* v_norm, void* stream) {
+  okvq_status st = check_dims(dims);
+  if (st != OKVQ_OK) return st;
+  if (n_tokens < 0 || !lens_host || (flags & ~(uint32_t)OKVQ_VALUE_EXACT)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(v) || !aligned16(modality) || !aligned16(v_rot) || !aligned16(v_codes) || !aligned16(v_norm))
+    return OKVQ_ERR_INVALID_ARGUMENT;
+  for (int b = 0; b < dims->batch; ++b) {
+    if (lens_host[b] < 0 || lens_host[b] > n_tokens) return OKVQ_ERR_INVALID_ARGUMENT;
+    if (lens_host[b] > dims->capacity) return OKVQ_ERR_CAPACITY;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Thresholds th = thresholds();
+  for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
+    const int nb = std::min(kMaxLenArgs, dims->batch - b0);
+    CodecJob j{};
+    j.src = v;
+    j.msrc = modality;
+    j.n_rows = n_tokens;
+    j.b0 = b0;
+    j.H = dims->num_kv_heads;
+    j.cap = dims->capacity;
+    int max_len = 0;
+    for (int i = 0; i < nb; ++i) {
+      j.lens.lens[i] = lens_host[b0 + i];
+      max_len = std::max(max_len, lens_host[b0 + i]);
+    }
+    st = hip_status(launch_quantize_values(j, nb, max_len, v_rot, th, (flags & OKVQ_VALUE_EXACT) != 0, v_codes, v_norm,
+                                           nullptr, s));
+    if (st != OKVQ_OK) return st;
+  }
+  return OKVQ_OK;
+}
+
+okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new, const uint16_t* v_new,
+                        const uint8_t* mod_new, const int32_t* n_new_host, const int32_t* n_new_dev, int32_t n_max,
+                        uint32_t flags, void* stream) {
+  okvq_status st = check_cache(cache);
+  if (st != OKVQ_OK) return st;
+  if (!lens_host || !n_new_host || n_max < 0 || (flags & ~(uint32_t)OKVQ_VALUE_EXACT)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(mod_new) || !aligned16(n_new_dev))
+    return OKVQ_ERR_INVALID_ARGUMENT;
+  const okvq_dims& d = cache->dims;
+  int span = 0;  // tokens from the first open window to the new end, largest over sequences
+  for (int b = 0; b < d.batch; ++b) {
+    const int L = lens_host[b], n = n_new_host[b];
+    if (L < 0 || n < 0 || n > n_max) return OKVQ_ERR_INVALID_ARGUMENT;
+    if (L > d.capacity || (int64_t)L + n > d.capacity) return OKVQ_ERR_CAPACITY;
+    if (n > 0) span = std::max(span, L + n - (L / 32) * 32);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (span > 0) {
+    CodecJob j{};
+    j.src = k_new;
+    j.msrc = mod_new;
+    j.n_rows = n_max;
+    j.begin_dev = cache->seq_lens;
+    j.count_dev = n_new_dev;
+    j.stage = cache->k_stage;
+    j.b0 = 0;
+    j.H = d.num_kv_heads;
+    j.cap = d.capacity;
+    st = hip_status(launch_quantize_keys(j, d.batch, span, cache->key_signs, cache->k_codes, cache->k_min,
+                                         cache->k_step, cache->k_norm, s));
+    if (st != OKVQ_OK) return st;
+    j.src = v_new;
+    j.stage = nullptr;
+    st = hip_status(launch_quantize_values(j, d.batch, span, cache->v_rot, thresholds(),
+                                           (flags & OKVQ_VALUE_EXACT) != 0, cache->v_codes, cache->v_norm,
+                                           cache->modality, s));
+    if (st != OKVQ_OK) return st;
+  }
+  return hip_status(launch_advance_lengths(cache->seq_lens, n_new_dev, d.batch, s));
+}
+
+size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len) {
+  if (check_dims(dims) != OKVQ_OK || max_seq_len < 0) return 0;
+  return decode_workspace_bytes(dims->batch, dims->num_kv_heads, dims->num_q_heads, max_seq_len);
+}
+
+okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q, float sm_scale,
+                                  uint32_t flags, float* out, void* workspace, size_t workspace_bytes, void* stream) {
+  okvq_status st = check_cache(cache);
+  if (st != OKVQ_OK) return st;
+  if (!lens_host || flags != 0 || !std::isfinite(sm_scale)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(q) || !aligned16(out)) return OKVQ_ERR_INVALID_ARGUMENT;
+  const okvq_dims& d = cache->dims;
+  int max_len = 0;
+  for (int b = 0; b < d.batch; ++b) {
+    if (lens_host[b] < 0) return OKVQ_ERR_INVALID_ARGUMENT;
+    if (lens_host[b] > d.capacity) return OKVQ_ERR_CAPACITY;
+    max_len = std::max(max_len, lens_host[b]);
+  }
+  const size_t need = decode_workspace_bytes(d.batch, d.num_kv_heads, d.num_q_heads, max_len);
+  if (!aligned16(workspace) || workspace_bytes < need) return OKVQ_ERR_WORKSPACE;
+  const DecodePlan plan = plan_decode(d.batch, d.num_kv_heads, max_len);
+  const Codebook& cb = codebook();
+  const uint32_t cb01 = cb.level16[0] | ((uint32_t)cb.level16[1] << 16);
+  const uint32_t cb23 = cb.level16[2] | ((uint32_t)cb.level16[3] << 16);
+  return hip_status(launch_decode(view(cache), q, sm_scale, out, workspace, plan, static_cast<hipStream_t>(stream),
+                                  cb01, cb23, max_len));
+}
+
+}  // extern "C"

@@ -1,0 +1,167 @@
+// Key codec on one wavefront: 64 consecutive tokens (two 32-token windows) of one
+// (sequence, KV head). Sec. 2.1 Eq. 2 (norm split, randomized Hadamard) and Sec. 2.3 Eq. 4
+// (per-window minimum and range of the rotated direction), 2-bit codes.
+//
+// Bit-exact operation order (per token row x, fp16):
+//   norm   t_c = x_c^2; halving tree t <- t[:n/2] + t[n/2:] to one value; n16 = fp16(sqrt_rn(.))
+//   dir    w = butterflies(s * x) for h = 1, 2, ..., 64; z = w * fl(kappa / n16) (z = 0 if n16 = 0)
+//   window lo = min z + 0, hi = max z + 0 over the window's valid tokens;
+//          step = fl(fl(hi - lo) / 3); m16 = fp16(lo), step16 = fp16(step)
+//   code   0 if step16 == 0, else clamp(rint(fl(fl(z - m16) * fl(1 / step16))), 0, 3)
+//
+// Lane mapping: phase A (lane = token) keeps the 128 channels of a row in registers, so the
+// norm tree and all seven butterfly stages run without cross-lane traffic. Phase B transposes
+// z through a wave-private LDS tile, 32 channels at a time (lane = channel of one window), for
+// the window min / max. Phase C (lane = token) computes and packs the codes.
+#pragma once
+
+#include "okvq_device.hpp"
+
+namespace okvq {
+
+constexpr int kKeyPitch = 33;  // LDS row pitch (floats) of the transpose tile: conflict-free columns
+constexpr int kKeyWaveLds = 64 * kKeyPitch + 2 * kD * 2;  // floats per wave: tile + (m, 1/step) x 2 windows
+
+struct KeyWaveOut {
+  uint8_t* codes;  // [cap][32] of this (sequence, head)
+  uint16_t* kmin;  // [cap/32][128]
+  uint16_t* kstep; // [cap/32][128]
+  uint16_t* knorm; // [cap]
+};
+
+// Sign-flip masks for an fp16 pair (channels c, c+1) from the 32 sign words (4 int8 signs each).
+__device__ __forceinline__ uint32_t sign_pair_mask(const uint32_t (&sw)[32], int c) {
+  const uint32_t w = sw[c >> 2];
+  return (c & 2) ? (((w & 0x00800000u) >> 8) | (w & 0x80000000u))
+                 : (((w & 0x00000080u) << 8) | ((w & 0x00008000u) << 16));
+}
+
+// raw: the token's 128 fp16 channels as 64 dwords (channel 2i in the low half of raw[i]).
+// Processes tokens [tok0, tok0 + 64); `len` is the sequence length; `store_end` bounds the slots
+// written (whole windows: padded slots below store_end get code 0 and norm 0).
+__device__ __forceinline__ void key_quantize_wave(const uint32_t (&raw)[64], int tok0, int len,
+                                                  const uint32_t (&sw)[32], KeyWaveOut out,
+                                                  float* lds) {
+  const int lane = lane_id();
+  const int tok = tok0 + lane;
+  const bool valid = tok < len;
+
+  // ---- phase A: norm and rotated direction (lane = token) ----
+  float x[kD];
+#pragma unroll
+  for (int i = 0; i < 64; ++i) {
+    const uint32_t r = raw[i] ^ sign_pair_mask(sw, 2 * i);
+    x[2 * i] = h2f(r & 0xffffu);
+    x[2 * i + 1] = h2f(r >> 16);
+  }
+  float n32;
+  {
+    float t[64];
+#pragma unroll
+    for (int c = 0; c < 64; ++c) t[c] = x[c] * x[c] + x[c + 64] * x[c + 64];
+#pragma unroll
+    for (int n = 32; n >= 1; n >>= 1) {
+#pragma unroll
+      for (int c = 0; c < n; ++c) t[c] = t[c] + t[c + n];
+    }
+    n32 = sqrt_rn(t[0]);
+  }
+  const uint32_t n16 = norm_to_f16(n32);
+#pragma unroll
+  for (int h = 1; h < kD; h <<= 1) {
+#pragma unroll
+    for (int j = 0; j < kD; ++j) {
+      if ((j & h) == 0) {
+        const float a = x[j], b = x[j + h];
+        x[j] = a + b;
+        x[j + h] = a - b;
+      }
+    }
+  }
+  const float n16f = h2f(n16);
+  const float cinv = div_rn(kKappa, n16f);
+  const bool zero_norm = (n16 == 0);
+#pragma unroll
+  for (int c = 0; c < kD; ++c) x[c] = zero_norm ? 0.0f : x[c] * cinv;
+
+  // ---- phase B: window min / max through LDS (lane = channel of window lane/32) ----
+  float* tile = lds;
+  float* stats = lds + 64 * kKeyPitch;  // [2][128] x (m32, inv32)
+  const int ch = lane & 31;
+  const int win = lane >> 5;
+  const int nvalid = min(max(len - (tok0 + 32 * win), 0), 32);
+  const int gwin = (tok0 >> 5) + win;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+#pragma unroll
+    for (int j = 0; j < 32; ++j) tile[lane * kKeyPitch + j] = x[32 * q + j];
+    wave_lds_sync();
+    float lo = __builtin_inff(), hi = -__builtin_inff();
+#pragma unroll
+    for (int r = 0; r < 32; ++r) {
+      const float v = tile[(32 * win + r) * kKeyPitch + ch];
+      if (r < nvalid) {
+        lo = fminf(lo, v);
+        hi = fmaxf(hi, v);
+      }
+    }
+    if (nvalid > 0) {
+      lo = lo + 0.0f;  // canonical +0
+      hi = hi + 0.0f;
+      const float step = div_rn(hi - lo, 3.0f);
+      const uint32_t m16 = f2h(lo);
+      const uint32_t s16 = f2h(step);
+      const int c = 32 * q + ch;
+      out.kmin[gwin * kD + c] = (uint16_t)m16;
+      out.kstep[gwin * kD + c] = (uint16_t)s16;
+      stats[(win * kD + c) * 2 + 0] = h2f(m16);
+      stats[(win * kD + c) * 2 + 1] = (s16 == 0) ? 0.0f : div_rn(1.0f, h2f(s16));
+    }
+    wave_lds_sync();
+  }
+
+  // ---- phase C: codes (lane = token) ----
+  const int my_win = lane >> 5;
+  const int store_slots = min(max(len - tok0 + 31, 0) / 32 * 32, 64);  // slots of valid windows
+  if (lane < store_slots) {
+    uint32_t dw[8];
+#pragma unroll
+    for (int d = 0; d < 8; ++d) dw[d] = 0;
+    if (valid) {
+      const float4* st = reinterpret_cast<const float4*>(stats + my_win * kD * 2);
+#pragma unroll
+      for (int c = 0; c < kD; c += 2) {
+        const float4 s = st[c >> 1];
+        const float t0 = (x[c] - s.x) * s.y;
+        const float t1 = (x[c + 1] - s.z) * s.w;
+        const uint32_t c0 = (uint32_t)fminf(fmaxf(__builtin_rintf(t0), 0.0f), 3.0f);
+        const uint32_t c1 = (uint32_t)fminf(fmaxf(__builtin_rintf(t1), 0.0f), 3.0f);
+        dw[c >> 4] |= (c0 << (2 * (c & 15))) | (c1 << (2 * ((c + 1) & 15)));
+      }
+    }
+    uint4* dst = reinterpret_cast<uint4*>(out.codes + (size_t)tok * 32);
+    dst[0] = make_uint4(dw[0], dw[1], dw[2], dw[3]);
+    dst[1] = make_uint4(dw[4], dw[5], dw[6], dw[7]);
+    out.knorm[tok] = valid ? (uint16_t)n16 : (uint16_t)0;
+  }
+}
+
+__device__ __forceinline__ void load_sign_words(const int8_t* signs, uint32_t (&sw)[32]) {
+  const uint32_t* s = reinterpret_cast<const uint32_t*>(signs);
+#pragma unroll
+  for (int i = 0; i < 32; ++i) sw[i] = __builtin_amdgcn_readfirstlane(s[i]);
+}
+
+__device__ __forceinline__ void load_row_f16(const uint16_t* row, uint32_t (&raw)[64]) {
+  const uint4* p = reinterpret_cast<const uint4*>(row);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const uint4 v = p[i];
+    raw[4 * i + 0] = v.x;
+    raw[4 * i + 1] = v.y;
+    raw[4 * i + 2] = v.z;
+    raw[4 * i + 3] = v.w;
+  }
+}
+
+}  // namespace okvq

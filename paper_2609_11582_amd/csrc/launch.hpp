@@ -1,0 +1,60 @@
+// Internal launchers shared by the C ABI (api.hip) and the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "okvq_device.hpp"
+#include "value_quant.hpp"
+
+namespace okvq {
+
+// Where the codec kernels read token rows. Stateless calls (begin_dev == nullptr) quantize tokens
+// [0, lens[b - b0]) of a dense block. Append quantizes tokens [begin_dev[b], begin_dev[b] +
+// count_dev[b]) whose rows are src row (token - begin); older rows of the open key window come
+// from the fp16 stage.
+struct CodecJob {
+  const uint16_t* src;       // [B][H][n_rows][128] fp16
+  const uint8_t* msrc;       // [B][n_rows] modality ids (values only)
+  int n_rows;
+  LenArgs lens;              // stateless lengths for batches b0 .. b0 + 255
+  const int32_t* begin_dev;  // append: current lengths (device)
+  const int32_t* count_dev;  // append: appended tokens (device)
+  uint16_t* stage;           // append: [B][H][32][128] raw keys of the open window
+  int b0, H, cap;
+};
+
+// max_tiles_tokens: tokens to cover from the first open window (host bound for the grid).
+hipError_t launch_quantize_keys(const CodecJob& j, int nb, int max_tiles_tokens, const int8_t* signs,
+                                uint8_t* k_codes, uint16_t* k_min, uint16_t* k_step, uint16_t* k_norm,
+                                hipStream_t s);
+hipError_t launch_quantize_values(const CodecJob& j, int nb, int max_tiles_tokens, const float* rot,
+                                  const Thresholds& th, bool exact, uint8_t* v_codes, uint16_t* v_norm,
+                                  uint8_t* mod_out, hipStream_t s);
+hipError_t launch_advance_lengths(int32_t* seq_lens, const int32_t* count, int B, hipStream_t s);
+
+struct CacheView {
+  int B, H, Hq, cap;
+  uint8_t* k_codes;
+  uint8_t* v_codes;
+  uint16_t* k_norm;
+  uint16_t* v_norm;
+  uint16_t* k_min;
+  uint16_t* k_step;
+  uint8_t* modality;
+  uint16_t* k_stage;
+  int32_t* seq_lens;
+  const int8_t* signs;
+  const float* rot;
+};
+
+struct DecodePlan {
+  int wins_per_split;  // 32-token windows per split-K work-group
+  int nsplit;          // splits per (sequence, KV head)
+};
+DecodePlan plan_decode(int B, int H, int max_len);
+size_t decode_workspace_bytes(int B, int H, int Hq, int max_len);
+hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, float* out, void* ws,
+                         const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int max_len);
+
+}  // namespace okvq

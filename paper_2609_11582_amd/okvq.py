@@ -1,0 +1,233 @@
+"""ctypes binding of libokvq.so (include/okvq.h): argument marshalling only.
+
+Every function here forwards to the C ABI function of the same name. Tensors are passed as
+device pointers (``data_ptr()``), host integer arrays as ctypes arrays, and the stream is
+torch's current HIP stream unless one is given. PyTorch provides device memory and streams;
+every step of the computation runs in the library's HIP kernels. There is no fallback: if the
+library is missing, importing the binding fails loudly.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libokvq.so")
+
+OKVQ_OK = 0
+OKVQ_VALUE_EXACT = 1
+BUFFERS = ("k_codes", "v_codes", "k_norm", "v_norm", "k_min", "k_step", "modality", "k_stage", "seq_lens")
+
+
+class OkvqError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+        self.status = status
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("window", ctypes.c_int32), ("capacity", ctypes.c_int32)]
+
+
+class CacheStruct(ctypes.Structure):
+    _fields_ = [("dims", Dims)] + [(n, ctypes.c_void_p) for n in BUFFERS] + [
+        ("key_signs", ctypes.c_void_p), ("v_rot", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, u32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_size_t
+        P = ctypes.POINTER
+        L.okvq_version.restype = i32
+        L.okvq_status_string.restype = ctypes.c_char_p
+        L.okvq_status_string.argtypes = [i32]
+        L.okvq_buffer_bytes.restype = sz
+        L.okvq_buffer_bytes.argtypes = [P(Dims), i32]
+        L.okvq_codebook.restype = i32
+        L.okvq_codebook.argtypes = [P(ctypes.c_float), P(ctypes.c_float)]
+        L.okvq_quantize_keys.restype = i32
+        L.okvq_quantize_keys.argtypes = [P(Dims), vp, i32, P(i32), vp, vp, vp, vp, vp, vp]
+        L.okvq_quantize_values.restype = i32
+        L.okvq_quantize_values.argtypes = [P(Dims), vp, vp, i32, P(i32), vp, u32, vp, vp, vp]
+        L.okvq_append.restype = i32
+        L.okvq_append.argtypes = [P(CacheStruct), P(i32), vp, vp, vp, P(i32), vp, i32, u32, vp]
+        L.okvq_decode_workspace_bytes.restype = sz
+        L.okvq_decode_workspace_bytes.argtypes = [P(Dims), i32]
+        L.okvq_decode_attention.restype = i32
+        L.okvq_decode_attention.argtypes = [P(CacheStruct), P(i32), vp, ctypes.c_float, u32, vp, vp, sz, vp]
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().okvq_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != OKVQ_OK:
+        raise OkvqError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _need(t: torch.Tensor, nbytes: int, name: str) -> None:
+    """The library trusts buffer sizes; check them here so that no kernel reads past a tensor."""
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous device tensor")
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{name}: {have} bytes, at least {nbytes} needed")
+
+
+def _need_len(xs, n: int, name: str) -> None:
+    if len(xs) != n:
+        raise ValueError(f"{name}: {len(xs)} entries, expected {n}")
+
+
+def _i32(xs: Sequence[int]):
+    return (ctypes.c_int32 * len(xs))(*[int(x) for x in xs])
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def make_dims(batch, num_kv_heads, num_q_heads, capacity, head_dim=128, window=32) -> Dims:
+    return Dims(batch, num_kv_heads, num_q_heads, head_dim, window, capacity)
+
+
+def okvq_version() -> int:
+    return lib().okvq_version()
+
+
+def okvq_buffer_bytes(dims: Dims, which: int) -> int:
+    return lib().okvq_buffer_bytes(ctypes.byref(dims), which)
+
+
+def okvq_codebook():
+    lv = (ctypes.c_float * 4)()
+    th = (ctypes.c_float * 3)()
+    _check(lib().okvq_codebook(lv, th), "okvq_codebook")
+    return list(lv), list(th)
+
+
+def okvq_quantize_keys(dims, k, n_tokens, lens, key_signs, k_codes, k_min, k_step, k_norm, stream=None,
+                       check=True) -> int:
+    B, H = dims.batch, dims.num_kv_heads
+    _need_len(lens, B, "lens")
+    _need(k, B * H * int(n_tokens) * 128 * 2, "k")
+    _need(key_signs, 128, "key_signs")
+    for i, (name, t) in {0: ("k_codes", k_codes), 2: ("k_norm", k_norm), 4: ("k_min", k_min),
+                         5: ("k_step", k_step)}.items():
+        _need(t, okvq_buffer_bytes(dims, i), name)
+    st = lib().okvq_quantize_keys(ctypes.byref(dims), _ptr(k), int(n_tokens), _i32(lens), _ptr(key_signs),
+                                  _ptr(k_codes), _ptr(k_min), _ptr(k_step), _ptr(k_norm), _stream(stream))
+    if check:
+        _check(st, "okvq_quantize_keys")
+    return st
+
+
+def okvq_quantize_values(dims, v, modality, n_tokens, lens, v_rot, flags, v_codes, v_norm, stream=None,
+                         check=True) -> int:
+    B, H = dims.batch, dims.num_kv_heads
+    _need_len(lens, B, "lens")
+    _need(v, B * H * int(n_tokens) * 128 * 2, "v")
+    _need(modality, B * int(n_tokens), "modality")
+    _need(v_rot, 3 * 128 * 128 * 4, "v_rot")
+    _need(v_codes, okvq_buffer_bytes(dims, 1), "v_codes")
+    _need(v_norm, okvq_buffer_bytes(dims, 3), "v_norm")
+    st = lib().okvq_quantize_values(ctypes.byref(dims), _ptr(v), _ptr(modality), int(n_tokens), _i32(lens),
+                                    _ptr(v_rot), int(flags), _ptr(v_codes), _ptr(v_norm), _stream(stream))
+    if check:
+        _check(st, "okvq_quantize_values")
+    return st
+
+
+def okvq_append(cache: "KVCache", lens, k_new, v_new, mod_new, n_new, n_new_dev, n_max, flags=0, stream=None,
+                check=True) -> int:
+    B, H = cache.dims.batch, cache.dims.num_kv_heads
+    _need_len(lens, B, "lens")
+    _need_len(n_new, B, "n_new")
+    _need(k_new, B * H * int(n_max) * 128 * 2, "k_new")
+    _need(v_new, B * H * int(n_max) * 128 * 2, "v_new")
+    _need(mod_new, B * int(n_max), "mod_new")
+    _need(n_new_dev, B * 4, "n_new_dev")
+    st = lib().okvq_append(ctypes.byref(cache.struct), _i32(lens), _ptr(k_new), _ptr(v_new), _ptr(mod_new),
+                           _i32(n_new), _ptr(n_new_dev), int(n_max), int(flags), _stream(stream))
+    if check:
+        _check(st, "okvq_append")
+    return st
+
+
+def okvq_decode_workspace_bytes(dims: Dims, max_seq_len: int) -> int:
+    return lib().okvq_decode_workspace_bytes(ctypes.byref(dims), int(max_seq_len))
+
+
+def okvq_decode_attention(cache: "KVCache", lens, q, sm_scale, out, workspace, workspace_bytes=None, flags=0,
+                          stream=None, check=True) -> int:
+    B, Hq = cache.dims.batch, cache.dims.num_q_heads
+    _need_len(lens, B, "lens")
+    _need(q, B * Hq * 128 * 2, "q")
+    _need(out, B * Hq * 128 * 4, "out")
+    have = workspace.numel() * workspace.element_size()
+    nbytes = have if workspace_bytes is None else min(int(workspace_bytes), have)
+    st = lib().okvq_decode_attention(ctypes.byref(cache.struct), _i32(lens), _ptr(q), float(sm_scale), int(flags),
+                                     _ptr(out), _ptr(workspace), int(nbytes), _stream(stream))
+    if check:
+        _check(st, "okvq_decode_attention")
+    return st
+
+
+_DTYPES = dict(k_codes=torch.uint8, v_codes=torch.uint8, k_norm=torch.float16, v_norm=torch.float16,
+               k_min=torch.float16, k_step=torch.float16, modality=torch.uint8, k_stage=torch.float16,
+               seq_lens=torch.int32)
+
+
+class KVCache:
+    """Device buffers of one layer's packed cache, sized by okvq_buffer_bytes (torch allocations)."""
+
+    def __init__(self, batch, num_kv_heads, num_q_heads, capacity, key_signs: torch.Tensor, v_rot: torch.Tensor,
+                 device="cuda"):
+        self.dims = make_dims(batch, num_kv_heads, num_q_heads, capacity)
+        self.key_signs = key_signs.to(device=device, dtype=torch.int8).contiguous()
+        self.v_rot = v_rot.to(device=device, dtype=torch.float32).contiguous()
+        self.buffers = {}
+        for i, name in enumerate(BUFFERS):
+            nbytes = okvq_buffer_bytes(self.dims, i)
+            if nbytes == 0:
+                raise OkvqError(-1, f"okvq_buffer_bytes({name})")
+            dt = _DTYPES[name]
+            n = nbytes // torch.tensor([], dtype=dt).element_size()
+            self.buffers[name] = torch.zeros(n, dtype=dt, device=device)
+        self.struct = CacheStruct(self.dims, *[self.buffers[n].data_ptr() for n in BUFFERS],
+                                  self.key_signs.data_ptr(), self.v_rot.data_ptr())
+
+    def __getitem__(self, name):
+        return self.buffers[name]
+
+    def views(self):
+        """The buffers reshaped to their documented layouts."""
+        d = self.dims
+        B, H, cap = d.batch, d.num_kv_heads, d.capacity
+        b = self.buffers
+        return dict(k_codes=b["k_codes"].view(B, H, cap, 32), v_codes=b["v_codes"].view(B, H, cap // 32, 1024),
+                    k_norm=b["k_norm"].view(B, H, cap), v_norm=b["v_norm"].view(B, H, cap),
+                    k_min=b["k_min"].view(B, H, cap // 32, 128), k_step=b["k_step"].view(B, H, cap // 32, 128),
+                    modality=b["modality"].view(B, cap), k_stage=b["k_stage"].view(B, H, 32, 128),
+                    seq_lens=b["seq_lens"])

@@ -107,7 +107,8 @@ def gen_keys(wid: int, layer: int, b: int, h: int, n: int, d: int = HEAD_DIM) ->
     x = rng_for(wid, layer, S_KEY_NOISE, b, h).standard_normal((n, d))
     n_drift = -(-n // 64)
     steps = 0.5 * rng_for(wid, layer, S_DRIFT, b, h).standard_normal((n_drift, d))
-    steps[0] = 0.0
+    if n_drift:
+        steps[0] = 0.0
     mu = np.cumsum(steps, axis=0)
     k = x + np.repeat(mu, 64, axis=0)[:n]
     outl = rng_for(wid, layer, S_OUTLIER, 0, h).choice(d, size=4, replace=False)
@@ -161,12 +162,13 @@ def gen_lengths(wl: Workload) -> np.ndarray:
 def gen_layer(wl: Workload, layer: int = 0, lengths: Optional[np.ndarray] = None, n_tokens: Optional[int] = None):
     """All inputs of one layer: dict with k, v [B][Hkv][N][D] fp16, modality [B][N] u8, lens, q, rot, signs.
 
-    Tokens beyond a sequence's length are zero-filled (they are ignored by every consumer).
+    B is len(lengths) when lengths are given, else the workload's batch. Tokens beyond a sequence's
+    length are zero-filled (they are ignored by every consumer).
     """
     if lengths is None:
         lengths = gen_lengths(wl)
     n = int(n_tokens if n_tokens is not None else wl.seq_len)
-    B, H = wl.batch, wl.num_kv_heads
+    B, H = len(lengths), wl.num_kv_heads
     k = np.zeros((B, H, n, HEAD_DIM), np.float16)
     v = np.zeros((B, H, n, HEAD_DIM), np.float16)
     mod = np.zeros((B, n), np.uint8)

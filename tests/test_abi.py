@@ -1,0 +1,108 @@
+"""Host-side checks of the C ABI that need no GPU: exports, codebook, byte accounting, validation."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle.codebook import codebook
+from oracle.layout import bits_per_element
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "okvq.h")
+
+
+def _lib():
+    from paper_2609_11582_amd import okvq
+    return okvq
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(okvq_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    okvq = _lib()
+    L = okvq.lib()
+    names = declared_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_codebook_matches_oracle_bit_for_bit():
+    okvq = _lib()
+    levels, thr = okvq.okvq_codebook()
+    cb, tau = codebook(128)
+    np.testing.assert_array_equal(np.array(levels, np.float32), cb.astype(np.float32))
+    np.testing.assert_array_equal(np.array(thr, np.float32), tau.astype(np.float32))
+
+
+def test_buffer_bytes_reproduce_tab3_accounting():
+    okvq = _lib()
+    d = okvq.make_dims(2, 4, 28, 32768)
+    names = ["k_codes", "v_codes", "k_norm", "v_norm", "k_min", "k_step"]
+    total = sum(okvq.okvq_buffer_bytes(d, i) for i in range(len(names)))
+    elems = 2 * 4 * 32768 * 128 * 2     # keys and values
+    assert total * 8 / elems == bits_per_element("ours_fp16_meta") == 2.625
+    assert okvq.okvq_buffer_bytes(d, 6) == 2 * 32768                  # modality map
+    assert okvq.okvq_buffer_bytes(d, 7) == 2 * 4 * 32 * 128 * 2       # key stage
+    assert okvq.okvq_buffer_bytes(d, 99) == 0
+    assert okvq.okvq_decode_workspace_bytes(d, 32768) > 0
+
+
+def test_invalid_arguments_rejected_before_any_launch():
+    okvq = _lib()
+    L = okvq.lib()
+    fake = ctypes.c_void_p(4096)    # aligned, never dereferenced: validation fails first
+    lens = (ctypes.c_int32 * 2)(10, 10)
+    ok_dims = okvq.make_dims(2, 2, 8, 64)
+    cases = [
+        (okvq.make_dims(2, 2, 8, 64, head_dim=64), -2),
+        (okvq.make_dims(2, 2, 8, 64, window=16), -2),
+        (okvq.make_dims(2, 2, 7, 64), -1),       # Hq not a multiple of H
+        (okvq.make_dims(2, 1, 16, 64), -2),      # group of 16 > 8
+        (okvq.make_dims(2, 2, 8, 48), -1),       # capacity not a multiple of 32
+        (okvq.make_dims(0, 2, 8, 64), -1),
+    ]
+    for dims, want in cases:
+        st = L.okvq_quantize_keys(ctypes.byref(dims), fake, 10, lens, fake, fake, fake, fake, fake, None)
+        assert st == want, (dims.head_dim, dims.window, st)
+    # misaligned pointer
+    st = L.okvq_quantize_keys(ctypes.byref(ok_dims), ctypes.c_void_p(4097), 10, lens, fake, fake, fake, fake, fake,
+                              None)
+    assert st == -1
+    # lengths beyond the block / beyond capacity
+    big = (ctypes.c_int32 * 2)(10, 11)
+    assert L.okvq_quantize_keys(ctypes.byref(ok_dims), fake, 10, big, fake, fake, fake, fake, fake, None) == -1
+    over = (ctypes.c_int32 * 2)(10, 65)
+    assert L.okvq_quantize_keys(ctypes.byref(ok_dims), fake, 100, over, fake, fake, fake, fake, fake, None) == -3
+    # unknown flag on values
+    assert L.okvq_quantize_values(ctypes.byref(ok_dims), fake, fake, 10, lens, fake, 8, fake, fake, None) == -1
+    # decode: workspace too small, bad flags, over capacity
+    cache = okvq.CacheStruct(ok_dims, *([4096] * 9), 4096, 4096)
+    q_lens = (ctypes.c_int32 * 2)(64, 64)
+    assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, 16,
+                                   None) == -4
+    assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 1, fake, fake, 1 << 30,
+                                   None) == -1
+    over_l = (ctypes.c_int32 * 2)(65, 0)
+    assert L.okvq_decode_attention(ctypes.byref(cache), over_l, fake, ctypes.c_float(0.1), 0, fake, fake, 1 << 30,
+                                   None) == -3
+    # append beyond capacity
+    n_new = (ctypes.c_int32 * 2)(40, 0)
+    lens_a = (ctypes.c_int32 * 2)(30, 0)
+    assert L.okvq_append(ctypes.byref(cache), lens_a, fake, fake, fake, n_new, fake, 40, 0, None) == -3
+    null_cache = okvq.CacheStruct(ok_dims, *([4096] * 8), 0, 4096, 4096)
+    assert L.okvq_append(ctypes.byref(null_cache), lens_a, fake, fake, fake, n_new, fake, 40, 0, None) == -1
+    assert okvq.status_string(-3) == "capacity exceeded"
+
+
+@pytest.mark.parametrize("which", range(9))
+def test_buffer_bytes_invalid_dims(which):
+    okvq = _lib()
+    assert okvq.okvq_buffer_bytes(okvq.make_dims(1, 1, 1, 33), which) == 0
