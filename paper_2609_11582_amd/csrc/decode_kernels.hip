@@ -1,16 +1,17 @@
 // Fused decode attention over the packed 2-bit cache (Eq. 1 with the codecs of Eq. 2, 4, 6).
 //
 // Split-K flash decoding. Work-group (split, KV head h, sequence b) = 4 waves; wave w takes the
-// split's 32-token windows w, w + 4, ... and keeps its own online-softmax state; the waves are
-// combined in LDS and one partial record per work-group is written. A second kernel merges the
-// splits (log-sum-exp) and applies the inverse value rotation once per modality.
+// split's window pairs (2w + 8k, 2w + 8k + 1) and keeps its own online-softmax state; the waves
+// are combined in LDS and one partial record per work-group is written. A second kernel merges
+// the splits (log-sum-exp) and applies the inverse value rotation once per modality.
 //
 // What one wave does per window (all G <= 8 query heads of the KV head from one read):
 //  * scores in the rotated key space (Sec. 2.3): s_i = n_i (q'.m_g + sum_c q'_c step_gc code_ic),
 //    q' = H q sm_scale log2(e) computed once per work-group. The per-window bias q'.m_g is a
-//    VALU dot product; the code term is one MFMA block-diagonal product: rows = 16 tokens, columns
-//    0-7 = heads for tokens 0-15 of the window and columns 8-15 = the same heads for tokens
-//    16-31 (K = 256 = two token rows of 128 channels), so a 16x16 tile holds all 32 tokens.
+//    VALU dot product; the code term is an MFMA block-diagonal over a window pair: rows = 16
+//    tokens, columns 0-7 = heads for window A and columns 8-15 = the same heads for window B
+//    (K = 256 = the two windows' 128 channels), so each lane builds the query-times-step operand
+//    of one window only, and two 16x16 tiles hold the pair's 64 tokens.
 //    Codes enter the MFMA unchanged as fp16 subnormals: (dword & (3 << 2j)) is code * 2^(2j-24),
 //    and the matching power of two is folded into the B operand q'_c step_gc 2^(k0 - 2j).
 //  * online softmax in base 2 (running max per head, rescale only when it grows);
@@ -27,11 +28,13 @@ namespace okvq {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kDecWaves = 4;
+constexpr int kDecWaves = 8;                         // waves per split work-group
 constexpr int kRecHeader = 32;                       // m[8], l[8], mask, pad
 constexpr int kRecFloats = kRecHeader + 3 * 8 * kD;  // + acc[3 modalities][8 heads][128]
-constexpr int kMinWps = 4;                           // fewest windows per split
+constexpr int kMinWps = 2 * kDecWaves;              // fewest windows per split (a pair per wave)
 constexpr int kMaxSplits = 1024;                     // most splits per (sequence, KV head)
+constexpr float kLazy = 8.0f;                        // log2 headroom of the lazily updated softmax max
+constexpr float kPvScale = 1.0f / 256.0f;            // 2^-kLazy: keeps p n_v within fp16
 
 struct DecodeArgs {
   const uint8_t* k_codes;
@@ -61,6 +64,12 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
 __device__ __forceinline__ uint32_t swap8(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xf, 0xf, false);
 }
+__device__ __forceinline__ float fswap8(float v) { return __builtin_bit_cast(float, swap8(__builtin_bit_cast(uint32_t, v))); }
+// lane l <- lane l ^ 16 and lane l ^ 32 (permutes between rows of 16, no LDS access)
+__device__ __forceinline__ float fxor16(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401f));
+}
+__device__ __forceinline__ float fxor32(float v) { return __shfl_xor(v, 32); }
 
 // Scale exponent of the fp16-subnormal code extraction for pair slot j (0..7) of a dword.
 __host__ __device__ constexpr int code_shift(int j) { return j <= 4 ? 2 * j : 2 * j - 10; }
@@ -79,51 +88,99 @@ __device__ __forceinline__ half8 key_a_operand(uint32_t d0, uint32_t d1, int kk)
   return h8(d & 0x03000300u, s & 0x00030003u, s & 0x000c000cu, s & 0x00300030u);
 }
 
-struct WinLoad {
-  uint2 kc0, kc1;  // key codes: token r and 16 + r, bytes 8g .. 8g+7
-  uint4 vc;        // value codes: the lane's 16 bytes of the window block
-  uint2 nk, nv;    // key / value norms of the lane's 4 score rows
-  uint32_t md;     // modality ids of those 4 tokens
-  uint32_t stp;    // step of channels 32g + 2col, +1 (fp16 pair)
-  uint32_t mnp;    // min of the same channels
+// Loads of one window pair (A = wA, B = wA + 1) for one lane. Lanes 0-7 of every row of 16
+// score window A, lanes 8-15 window B ("side"); both sides need both windows' key codes (the
+// score MFMA is block-diagonal over the pair) and value codes (one PV MFMA per window).
+struct PairLoad {
+  uint2 ka0, ka1, kb0, kb1;  // key codes of tokens r and 16 + r of windows A, B (bytes 8g .. 8g+7)
+  uint4 va, vb;              // value codes of windows A, B (the lane's 16 bytes of each block)
+  uint2 nk0, nk1;            // key norms of the side window, tokens 4g .. 4g+3 and 16+4g .. 16+4g+3
+  uint2 nv0, nv1;            // value norms of the same tokens
+  uint32_t md0, md1;         // modality ids of the same tokens
+  uint2 stp, mnp;            // step / min of channels 32g + 4 (col % 8) .. +3 of the side window
 };
 
-__device__ __forceinline__ WinLoad load_window(const DecodeArgs& p, size_t seq, int b, int w, int lane) {
-  const int col = lane & 15, g = lane >> 4, r = lane & 15;
-  const int own_tok = 16 * (col >= 8 ? 1 : 0) + 4 * g;
-  const int t0 = w * kW;
-  const uint8_t* kc = p.k_codes + (seq * p.cap + t0) * 32;
-  WinLoad d;
-  d.kc0 = *reinterpret_cast<const uint2*>(kc + r * 32 + 8 * g);
-  d.kc1 = *reinterpret_cast<const uint2*>(kc + (16 + r) * 32 + 8 * g);
-  d.vc = *reinterpret_cast<const uint4*>(p.v_codes + (seq * (p.cap / kW) + w) * 1024 + 16 * lane);
-  d.nk = *reinterpret_cast<const uint2*>(p.k_norm + seq * p.cap + t0 + own_tok);
-  d.nv = *reinterpret_cast<const uint2*>(p.v_norm + seq * p.cap + t0 + own_tok);
-  d.md = *reinterpret_cast<const uint32_t*>(p.modality + (size_t)b * p.cap + t0 + own_tok);
-  const size_t meta = (seq * (p.cap / kW) + w) * kD + 32 * g + 2 * col;
-  d.stp = *reinterpret_cast<const uint32_t*>(p.k_step + meta);
-  d.mnp = *reinterpret_cast<const uint32_t*>(p.k_min + meta);
+__device__ __forceinline__ PairLoad load_pair(const DecodeArgs& p, size_t seq, int b, int wA, bool hasB, int lane) {
+  const int col = lane & 15, g = lane >> 4, r = lane & 15, side = col >> 3;
+  const size_t nwcap = p.cap / kW;
+  const uint8_t* kc = p.k_codes + seq * p.cap * 32;
+  const uint8_t* vc = p.v_codes + seq * nwcap * 1024 + 16 * lane;
+  PairLoad d;
+  d.ka0 = *reinterpret_cast<const uint2*>(kc + (size_t)(kW * wA + r) * 32 + 8 * g);
+  d.ka1 = *reinterpret_cast<const uint2*>(kc + (size_t)(kW * wA + 16 + r) * 32 + 8 * g);
+  d.va = *reinterpret_cast<const uint4*>(vc + (size_t)wA * 1024);
+  if (hasB) {
+    d.kb0 = *reinterpret_cast<const uint2*>(kc + (size_t)(kW * (wA + 1) + r) * 32 + 8 * g);
+    d.kb1 = *reinterpret_cast<const uint2*>(kc + (size_t)(kW * (wA + 1) + 16 + r) * 32 + 8 * g);
+    d.vb = *reinterpret_cast<const uint4*>(vc + (size_t)(wA + 1) * 1024);
+  } else {
+    d.kb0 = d.kb1 = make_uint2(0, 0);
+    d.vb = make_uint4(0, 0, 0, 0);
+  }
+  if (side == 0 || hasB) {
+    const int wS = wA + side;
+    const size_t t = seq * p.cap + (size_t)kW * wS + 4 * g;
+    d.nk0 = *reinterpret_cast<const uint2*>(p.k_norm + t);
+    d.nk1 = *reinterpret_cast<const uint2*>(p.k_norm + t + 16);
+    d.nv0 = *reinterpret_cast<const uint2*>(p.v_norm + t);
+    d.nv1 = *reinterpret_cast<const uint2*>(p.v_norm + t + 16);
+    const uint8_t* md = p.modality + (size_t)b * p.cap + kW * wS + 4 * g;
+    d.md0 = *reinterpret_cast<const uint32_t*>(md);
+    d.md1 = *reinterpret_cast<const uint32_t*>(md + 16);
+    const size_t mt = (seq * nwcap + wS) * kD + 32 * g + 4 * (col & 7);
+    d.stp = *reinterpret_cast<const uint2*>(p.k_step + mt);
+    d.mnp = *reinterpret_cast<const uint2*>(p.k_min + mt);
+  } else {
+    d.nk0 = d.nk1 = d.nv0 = d.nv1 = d.stp = d.mnp = make_uint2(0, 0);
+    d.md0 = d.md1 = 0;
+  }
   return d;
 }
 
-__global__ __launch_bounds__(256, 2) void k_decode_split(DecodeArgs p) {
+__device__ __forceinline__ half8 lut_op(const uint2* vlut, uint4 vc, int nb) {
+  const uint32_t vw[4] = {vc.x, vc.y, vc.z, vc.w};
+  const uint32_t b0 = (vw[nb >> 2] >> (8 * (nb & 3))) & 0xffu;        // tokens 4g .. 4g+3
+  const uint32_t b1 = (vw[2 + (nb >> 2)] >> (8 * (nb & 3))) & 0xffu;  // tokens 16+4g .. 16+4g+3
+  const uint2 x0 = vlut[b0];
+  const uint2 x1 = vlut[b1];
+  return h8(x0.x, x0.y, x1.x, x1.y);
+}
+
+__global__ __launch_bounds__(64 * kDecWaves) void k_decode_split(DecodeArgs p) {
   __shared__ __attribute__((aligned(16))) uint2 vlut[256];
-  __shared__ __attribute__((aligned(16))) float qs[kDecWaves][8][kD];          // per wave: rotated queries
-  __shared__ __attribute__((aligned(16))) uint32_t meta[kDecWaves][2][kD / 2];  // per wave: step, min
-  __shared__ float wstate[kDecWaves][2][8];                                     // m, l per wave and head
+  __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];                     // rotated queries (padded rows)
+  __shared__ float amax_w[kDecWaves];
+  __shared__ __attribute__((aligned(16))) uint32_t meta[kDecWaves][2][2][kD / 2];  // [wave][side][step, min]
+  __shared__ float wstate[kDecWaves][2][8];                                        // m, l per wave and head
   __shared__ uint32_t wmask[kDecWaves];
-  __shared__ __attribute__((aligned(16))) float wacc[kDecWaves][24][kD];        // rows 0-15 set 1, 16-23 set 2
+  // per wave: accumulator rows for the combine (rows 0-15 set 1, 16-23 set 2)
+  __shared__ __attribute__((aligned(16))) float wacc[kDecWaves][24][kD + 4];  // padded rows: conflict-free
 
   const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
-  const int col = lane & 15, g = lane >> 4, hd = col & 7;
-  const bool upper = col >= 8;  // this lane's QK column holds tokens 16..31 of the window
-  const int len = min(p.seq_lens[b], p.cap);  // memory-safe if device and host lengths disagree
-  const int nwin = (len + kW - 1) / kW;
-  const int w_begin = split * p.wps;
-  const int w_end = min(w_begin + p.wps, nwin);
+  const int col = lane & 15, g = lane >> 4, hd = col & 7, side = col >> 3;
+  const bool upper = side != 0;
   const size_t seq = (size_t)b * p.H + h;
   float* rec = p.ws + (seq * p.nsplit + split) * kRecFloats;
+  const int w_begin = split * p.wps;
+  const int w_plan = min(w_begin + p.wps, p.cap / kW);  // windows of this split by the plan
+  const int wA0 = w_begin + 2 * wave;                    // this wave's pairs: (wA0 + 16 k, +1)
+
+  // ---- every global load of the prologue goes out before any of them is used: the query rows
+  // (waves 0-3), the first pair (speculatively: windows within the plan, the length is checked
+  // later), and the sequence length ----
+  const int hr = 2 * wave + (lane >> 5), c4 = 4 * (lane & 31);
+  uint2 qraw = make_uint2(0, 0);
+  uint32_t qsgn = 0;
+  if (wave < 4 && hr < p.G) {
+    qraw = *reinterpret_cast<const uint2*>(p.q + ((size_t)b * p.Hq + h * p.G + hr) * kD + c4);
+    qsgn = *reinterpret_cast<const uint32_t*>(p.signs + c4);
+  }
+  PairLoad cur;
+  if (wA0 < w_plan) cur = load_pair(p, seq, b, wA0, wA0 + 1 < w_plan, lane);
+  const int len = min(p.seq_lens[b], p.cap);  // memory-safe if device and host lengths disagree
+  const int nwin = (len + kW - 1) / kW;
+  const int w_end = min(w_plan, nwin);
   if (w_begin >= w_end) {  // empty split (ragged batch): mark and leave
     if (tid < 8) {
       rec[tid] = -__builtin_inff();
@@ -132,89 +189,58 @@ __global__ __launch_bounds__(256, 2) void k_decode_split(DecodeArgs p) {
     if (tid == 0) reinterpret_cast<uint32_t*>(rec)[16] = 0u;
     return;
   }
-  // first window's loads go out before the prologue
-  const int w0 = w_begin + wave;
-  WinLoad cur;
-  if (w0 < w_end) cur = load_window(p, seq, b, w0, lane);
 
-  {  // code-byte table: byte -> four fp16 codebook levels (tokens 0..3 of the byte)
+  if (tid < 256) {  // code-byte table: byte -> four fp16 codebook levels (tokens 0..3 of the byte)
     const uint32_t lv[4] = {p.cb01 & 0xffffu, p.cb01 >> 16, p.cb23 & 0xffffu, p.cb23 >> 16};
     vlut[tid] = make_uint2(lv[tid & 3] | (lv[(tid >> 2) & 3] << 16), lv[(tid >> 4) & 3] | (lv[tid >> 6] << 16));
   }
-
-  // ---- per-wave query rotation: lane holds channels 16 (l % 8) + i of head l / 8 ----
-  float qv[16];
-  {
-    const int hr = lane >> 3, cb = 16 * (lane & 7);
-    if (hr < p.G) {
-      const uint4* src = reinterpret_cast<const uint4*>(p.q + ((size_t)b * p.Hq + h * p.G + hr) * kD + cb);
-      const uint4 a = src[0], c = src[1];
-      const uint4 sg = *reinterpret_cast<const uint4*>(p.signs + cb);
-      const uint32_t qw[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
-      const uint32_t sw[4] = {sg.x, sg.y, sg.z, sg.w};
+  // ---- query rotation: wave w < 4 rotates heads 2w, 2w+1; lane holds channels c4 .. c4+3 ----
+  float x[4] = {0.f, 0.f, 0.f, 0.f};
+  if (wave < 4) {
+    const uint32_t rr[2] = {qraw.x, qraw.y};
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float x = h2f((qw[i >> 1] >> (16 * (i & 1))) & 0xffffu);
-        qv[i] = (sw[i >> 2] >> (8 * (i & 3) + 7)) & 1u ? -x : x;
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) qv[i] = 0.0f;
+    for (int i = 0; i < 4; ++i) {
+      const float v = h2f((rr[i >> 1] >> (16 * (i & 1))) & 0xffffu);
+      x[i] = ((qsgn >> (8 * i + 7)) & 1u) ? -v : v;
+    }
+    {  // channel bits 0, 1 in lane
+      const float a = x[0] + x[1], c = x[0] - x[1], d = x[2] + x[3], e = x[2] - x[3];
+      x[0] = a + d;
+      x[2] = a - d;
+      x[1] = c + e;
+      x[3] = c - e;
     }
 #pragma unroll
-    for (int hs = 1; hs < 16; hs <<= 1) {  // butterflies on channel bits 0..3 (in lane)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        if ((i & hs) == 0) {
-          const float a = qv[i], c = qv[i + hs];
-          qv[i] = a + c;
-          qv[i + hs] = a - c;
-        }
-      }
-    }
-#pragma unroll
-    for (int lb = 1; lb < 8; lb <<= 1) {  // channel bits 4..6 live in lane bits 0..2
+    for (int lb = 1; lb < 32; lb <<= 1) {  // channel bits 2..6 are lane bits 0..4
       const bool hi = (lane & lb) != 0;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float o = __shfl_xor(qv[i], lb);
-        qv[i] = hi ? o - qv[i] : qv[i] + o;
+      for (int i = 0; i < 4; ++i) {
+        const float o = __shfl_xor(x[i], lb);
+        x[i] = hi ? o - x[i] : x[i] + o;
       }
     }
-  }
-  float amax = 0.0f;
+    float am = 0.0f;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    qv[i] *= p.qscale;
-    amax = fmaxf(amax, fabsf(qv[i]));
-  }
+    for (int i = 0; i < 4; ++i) {
+      x[i] *= p.qscale;
+      am = fmaxf(am, fabsf(x[i]));
+    }
 #pragma unroll
-  for (int lb = 1; lb < 64; lb <<= 1) amax = fmaxf(amax, __shfl_xor(amax, lb));
+    for (int lb = 1; lb < 64; lb <<= 1) am = fmaxf(am, __shfl_xor(am, lb));
+    if (lane == 0) amax_w[wave] = am;
+  }
+  __syncthreads();
+  const float amax = fmaxf(fmaxf(amax_w[0], amax_w[1]), fmaxf(amax_w[2], amax_w[3]));  // waves 0-3 rotate
   // power-of-two scale k0 keeps |q'_c step_c 2^(k0 - 2j)| <= 2^15 (|step| <= 2/3 + rounding)
   const int k0 = (amax > 0.0f) ? min(max(14 - ilogbf(amax), -60), 60) : 0;
   const float kscale = ldexpf(1.0f, 24 - k0);  // undoes 2^(k0 - 24) on the MFMA result
-  {
-    float4* dst = reinterpret_cast<float4*>(&qs[wave][lane >> 3][16 * (lane & 7)]);
+  if (wave < 4) {  // store q' pre-scaled by 2^(k0 - shift(c)), shift(c) = code_shift(c % 8)
+    float o[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dst[i] = make_float4(qv[4 * i], qv[4 * i + 1], qv[4 * i + 2], qv[4 * i + 3]);
+    for (int i = 0; i < 4; ++i) o[i] = ldexpf(x[i], k0 - code_shift((c4 + i) & 7));
+    *reinterpret_cast<float4*>(&qs[hr][c4]) = make_float4(o[0], o[1], o[2], o[3]);
   }
-  wave_lds_sync();
-  // qk[kk][i][hh] = q'[hd][32 g + slot channel] * 2^(k0 - shift of pair 4 (kk & 1) + i)
-  float qk[4][4][2];
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const float4 v4 = *reinterpret_cast<const float4*>(&qs[wave][hd][32 * g + 16 * (kk >> 1) + 8 * hh + 4 * (kk & 1)]);
-      const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float x = (hd < p.G) ? vv[i] : 0.0f;
-        qk[kk][i][hh] = ldexpf(x, k0 - code_shift(4 * (kk & 1) + i));
-      }
-    }
-  }
-  __syncthreads();  // code-byte table ready
+  __syncthreads();
 
   floatx4 acc1[8], acc2[8];
 #pragma unroll
@@ -224,30 +250,38 @@ __global__ __launch_bounds__(256, 2) void k_decode_split(DecodeArgs p) {
   }
   float m_run = -__builtin_inff(), l_run = 0.0f;
   uint32_t seen = 0;  // modalities seen by this wave
-  const int own_tok = 16 * (upper ? 1 : 0) + 4 * g;  // first of this lane's 4 score rows
+  uint32_t* mw = &meta[wave][side][0][0];
 
-  for (int w = w0; w < w_end; w += kDecWaves) {
-    const int t0 = w * kW;
-    WinLoad nxt = cur;
-    if (w + kDecWaves < w_end) nxt = load_window(p, seq, b, w + kDecWaves, lane);  // prefetch
+  for (int wA = wA0; wA < w_end; wA += 2 * kDecWaves) {
+    const bool hasB = wA + 1 < w_end;
+    const int wS = wA + side;
+    const bool side_ok = !upper || hasB;
+    PairLoad nxt = cur;
+    {
+      const int wn = wA + 2 * kDecWaves;
+      if (wn < w_end) nxt = load_pair(p, seq, b, wn, wn + 1 < w_end, lane);  // prefetch
+    }
 
-    // ---- per-window metadata through wave-private LDS ----
-    meta[wave][0][16 * g + col] = cur.stp;
-    meta[wave][1][16 * g + col] = cur.mnp;
+    // ---- side window metadata through wave-private LDS ----
+    *reinterpret_cast<uint2*>(&mw[16 * g + 2 * (col & 7)]) = cur.stp;
+    *reinterpret_cast<uint2*>(&mw[kD / 2 + 16 * g + 2 * (col & 7)]) = cur.mnp;
     wave_lds_sync();
 
-    // ---- B operands (q' step 2^(k0 - shift)) and the per-window bias q'.m, by shift class ----
+    // ---- B operand (q' step 2^(k0 - shift)) and the bias q'.m of the side window ----
     uint32_t bq[4][4];
     float bsum[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const int dw = 16 * g + 8 * (kk >> 1) + 2 * (kk & 1);  // dword of channel 32g + 16(kk>>1) + 4(kk&1)
-      const uint2 s0 = *reinterpret_cast<const uint2*>(&meta[wave][0][dw]);
-      const uint2 s1 = *reinterpret_cast<const uint2*>(&meta[wave][0][dw + 4]);
-      const uint2 m0 = *reinterpret_cast<const uint2*>(&meta[wave][1][dw]);
-      const uint2 m1 = *reinterpret_cast<const uint2*>(&meta[wave][1][dw + 4]);
+      const uint2 s0 = *reinterpret_cast<const uint2*>(&mw[dw]);
+      const uint2 s1 = *reinterpret_cast<const uint2*>(&mw[dw + 4]);
+      const uint2 m0 = *reinterpret_cast<const uint2*>(&mw[kD / 2 + dw]);
+      const uint2 m1 = *reinterpret_cast<const uint2*>(&mw[kD / 2 + dw + 4]);
       const uint32_t sh[2][2] = {{s0.x, s0.y}, {s1.x, s1.y}};
       const uint32_t mh[2][2] = {{m0.x, m0.y}, {m1.x, m1.y}};
+      const float4 q0 = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 16 * (kk >> 1) + 4 * (kk & 1)]);
+      const float4 q1 = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 16 * (kk >> 1) + 8 + 4 * (kk & 1)]);
+      const float qk[2][4] = {{q0.x, q0.y, q0.z, q0.w}, {q1.x, q1.y, q1.z, q1.w}};  // zero rows for heads >= G
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int cls = code_shift(4 * (kk & 1) + i) >> 1;
@@ -256,45 +290,51 @@ __global__ __launch_bounds__(256, 2) void k_decode_split(DecodeArgs p) {
         for (int hh = 0; hh < 2; ++hh) {
           const float stf = h2f((sh[hh][i >> 1] >> (16 * (i & 1))) & 0xffffu);
           const float mnf = h2f((mh[hh][i >> 1] >> (16 * (i & 1))) & 0xffffu);
-          prod[hh] = qk[kk][i][hh] * stf;
-          bsum[cls] = __builtin_fmaf(qk[kk][i][hh], mnf, bsum[cls]);
+          prod[hh] = qk[hh][i] * stf;
+          bsum[cls] = __builtin_fmaf(qk[hh][i], mnf, bsum[cls]);
         }
         bq[kk][i] = pack2(prod[0], prod[1]);
       }
     }
     float bias = bsum[0] + 4.0f * bsum[1] + 16.0f * bsum[2] + 64.0f * bsum[3] + 256.0f * bsum[4];
-    bias += __shfl_xor(bias, 16);
-    bias += __shfl_xor(bias, 32);
+    bias += fxor16(bias);
+    bias += fxor32(bias);
     bias = ldexpf(bias, -k0);
-    wave_lds_sync();  // metadata reads done before the next window overwrites it
+    wave_lds_sync();  // metadata reads done before the next pair overwrites it
 
-    // ---- scores: 8 MFMAs, block-diagonal over the two token halves ----
-    floatx4 sc = {0.f, 0.f, 0.f, 0.f};
+    // ---- scores: two 16-token tiles, each 8 MFMAs block-diagonal over the pair ----
+    floatx4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
       const bool mine = (kk >= 4) == upper;
       const half8 bop = mine ? h8(bq[kk & 3][0], bq[kk & 3][1], bq[kk & 3][2], bq[kk & 3][3]) : h8(0, 0, 0, 0);
-      const half8 aop =
-          (kk < 4) ? key_a_operand(cur.kc0.x, cur.kc0.y, kk & 3) : key_a_operand(cur.kc1.x, cur.kc1.y, kk & 3);
-      sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, bop, sc, 0, 0, 0);
+      const half8 a0 = (kk < 4) ? key_a_operand(cur.ka0.x, cur.ka0.y, kk & 3) : key_a_operand(cur.kb0.x, cur.kb0.y, kk & 3);
+      const half8 a1 = (kk < 4) ? key_a_operand(cur.ka1.x, cur.ka1.y, kk & 3) : key_a_operand(cur.kb1.x, cur.kb1.y, kk & 3);
+      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bop, sc0, 0, 0, 0);
+      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bop, sc1, 0, 0, 0);
     }
 
-    // ---- online softmax (base 2) ----
-    const float nkf[4] = {h2f(cur.nk.x & 0xffffu), h2f(cur.nk.x >> 16), h2f(cur.nk.y & 0xffffu), h2f(cur.nk.y >> 16)};
-    const float nvf[4] = {h2f(cur.nv.x & 0xffffu), h2f(cur.nv.x >> 16), h2f(cur.nv.y & 0xffffu), h2f(cur.nv.y >> 16)};
-    float s[4];
+    // ---- online softmax (base 2) over the pair's 64 tokens ----
+    const uint32_t nkw[4] = {cur.nk0.x, cur.nk0.y, cur.nk1.x, cur.nk1.y};
+    const uint32_t nvw[4] = {cur.nv0.x, cur.nv0.y, cur.nv1.x, cur.nv1.y};
+    float s[8];
     float wmax = -__builtin_inff();
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const bool valid = (t0 + own_tok + i) < len;
-      s[i] = valid ? nkf[i] * __builtin_fmaf(sc[i], kscale, bias) : -__builtin_inff();
-      wmax = fmaxf(wmax, s[i]);
+    for (int e = 0; e < 8; ++e) {  // e = 4 t + i: token 16 t + 4 g + i of the side window
+      const int t = e >> 2, i = e & 3;
+      const bool valid = side_ok && (kW * wS + 16 * t + 4 * g + i) < len;
+      const float nkf = h2f((nkw[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+      const float raw = t ? sc1[i] : sc0[i];
+      s[e] = valid ? nkf * __builtin_fmaf(raw, kscale, bias) : -__builtin_inff();
+      wmax = fmaxf(wmax, s[e]);
     }
-    wmax = fmaxf(wmax, __shfl_xor(wmax, 8));
-    wmax = fmaxf(wmax, __shfl_xor(wmax, 16));
-    wmax = fmaxf(wmax, __shfl_xor(wmax, 32));
-    const float m_new = fmaxf(m_run, wmax);
-    if (__any(m_new > m_run)) {
+    wmax = fmaxf(wmax, fswap8(wmax));
+    wmax = fmaxf(wmax, fxor16(wmax));
+    wmax = fmaxf(wmax, fxor32(wmax));
+    // lazy rescale: the reference m_run moves only when the max exceeds it by more than 2^8, so
+    // p = 2^(s - m_run) <= 2^8; p n_v is stored as fp16 times 2^-8 (undone in the epilogue)
+    if (__any(wmax > m_run + kLazy)) {
+      const float m_new = fmaxf(m_run, wmax);
       const float alpha = exp2f(m_run - m_new);
       l_run *= alpha;
       float arow[4];
@@ -310,60 +350,71 @@ __global__ __launch_bounds__(256, 2) void k_decode_split(DecodeArgs p) {
       }
       m_run = m_new;
     }
-    float pv[4];
+    float pv[8];
     uint32_t mods = 0;
+    const uint32_t mdw[2] = {cur.md0, cur.md1};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float pr = exp2f(s[i] - m_run);
+    for (int e = 0; e < 8; ++e) {
+      const int t = e >> 2, i = e & 3;
+      const float pr = exp2f(s[e] - m_run);
       l_run += pr;
-      const bool valid = (t0 + own_tok + i) < len;
-      pv[i] = valid ? pr * nvf[i] : 0.0f;
-      if (valid) mods |= 1u << ((cur.md >> (8 * i)) & 3u);
+      const bool valid = side_ok && (kW * wS + 16 * t + 4 * g + i) < len;
+      const float nvf = h2f((nvw[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+      pv[e] = valid ? pr * nvf * kPvScale : 0.0f;
+      if (valid) mods |= 1u << ((mdw[t] >> (8 * i)) & 3u);
     }
     const bool any_av = __any((mods & 3u) != 0);
     const bool any_t = __any((mods & 4u) != 0);
     seen |= (__any((mods & 1u) != 0) ? 1u : 0u) | (__any((mods & 2u) != 0) ? 2u : 0u) | (any_t ? 4u : 0u);
 
-    // ---- value B operands from the code-byte table ----
-    const uint32_t vw[4] = {cur.vc.x, cur.vc.y, cur.vc.z, cur.vc.w};
-    auto vop = [&](int nb) -> half8 {
-      const uint32_t b0 = (vw[nb >> 2] >> (8 * (nb & 3))) & 0xffu;        // tokens 4g .. 4g+3
-      const uint32_t b1 = (vw[2 + (nb >> 2)] >> (8 * (nb & 3))) & 0xffu;  // tokens 16+4g ..
-      const uint2 x0 = vlut[b0];
-      const uint2 x1 = vlut[b1];
-      return h8(x0.x, x0.y, x1.x, x1.y);
-    };
-
-    if (any_av) {
-      float keep[4], send[4];
+    // ---- values: one PV MFMA per window and 16-channel block, A = masked p n_v ----
+    if (any_av) {  // set 1: rows 0-7 audio heads, rows 8-15 video heads
+      uint32_t keep[4], send[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t mi = (cur.md >> (8 * i)) & 0xffu;
-        const float pa = (mi == 0u) ? pv[i] : 0.0f;    // audio
-        const float pvid = (mi == 1u) ? pv[i] : 0.0f;  // video
-        keep[i] = upper ? pvid : pa;
-        send[i] = upper ? pa : pvid;
+      for (int q = 0; q < 4; ++q) {
+        float kv[2], sv[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int e = 2 * q + u, t = e >> 2, i = e & 3;
+          const uint32_t mi = (mdw[t] >> (8 * i)) & 0xffu;
+          const float pa = (mi == 0u) ? pv[e] : 0.0f;
+          const float pvid = (mi == 1u) ? pv[e] : 0.0f;
+          kv[u] = upper ? pvid : pa;
+          sv[u] = upper ? pa : pvid;
+        }
+        keep[q] = pack2(kv[0], kv[1]);
+        send[q] = swap8(pack2(sv[0], sv[1]));
       }
-      const uint32_t k01 = pack2(keep[0], keep[1]), k23 = pack2(keep[2], keep[3]);
-      const uint32_t r01 = swap8(pack2(send[0], send[1])), r23 = swap8(pack2(send[2], send[3]));
-      const half8 aop = upper ? h8(r01, r23, k01, k23) : h8(k01, k23, r01, r23);
+      const half8 opA = upper ? h8(send[0], send[1], send[2], send[3]) : h8(keep[0], keep[1], keep[2], keep[3]);
+      const half8 opB = upper ? h8(keep[0], keep[1], keep[2], keep[3]) : h8(send[0], send[1], send[2], send[3]);
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, vop(nb), acc1[nb], 0, 0, 0);
+      for (int nb = 0; nb < 8; ++nb) {
+        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(opA, lut_op(vlut, cur.va, nb), acc1[nb], 0, 0, 0);
+        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(opB, lut_op(vlut, cur.vb, nb), acc1[nb], 0, 0, 0);
+      }
     }
-    if (any_t) {
-      float keep[4], send[4];
+    if (any_t) {  // set 2: rows 0-7 text heads
+      uint32_t keep[4], recv[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t mi = (cur.md >> (8 * i)) & 0xffu;
-        const float pt = (mi == 2u) ? pv[i] : 0.0f;
-        keep[i] = upper ? 0.0f : pt;
-        send[i] = upper ? pt : 0.0f;
+      for (int q = 0; q < 4; ++q) {
+        float kv[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int e = 2 * q + u, t = e >> 2, i = e & 3;
+          const uint32_t mi = (mdw[t] >> (8 * i)) & 0xffu;
+          kv[u] = (mi == 2u) ? pv[e] : 0.0f;
+        }
+        keep[q] = pack2(kv[0], kv[1]);
+        recv[q] = swap8(keep[q]);
       }
-      const uint32_t k01 = pack2(keep[0], keep[1]), k23 = pack2(keep[2], keep[3]);
-      const uint32_t r01 = swap8(pack2(send[0], send[1])), r23 = swap8(pack2(send[2], send[3]));
-      const half8 aop = upper ? h8(0, 0, 0, 0) : h8(k01, k23, r01, r23);
+      const half8 zero = h8(0, 0, 0, 0);
+      const half8 opA = upper ? zero : h8(keep[0], keep[1], keep[2], keep[3]);
+      const half8 opB = upper ? zero : h8(recv[0], recv[1], recv[2], recv[3]);
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) acc2[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(aop, vop(nb), acc2[nb], 0, 0, 0);
+      for (int nb = 0; nb < 8; ++nb) {
+        acc2[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(opA, lut_op(vlut, cur.va, nb), acc2[nb], 0, 0, 0);
+        acc2[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(opB, lut_op(vlut, cur.vb, nb), acc2[nb], 0, 0, 0);
+      }
     }
     cur = nxt;
   }
@@ -377,18 +428,32 @@ __global__ __launch_bounds__(256, 2) void k_decode_split(DecodeArgs p) {
     wstate[wave][1][lane] = l_run;
   }
   if (lane == 0) wmask[wave] = seen;
-#pragma unroll
-  for (int nb = 0; nb < 8; ++nb) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      wacc[wave][4 * g + i][16 * nb + col] = acc1[nb][i];
-      if (g < 2) wacc[wave][16 + 4 * g + i][16 * nb + col] = acc2[nb][i];
-    }
-  }
   __syncthreads();
   uint32_t mask = 0;
 #pragma unroll
   for (int w = 0; w < kDecWaves; ++w) mask |= wmask[w];
+  float frow[4];  // 2^(m_wave - M) for this lane's accumulator rows (head (4g + i) % 8)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int head = (4 * g + i) & 7;
+    float M = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, wstate[w][0][head]);
+    const float mwv = wstate[wave][0][head];
+    frow[i] = (mwv == -__builtin_inff()) ? 0.0f : exp2f(mwv - M) * (1.0f / kPvScale);
+  }
+  if (mask & 3u) {
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) wacc[wave][4 * g + i][16 * nb + col] = acc1[nb][i] * frow[i];
+  }
+  if ((mask & 4u) && g < 2) {
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) wacc[wave][16 + 4 * g + i][16 * nb + col] = acc2[nb][i] * frow[i];
+  }
   if (tid < 8) {
     float M = -__builtin_inff();
 #pragma unroll
@@ -396,150 +461,190 @@ __global__ __launch_bounds__(256, 2) void k_decode_split(DecodeArgs p) {
     float L = 0.0f;
 #pragma unroll
     for (int w = 0; w < kDecWaves; ++w) {
-      const float mw = wstate[w][0][tid];
-      L += (mw == -__builtin_inff()) ? 0.0f : wstate[w][1][tid] * exp2f(mw - M);
+      const float mwv = wstate[w][0][tid];
+      L += (mwv == -__builtin_inff()) ? 0.0f : wstate[w][1][tid] * exp2f(mwv - M);
     }
     rec[tid] = M;
     rec[8 + tid] = L;
   }
   if (tid == 0) reinterpret_cast<uint32_t*>(rec)[16] = mask;
+  __syncthreads();
   // acc rows: 0-7 audio, 8-15 video (set 1), 16-23 text (set 2) -> record [modality][head][ch]
-  for (int idx = tid; idx < 24 * kD; idx += 256) {
-    const int row = idx >> 7, ch = idx & 127;
-    const int mod = row >> 3, head = row & 7;
-    if (!(mask & (1u << mod))) continue;
-    float M = -__builtin_inff();
+  for (int idx4 = tid; idx4 < 24 * kD / 4; idx4 += 64 * kDecWaves) {
+    const int row = idx4 >> 5, c4 = (idx4 & 31) * 4;
+    if (!(mask & (1u << (row >> 3)))) continue;
+    float4 a = *reinterpret_cast<const float4*>(&wacc[0][row][c4]);
 #pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, wstate[w][0][head]);
-    float a = 0.0f;
-#pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) {
-      const float mw = wstate[w][0][head];
-      if (mw != -__builtin_inff()) a += wacc[w][row][ch] * exp2f(mw - M);
+    for (int w = 1; w < kDecWaves; ++w) {
+      const float4 v = *reinterpret_cast<const float4*>(&wacc[w][row][c4]);
+      a.x += v.x;
+      a.y += v.y;
+      a.z += v.z;
+      a.w += v.w;
     }
-    rec[kRecHeader + idx] = a;
+    *reinterpret_cast<float4*>(rec + kRecHeader + row * kD + c4) = a;
   }
 }
 
-// ---- log-sum-exp merge over splits and the inverse value rotation, fused ----
-// One block (256 threads) per (query head j, 16-channel slice of the output, sequence b):
-//  1. M = max_s m_s, weights w_s = 2^(m_s - M), L = sum_s w_s l_s;
-//  2. acc_m = sum_s w_s acc_{s,m} for the three modalities (all 128 rotated channels);
-//  3. o_c = sum_m sum_k acc_m[k] R_m[k][c] / L for the slice's 16 channels (Sec. 2.3: once per
-//     modality after aggregation, not once per cached value).
-__global__ __launch_bounds__(256) void k_decode_merge(const float* __restrict__ ws, const int32_t* __restrict__ seq_lens,
-                                                      const float* __restrict__ rot, int H, int Hq, int G, int wps,
-                                                      int nsplit, int cap, float* __restrict__ out) {
-  __shared__ float wts[kMaxSplits];
-  __shared__ uint32_t msk[kMaxSplits];
-  __shared__ float red[256];
-  __shared__ __attribute__((aligned(16))) float part[8][3][kD];
-  __shared__ float acc[3][kD];
+// ---- merge over splits and inverse value rotation, fused ----
+// One block (512 threads) per (query head j, 32-channel slice of the output, sequence b):
+//  1. M = max_s m_s, w_s = 2^(m_s - M), L = sum_s w_s l_s (log-sum-exp merge of the splits);
+//  2. acc_m = sum_s w_s acc_{s,m} for the three modalities, all 128 rotated channels;
+//  3. o_c = sum_m sum_k acc_m[k] R_m[k][c] / L for the slice (the inverse rotation is applied
+//     once per modality after aggregation, Sec. 2.3).
+constexpr int kMergeThreads = 512;
+constexpr int kMergeWaves = kMergeThreads / 64;
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int lb = 1; lb < 64; lb <<= 1) v = fmaxf(v, __shfl_xor(v, lb));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int lb = 1; lb < 64; lb <<= 1) v += __shfl_xor(v, lb);
+  return v;
+}
+
+__global__ __launch_bounds__(kMergeThreads) void k_decode_merge(const float* __restrict__ ws,
+                                                                const int32_t* __restrict__ seq_lens,
+                                                                const float* __restrict__ rot, int H, int Hq, int G,
+                                                                int wps, int nsplit, int cap, float* __restrict__ out) {
+  __shared__ float wred[2][kMergeWaves];
+  __shared__ __attribute__((aligned(16))) float part[16][3][kD];
+  __shared__ float acc[3 * kD];
+  __shared__ float ored[16][32];
   const int j = blockIdx.x, slice = blockIdx.y, b = blockIdx.z;
   const int h = j / G, hd = j % G;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, wave = tid >> 6;
+  const int q4 = tid & 31, grp = tid >> 5;               // channel quad, split group of 16
+  const int c = 32 * slice + (tid & 31), ks = tid >> 5;  // output channel, one of 16 slices of (m, k)
+  const float* base = ws + ((size_t)b * H + h) * nsplit * kRecFloats;
+  const float* colp = base + kRecHeader + hd * kD + 4 * q4;
+
+  // ---- every global load goes out first: rotation column slice, the length, and the first 64
+  // splits' headers and accumulator quads (read unconditionally, selected by the mask later) ----
+  float rv[24];
+#pragma unroll
+  for (int i = 0; i < 24; ++i) rv[i] = rot[(size_t)(ks * 24 + i) * kD + c];
   const int len = min(seq_lens[b], cap);
   const int ns = min((len + kW - 1) / kW + wps - 1, nsplit * wps) / wps;  // non-empty splits
-  const float* base = ws + ((size_t)b * H + h) * nsplit * kRecFloats;
+  float4 v[4][3];
+  float mh[4];
+  uint32_t mk[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int sidx = grp + 16 * t;
+    const bool ok = sidx < ns;
+    const float* rs = base + (size_t)(ok ? sidx : 0) * kRecFloats;
+    mh[t] = ok ? rs[hd] : -__builtin_inff();
+    mk[t] = ok ? reinterpret_cast<const uint32_t*>(rs)[16] : 0u;
+#pragma unroll
+    for (int m = 0; m < 3; ++m)
+      v[t][m] = ok ? *reinterpret_cast<const float4*>(colp + (size_t)sidx * kRecFloats + m * 8 * kD)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
 
+  // ---- M = max_s m_s, L = sum_s 2^(m_s - M) l_s ----
   float mloc = -__builtin_inff();
-  for (int s = tid; s < ns; s += 256) mloc = fmaxf(mloc, base[(size_t)s * kRecFloats + hd]);
-  red[tid] = mloc;
+  for (int sidx = tid; sidx < ns; sidx += kMergeThreads) mloc = fmaxf(mloc, base[(size_t)sidx * kRecFloats + hd]);
+  mloc = wave_max(mloc);
+  if ((tid & 63) == 0) wred[0][wave] = mloc;
   __syncthreads();
-  for (int st = 128; st > 0; st >>= 1) {
-    if (tid < st) red[tid] = fmaxf(red[tid], red[tid + st]);
-    __syncthreads();
-  }
-  const float M = red[0];
-  __syncthreads();
+  float M = wred[0][0];
+#pragma unroll
+  for (int w = 1; w < kMergeWaves; ++w) M = fmaxf(M, wred[0][w]);
   float lloc = 0.0f;
-  for (int s = tid; s < ns; s += 256) {
-    const float* rs = base + (size_t)s * kRecFloats;
+  for (int sidx = tid; sidx < ns; sidx += kMergeThreads) {
+    const float* rs = base + (size_t)sidx * kRecFloats;
     const float ms = rs[hd];
-    const float wgt = (ms == -__builtin_inff()) ? 0.0f : exp2f(ms - M);
-    wts[s] = wgt;
-    msk[s] = reinterpret_cast<const uint32_t*>(rs)[16];
-    lloc += wgt * rs[8 + hd];
+    lloc += (ms == -__builtin_inff()) ? 0.0f : exp2f(ms - M) * rs[8 + hd];
   }
-  red[tid] = lloc;
-  __syncthreads();
-  for (int st = 128; st > 0; st >>= 1) {
-    if (tid < st) red[tid] += red[tid + st];
-    __syncthreads();
-  }
-  const float L = red[0];
+  lloc = wave_sum(lloc);
+  if ((tid & 63) == 0) wred[1][wave] = lloc;
 
-  // 2. weighted sum over splits: thread = (channel quad, split group of 8)
-  {
-    const int qd = tid & 31, grp = tid >> 5;
-    float4 a[3] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
-    for (int s = grp; s < ns; s += 8) {
-      const float wgt = wts[s];
-      const uint32_t mk = msk[s];
-      const float* rs = base + (size_t)s * kRecFloats + kRecHeader;
+  // ---- weighted sum of the accumulators over splits ----
+  float4 a[3];
+#pragma unroll
+  for (int m = 0; m < 3; ++m) a[m] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = 0;; s0 += 64) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const float wgt = (mh[t] == -__builtin_inff()) ? 0.0f : exp2f(mh[t] - M);
 #pragma unroll
       for (int m = 0; m < 3; ++m) {
-        if (mk & (1u << m)) {
-          const float4 v = *reinterpret_cast<const float4*>(rs + (m * 8 + hd) * kD + 4 * qd);
-          a[m].x += wgt * v.x;
-          a[m].y += wgt * v.y;
-          a[m].z += wgt * v.z;
-          a[m].w += wgt * v.w;
-        }
+        const bool has = (mk[t] >> m) & 1u;  // absent modality: region never written, skip it
+        const float4 x = has ? v[t][m] : make_float4(0.f, 0.f, 0.f, 0.f);
+        a[m].x = __builtin_fmaf(wgt, x.x, a[m].x);
+        a[m].y = __builtin_fmaf(wgt, x.y, a[m].y);
+        a[m].z = __builtin_fmaf(wgt, x.z, a[m].z);
+        a[m].w = __builtin_fmaf(wgt, x.w, a[m].w);
       }
     }
+    if (s0 + 64 >= ns) break;
 #pragma unroll
-    for (int m = 0; m < 3; ++m) *reinterpret_cast<float4*>(&part[grp][m][4 * qd]) = a[m];
-  }
-  __syncthreads();
-  for (int idx = tid; idx < 3 * kD; idx += 256) {
-    const int m = idx >> 7, k = idx & 127;
-    float sacc = 0.0f;
+    for (int t = 0; t < 4; ++t) {  // more than 64 splits: next chunk
+      const int sidx = s0 + 64 + grp + 16 * t;
+      const bool ok = sidx < ns;
+      const float* rs = base + (size_t)(ok ? sidx : 0) * kRecFloats;
+      mh[t] = ok ? rs[hd] : -__builtin_inff();
+      mk[t] = ok ? reinterpret_cast<const uint32_t*>(rs)[16] : 0u;
 #pragma unroll
-    for (int g8 = 0; g8 < 8; ++g8) sacc += part[g8][m][k];
-    acc[m][k] = sacc;
+      for (int m = 0; m < 3; ++m)
+        v[t][m] = ok ? *reinterpret_cast<const float4*>(colp + (size_t)sidx * kRecFloats + m * 8 * kD)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
   }
+#pragma unroll
+  for (int m = 0; m < 3; ++m) *reinterpret_cast<float4*>(&part[grp][m][4 * q4]) = a[m];
   __syncthreads();
-
-  // 3. un-rotate the slice: thread = (channel of the slice, one of 16 k-slices of 24 (m, k) pairs)
-  const int c = 16 * slice + (tid & 15), ks = tid >> 4;
-  float o = 0.0f;
-#pragma unroll 4
-  for (int i = 0; i < 24; ++i) {
-    const int idx = ks * 24 + i;
-    const int m = idx >> 7, k = idx & 127;
-    o = __builtin_fmaf(acc[m][k], rot[((size_t)m * kD + k) * kD + c], o);
-  }
-  red[tid] = o;
-  __syncthreads();
-  if (tid < 16) {
+  float L = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kMergeWaves; ++w) L += wred[1][w];
+  if (tid < 3 * kD) {
+    const int m = tid >> 7, k = tid & 127;
     float t = 0.0f;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) t += red[q * 16 + tid];
-    out[((size_t)b * Hq + j) * kD + 16 * slice + tid] = (L > 0.0f) ? t / L : 0.0f;
+    for (int q = 0; q < 16; ++q) t += part[q][m][k];
+    acc[tid] = t;
+  }
+  __syncthreads();
+  // ---- inverse rotation of the slice: o_c = sum_m sum_k acc_m[k] R_m[k][c] / L ----
+  float o = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 24; ++i) o = __builtin_fmaf(acc[ks * 24 + i], rv[i], o);  // index = m * 128 + k
+  ored[ks][tid & 31] = o;
+  __syncthreads();
+  if (tid < 32) {
+    float t = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) t += ored[q][tid];
+    out[((size_t)b * Hq + j) * kD + 32 * slice + tid] = (L > 0.0f) ? t / L : 0.0f;
   }
 }
 
 DecodePlan plan_decode(int B, int H, int max_len) {
   const int nwin = (max_len + kW - 1) / kW;
   const long units = (long)B * H;
-  long target_groups = 512;  // about two work-groups per compute unit
+  long target_groups = 256;  // one work-group per compute unit
   if (const char* env = getenv("OKVQ_DECODE_GROUPS")) target_groups = std::max(1L, atol(env));
   int wps = (int)((nwin * units + target_groups - 1) / target_groups);
   wps = std::max(wps, kMinWps);
   wps = std::max(wps, (nwin + kMaxSplits - 1) / kMaxSplits);
+  wps = (wps + 1) / 2 * 2;  // whole window pairs
   DecodePlan p;
   p.wins_per_split = wps;
   p.nsplit = nwin > 0 ? (nwin + wps - 1) / wps : 1;
   return p;
 }
 
-size_t decode_workspace_bytes(int B, int H, int /*Hq*/, int max_len) {
+static size_t record_bytes(int B, int H, int max_len) {
   const int nwin = (max_len + kW - 1) / kW;
-  const int wps_min = std::max(kMinWps, (nwin + kMaxSplits - 1) / kMaxSplits);
-  const int nsplit_max = nwin > 0 ? (nwin + wps_min - 1) / wps_min : 1;
-  return (size_t)B * H * nsplit_max * kRecFloats * sizeof(float);
+  const int nsplit_max = nwin > 0 ? (nwin + kMinWps - 1) / kMinWps : 1;
+  return (size_t)B * H * std::min(nsplit_max, kMaxSplits) * kRecFloats * sizeof(float);
 }
+
+size_t decode_workspace_bytes(int B, int H, int /*Hq*/, int max_len) { return record_bytes(B, H, max_len); }
 
 hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, float* out, void* ws,
                          const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int /*max_len*/) {
@@ -565,11 +670,11 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
   a.qscale = sm_scale * 1.4426950408889634f * 0.08838834764831845f;
   a.cb01 = cb01;
   a.cb23 = cb23;
-  hipLaunchKernelGGL(k_decode_split, dim3(plan.nsplit, c.H, c.B), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_decode_split, dim3(plan.nsplit, c.H, c.B), dim3(64 * kDecWaves), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_decode_merge, dim3(c.Hq, kD / 16, c.B), dim3(256), 0, s, a.ws, c.seq_lens, c.rot, c.H, c.Hq,
-                     G, plan.wins_per_split, plan.nsplit, c.cap, out);
+  hipLaunchKernelGGL(k_decode_merge, dim3(c.Hq, kD / 32, c.B), dim3(kMergeThreads), 0, s, a.ws, c.seq_lens, c.rot,
+                     c.H, c.Hq, G, plan.wins_per_split, plan.nsplit, c.cap, out);
   return hipGetLastError();
 }
 
