@@ -11,15 +11,15 @@
 //
 // Lane mapping: phase A (lane = token) keeps the 128 channels of a row in registers, so the
 // norm tree and all seven butterfly stages run without cross-lane traffic. Phase B transposes
-// z through a wave-private LDS tile, 32 channels at a time (lane = channel of one window), for
-// the window min / max. Phase C (lane = token) computes and packs the codes.
+// z through a wave-private LDS tile, 64 channels at a time (lane = channel quad of half a
+// window), for the window min / max. Phase C (lane = token) computes and packs the codes.
 #pragma once
 
 #include "okvq_device.hpp"
 
 namespace okvq {
 
-constexpr int kKeyPitch = 33;  // LDS row pitch (floats) of the transpose tile: conflict-free columns
+constexpr int kKeyPitch = 68;  // LDS row pitch (floats) of the 64-channel transpose tile: 16 lanes hit distinct banks
 constexpr int kKeyWaveLds = 64 * kKeyPitch + 2 * kD * 2;  // floats per wave: tile + (m, 1/step) x 2 windows
 
 struct KeyWaveOut {
@@ -78,44 +78,82 @@ __device__ __forceinline__ void key_quantize_wave(const uint32_t (&raw)[64], int
       }
     }
   }
-  const float n16f = h2f(n16);
-  const float cinv = div_rn(kKappa, n16f);
-  const bool zero_norm = (n16 == 0);
+  // n16 == 0 only for an all-zero row (a nonzero fp16 element has a square >= 2^-48), whose
+  // butterflies are all +-0: a zero factor gives z = +-0, which min/max (+0 canonicalization) and
+  // the code formula treat exactly like z = 0.
+  const float cinv = (n16 == 0) ? 0.0f : div_rn(kKappa, h2f(n16));
 #pragma unroll
-  for (int c = 0; c < kD; ++c) x[c] = zero_norm ? 0.0f : x[c] * cinv;
+  for (int c = 0; c < kD; ++c) x[c] = x[c] * cinv;
 
-  // ---- phase B: window min / max through LDS (lane = channel of window lane/32) ----
-  float* tile = lds;
-  float* stats = lds + 64 * kKeyPitch;  // [2][128] x (m32, inv32)
-  const int ch = lane & 31;
-  const int win = lane >> 5;
+  // ---- phase B: window min / max through LDS, 64 channels at a time. Lane l reads channel quad
+  // l % 16 of rows 16 ((l / 16) % 2) .. +15 of window l / 32; the two row halves are combined with
+  // lane l ^ 16. Rows beyond a partial window's length re-read its last valid row. ----
+  float* tile = lds;                          // [64 tokens][kKeyPitch]
+  float* stats = lds + 64 * kKeyPitch;        // [2 windows][128 channels] x (m32, inv32)
+  const int qd = lane & 15, half = (lane >> 4) & 1, win = lane >> 5;
   const int nvalid = min(max(len - (tok0 + 32 * win), 0), 32);
+  const bool full = __all(nvalid == 32);      // both windows complete: constant row offsets
   const int gwin = (tok0 >> 5) + win;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
+  for (int q = 0; q < 2; ++q) {
 #pragma unroll
-    for (int j = 0; j < 32; ++j) tile[lane * kKeyPitch + j] = x[32 * q + j];
+    for (int j = 0; j < 16; ++j)
+      *reinterpret_cast<float4*>(&tile[lane * kKeyPitch + 4 * j]) =
+          make_float4(x[64 * q + 4 * j], x[64 * q + 4 * j + 1], x[64 * q + 4 * j + 2], x[64 * q + 4 * j + 3]);
     wave_lds_sync();
-    float lo = __builtin_inff(), hi = -__builtin_inff();
+    float lo[4], hi[4];
 #pragma unroll
-    for (int r = 0; r < 32; ++r) {
-      const float v = tile[(32 * win + r) * kKeyPitch + ch];
-      if (r < nvalid) {
-        lo = fminf(lo, v);
-        hi = fmaxf(hi, v);
+    for (int i = 0; i < 4; ++i) {
+      lo[i] = __builtin_inff();
+      hi[i] = -__builtin_inff();
+    }
+    const float* colp = tile + (32 * win + 16 * half) * kKeyPitch + 4 * qd;
+    if (full) {
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const float4 v = *reinterpret_cast<const float4*>(colp + rr * kKeyPitch);
+        lo[0] = __builtin_fminf(lo[0], v.x); hi[0] = __builtin_fmaxf(hi[0], v.x);
+        lo[1] = __builtin_fminf(lo[1], v.y); hi[1] = __builtin_fmaxf(hi[1], v.y);
+        lo[2] = __builtin_fminf(lo[2], v.z); hi[2] = __builtin_fmaxf(hi[2], v.z);
+        lo[3] = __builtin_fminf(lo[3], v.w); hi[3] = __builtin_fmaxf(hi[3], v.w);
+      }
+    } else {
+      const float* rowbase = tile + 32 * win * kKeyPitch + 4 * qd;
+      const int last = max(nvalid - 1, 0);
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const int row = min(16 * half + rr, last);
+        const float4 v = *reinterpret_cast<const float4*>(rowbase + row * kKeyPitch);
+        lo[0] = __builtin_fminf(lo[0], v.x); hi[0] = __builtin_fmaxf(hi[0], v.x);
+        lo[1] = __builtin_fminf(lo[1], v.y); hi[1] = __builtin_fmaxf(hi[1], v.y);
+        lo[2] = __builtin_fminf(lo[2], v.z); hi[2] = __builtin_fmaxf(hi[2], v.z);
+        lo[3] = __builtin_fminf(lo[3], v.w); hi[3] = __builtin_fmaxf(hi[3], v.w);
       }
     }
-    if (nvalid > 0) {
-      lo = lo + 0.0f;  // canonical +0
-      hi = hi + 0.0f;
-      const float step = div_rn(hi - lo, 3.0f);
-      const uint32_t m16 = f2h(lo);
-      const uint32_t s16 = f2h(step);
-      const int c = 32 * q + ch;
-      out.kmin[gwin * kD + c] = (uint16_t)m16;
-      out.kstep[gwin * kD + c] = (uint16_t)s16;
-      stats[(win * kD + c) * 2 + 0] = h2f(m16);
-      stats[(win * kD + c) * 2 + 1] = (s16 == 0) ? 0.0f : div_rn(1.0f, h2f(s16));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      lo[i] = __builtin_fminf(lo[i], __shfl_xor(lo[i], 16));
+      hi[i] = __builtin_fmaxf(hi[i], __shfl_xor(hi[i], 16));
+    }
+    if (half == 0 && nvalid > 0) {
+      uint32_t m16[4], s16[4];
+      float st[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float l0 = lo[i] + 0.0f;  // canonical +0
+        const float h0 = hi[i] + 0.0f;
+        const float step = div_rn(h0 - l0, 3.0f);
+        m16[i] = f2h(l0);
+        s16[i] = f2h(step);
+        st[2 * i] = h2f(m16[i]);
+        st[2 * i + 1] = (s16[i] == 0) ? 0.0f : div_rn(1.0f, h2f(s16[i]));
+      }
+      const int c = 64 * q + 4 * qd;
+      *reinterpret_cast<uint2*>(out.kmin + gwin * kD + c) = make_uint2(m16[0] | (m16[1] << 16), m16[2] | (m16[3] << 16));
+      *reinterpret_cast<uint2*>(out.kstep + gwin * kD + c) = make_uint2(s16[0] | (s16[1] << 16), s16[2] | (s16[3] << 16));
+      float4* sp = reinterpret_cast<float4*>(stats + (win * kD + c) * 2);
+      sp[0] = make_float4(st[0], st[1], st[2], st[3]);
+      sp[1] = make_float4(st[4], st[5], st[6], st[7]);
     }
     wave_lds_sync();
   }

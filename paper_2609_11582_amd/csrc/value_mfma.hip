@@ -154,35 +154,33 @@ __global__ __launch_bounds__(256, 2) void k_quantize_values_mfma(CodecJob j, con
     }
     __syncthreads();
     if (!(wave_present & (1u << m))) continue;  // wave-uniform
-    uint32_t rb_mask = 0;
+    // one straight-line MFMA sweep (8 output blocks x 4 k-blocks x hi/lo) per 16-token row block that
+    // holds modality m; row blocks without it are skipped by a wave-uniform branch
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
-      if (__ballot((mymod == m) && ((lane >> 4) == rb))) rb_mask |= 1u << rb;
+    for (int rb = 0; rb < 4; ++rb) {
+      if (!__ballot((mymod == m) && ((lane >> 4) == rb))) continue;
+      floatx4 acc[8];
 #pragma unroll
-    for (int nb = 0; nb < 8; ++nb) {
-      floatx4 acc[4];
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb) acc[rb] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int nb = 0; nb < 8; ++nb) acc[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const int off = (16 * nb + r) * kRPitch + 32 * kk + 8 * g;
-        const half8 bh = *reinterpret_cast<const half8*>(rhi + off);
-        const half8 bl = *reinterpret_cast<const half8*>(rlo + off);
+        const half8 av = as_half8(a[rb][kk]);
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb) {
-          if (rb_mask & (1u << rb)) {
-            acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(a[rb][kk]), bh, acc[rb], 0, 0, 0);
-            acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(a[rb][kk]), bl, acc[rb], 0, 0, 0);
+        for (int part = 0; part < 2; ++part) {  // hi then lo: eight independent accumulators in between
+          const _Float16* rp = part ? rlo : rhi;
+#pragma unroll
+          for (int nb = 0; nb < 8; ++nb) {
+            const half8 bv = *reinterpret_cast<const half8*>(rp + (16 * nb + r) * kRPitch + 32 * kk + 8 * g);
+            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bv, acc[nb], 0, 0, 0);
           }
         }
       }
 #pragma unroll
-      for (int rb = 0; rb < 4; ++rb) {
-        if (!(rb_mask & (1u << rb))) continue;
+      for (int nb = 0; nb < 8; ++nb) {
         uint32_t byte = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const uint32_t code = value_code(acc[rb][i], nrow[rb][i], th);
+          const uint32_t code = value_code(acc[nb][i], nrow[rb][i], th);
           byte |= (mrow[rb][i] == m ? code : 0u) << (2 * i);
         }
         bytes[rb][nb >> 2] |= byte << (8 * (nb & 3));
