@@ -138,8 +138,7 @@ def main():
         for name in c.buffers:
             c.buffers[name].copy_(caches[0].buffers[name])
     q = torch.from_numpy(gen_queries(wl.wid, 0, B, Hq)).to(dev)
-    ws_bytes = okvq.okvq_decode_workspace_bytes(caches[0].dims, max(lens))
-    ws = torch.empty(ws_bytes // 4 + 4, dtype=torch.float32, device=dev)
+    ws = okvq.decode_workspace(caches[0].dims, max(lens), device=dev)
     out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
     sm = 1 / math.sqrt(128)
 

@@ -100,6 +100,9 @@ typedef struct {               /* all pointers are device memory, laid out as ab
   int32_t* seq_lens;
   const int8_t* key_signs;     /* [128] +1 / -1: H = Had diag(s) / sqrt(128) (Eq. 2)        */
   const float* v_rot;          /* [3][128][128] fp32 row-major R_m, z = R_m u (Eq. 6)       */
+  const uint16_t* v_rot16;     /* [128][3][128] fp16, written by okvq_prepare_rotation from
+                                  v_rot: element (c, m, k) = R_m[k][c], the inverse rotation
+                                  that decode applies once per modality (Sec. 2.3)           */
 } okvq_cache;
 
 /* Library version (major * 10000 + minor * 100 + patch). */
@@ -155,17 +158,27 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
                         const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
                         const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream);
 
-/* Device workspace bytes needed by okvq_decode_attention for sequences up to max_seq_len. */
+/* Inverse value rotation table for decode (Sec. 2.3: the inverse rotation is applied once per
+ * modality after aggregation). Per layer, once: v_rot16[c][m][k] = fp16(v_rot[m][k][c]) (RNE).
+ *   v_rot    device f32 [3][128][128]
+ *   v_rot16  device f16 [128][3][128] (98304 bytes), the okvq_cache.v_rot16 of every cache
+ *            that uses v_rot */
+okvq_status okvq_prepare_rotation(const float* v_rot, uint16_t* v_rot16, void* stream);
+
+/* Device workspace bytes needed by okvq_decode_attention for sequences up to max_seq_len (the
+ * partial results of the split-K launch; no initial contents are needed). */
 size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len);
 
-/* One decode step: attention of one query per head over the packed cache (Eq. 1).
+/* One decode step: attention of one query per head over the packed cache (Eq. 1): a split-K
+ * launch over windows and a log-sum-exp merge launch.
  *   lens_host  host i32 [B] (plans the split-K launch; the kernels read cache->seq_lens)
  *   q          device f16 [B][Hq][128]
  *   sm_scale   softmax scale, normally 1/sqrt(128)
  *   out        device f32 [B][Hq][128]
  *   workspace  device, at least okvq_decode_workspace_bytes(dims, max(lens_host)) bytes
- * A sequence of length 0 yields zeros. fp32 accumulation; the result matches float64 attention
- * over the dequantized cache within 2e-3 of the output norm. */
+ * Needs cache->v_rot16 (okvq_prepare_rotation). A sequence of length 0 yields zeros. fp32
+ * accumulation; the result matches float64 attention over the dequantized cache within 2e-3 of
+ * the output norm. */
 okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,
                                   float sm_scale, uint32_t flags, float* out, void* workspace,
                                   size_t workspace_bytes, void* stream);

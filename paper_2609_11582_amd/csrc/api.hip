@@ -80,7 +80,7 @@ okvq_status check_cache(const okvq_cache* c) {
   okvq_status st = check_dims(&c->dims);
   if (st != OKVQ_OK) return st;
   const void* ptrs[] = {c->k_codes, c->v_codes, c->k_norm, c->v_norm, c->k_min, c->k_step,
-                        c->modality, c->k_stage, c->seq_lens, c->key_signs, c->v_rot};
+                        c->modality, c->k_stage, c->seq_lens, c->key_signs, c->v_rot, c->v_rot16};
   for (const void* p : ptrs)
     if (!aligned16(p)) return OKVQ_ERR_INVALID_ARGUMENT;
   return OKVQ_OK;
@@ -103,6 +103,7 @@ CacheView view(const okvq_cache* c) {
   v.seq_lens = c->seq_lens;
   v.signs = c->key_signs;
   v.rot = c->v_rot;
+  v.rot16t = c->v_rot16;
   return v;
 }
 
@@ -258,6 +259,11 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
     if (st != OKVQ_OK) return st;
   }
   return hip_status(launch_advance_lengths(cache->seq_lens, n_new_dev, d.batch, s));
+}
+
+okvq_status okvq_prepare_rotation(const float* v_rot, uint16_t* v_rot16, void* stream) {
+  if (!aligned16(v_rot) || !aligned16(v_rot16)) return OKVQ_ERR_INVALID_ARGUMENT;
+  return hip_status(launch_prepare_rotation(v_rot, v_rot16, static_cast<hipStream_t>(stream)));
 }
 
 size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len) {

@@ -1,9 +1,11 @@
 // Fused decode attention over the packed 2-bit cache (Eq. 1 with the codecs of Eq. 2, 4, 6).
 //
-// Split-K flash decoding. Work-group (split, KV head h, sequence b) = 4 waves; wave w takes the
-// split's window pairs (2w + 8k, 2w + 8k + 1) and keeps its own online-softmax state; the waves
-// are combined in LDS and one partial record per work-group is written. A second kernel merges
-// the splits (log-sum-exp) and applies the inverse value rotation once per modality.
+// Split-K flash decoding in two launches. k_decode: work-group (split, KV head h, sequence b) =
+// 8 waves; wave w takes the split's window pairs (2w + 16k, 2w + 16k + 1) and keeps its own
+// online-softmax state. The waves are combined in LDS, the split's per-modality accumulators are
+// un-rotated on MFMA (the inverse rotation is linear, so applying it per split and then merging
+// equals applying it once per modality after aggregation, Sec. 2.3) and one normalized partial
+// output per split is written. k_decode_merge combines the splits by log-sum-exp.
 //
 // What one wave does per window (all G <= 8 query heads of the KV head from one read):
 //  * scores in the rotated key space (Sec. 2.3): s_i = n_i (q'.m_g + sum_c q'_c step_gc code_ic),
@@ -29,8 +31,9 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kDecWaves = 8;                         // waves per split work-group
-constexpr int kRecHeader = 32;                       // m[8], l[8], mask, pad
-constexpr int kRecFloats = kRecHeader + 3 * 8 * kD;  // + acc[3 modalities][8 heads][128]
+constexpr int kRecHeader = 32;                       // m[8], l[8], pad
+constexpr int kRecFloats = kRecHeader + 8 * kD;      // + o[8 heads][128], un-rotated, divided by l
+constexpr int kATile = 3 * kD + 8;                   // fp16 row pitch of the un-rotation A tile
 constexpr int kMinWps = 2 * kDecWaves;              // fewest windows per split (a pair per wave)
 constexpr int kMaxSplits = 1024;                     // most splits per (sequence, KV head)
 constexpr float kLazy = 8.0f;                        // log2 headroom of the lazily updated softmax max
@@ -47,7 +50,8 @@ struct DecodeArgs {
   const int32_t* seq_lens;
   const int8_t* signs;
   const uint16_t* q;
-  float* ws;
+  const uint16_t* rot16t;  // [128][3][128] fp16: (c, m, k) -> R_m[k][c]
+  float* ws;               // partial records [B][H][nsplit][kRecFloats]
   int H, Hq, G, cap, wps, nsplit;
   float qscale;      // sm_scale * log2(e) / sqrt(128)
   uint32_t cb01;     // fp16 codebook levels 0, 1 (low, high half)
@@ -146,15 +150,34 @@ __device__ __forceinline__ half8 lut_op(const uint2* vlut, uint4 vc, int nb) {
   return h8(x0.x, x0.y, x1.x, x1.y);
 }
 
-__global__ __launch_bounds__(64 * kDecWaves) void k_decode_split(DecodeArgs p) {
+typedef unsigned short ushort2v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pkmax_u16(uint32_t a, uint32_t b) {
+  return __builtin_bit_cast(uint32_t,
+                            __builtin_elementwise_max(__builtin_bit_cast(ushort2v, a), __builtin_bit_cast(ushort2v, b)));
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int lb = 1; lb < 64; lb <<= 1) v = fmaxf(v, __shfl_xor(v, lb));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int lb = 1; lb < 64; lb <<= 1) v += __shfl_xor(v, lb);
+  return v;
+}
+
+__global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   __shared__ __attribute__((aligned(16))) uint2 vlut[256];
   __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];                     // rotated queries (padded rows)
   __shared__ float amax_w[kDecWaves];
   __shared__ __attribute__((aligned(16))) uint32_t meta[kDecWaves][2][2][kD / 2];  // [wave][side][step, min]
   __shared__ float wstate[kDecWaves][2][8];                                        // m, l per wave and head
   __shared__ uint32_t wmask[kDecWaves];
-  // per wave: accumulator rows for the combine (rows 0-15 set 1, 16-23 set 2)
+  __shared__ uint32_t wnv[kDecWaves];                                              // value-norm maxima
+  // per wave: accumulator rows for the combine (rows 0-15 set 1, 16-23 set 2); the merge reuses it
   __shared__ __attribute__((aligned(16))) float wacc[kDecWaves][24][kD + 4];  // padded rows: conflict-free
+  __shared__ __attribute__((aligned(16))) _Float16 atile[8][kATile];         // merged rows, fp16
+  __shared__ float hst[8];                                                   // per head: scale
 
   const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
@@ -181,12 +204,11 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode_split(DecodeArgs p) {
   const int len = min(p.seq_lens[b], p.cap);  // memory-safe if device and host lengths disagree
   const int nwin = (len + kW - 1) / kW;
   const int w_end = min(w_plan, nwin);
-  if (w_begin >= w_end) {  // empty split (ragged batch): mark and leave
+  if (w_begin >= w_end) {  // empty split (ragged batch): a header the merge skips
     if (tid < 8) {
       rec[tid] = -__builtin_inff();
       rec[8 + tid] = 0.0f;
     }
-    if (tid == 0) reinterpret_cast<uint32_t*>(rec)[16] = 0u;
     return;
   }
 
@@ -250,6 +272,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode_split(DecodeArgs p) {
   }
   float m_run = -__builtin_inff(), l_run = 0.0f;
   uint32_t seen = 0;  // modalities seen by this wave
+  uint32_t nvm = 0;   // largest value norm seen by this lane (two fp16 halves, non-negative)
   uint32_t* mw = &meta[wave][side][0][0];
 
   for (int wA = wA0; wA < w_end; wA += 2 * kDecWaves) {
@@ -317,6 +340,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode_split(DecodeArgs p) {
     // ---- online softmax (base 2) over the pair's 64 tokens ----
     const uint32_t nkw[4] = {cur.nk0.x, cur.nk0.y, cur.nk1.x, cur.nk1.y};
     const uint32_t nvw[4] = {cur.nv0.x, cur.nv0.y, cur.nv1.x, cur.nv1.y};
+    nvm = pkmax_u16(nvm, pkmax_u16(pkmax_u16(nvw[0], nvw[1]), pkmax_u16(nvw[2], nvw[3])));
     float s[8];
     float wmax = -__builtin_inff();
 #pragma unroll
@@ -419,19 +443,42 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode_split(DecodeArgs p) {
     cur = nxt;
   }
 
+  // ---- epilogue. This wave's slice of the inverse-rotation table (output channels 16 wave ..
+  // 16 wave + 15, all 384 (modality, k) rows) as MFMA B operands, loaded first so that the
+  // combine below hides the latency ----
+  uint4 rb[12];
+  {
+    const uint4* rp = reinterpret_cast<const uint4*>(p.rot16t) + (size_t)(16 * wave + (lane & 15)) * 48 + (lane >> 4);
+#pragma unroll
+    for (int kk = 0; kk < 12; ++kk) rb[kk] = rp[4 * kk];
+  }
+
   // ---- combine the waves of the work-group ----
   l_run += __shfl_xor(l_run, 8);
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
+#pragma unroll
+  for (int lb = 1; lb < 64; lb <<= 1) nvm = pkmax_u16(nvm, (uint32_t)__shfl_xor((int)nvm, lb));
   if (lane < 8) {
     wstate[wave][0][lane] = m_run;
     wstate[wave][1][lane] = l_run;
   }
-  if (lane == 0) wmask[wave] = seen;
+  if (lane == 0) {
+    wmask[wave] = seen;
+    wnv[wave] = max(nvm & 0xffffu, nvm >> 16);
+  }
   __syncthreads();
-  uint32_t mask = 0;
+  uint32_t mask = 0, nmax = 0;
 #pragma unroll
-  for (int w = 0; w < kDecWaves; ++w) mask |= wmask[w];
+  for (int w = 0; w < kDecWaves; ++w) {
+    mask |= wmask[w];
+    nmax = max(nmax, wnv[w]);
+  }
+  // Every merged row divided by its softmax sum is a convex combination of n_v cb vectors, so
+  // its entries are below n_max * 2^-2.9 (the largest codebook level is 0.1335): the factor
+  // 2^e / L with e = 15 - ilogb(n_max) keeps the fp16 A tile below 2^13.
+  const float nmf = h2f(nmax);
+  const int e = (nmf > 0.0f) ? 15 - min(max(ilogbf(nmf), -30), 20) : 0;
   float frow[4];  // 2^(m_wave - M) for this lane's accumulator rows (head (4g + i) % 8)
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -464,15 +511,16 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode_split(DecodeArgs p) {
       const float mwv = wstate[w][0][tid];
       L += (mwv == -__builtin_inff()) ? 0.0f : wstate[w][1][tid] * exp2f(mwv - M);
     }
+    hst[tid] = (tid < p.G && L > 0.0f) ? ldexpf(1.0f / L, e) : 0.0f;
     rec[tid] = M;
     rec[8 + tid] = L;
   }
-  if (tid == 0) reinterpret_cast<uint32_t*>(rec)[16] = mask;
   __syncthreads();
-  // acc rows: 0-7 audio, 8-15 video (set 1), 16-23 text (set 2) -> record [modality][head][ch]
+  // acc rows 0-7 audio, 8-15 video (set 1), 16-23 text (set 2), summed over the waves and scaled
+  // -> A tile [head][128 m + k] (fp16)
   for (int idx4 = tid; idx4 < 24 * kD / 4; idx4 += 64 * kDecWaves) {
-    const int row = idx4 >> 5, c4 = (idx4 & 31) * 4;
-    if (!(mask & (1u << (row >> 3)))) continue;
+    const int row = idx4 >> 5, c4 = (idx4 & 31) * 4, m = row >> 3, head = row & 7;
+    if (!(mask & (1u << m))) continue;
     float4 a = *reinterpret_cast<const float4*>(&wacc[0][row][c4]);
 #pragma unroll
     for (int w = 1; w < kDecWaves; ++w) {
@@ -482,144 +530,114 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode_split(DecodeArgs p) {
       a.z += v.z;
       a.w += v.w;
     }
-    *reinterpret_cast<float4*>(rec + kRecHeader + row * kD + c4) = a;
+    const float f = hst[head];
+    *reinterpret_cast<uint2*>(&atile[head][m * kD + c4]) = make_uint2(pack2(a.x * f, a.y * f), pack2(a.z * f, a.w * f));
+  }
+  __syncthreads();
+  // ---- inverse rotation on MFMA, once per present modality: wave w computes channels
+  // c = 16 w .. 16 w + 15 of o[head][c] = sum_m sum_k A[head][128 m + k] R_m[k][c]. A rows 8-15
+  // (lanes whose row is >= 8) only feed output rows that are not stored. ----
+  floatx4 dacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int m = 0; m < 3; ++m) {
+    if (!(mask & (1u << m))) continue;
+#pragma unroll
+    for (int k4 = 0; k4 < 4; ++k4) {
+      const int kk = 4 * m + k4;
+      const half8 a = *reinterpret_cast<const half8*>(&atile[lane & 7][32 * kk + 8 * (lane >> 4)]);
+      dacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(half8, rb[kk]), dacc, 0, 0, 0);
+    }
+  }
+  if (lane < 32) {
+    const float sc = ldexpf(1.0f, -e);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rec[kRecHeader + (4 * (lane >> 4) + i) * kD + 16 * wave + (lane & 15)] = dacc[i] * sc;
   }
 }
 
-// ---- merge over splits and inverse value rotation, fused ----
-// One block (512 threads) per (query head j, 32-channel slice of the output, sequence b):
-//  1. M = max_s m_s, w_s = 2^(m_s - M), L = sum_s w_s l_s (log-sum-exp merge of the splits);
-//  2. acc_m = sum_s w_s acc_{s,m} for the three modalities, all 128 rotated channels;
-//  3. o_c = sum_m sum_k acc_m[k] R_m[k][c] / L for the slice (the inverse rotation is applied
-//     once per modality after aggregation, Sec. 2.3).
-constexpr int kMergeThreads = 512;
-constexpr int kMergeWaves = kMergeThreads / 64;
+// ---- merge over splits: o = sum_s 2^(M_s - M) L_s o_s / sum_s 2^(M_s - M) L_s (log-sum-exp) ----
+// One work-group of 256 threads per (query head j, sequence b): thread (split group sg, channel
+// quad q4) sums the splits s = sg (mod 8). Every load is issued before any is used; empty splits
+// carry M = -inf and are skipped (their outputs were never written).
+constexpr int kMergeThreads = 256;
+constexpr int kMergeUnroll = 8;  // splits per thread held in registers at once
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int lb = 1; lb < 64; lb <<= 1) v = fmaxf(v, __shfl_xor(v, lb));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int lb = 1; lb < 64; lb <<= 1) v += __shfl_xor(v, lb);
-  return v;
-}
-
-__global__ __launch_bounds__(kMergeThreads) void k_decode_merge(const float* __restrict__ ws,
-                                                                const int32_t* __restrict__ seq_lens,
-                                                                const float* __restrict__ rot, int H, int Hq, int G,
-                                                                int wps, int nsplit, int cap, float* __restrict__ out) {
-  __shared__ float wred[2][kMergeWaves];
-  __shared__ __attribute__((aligned(16))) float part[16][3][kD];
-  __shared__ float acc[3 * kD];
-  __shared__ float ored[16][32];
-  const int j = blockIdx.x, slice = blockIdx.y, b = blockIdx.z;
+__global__ __launch_bounds__(kMergeThreads) void k_decode_merge(const float* __restrict__ ws, int H, int Hq, int G,
+                                                                int nsplit, float* __restrict__ out) {
+  __shared__ float red[2][kMergeThreads / 64];
+  __shared__ __attribute__((aligned(16))) float4 part[8][32];
+  const int j = blockIdx.x, b = blockIdx.y;
   const int h = j / G, hd = j % G;
-  const int tid = threadIdx.x, wave = tid >> 6;
-  const int q4 = tid & 31, grp = tid >> 5;               // channel quad, split group of 16
-  const int c = 32 * slice + (tid & 31), ks = tid >> 5;  // output channel, one of 16 slices of (m, k)
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int q4 = tid & 31, sg = tid >> 5;
   const float* base = ws + ((size_t)b * H + h) * nsplit * kRecFloats;
-  const float* colp = base + kRecHeader + hd * kD + 4 * q4;
 
-  // ---- every global load goes out first: rotation column slice, the length, and the first 64
-  // splits' headers and accumulator quads (read unconditionally, selected by the mask later) ----
-  float rv[24];
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  float M = -__builtin_inff(), L = 0.0f;
+  // running (M, L, o) over this thread's splits: one pass, all loads of a chunk up front
+  for (int s0 = sg; s0 < nsplit; s0 += 8 * kMergeUnroll) {
+    float ms[kMergeUnroll], ls[kMergeUnroll];
+    float4 v[kMergeUnroll];
 #pragma unroll
-  for (int i = 0; i < 24; ++i) rv[i] = rot[(size_t)(ks * 24 + i) * kD + c];
-  const int len = min(seq_lens[b], cap);
-  const int ns = min((len + kW - 1) / kW + wps - 1, nsplit * wps) / wps;  // non-empty splits
-  float4 v[4][3];
-  float mh[4];
-  uint32_t mk[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int sidx = grp + 16 * t;
-    const bool ok = sidx < ns;
-    const float* rs = base + (size_t)(ok ? sidx : 0) * kRecFloats;
-    mh[t] = ok ? rs[hd] : -__builtin_inff();
-    mk[t] = ok ? reinterpret_cast<const uint32_t*>(rs)[16] : 0u;
-#pragma unroll
-    for (int m = 0; m < 3; ++m)
-      v[t][m] = ok ? *reinterpret_cast<const float4*>(colp + (size_t)sidx * kRecFloats + m * 8 * kD)
-                   : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-
-  // ---- M = max_s m_s, L = sum_s 2^(m_s - M) l_s ----
-  float mloc = -__builtin_inff();
-  for (int sidx = tid; sidx < ns; sidx += kMergeThreads) mloc = fmaxf(mloc, base[(size_t)sidx * kRecFloats + hd]);
-  mloc = wave_max(mloc);
-  if ((tid & 63) == 0) wred[0][wave] = mloc;
-  __syncthreads();
-  float M = wred[0][0];
-#pragma unroll
-  for (int w = 1; w < kMergeWaves; ++w) M = fmaxf(M, wred[0][w]);
-  float lloc = 0.0f;
-  for (int sidx = tid; sidx < ns; sidx += kMergeThreads) {
-    const float* rs = base + (size_t)sidx * kRecFloats;
-    const float ms = rs[hd];
-    lloc += (ms == -__builtin_inff()) ? 0.0f : exp2f(ms - M) * rs[8 + hd];
-  }
-  lloc = wave_sum(lloc);
-  if ((tid & 63) == 0) wred[1][wave] = lloc;
-
-  // ---- weighted sum of the accumulators over splits ----
-  float4 a[3];
-#pragma unroll
-  for (int m = 0; m < 3; ++m) a[m] = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s0 = 0;; s0 += 64) {
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const float wgt = (mh[t] == -__builtin_inff()) ? 0.0f : exp2f(mh[t] - M);
-#pragma unroll
-      for (int m = 0; m < 3; ++m) {
-        const bool has = (mk[t] >> m) & 1u;  // absent modality: region never written, skip it
-        const float4 x = has ? v[t][m] : make_float4(0.f, 0.f, 0.f, 0.f);
-        a[m].x = __builtin_fmaf(wgt, x.x, a[m].x);
-        a[m].y = __builtin_fmaf(wgt, x.y, a[m].y);
-        a[m].z = __builtin_fmaf(wgt, x.z, a[m].z);
-        a[m].w = __builtin_fmaf(wgt, x.w, a[m].w);
-      }
+    for (int u = 0; u < kMergeUnroll; ++u) {
+      const int s = s0 + 8 * u;
+      const float* rs = base + (size_t)min(s, nsplit - 1) * kRecFloats;
+      ms[u] = (s < nsplit) ? rs[hd] : -__builtin_inff();
+      ls[u] = rs[8 + hd];
+      v[u] = *reinterpret_cast<const float4*>(rs + kRecHeader + hd * kD + 4 * q4);
     }
-    if (s0 + 64 >= ns) break;
+    float mc = M;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {  // more than 64 splits: next chunk
-      const int sidx = s0 + 64 + grp + 16 * t;
-      const bool ok = sidx < ns;
-      const float* rs = base + (size_t)(ok ? sidx : 0) * kRecFloats;
-      mh[t] = ok ? rs[hd] : -__builtin_inff();
-      mk[t] = ok ? reinterpret_cast<const uint32_t*>(rs)[16] : 0u;
+    for (int u = 0; u < kMergeUnroll; ++u) mc = fmaxf(mc, ms[u]);
+    if (mc == -__builtin_inff()) continue;
+    const float a = exp2f(M - mc);  // M = -inf -> 0
+    L *= a;
+    o.x *= a;
+    o.y *= a;
+    o.z *= a;
+    o.w *= a;
 #pragma unroll
-      for (int m = 0; m < 3; ++m)
-        v[t][m] = ok ? *reinterpret_cast<const float4*>(colp + (size_t)sidx * kRecFloats + m * 8 * kD)
-                     : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int u = 0; u < kMergeUnroll; ++u) {
+      if (ms[u] == -__builtin_inff()) continue;
+      const float w = exp2f(ms[u] - mc) * ls[u];
+      L += w;
+      o.x = __builtin_fmaf(w, v[u].x, o.x);
+      o.y = __builtin_fmaf(w, v[u].y, o.y);
+      o.z = __builtin_fmaf(w, v[u].z, o.z);
+      o.w = __builtin_fmaf(w, v[u].w, o.w);
     }
+    M = mc;
   }
-#pragma unroll
-  for (int m = 0; m < 3; ++m) *reinterpret_cast<float4*>(&part[grp][m][4 * q4]) = a[m];
+  // combine the 8 split groups: global max, then rescale
+  float mw = wave_max(M);
+  if (lane == 0) red[0][wave] = mw;
   __syncthreads();
-  float L = 0.0f;
+  float Mt = red[0][0];
 #pragma unroll
-  for (int w = 0; w < kMergeWaves; ++w) L += wred[1][w];
-  if (tid < 3 * kD) {
-    const int m = tid >> 7, k = tid & 127;
-    float t = 0.0f;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) t += part[q][m][k];
-    acc[tid] = t;
-  }
-  __syncthreads();
-  // ---- inverse rotation of the slice: o_c = sum_m sum_k acc_m[k] R_m[k][c] / L ----
-  float o = 0.0f;
-#pragma unroll
-  for (int i = 0; i < 24; ++i) o = __builtin_fmaf(acc[ks * 24 + i], rv[i], o);  // index = m * 128 + k
-  ored[ks][tid & 31] = o;
+  for (int w = 1; w < kMergeThreads / 64; ++w) Mt = fmaxf(Mt, red[0][w]);
+  const float a = (M == -__builtin_inff()) ? 0.0f : exp2f(M - Mt);
+  // L is the same for every channel quad of a split group: count it once per group
+  float lw = (q4 == 0) ? L * a : 0.0f;
+  lw = wave_sum(lw);
+  if (lane == 0) red[1][wave] = lw;
+  part[sg][q4] = make_float4(o.x * a, o.y * a, o.z * a, o.w * a);
   __syncthreads();
   if (tid < 32) {
-    float t = 0.0f;
+    float Lt = 0.0f;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) t += ored[q][tid];
-    out[((size_t)b * Hq + j) * kD + 32 * slice + tid] = (L > 0.0f) ? t / L : 0.0f;
+    for (int w = 0; w < kMergeThreads / 64; ++w) Lt += red[1][w];
+    float4 t = part[0][tid];
+#pragma unroll
+    for (int g = 1; g < 8; ++g) {
+      const float4 u = part[g][tid];
+      t.x += u.x;
+      t.y += u.y;
+      t.z += u.z;
+      t.w += u.w;
+    }
+    const float inv = (Lt > 0.0f) ? 1.0f / Lt : 0.0f;
+    *reinterpret_cast<float4*>(out + ((size_t)b * Hq + j) * kD + 4 * tid) =
+        make_float4(t.x * inv, t.y * inv, t.z * inv, t.w * inv);
   }
 }
 
@@ -660,6 +678,7 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
   a.seq_lens = c.seq_lens;
   a.signs = c.signs;
   a.q = q;
+  a.rot16t = c.rot16t;
   a.ws = static_cast<float*>(ws);
   a.H = c.H;
   a.Hq = c.Hq;
@@ -670,11 +689,24 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
   a.qscale = sm_scale * 1.4426950408889634f * 0.08838834764831845f;
   a.cb01 = cb01;
   a.cb23 = cb23;
-  hipLaunchKernelGGL(k_decode_split, dim3(plan.nsplit, c.H, c.B), dim3(64 * kDecWaves), 0, s, a);
+  hipLaunchKernelGGL(k_decode, dim3(plan.nsplit, c.H, c.B), dim3(64 * kDecWaves), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_decode_merge, dim3(c.Hq, kD / 32, c.B), dim3(kMergeThreads), 0, s, a.ws, c.seq_lens, c.rot,
-                     c.H, c.Hq, G, plan.wins_per_split, plan.nsplit, c.cap, out);
+  hipLaunchKernelGGL(k_decode_merge, dim3(c.Hq, c.B), dim3(kMergeThreads), 0, s, a.ws, c.H, c.Hq, G, plan.nsplit, out);
+  return hipGetLastError();
+}
+
+// Inverse-rotation table: element (c, m, k) = fp16(R_m[k][c]), one thread per pair of k.
+__global__ __launch_bounds__(256) void k_prepare_rotation(const float* __restrict__ rot, uint16_t* __restrict__ rot16t) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= kD * 3 * kD / 2) return;
+  const int c = idx / (3 * kD / 2), r = idx % (3 * kD / 2), m = r / (kD / 2), k = 2 * (r % (kD / 2));
+  const float lo = rot[((size_t)m * kD + k) * kD + c], hi = rot[((size_t)m * kD + k + 1) * kD + c];
+  reinterpret_cast<uint32_t*>(rot16t)[idx] = f2h(lo) | (f2h(hi) << 16);
+}
+
+hipError_t launch_prepare_rotation(const float* rot, uint16_t* rot16t, hipStream_t s) {
+  hipLaunchKernelGGL(k_prepare_rotation, dim3(kD * 3 * kD / 2 / 256), dim3(256), 0, s, rot, rot16t);
   return hipGetLastError();
 }
 

@@ -46,6 +46,7 @@ struct CacheView {
   int32_t* seq_lens;
   const int8_t* signs;
   const float* rot;
+  const uint16_t* rot16t;  // [128][3][128] fp16 inverse-rotation table
 };
 
 struct DecodePlan {
@@ -54,6 +55,7 @@ struct DecodePlan {
 };
 DecodePlan plan_decode(int B, int H, int max_len);
 size_t decode_workspace_bytes(int B, int H, int Hq, int max_len);
+hipError_t launch_prepare_rotation(const float* rot, uint16_t* rot16t, hipStream_t s);
 hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, float* out, void* ws,
                          const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int max_len);
 

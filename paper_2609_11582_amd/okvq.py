@@ -36,7 +36,7 @@ class Dims(ctypes.Structure):
 
 class CacheStruct(ctypes.Structure):
     _fields_ = [("dims", Dims)] + [(n, ctypes.c_void_p) for n in BUFFERS] + [
-        ("key_signs", ctypes.c_void_p), ("v_rot", ctypes.c_void_p)]
+        ("key_signs", ctypes.c_void_p), ("v_rot", ctypes.c_void_p), ("v_rot16", ctypes.c_void_p)]
 
 
 _lib = None
@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
         L.okvq_quantize_values.argtypes = [P(Dims), vp, vp, i32, P(i32), vp, u32, vp, vp, vp]
         L.okvq_append.restype = i32
         L.okvq_append.argtypes = [P(CacheStruct), P(i32), vp, vp, vp, P(i32), vp, i32, u32, vp]
+        L.okvq_prepare_rotation.restype = i32
+        L.okvq_prepare_rotation.argtypes = [vp, vp, vp]
         L.okvq_decode_workspace_bytes.restype = sz
         L.okvq_decode_workspace_bytes.argtypes = [P(Dims), i32]
         L.okvq_decode_attention.restype = i32
@@ -175,8 +177,23 @@ def okvq_append(cache: "KVCache", lens, k_new, v_new, mod_new, n_new, n_new_dev,
     return st
 
 
+def okvq_prepare_rotation(v_rot, v_rot16, stream=None, check=True) -> int:
+    _need(v_rot, 3 * 128 * 128 * 4, "v_rot")
+    _need(v_rot16, 3 * 128 * 128 * 2, "v_rot16")
+    st = lib().okvq_prepare_rotation(_ptr(v_rot), _ptr(v_rot16), _stream(stream))
+    if check:
+        _check(st, "okvq_prepare_rotation")
+    return st
+
+
 def okvq_decode_workspace_bytes(dims: Dims, max_seq_len: int) -> int:
     return lib().okvq_decode_workspace_bytes(ctypes.byref(dims), int(max_seq_len))
+
+
+def decode_workspace(dims: Dims, max_seq_len: int, device="cuda") -> torch.Tensor:
+    """A decode workspace of okvq_decode_workspace_bytes bytes (zero-filled, though no contents are needed)."""
+    nbytes = max(okvq_decode_workspace_bytes(dims, max_seq_len), 16)
+    return torch.zeros((nbytes + 15) // 16 * 4, dtype=torch.float32, device=device)
 
 
 def okvq_decode_attention(cache: "KVCache", lens, q, sm_scale, out, workspace, workspace_bytes=None, flags=0,
@@ -200,13 +217,16 @@ _DTYPES = dict(k_codes=torch.uint8, v_codes=torch.uint8, k_norm=torch.float16, v
 
 
 class KVCache:
-    """Device buffers of one layer's packed cache, sized by okvq_buffer_bytes (torch allocations)."""
+    """Device buffers of one layer's packed cache, sized by okvq_buffer_bytes (torch allocations),
+    with the layer's key signs, value rotations and the decode's inverse-rotation table."""
 
     def __init__(self, batch, num_kv_heads, num_q_heads, capacity, key_signs: torch.Tensor, v_rot: torch.Tensor,
                  device="cuda"):
         self.dims = make_dims(batch, num_kv_heads, num_q_heads, capacity)
         self.key_signs = key_signs.to(device=device, dtype=torch.int8).contiguous()
         self.v_rot = v_rot.to(device=device, dtype=torch.float32).contiguous()
+        self.v_rot16 = torch.empty((128, 3 * 128), dtype=torch.float16, device=device)
+        okvq_prepare_rotation(self.v_rot, self.v_rot16)
         self.buffers = {}
         for i, name in enumerate(BUFFERS):
             nbytes = okvq_buffer_bytes(self.dims, i)
@@ -216,7 +236,7 @@ class KVCache:
             n = nbytes // torch.tensor([], dtype=dt).element_size()
             self.buffers[name] = torch.zeros(n, dtype=dt, device=device)
         self.struct = CacheStruct(self.dims, *[self.buffers[n].data_ptr() for n in BUFFERS],
-                                  self.key_signs.data_ptr(), self.v_rot.data_ptr())
+                                  self.key_signs.data_ptr(), self.v_rot.data_ptr(), self.v_rot16.data_ptr())
 
     def __getitem__(self, name):
         return self.buffers[name]

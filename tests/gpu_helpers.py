@@ -88,8 +88,7 @@ def cache_to_numpy(cache):
 
 def decode(cache, q, lens, sm_scale=1 / math.sqrt(128)):
     B, Hq, D = q.shape
-    ws_bytes = okvq.okvq_decode_workspace_bytes(cache.dims, int(max(lens)))
-    ws = torch.empty(max(ws_bytes, 16) // 4 + 4, dtype=torch.float32, device="cuda")
+    ws = okvq.decode_workspace(cache.dims, int(max(lens)))
     out = torch.full((B, Hq, D), float("nan"), dtype=torch.float32, device="cuda")
     okvq.okvq_decode_attention(cache, list(lens), f16dev(q), sm_scale, out, ws)
     torch.cuda.synchronize()

@@ -84,7 +84,7 @@ def test_invalid_arguments_rejected_before_any_launch():
     # unknown flag on values
     assert L.okvq_quantize_values(ctypes.byref(ok_dims), fake, fake, 10, lens, fake, 8, fake, fake, None) == -1
     # decode: workspace too small, bad flags, over capacity
-    cache = okvq.CacheStruct(ok_dims, *([4096] * 9), 4096, 4096)
+    cache = okvq.CacheStruct(ok_dims, *([4096] * 9), 4096, 4096, 4096)
     q_lens = (ctypes.c_int32 * 2)(64, 64)
     assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, 16,
                                    None) == -4
@@ -97,12 +97,27 @@ def test_invalid_arguments_rejected_before_any_launch():
     n_new = (ctypes.c_int32 * 2)(40, 0)
     lens_a = (ctypes.c_int32 * 2)(30, 0)
     assert L.okvq_append(ctypes.byref(cache), lens_a, fake, fake, fake, n_new, fake, 40, 0, None) == -3
-    null_cache = okvq.CacheStruct(ok_dims, *([4096] * 8), 0, 4096, 4096)
+    null_cache = okvq.CacheStruct(ok_dims, *([4096] * 8), 0, 4096, 4096, 4096)
     assert L.okvq_append(ctypes.byref(null_cache), lens_a, fake, fake, fake, n_new, fake, 40, 0, None) == -1
     assert okvq.status_string(-3) == "capacity exceeded"
+    # a cache without the inverse-rotation table, and a misaligned table
+    no_table = okvq.CacheStruct(ok_dims, *([4096] * 9), 4096, 4096, 0)
+    assert L.okvq_decode_attention(ctypes.byref(no_table), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, 1 << 30,
+                                   None) == -1
+    assert L.okvq_prepare_rotation(fake, ctypes.c_void_p(4098), None) == -1
 
 
 @pytest.mark.parametrize("which", range(9))
 def test_buffer_bytes_invalid_dims(which):
     okvq = _lib()
     assert okvq.okvq_buffer_bytes(okvq.make_dims(1, 1, 1, 33), which) == 0
+
+
+def test_package_exports_a_binding_for_every_declared_function():
+    import paper_2609_11582_amd as pkg
+    for n in declared_functions():
+        if n in ("okvq_status_string",):
+            assert hasattr(pkg, "status_string")
+            continue
+        assert hasattr(pkg, n), n
+    assert hasattr(pkg, "decode_workspace") and hasattr(pkg, "KVCache")

@@ -93,3 +93,56 @@ def test_decode_full_size_omni7b_32k():
     r = gh.attention_close(out, ref)
     print(f"omni7b_32k worst err / norm = {r:.2e}")
     assert r <= TOL
+
+
+def test_decode_workspace_reused_across_plans():
+    """One workspace (never cleared) for consecutive calls whose split plans differ."""
+    import torch
+
+    import gpu_helpers as gh
+    import paper_2609_11582_amd as okvq
+    out_a, ref_a, ctx_a = _run("omni7b_32k", [3000, 129], H=2, Hq=14)
+    out_b, ref_b, ctx_b = _run("omni7b_32k", [40], H=2, Hq=14)
+    dims = ctx_a["cache"].dims
+    ws = okvq.decode_workspace(dims, 3000)
+    ws.fill_(float("nan"))  # stale contents must not leak into the result
+    for cache, q, lens, ref in ((ctx_a["cache"], ctx_a["q"], [3000, 129], ref_a),
+                                (ctx_b["cache"], ctx_b["q"], [40], ref_b),
+                                (ctx_a["cache"], ctx_a["q"], [3000, 129], ref_a)):
+        _announce(f"decode reuse lens={lens}")
+        out = torch.full((len(lens), 14, 128), float("nan"), dtype=torch.float32, device="cuda")
+        okvq.okvq_decode_attention(cache, lens, gh.f16dev(q), SM, out, ws)
+        torch.cuda.synchronize()
+        assert gh.attention_close(out.cpu().numpy().astype(np.float64), ref) <= TOL
+
+
+def test_decode_split_count_changes_only_rounding(monkeypatch):
+    """Fewer and more work-groups than the default plan: the log-sum-exp merge gives the same answer
+    up to the fp16 operands (p n_v, and each split's merged rows before the inverse rotation), whose
+    rounding points move with the split boundaries: a few 2^-12 relative steps of the output norm."""
+    import gpu_helpers as gh
+    lens = [5000, 2100]
+    out, ref, ctx = _run("omni7b_32k", lens, H=2, Hq=14)
+    for groups in ("2", "8", "24"):  # 1, 2 and 6 splits per sequence and head instead of 10
+        monkeypatch.setenv("OKVQ_DECODE_GROUPS", groups)
+        _announce(f"decode groups={groups}")
+        o2 = gh.decode(ctx["cache"], ctx["q"], lens)
+        assert gh.attention_close(o2, ref) <= TOL
+        assert gh.attention_close(o2, out) <= 5e-4
+
+
+def test_prepare_rotation_is_fp16_transpose():
+    import torch
+
+    import paper_2609_11582_amd as okvq
+    from synth import gen_rotations
+    rot = gen_rotations(2, 3)
+    rot[1, 5, 7] = 1.0 / 3.0            # a value that is not exact in fp16 (rounds to nearest even)
+    rot[2, 0, 0] = 2.0 ** -25 * 1.5     # an fp16 subnormal after rounding
+    want = np.ascontiguousarray(rot.transpose(2, 0, 1)).astype(np.float16).reshape(128, 384)
+    r_dev = torch.from_numpy(rot).cuda()
+    got = torch.full((128, 384), float("nan"), dtype=torch.float16, device="cuda")
+    _announce("prepare_rotation")
+    okvq.okvq_prepare_rotation(r_dev, got)
+    torch.cuda.synchronize()
+    assert np.array_equal(got.cpu().numpy().view(np.uint16), want.view(np.uint16))
