@@ -10,11 +10,19 @@ dim 128, 32768 cached tokens in 2-second audio-visual chunks (150 video + 25 aud
 per-modality subspaces (seeded generators, no dataset).
 
 Reported (one JSON line):
-  value           decode-attention effective GB/s = algorithmic decode bytes / decode time, with
-                  the cache cold in HBM (the decode cycles through >= 1 GB of cache replicas)
+  value           decode-attention effective GB/s = algorithmic decode bytes / decode time (both
+                  launches, back to back), with the cache cold in HBM (the decode cycles through
+                  >= 1 GB of cache replicas)
   ms_per_step     one step (append prefill + decode), mean over the timed steps
-  roofline        the decode call against the HBM peak; roofline_append the prefill append
+  roofline        the split-K decode kernel (k_decode, the dominant decode launch) against the HBM
+                  peak: algorithmic bytes / its mean duration, timed with HIP events around it;
+                  roofline_append: the whole append call (key, value and length launches)
+  kernels_us      mean duration of each launch, from the same events
   cpu_baseline    the float64 CPU oracle's decode on the same cache, on this host
+
+--profile-pass runs a short fixed sequence for rocprofv3 counter collection: a 256 MiB device
+copy (calibrates FETCH_SIZE / WRITE_SIZE against a known byte count), 8 decode calls on cold
+cache replicas and 2 prefill appends.
 """
 
 from __future__ import annotations
@@ -36,6 +44,7 @@ WORKLOAD = "omni7b_32k"
 DECODE_BYTES_PER_WINDOW_HEAD = 2 * 1024 + 2 * 64 + 2 * 256   # codes K, V + norms K, V + min/step
 APPEND_BYTES_PER_TOKEN_HEAD = 2 * 256 + 84                   # read K, V fp16; write the packed cache
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
+CALIBRATION_COPY_BYTES = 256 << 20
 KERNEL_SOURCES = ("codec_kernels.hip", "value_mfma.hip", "decode_kernels.hip", "key_quant.hpp", "value_quant.hpp",
                   "okvq_device.hpp")
 
@@ -48,10 +57,11 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def decode_algorithmic_bytes(B, H, Hq, lens):
+def decode_algorithmic_bytes(B, H, Hq, lens, with_output=True):
     nwin = sum(-(-int(L) // 32) for L in lens)
     return (nwin * H * DECODE_BYTES_PER_WINDOW_HEAD + nwin * 32      # cache + modality map
-            + B * Hq * 128 * (2 + 4) + 3 * 128 * 128 * 4)            # q in, out, rotations
+            + B * Hq * 128 * (2 + (4 if with_output else 0))          # q in, out
+            + 3 * 128 * 128 * 4)                                      # rotations
 
 
 def append_algorithmic_bytes(B, H, lens):
@@ -83,7 +93,7 @@ def cpu_baseline(cache_np, q, lens, signs, rot, bytes_per_call, min_seconds=10.0
         decode_layer(cache_np, q, lens, signs, rot, 1 / math.sqrt(128))
         calls += 1
         el = time.perf_counter() - t0
-        if el >= min_seconds or calls >= 20:
+        if el >= min_seconds or calls >= 200:
             break
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     return dict(value=round(bytes_per_call * calls / el / 1e9, 4), unit="GB/s", cores=int(threads), kind="oracle",
@@ -98,6 +108,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--decode-iters", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-pass", action="store_true", help="short fixed sequence for rocprofv3 --pmc runs")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by KV head "
@@ -149,6 +160,23 @@ def main():
     def decode(ci):
         okvq.okvq_decode_attention(caches[ci], lens, q, sm, out, ws, stream=stream)
 
+    if args.profile_pass:
+        src = torch.empty(CALIBRATION_COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)  # one copy kernel of known size: reads and writes CALIBRATION_COPY_BYTES
+        torch.cuda.synchronize()
+        for i in range(8):
+            decode((7 * i + 3) % n_cache)
+        torch.cuda.synchronize()
+        for i in range(2):
+            append_into((i + 1) % n_cache, (i + 1) % n_in)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_pass": True, "copy_bytes": CALIBRATION_COPY_BYTES, "decode_calls": 8,
+                          "append_calls": 2, "decode_algorithmic_bytes": decode_algorithmic_bytes(B, H, Hq, lens),
+                          "append_algorithmic_bytes": append_algorithmic_bytes(B, H, lens)}), flush=True)
+        return
+
     # ---- steps: append the prefill into cache replica s, decode a cold replica ----
     for s in range(args.warmup):
         append_into(s % n_cache, s % n_in)
@@ -184,6 +212,20 @@ def main():
         reps.append(e0.elapsed_time(e1) * 1e3 / args.decode_iters)
     decode_us = float(np.median(reps))
 
+    # per-launch durations: HIP events bound to the split-K and merge dispatches (start and end of
+    # each kernel's execution, as the profiler sees them), over cold replicas
+    n_ev = args.decode_iters
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_ev)]
+    for e3 in evs:
+        for e in e3:
+            e.record(stream)  # creates the event handle
+    torch.cuda.synchronize()
+    for i in range(n_ev):
+        okvq.okvq_decode_attention_timed(caches[(i * 7 + 5) % n_cache], lens, q, sm, out, ws, evs[i], stream=stream)
+    torch.cuda.synchronize()
+    split_us = float(np.mean([evs[i][0].elapsed_time(evs[i][1]) for i in range(n_ev)])) * 1e3
+    merge_us = float(np.mean([evs[i][2].elapsed_time(evs[i][3]) for i in range(n_ev)])) * 1e3
+
     # single-call latency including dispatch
     lat = []
     for i in range(30):
@@ -194,6 +236,8 @@ def main():
         lat.append((time.perf_counter() - t0) * 1e6)
 
     dbytes = decode_algorithmic_bytes(B, H, Hq, lens)
+    split_bytes = decode_algorithmic_bytes(B, H, Hq, lens, with_output=False)  # the merge writes the output
+    split_gbps = split_bytes / (split_us * 1e-6) / 1e9
     abytes = append_algorithmic_bytes(B, H, lens)
     decode_gbps = dbytes / (decode_us * 1e-6) / 1e9
     append_us = float(np.mean(append_ms)) * 1e3
@@ -221,13 +265,14 @@ def main():
         "append_us": round(append_us, 3),
         "append_GBps": round(append_gbps, 2),
         "wall_ms_timed_steps": round(wall_ms, 3),
-        "roofline": {"bound": "hbm", "achieved": round(decode_gbps, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(decode_gbps / HBM_PEAK_GBPS, 4), "traffic": measured_traffic("decode"),
-                     "kernel": "okvq_decode_attention (split-K + merge + unrotate launches)",
-                     "algorithmic_bytes": dbytes},
+        "roofline": {"bound": "hbm", "achieved": round(split_gbps, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(split_gbps / HBM_PEAK_GBPS, 4), "traffic": measured_traffic("k_decode"),
+                     "kernel": "k_decode (split-K decode attention with per-split inverse rotation)",
+                     "algorithmic_bytes": split_bytes, "avg_launch_us": round(split_us, 3)},
+        "kernels_us": {"k_decode": round(split_us, 3), "k_decode_merge": round(merge_us, 3)},
         "roofline_append": {"bound": "hbm", "achieved": round(append_gbps, 2), "peak": HBM_PEAK_GBPS,
                             "unit": "GB/s", "frac": round(append_gbps / HBM_PEAK_GBPS, 4),
-                            "traffic": measured_traffic("append"),
+                            "traffic": None,
                             "kernel": "okvq_append (key + value codec launches)", "algorithmic_bytes": abytes},
         "cache_replicas": n_cache,
     }

@@ -183,6 +183,14 @@ okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_h
                                   float sm_scale, uint32_t flags, float* out, void* workspace,
                                   size_t workspace_bytes, void* stream);
 
+/* okvq_decode_attention that also times its two launches: events[0] and events[1] are recorded
+ * at the start and end of the split-K kernel's execution, events[2] and events[3] at those of
+ * the merge kernel (hipEvent_t handles created by the caller; hipEventElapsedTime of a pair is
+ * that kernel's duration). */
+okvq_status okvq_decode_attention_timed(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,
+                                        float sm_scale, uint32_t flags, float* out, void* workspace,
+                                        size_t workspace_bytes, void* stream, void* const* events);
+
 #ifdef __cplusplus
 }
 #endif

@@ -271,8 +271,9 @@ size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len) {
   return decode_workspace_bytes(dims->batch, dims->num_kv_heads, dims->num_q_heads, max_seq_len);
 }
 
-okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q, float sm_scale,
-                                  uint32_t flags, float* out, void* workspace, size_t workspace_bytes, void* stream) {
+static okvq_status decode_impl(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q, float sm_scale,
+                               uint32_t flags, float* out, void* workspace, size_t workspace_bytes, void* stream,
+                               void* const* events) {
   okvq_status st = check_cache(cache);
   if (st != OKVQ_OK) return st;
   if (!lens_host || flags != 0 || !std::isfinite(sm_scale)) return OKVQ_ERR_INVALID_ARGUMENT;
@@ -290,8 +291,27 @@ okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_h
   const Codebook& cb = codebook();
   const uint32_t cb01 = cb.level16[0] | ((uint32_t)cb.level16[1] << 16);
   const uint32_t cb23 = cb.level16[2] | ((uint32_t)cb.level16[3] << 16);
+  hipEvent_t ev[4];
+  if (events) {
+    for (int i = 0; i < 4; ++i) {
+      if (!events[i]) return OKVQ_ERR_INVALID_ARGUMENT;
+      ev[i] = static_cast<hipEvent_t>(events[i]);
+    }
+  }
   return hip_status(launch_decode(view(cache), q, sm_scale, out, workspace, plan, static_cast<hipStream_t>(stream),
-                                  cb01, cb23, max_len));
+                                  cb01, cb23, max_len, events ? ev : nullptr));
+}
+
+okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q, float sm_scale,
+                                  uint32_t flags, float* out, void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_impl(cache, lens_host, q, sm_scale, flags, out, workspace, workspace_bytes, stream, nullptr);
+}
+
+okvq_status okvq_decode_attention_timed(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,
+                                        float sm_scale, uint32_t flags, float* out, void* workspace,
+                                        size_t workspace_bytes, void* stream, void* const* events) {
+  if (!events) return OKVQ_ERR_INVALID_ARGUMENT;
+  return decode_impl(cache, lens_host, q, sm_scale, flags, out, workspace, workspace_bytes, stream, events);
 }
 
 }  // extern "C"

@@ -20,6 +20,8 @@
 //  * values stay rotated (Sec. 2.3): two accumulator sets, rows 0-7 audio / 8-15 video heads and
 //    rows 0-7 text heads; p n_v is masked per modality. B operands come from a 256-entry LDS
 //    table mapping a code byte (one channel, four tokens) to four fp16 codebook values.
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 #include <cstdlib>
 
@@ -665,7 +667,8 @@ static size_t record_bytes(int B, int H, int max_len) {
 size_t decode_workspace_bytes(int B, int H, int /*Hq*/, int max_len) { return record_bytes(B, H, max_len); }
 
 hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, float* out, void* ws,
-                         const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int /*max_len*/) {
+                         const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int /*max_len*/,
+                         hipEvent_t const* events) {
   const int G = c.Hq / c.H;
   DecodeArgs a;
   a.k_codes = c.k_codes;
@@ -689,10 +692,21 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
   a.qscale = sm_scale * 1.4426950408889634f * 0.08838834764831845f;
   a.cb01 = cb01;
   a.cb23 = cb23;
-  hipLaunchKernelGGL(k_decode, dim3(plan.nsplit, c.H, c.B), dim3(64 * kDecWaves), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_decode_merge, dim3(c.Hq, c.B), dim3(kMergeThreads), 0, s, a.ws, c.H, c.Hq, G, plan.nsplit, out);
+  hipError_t e;
+  if (events) {  // events bound to the two dispatches: start and end of each kernel's execution
+    hipExtLaunchKernelGGL(k_decode, dim3(plan.nsplit, c.H, c.B), dim3(64 * kDecWaves), 0, s, events[0], events[1], 0,
+                          a);
+  } else {
+    hipLaunchKernelGGL(k_decode, dim3(plan.nsplit, c.H, c.B), dim3(64 * kDecWaves), 0, s, a);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (events) {
+    hipExtLaunchKernelGGL(k_decode_merge, dim3(c.Hq, c.B), dim3(kMergeThreads), 0, s, events[2], events[3], 0,
+                          static_cast<const float*>(a.ws), c.H, c.Hq, G, plan.nsplit, out);
+  } else {
+    hipLaunchKernelGGL(k_decode_merge, dim3(c.Hq, c.B), dim3(kMergeThreads), 0, s, a.ws, c.H, c.Hq, G, plan.nsplit,
+                       out);
+  }
   return hipGetLastError();
 }
 

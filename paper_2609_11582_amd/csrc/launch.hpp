@@ -56,7 +56,9 @@ struct DecodePlan {
 DecodePlan plan_decode(int B, int H, int max_len);
 size_t decode_workspace_bytes(int B, int H, int Hq, int max_len);
 hipError_t launch_prepare_rotation(const float* rot, uint16_t* rot16t, hipStream_t s);
+// events: nullptr, or four events bound to the launches: split-K start, end; merge start, end
 hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, float* out, void* ws,
-                         const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int max_len);
+                         const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int max_len,
+                         hipEvent_t const* events);
 
 }  // namespace okvq

@@ -69,6 +69,9 @@ def lib() -> ctypes.CDLL:
         L.okvq_decode_workspace_bytes.argtypes = [P(Dims), i32]
         L.okvq_decode_attention.restype = i32
         L.okvq_decode_attention.argtypes = [P(CacheStruct), P(i32), vp, ctypes.c_float, u32, vp, vp, sz, vp]
+        L.okvq_decode_attention_timed.restype = i32
+        L.okvq_decode_attention_timed.argtypes = [P(CacheStruct), P(i32), vp, ctypes.c_float, u32, vp, vp, sz, vp,
+                                                  P(vp)]
         _lib = L
     return _lib
 
@@ -208,6 +211,27 @@ def okvq_decode_attention(cache: "KVCache", lens, q, sm_scale, out, workspace, w
                                      _ptr(out), _ptr(workspace), int(nbytes), _stream(stream))
     if check:
         _check(st, "okvq_decode_attention")
+    return st
+
+
+def okvq_decode_attention_timed(cache: "KVCache", lens, q, sm_scale, out, workspace, events, workspace_bytes=None,
+                                flags=0, stream=None, check=True) -> int:
+    """okvq_decode_attention that records four torch.cuda.Event objects at the start and end of
+    its split-K kernel and of its merge kernel."""
+    B, Hq = cache.dims.batch, cache.dims.num_q_heads
+    _need_len(lens, B, "lens")
+    _need(q, B * Hq * 128 * 2, "q")
+    _need(out, B * Hq * 128 * 4, "out")
+    _need_len(events, 4, "events")
+    handles = (ctypes.c_void_p * 4)(*[ctypes.c_void_p(e.cuda_event) for e in events])
+    if not all(handles):
+        raise ValueError("events: record each torch.cuda.Event once before passing it (torch creates them lazily)")
+    have = workspace.numel() * workspace.element_size()
+    nbytes = have if workspace_bytes is None else min(int(workspace_bytes), have)
+    st = lib().okvq_decode_attention_timed(ctypes.byref(cache.struct), _i32(lens), _ptr(q), float(sm_scale), int(flags),
+                                           _ptr(out), _ptr(workspace), int(nbytes), _stream(stream), handles)
+    if check:
+        _check(st, "okvq_decode_attention_timed")
     return st
 
 

@@ -146,3 +146,24 @@ def test_prepare_rotation_is_fp16_transpose():
     okvq.okvq_prepare_rotation(r_dev, got)
     torch.cuda.synchronize()
     assert np.array_equal(got.cpu().numpy().view(np.uint16), want.view(np.uint16))
+
+
+def test_timed_decode_matches_untimed_and_reports_durations():
+    import torch
+
+    import gpu_helpers as gh
+    import paper_2609_11582_amd as okvq
+    lens = [2000]
+    out, ref, ctx = _run("omni7b_32k", lens, H=2, Hq=14)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in evs:
+        e.record()
+    ws = okvq.decode_workspace(ctx["cache"].dims, 2000)
+    o2 = torch.full((1, 14, 128), float("nan"), dtype=torch.float32, device="cuda")
+    _announce("decode timed")
+    okvq.okvq_decode_attention_timed(ctx["cache"], lens, gh.f16dev(ctx["q"]), SM, o2, ws, evs)
+    torch.cuda.synchronize()
+    assert np.array_equal(o2.cpu().numpy().astype(np.float64), out)
+    t_split, t_merge = evs[0].elapsed_time(evs[1]), evs[2].elapsed_time(evs[3])
+    print(f"split {t_split * 1e3:.2f} us, merge {t_merge * 1e3:.2f} us")
+    assert 0.0 < t_split < 1000.0 and 0.0 < t_merge < 1000.0
