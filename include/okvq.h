@@ -30,7 +30,9 @@
  *
  * Cache layout (per layer; B = batch, H = num_kv_heads, cap = capacity, a multiple of 32)
  * ------------------------------------------------------------------------------------------
- *   k_codes  u8  [B][H][cap][32]      token i, channel c -> byte 32i + c/4, bits 2(c%4)..+1
+ *   k_codes  u8  [B][H][cap][32]      token i, channel c -> byte 32i + 4(c/16) + 2(c%2) + (c/8)%2,
+ *                                      bits 2((c/2)%4)..+1 (32-bit word t: channels 16t..16t+15,
+ *                                      even ones in the low half, odd ones in the high half)
  *   v_codes  u8  [B][H][cap/32][1024] window token t, channel c -> byte
  *                                      16*((c%16) + 16*((t/4)%4)) + 8*(t/16) + c/16,
  *                                      bits 2(t%4)..+1 (one channel of 4 consecutive tokens)

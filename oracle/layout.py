@@ -6,7 +6,11 @@ placement of the codes (the pack map) is this implementation's choice and is
 part of its ABI; it is written out here from its definition.
 
 Key codes, per (sequence, KV head): ``u8[cap][32]`` -- token i, channel c sits in
-byte 32 i + (c >> 2) at bits 2 (c & 3) .. 2 (c & 3) + 1.
+byte 32 i + 4 (c >> 4) + 2 (c & 1) + ((c >> 3) & 1) at bits 2 ((c >> 1) & 3) .. +1.
+Read as little-endian 32-bit words, word t of a token holds channels 16 t .. 16 t + 15:
+the even channels in its low half and the odd channels in its high half, two bits each
+in channel order, so masking a word with 3 * 0x00010001 << 2 j leaves the codes of the
+channel pair (16 t + 2 j, 16 t + 2 j + 1) in the two 16-bit halves.
 
 Value codes, per (sequence, KV head): ``u8[cap / 32][1024]``, one 1024-byte
 block per 32-token window. Inside a block, the code of window token t and
@@ -29,16 +33,29 @@ WINDOW = 32
 HEAD_DIM = 128
 
 
+def key_byte_index(c):
+    """Byte (within a token's 32) and bit shift of key channel c."""
+    c = np.asarray(c)
+    return 4 * (c >> 4) + 2 * (c & 1) + ((c >> 3) & 1), 2 * ((c >> 1) & 3)
+
+
 def pack_keys(codes: np.ndarray) -> np.ndarray:
     """uint8 codes [n][128] (0..3) -> packed [n][32]."""
-    c = np.asarray(codes, np.uint8).reshape(codes.shape[0], HEAD_DIM // 4, 4)
-    return (c[..., 0] | (c[..., 1] << 2) | (c[..., 2] << 4) | (c[..., 3] << 6)).astype(np.uint8)
+    codes = np.asarray(codes, np.uint8)
+    out = np.zeros((codes.shape[0], HEAD_DIM // 4), np.uint8)
+    for c in range(HEAD_DIM):
+        byte, shift = key_byte_index(c)
+        out[:, byte] |= (codes[:, c] << shift).astype(np.uint8)
+    return out
 
 
 def unpack_keys(packed: np.ndarray) -> np.ndarray:
     p = np.asarray(packed, np.uint8)
-    out = np.stack([(p >> (2 * j)) & 3 for j in range(4)], axis=-1)
-    return out.reshape(p.shape[0], HEAD_DIM).astype(np.uint8)
+    out = np.zeros((p.shape[0], HEAD_DIM), np.uint8)
+    for c in range(HEAD_DIM):
+        byte, shift = key_byte_index(c)
+        out[:, c] = (p[:, byte] >> shift) & 3
+    return out
 
 
 def value_byte_index(t: np.ndarray, c: np.ndarray) -> np.ndarray:

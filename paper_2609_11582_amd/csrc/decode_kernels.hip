@@ -7,19 +7,22 @@
 // equals applying it once per modality after aggregation, Sec. 2.3) and one normalized partial
 // output per split is written. k_decode_merge combines the splits by log-sum-exp.
 //
-// What one wave does per window (all G <= 8 query heads of the KV head from one read):
+// What one wave does per window pair (all G <= 8 query heads of the KV head from one read):
 //  * scores in the rotated key space (Sec. 2.3): s_i = n_i (q'.m_g + sum_c q'_c step_gc code_ic),
-//    q' = H q sm_scale log2(e) computed once per work-group. The per-window bias q'.m_g is a
-//    VALU dot product; the code term is an MFMA block-diagonal over a window pair: rows = 16
-//    tokens, columns 0-7 = heads for window A and columns 8-15 = the same heads for window B
-//    (K = 256 = the two windows' 128 channels), so each lane builds the query-times-step operand
-//    of one window only, and two 16x16 tiles hold the pair's 64 tokens.
-//    Codes enter the MFMA unchanged as fp16 subnormals: (dword & (3 << 2j)) is code * 2^(2j-24),
-//    and the matching power of two is folded into the B operand q'_c step_gc 2^(k0 - 2j).
-//  * online softmax in base 2 (running max per head, rescale only when it grows);
-//  * values stay rotated (Sec. 2.3): two accumulator sets, rows 0-7 audio / 8-15 video heads and
-//    rows 0-7 text heads; p n_v is masked per modality. B operands come from a 256-entry LDS
-//    table mapping a code byte (one channel, four tokens) to four fp16 codebook values.
+//    q' = H q sm_scale log2(e) computed once per work-group. The bias q'.m_g is an fp32 dot
+//    product; the code term is an MFMA block-diagonal over the pair: rows = 16 tokens, columns
+//    0-7 = heads for window A and 8-15 = the same heads for window B, K = 256 = the two windows'
+//    128 channels. Codes enter the MFMA unchanged as fp16 subnormals (a key code word masked with
+//    3 * 0x00010001 << 2j is the channel pair's codes times 2^(2j-24)); the matching power of two
+//    is folded into the B operand q'_c step_gc 2^(k0 - 2j), a packed fp16 product of a per-lane
+//    query register (zero for the other window of the pair) and the window's steps.
+//  * online softmax in base 2 (running max per head, rescaled only when it grows by 2^8);
+//  * values stay rotated (Sec. 2.3): the register accumulator has rows 0-7 = audio heads and
+//    8-15 = video heads; text rows (the prompt, a few windows) are accumulated in the wave's slot
+//    of the LDS combine tile. The A operand p n_v is masked per modality with a byte-table lookup
+//    (v_perm) and the two row halves exchange window halves with one DPP row rotation under a
+//    bank mask. B operands come from a 256-entry LDS table mapping a code byte (one channel,
+//    four tokens) to four fp16 codebook values.
 #include <hip/hip_ext.h>
 
 #include <algorithm>
@@ -30,16 +33,17 @@
 namespace okvq {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kDecWaves = 8;                         // waves per split work-group
-constexpr int kRecHeader = 32;                       // m[8], l[8], pad
-constexpr int kRecFloats = kRecHeader + 8 * kD;      // + o[8 heads][128], un-rotated, divided by l
-constexpr int kATile = 3 * kD + 8;                   // fp16 row pitch of the un-rotation A tile
-constexpr int kMinWps = 2 * kDecWaves;              // fewest windows per split (a pair per wave)
-constexpr int kMaxSplits = 1024;                     // most splits per (sequence, KV head)
-constexpr float kLazy = 8.0f;                        // log2 headroom of the lazily updated softmax max
-constexpr float kPvScale = 1.0f / 256.0f;            // 2^-kLazy: keeps p n_v within fp16
+constexpr int kDecWaves = 8;                    // waves per split work-group
+constexpr int kRecHeader = 32;                  // m[8], l[8], pad
+constexpr int kRecFloats = kRecHeader + 8 * kD; // + o[8 heads][128], un-rotated, divided by l
+constexpr int kATile = 3 * kD + 8;              // fp16 row pitch of the un-rotation A tile
+constexpr int kAccPitch = 28;                   // combine tile [channel][24 rows + 4]: conflict-free b128
+constexpr int kMinWps = 2 * kDecWaves;          // fewest windows per split (a pair per wave)
+constexpr int kMaxSplits = 1024;                // most splits per (sequence, KV head)
+constexpr float kLazy = 8.0f;                   // log2 headroom of the lazily updated softmax max
 
 struct DecodeArgs {
   const uint8_t* k_codes;
@@ -63,94 +67,35 @@ struct DecodeArgs {
 __device__ __forceinline__ half8 h8(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
   return __builtin_bit_cast(half8, make_uint4(a, b, c, d));
 }
-__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
-  return f2h(lo) | (f2h(hi) << 16);
+__device__ __forceinline__ half8 h8(const uint32_t (&v)[4]) { return h8(v[0], v[1], v[2], v[3]); }
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) { return f2h(lo) | (f2h(hi) << 16); }
+__device__ __forceinline__ uint32_t pk_mul(uint32_t a, uint32_t b) {  // packed fp16 product
+  return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, a) * __builtin_bit_cast(half2v, b));
 }
+__device__ __forceinline__ float lo_f16(uint32_t w) { return (float)__builtin_bit_cast(half2v, w)[0]; }
+__device__ __forceinline__ float hi_f16(uint32_t w) { return (float)__builtin_bit_cast(half2v, w)[1]; }
+__device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
+  const half2v v = {(_Float16)lo, (_Float16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+// 2^x on the hardware unit; results below 2^-126 flush to zero (weights that small do not count)
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 // lane l <- lane l ^ 8 within each row of 16 lanes (DPP row rotate by 8)
-__device__ __forceinline__ uint32_t swap8(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xf, 0xf, false);
+constexpr int kRowRor8 = 0x128;
+__device__ __forceinline__ float fswap8(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), kRowRor8, 0xf, 0xf, false));
 }
-__device__ __forceinline__ float fswap8(float v) { return __builtin_bit_cast(float, swap8(__builtin_bit_cast(uint32_t, v))); }
+// lanes of the given banks (4-lane groups of each row; 0x3 = lanes 0-7, 0xc = lanes 8-15) take
+// lane ^ 8's src, the others keep old
+template <int kBanks>
+__device__ __forceinline__ uint32_t take_partner(uint32_t old, uint32_t src) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)src, kRowRor8, 0xf, kBanks, false);
+}
 // lane l <- lane l ^ 16 and lane l ^ 32 (permutes between rows of 16, no LDS access)
 __device__ __forceinline__ float fxor16(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401f));
 }
 __device__ __forceinline__ float fxor32(float v) { return __shfl_xor(v, 32); }
-
-// Scale exponent of the fp16-subnormal code extraction for pair slot j (0..7) of a dword.
-__host__ __device__ constexpr int code_shift(int j) { return j <= 4 ? 2 * j : 2 * j - 10; }
-// Channel (0..31 within the lane group's 32) of MFMA k-block kk (0..3), slot e (0..7).
-__host__ __device__ constexpr int slot_channel(int kk, int e) {
-  return 16 * (kk >> 1) + 8 * (e & 1) + 4 * (kk & 1) + (e >> 1);
-}
-
-// A operand (token row half) of k-block kk from the two code dwords of the lane group.
-__device__ __forceinline__ half8 key_a_operand(uint32_t d0, uint32_t d1, int kk) {
-  const uint32_t d = (kk >> 1) ? d1 : d0;
-  if ((kk & 1) == 0) {
-    return h8(d & 0x00030003u, d & 0x000c000cu, d & 0x00300030u, d & 0x00c000c0u);
-  }
-  const uint32_t s = d >> 10;
-  return h8(d & 0x03000300u, s & 0x00030003u, s & 0x000c000cu, s & 0x00300030u);
-}
-
-// Loads of one window pair (A = wA, B = wA + 1) for one lane. Lanes 0-7 of every row of 16
-// score window A, lanes 8-15 window B ("side"); both sides need both windows' key codes (the
-// score MFMA is block-diagonal over the pair) and value codes (one PV MFMA per window).
-struct PairLoad {
-  uint2 ka0, ka1, kb0, kb1;  // key codes of tokens r and 16 + r of windows A, B (bytes 8g .. 8g+7)
-  uint4 va, vb;              // value codes of windows A, B (the lane's 16 bytes of each block)
-  uint2 nk0, nk1;            // key norms of the side window, tokens 4g .. 4g+3 and 16+4g .. 16+4g+3
-  uint2 nv0, nv1;            // value norms of the same tokens
-  uint32_t md0, md1;         // modality ids of the same tokens
-  uint2 stp, mnp;            // step / min of channels 32g + 4 (col % 8) .. +3 of the side window
-};
-
-__device__ __forceinline__ PairLoad load_pair(const DecodeArgs& p, size_t seq, int b, int wA, bool hasB, int lane) {
-  const int col = lane & 15, g = lane >> 4, r = lane & 15, side = col >> 3;
-  const size_t nwcap = p.cap / kW;
-  const uint8_t* kc = p.k_codes + seq * p.cap * 32;
-  const uint8_t* vc = p.v_codes + seq * nwcap * 1024 + 16 * lane;
-  PairLoad d;
-  d.ka0 = *reinterpret_cast<const uint2*>(kc + (size_t)(kW * wA + r) * 32 + 8 * g);
-  d.ka1 = *reinterpret_cast<const uint2*>(kc + (size_t)(kW * wA + 16 + r) * 32 + 8 * g);
-  d.va = *reinterpret_cast<const uint4*>(vc + (size_t)wA * 1024);
-  if (hasB) {
-    d.kb0 = *reinterpret_cast<const uint2*>(kc + (size_t)(kW * (wA + 1) + r) * 32 + 8 * g);
-    d.kb1 = *reinterpret_cast<const uint2*>(kc + (size_t)(kW * (wA + 1) + 16 + r) * 32 + 8 * g);
-    d.vb = *reinterpret_cast<const uint4*>(vc + (size_t)(wA + 1) * 1024);
-  } else {
-    d.kb0 = d.kb1 = make_uint2(0, 0);
-    d.vb = make_uint4(0, 0, 0, 0);
-  }
-  if (side == 0 || hasB) {
-    const int wS = wA + side;
-    const size_t t = seq * p.cap + (size_t)kW * wS + 4 * g;
-    d.nk0 = *reinterpret_cast<const uint2*>(p.k_norm + t);
-    d.nk1 = *reinterpret_cast<const uint2*>(p.k_norm + t + 16);
-    d.nv0 = *reinterpret_cast<const uint2*>(p.v_norm + t);
-    d.nv1 = *reinterpret_cast<const uint2*>(p.v_norm + t + 16);
-    const uint8_t* md = p.modality + (size_t)b * p.cap + kW * wS + 4 * g;
-    d.md0 = *reinterpret_cast<const uint32_t*>(md);
-    d.md1 = *reinterpret_cast<const uint32_t*>(md + 16);
-    const size_t mt = (seq * nwcap + wS) * kD + 32 * g + 4 * (col & 7);
-    d.stp = *reinterpret_cast<const uint2*>(p.k_step + mt);
-    d.mnp = *reinterpret_cast<const uint2*>(p.k_min + mt);
-  } else {
-    d.nk0 = d.nk1 = d.nv0 = d.nv1 = d.stp = d.mnp = make_uint2(0, 0);
-    d.md0 = d.md1 = 0;
-  }
-  return d;
-}
-
-__device__ __forceinline__ half8 lut_op(const uint2* vlut, uint4 vc, int nb) {
-  const uint32_t vw[4] = {vc.x, vc.y, vc.z, vc.w};
-  const uint32_t b0 = (vw[nb >> 2] >> (8 * (nb & 3))) & 0xffu;        // tokens 4g .. 4g+3
-  const uint32_t b1 = (vw[2 + (nb >> 2)] >> (8 * (nb & 3))) & 0xffu;  // tokens 16+4g .. 16+4g+3
-  const uint2 x0 = vlut[b0];
-  const uint2 x1 = vlut[b1];
-  return h8(x0.x, x0.y, x1.x, x1.y);
-}
 
 typedef unsigned short ushort2v __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pkmax_u16(uint32_t a, uint32_t b) {
@@ -168,32 +113,114 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Scale exponent of the fp16-subnormal code extraction for channel pair j (0..7) of a key word.
+__host__ __device__ constexpr int code_shift(int j) { return j <= 4 ? 2 * j : 2 * j - 10; }
+
+// A operand (one token row, channels 8 kk' .. 8 kk' + 7 of the lane group's 32, kk' = kk & 3)
+// from the two code words of the lane group: the channel pairs (2j, 2j + 1) of a word sit in
+// its two 16-bit halves at bits 2j; pairs 5-7 are shifted down by 10 to stay subnormal.
+__device__ __forceinline__ half8 key_a_operand(uint2 w, int kk) {
+  const uint32_t d = (kk & 2) ? w.y : w.x;
+  if ((kk & 1) == 0) return h8(d & 0x00030003u, d & 0x000c000cu, d & 0x00300030u, d & 0x00c000c0u);
+  const uint32_t s = d >> 10;
+  return h8(d & 0x03000300u, s & 0x00030003u, s & 0x000c000cu, s & 0x00300030u);
+}
+
+// Modality byte tables for v_perm: byte m of a table is 0xff where the modality m is kept.
+// Byte 3 is the modality of an invalid token (never kept).
+constexpr uint32_t kTabAudio = 0x000000ffu, kTabVideo = 0x0000ff00u, kTabText = 0x00ff0000u;
+constexpr uint32_t kTabBits = 0x00040201u;  // byte m -> 1 << m (presence bits)
+
+// Loads of one window pair (A = wA, B = wA + 1) for one lane. Lanes 0-7 of every row of 16 score
+// window A, lanes 8-15 window B ("side"); both sides need both windows' key codes (the score MFMA
+// is block-diagonal over the pair) and value codes (one PV MFMA per window). A window beyond the
+// split re-reads window A: its tokens are masked as invalid, so its contents never matter.
+struct PairLoad {
+  uint2 ka0, ka1, kb0, kb1;  // key codes of tokens r and 16 + r of windows A, B (bytes 8g .. 8g+7)
+  uint4 va, vb;              // value codes of windows A, B (the lane's 16 bytes of each block)
+  uint2 nk0, nk1;            // key norms of the side window, tokens 4g .. 4g+3 and 16+4g .. 16+4g+3
+  uint2 nv0, nv1;            // value norms of the same tokens
+  uint32_t md0, md1;         // modality ids of the same tokens
+  uint2 stp, mnp;            // step / min of channels 32g + 4 (col % 8) .. +3 of the side window
+};
+
+struct SeqPtrs {  // uniform per work-group
+  const uint8_t* kc;
+  const uint8_t* vc;
+  const uint16_t* kn;
+  const uint16_t* vn;
+  const uint16_t* kmin;
+  const uint16_t* kstep;
+  const uint8_t* md;
+};
+
+__device__ __forceinline__ PairLoad load_pair(const SeqPtrs& sp, int wA, bool hasB, int lane) {
+  const int col = lane & 15, g = lane >> 4, r = lane & 15, side = col >> 3;
+  const uint32_t wB = hasB ? wA + 1 : wA;
+  const uint32_t wS = side ? wB : (uint32_t)wA;
+  PairLoad d;
+  d.ka0 = *reinterpret_cast<const uint2*>(sp.kc + ((uint32_t)(kW * wA + r) * 32u + 8u * g));
+  d.ka1 = *reinterpret_cast<const uint2*>(sp.kc + ((uint32_t)(kW * wA + 16 + r) * 32u + 8u * g));
+  d.kb0 = *reinterpret_cast<const uint2*>(sp.kc + ((kW * wB + r) * 32u + 8u * g));
+  d.kb1 = *reinterpret_cast<const uint2*>(sp.kc + ((kW * wB + 16 + r) * 32u + 8u * g));
+  d.va = *reinterpret_cast<const uint4*>(sp.vc + ((uint32_t)wA * 1024u + 16u * lane));
+  d.vb = *reinterpret_cast<const uint4*>(sp.vc + (wB * 1024u + 16u * lane));
+  const uint32_t t = kW * wS + 4u * g;
+  d.nk0 = *reinterpret_cast<const uint2*>(sp.kn + t);
+  d.nk1 = *reinterpret_cast<const uint2*>(sp.kn + t + 16);
+  d.nv0 = *reinterpret_cast<const uint2*>(sp.vn + t);
+  d.nv1 = *reinterpret_cast<const uint2*>(sp.vn + t + 16);
+  d.md0 = *reinterpret_cast<const uint32_t*>(sp.md + t);
+  d.md1 = *reinterpret_cast<const uint32_t*>(sp.md + t + 16);
+  const uint32_t mt = wS * kD + 32u * g + 4u * (col & 7);
+  d.stp = *reinterpret_cast<const uint2*>(sp.kstep + mt);
+  d.mnp = *reinterpret_cast<const uint2*>(sp.kmin + mt);
+  return d;
+}
+
+// B operand of the value MFMA for 16-channel block nb: code bytes of tokens 4g..4g+3 and
+// 16+4g..16+4g+3 of the lane's channel, each turned into four fp16 codebook levels.
+__device__ __forceinline__ half8 lut_op(const uint2* vlut, uint4 vc, int nb) {
+  const uint32_t vw[4] = {vc.x, vc.y, vc.z, vc.w};
+  const uint32_t b0 = (vw[nb >> 2] >> (8 * (nb & 3))) & 0xffu;
+  const uint32_t b1 = (vw[2 + (nb >> 2)] >> (8 * (nb & 3))) & 0xffu;
+  const uint2 x0 = vlut[b0];
+  const uint2 x1 = vlut[b1];
+  return h8(x0.x, x0.y, x1.x, x1.y);
+}
+
 __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   __shared__ __attribute__((aligned(16))) uint2 vlut[256];
-  __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];                     // rotated queries (padded rows)
+  __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];                     // q' (fp32, padded rows)
   __shared__ float amax_w[kDecWaves];
   __shared__ __attribute__((aligned(16))) uint32_t meta[kDecWaves][2][2][kD / 2];  // [wave][side][step, min]
-  __shared__ float wstate[kDecWaves][2][8];                                        // m, l per wave and head
+  __shared__ __attribute__((aligned(16))) uint32_t zeros[kD / 2];                  // steps of "no window"
+  __shared__ __attribute__((aligned(16))) float wst[2][8][kDecWaves];              // [m, l][head][wave]
   __shared__ uint32_t wmask[kDecWaves];
-  __shared__ uint32_t wnv[kDecWaves];                                              // value-norm maxima
-  // per wave: accumulator rows for the combine (rows 0-15 set 1, 16-23 set 2); the merge reuses it
-  __shared__ __attribute__((aligned(16))) float wacc[kDecWaves][24][kD + 4];  // padded rows: conflict-free
-  __shared__ __attribute__((aligned(16))) _Float16 atile[8][kATile];         // merged rows, fp16
-  __shared__ float hst[8];                                                   // per head: scale
+  __shared__ uint32_t wnv[kDecWaves];  // value-norm maxima
+  // per wave, column-major accumulator tile for the combine: [channel][row], rows 0-7 audio,
+  // 8-15 video, 16-23 text heads
+  __shared__ __attribute__((aligned(16))) float wacc[kDecWaves][kD][kAccPitch];
+  __shared__ __attribute__((aligned(16))) _Float16 atile[8][kATile];  // merged rows, fp16
+  __shared__ __attribute__((aligned(16))) float fac[8][kDecWaves];    // per head and wave: combine factor
 
   const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
-  const int col = lane & 15, g = lane >> 4, hd = col & 7, side = col >> 3;
-  const bool upper = side != 0;
+  const int tid = threadIdx.x, lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar) for the compiler
+  const int col = lane & 15, g = lane >> 4, hd = col & 7, side = col >> 3, c7 = col & 7;
   const size_t seq = (size_t)b * p.H + h;
   float* rec = p.ws + (seq * p.nsplit + split) * kRecFloats;
   const int w_begin = split * p.wps;
   const int w_plan = min(w_begin + p.wps, p.cap / kW);  // windows of this split by the plan
   const int wA0 = w_begin + 2 * wave;                    // this wave's pairs: (wA0 + 16 k, +1)
+  const size_t nwcap = p.cap / kW;
+  const SeqPtrs sp{p.k_codes + seq * p.cap * 32,       p.v_codes + seq * nwcap * 1024, p.k_norm + seq * p.cap,
+                   p.v_norm + seq * p.cap,             p.k_min + seq * nwcap * kD,     p.k_step + seq * nwcap * kD,
+                   p.modality + (size_t)b * p.cap};
 
   // ---- every global load of the prologue goes out before any of them is used: the query rows
   // (waves 0-3), the first pair (speculatively: windows within the plan, the length is checked
-  // later), and the sequence length ----
+  // later), the sequence length, and a touch of the inverse-rotation table (to the L2) ----
   const int hr = 2 * wave + (lane >> 5), c4 = 4 * (lane & 31);
   uint2 qraw = make_uint2(0, 0);
   uint32_t qsgn = 0;
@@ -201,8 +228,9 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     qraw = *reinterpret_cast<const uint2*>(p.q + ((size_t)b * p.Hq + h * p.G + hr) * kD + c4);
     qsgn = *reinterpret_cast<const uint32_t*>(p.signs + c4);
   }
-  PairLoad cur;
-  if (wA0 < w_plan) cur = load_pair(p, seq, b, wA0, wA0 + 1 < w_plan, lane);
+  PairLoad bufA, bufB;
+  if (wA0 < w_plan) bufA = load_pair(sp, wA0, wA0 + 1 < w_plan, lane);
+  const uint32_t touch = reinterpret_cast<const uint32_t*>(p.rot16t)[tid * 48];  // one dword per 192 B
   const int len = min(p.seq_lens[b], p.cap);  // memory-safe if device and host lengths disagree
   const int nwin = (len + kW - 1) / kW;
   const int w_end = min(w_plan, nwin);
@@ -218,9 +246,15 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     const uint32_t lv[4] = {p.cb01 & 0xffffu, p.cb01 >> 16, p.cb23 & 0xffffu, p.cb23 >> 16};
     vlut[tid] = make_uint2(lv[tid & 3] | (lv[(tid >> 2) & 3] << 16), lv[(tid >> 4) & 3] | (lv[tid >> 6] << 16));
   }
+  if (tid < kD / 2) zeros[tid] = 0u;
+  if (g < 2) {  // text rows of this wave's combine slot start at zero
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb)
+      *reinterpret_cast<float4*>(&wacc[wave][16 * nb + col][16 + 4 * g]) = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   // ---- query rotation: wave w < 4 rotates heads 2w, 2w+1; lane holds channels c4 .. c4+3 ----
-  float x[4] = {0.f, 0.f, 0.f, 0.f};
   if (wave < 4) {
+    float x[4];
     const uint32_t rr[2] = {qraw.x, qraw.y};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -252,116 +286,125 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 #pragma unroll
     for (int lb = 1; lb < 64; lb <<= 1) am = fmaxf(am, __shfl_xor(am, lb));
     if (lane == 0) amax_w[wave] = am;
+    *reinterpret_cast<float4*>(&qs[hr][c4]) = make_float4(x[0], x[1], x[2], x[3]);  // zero rows for heads >= G
   }
   __syncthreads();
-  const float amax = fmaxf(fmaxf(amax_w[0], amax_w[1]), fmaxf(amax_w[2], amax_w[3]));  // waves 0-3 rotate
-  // power-of-two scale k0 keeps |q'_c step_c 2^(k0 - 2j)| <= 2^15 (|step| <= 2/3 + rounding)
+  const float amax = fmaxf(fmaxf(amax_w[0], amax_w[1]), fmaxf(amax_w[2], amax_w[3]));
+  // power-of-two scale k0 keeps |q'_c step_c 2^(k0 - shift)| <= 2^15 (|step| <= 2/3 + rounding)
   const int k0 = (amax > 0.0f) ? min(max(14 - ilogbf(amax), -60), 60) : 0;
   const float kscale = ldexpf(1.0f, 24 - k0);  // undoes 2^(k0 - 24) on the MFMA result
-  if (wave < 4) {  // store q' pre-scaled by 2^(k0 - shift(c)), shift(c) = code_shift(c % 8)
-    float o[4];
+  // Per-lane query operand of the score MFMA, constant over the pairs: for channels
+  // 32g + 8 k4 .. +7, fp16(q'[hd][c] 2^(k0 - shift(c))). The other window's k-blocks multiply it
+  // by zero steps (read from `zeros`).
+  uint32_t qm[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) o[i] = ldexpf(x[i], k0 - code_shift((c4 + i) & 7));
-    *reinterpret_cast<float4*>(&qs[hr][c4]) = make_float4(o[0], o[1], o[2], o[3]);
+  for (int k4 = 0; k4 < 4; ++k4) {
+    const float4 qa = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 8 * k4]);
+    const float4 qb = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 8 * k4 + 4]);
+    const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {  // channel pair 4 (k4 & 1) + j of the word
+      const int sh = k0 - code_shift(4 * (k4 & 1) + j);
+      qm[k4][j] = pack2(ldexpf(qv[2 * j], sh), ldexpf(qv[2 * j + 1], sh));
+    }
   }
-  __syncthreads();
+  // modality tables of this lane: its own row half (set 1: audio for side 0, video for side 1),
+  // the partner's, and the text rows (side 0 only)
+  const uint32_t tab_own = side ? kTabVideo : kTabAudio;
+  const uint32_t tab_oth = side ? kTabAudio : kTabVideo;
+  const uint32_t tab_txt0 = side ? 0u : kTabText;
 
-  floatx4 acc1[8], acc2[8];
+  floatx4 acc1[8];
 #pragma unroll
-  for (int nb = 0; nb < 8; ++nb) {
-    acc1[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    acc2[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int nb = 0; nb < 8; ++nb) acc1[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -__builtin_inff(), l_run = 0.0f;
+  bool started = false;  // a pair has been processed (wave-uniform)
   uint32_t seen = 0;  // modalities seen by this wave
   uint32_t nvm = 0;   // largest value norm seen by this lane (two fp16 halves, non-negative)
   uint32_t* mw = &meta[wave][side][0][0];
+  const float* qrow = &qs[hd][32 * g];
+  // steps read for the two windows' k-blocks: the lane's own window, zeros for the other one
+  const uint32_t* stA = side ? zeros : &meta[wave][0][0][0];
+  const uint32_t* stB = side ? &meta[wave][1][0][0] : zeros;
+  float* tacc = &wacc[wave][col][16 + 4 * g];  // text rows of this lane (g < 2), channel 16 nb + col
 
-  for (int wA = wA0; wA < w_end; wA += 2 * kDecWaves) {
+  auto process = [&](const PairLoad& cur, int wA) {
     const bool hasB = wA + 1 < w_end;
+    const bool full = hasB && kW * (wA + 2) <= len;  // every token of both windows is valid
     const int wS = wA + side;
-    const bool side_ok = !upper || hasB;
-    PairLoad nxt = cur;
-    {
-      const int wn = wA + 2 * kDecWaves;
-      if (wn < w_end) nxt = load_pair(p, seq, b, wn, wn + 1 < w_end, lane);  // prefetch
-    }
 
-    // ---- side window metadata through wave-private LDS ----
-    *reinterpret_cast<uint2*>(&mw[16 * g + 2 * (col & 7)]) = cur.stp;
-    *reinterpret_cast<uint2*>(&mw[kD / 2 + 16 * g + 2 * (col & 7)]) = cur.mnp;
+    // ---- side window metadata through wave-private LDS, natural channel order ----
+    *reinterpret_cast<uint2*>(&mw[16 * g + 2 * c7]) = cur.stp;
+    *reinterpret_cast<uint2*>(&mw[kD / 2 + 16 * g + 2 * c7]) = cur.mnp;
     wave_lds_sync();
-
-    // ---- B operand (q' step 2^(k0 - shift)) and the bias q'.m of the side window ----
-    uint32_t bq[4][4];
-    float bsum[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+    uint4 mn4[4];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int dw = 16 * g + 8 * (kk >> 1) + 2 * (kk & 1);  // dword of channel 32g + 16(kk>>1) + 4(kk&1)
-      const uint2 s0 = *reinterpret_cast<const uint2*>(&mw[dw]);
-      const uint2 s1 = *reinterpret_cast<const uint2*>(&mw[dw + 4]);
-      const uint2 m0 = *reinterpret_cast<const uint2*>(&mw[kD / 2 + dw]);
-      const uint2 m1 = *reinterpret_cast<const uint2*>(&mw[kD / 2 + dw + 4]);
-      const uint32_t sh[2][2] = {{s0.x, s0.y}, {s1.x, s1.y}};
-      const uint32_t mh[2][2] = {{m0.x, m0.y}, {m1.x, m1.y}};
-      const float4 q0 = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 16 * (kk >> 1) + 4 * (kk & 1)]);
-      const float4 q1 = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 16 * (kk >> 1) + 8 + 4 * (kk & 1)]);
-      const float qk[2][4] = {{q0.x, q0.y, q0.z, q0.w}, {q1.x, q1.y, q1.z, q1.w}};  // zero rows for heads >= G
+    for (int k4 = 0; k4 < 4; ++k4) mn4[k4] = *reinterpret_cast<const uint4*>(&mw[kD / 2 + 16 * g + 4 * k4]);
+    // ---- bias q'.m of the side window (fp32): 32 channels per lane, then the 4 lane groups ----
+    float bias = 0.0f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int cls = code_shift(4 * (kk & 1) + i) >> 1;
-        float prod[2];
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const float stf = h2f((sh[hh][i >> 1] >> (16 * (i & 1))) & 0xffffu);
-          const float mnf = h2f((mh[hh][i >> 1] >> (16 * (i & 1))) & 0xffffu);
-          prod[hh] = qk[hh][i] * stf;
-          bsum[cls] = __builtin_fmaf(qk[hh][i], mnf, bsum[cls]);
-        }
-        bq[kk][i] = pack2(prod[0], prod[1]);
-      }
+    for (int k4 = 0; k4 < 4; ++k4) {
+      const float4 qa = *reinterpret_cast<const float4*>(qrow + 8 * k4);
+      const float4 qb = *reinterpret_cast<const float4*>(qrow + 8 * k4 + 4);
+      const uint4 m = mn4[k4];
+      bias = __builtin_fmaf(qa.x, lo_f16(m.x), bias);
+      bias = __builtin_fmaf(qa.y, hi_f16(m.x), bias);
+      bias = __builtin_fmaf(qa.z, lo_f16(m.y), bias);
+      bias = __builtin_fmaf(qa.w, hi_f16(m.y), bias);
+      bias = __builtin_fmaf(qb.x, lo_f16(m.z), bias);
+      bias = __builtin_fmaf(qb.y, hi_f16(m.z), bias);
+      bias = __builtin_fmaf(qb.z, lo_f16(m.w), bias);
+      bias = __builtin_fmaf(qb.w, hi_f16(m.w), bias);
     }
-    float bias = bsum[0] + 4.0f * bsum[1] + 16.0f * bsum[2] + 64.0f * bsum[3] + 256.0f * bsum[4];
     bias += fxor16(bias);
     bias += fxor32(bias);
-    bias = ldexpf(bias, -k0);
-    wave_lds_sync();  // metadata reads done before the next pair overwrites it
 
     // ---- scores: two 16-token tiles, each 8 MFMAs block-diagonal over the pair ----
     floatx4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
-      const bool mine = (kk >= 4) == upper;
-      const half8 bop = mine ? h8(bq[kk & 3][0], bq[kk & 3][1], bq[kk & 3][2], bq[kk & 3][3]) : h8(0, 0, 0, 0);
-      const half8 a0 = (kk < 4) ? key_a_operand(cur.ka0.x, cur.ka0.y, kk & 3) : key_a_operand(cur.kb0.x, cur.kb0.y, kk & 3);
-      const half8 a1 = (kk < 4) ? key_a_operand(cur.ka1.x, cur.ka1.y, kk & 3) : key_a_operand(cur.kb1.x, cur.kb1.y, kk & 3);
-      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bop, sc0, 0, 0, 0);
-      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bop, sc1, 0, 0, 0);
+      const uint4 sv = *reinterpret_cast<const uint4*>(&(kk < 4 ? stA : stB)[16 * g + 4 * (kk & 3)]);
+      const uint32_t* q = qm[kk & 3];
+      const half8 bop = h8(pk_mul(q[0], sv.x), pk_mul(q[1], sv.y), pk_mul(q[2], sv.z), pk_mul(q[3], sv.w));
+      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka0 : cur.kb0, kk), bop, sc0, 0, 0, 0);
+      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka1 : cur.kb1, kk), bop, sc1, 0, 0, 0);
     }
+    wave_lds_sync();  // metadata reads done before the next pair overwrites it
 
     // ---- online softmax (base 2) over the pair's 64 tokens ----
     const uint32_t nkw[4] = {cur.nk0.x, cur.nk0.y, cur.nk1.x, cur.nk1.y};
     const uint32_t nvw[4] = {cur.nv0.x, cur.nv0.y, cur.nv1.x, cur.nv1.y};
-    nvm = pkmax_u16(nvm, pkmax_u16(pkmax_u16(nvw[0], nvw[1]), pkmax_u16(nvw[2], nvw[3])));
+    uint32_t md[2] = {cur.md0, cur.md1};
     float s[8];
-    float wmax = -__builtin_inff();
 #pragma unroll
     for (int e = 0; e < 8; ++e) {  // e = 4 t + i: token 16 t + 4 g + i of the side window
-      const int t = e >> 2, i = e & 3;
-      const bool valid = side_ok && (kW * wS + 16 * t + 4 * g + i) < len;
-      const float nkf = h2f((nkw[e >> 1] >> (16 * (e & 1))) & 0xffffu);
-      const float raw = t ? sc1[i] : sc0[i];
-      s[e] = valid ? nkf * __builtin_fmaf(raw, kscale, bias) : -__builtin_inff();
-      wmax = fmaxf(wmax, s[e]);
+      const float raw = (e >> 2) ? sc1[e & 3] : sc0[e & 3];
+      const float nkf = (e & 1) ? hi_f16(nkw[e >> 1]) : lo_f16(nkw[e >> 1]);
+      s[e] = nkf * __builtin_fmaf(raw, kscale, bias);
     }
+    if (!full) {  // partial pair: tokens beyond the length (or a missing window B) do not count
+      const bool side_ok = !side || hasB;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int nvalid = side_ok ? min(max(len - (kW * wS + 16 * t + 4 * g), 0), 4) : 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (i >= nvalid) s[4 * t + i] = -__builtin_inff();
+        md[t] |= (nvalid >= 4) ? 0u : (0x03030303u << (8 * nvalid));  // modality 3: invalid
+      }
+    }
+    float wmax = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
     wmax = fmaxf(wmax, fswap8(wmax));
     wmax = fmaxf(wmax, fxor16(wmax));
     wmax = fmaxf(wmax, fxor32(wmax));
     // lazy rescale: the reference m_run moves only when the max exceeds it by more than 2^8, so
-    // p = 2^(s - m_run) <= 2^8; p n_v is stored as fp16 times 2^-8 (undone in the epilogue)
-    if (__any(wmax > m_run + kLazy)) {
+    // p = 2^(s - m_run - 8) <= 1 and p n_v fits fp16
+    if (!started) {  // first pair: nothing accumulated yet, the reference is just set
+      m_run = wmax;
+      started = true;
+    } else if (__any(wmax > m_run + kLazy)) {
       const float m_new = fmaxf(m_run, wmax);
-      const float alpha = exp2f(m_run - m_new);
+      const float alpha = fast_exp2(m_run - m_new);
       l_run *= alpha;
       float arow[4];
 #pragma unroll
@@ -369,80 +412,89 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          acc1[nb][i] *= arow[i];
-          acc2[nb][i] *= arow[i];
+        for (int i = 0; i < 4; ++i) acc1[nb][i] *= arow[i];
+      }
+      if (g < 2) {
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) {
+          float4* t = reinterpret_cast<float4*>(tacc + 16 * nb * kAccPitch);
+          const float4 v = *t;
+          *t = make_float4(v.x * arow[0], v.y * arow[1], v.z * arow[2], v.w * arow[3]);
         }
       }
       m_run = m_new;
     }
-    float pv[8];
-    uint32_t mods = 0;
-    const uint32_t mdw[2] = {cur.md0, cur.md1};
+    const float mref = m_run + kLazy;
+    float pr[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int t = e >> 2, i = e & 3;
-      const float pr = exp2f(s[e] - m_run);
-      l_run += pr;
-      const bool valid = side_ok && (kW * wS + 16 * t + 4 * g + i) < len;
-      const float nvf = h2f((nvw[e >> 1] >> (16 * (e & 1))) & 0xffffu);
-      pv[e] = valid ? pr * nvf * kPvScale : 0.0f;
-      if (valid) mods |= 1u << ((mdw[t] >> (8 * i)) & 3u);
+      pr[e] = fast_exp2(s[e] - mref);
+      l_run += pr[e];
     }
-    const bool any_av = __any((mods & 3u) != 0);
-    const bool any_t = __any((mods & 4u) != 0);
-    seen |= (__any((mods & 1u) != 0) ? 1u : 0u) | (__any((mods & 2u) != 0) ? 2u : 0u) | (any_t ? 4u : 0u);
+    uint32_t pv[4];  // p n_v (fp16 pairs), tokens (4g, 4g+1), (4g+2, 4g+3), (16+4g, ..), (16+4g+2, ..)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) pv[q] = pk_mul(pack_f16(pr[2 * q], pr[2 * q + 1]), nvw[q]);
+    nvm = pkmax_u16(nvm, pkmax_u16(pkmax_u16(nvw[0], nvw[1]), pkmax_u16(nvw[2], nvw[3])));
 
-    // ---- values: one PV MFMA per window and 16-channel block, A = masked p n_v ----
-    if (any_av) {  // set 1: rows 0-7 audio heads, rows 8-15 video heads
-      uint32_t keep[4], send[4];
+    // ---- modalities present (wave-uniform) and the v_perm selectors of the token pairs ----
+    uint32_t pres = __builtin_amdgcn_perm(kTabBits, kTabBits, md[0]) | __builtin_amdgcn_perm(kTabBits, kTabBits, md[1]);
+    pres |= pres >> 16;
+    pres |= pres >> 8;
+    const bool has_a = __any(pres & 1u), has_v = __any(pres & 2u), has_t = __any(pres & 4u);
+    seen |= (has_a ? 1u : 0u) | (has_v ? 2u : 0u) | (has_t ? 4u : 0u);  // all wave-uniform
+    uint32_t sel[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sel[q] = __builtin_amdgcn_perm(md[q >> 1], md[q >> 1], (q & 1) ? 0x03030202u : 0x01010000u);
+
+    // ---- values: one PV MFMA per window and 16-channel block. Set 1 (rows 0-7 audio heads from
+    // the side-0 lanes, rows 8-15 video heads from the side-1 lanes) runs for every pair: a branch
+    // around it would give the accumulators two register homes ----
+    {
+      uint32_t opA[4], opB[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float kv[2], sv[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int e = 2 * q + u, t = e >> 2, i = e & 3;
-          const uint32_t mi = (mdw[t] >> (8 * i)) & 0xffu;
-          const float pa = (mi == 0u) ? pv[e] : 0.0f;
-          const float pvid = (mi == 1u) ? pv[e] : 0.0f;
-          kv[u] = upper ? pvid : pa;
-          sv[u] = upper ? pa : pvid;
-        }
-        keep[q] = pack2(kv[0], kv[1]);
-        send[q] = swap8(pack2(sv[0], sv[1]));
+        const uint32_t own = pv[q] & __builtin_amdgcn_perm(tab_own, tab_own, sel[q]);
+        const uint32_t oth = pv[q] & __builtin_amdgcn_perm(tab_oth, tab_oth, sel[q]);
+        opA[q] = take_partner<0xc>(own, oth);  // window A tokens: video rows from the side-0 partner
+        opB[q] = take_partner<0x3>(own, oth);  // window B tokens: audio rows from the side-1 partner
       }
-      const half8 opA = upper ? h8(send[0], send[1], send[2], send[3]) : h8(keep[0], keep[1], keep[2], keep[3]);
-      const half8 opB = upper ? h8(keep[0], keep[1], keep[2], keep[3]) : h8(send[0], send[1], send[2], send[3]);
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
-        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(opA, lut_op(vlut, cur.va, nb), acc1[nb], 0, 0, 0);
-        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(opB, lut_op(vlut, cur.vb, nb), acc1[nb], 0, 0, 0);
+        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, cur.va, nb), acc1[nb], 0, 0, 0);
+        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, cur.vb, nb), acc1[nb], 0, 0, 0);
       }
     }
-    if (any_t) {  // set 2: rows 0-7 text heads
-      uint32_t keep[4], recv[4];
+    if (has_t) {  // set 2: rows 0-7 text heads (side-0 lanes), rows 8-15 zero
+      uint32_t opA[4], opB[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float kv[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int e = 2 * q + u, t = e >> 2, i = e & 3;
-          const uint32_t mi = (mdw[t] >> (8 * i)) & 0xffu;
-          kv[u] = (mi == 2u) ? pv[e] : 0.0f;
-        }
-        keep[q] = pack2(kv[0], kv[1]);
-        recv[q] = swap8(keep[q]);
+        opA[q] = pv[q] & __builtin_amdgcn_perm(tab_txt0, tab_txt0, sel[q]);
+        const uint32_t txt = pv[q] & __builtin_amdgcn_perm(kTabText, kTabText, sel[q]);
+        opB[q] = take_partner<0x3>(0u, txt);
       }
-      const half8 zero = h8(0, 0, 0, 0);
-      const half8 opA = upper ? zero : h8(keep[0], keep[1], keep[2], keep[3]);
-      const half8 opB = upper ? zero : h8(recv[0], recv[1], recv[2], recv[3]);
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
-        acc2[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(opA, lut_op(vlut, cur.va, nb), acc2[nb], 0, 0, 0);
-        acc2[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(opB, lut_op(vlut, cur.vb, nb), acc2[nb], 0, 0, 0);
+        floatx4 t = {0.f, 0.f, 0.f, 0.f};
+        t = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, cur.va, nb), t, 0, 0, 0);
+        t = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, cur.vb, nb), t, 0, 0, 0);
+        if (g < 2) {
+          float4* ta = reinterpret_cast<float4*>(tacc + 16 * nb * kAccPitch);
+          const float4 v = *ta;
+          *ta = make_float4(v.x + t[0], v.y + t[1], v.z + t[2], v.w + t[3]);
+        }
       }
     }
-    cur = nxt;
+  };
+
+  // ---- window pairs, double-buffered loads without register copies ----
+  for (int wA = wA0; wA < w_end; wA += 4 * kDecWaves) {
+    const int wA2 = wA + 2 * kDecWaves;
+    if (wA2 < w_end) bufB = load_pair(sp, wA2, wA2 + 1 < w_end, lane);
+    process(bufA, wA);
+    if (wA2 >= w_end) break;
+    const int wA3 = wA2 + 2 * kDecWaves;
+    if (wA3 < w_end) bufA = load_pair(sp, wA3, wA3 + 1 < w_end, lane);
+    process(bufB, wA2);
   }
 
   // ---- epilogue. This wave's slice of the inverse-rotation table (output channels 16 wave ..
@@ -455,20 +507,33 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     for (int kk = 0; kk < 12; ++kk) rb[kk] = rp[4 * kk];
   }
 
-  // ---- combine the waves of the work-group ----
-  l_run += __shfl_xor(l_run, 8);
-  l_run += __shfl_xor(l_run, 16);
-  l_run += __shfl_xor(l_run, 32);
-#pragma unroll
-  for (int lb = 1; lb < 64; lb <<= 1) nvm = pkmax_u16(nvm, (uint32_t)__shfl_xor((int)nvm, lb));
+  // ---- combine the waves of the work-group: every wave writes its raw accumulators and its
+  // per-head (m, l); the combining threads derive the factors 2^(m_w - M) themselves ----
+  l_run += fswap8(l_run);
+  l_run += fxor16(l_run);
+  l_run += fxor32(l_run);
+  {
+    uint32_t t = nvm;
+    t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_mov_dpp((int)t, kRowRor8, 0xf, 0xf, false));
+    t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_ds_swizzle((int)t, 0x401f));
+    t = pkmax_u16(t, (uint32_t)__shfl_xor((int)t, 32));
+    t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_mov_dpp((int)t, 0x124, 0xf, 0xf, false));  // row_ror:4
+    t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_mov_dpp((int)t, 0x122, 0xf, 0xf, false));  // row_ror:2
+    t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_mov_dpp((int)t, 0x121, 0xf, 0xf, false));  // row_ror:1
+    nvm = t;
+  }
   if (lane < 8) {
-    wstate[wave][0][lane] = m_run;
-    wstate[wave][1][lane] = l_run;
+    wst[0][lane][wave] = m_run;
+    wst[1][lane][wave] = l_run;
   }
   if (lane == 0) {
     wmask[wave] = seen;
     wnv[wave] = max(nvm & 0xffffu, nvm >> 16);
   }
+#pragma unroll
+  for (int nb = 0; nb < 8; ++nb)  // rows 4g .. 4g + 3 of set 1 (audio, video heads), channel 16 nb + col
+    *reinterpret_cast<float4*>(&wacc[wave][16 * nb + col][4 * g]) =
+        make_float4(acc1[nb][0], acc1[nb][1], acc1[nb][2], acc1[nb][3]);
   __syncthreads();
   uint32_t mask = 0, nmax = 0;
 #pragma unroll
@@ -481,59 +546,56 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   // 2^e / L with e = 15 - ilogb(n_max) keeps the fp16 A tile below 2^13.
   const float nmf = h2f(nmax);
   const int e = (nmf > 0.0f) ? 15 - min(max(ilogbf(nmf), -30), 20) : 0;
-  float frow[4];  // 2^(m_wave - M) for this lane's accumulator rows (head (4g + i) % 8)
+  // factor table fac[head][wave] = 2^(m_w - M) 2^e / L (zero for heads >= G and empty waves):
+  // one thread per (head, wave)
+  if (tid < 8 * kDecWaves) {
+    const int hh = tid >> 3, w = tid & 7;
+    const float4 m0 = *reinterpret_cast<const float4*>(&wst[0][hh][0]);
+    const float4 m1 = *reinterpret_cast<const float4*>(&wst[0][hh][4]);
+    const float4 l0 = *reinterpret_cast<const float4*>(&wst[1][hh][0]);
+    const float4 l1 = *reinterpret_cast<const float4*>(&wst[1][hh][4]);
+    const float mv[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+    const float lv[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+    float M = mv[0];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int head = (4 * g + i) & 7;
-    float M = -__builtin_inff();
-#pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, wstate[w][0][head]);
-    const float mwv = wstate[wave][0][head];
-    frow[i] = (mwv == -__builtin_inff()) ? 0.0f : exp2f(mwv - M) * (1.0f / kPvScale);
-  }
-  if (mask & 3u) {
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) wacc[wave][4 * g + i][16 * nb + col] = acc1[nb][i] * frow[i];
-  }
-  if ((mask & 4u) && g < 2) {
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) wacc[wave][16 + 4 * g + i][16 * nb + col] = acc2[nb][i] * frow[i];
-  }
-  if (tid < 8) {
-    float M = -__builtin_inff();
-#pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) M = fmaxf(M, wstate[w][0][tid]);
+    for (int u = 1; u < kDecWaves; ++u) M = fmaxf(M, mv[u]);
     float L = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) {
-      const float mwv = wstate[w][0][tid];
-      L += (mwv == -__builtin_inff()) ? 0.0f : wstate[w][1][tid] * exp2f(mwv - M);
+    for (int u = 0; u < kDecWaves; ++u) L += (mv[u] == -__builtin_inff()) ? 0.0f : lv[u] * fast_exp2(mv[u] - M);
+    const float sc = (hh < p.G && L > 0.0f) ? ldexpf(1.0f / L, e) : 0.0f;
+    fac[hh][w] = (mv[w] == -__builtin_inff()) ? 0.0f : fast_exp2(mv[w] - M) * sc;
+    if (w == 0) {
+      rec[hh] = M;
+      rec[8 + hh] = L;
     }
-    hst[tid] = (tid < p.G && L > 0.0f) ? ldexpf(1.0f / L, e) : 0.0f;
-    rec[tid] = M;
-    rec[8 + tid] = L;
   }
   __syncthreads();
-  // acc rows 0-7 audio, 8-15 video (set 1), 16-23 text (set 2), summed over the waves and scaled
-  // -> A tile [head][128 m + k] (fp16)
-  for (int idx4 = tid; idx4 < 24 * kD / 4; idx4 += 64 * kDecWaves) {
-    const int row = idx4 >> 5, c4 = (idx4 & 31) * 4, m = row >> 3, head = row & 7;
+  // rows summed over the waves with their factors -> A tile [head][128 m + k] (fp16); thread =
+  // (row quad rq, channel k), rows 4 rq .. 4 rq + 3 = heads 4 (rq & 1) .. +3 of modality rq / 2
+  for (int idx = tid; idx < 6 * kD; idx += 64 * kDecWaves) {
+    const int rq = idx >> 7, k = idx & (kD - 1), m = rq >> 1, h0 = 4 * (rq & 1);
     if (!(mask & (1u << m))) continue;
-    float4 a = *reinterpret_cast<const float4*>(&wacc[0][row][c4]);
+    float a[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int w = 1; w < kDecWaves; ++w) {
-      const float4 v = *reinterpret_cast<const float4*>(&wacc[w][row][c4]);
-      a.x += v.x;
-      a.y += v.y;
-      a.z += v.z;
-      a.w += v.w;
+    for (int w4 = 0; w4 < kDecWaves; w4 += 4) {
+      float4 f[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) f[i] = *reinterpret_cast<const float4*>(&fac[h0 + i][w4]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float4 v = *reinterpret_cast<const float4*>(&wacc[w4 + u][k][4 * rq]);
+        const float fu[4] = {u == 0 ? f[0].x : u == 1 ? f[0].y : u == 2 ? f[0].z : f[0].w,
+                             u == 0 ? f[1].x : u == 1 ? f[1].y : u == 2 ? f[1].z : f[1].w,
+                             u == 0 ? f[2].x : u == 1 ? f[2].y : u == 2 ? f[2].z : f[2].w,
+                             u == 0 ? f[3].x : u == 1 ? f[3].y : u == 2 ? f[3].z : f[3].w};
+        a[0] = __builtin_fmaf(v.x, fu[0], a[0]);
+        a[1] = __builtin_fmaf(v.y, fu[1], a[1]);
+        a[2] = __builtin_fmaf(v.z, fu[2], a[2]);
+        a[3] = __builtin_fmaf(v.w, fu[3], a[3]);
+      }
     }
-    const float f = hst[head];
-    *reinterpret_cast<uint2*>(&atile[head][m * kD + c4]) = make_uint2(pack2(a.x * f, a.y * f), pack2(a.z * f, a.w * f));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) atile[h0 + i][m * kD + k] = (_Float16)a[i];
   }
   __syncthreads();
   // ---- inverse rotation on MFMA, once per present modality: wave w computes channels
@@ -555,6 +617,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) rec[kRecHeader + (4 * (lane >> 4) + i) * kD + 16 * wave + (lane & 15)] = dacc[i] * sc;
   }
+  if (touch == 0x7fc00001u && p.H < 0) rec[0] = 0.0f;  // keeps the table touch (never true)
 }
 
 // ---- merge over splits: o = sum_s 2^(M_s - M) L_s o_s / sum_s 2^(M_s - M) L_s (log-sum-exp) ----

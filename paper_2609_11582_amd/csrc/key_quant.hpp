@@ -174,7 +174,7 @@ __device__ __forceinline__ void key_quantize_wave(const uint32_t (&raw)[64], int
         const float t1 = (x[c + 1] - s.z) * s.w;
         const uint32_t c0 = (uint32_t)fminf(fmaxf(__builtin_rintf(t0), 0.0f), 3.0f);
         const uint32_t c1 = (uint32_t)fminf(fmaxf(__builtin_rintf(t1), 0.0f), 3.0f);
-        dw[c >> 4] |= (c0 << (2 * (c & 15))) | (c1 << (2 * ((c + 1) & 15)));
+        dw[c >> 4] |= (c0 << (c & 14)) | (c1 << (16 + (c & 14)));  // even channels low half, odd high
       }
     }
     uint4* dst = reinterpret_cast<uint4*>(out.codes + (size_t)tok * 32);

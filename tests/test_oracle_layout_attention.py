@@ -25,9 +25,14 @@ def test_tab3_bits_per_element(golden):
 
 def test_key_pack_examples_and_roundtrip():
     codes = np.zeros((3, 128), np.uint8)
-    codes[2, 5] = 3
+    codes[2, 5] = 3        # odd channel of pair 2 in word 0: high half, bits 16 + 4
+    codes[1, 8] = 1        # even channel of pair 4: low half, bits 8
+    codes[0, 127] = 2      # odd channel of pair 7 in word 7: high half, bits 16 + 14
     p = pack_keys(codes)
-    assert p[2, 1] == 0b1100 and p.sum() == 12
+    assert p[2, 2] == 0b110000 and p[1, 1] == 0b1 and p[0, 31] == 0b10000000
+    assert int(p.astype(np.int64).sum()) == 48 + 1 + 128
+    words = p.view("<u4")  # word t of a token: channel pair (16 t + 2 j, +1) under mask 3 * 0x00010001 << 2 j
+    assert (int(words[2, 0]) >> 16) & 0b110000 == 0b110000 and int(words[1, 0]) & (0x00030003 << 8) == 1 << 8
     rng = np.random.default_rng(0)
     c = rng.integers(0, 4, (64, 128)).astype(np.uint8)
     np.testing.assert_array_equal(unpack_keys(pack_keys(c)), c)
