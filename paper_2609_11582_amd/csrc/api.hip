@@ -237,7 +237,8 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
     if (n > 0) span = std::max(span, L + n - (L / 32) * 32);
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (span > 0) {
+  for (int b0 = 0; span > 0 && b0 < d.batch; b0 += kMaxLenArgs) {  // launches of up to 256 sequences
+    const int nb = std::min(kMaxLenArgs, d.batch - b0);
     CodecJob j{};
     j.src = k_new;
     j.msrc = mod_new;
@@ -245,15 +246,23 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
     j.begin_dev = cache->seq_lens;
     j.count_dev = n_new_dev;
     j.stage = cache->k_stage;
-    j.b0 = 0;
+    j.b0 = b0;
     j.H = d.num_kv_heads;
     j.cap = d.capacity;
-    st = hip_status(launch_quantize_keys(j, d.batch, span, cache->key_signs, cache->k_codes, cache->k_min,
+    int chunk_span = 0;
+    for (int i = 0; i < nb; ++i) {
+      const int L = lens_host[b0 + i], n = n_new_host[b0 + i];
+      j.lens.lens[i] = L;
+      j.cnts.lens[i] = n;
+      if (n > 0) chunk_span = std::max(chunk_span, L + n - (L / 32) * 32);
+    }
+    if (chunk_span == 0) continue;
+    st = hip_status(launch_quantize_keys(j, nb, chunk_span, cache->key_signs, cache->k_codes, cache->k_min,
                                          cache->k_step, cache->k_norm, s));
     if (st != OKVQ_OK) return st;
     j.src = v_new;
     j.stage = nullptr;
-    st = hip_status(launch_quantize_values(j, d.batch, span, cache->v_rot, thresholds(),
+    st = hip_status(launch_quantize_values(j, nb, chunk_span, cache->v_rot, thresholds(),
                                            (flags & OKVQ_VALUE_EXACT) != 0, cache->v_codes, cache->v_norm,
                                            cache->modality, s));
     if (st != OKVQ_OK) return st;

@@ -12,9 +12,9 @@
 namespace okvq {
 
 __device__ __forceinline__ void job_range(const CodecJob& j, int bz, int b, int& begin, int& len) {
-  if (j.begin_dev) {
-    begin = j.begin_dev[b];
-    len = begin + j.count_dev[b];
+  if (j.begin_dev) {  // clamped: device lengths outside the contract stay memory-safe
+    begin = min(max(j.begin_dev[b], 0), j.cap);
+    len = min(begin + min(max(j.count_dev[b], 0), j.n_rows), j.cap);
   } else {
     begin = 0;
     len = j.lens.lens[bz];
@@ -25,23 +25,11 @@ __device__ __forceinline__ void job_range(const CodecJob& j, int bz, int b, int&
 // Keys: grid (tiles of 256 tokens from the first open window, H, batches); 4 waves per block,
 // 64 tokens (two windows) per wave.
 // ------------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_quantize_keys(CodecJob j, const int8_t* __restrict__ signs,
-                                                       uint8_t* __restrict__ k_codes, uint16_t* __restrict__ k_min,
-                                                       uint16_t* __restrict__ k_step, uint16_t* __restrict__ k_norm) {
-  __shared__ __attribute__((aligned(16))) float lds[4 * kKeyWaveLds];
-  const int wave = threadIdx.x >> 6;
-  const int h = blockIdx.y, bz = blockIdx.z, b = j.b0 + bz;
-  int begin, len;
-  job_range(j, bz, b, begin, len);
-  if (len <= begin) return;
-  const int first = (begin / kW) * kW;  // first token of the first open window
-  const int tok0 = first + (blockIdx.x * 4 + wave) * 64;
-  if (tok0 >= len) return;  // no block-level barrier is used below
-  uint32_t sw[32];
-  load_sign_words(signs, sw);
-  const size_t seq = (size_t)b * j.H + h;
+// Token rows of one wave: older rows of the open window from the stage, then the new rows;
+// zeros beyond the length.
+__device__ __forceinline__ void load_key_rows(const CodecJob& j, size_t seq, int begin, int len, int first, int tok0,
+                                              uint32_t (&raw)[64]) {
   const int tok = tok0 + lane_id();
-  uint32_t raw[64];
   if (tok < begin) {
     load_row_f16(j.stage + (seq * kW + (tok - first)) * kD, raw);
   } else if (tok < len) {
@@ -50,6 +38,37 @@ __global__ __launch_bounds__(256) void k_quantize_keys(CodecJob j, const int8_t*
 #pragma unroll
     for (int i = 0; i < 64; ++i) raw[i] = 0;
   }
+}
+
+__global__ __launch_bounds__(256) void k_quantize_keys(CodecJob j, const int8_t* __restrict__ signs,
+                                                       uint8_t* __restrict__ k_codes, uint16_t* __restrict__ k_min,
+                                                       uint16_t* __restrict__ k_step, uint16_t* __restrict__ k_norm) {
+  __shared__ __attribute__((aligned(16))) float lds[4 * kKeyWaveLds];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform for the compiler
+  const int h = blockIdx.y, bz = blockIdx.z, b = j.b0 + bz;
+  const size_t seq = (size_t)b * j.H + h;
+  // rows from the planned lengths (append: the host's copy), then the device lengths decide
+  int begin = j.begin_dev ? j.lens.lens[bz] : 0;
+  int len = j.begin_dev ? begin + j.cnts.lens[bz] : j.lens.lens[bz];
+  int first = (begin / kW) * kW;  // first token of the first open window
+  int tok0 = first + (blockIdx.x * 4 + wave) * 64;
+  uint32_t raw[64];
+  load_key_rows(j, seq, begin, len, first, tok0, raw);
+  if (j.begin_dev) {
+    const int bd = min(max(j.begin_dev[b], 0), j.cap);
+    const int ld = min(bd + min(max(j.count_dev[b], 0), j.n_rows), j.cap);
+    if (bd != begin || ld != len) {  // stale host lengths: reload from the device ones
+      begin = bd;
+      len = ld;
+      first = (begin / kW) * kW;
+      tok0 = first + (blockIdx.x * 4 + wave) * 64;
+      load_key_rows(j, seq, begin, len, first, tok0, raw);
+    }
+  }
+  if (len <= begin || tok0 >= len) return;  // no block-level barrier is used below
+  uint32_t sw[32];
+  load_sign_words(signs, sw);
+  const int tok = tok0 + lane_id();
   if (j.stage && tok0 == first) {
     // The wave holding the old open window rewrites the stage with the raw rows of the new
     // open window [open, len). Only this wave reads or writes the stage of (b, h).

@@ -12,12 +12,14 @@ namespace okvq {
 // Where the codec kernels read token rows. Stateless calls (begin_dev == nullptr) quantize tokens
 // [0, lens[b - b0]) of a dense block. Append quantizes tokens [begin_dev[b], begin_dev[b] +
 // count_dev[b]) whose rows are src row (token - begin); older rows of the open key window come
-// from the fp16 stage.
+// from the fp16 stage. For append, lens / cnts hold the host's copy of the same lengths: the
+// kernels issue their row loads from them and then check the device values (which decide).
 struct CodecJob {
   const uint16_t* src;       // [B][H][n_rows][128] fp16
   const uint8_t* msrc;       // [B][n_rows] modality ids (values only)
   int n_rows;
-  LenArgs lens;              // stateless lengths for batches b0 .. b0 + 255
+  LenArgs lens;              // lengths (stateless) or current lengths (append) of batches b0 .. b0 + 255
+  LenArgs cnts;              // append: appended tokens of the same batches
   const int32_t* begin_dev;  // append: current lengths (device)
   const int32_t* count_dev;  // append: appended tokens (device)
   uint16_t* stage;           // append: [B][H][32][128] raw keys of the open window
