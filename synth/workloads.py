@@ -181,3 +181,27 @@ def gen_layer(wl: Workload, layer: int = 0, lengths: Optional[np.ndarray] = None
     return dict(k=k, v=v, modality=mod, lens=np.asarray(lengths, np.int32),
                 q=gen_queries(wl.wid, layer, B, wl.num_q_heads),
                 rot=gen_rotations(wl.wid, layer), signs=gen_signs(wl.wid, layer))
+
+
+def gen_stream_layer(wl: Workload, layer: int = 0):
+    """A prefill of wl.seq_len tokens followed by wl.stream_steps chunks of wl.stream_tokens tokens.
+
+    The prefill follows ``modality_layout`` (audio-visual chunks, then the text tail); the streamed
+    tokens continue the audio-visual pattern. Keys and values cover all tokens; the key drift walk
+    runs on through the streamed part. Returns the ``gen_layer`` fields plus ``prefill``.
+    """
+    pre = wl.seq_len
+    n = pre + wl.stream_steps * wl.stream_tokens
+    first = modality_layout(pre, wl.video_per_chunk, wl.audio_per_chunk, wl.text_tail)
+    rest = stream_chunk_modalities(wl, max(pre - wl.text_tail, 0), n - pre)
+    mod1 = np.concatenate([first, rest])
+    B, H = wl.batch, wl.num_kv_heads
+    k = np.zeros((B, H, n, HEAD_DIM), np.float16)
+    v = np.zeros((B, H, n, HEAD_DIM), np.float16)
+    for b in range(B):
+        for h in range(H):
+            k[b, h] = gen_keys(wl.wid, layer, b, h, n)
+            v[b, h] = gen_values(wl.wid, layer, b, h, mod1)
+    return dict(k=k, v=v, modality=np.tile(mod1, (B, 1)), lens=np.full(B, n, np.int32), prefill=pre,
+                q=gen_queries(wl.wid, layer, B, wl.num_q_heads),
+                rot=gen_rotations(wl.wid, layer), signs=gen_signs(wl.wid, layer))

@@ -111,3 +111,44 @@ def attention_close(out, ref, tol=2e-3):
     nrm = np.linalg.norm(ref, axis=-1)
     ratio = err / np.maximum(nrm, 1e-30)
     return float(np.nanmax(ratio))
+
+
+def band_compare(gpu_vcodes, v16, modality, rot, length):
+    """MFMA-mode value codes equal the exact order except where y is within the band of a threshold.
+
+    Returns (codes that differ, codes in the band)."""
+    from oracle.layout import unpack_values
+    from oracle.values import quantize_values_fmt, rotation_error_bound
+    ref = quantize_values_fmt(v16, modality, rot, length)
+    got = unpack_values(gpu_vcodes)[:length]
+    eps = rotation_error_bound(v16[:length], modality[:length], rot)
+    dist = np.abs(ref["y"][:, :, None].astype(np.float64) - ref["thr"][:, None, :].astype(np.float64)).min(-1)
+    in_band = dist <= eps
+    diff = got != ref["codes"]
+    assert not np.any(diff & ~in_band), f"{int((diff & ~in_band).sum())} codes differ outside the band"
+    assert np.all(np.abs(got.astype(int) - ref["codes"].astype(int)) <= 1)
+    return int(diff.sum()), int(in_band.sum())
+
+
+def check_window(arrays, k16, v16, modality, signs, rot, b, h, w, length):
+    """One 32-token window of a GPU-written cache against the oracle: key fields bit-exact, value
+    norms bit-exact, value codes by the band rule, padded slots zero. ``length`` is the sequence
+    length; k16 / v16 / modality are the sequence's full inputs."""
+    from oracle.keys import quantize_keys_fmt
+    from oracle.layout import pack_keys, unpack_values
+    from oracle.values import quantize_values_fmt
+    a = 32 * w
+    n = min(32, length - a)
+    assert n > 0
+    kq = quantize_keys_fmt(k16[a:a + n], n, signs)
+    np.testing.assert_array_equal(arrays["k_norm"][b, h, a:a + n].view(np.uint16), kq["n16"][:n].view(np.uint16))
+    np.testing.assert_array_equal(arrays["k_min"][b, h, w].view(np.uint16), kq["m16"][0].view(np.uint16))
+    np.testing.assert_array_equal(arrays["k_step"][b, h, w].view(np.uint16), kq["step16"][0].view(np.uint16))
+    np.testing.assert_array_equal(arrays["k_codes"][b, h, a:a + n], pack_keys(kq["codes"][:n]))
+    vq = quantize_values_fmt(v16[a:a + n], modality[a:a + n], rot, n)
+    np.testing.assert_array_equal(arrays["v_norm"][b, h, a:a + n].view(np.uint16), vq["n16"].view(np.uint16))
+    band_compare(arrays["v_codes"][b, h, w:w + 1], v16[a:a + n], modality[a:a + n], rot, n)
+    np.testing.assert_array_equal(arrays["modality"][b, a:a + n], modality[a:a + n])
+    if n < 32:
+        assert not np.any(arrays["k_codes"][b, h, a + n:a + 32])
+        assert not np.any(unpack_values(arrays["v_codes"][b, h, w:w + 1])[n:])
