@@ -74,6 +74,9 @@ enum {
   OKVQ_VALUE_EXACT = 1u << 0 /* value rotation as a sequential fp32 dot product (bit-exact codes) */
 };
 
+/* bytes of the prepared rotation tables (okvq_cache.v_rot16, okvq_prepare_rotation) */
+#define OKVQ_ROTATION_TABLE_BYTES 294912
+
 /* which_buffer for okvq_buffer_bytes */
 enum {
   OKVQ_BUF_K_CODES = 0, OKVQ_BUF_V_CODES, OKVQ_BUF_K_NORM, OKVQ_BUF_V_NORM, OKVQ_BUF_K_MIN,
@@ -102,9 +105,10 @@ typedef struct {               /* all pointers are device memory, laid out as ab
   int32_t* seq_lens;
   const int8_t* key_signs;     /* [128] +1 / -1: H = Had diag(s) / sqrt(128) (Eq. 2)        */
   const float* v_rot;          /* [3][128][128] fp32 row-major R_m, z = R_m u (Eq. 6)       */
-  const uint16_t* v_rot16;     /* [128][3][128] fp16, written by okvq_prepare_rotation from
-                                  v_rot: element (c, m, k) = R_m[k][c], the inverse rotation
-                                  that decode applies once per modality (Sec. 2.3)           */
+  const uint16_t* v_rot16;     /* OKVQ_ROTATION_TABLE_BYTES written by okvq_prepare_rotation
+                                  from v_rot: the inverse rotation that decode applies once per
+                                  modality (Sec. 2.3), then the forward rotation of append in
+                                  the operand layout of its matrix-core kernel              */
 } okvq_cache;
 
 /* Library version (major * 10000 + minor * 100 + patch). */
@@ -155,15 +159,21 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
  * The open key window is re-quantized from the staged raw keys plus the new ones, so any
  * chunking of a sequence yields the same cache bytes as one quantization of the whole sequence.
  * cache->seq_lens[b] is advanced by n_new[b] on the device. Fails with OKVQ_ERR_CAPACITY if
- * lens_host[b] + n_new_host[b] > capacity. */
+ * lens_host[b] + n_new_host[b] > capacity. The MFMA-mode values read the forward rotation from
+ * cache->v_rot16 (okvq_prepare_rotation); OKVQ_VALUE_EXACT reads cache->v_rot. */
 okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
                         const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
                         const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream);
 
-/* Inverse value rotation table for decode (Sec. 2.3: the inverse rotation is applied once per
- * modality after aggregation). Per layer, once: v_rot16[c][m][k] = fp16(v_rot[m][k][c]) (RNE).
+/* Rotation tables of a layer, prepared once from v_rot (fp16, round to nearest even):
+ *   bytes [0, 98304)       inverse rotation for decode (Sec. 2.3: applied once per modality after
+ *                          aggregation): [128][3][128], element (c, m, k) = fp16(R_m[k][c]);
+ *   bytes [98304, 294912)  forward rotation for the MFMA-mode values of append (Eq. 6): 192
+ *                          blocks of 64 x 8 fp16, block ((m 8 + nb) 4 + kk) 2 + part, row l,
+ *                          element e = part(R_m[16 nb + l % 16][32 kk + 8 (l / 16) + e]) with
+ *                          part 0 = fp16(R), part 1 = fp16(R - fp16(R)) (fp32 difference).
  *   v_rot    device f32 [3][128][128]
- *   v_rot16  device f16 [128][3][128] (98304 bytes), the okvq_cache.v_rot16 of every cache
+ *   v_rot16  device, OKVQ_ROTATION_TABLE_BYTES bytes: the okvq_cache.v_rot16 of every cache
  *            that uses v_rot */
 okvq_status okvq_prepare_rotation(const float* v_rot, uint16_t* v_rot16, void* stream);
 

@@ -109,6 +109,12 @@ CacheView view(const okvq_cache* c) {
 
 okvq_status hip_status(hipError_t e) { return e == hipSuccess ? OKVQ_OK : OKVQ_ERR_HIP; }
 
+// Tiles of 256 tokens covering `span` tokens from each sequence's first open window.
+void plan_tiles(CodecArgs& a, int nb, int span) {
+  a.ntx = (span + 255) / 256;
+  a.ntiles = a.ntx * a.j.H * nb;
+}
+
 }  // namespace
 
 extern "C" {
@@ -168,18 +174,24 @@ okvq_status okvq_quantize_keys(const okvq_dims* dims, const uint16_t* k, int32_t
   hipStream_t s = static_cast<hipStream_t>(stream);
   for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
     const int nb = std::min(kMaxLenArgs, dims->batch - b0);
-    CodecJob j{};
-    j.src = k;
-    j.n_rows = n_tokens;
-    j.b0 = b0;
-    j.H = dims->num_kv_heads;
-    j.cap = dims->capacity;
+    CodecArgs a{};
+    a.j.src = k;
+    a.j.n_rows = n_tokens;
+    a.j.b0 = b0;
+    a.j.H = dims->num_kv_heads;
+    a.j.cap = dims->capacity;
     int max_len = 0;
     for (int i = 0; i < nb; ++i) {
-      j.lens.lens[i] = lens_host[b0 + i];
+      a.j.lens.lens[i] = lens_host[b0 + i];
       max_len = std::max(max_len, lens_host[b0 + i]);
     }
-    st = hip_status(launch_quantize_keys(j, nb, max_len, key_signs, k_codes, k_min, k_step, k_norm, s));
+    plan_tiles(a, nb, max_len);
+    a.signs = key_signs;
+    a.k_codes = k_codes;
+    a.k_min = k_min;
+    a.k_step = k_step;
+    a.k_norm = k_norm;
+    st = hip_status(launch_codec(a, true, false, s));
     if (st != OKVQ_OK) return st;
   }
   return OKVQ_OK;
@@ -198,23 +210,32 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
     if (lens_host[b] > dims->capacity) return OKVQ_ERR_CAPACITY;
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const Thresholds th = thresholds();
+  const bool exact = (flags & OKVQ_VALUE_EXACT) != 0;
   for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
     const int nb = std::min(kMaxLenArgs, dims->batch - b0);
-    CodecJob j{};
-    j.src = v;
-    j.msrc = modality;
-    j.n_rows = n_tokens;
-    j.b0 = b0;
-    j.H = dims->num_kv_heads;
-    j.cap = dims->capacity;
+    CodecArgs a{};
+    a.j.src = v;
+    a.j.msrc = modality;
+    a.j.n_rows = n_tokens;
+    a.j.b0 = b0;
+    a.j.H = dims->num_kv_heads;
+    a.j.cap = dims->capacity;
     int max_len = 0;
     for (int i = 0; i < nb; ++i) {
-      j.lens.lens[i] = lens_host[b0 + i];
+      a.j.lens.lens[i] = lens_host[b0 + i];
       max_len = std::max(max_len, lens_host[b0 + i]);
     }
-    st = hip_status(launch_quantize_values(j, nb, max_len, v_rot, th, (flags & OKVQ_VALUE_EXACT) != 0, v_codes, v_norm,
-                                           nullptr, s));
+    if (exact) {
+      st = hip_status(launch_quantize_values_exact(a.j, nb, max_len, v_rot, thresholds(), v_codes, v_norm, nullptr, s));
+    } else {
+      plan_tiles(a, nb, max_len);
+      a.vsrc = v;
+      a.rot = v_rot;
+      a.th = thresholds();
+      a.v_codes = v_codes;
+      a.v_norm = v_norm;
+      st = hip_status(launch_codec(a, false, true, s));
+    }
     if (st != OKVQ_OK) return st;
   }
   return OKVQ_OK;
@@ -237,34 +258,50 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
     if (n > 0) span = std::max(span, L + n - (L / 32) * 32);
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool exact = (flags & OKVQ_VALUE_EXACT) != 0;
   for (int b0 = 0; span > 0 && b0 < d.batch; b0 += kMaxLenArgs) {  // launches of up to 256 sequences
     const int nb = std::min(kMaxLenArgs, d.batch - b0);
-    CodecJob j{};
-    j.src = k_new;
-    j.msrc = mod_new;
-    j.n_rows = n_max;
-    j.begin_dev = cache->seq_lens;
-    j.count_dev = n_new_dev;
-    j.stage = cache->k_stage;
-    j.b0 = b0;
-    j.H = d.num_kv_heads;
-    j.cap = d.capacity;
+    CodecArgs a{};
+    a.j.src = k_new;
+    a.j.msrc = mod_new;
+    a.j.n_rows = n_max;
+    a.j.begin_dev = cache->seq_lens;
+    a.j.count_dev = n_new_dev;
+    a.j.stage = cache->k_stage;
+    a.j.b0 = b0;
+    a.j.H = d.num_kv_heads;
+    a.j.cap = d.capacity;
     int chunk_span = 0;
     for (int i = 0; i < nb; ++i) {
       const int L = lens_host[b0 + i], n = n_new_host[b0 + i];
-      j.lens.lens[i] = L;
-      j.cnts.lens[i] = n;
+      a.j.lens.lens[i] = L;
+      a.j.cnts.lens[i] = n;
       if (n > 0) chunk_span = std::max(chunk_span, L + n - (L / 32) * 32);
     }
     if (chunk_span == 0) continue;
-    st = hip_status(launch_quantize_keys(j, nb, chunk_span, cache->key_signs, cache->k_codes, cache->k_min,
-                                         cache->k_step, cache->k_norm, s));
-    if (st != OKVQ_OK) return st;
-    j.src = v_new;
-    j.stage = nullptr;
-    st = hip_status(launch_quantize_values(j, nb, chunk_span, cache->v_rot, thresholds(),
-                                           (flags & OKVQ_VALUE_EXACT) != 0, cache->v_codes, cache->v_norm,
-                                           cache->modality, s));
+    plan_tiles(a, nb, chunk_span);
+    a.signs = cache->key_signs;
+    a.k_codes = cache->k_codes;
+    a.k_min = cache->k_min;
+    a.k_step = cache->k_step;
+    a.k_norm = cache->k_norm;
+    a.th = thresholds();
+    a.v_codes = cache->v_codes;
+    a.v_norm = cache->v_norm;
+    a.mod_out = cache->modality;
+    if (exact) {
+      st = hip_status(launch_codec(a, true, false, s));
+      if (st != OKVQ_OK) return st;
+      CodecJob jv = a.j;
+      jv.src = v_new;
+      jv.stage = nullptr;
+      st = hip_status(launch_quantize_values_exact(jv, nb, chunk_span, cache->v_rot, a.th, cache->v_codes,
+                                                   cache->v_norm, cache->modality, s));
+    } else {
+      a.vsrc = v_new;
+      a.rotfrag = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cache->v_rot16) + kRotInverseBytes);
+      st = hip_status(launch_codec(a, true, true, s));
+    }
     if (st != OKVQ_OK) return st;
   }
   return hip_status(launch_advance_lengths(cache->seq_lens, n_new_dev, d.batch, s));
@@ -272,7 +309,11 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
 
 okvq_status okvq_prepare_rotation(const float* v_rot, uint16_t* v_rot16, void* stream) {
   if (!aligned16(v_rot) || !aligned16(v_rot16)) return OKVQ_ERR_INVALID_ARGUMENT;
-  return hip_status(launch_prepare_rotation(v_rot, v_rot16, static_cast<hipStream_t>(stream)));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  okvq_status st = hip_status(launch_prepare_rotation(v_rot, v_rot16, s));
+  if (st != OKVQ_OK) return st;
+  return hip_status(launch_prepare_fragments(
+      v_rot, reinterpret_cast<uint4*>(reinterpret_cast<char*>(v_rot16) + kRotInverseBytes), s));
 }
 
 size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len) {

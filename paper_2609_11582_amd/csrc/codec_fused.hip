@@ -1,0 +1,487 @@
+// Key and value codecs of append and of the stateless MFMA-mode calls, in one persistent launch
+// (Sec. 2.1 Eq. 2 and Sec. 2.3 Eq. 4 for keys; Sec. 2.3 Eq. 6 with the codebook of Eq. 3 for
+// values).
+//
+// Work unit: a tile of 256 consecutive tokens of one (sequence, KV head), counted from the
+// sequence's first open window. A work-group has one or both of two roles, fixed per wave:
+//  * key waves (4): wave k quantizes tokens [64 k, 64 k + 64) of the tile (key_quant.hpp);
+//  * value waves (4): phase 1 -- wave v takes tokens [64 v, 64 v + 64): fp16 norms, decision
+//    scales and per-modality token masks go to a work-group table; phase 2 -- wave v takes
+//    output channels [32 v, 32 v + 32) of all 256 tokens: y = R_m v on the matrix cores with the
+//    wave's slice of R_m held in registers as MFMA B operands (fp16 hi + lo, fp32 accumulation),
+//    one modality at a time, then the codes.
+// Key waves never wait for value waves. The value waves' one dependency (phase 1 -> phase 2) is
+// an arrival counter in LDS, not a work-group barrier, so the key waves' VALU work overlaps the
+// value waves' loads and MFMAs on the same SIMDs. The grid is persistent: work-group i walks the
+// tiles i, i + gridDim.x, ...; a key wave loads its next tile's rows straight into LDS while it
+// computes the codes of the current one.
+//
+// Value decision: the thresholds are symmetric (-T, 0, T with T = fl(n16 tau_2)), so the code is
+// clamp(floor(y / T) + 2, 0, 3), formed as RNE(y fl(1/T) - 1/2) + 2 by adding 1.5 * 2^23. The
+// result can differ from the comparisons only where y lies within about 2^-21 T of a threshold,
+// far inside the 2^-16 sum_j |R_cj v_j| band that separates MFMA mode from the sequential order.
+//
+// MFMA 16x16x32 f16 lane mapping (wave64): lane l holds A[l % 16][8 (l / 16) + e], e = 0..7,
+// B[8 (l / 16) + e][l % 16], and D[4 (l / 16) + i][l % 16], i = 0..3. With rows = tokens and
+// columns = output channels, lane l ends with channel 16 nb + l % 16 of four consecutive tokens:
+// one byte of the value-code layout, at offset 16 l + 8 (rb & 1) + nb of the window block.
+#include <algorithm>
+
+#include "key_quant.hpp"
+#include "launch.hpp"
+
+namespace okvq {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ half8 as_half8(uint4 u) { return __builtin_bit_cast(half8, u); }
+
+constexpr int kTile = 256;          // tokens per tile
+constexpr int kSpinLimit = 1 << 22;  // polls of the value-wave arrival counter before giving up
+
+struct TileCtx {
+  int b, bz, h;
+  size_t seq;
+  int begin, len;  // the tokens [begin, len) are new (stateless: begin = 0)
+  int first;       // first token of the first open window
+  int tile0;       // first token of the tile
+};
+
+// Tile t of the launch from the host's lengths; t enumerates (x, h, bz), x fastest.
+__device__ __forceinline__ TileCtx tile_from_hint(const CodecJob& j, int ntx, int t) {
+  TileCtx c;
+  const int x = t % ntx, r = t / ntx;
+  c.h = r % j.H;
+  c.bz = r / j.H;
+  c.b = j.b0 + c.bz;
+  c.seq = (size_t)c.b * j.H + c.h;
+  if (j.begin_dev) {
+    c.begin = j.lens.lens[c.bz];
+    c.len = c.begin + j.cnts.lens[c.bz];
+  } else {
+    c.begin = 0;
+    c.len = j.lens.lens[c.bz];
+  }
+  c.first = (c.begin / kW) * kW;
+  c.tile0 = c.first + kTile * x;
+  return c;
+}
+
+// Append: the device lengths decide (clamped, so that values outside the contract stay memory
+// safe). Returns true where they differ from the host's copy the tile was planned with.
+__device__ __forceinline__ bool tile_check_device(const CodecJob& j, int ntx, int t, TileCtx& c) {
+  if (!j.begin_dev) return false;
+  const int bd = min(max(j.begin_dev[c.b], 0), j.cap);
+  const int ld = min(bd + min(max(j.count_dev[c.b], 0), j.n_rows), j.cap);
+  if (bd == c.begin && ld == c.len) return false;
+  c.begin = bd;
+  c.len = ld;
+  c.first = (bd / kW) * kW;
+  c.tile0 = c.first + kTile * (t % ntx);
+  return true;
+}
+
+// ------------------------------------------------------------------------------------------------
+// Key role
+// ------------------------------------------------------------------------------------------------
+// Rows of tokens tok0 + lane into the wave's LDS row buffer (16 blocks of 64 lanes x 16 bytes),
+// straight from memory without passing through registers: older rows of the open window from the
+// stage, then the new rows. Lanes beyond the length load nothing.
+__device__ __forceinline__ void prefetch_key_rows(const CodecJob& j, const TileCtx& c, int tok0, uint4* buf) {
+  const int tok = tok0 + lane_id();
+  if (tok >= c.len) return;
+  const uint4* row = reinterpret_cast<const uint4*>(tok < c.begin ? j.stage + (c.seq * kW + (tok - c.first)) * kD
+                                                                   : j.src + (c.seq * j.n_rows + (tok - c.begin)) * kD);
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    __builtin_amdgcn_global_load_lds(row + i, (__attribute__((address_space(3))) void*)(buf + 64 * i), 16, 0, 0);
+}
+
+// The lane's row from the buffer once every load of the wave has landed; zeros beyond the length.
+__device__ __forceinline__ void read_key_rows(const TileCtx& c, int tok0, const uint4* buf, uint32_t (&raw)[64]) {
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  const int lane = lane_id();
+  const bool valid = tok0 + lane < c.len;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const uint4 v = buf[64 * i + lane];
+    raw[4 * i + 0] = valid ? v.x : 0u;
+    raw[4 * i + 1] = valid ? v.y : 0u;
+    raw[4 * i + 2] = valid ? v.z : 0u;
+    raw[4 * i + 3] = valid ? v.w : 0u;
+  }
+}
+
+// The wave holding the old open window rewrites the stage with the raw rows of the new open
+// window [open, len). Only this wave reads or writes the stage of (b, h) during the launch.
+__device__ __forceinline__ void rewrite_stage(const CodecJob& j, const TileCtx& c, int tok0, const uint32_t (&raw)[64]) {
+  const int open = (c.len / kW) * kW;
+  if (open >= c.len) return;  // (the stage reads of this tile have landed: raw was read from them)
+  const int lane = lane_id(), tok = tok0 + lane;
+  const int slot = lane & 31;
+  uint16_t* dst = j.stage + (c.seq * kW + slot) * kD;
+  if (open < tok0 + 64) {
+    if (tok >= open && tok < c.len) {
+      uint4* d4 = reinterpret_cast<uint4*>(dst);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) d4[i] = make_uint4(raw[4 * i], raw[4 * i + 1], raw[4 * i + 2], raw[4 * i + 3]);
+    }
+  } else if (lane < 32 && open + slot < c.len) {
+    const uint4* s4 = reinterpret_cast<const uint4*>(j.src + (c.seq * j.n_rows + (open + slot - c.begin)) * kD);
+    uint4* d4 = reinterpret_cast<uint4*>(dst);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) d4[i] = s4[i];
+  }
+}
+
+__device__ __forceinline__ void key_role(const CodecArgs& a, int kw, float* lds) {
+  const CodecJob& j = a.j;
+  int t = blockIdx.x;
+  if (t >= a.ntiles) return;
+  // The transpose tile of phase B doubles as the row buffer: the next tile's rows are loaded into
+  // it after phase B has read it for the last time.
+  uint4* pf = reinterpret_cast<uint4*>(lds);
+  static_assert(16 * 64 * 16 <= 64 * kKeyPitch * 4, "row buffer fits the transpose tile");
+  TileCtx c = tile_from_hint(j, a.ntx, t);
+  prefetch_key_rows(j, c, c.tile0 + 64 * kw, pf);
+  for (;;) {
+    if (tile_check_device(j, a.ntx, t, c)) prefetch_key_rows(j, c, c.tile0 + 64 * kw, pf);
+    const int tok0 = c.tile0 + 64 * kw;
+    const bool work = c.len > c.begin && tok0 < c.len;  // wave-uniform
+    float x[kD];
+    uint32_t n16 = 0;
+    if (work) {
+      uint32_t raw[64];
+      read_key_rows(c, tok0, pf, raw);
+      uint32_t sw[32];  // sign words, loaded where they are used (scalar registers are scarce)
+      load_sign_words(a.signs, sw);
+      key_unpack(raw, sw, x);
+      if (j.stage && tok0 == c.first) rewrite_stage(j, c, tok0, raw);
+      n16 = key_norm(x);
+    }
+    const int tn = t + gridDim.x;
+    TileCtx cn = c;
+    auto prefetch = [&]() {  // the next tile's rows, in flight during phase C and the tile change
+      if (tn < a.ntiles) {
+        cn = tile_from_hint(j, a.ntx, tn);
+        prefetch_key_rows(j, cn, cn.tile0 + 64 * kw, pf);
+      }
+    };
+    if (work) {
+      KeyWaveOut out{a.k_codes + c.seq * j.cap * 32, a.k_min + c.seq * (j.cap / kW) * kD,
+                     a.k_step + c.seq * (j.cap / kW) * kD, a.k_norm + c.seq * j.cap};
+      key_quantize_rows(x, n16, tok0, c.len, out, lds, prefetch);
+    } else {
+      prefetch();
+    }
+    if (tn >= a.ntiles) break;
+    t = tn;
+    c = cn;
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Value role
+// ------------------------------------------------------------------------------------------------
+struct ValueShared {
+  float itab[2][kTile];       // per tile (double-buffered): fl(1 / T) of each token
+  uint8_t ktab[2][3][64];     // per modality and token quad: 2-bit masks of the quad's coded tokens
+  uint32_t rbm[2][4];         // per phase-1 wave: its row blocks holding each modality (4 bits at 4 m)
+  uint32_t count;             // arrivals of the value waves at the phase-1 -> phase-2 point
+};
+
+// The four value waves wait for each other (LDS counter, monotonically increasing).
+__device__ __forceinline__ void value_wave_sync(uint32_t* count, uint32_t target) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");  // this wave's table writes are done
+  if (lane_id() == 0) __hip_atomic_fetch_add(count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  for (int i = 0; i < kSpinLimit; ++i) {
+    const uint32_t seen =
+        __builtin_amdgcn_readfirstlane(__hip_atomic_load(count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
+    if (seen >= target) break;
+    __builtin_amdgcn_s_sleep(1);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// The wave's slice of R_m as B operands: bf[u][kk][part] for output block nb = 2 v + u, k-block kk,
+// part 0 = fp16(R) and 1 = fp16(R - fp16(R)). From the prepared fragments when there are any,
+// else converted here from the fp32 matrix.
+__device__ __forceinline__ void load_rot_slice(const CodecArgs& a, int m, int v, uint4 (&bf)[2][4][2]) {
+  const int lane = lane_id();
+  if (a.rotfrag) {
+    const uint4* src = a.rotfrag + (size_t)(m * 8 + 2 * v) * 8 * 64 + lane;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int part = 0; part < 2; ++part) bf[u][kk][part] = src[((u * 4 + kk) * 2 + part) * 64];
+    return;
+  }
+  const int r = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const float4* p = reinterpret_cast<const float4*>(a.rot + ((size_t)(m * kD + 16 * (2 * v + u) + r)) * kD + 32 * kk + 8 * g);
+      const float4 f0 = p[0], f1 = p[1];
+      const float fv[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+      half8 hv, lv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        hv[e] = (_Float16)fv[e];
+        lv[e] = (_Float16)(fv[e] - (float)hv[e]);
+      }
+      bf[u][kk][0] = __builtin_bit_cast(uint4, hv);
+      bf[u][kk][1] = __builtin_bit_cast(uint4, lv);
+    }
+}
+
+// A operands of row block rb of the tile (16 tokens, the lane's 8-channel slices of its row).
+// Rows outside [begin, len) read a clamped row: their codes are masked.
+__device__ __forceinline__ void load_a_block(const CodecArgs& a, const TileCtx& c, int rb, uint4 (&av)[4]) {
+  const int lane = lane_id(), r = lane & 15, g = lane >> 4;
+  const int tok = c.tile0 + 16 * rb + r;
+  const int row = min(max(tok - c.begin, 0), a.j.n_rows - 1);
+  const uint4* p = reinterpret_cast<const uint4*>(a.vsrc + (c.seq * a.j.n_rows + row) * kD);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) av[kk] = p[4 * kk + g];
+}
+
+// Two code bytes (output blocks 2v, 2v+1) of the lane's four tokens.
+__device__ __forceinline__ uint32_t value_bytes(floatx4 y0, floatx4 y1, float4 it) {
+  constexpr float kRound = 12582912.0f;  // 1.5 * 2^23
+  constexpr int kBase = 0x4B400000;      // its bit pattern
+  const float iv[4] = {it.x, it.y, it.z, it.w};
+  uint32_t s0 = 0, s1 = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    int q0 = __builtin_bit_cast(int, __builtin_fmaf(y0[i], iv[i], -0.5f) + kRound);
+    int q1 = __builtin_bit_cast(int, __builtin_fmaf(y1[i], iv[i], -0.5f) + kRound);
+    q0 = min(max(q0, kBase - 2), kBase + 1);  // floor(y / T) in [-2, 1], plus the base pattern
+    q1 = min(max(q1, kBase - 2), kBase + 1);
+    s0 += (uint32_t)q0 << (2 * i);  // the base pattern only reaches bits 22 and up
+    s1 += (uint32_t)q1 << (2 * i);
+  }
+  return ((s0 + 0xAAu) & 0xFFu) | (((s1 + 0xAAu) & 0xFFu) << 8);  // + 2 per token
+}
+
+__device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShared& sh) {
+  const CodecJob& j = a.j;
+  const int lane = lane_id(), r = lane & 15, g = lane >> 4;
+  const int ncw = j.cap / kW;
+  uint32_t synced = 0;
+  for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
+    TileCtx c = tile_from_hint(j, a.ntx, t);
+    tile_check_device(j, a.ntx, t, c);
+    if (c.len <= c.begin || c.tile0 >= c.len) continue;  // uniform over the work-group
+    const int buf = synced & 1;
+    const int wend = ((c.len + kW - 1) / kW) * kW;  // end of the last window
+
+    // ---- phase 1: tokens [64 v, 64 v + 64) of the tile ----
+    const int wtok0 = c.tile0 + 64 * v;
+    uint4 av[4][4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      const int tok = wtok0 + 16 * rb + r;
+      const bool fresh = tok >= c.begin && tok < c.len;
+      const int row = min(max(tok - c.begin, 0), j.n_rows - 1);
+      const uint4* p = reinterpret_cast<const uint4*>(a.vsrc + (c.seq * j.n_rows + row) * kD);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) av[rb][kk] = fresh ? p[4 * kk + g] : make_uint4(0, 0, 0, 0);
+    }
+    const int mytok = wtok0 + lane;
+    const bool myfresh = mytok >= c.begin && mytok < c.len;
+    const int mymod = myfresh ? (int)j.msrc[(size_t)c.b * j.n_rows + min(max(mytok - c.begin, 0), j.n_rows - 1)] : 3;
+    uint4 bf[2][4][2];
+    if (a.rotfrag) load_rot_slice(a, 1, v, bf);  // video slice, in flight during phase 1
+
+    // norms by the halving tree: levels 64 and 32 stay in the lane (k-blocks kk, kk + 2 and
+    // 0, 1); level 16 pairs lane groups g, g ^ 2 and level 8 pairs g, g ^ 1, each exchange
+    // halving the row blocks a lane keeps, so that lane l ends with token 16 g + r = l
+    float p[4][8];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      const half8 x0 = as_half8(av[rb][0]), x1 = as_half8(av[rb][1]), x2 = as_half8(av[rb][2]),
+                  x3 = as_half8(av[rb][3]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float f0 = (float)x0[e], f1 = (float)x1[e], f2 = (float)x2[e], f3 = (float)x3[e];
+        const float l0 = __builtin_fmaf(f0, f0, f2 * f2);  // squares of fp16 values are exact
+        const float l1 = __builtin_fmaf(f1, f1, f3 * f3);
+        p[rb][e] = l0 + l1;
+      }
+    }
+    const bool upper = g >= 2;
+    float q[2][8];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float keep = upper ? p[2 + i][e] : p[i][e];
+        const float send = upper ? p[i][e] : p[2 + i][e];
+        q[i][e] = keep + __shfl_xor(send, 32);
+      }
+    const bool odd = (g & 1) != 0;
+    float s[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float keep = odd ? q[1][e] : q[0][e];
+      const float send = odd ? q[0][e] : q[1][e];
+      s[e] = keep + __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, send), 0x401f));
+    }
+#pragma unroll
+    for (int n = 4; n >= 1; n >>= 1) {
+#pragma unroll
+      for (int e = 0; e < n; ++e) s[e] = s[e] + s[e + n];
+    }
+    const uint32_t n16 = myfresh ? norm_to_f16(sqrt_rn(s[0])) : 0u;
+    const int mt = (n16 != 0 && (uint32_t)mymod <= 2u) ? mymod : 3;  // 3: no code
+    sh.itab[buf][64 * v + lane] = (n16 != 0) ? __builtin_amdgcn_rcpf(h2f(n16) * a.th.t2) : 0.0f;
+    if (mytok >= c.begin && mytok < wend) a.v_norm[c.seq * j.cap + mytok] = (uint16_t)n16;
+    if (myfresh && a.mod_out && c.h == 0) a.mod_out[(size_t)c.b * j.cap + mytok] = (uint8_t)mymod;
+    uint32_t rbw = 0;
+#pragma unroll
+    for (int m = 0; m < 3; ++m) {
+      const uint64_t mb = __ballot(mt == m);
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb)
+        if ((mb >> (16 * rb)) & 0xffffu) rbw |= 1u << (4 * m + rb);
+      if (lane < 16) {  // quad `lane`: tokens 4 lane .. 4 lane + 3 -> bits 2i, 2i + 1
+        const uint32_t b4 = (uint32_t)(mb >> (4 * lane)) & 15u;
+        const uint32_t spread = (b4 & 1u) | ((b4 & 2u) << 1) | ((b4 & 4u) << 2) | ((b4 & 8u) << 3);
+        sh.ktab[buf][m][16 * v + lane] = (uint8_t)(spread * 3u);
+      }
+    }
+    if (lane == 0) sh.rbm[buf][v] = rbw;
+    ++synced;
+    value_wave_sync(&sh.count, 4 * synced);
+
+    // ---- phase 2: output channels [32 v, 32 v + 32) of all 256 tokens ----
+    uint32_t rbmask[3];
+    {
+      const uint4 w4 = *reinterpret_cast<const uint4*>(&sh.rbm[buf][0]);
+      const uint32_t ws[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+      for (int m = 0; m < 3; ++m) {
+        rbmask[m] = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) rbmask[m] |= ((ws[u] >> (4 * m)) & 15u) << (4 * u);
+        rbmask[m] = __builtin_amdgcn_readfirstlane(rbmask[m]);
+      }
+    }
+    uint32_t vb[8];  // window ww: bits 0-15 row block 2 ww, bits 16-31 row block 2 ww + 1
+#pragma unroll
+    for (int ww = 0; ww < 8; ++ww) vb[ww] = 0;
+    for (int mi = 0; mi < 3; ++mi) {
+      const int m = (mi == 0) ? 1 : (mi == 1 ? 0 : 2);  // video, audio, text
+      const uint32_t rbs = rbmask[m];
+      if (rbs == 0) continue;
+      if (mi > 0 || !a.rotfrag) load_rot_slice(a, m, v, bf);
+      uint4 ab[2][4];  // A operands, by row-block parity: the next present row block is prefetched
+#pragma unroll
+      for (int rb = 0; rb < 16; ++rb) {
+        if (!((rbs >> rb) & 1u)) continue;
+        if (rb == 0 || !((rbs >> (rb - 1)) & 1u)) load_a_block(a, c, rb, ab[rb & 1]);
+        if (rb < 15 && ((rbs >> (rb + 1)) & 1u)) load_a_block(a, c, rb + 1, ab[(rb + 1) & 1]);
+        floatx4 y0 = {0.f, 0.f, 0.f, 0.f}, y1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const half8 x = as_half8(ab[rb & 1][kk]);
+#pragma unroll
+          for (int part = 0; part < 2; ++part) {
+            y0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(x, as_half8(bf[0][kk][part]), y0, 0, 0, 0);
+            y1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(x, as_half8(bf[1][kk][part]), y1, 0, 0, 0);
+          }
+        }
+        const float4 it = *reinterpret_cast<const float4*>(&sh.itab[buf][16 * rb + 4 * g]);
+        const uint32_t keep = (uint32_t)sh.ktab[buf][m][4 * rb + g] * 0x0101u;
+        vb[rb >> 1] |= (value_bytes(y0, y1, it) & keep) << (16 * (rb & 1));
+      }
+    }
+
+    // ---- store: two bytes per lane and row block, windows that hold a token below the length ----
+#pragma unroll
+    for (int ww = 0; ww < 8; ++ww) {
+      const int ws = c.tile0 + 32 * ww;
+      if (ws >= c.len) break;
+      uint16_t* dst = reinterpret_cast<uint16_t*>(a.v_codes + (c.seq * ncw + ws / kW) * 1024 + 16 * lane + 2 * v);
+      uint32_t w0 = vb[ww] & 0xffffu, w1 = vb[ww] >> 16;
+      if (ws < c.begin) {  // the window holds older tokens: keep their code bits
+        const int old0 = min(max(c.begin - (ws + 4 * g), 0), 4);       // tokens 4g .. 4g+3
+        const int old1 = min(max(c.begin - (ws + 16 + 4 * g), 0), 4);  // tokens 16+4g ..
+        const uint32_t k0 = ((1u << (2 * old0)) - 1u) * 0x0101u;
+        const uint32_t k1 = ((1u << (2 * old1)) - 1u) * 0x0101u;
+        w0 = ((uint32_t)dst[0] & k0) | (w0 & ~k0);
+        w1 = ((uint32_t)dst[4] & k1) | (w1 & ~k1);
+      }
+      dst[0] = (uint16_t)w0;
+      dst[4] = (uint16_t)w1;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+template <bool kKeys, bool kValues>
+__global__ __launch_bounds__(256 * (kKeys + kValues), (kKeys && kValues) ? 1 : 2) void k_codec(CodecArgs a) {
+  __shared__ __attribute__((aligned(16))) float key_lds[kKeys ? 4 * kKeyWaveLds : 4];
+  __shared__ __attribute__((aligned(16))) ValueShared vsh;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform for the compiler
+  if (kValues) {
+    if (threadIdx.x == 0) vsh.count = 0;
+    __syncthreads();  // the only work-group barrier; every wave reaches it
+  }
+  if (kKeys && wave < 4) {
+    key_role(a, wave, key_lds + wave * kKeyWaveLds);
+  } else if (kValues) {
+    value_role(a, wave - (kKeys ? 4 : 0), vsh);
+  }
+}
+
+// Forward rotation fragments: fragment f = ((m 8 + nb) 4 + kk) 2 + part, lane l, element e is
+// part(R_m[16 nb + l % 16][32 kk + 8 (l / 16) + e]), part 0 = fp16(R) (RNE), 1 = fp16 of the residual.
+__global__ __launch_bounds__(256) void k_prepare_fragments(const float* __restrict__ rot, uint4* __restrict__ frag) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;  // (fragment pair, lane)
+  if (idx >= kRotFragments / 2 * 64) return;
+  const int lane = idx & 63, fp = idx >> 6;  // fp = (m 8 + nb) 4 + kk
+  const int kk = fp & 3, nb = (fp >> 2) & 7, m = fp >> 5;
+  const float* src = rot + ((size_t)(m * kD + 16 * nb + (lane & 15))) * kD + 32 * kk + 8 * (lane >> 4);
+  half8 hv, lv;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float f = src[e];
+    hv[e] = (_Float16)f;
+    lv[e] = (_Float16)(f - (float)hv[e]);
+  }
+  frag[(2 * fp) * 64 + lane] = __builtin_bit_cast(uint4, hv);
+  frag[(2 * fp + 1) * 64 + lane] = __builtin_bit_cast(uint4, lv);
+}
+
+hipError_t launch_prepare_fragments(const float* rot, uint4* frag, hipStream_t s) {
+  hipLaunchKernelGGL(k_prepare_fragments, dim3(kRotFragments / 2 * 64 / 256), dim3(256), 0, s, rot, frag);
+  return hipGetLastError();
+}
+
+hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t s) {
+  if (a.ntiles <= 0 || (!keys && !values)) return hipSuccess;
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) cus = n;
+  }
+  // resident work-groups: both roles fill a compute unit (8 waves at up to 256 VGPRs); one role
+  // leaves room for two
+  const int per_cu = (keys && values) ? 1 : 2;
+  const int grid = std::min(a.ntiles, per_cu * cus);
+  if (keys && values) {
+    hipLaunchKernelGGL((k_codec<true, true>), dim3(grid), dim3(512), 0, s, a);
+  } else if (keys) {
+    hipLaunchKernelGGL((k_codec<true, false>), dim3(grid), dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((k_codec<false, true>), dim3(grid), dim3(256), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace okvq

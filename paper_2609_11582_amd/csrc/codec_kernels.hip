@@ -1,11 +1,9 @@
-// Key and value codec kernels, shared by the stateless calls and by append.
+// Exact-mode value codec and the length update of append.
 //
 // A "job" names where token rows come from. Stateless calls quantize tokens [0, len) of a
 // dense block. Append quantizes the tokens [begin, begin + count) that follow a sequence's
-// current length `begin` (device values): keys from the first window that is still open (its
-// older raw rows come from the fp16 stage, so the window is re-quantized as a whole), values
-// token by token (the code bytes shared with older tokens are merged, not overwritten).
-#include "key_quant.hpp"
+// current length `begin` (device values), token by token (the code bytes shared with older
+// tokens are merged, not overwritten). The MFMA-mode values and the keys: codec_fused.hip.
 #include "launch.hpp"
 #include "value_quant.hpp"
 
@@ -19,91 +17,6 @@ __device__ __forceinline__ void job_range(const CodecJob& j, int bz, int b, int&
     begin = 0;
     len = j.lens.lens[bz];
   }
-}
-
-// ------------------------------------------------------------------------------------------------
-// Keys: grid (tiles of 256 tokens from the first open window, H, batches); 4 waves per block,
-// 64 tokens (two windows) per wave.
-// ------------------------------------------------------------------------------------------------
-// Token rows of one wave: older rows of the open window from the stage, then the new rows;
-// zeros beyond the length.
-__device__ __forceinline__ void load_key_rows(const CodecJob& j, size_t seq, int begin, int len, int first, int tok0,
-                                              uint32_t (&raw)[64]) {
-  const int tok = tok0 + lane_id();
-  if (tok < begin) {
-    load_row_f16(j.stage + (seq * kW + (tok - first)) * kD, raw);
-  } else if (tok < len) {
-    load_row_f16(j.src + (seq * j.n_rows + (tok - begin)) * kD, raw);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 64; ++i) raw[i] = 0;
-  }
-}
-
-__global__ __launch_bounds__(256) void k_quantize_keys(CodecJob j, const int8_t* __restrict__ signs,
-                                                       uint8_t* __restrict__ k_codes, uint16_t* __restrict__ k_min,
-                                                       uint16_t* __restrict__ k_step, uint16_t* __restrict__ k_norm) {
-  __shared__ __attribute__((aligned(16))) float lds[4 * kKeyWaveLds];
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform for the compiler
-  const int h = blockIdx.y, bz = blockIdx.z, b = j.b0 + bz;
-  const size_t seq = (size_t)b * j.H + h;
-  // rows from the planned lengths (append: the host's copy), then the device lengths decide
-  int begin = j.begin_dev ? j.lens.lens[bz] : 0;
-  int len = j.begin_dev ? begin + j.cnts.lens[bz] : j.lens.lens[bz];
-  int first = (begin / kW) * kW;  // first token of the first open window
-  int tok0 = first + (blockIdx.x * 4 + wave) * 64;
-  uint32_t raw[64];
-  load_key_rows(j, seq, begin, len, first, tok0, raw);
-  if (j.begin_dev) {
-    const int bd = min(max(j.begin_dev[b], 0), j.cap);
-    const int ld = min(bd + min(max(j.count_dev[b], 0), j.n_rows), j.cap);
-    if (bd != begin || ld != len) {  // stale host lengths: reload from the device ones
-      begin = bd;
-      len = ld;
-      first = (begin / kW) * kW;
-      tok0 = first + (blockIdx.x * 4 + wave) * 64;
-      load_key_rows(j, seq, begin, len, first, tok0, raw);
-    }
-  }
-  if (len <= begin || tok0 >= len) return;  // no block-level barrier is used below
-  uint32_t sw[32];
-  load_sign_words(signs, sw);
-  const int tok = tok0 + lane_id();
-  if (j.stage && tok0 == first) {
-    // The wave holding the old open window rewrites the stage with the raw rows of the new
-    // open window [open, len). Only this wave reads or writes the stage of (b, h).
-    const int open = (len / kW) * kW;
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");  // the stage reads above have completed
-    if (open < len) {
-      const int slot = lane_id() & 31;
-      const int src_tok = open + slot;
-      uint16_t* dst = j.stage + (seq * kW + slot) * kD;
-      if (open < tok0 + 64) {
-        if (tok >= open && tok < len) {
-          uint4* d4 = reinterpret_cast<uint4*>(dst);
-#pragma unroll
-          for (int i = 0; i < 16; ++i) d4[i] = make_uint4(raw[4 * i], raw[4 * i + 1], raw[4 * i + 2], raw[4 * i + 3]);
-        }
-      } else if (lane_id() < 32 && src_tok < len) {
-        const uint4* s4 = reinterpret_cast<const uint4*>(j.src + (seq * j.n_rows + (src_tok - begin)) * kD);
-        uint4* d4 = reinterpret_cast<uint4*>(dst);
-#pragma unroll
-        for (int i = 0; i < 16; ++i) d4[i] = s4[i];
-      }
-    }
-  }
-  KeyWaveOut out{k_codes + seq * j.cap * 32, k_min + seq * (j.cap / kW) * kD, k_step + seq * (j.cap / kW) * kD,
-                 k_norm + seq * j.cap};
-  key_quantize_wave(raw, tok0, len, sw, out, lds + wave * kKeyWaveLds);
-}
-
-hipError_t launch_quantize_keys(const CodecJob& j, int nb, int max_tiles_tokens, const int8_t* signs,
-                                uint8_t* k_codes, uint16_t* k_min, uint16_t* k_step, uint16_t* k_norm,
-                                hipStream_t s) {
-  if (max_tiles_tokens <= 0 || nb <= 0) return hipSuccess;
-  dim3 grid((max_tiles_tokens + 255) / 256, j.H, nb);
-  hipLaunchKernelGGL(k_quantize_keys, grid, dim3(256), 0, s, j, signs, k_codes, k_min, k_step, k_norm);
-  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -185,15 +98,10 @@ __global__ __launch_bounds__(128) void k_quantize_values_exact(CodecJob j, const
   }
 }
 
-hipError_t launch_quantize_values_mfma(const CodecJob& j, int nb, int max_tiles_tokens, const float* rot,
-                                       const Thresholds& th, uint8_t* v_codes, uint16_t* v_norm,
-                                       uint8_t* mod_out, hipStream_t s);
-
-hipError_t launch_quantize_values(const CodecJob& j, int nb, int max_tiles_tokens, const float* rot,
-                                  const Thresholds& th, bool exact, uint8_t* v_codes, uint16_t* v_norm,
-                                  uint8_t* mod_out, hipStream_t s) {
+hipError_t launch_quantize_values_exact(const CodecJob& j, int nb, int max_tiles_tokens, const float* rot,
+                                        const Thresholds& th, uint8_t* v_codes, uint16_t* v_norm, uint8_t* mod_out,
+                                        hipStream_t s) {
   if (max_tiles_tokens <= 0 || nb <= 0) return hipSuccess;
-  if (!exact) return launch_quantize_values_mfma(j, nb, max_tiles_tokens, rot, th, v_codes, v_norm, mod_out, s);
   dim3 grid((max_tiles_tokens + kW - 1) / kW, j.H, nb);
   hipLaunchKernelGGL(k_quantize_values_exact, grid, dim3(128), 0, s, j, rot, th, v_codes, v_norm, mod_out);
   return hipGetLastError();

@@ -36,37 +36,41 @@ __device__ __forceinline__ uint32_t sign_pair_mask(const uint32_t (&sw)[32], int
                  : (((w & 0x00000080u) << 8) | ((w & 0x00008000u) << 16));
 }
 
-// raw: the token's 128 fp16 channels as 64 dwords (channel 2i in the low half of raw[i]).
-// Processes tokens [tok0, tok0 + 64); `len` is the sequence length; `store_end` bounds the slots
-// written (whole windows: padded slots below store_end get code 0 and norm 0).
-__device__ __forceinline__ void key_quantize_wave(const uint32_t (&raw)[64], int tok0, int len,
-                                                  const uint32_t (&sw)[32], KeyWaveOut out,
-                                                  float* lds) {
-  const int lane = lane_id();
-  const int tok = tok0 + lane;
-  const bool valid = tok < len;
-
-  // ---- phase A: norm and rotated direction (lane = token) ----
-  float x[kD];
+// Phase A, first steps: sign flip and fp16 -> fp32 of the token row held by this lane. raw: the
+// row's 128 fp16 channels as 64 dwords (channel 2i in the low half of raw[i]).
+__device__ __forceinline__ void key_unpack(const uint32_t (&raw)[64], const uint32_t (&sw)[32], float (&x)[kD]) {
 #pragma unroll
   for (int i = 0; i < 64; ++i) {
     const uint32_t r = raw[i] ^ sign_pair_mask(sw, 2 * i);
     x[2 * i] = h2f(r & 0xffffu);
     x[2 * i + 1] = h2f(r >> 16);
   }
-  float n32;
-  {
-    float t[64];
+}
+
+// fp16 norm of the row: squares, then the halving tree t <- t[:n/2] + t[n/2:] (sign flips do not
+// change the squares).
+__device__ __forceinline__ uint32_t key_norm(const float (&x)[kD]) {
+  float t[64];
 #pragma unroll
-    for (int c = 0; c < 64; ++c) t[c] = x[c] * x[c] + x[c + 64] * x[c + 64];
+  for (int c = 0; c < 64; ++c) t[c] = x[c] * x[c] + x[c + 64] * x[c + 64];
 #pragma unroll
-    for (int n = 32; n >= 1; n >>= 1) {
+  for (int n = 32; n >= 1; n >>= 1) {
 #pragma unroll
-      for (int c = 0; c < n; ++c) t[c] = t[c] + t[c + n];
-    }
-    n32 = sqrt_rn(t[0]);
+    for (int c = 0; c < n; ++c) t[c] = t[c] + t[c + n];
   }
-  const uint32_t n16 = norm_to_f16(n32);
+  return norm_to_f16(sqrt_rn(t[0]));
+}
+
+// Phase A, second half, and phases B and C for the 64 tokens [tok0, tok0 + 64) of one wave
+// (lane = token). `len` is the sequence length; the slots of every window that holds a valid
+// token are written (padded slots get code 0 and norm 0). between_bc() runs after phase B (the
+// caller's loads for its next rows go out there, when fewer registers are live).
+template <typename F>
+__device__ __forceinline__ void key_quantize_rows(float (&x)[kD], uint32_t n16, int tok0, int len, KeyWaveOut out,
+                                                  float* lds, F&& between_bc) {
+  const int lane = lane_id();
+  const int tok = tok0 + lane;
+  const bool valid = tok < len;
 #pragma unroll
   for (int h = 1; h < kD; h <<= 1) {
 #pragma unroll
@@ -158,7 +162,12 @@ __device__ __forceinline__ void key_quantize_wave(const uint32_t (&raw)[64], int
     wave_lds_sync();
   }
 
-  // ---- phase C: codes (lane = token) ----
+  between_bc();
+
+  // ---- phase C: codes (lane = token). t = fl(fl(z - m16) fl(1 / step16)) is clamped to [0, 3]
+  // and rounded to an integer (ties to even) by adding 2^23, which leaves the code in the low bits
+  // of the sum's bit pattern; eight such patterns shifted by 2j and OR-ed give the channels' 16
+  // code bits in the low half (bits 24 and up only hold the shifted exponent) ----
   const int my_win = lane >> 5;
   const int store_slots = min(max(len - tok0 + 31, 0) / 32 * 32, 64);  // slots of valid windows
   if (lane < store_slots) {
@@ -167,14 +176,23 @@ __device__ __forceinline__ void key_quantize_wave(const uint32_t (&raw)[64], int
     for (int d = 0; d < 8; ++d) dw[d] = 0;
     if (valid) {
       const float4* st = reinterpret_cast<const float4*>(stats + my_win * kD * 2);
+      constexpr float kRound = 8388608.0f;  // 2^23
 #pragma unroll
-      for (int c = 0; c < kD; c += 2) {
-        const float4 s = st[c >> 1];
-        const float t0 = (x[c] - s.x) * s.y;
-        const float t1 = (x[c + 1] - s.z) * s.w;
-        const uint32_t c0 = (uint32_t)fminf(fmaxf(__builtin_rintf(t0), 0.0f), 3.0f);
-        const uint32_t c1 = (uint32_t)fminf(fmaxf(__builtin_rintf(t1), 0.0f), 3.0f);
-        dw[c >> 4] |= (c0 << (c & 14)) | (c1 << (16 + (c & 14)));  // even channels low half, odd high
+      for (int u = 0; u < 8; ++u) {  // word u: channels 16u .. 16u + 15, even ones low, odd ones high
+        uint32_t lo = 0, hi = 0;
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          const int c = 16 * u + 2 * jj;
+          const float4 s = st[c >> 1];
+          const float t0 = (x[c] - s.x) * s.y;
+          const float t1 = (x[c + 1] - s.z) * s.w;
+          const uint32_t q0 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_fmed3f(t0, 0.0f, 3.0f) + kRound);
+          const uint32_t q1 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_fmed3f(t1, 0.0f, 3.0f) + kRound);
+          lo |= q0 << (2 * jj);
+          hi |= q1 << (2 * jj);
+        }
+        dw[u] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);  // low halves of lo and hi
+        __builtin_amdgcn_sched_barrier(0);  // keeps the statistics reads of later words from piling up in registers
       }
     }
     uint4* dst = reinterpret_cast<uint4*>(out.codes + (size_t)tok * 32);

@@ -26,13 +26,39 @@ struct CodecJob {
   int b0, H, cap;
 };
 
-// max_tiles_tokens: tokens to cover from the first open window (host bound for the grid).
-hipError_t launch_quantize_keys(const CodecJob& j, int nb, int max_tiles_tokens, const int8_t* signs,
-                                uint8_t* k_codes, uint16_t* k_min, uint16_t* k_step, uint16_t* k_norm,
-                                hipStream_t s);
-hipError_t launch_quantize_values(const CodecJob& j, int nb, int max_tiles_tokens, const float* rot,
-                                  const Thresholds& th, bool exact, uint8_t* v_codes, uint16_t* v_norm,
-                                  uint8_t* mod_out, hipStream_t s);
+// Exact-mode values (OKVQ_VALUE_EXACT): one work-group per 32-token window.
+hipError_t launch_quantize_values_exact(const CodecJob& j, int nb, int max_tiles_tokens, const float* rot,
+                                        const Thresholds& th, uint8_t* v_codes, uint16_t* v_norm, uint8_t* mod_out,
+                                        hipStream_t s);
+
+// Forward rotation of the MFMA-mode values as ready-made MFMA B operands: 3 modalities x 8 output
+// blocks x 4 k-blocks x (fp16 hi, fp16 lo) fragments of 64 lanes x 16 bytes.
+constexpr int kRotFragments = 3 * 8 * 4 * 2;
+constexpr size_t kRotInverseBytes = 128 * 3 * 128 * 2;          // decode's inverse-rotation table
+constexpr size_t kRotFragmentBytes = (size_t)kRotFragments * 1024;
+
+// Arguments of the fused codec launch (keys, MFMA-mode values, or both) over tiles of 256 tokens.
+struct CodecArgs {
+  CodecJob j;
+  int ntx;     // tiles per sequence (covering the longest span from a first open window)
+  int ntiles;  // ntx * H * sequences in the launch
+  // keys
+  const int8_t* signs;
+  uint8_t* k_codes;
+  uint16_t* k_min;
+  uint16_t* k_step;
+  uint16_t* k_norm;
+  // values
+  const uint16_t* vsrc;  // value rows, laid out like j.src (the key rows)
+  const float* rot;      // fp32 R_m (used when rotfrag is null)
+  const uint4* rotfrag;  // prepared forward fragments, or null
+  Thresholds th;
+  uint8_t* v_codes;
+  uint16_t* v_norm;
+  uint8_t* mod_out;  // append: the cache's modality map (written for KV head 0), else null
+};
+hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t s);
+hipError_t launch_prepare_fragments(const float* rot, uint4* frag, hipStream_t s);
 hipError_t launch_advance_lengths(int32_t* seq_lens, const int32_t* count, int B, hipStream_t s);
 
 struct CacheView {
@@ -48,7 +74,7 @@ struct CacheView {
   int32_t* seq_lens;
   const int8_t* signs;
   const float* rot;
-  const uint16_t* rot16t;  // [128][3][128] fp16 inverse-rotation table
+  const uint16_t* rot16t;  // prepared rotation tables: [128][3][128] fp16 inverse, then forward fragments
 };
 
 struct DecodePlan {

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libokvq.so")
 
 OKVQ_OK = 0
 OKVQ_VALUE_EXACT = 1
+ROTATION_TABLE_BYTES = 294912  # OKVQ_ROTATION_TABLE_BYTES
 BUFFERS = ("k_codes", "v_codes", "k_norm", "v_norm", "k_min", "k_step", "modality", "k_stage", "seq_lens")
 
 
@@ -182,7 +183,7 @@ def okvq_append(cache: "KVCache", lens, k_new, v_new, mod_new, n_new, n_new_dev,
 
 def okvq_prepare_rotation(v_rot, v_rot16, stream=None, check=True) -> int:
     _need(v_rot, 3 * 128 * 128 * 4, "v_rot")
-    _need(v_rot16, 3 * 128 * 128 * 2, "v_rot16")
+    _need(v_rot16, ROTATION_TABLE_BYTES, "v_rot16")
     st = lib().okvq_prepare_rotation(_ptr(v_rot), _ptr(v_rot16), _stream(stream))
     if check:
         _check(st, "okvq_prepare_rotation")
@@ -249,7 +250,7 @@ class KVCache:
         self.dims = make_dims(batch, num_kv_heads, num_q_heads, capacity)
         self.key_signs = key_signs.to(device=device, dtype=torch.int8).contiguous()
         self.v_rot = v_rot.to(device=device, dtype=torch.float32).contiguous()
-        self.v_rot16 = torch.empty((128, 3 * 128), dtype=torch.float16, device=device)
+        self.v_rot16 = torch.empty(ROTATION_TABLE_BYTES // 2, dtype=torch.float16, device=device)
         okvq_prepare_rotation(self.v_rot, self.v_rot16)
         self.buffers = {}
         for i, name in enumerate(BUFFERS):

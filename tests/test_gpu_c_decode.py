@@ -131,7 +131,8 @@ def test_decode_split_count_changes_only_rounding(monkeypatch):
         assert gh.attention_close(o2, out) <= 5e-4
 
 
-def test_prepare_rotation_is_fp16_transpose():
+def test_prepare_rotation_tables():
+    """Inverse table = fp16 transpose; forward fragments = fp16 hi / lo split in the operand layout."""
     import torch
 
     import paper_2609_11582_amd as okvq
@@ -139,13 +140,28 @@ def test_prepare_rotation_is_fp16_transpose():
     rot = gen_rotations(2, 3)
     rot[1, 5, 7] = 1.0 / 3.0            # a value that is not exact in fp16 (rounds to nearest even)
     rot[2, 0, 0] = 2.0 ** -25 * 1.5     # an fp16 subnormal after rounding
-    want = np.ascontiguousarray(rot.transpose(2, 0, 1)).astype(np.float16).reshape(128, 384)
+    want = np.ascontiguousarray(rot.transpose(2, 0, 1)).astype(np.float16).reshape(-1)
+    hi = rot.astype(np.float16)
+    lo = (rot - hi.astype(np.float32)).astype(np.float16)
+    # block ((m 8 + nb) 4 + kk) 2 + part, row l, element e <- R_m[16 nb + l % 16][32 kk + 8 (l / 16) + e]
+    lane = np.arange(64)
+    frag = np.empty((3, 8, 4, 2, 64, 8), np.float16)
+    for m in range(3):
+        for nb in range(8):
+            for kk in range(4):
+                rows = 16 * nb + lane % 16
+                cols = 32 * kk + 8 * (lane // 16)
+                idx = cols[:, None] + np.arange(8)[None, :]
+                frag[m, nb, kk, 0] = hi[m][rows[:, None], idx]
+                frag[m, nb, kk, 1] = lo[m][rows[:, None], idx]
     r_dev = torch.from_numpy(rot).cuda()
-    got = torch.full((128, 384), float("nan"), dtype=torch.float16, device="cuda")
+    got = torch.full((okvq.okvq.ROTATION_TABLE_BYTES // 2,), float("nan"), dtype=torch.float16, device="cuda")
     _announce("prepare_rotation")
     okvq.okvq_prepare_rotation(r_dev, got)
     torch.cuda.synchronize()
-    assert np.array_equal(got.cpu().numpy().view(np.uint16), want.view(np.uint16))
+    g = got.cpu().numpy().view(np.uint16)
+    assert np.array_equal(g[:want.size], want.view(np.uint16))
+    assert np.array_equal(g[want.size:], frag.reshape(-1).view(np.uint16))
 
 
 def test_timed_decode_matches_untimed_and_reports_durations():
