@@ -5,21 +5,23 @@
 // Work unit: a tile of 256 consecutive tokens of one (sequence, KV head), counted from the
 // sequence's first open window. A work-group has one or both of two roles, fixed per wave:
 //  * key waves (4): wave k quantizes tokens [64 k, 64 k + 64) of the tile (key_quant.hpp);
-//  * value waves (4): phase 1 -- wave v takes tokens [64 v, 64 v + 64): fp16 norms, decision
-//    scales and per-modality token masks go to a work-group table; phase 2 -- wave v takes
+//  * value waves (4): phase 1 -- wave v loads the rows of tokens [64 v, 64 v + 64) straight into
+//    the work-group's LDS A tile and puts their fp16 norms, decision scales and per-modality
+//    token masks into a work-group table; phase 2 -- wave v takes
 //    output channels [32 v, 32 v + 32) of all 256 tokens: y = R_m v on the matrix cores with the
 //    wave's slice of R_m held in registers as MFMA B operands (fp16 hi + lo, fp32 accumulation),
 //    one modality at a time, then the codes.
-// Key waves never wait for value waves. The value waves' one dependency (phase 1 -> phase 2) is
-// an arrival counter in LDS, not a work-group barrier, so the key waves' VALU work overlaps the
+// Key waves never wait for value waves. The value waves synchronize twice per tile (tables
+// written -> read -> free again) through an arrival counter in LDS, not a work-group barrier, so the key waves' VALU work overlaps the
 // value waves' loads and MFMAs on the same SIMDs. The grid is persistent: work-group i walks the
 // tiles i, i + gridDim.x, ...; a key wave loads its next tile's rows straight into LDS while it
 // computes the codes of the current one.
 //
 // Value decision: the thresholds are symmetric (-T, 0, T with T = fl(n16 tau_2)), so the code is
-// clamp(floor(y / T) + 2, 0, 3), formed as RNE(y fl(1/T) - 1/2) + 2 by adding 1.5 * 2^23. The
-// result can differ from the comparisons only where y lies within about 2^-21 T of a threshold,
-// far inside the 2^-16 sum_j |R_cj v_j| band that separates MFMA mode from the sequential order.
+// clamp(floor(y fl(1/T)) + 2, 0, 3). At 0 it is exact (the product has the sign of y); at +-T it
+// can differ from the comparisons only where y lies within about 2^-21 T of the threshold, far
+// inside the 2^-16 sum_j |R_cj v_j| band (at least 2^-16 |y|) that separates MFMA mode from the
+// sequential order.
 //
 // MFMA 16x16x32 f16 lane mapping (wave64): lane l holds A[l % 16][8 (l / 16) + e], e = 0..7,
 // B[8 (l / 16) + e][l % 16], and D[4 (l / 16) + i][l % 16], i = 0..3. With rows = tokens and
@@ -185,10 +187,11 @@ __device__ __forceinline__ void key_role(const CodecArgs& a, int kw, float* lds)
 // Value role
 // ------------------------------------------------------------------------------------------------
 struct ValueShared {
-  float itab[2][kTile];       // per tile (double-buffered): fl(1 / T) of each token
-  uint8_t ktab[2][3][64];     // per modality and token quad: 2-bit masks of the quad's coded tokens
-  uint32_t rbm[2][4];         // per phase-1 wave: its row blocks holding each modality (4 bits at 4 m)
-  uint32_t count;             // arrivals of the value waves at the phase-1 -> phase-2 point
+  uint4 atile[16][4][64];     // the tile's value rows as MFMA A operands: [row block][k-block][lane]
+  float itab[kTile];          // fl(1 / T) of each token
+  uint8_t ktab[3][64];        // per modality and token quad: 2-bit masks of the quad's coded tokens
+  uint32_t rbm[4];            // per phase-1 wave: its row blocks holding each modality (4 bits at 4 m)
+  uint32_t count;             // arrivals of the value waves at their synchronization points
 };
 
 // The four value waves wait for each other (LDS counter, monotonically increasing).
@@ -210,13 +213,17 @@ __device__ __forceinline__ void value_wave_sync(uint32_t* count, uint32_t target
 __device__ __forceinline__ void load_rot_slice(const CodecArgs& a, int m, int v, uint4 (&bf)[2][4][2]) {
   const int lane = lane_id();
   if (a.rotfrag) {
-    const uint4* src = a.rotfrag + (size_t)(m * 8 + 2 * v) * 8 * 64 + lane;
+    // uniform fragment base plus the lane's 16-byte offset (scalar base, one offset register)
+    const char* base = reinterpret_cast<const char*>(a.rotfrag) + (size_t)(m * 8 + 2 * v) * 8 * 1024;
+    uint32_t off = 16u * (uint32_t)lane;
+    __asm__ volatile("" : "+v"(off));  // computed here, not hoisted as 16 addresses held across the loop
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-        for (int part = 0; part < 2; ++part) bf[u][kk][part] = src[((u * 4 + kk) * 2 + part) * 64];
+        for (int part = 0; part < 2; ++part)
+          bf[u][kk][part] = *reinterpret_cast<const uint4*>(base + ((u * 4 + kk) * 2 + part) * 1024 + off);
     return;
   }
   const int r = lane & 15, g = lane >> 4;
@@ -238,64 +245,98 @@ __device__ __forceinline__ void load_rot_slice(const CodecArgs& a, int m, int v,
     }
 }
 
-// A operands of row block rb of the tile (16 tokens, the lane's 8-channel slices of its row).
-// Rows outside [begin, len) read a clamped row: their codes are masked.
-__device__ __forceinline__ void load_a_block(const CodecArgs& a, const TileCtx& c, int rb, uint4 (&av)[4]) {
-  const int lane = lane_id(), r = lane & 15, g = lane >> 4;
-  const int tok = c.tile0 + 16 * rb + r;
-  const int row = min(max(tok - c.begin, 0), a.j.n_rows - 1);
-  const uint4* p = reinterpret_cast<const uint4*>(a.vsrc + (c.seq * a.j.n_rows + row) * kD);
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) av[kk] = p[4 * kk + g];
+// floor(x) as an integer in one instruction (v_cvt_flr_i32_f32)
+__device__ __forceinline__ int floor_i32(float x) {
+  int r;
+  __asm__("v_cvt_flr_i32_f32 %0, %1" : "=v"(r) : "v"(x));
+  return r;
 }
 
-// Two code bytes (output blocks 2v, 2v+1) of the lane's four tokens.
+// Two code bytes (output blocks 2v, 2v+1) of the lane's four tokens: code = clamp(floor(y / T) + 2,
+// 0, 3) with y / T taken as y fl(1 / T), whose sign is exactly that of y.
 __device__ __forceinline__ uint32_t value_bytes(floatx4 y0, floatx4 y1, float4 it) {
-  constexpr float kRound = 12582912.0f;  // 1.5 * 2^23
-  constexpr int kBase = 0x4B400000;      // its bit pattern
   const float iv[4] = {it.x, it.y, it.z, it.w};
   uint32_t s0 = 0, s1 = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    int q0 = __builtin_bit_cast(int, __builtin_fmaf(y0[i], iv[i], -0.5f) + kRound);
-    int q1 = __builtin_bit_cast(int, __builtin_fmaf(y1[i], iv[i], -0.5f) + kRound);
-    q0 = min(max(q0, kBase - 2), kBase + 1);  // floor(y / T) in [-2, 1], plus the base pattern
-    q1 = min(max(q1, kBase - 2), kBase + 1);
-    s0 += (uint32_t)q0 << (2 * i);  // the base pattern only reaches bits 22 and up
-    s1 += (uint32_t)q1 << (2 * i);
+    const int f0 = min(max(floor_i32(y0[i] * iv[i]), -2), 1);
+    const int f1 = min(max(floor_i32(y1[i] * iv[i]), -2), 1);
+    s0 += (uint32_t)f0 << (2 * i);
+    s1 += (uint32_t)f1 << (2 * i);
   }
   return ((s0 + 0xAAu) & 0xFFu) | (((s1 + 0xAAu) & 0xFFu) << 8);  // + 2 per token
+}
+
+// The value-code bytes of a finished tile: two bytes per lane and row block, for the windows that
+// hold a token below the length.
+__device__ __forceinline__ void store_value_codes(const CodecArgs& a, const TileCtx& c, int v, const uint32_t (&vb)[8]) {
+  const int lane = lane_id(), g = lane >> 4;
+  const int ncw = a.j.cap / kW;
+#pragma unroll
+  for (int ww = 0; ww < 8; ++ww) {
+    const int ws = c.tile0 + 32 * ww;
+    if (ws >= c.len) break;
+    uint16_t* dst = reinterpret_cast<uint16_t*>(a.v_codes + (c.seq * ncw + ws / kW) * 1024 + 16 * lane + 2 * v);
+    uint32_t w0 = vb[ww] & 0xffffu, w1 = vb[ww] >> 16;
+    if (ws < c.begin) {  // the window holds older tokens: keep their code bits
+      const int old0 = min(max(c.begin - (ws + 4 * g), 0), 4);       // tokens 4g .. 4g+3
+      const int old1 = min(max(c.begin - (ws + 16 + 4 * g), 0), 4);  // tokens 16+4g ..
+      const uint32_t k0 = ((1u << (2 * old0)) - 1u) * 0x0101u;
+      const uint32_t k1 = ((1u << (2 * old1)) - 1u) * 0x0101u;
+      w0 = ((uint32_t)dst[0] & k0) | (w0 & ~k0);
+      w1 = ((uint32_t)dst[4] & k1) | (w1 & ~k1);
+    }
+    dst[0] = (uint16_t)w0;
+    dst[4] = (uint16_t)w1;
+  }
 }
 
 __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShared& sh) {
   const CodecJob& j = a.j;
   const int lane = lane_id(), r = lane & 15, g = lane >> 4;
-  const int ncw = j.cap / kW;
-  uint32_t synced = 0;
+  uint32_t syncs = 0;
+  TileCtx pend{};
+  uint32_t pvb[8];
+  bool has_pend = false;
   for (int t = blockIdx.x; t < a.ntiles; t += gridDim.x) {
     TileCtx c = tile_from_hint(j, a.ntx, t);
     tile_check_device(j, a.ntx, t, c);
     if (c.len <= c.begin || c.tile0 >= c.len) continue;  // uniform over the work-group
-    const int buf = synced & 1;
     const int wend = ((c.len + kW - 1) / kW) * kW;  // end of the last window
 
-    // ---- phase 1: tokens [64 v, 64 v + 64) of the tile ----
+    // ---- phase 1: tokens [64 v, 64 v + 64) of the tile. Their rows go straight to the A tile
+    // (lane l of block (rb, kk) holds channels 32 kk + 8 (l / 16) .. + 7 of row 16 rb + l % 16);
+    // rows outside [begin, len) are not loaded and read as zero here, their codes are masked ----
     const int wtok0 = c.tile0 + 64 * v;
-    uint4 av[4][4];
 #pragma unroll
     for (int rb = 0; rb < 4; ++rb) {
       const int tok = wtok0 + 16 * rb + r;
-      const bool fresh = tok >= c.begin && tok < c.len;
-      const int row = min(max(tok - c.begin, 0), j.n_rows - 1);
-      const uint4* p = reinterpret_cast<const uint4*>(a.vsrc + (c.seq * j.n_rows + row) * kD);
+      if (tok >= c.begin && tok < c.len) {
+        const uint4* p = reinterpret_cast<const uint4*>(a.vsrc + (c.seq * j.n_rows + (tok - c.begin)) * kD);
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) av[rb][kk] = fresh ? p[4 * kk + g] : make_uint4(0, 0, 0, 0);
+        for (int kk = 0; kk < 4; ++kk)
+          __builtin_amdgcn_global_load_lds(p + 4 * kk + g,
+                                           (__attribute__((address_space(3))) void*)&sh.atile[4 * v + rb][kk][0], 16, 0, 0);
+      }
+    }
+    if (has_pend) {  // the previous tile's codes, once this tile's row loads are out
+      store_value_codes(a, pend, v, pvb);
+      has_pend = false;
     }
     const int mytok = wtok0 + lane;
     const bool myfresh = mytok >= c.begin && mytok < c.len;
     const int mymod = myfresh ? (int)j.msrc[(size_t)c.b * j.n_rows + min(max(mytok - c.begin, 0), j.n_rows - 1)] : 3;
     uint4 bf[2][4][2];
     if (a.rotfrag) load_rot_slice(a, 1, v, bf);  // video slice, in flight during phase 1
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    uint4 av[4][4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      const int tok = wtok0 + 16 * rb + r;
+      const bool fresh = tok >= c.begin && tok < c.len;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) av[rb][kk] = fresh ? sh.atile[4 * v + rb][kk][lane] : make_uint4(0, 0, 0, 0);
+    }
 
     // norms by the halving tree: levels 64 and 32 stay in the lane (k-blocks kk, kk + 2 and
     // 0, 1); level 16 pairs lane groups g, g ^ 2 and level 8 pairs g, g ^ 1, each exchange
@@ -338,7 +379,7 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
     }
     const uint32_t n16 = myfresh ? norm_to_f16(sqrt_rn(s[0])) : 0u;
     const int mt = (n16 != 0 && (uint32_t)mymod <= 2u) ? mymod : 3;  // 3: no code
-    sh.itab[buf][64 * v + lane] = (n16 != 0) ? __builtin_amdgcn_rcpf(h2f(n16) * a.th.t2) : 0.0f;
+    sh.itab[64 * v + lane] = (n16 != 0) ? __builtin_amdgcn_rcpf(h2f(n16) * a.th.t2) : 0.0f;
     if (mytok >= c.begin && mytok < wend) a.v_norm[c.seq * j.cap + mytok] = (uint16_t)n16;
     if (myfresh && a.mod_out && c.h == 0) a.mod_out[(size_t)c.b * j.cap + mytok] = (uint8_t)mymod;
     uint32_t rbw = 0;
@@ -351,17 +392,16 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
       if (lane < 16) {  // quad `lane`: tokens 4 lane .. 4 lane + 3 -> bits 2i, 2i + 1
         const uint32_t b4 = (uint32_t)(mb >> (4 * lane)) & 15u;
         const uint32_t spread = (b4 & 1u) | ((b4 & 2u) << 1) | ((b4 & 4u) << 2) | ((b4 & 8u) << 3);
-        sh.ktab[buf][m][16 * v + lane] = (uint8_t)(spread * 3u);
+        sh.ktab[m][16 * v + lane] = (uint8_t)(spread * 3u);
       }
     }
-    if (lane == 0) sh.rbm[buf][v] = rbw;
-    ++synced;
-    value_wave_sync(&sh.count, 4 * synced);
+    if (lane == 0) sh.rbm[v] = rbw;
+    value_wave_sync(&sh.count, 4 * ++syncs);
 
     // ---- phase 2: output channels [32 v, 32 v + 32) of all 256 tokens ----
     uint32_t rbmask[3];
     {
-      const uint4 w4 = *reinterpret_cast<const uint4*>(&sh.rbm[buf][0]);
+      const uint4 w4 = *reinterpret_cast<const uint4*>(&sh.rbm[0]);
       const uint32_t ws[4] = {w4.x, w4.y, w4.z, w4.w};
 #pragma unroll
       for (int m = 0; m < 3; ++m) {
@@ -379,47 +419,34 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
       const uint32_t rbs = rbmask[m];
       if (rbs == 0) continue;
       if (mi > 0 || !a.rotfrag) load_rot_slice(a, m, v, bf);
-      uint4 ab[2][4];  // A operands, by row-block parity: the next present row block is prefetched
-#pragma unroll
-      for (int rb = 0; rb < 16; ++rb) {
-        if (!((rbs >> rb) & 1u)) continue;
-        if (rb == 0 || !((rbs >> (rb - 1)) & 1u)) load_a_block(a, c, rb, ab[rb & 1]);
-        if (rb < 15 && ((rbs >> (rb + 1)) & 1u)) load_a_block(a, c, rb + 1, ab[(rb + 1) & 1]);
+      // one row block: 16 MFMAs (two output blocks x four k-blocks x hi, lo), then the codes
+      auto row_block = [&](int rb) {
         floatx4 y0 = {0.f, 0.f, 0.f, 0.f}, y1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const half8 x = as_half8(ab[rb & 1][kk]);
+          const half8 x = as_half8(sh.atile[rb][kk][lane]);
 #pragma unroll
           for (int part = 0; part < 2; ++part) {
             y0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(x, as_half8(bf[0][kk][part]), y0, 0, 0, 0);
             y1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(x, as_half8(bf[1][kk][part]), y1, 0, 0, 0);
           }
         }
-        const float4 it = *reinterpret_cast<const float4*>(&sh.itab[buf][16 * rb + 4 * g]);
-        const uint32_t keep = (uint32_t)sh.ktab[buf][m][4 * rb + g] * 0x0101u;
+        const float4 it = *reinterpret_cast<const float4*>(&sh.itab[16 * rb + 4 * g]);
+        const uint32_t keep = (uint32_t)sh.ktab[m][4 * rb + g] * 0x0101u;
         vb[rb >> 1] |= (value_bytes(y0, y1, it) & keep) << (16 * (rb & 1));
-      }
-    }
-
-    // ---- store: two bytes per lane and row block, windows that hold a token below the length ----
+      };
 #pragma unroll
-    for (int ww = 0; ww < 8; ++ww) {
-      const int ws = c.tile0 + 32 * ww;
-      if (ws >= c.len) break;
-      uint16_t* dst = reinterpret_cast<uint16_t*>(a.v_codes + (c.seq * ncw + ws / kW) * 1024 + 16 * lane + 2 * v);
-      uint32_t w0 = vb[ww] & 0xffffu, w1 = vb[ww] >> 16;
-      if (ws < c.begin) {  // the window holds older tokens: keep their code bits
-        const int old0 = min(max(c.begin - (ws + 4 * g), 0), 4);       // tokens 4g .. 4g+3
-        const int old1 = min(max(c.begin - (ws + 16 + 4 * g), 0), 4);  // tokens 16+4g ..
-        const uint32_t k0 = ((1u << (2 * old0)) - 1u) * 0x0101u;
-        const uint32_t k1 = ((1u << (2 * old1)) - 1u) * 0x0101u;
-        w0 = ((uint32_t)dst[0] & k0) | (w0 & ~k0);
-        w1 = ((uint32_t)dst[4] & k1) | (w1 & ~k1);
-      }
-      dst[0] = (uint16_t)w0;
-      dst[4] = (uint16_t)w1;
+      for (int rb = 0; rb < 16; ++rb)
+        if ((rbs >> rb) & 1u) row_block(rb);
     }
+    value_wave_sync(&sh.count, 4 * ++syncs);  // the tables are read: the next tile may refill them
+
+    pend = c;  // stored once the next tile's row loads are out
+#pragma unroll
+    for (int ww = 0; ww < 8; ++ww) pvb[ww] = vb[ww];
+    has_pend = true;
   }
+  if (has_pend) store_value_codes(a, pend, v, pvb);
 }
 
 // ------------------------------------------------------------------------------------------------
