@@ -91,16 +91,62 @@ template <int kBanks>
 __device__ __forceinline__ uint32_t take_partner(uint32_t old, uint32_t src) {
   return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)src, kRowRor8, 0xf, kBanks, false);
 }
-// lane l <- lane l ^ 16 and lane l ^ 32 (permutes between rows of 16, no LDS access)
-__device__ __forceinline__ float fxor16(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401f));
+// Pairwise combination of lanes l and l ^ 16 (or l ^ 32) with the VALU row swaps of gfx950
+// (v_permlane16_swap / v_permlane32_swap): swapping a register with a copy of itself leaves the
+// lane's own value in one result and its partner's in the other, so a symmetric op of the two
+// results is the pair's value in both lanes, with no LDS-pipe shuffle. The copy is made opaque:
+// given the same value twice, the compiler folds the two results into one.
+__device__ __forceinline__ uint32_t opaque_copy(uint32_t v) {
+  __asm__ volatile("" : "+v"(v));
+  return v;
 }
-__device__ __forceinline__ float fxor32(float v) { return __shfl_xor(v, 32); }
+__device__ __forceinline__ void swap16(uint32_t v, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(v, opaque_copy(v), false, false);
+  a = r[0];
+  b = r[1];
+}
+__device__ __forceinline__ void swap32(uint32_t v, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(v, opaque_copy(v), false, false);
+  a = r[0];
+  b = r[1];
+}
+__device__ __forceinline__ float sum16(float v) {
+  uint32_t a, b;
+  swap16(__builtin_bit_cast(uint32_t, v), a, b);
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+}
+__device__ __forceinline__ float sum32(float v) {
+  uint32_t a, b;
+  swap32(__builtin_bit_cast(uint32_t, v), a, b);
+  return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
+}
+__device__ __forceinline__ float max16(float v) {
+  uint32_t a, b;
+  swap16(__builtin_bit_cast(uint32_t, v), a, b);
+  return fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
+__device__ __forceinline__ float max32(float v) {
+  uint32_t a, b;
+  swap32(__builtin_bit_cast(uint32_t, v), a, b);
+  return fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
+__device__ __forceinline__ uint32_t pkmax16(uint32_t v);
+__device__ __forceinline__ uint32_t pkmax32(uint32_t v);
 
 typedef unsigned short ushort2v __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pkmax_u16(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(uint32_t,
                             __builtin_elementwise_max(__builtin_bit_cast(ushort2v, a), __builtin_bit_cast(ushort2v, b)));
+}
+__device__ __forceinline__ uint32_t pkmax16(uint32_t v) {
+  uint32_t a, b;
+  swap16(v, a, b);
+  return pkmax_u16(a, b);
+}
+__device__ __forceinline__ uint32_t pkmax32(uint32_t v) {
+  uint32_t a, b;
+  swap32(v, a, b);
+  return pkmax_u16(a, b);
 }
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
@@ -341,23 +387,24 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 #pragma unroll
     for (int k4 = 0; k4 < 4; ++k4) mn4[k4] = *reinterpret_cast<const uint4*>(&mw[kD / 2 + 16 * g + 4 * k4]);
     // ---- bias q'.m of the side window (fp32): 32 channels per lane, then the 4 lane groups ----
-    float bias = 0.0f;
+    float bp[4];  // four independent partial sums (short dependency chains)
 #pragma unroll
     for (int k4 = 0; k4 < 4; ++k4) {
       const float4 qa = *reinterpret_cast<const float4*>(qrow + 8 * k4);
       const float4 qb = *reinterpret_cast<const float4*>(qrow + 8 * k4 + 4);
       const uint4 m = mn4[k4];
-      bias = __builtin_fmaf(qa.x, lo_f16(m.x), bias);
-      bias = __builtin_fmaf(qa.y, hi_f16(m.x), bias);
-      bias = __builtin_fmaf(qa.z, lo_f16(m.y), bias);
-      bias = __builtin_fmaf(qa.w, hi_f16(m.y), bias);
-      bias = __builtin_fmaf(qb.x, lo_f16(m.z), bias);
-      bias = __builtin_fmaf(qb.y, hi_f16(m.z), bias);
-      bias = __builtin_fmaf(qb.z, lo_f16(m.w), bias);
-      bias = __builtin_fmaf(qb.w, hi_f16(m.w), bias);
+      float b = qa.x * lo_f16(m.x);
+      b = __builtin_fmaf(qa.y, hi_f16(m.x), b);
+      b = __builtin_fmaf(qa.z, lo_f16(m.y), b);
+      b = __builtin_fmaf(qa.w, hi_f16(m.y), b);
+      b = __builtin_fmaf(qb.x, lo_f16(m.z), b);
+      b = __builtin_fmaf(qb.y, hi_f16(m.z), b);
+      b = __builtin_fmaf(qb.z, lo_f16(m.w), b);
+      b = __builtin_fmaf(qb.w, hi_f16(m.w), b);
+      bp[k4] = b;
     }
-    bias += fxor16(bias);
-    bias += fxor32(bias);
+    float bias = (bp[0] + bp[1]) + (bp[2] + bp[3]);
+    bias = sum32(sum16(bias));
 
     // ---- scores: two 16-token tiles, each 8 MFMAs block-diagonal over the pair ----
     floatx4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = {0.f, 0.f, 0.f, 0.f};
@@ -395,8 +442,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     }
     float wmax = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
     wmax = fmaxf(wmax, fswap8(wmax));
-    wmax = fmaxf(wmax, fxor16(wmax));
-    wmax = fmaxf(wmax, fxor32(wmax));
+    wmax = max32(max16(wmax));
     // lazy rescale: the reference m_run moves only when the max exceeds it by more than 2^8, so
     // p = 2^(s - m_run - 8) <= 1 and p n_v fits fp16
     if (!started) {  // first pair: nothing accumulated yet, the reference is just set
@@ -510,13 +556,11 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   // ---- combine the waves of the work-group: every wave writes its raw accumulators and its
   // per-head (m, l); the combining threads derive the factors 2^(m_w - M) themselves ----
   l_run += fswap8(l_run);
-  l_run += fxor16(l_run);
-  l_run += fxor32(l_run);
+  l_run = sum32(sum16(l_run));
   {
     uint32_t t = nvm;
     t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_mov_dpp((int)t, kRowRor8, 0xf, 0xf, false));
-    t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_ds_swizzle((int)t, 0x401f));
-    t = pkmax_u16(t, (uint32_t)__shfl_xor((int)t, 32));
+    t = pkmax32(pkmax16(t));
     t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_mov_dpp((int)t, 0x124, 0xf, 0xf, false));  // row_ror:4
     t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_mov_dpp((int)t, 0x122, 0xf, 0xf, false));  // row_ror:2
     t = pkmax_u16(t, (uint32_t)__builtin_amdgcn_mov_dpp((int)t, 0x121, 0xf, 0xf, false));  // row_ror:1
