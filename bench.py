@@ -15,14 +15,22 @@ Reported (one JSON line):
                   >= 1 GB of cache replicas)
   ms_per_step     one step (append prefill + decode), mean over the timed steps
   roofline        the split-K decode kernel (k_decode, the dominant decode launch) against the HBM
-                  peak: algorithmic bytes / its mean duration, timed with HIP events around it;
-                  roofline_append: the whole append call (key, value and length launches)
+                  peak: algorithmic bytes / its mean duration, timed with HIP events bound to its
+                  dispatch; traffic = HBM bytes per launch from the committed rocprofv3 counter
+                  summary while the kernel sources are unchanged, else null;
+                  roofline_append: the whole append call (the fused codec launch and the length
+                  update)
   kernels_us      mean duration of each launch, from the same events
   cpu_baseline    the float64 CPU oracle's decode on the same cache, on this host
 
 --profile-pass runs a short fixed sequence for rocprofv3 counter collection: a 256 MiB device
 copy (calibrates FETCH_SIZE / WRITE_SIZE against a known byte count), 8 decode calls on cold
 cache replicas and 2 prefill appends.
+
+--shape-scan times decode alone at the other workload shapes (batch 16 with ragged lengths up to
+16384, batch 4 x 65536 with 2 KV heads and 16 query heads, 131072 tokens with 32 query heads, and
+batch 32 x 32768), one JSON line each, on caches filled with random codes and metadata (the
+kernel's work does not depend on the values).
 """
 
 from __future__ import annotations
@@ -45,8 +53,8 @@ DECODE_BYTES_PER_WINDOW_HEAD = 2 * 1024 + 2 * 64 + 2 * 256   # codes K, V + norm
 APPEND_BYTES_PER_TOKEN_HEAD = 2 * 256 + 84                   # read K, V fp16; write the packed cache
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
 CALIBRATION_COPY_BYTES = 256 << 20
-KERNEL_SOURCES = ("codec_kernels.hip", "value_mfma.hip", "decode_kernels.hip", "key_quant.hpp", "value_quant.hpp",
-                  "okvq_device.hpp")
+KERNEL_SOURCES = ("codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "key_quant.hpp", "value_quant.hpp",
+                  "okvq_device.hpp", "launch.hpp")
 
 
 def kernel_source_hash() -> str:
@@ -101,6 +109,57 @@ def cpu_baseline(cache_np, q, lens, signs, rot, bytes_per_call, min_seconds=10.0
                        f"tokens), float64, {el:.1f} s")
 
 
+def shape_scan(okvq, torch, np, workload, gen_lengths):
+    """Decode alone at larger shapes: per-call time over cycled cache replicas, effective GB/s."""
+    dev = torch.device("cuda:0")
+    sm = 1 / math.sqrt(128)
+    cases = [("omni7b_b16_ragged16k", None), ("omni3b_b4_64k_stream", None), ("omni30b_128k_48layer", None),
+             ("omni7b_32k", 32)]
+    for name, batch in cases:
+        wl = workload(name)
+        B = batch or wl.batch
+        lens = [int(x) for x in gen_lengths(wl)] if batch is None else [wl.seq_len] * B
+        H, Hq = wl.num_kv_heads, wl.num_q_heads
+        cap = (max(lens) + 31) // 32 * 32
+        dims = okvq.make_dims(B, H, Hq, cap)
+        per_cache = sum(okvq.okvq_buffer_bytes(dims, i) for i in range(9))
+        reps = max(2, min(16, int(math.ceil(1.05e9 / per_cache))))
+        g = torch.Generator(device=dev).manual_seed(7)
+        caches = []
+        for r in range(reps):
+            c = okvq.KVCache(B, H, Hq, cap, torch.ones(128, dtype=torch.int8), torch.eye(128).repeat(3, 1, 1), device=dev)
+            for n, t in c.buffers.items():
+                if n == "seq_lens":
+                    t.copy_(torch.tensor(lens, dtype=torch.int32))
+                elif n == "modality":
+                    t.random_(0, 3, generator=g)
+                elif t.dtype == torch.float16:
+                    t.copy_((torch.rand(t.shape, device=dev, generator=g) * 0.5 + 0.1).half())
+                elif t.dtype == torch.uint8:
+                    t.random_(0, 256, generator=g)
+            caches.append(c)
+        q = torch.randn(B, Hq, 128, device=dev, generator=g).half()
+        ws = okvq.decode_workspace(caches[0].dims, max(lens), device=dev)
+        out = torch.empty(B, Hq, 128, device=dev)
+        for i in range(10):
+            okvq.okvq_decode_attention(caches[i % reps], lens, q, sm, out, ws)
+        torch.cuda.synchronize()
+        n = 100
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(n):
+            okvq.okvq_decode_attention(caches[i % reps], lens, q, sm, out, ws)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / n
+        nbytes = decode_algorithmic_bytes(B, H, Hq, lens)
+        print(json.dumps({"shape_scan": name, "batch": B, "kv_heads": H, "q_heads": Hq, "max_len": max(lens),
+                          "decode_us": round(us, 2), "algorithmic_MB": round(nbytes / 1e6, 2),
+                          "GBps": round(nbytes / us / 1e3, 1), "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBPS, 4)}),
+              flush=True)
+        del caches
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -109,6 +168,7 @@ def main():
     ap.add_argument("--decode-iters", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-pass", action="store_true", help="short fixed sequence for rocprofv3 --pmc runs")
+    ap.add_argument("--shape-scan", action="store_true", help="decode throughput at the other workload shapes")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path shards by KV head "
@@ -119,7 +179,11 @@ def main():
     import torch
 
     import paper_2609_11582_amd as okvq
-    from synth import gen_layer, gen_queries, workload
+    from synth import gen_layer, gen_lengths, gen_queries, workload
+
+    if args.shape_scan:
+        shape_scan(okvq, torch, np, workload, gen_lengths)
+        return
 
     wl = workload(WORKLOAD)
     B, H, Hq, N = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.seq_len
@@ -273,7 +337,8 @@ def main():
         "roofline_append": {"bound": "hbm", "achieved": round(append_gbps, 2), "peak": HBM_PEAK_GBPS,
                             "unit": "GB/s", "frac": round(append_gbps / HBM_PEAK_GBPS, 4),
                             "traffic": None,
-                            "kernel": "okvq_append (key + value codec launches)", "algorithmic_bytes": abytes},
+                            "kernel": "okvq_append (fused key + value codec launch, length update)",
+                            "algorithmic_bytes": abytes},
         "cache_replicas": n_cache,
     }
     if not args.no_cpu_baseline:
