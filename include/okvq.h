@@ -42,7 +42,8 @@
  *   k_step   f16 [B][H][cap/32][128]  per (window, channel) step = (max - min) / 3
  *   modality u8  [B][cap]             0 audio, 1 video, 2 text
  *   k_stage  f16 [B][H][32][128]      raw keys of the open (partial) window, used by append
- *   seq_lens i32 [B]                  current lengths (device copy)
+ *   seq_lens i32 [B + 1]              current lengths (device copy), then one word append uses as
+ *                                      a work-group counter (zero initially; append leaves it zero)
  * Slots of the last window beyond a sequence's length hold code 0 and norm 0.
  * Storage is 84 bytes per token per KV head: 2.625 bits per element, the "FP16 meta." row of
  * the paper's Tab. 3.

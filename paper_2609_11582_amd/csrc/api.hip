@@ -145,7 +145,7 @@ size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
     case OKVQ_BUF_K_STEP: return B * H * (cap / W) * D * 2;
     case OKVQ_BUF_MODALITY: return B * cap;
     case OKVQ_BUF_K_STAGE: return B * H * W * D * 2;
-    case OKVQ_BUF_SEQ_LENS: return B * 4;
+    case OKVQ_BUF_SEQ_LENS: return B * 4 + 4;  // the lengths and append's work-group counter
     default: return 0;
   }
 }
@@ -297,14 +297,18 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
       jv.stage = nullptr;
       st = hip_status(launch_quantize_values_exact(jv, nb, chunk_span, cache->v_rot, a.th, cache->v_codes,
                                                    cache->v_norm, cache->modality, s));
+      if (st != OKVQ_OK) return st;
+      st = hip_status(launch_advance_lengths(cache->seq_lens + b0, n_new_dev + b0, nb, s));
     } else {
       a.vsrc = v_new;
       a.rotfrag = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cache->v_rot16) + kRotInverseBytes);
+      a.seq_lens_out = cache->seq_lens;
+      a.ticket = reinterpret_cast<uint32_t*>(cache->seq_lens + d.batch);
       st = hip_status(launch_codec(a, true, true, s));
     }
     if (st != OKVQ_OK) return st;
   }
-  return hip_status(launch_advance_lengths(cache->seq_lens, n_new_dev, d.batch, s));
+  return OKVQ_OK;
 }
 
 okvq_status okvq_prepare_rotation(const float* v_rot, uint16_t* v_rot16, void* stream) {

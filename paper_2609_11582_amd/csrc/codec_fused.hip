@@ -139,8 +139,7 @@ __device__ __forceinline__ void rewrite_stage(const CodecJob& j, const TileCtx& 
 
 __device__ __forceinline__ void key_role(const CodecArgs& a, int kw, float* lds) {
   const CodecJob& j = a.j;
-  int t = blockIdx.x;
-  if (t >= a.ntiles) return;
+  int t = blockIdx.x;  // < ntiles: the grid is never larger
   // The transpose tile of phase B doubles as the row buffer: the next tile's rows are loaded into
   // it after phase B has read it for the last time.
   uint4* pf = reinterpret_cast<uint4*>(lds);
@@ -463,6 +462,21 @@ __global__ __launch_bounds__(256 * (kKeys + kValues), (kKeys && kValues) ? 1 : 2
     key_role(a, wave, key_lds + wave * kKeyWaveLds);
   } else if (kValues) {
     value_role(a, wave - (kKeys ? 4 : 0), vsh);
+  }
+  if (a.ticket) {
+    // Append: the lengths advance once every work-group has read them. Each work-group counts
+    // itself after all its waves are done; the last one writes the new lengths and clears the
+    // counter for the next launch.
+    __shared__ uint32_t last;
+    __syncthreads();
+    if (threadIdx.x == 0)
+      last = (__hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gridDim.x - 1) ? 1u : 0u;
+    __syncthreads();
+    if (last) {
+      const int nb = a.ntiles / (a.ntx * a.j.H);
+      for (int i = threadIdx.x; i < nb; i += blockDim.x) a.seq_lens_out[a.j.b0 + i] += a.j.count_dev[a.j.b0 + i];
+      if (threadIdx.x == 0) __hip_atomic_store(a.ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 

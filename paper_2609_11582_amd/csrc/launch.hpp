@@ -56,6 +56,10 @@ struct CodecArgs {
   uint8_t* v_codes;
   uint16_t* v_norm;
   uint8_t* mod_out;  // append: the cache's modality map (written for KV head 0), else null
+  // append: the last work-group to finish adds count_dev[b] to seq_lens[b] for the launch's
+  // sequences; `ticket` counts finished work-groups and is returned to zero
+  int32_t* seq_lens_out;
+  uint32_t* ticket;
 };
 hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t s);
 hipError_t launch_prepare_fragments(const float* rot, uint4* frag, hipStream_t s);

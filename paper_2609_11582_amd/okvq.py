@@ -275,4 +275,4 @@ class KVCache:
                     k_norm=b["k_norm"].view(B, H, cap), v_norm=b["v_norm"].view(B, H, cap),
                     k_min=b["k_min"].view(B, H, cap // 32, 128), k_step=b["k_step"].view(B, H, cap // 32, 128),
                     modality=b["modality"].view(B, cap), k_stage=b["k_stage"].view(B, H, 32, 128),
-                    seq_lens=b["seq_lens"])
+                    seq_lens=b["seq_lens"][:B])

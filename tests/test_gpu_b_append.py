@@ -67,6 +67,9 @@ def test_mfma_append_matches_stateless_mfma():
     st = gh.quantize_stateless(lay["k"], lay["v"], lay["modality"], lens, lay["signs"], lay["rot"], 1024, 16)
     for name in ("k_codes", "k_norm", "k_min", "k_step", "v_codes", "v_norm", "modality"):
         assert np.array_equal(got[name], st[name]), name
+    # the fused launch advanced the lengths and returned its work-group counter to zero
+    assert np.array_equal(got["seq_lens"], np.asarray(lens, np.int32))
+    assert int(cache.buffers["seq_lens"][-1].item()) == 0
 
 
 def test_streaming_append_then_decode_each_step():

@@ -112,6 +112,7 @@ def test_omni3b_streaming_full_size():
             _check_decode(out, gh.cache_to_numpy(cache), q, lens, lay, pairs)
     arrays = gh.cache_to_numpy(cache)
     assert np.array_equal(arrays["seq_lens"], np.full(B, cur, np.int32))
+    assert int(cache.buffers["seq_lens"][-1].item()) == 0  # append's work-group counter
     _check_windows(arrays, lay, pairs, np.full(B, cur), per_pair=6, seed=1)
     # the windows either side of the prefill / stream boundary
     for b, h in pairs:
