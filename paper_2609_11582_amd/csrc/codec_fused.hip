@@ -418,25 +418,36 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
       const uint32_t rbs = rbmask[m];
       if (rbs == 0) continue;
       if (mi > 0 || !a.rotfrag) load_rot_slice(a, m, v, bf);
-      // one row block: 16 MFMAs (two output blocks x four k-blocks x hi, lo), then the codes
-      auto row_block = [&](int rb) {
-        floatx4 y0 = {0.f, 0.f, 0.f, 0.f}, y1 = {0.f, 0.f, 0.f, 0.f};
+      // one window (row blocks 2 ww, 2 ww + 1): 32 MFMAs in four independent chains (two row blocks x
+      // two output blocks, each over four k-blocks x hi, lo), then the codes; a row block without
+      // the modality has an all-zero keep mask
+      auto window = [&](int ww) {
+        floatx4 y[2][2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) y[h][0] = y[h][1] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const half8 x = as_half8(sh.atile[rb][kk][lane]);
+          const half8 x0 = as_half8(sh.atile[2 * ww][kk][lane]);
+          const half8 x1 = as_half8(sh.atile[2 * ww + 1][kk][lane]);
 #pragma unroll
           for (int part = 0; part < 2; ++part) {
-            y0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(x, as_half8(bf[0][kk][part]), y0, 0, 0, 0);
-            y1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(x, as_half8(bf[1][kk][part]), y1, 0, 0, 0);
+            y[0][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(x0, as_half8(bf[0][kk][part]), y[0][0], 0, 0, 0);
+            y[0][1] = __builtin_amdgcn_mfma_f32_16x16x32_f16(x0, as_half8(bf[1][kk][part]), y[0][1], 0, 0, 0);
+            y[1][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(x1, as_half8(bf[0][kk][part]), y[1][0], 0, 0, 0);
+            y[1][1] = __builtin_amdgcn_mfma_f32_16x16x32_f16(x1, as_half8(bf[1][kk][part]), y[1][1], 0, 0, 0);
           }
         }
-        const float4 it = *reinterpret_cast<const float4*>(&sh.itab[16 * rb + 4 * g]);
-        const uint32_t keep = (uint32_t)sh.ktab[m][4 * rb + g] * 0x0101u;
-        vb[rb >> 1] |= (value_bytes(y0, y1, it) & keep) << (16 * (rb & 1));
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int rb = 2 * ww + h;
+          const float4 it = *reinterpret_cast<const float4*>(&sh.itab[16 * rb + 4 * g]);
+          const uint32_t keep = (uint32_t)sh.ktab[m][4 * rb + g] * 0x0101u;
+          vb[ww] |= (value_bytes(y[h][0], y[h][1], it) & keep) << (16 * h);
+        }
       };
 #pragma unroll
-      for (int rb = 0; rb < 16; ++rb)
-        if ((rbs >> rb) & 1u) row_block(rb);
+      for (int ww = 0; ww < 8; ++ww)
+        if ((rbs >> (2 * ww)) & 3u) window(ww);
     }
     value_wave_sync(&sh.count, 4 * ++syncs);  // the tables are read: the next tile may refill them
 

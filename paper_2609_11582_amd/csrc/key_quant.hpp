@@ -192,7 +192,6 @@ __device__ __forceinline__ void key_quantize_rows(float (&x)[kD], uint32_t n16, 
           hi |= q1 << (2 * jj);
         }
         dw[u] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);  // low halves of lo and hi
-        __builtin_amdgcn_sched_barrier(0);  // keeps the statistics reads of later words from piling up in registers
       }
     }
     uint4* dst = reinterpret_cast<uint4*>(out.codes + (size_t)tok * 32);
