@@ -130,7 +130,7 @@ def shape_scan(okvq, torch, np, workload, gen_lengths):
             c = okvq.KVCache(B, H, Hq, cap, torch.ones(128, dtype=torch.int8), torch.eye(128).repeat(3, 1, 1), device=dev)
             for n, t in c.buffers.items():
                 if n == "seq_lens":
-                    t.copy_(torch.tensor(lens, dtype=torch.int32))
+                    t[:B].copy_(torch.tensor(lens, dtype=torch.int32))
                 elif n == "modality":
                     t.random_(0, 3, generator=g)
                 elif t.dtype == torch.float16:
