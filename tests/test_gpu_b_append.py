@@ -107,3 +107,37 @@ def test_streaming_append_then_decode_each_step():
                            1 / math.sqrt(128))
         assert gh.attention_close(out, ref) <= 2e-3
     del plan
+
+
+def test_append_and_decode_beyond_256_sequences():
+    """300 sequences: append and decode split the batch into several launches (256 sequences each);
+    every sequence matches the one-shot oracle quantization and the decode oracle."""
+    import math
+
+    import gpu_helpers as gh
+    from oracle.cache import decode_layer
+    from synth import gen_queries
+    rng = np.random.default_rng(5)
+    lens = rng.integers(1, 80, 300).tolist()
+    wl = workload("tiny_1k")
+    lay = gen_layer(wl, 3, lengths=np.asarray(lens, np.int32), n_tokens=max(lens))
+    cache = gh.new_cache(300, 1, 4, 96, lay["signs"], lay["rot"])
+    _announce("append B=300 (two launches)")
+    gh.append_chunks(cache, lay["k"], lay["v"], lay["modality"], lens, [[40] * 300, [100] * 300])
+    got = gh.cache_to_numpy(cache)
+    assert np.array_equal(got["seq_lens"], np.asarray(lens, np.int32))
+    assert int(cache.buffers["seq_lens"][-1].item()) == 0
+    st = gh.quantize_stateless(lay["k"], lay["v"], lay["modality"], lens, lay["signs"], lay["rot"], 96, 4)
+    for name in ("k_codes", "k_norm", "k_min", "k_step", "v_codes", "v_norm", "modality"):
+        assert np.array_equal(got[name], st[name]), name
+    ref = quantize_layer(lay["k"], lay["v"], lay["modality"], np.asarray(lens), lay["signs"], lay["rot"], 96)
+    for name in ("k_codes", "k_norm", "k_min", "k_step"):
+        a, b = got[name], ref[name]
+        if a.dtype == np.float16:
+            a, b = a.view(np.uint16), b.view(np.uint16)
+        assert np.array_equal(a, b), name
+    q = gen_queries(wl.wid, 3, 300, 4)
+    out = gh.decode(cache, q, lens)
+    dec = decode_layer(got, q, np.asarray(lens), lay["signs"], lay["rot"], 1 / math.sqrt(128),
+                       heads={(b, 0) for b in (0, 1, 255, 256, 299)})
+    assert gh.attention_close(out, dec) <= 2e-3
