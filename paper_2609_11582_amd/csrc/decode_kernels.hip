@@ -239,7 +239,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   __shared__ __attribute__((aligned(16))) uint2 vlut[256];
   __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];                     // q' (fp32, padded rows)
   __shared__ float amax_w[kDecWaves];
-  __shared__ __attribute__((aligned(16))) uint32_t meta[kDecWaves][2][2][2][kD / 2];  // [wave][buffer][side][step, min]
+  __shared__ __attribute__((aligned(16))) uint32_t meta[kDecWaves][2][2][kD / 2];  // [wave][side][step, min]
   __shared__ __attribute__((aligned(16))) uint32_t zeros[kD / 2];                  // steps of "no window"
   __shared__ __attribute__((aligned(16))) float wst[2][8][kDecWaves];              // [m, l][head][wave]
   __shared__ uint32_t wmask[kDecWaves];
@@ -367,34 +367,22 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   bool started = false;  // a pair has been processed (wave-uniform)
   uint32_t seen = 0;  // modalities seen by this wave
   uint32_t nvm = 0;   // largest value norm seen by this lane (two fp16 halves, non-negative)
+  uint32_t* mw = &meta[wave][side][0][0];
   const float* qrow = &qs[hd][32 * g];
+  // steps read for the two windows' k-blocks: the lane's own window, zeros for the other one
+  const uint32_t* stA = side ? zeros : &meta[wave][0][0][0];
+  const uint32_t* stB = side ? &meta[wave][1][0][0] : zeros;
   float* tacc = &wacc[wave][col][16 + 4 * g];  // text rows of this lane (g < 2), channel 16 nb + col
 
-  // What the PV stage of a pair needs from its first stage.
-  struct PvState {
-    uint4 va, vb;     // value codes of windows A, B
-    uint32_t pv[4];   // p n_v, fp16 pairs: tokens (4g, 4g+1), (4g+2, 4g+3), (16+4g, ..), (16+4g+2, ..)
-    uint32_t sel[4];  // v_perm selectors of the same token pairs' modalities
-    bool has_t;       // text tokens in the pair (wave-uniform)
-  };
+  auto process = [&](const PairLoad& cur, int wA) {
+    const bool hasB = wA + 1 < w_end;
+    const bool full = hasB && kW * (wA + 2) <= len;  // every token of both windows is valid
+    const int wS = wA + side;
 
-  // The side window's step and min through wave-private LDS (buffer mb), natural channel order.
-  auto stage_meta = [&](const PairLoad& cur, int mb) {
-    uint32_t* mw = &meta[wave][mb][side][0][0];
+    // ---- side window metadata through wave-private LDS, natural channel order ----
     *reinterpret_cast<uint2*>(&mw[16 * g + 2 * c7]) = cur.stp;
     *reinterpret_cast<uint2*>(&mw[kD / 2 + 16 * g + 2 * c7]) = cur.mnp;
-  };
-
-  // First stage of a pair (metadata staged in buffer mb and synchronized): bias, scores, online
-  // softmax, p n_v and the modality selectors. Branch-free, so that the compiler can interleave it
-  // with the previous pair's PV stage. The softmax reference moves lazily (only when the max
-  // exceeds it by more than 2^8, so p = 2^(s - m_run - 8) <= 1 and p n_v fits fp16); `alpha`
-  // is the factor the accumulators must be scaled by before this pair's PV, `resc` whether any
-  // lane needs it (wave-uniform).
-  auto stage1 = [&](const PairLoad& cur, int wA, int mb, PvState& st, float& alpha, bool& resc) {
-    const bool hasB = wA + 1 < w_end;
-    const int wS = wA + side;
-    const uint32_t* mw = &meta[wave][mb][side][0][0];
+    wave_lds_sync();
     uint4 mn4[4];
 #pragma unroll
     for (int k4 = 0; k4 < 4; ++k4) mn4[k4] = *reinterpret_cast<const uint4*>(&mw[kD / 2 + 16 * g + 4 * k4]);
@@ -418,10 +406,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     float bias = (bp[0] + bp[1]) + (bp[2] + bp[3]);
     bias = sum32(sum16(bias));
 
-    // ---- scores: two 16-token tiles, each 8 MFMAs block-diagonal over the pair; the other
-    // window's k-blocks read zero steps ----
-    const uint32_t* stA = side ? zeros : &meta[wave][mb][0][0][0];
-    const uint32_t* stB = side ? &meta[wave][mb][1][0][0] : zeros;
+    // ---- scores: two 16-token tiles, each 8 MFMAs block-diagonal over the pair ----
     floatx4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
@@ -431,36 +416,60 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
       sc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka0 : cur.kb0, kk), bop, sc0, 0, 0, 0);
       sc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka1 : cur.kb1, kk), bop, sc1, 0, 0, 0);
     }
+    wave_lds_sync();  // metadata reads done before the next pair overwrites it
 
-    // ---- online softmax (base 2) over the pair's 64 tokens; tokens beyond the length (or of a
-    // missing window B) get -inf and modality 3 (invalid) ----
+    // ---- online softmax (base 2) over the pair's 64 tokens ----
     const uint32_t nkw[4] = {cur.nk0.x, cur.nk0.y, cur.nk1.x, cur.nk1.y};
     const uint32_t nvw[4] = {cur.nv0.x, cur.nv0.y, cur.nv1.x, cur.nv1.y};
     uint32_t md[2] = {cur.md0, cur.md1};
-    const bool side_ok = !side || hasB;
     float s[8];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int nvalid = side_ok ? min(max(len - (kW * wS + 16 * t + 4 * g), 0), 4) : 0;
+    for (int e = 0; e < 8; ++e) {  // e = 4 t + i: token 16 t + 4 g + i of the side window
+      const float raw = (e >> 2) ? sc1[e & 3] : sc0[e & 3];
+      const float nkf = (e & 1) ? hi_f16(nkw[e >> 1]) : lo_f16(nkw[e >> 1]);
+      s[e] = nkf * __builtin_fmaf(raw, kscale, bias);
+    }
+    if (!full) {  // partial pair: tokens beyond the length (or a missing window B) do not count
+      const bool side_ok = !side || hasB;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {  // token 16 t + 4 g + i of the side window
-        const int e = 4 * t + i;
-        const float raw = t ? sc1[i] : sc0[i];
-        const float nkf = (e & 1) ? hi_f16(nkw[e >> 1]) : lo_f16(nkw[e >> 1]);
-        const float v = nkf * __builtin_fmaf(raw, kscale, bias);
-        s[e] = (i < nvalid) ? v : -__builtin_inff();
+      for (int t = 0; t < 2; ++t) {
+        const int nvalid = side_ok ? min(max(len - (kW * wS + 16 * t + 4 * g), 0), 4) : 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (i >= nvalid) s[4 * t + i] = -__builtin_inff();
+        md[t] |= (nvalid >= 4) ? 0u : (0x03030303u << (8 * nvalid));  // modality 3: invalid
       }
-      md[t] |= (nvalid >= 4) ? 0u : (0x03030303u << (8 * nvalid));
     }
     float wmax = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
     wmax = fmaxf(wmax, fswap8(wmax));
     wmax = max32(max16(wmax));
-    resc = started && __any(wmax > m_run + kLazy);
-    const float m_new = !started ? wmax : (resc ? fmaxf(m_run, wmax) : m_run);
-    alpha = started ? fast_exp2(m_run - m_new) : 1.0f;  // exactly 1 where the reference stays
-    l_run *= alpha;
-    m_run = m_new;
-    started = true;
+    // lazy rescale: the reference m_run moves only when the max exceeds it by more than 2^8, so
+    // p = 2^(s - m_run - 8) <= 1 and p n_v fits fp16
+    if (!started) {  // first pair: nothing accumulated yet, the reference is just set
+      m_run = wmax;
+      started = true;
+    } else if (__any(wmax > m_run + kLazy)) {
+      const float m_new = fmaxf(m_run, wmax);
+      const float alpha = fast_exp2(m_run - m_new);
+      l_run *= alpha;
+      float arow[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) arow[i] = __shfl(alpha, (4 * g + i) & 7);
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc1[nb][i] *= arow[i];
+      }
+      if (g < 2) {
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) {
+          float4* t = reinterpret_cast<float4*>(tacc + 16 * nb * kAccPitch);
+          const float4 v = *t;
+          *t = make_float4(v.x * arow[0], v.y * arow[1], v.z * arow[2], v.w * arow[3]);
+        }
+      }
+      m_run = m_new;
+    }
     const float mref = m_run + kLazy;
     float pr[8];
 #pragma unroll
@@ -468,125 +477,70 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
       pr[e] = fast_exp2(s[e] - mref);
       l_run += pr[e];
     }
+    uint32_t pv[4];  // p n_v (fp16 pairs), tokens (4g, 4g+1), (4g+2, 4g+3), (16+4g, ..), (16+4g+2, ..)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) st.pv[q] = pk_mul(pack_f16(pr[2 * q], pr[2 * q + 1]), nvw[q]);
+    for (int q = 0; q < 4; ++q) pv[q] = pk_mul(pack_f16(pr[2 * q], pr[2 * q + 1]), nvw[q]);
     nvm = pkmax_u16(nvm, pkmax_u16(pkmax_u16(nvw[0], nvw[1]), pkmax_u16(nvw[2], nvw[3])));
 
     // ---- modalities present (wave-uniform) and the v_perm selectors of the token pairs ----
     uint32_t pres = __builtin_amdgcn_perm(kTabBits, kTabBits, md[0]) | __builtin_amdgcn_perm(kTabBits, kTabBits, md[1]);
     pres |= pres >> 16;
     pres |= pres >> 8;
-    const bool has_a = __any(pres & 1u), has_v = __any(pres & 2u);
-    st.has_t = __any(pres & 4u);
-    seen |= (has_a ? 1u : 0u) | (has_v ? 2u : 0u) | (st.has_t ? 4u : 0u);  // all wave-uniform
+    const bool has_a = __any(pres & 1u), has_v = __any(pres & 2u), has_t = __any(pres & 4u);
+    seen |= (has_a ? 1u : 0u) | (has_v ? 2u : 0u) | (has_t ? 4u : 0u);  // all wave-uniform
+    uint32_t sel[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      st.sel[q] = __builtin_amdgcn_perm(md[q >> 1], md[q >> 1], (q & 1) ? 0x03030202u : 0x01010000u);
-    st.va = cur.va;
-    st.vb = cur.vb;
-  };
+    for (int q = 0; q < 4; ++q) sel[q] = __builtin_amdgcn_perm(md[q >> 1], md[q >> 1], (q & 1) ? 0x03030202u : 0x01010000u);
 
-  // PV of set 1 (rows 0-7 audio heads from the side-0 lanes, rows 8-15 video heads from the side-1
-  // lanes): one MFMA per window and 16-channel block, for every pair (a branch around it would give
-  // the accumulators two register homes).
-  auto stage2 = [&](const PvState& st) {
-    uint32_t opA[4], opB[4];
+    // ---- values: one PV MFMA per window and 16-channel block. Set 1 (rows 0-7 audio heads from
+    // the side-0 lanes, rows 8-15 video heads from the side-1 lanes) runs for every pair: a branch
+    // around it would give the accumulators two register homes ----
+    {
+      uint32_t opA[4], opB[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t own = st.pv[q] & __builtin_amdgcn_perm(tab_own, tab_own, st.sel[q]);
-      const uint32_t oth = st.pv[q] & __builtin_amdgcn_perm(tab_oth, tab_oth, st.sel[q]);
-      opA[q] = take_partner<0xc>(own, oth);  // window A tokens: video rows from the side-0 partner
-      opB[q] = take_partner<0x3>(own, oth);  // window B tokens: audio rows from the side-1 partner
-    }
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb) {
-      acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, st.va, nb), acc1[nb], 0, 0, 0);
-      acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, st.vb, nb), acc1[nb], 0, 0, 0);
-    }
-  };
-
-  // Set 2 (text; rows 0-7 text heads from the side-0 lanes, rows 8-15 zero) into the wave's LDS
-  // slot; only pairs that hold text tokens.
-  auto stage2_text = [&](const PvState& st) {
-    uint32_t opA[4], opB[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      opA[q] = st.pv[q] & __builtin_amdgcn_perm(tab_txt0, tab_txt0, st.sel[q]);
-      const uint32_t txt = st.pv[q] & __builtin_amdgcn_perm(kTabText, kTabText, st.sel[q]);
-      opB[q] = take_partner<0x3>(0u, txt);
-    }
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb) {
-      floatx4 t = {0.f, 0.f, 0.f, 0.f};
-      t = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, st.va, nb), t, 0, 0, 0);
-      t = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, st.vb, nb), t, 0, 0, 0);
-      if (g < 2) {
-        float4* ta = reinterpret_cast<float4*>(tacc + 16 * nb * kAccPitch);
-        const float4 v = *ta;
-        *ta = make_float4(v.x + t[0], v.y + t[1], v.z + t[2], v.w + t[3]);
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t own = pv[q] & __builtin_amdgcn_perm(tab_own, tab_own, sel[q]);
+        const uint32_t oth = pv[q] & __builtin_amdgcn_perm(tab_oth, tab_oth, sel[q]);
+        opA[q] = take_partner<0xc>(own, oth);  // window A tokens: video rows from the side-0 partner
+        opB[q] = take_partner<0x3>(own, oth);  // window B tokens: audio rows from the side-1 partner
       }
-    }
-  };
-
-  // Scale the accumulators (registers and the LDS text rows) by the lanes' alpha, per head row.
-  auto rescale = [&](float alpha) {
-    float arow[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) arow[i] = __shfl(alpha, (4 * g + i) & 7);
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) acc1[nb][i] *= arow[i];
-    }
-    if (g < 2) {
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
-        float4* t = reinterpret_cast<float4*>(tacc + 16 * nb * kAccPitch);
-        const float4 v = *t;
-        *t = make_float4(v.x * arow[0], v.y * arow[1], v.z * arow[2], v.w * arow[3]);
+        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, cur.va, nb), acc1[nb], 0, 0, 0);
+        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, cur.vb, nb), acc1[nb], 0, 0, 0);
+      }
+    }
+    if (has_t) {  // set 2: rows 0-7 text heads (side-0 lanes), rows 8-15 zero
+      uint32_t opA[4], opB[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        opA[q] = pv[q] & __builtin_amdgcn_perm(tab_txt0, tab_txt0, sel[q]);
+        const uint32_t txt = pv[q] & __builtin_amdgcn_perm(kTabText, kTabText, sel[q]);
+        opB[q] = take_partner<0x3>(0u, txt);
+      }
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        floatx4 t = {0.f, 0.f, 0.f, 0.f};
+        t = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, cur.va, nb), t, 0, 0, 0);
+        t = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, cur.vb, nb), t, 0, 0, 0);
+        if (g < 2) {
+          float4* ta = reinterpret_cast<float4*>(tacc + 16 * nb * kAccPitch);
+          const float4 v = *ta;
+          *ta = make_float4(v.x + t[0], v.y + t[1], v.z + t[2], v.w + t[3]);
+        }
       }
     }
   };
 
-  // ---- the wave's window pairs wA0 + 16 k, software-pipelined: the PV stage of pair k runs with
-  // the first stage of pair k + 1, whose loads went out a pair earlier. Buffers alternate (A for
-  // even k, B for odd k) so that nothing is copied between registers ----
-  if (wA0 < w_end) {
-    PvState psA, psB;
-    float alpha;
-    bool resc;
-    constexpr int kStride = 2 * kDecWaves;
-    int wA = wA0;
-    if (wA + kStride < w_end) bufB = load_pair(sp, wA + kStride, wA + kStride + 1 < w_end, lane);
-    stage_meta(bufA, 0);
-    wave_lds_sync();
-    stage1(bufA, wA, 0, psA, alpha, resc);  // the first pair sets the reference: no rescale
-    for (;;) {
-      // even step: pair wA in psA, pair wA + kStride (if any) loaded in bufB
-      int wN = wA + kStride;
-      if (wN + kStride < w_end) bufA = load_pair(sp, wN + kStride, wN + kStride + 1 < w_end, lane);
-      if (wN < w_end) {
-        stage_meta(bufB, 1);
-        wave_lds_sync();
-        stage1(bufB, wN, 1, psB, alpha, resc);
-      }
-      stage2(psA);
-      if (psA.has_t) stage2_text(psA);
-      if (wN >= w_end) break;
-      if (resc) rescale(alpha);
-      // odd step: pair wN in psB, pair wN + kStride (if any) loaded in bufA
-      wA = wN + kStride;
-      if (wA + kStride < w_end) bufB = load_pair(sp, wA + kStride, wA + kStride + 1 < w_end, lane);
-      if (wA < w_end) {
-        stage_meta(bufA, 0);
-        wave_lds_sync();
-        stage1(bufA, wA, 0, psA, alpha, resc);
-      }
-      stage2(psB);
-      if (psB.has_t) stage2_text(psB);
-      if (wA >= w_end) break;
-      if (resc) rescale(alpha);
-    }
+  // ---- window pairs, double-buffered loads without register copies ----
+  for (int wA = wA0; wA < w_end; wA += 4 * kDecWaves) {
+    const int wA2 = wA + 2 * kDecWaves;
+    if (wA2 < w_end) bufB = load_pair(sp, wA2, wA2 + 1 < w_end, lane);
+    process(bufA, wA);
+    if (wA2 >= w_end) break;
+    const int wA3 = wA2 + 2 * kDecWaves;
+    if (wA3 < w_end) bufA = load_pair(sp, wA3, wA3 + 1 < w_end, lane);
+    process(bufB, wA2);
   }
 
   // ---- epilogue. This wave's slice of the inverse-rotation table (output channels 16 wave ..
