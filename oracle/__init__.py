@@ -22,6 +22,7 @@ Modules
 codebook   Lloyd-Max codebook for N(0, 1/d) (Eq. 3)
 hadamard   Sylvester Hadamard matrix, randomized H, fp32 butterfly order (Eq. 2)
 keys       key codec: norm split, Hadamard, per-window min/step, codes (Eq. 2, Eq. 4)
+mxfp4      MXFP4 (E2M1 elements, E8M0 block scales) storage of the key window metadata
 values     value codec with per-modality rotation R_m (Eq. 6, Eq. 3)
 layout     packed byte layouts and the bits-per-element accounting (Tab. 3)
 attention  decode attention over the quantized cache, two formulations (Eq. 1)

@@ -13,13 +13,18 @@ from __future__ import annotations
 import numpy as np
 
 from .attention import decode_bruteforce, decode_dense, decode_rotated
-from .keys import quantize_keys_fmt
-from .layout import WINDOW, pack_keys, pack_values, unpack_keys, unpack_values
+from .keys import quantize_keys_fmt, quantize_keys_mx_fmt
+from .layout import MX_RECORD, WINDOW, pack_keys, pack_mx_meta, pack_values, unpack_keys, unpack_mx_meta, unpack_values
+from .mxfp4 import mx_dequantize
 from .values import quantize_values_fmt
 
 
-def quantize_layer(k, v, modality, lens, signs, rot, capacity=None):
-    """Dict of packed buffers (numpy) for k, v [B][H][N][d] fp16, modality [B][N], lens [B]."""
+def quantize_layer(k, v, modality, lens, signs, rot, capacity=None, key_meta="fp16"):
+    """Dict of packed buffers (numpy) for k, v [B][H][N][d] fp16, modality [B][N], lens [B].
+
+    key_meta "fp16": fp16 window minimum and step (k_min, k_step); "mxfp4": one 136-byte MXFP4
+    record per window (k_mx, layout in ``oracle.layout``).
+    """
     B, H, N, D = k.shape
     cap = int(capacity or -(-N // WINDOW) * WINDOW)
     nw = cap // WINDOW
@@ -28,20 +33,31 @@ def quantize_layer(k, v, modality, lens, signs, rot, capacity=None):
         v_codes=np.zeros((B, H, nw, 1024), np.uint8),
         k_norm=np.zeros((B, H, cap), np.float16),
         v_norm=np.zeros((B, H, cap), np.float16),
-        k_min=np.zeros((B, H, nw, D), np.float16),
-        k_step=np.zeros((B, H, nw, D), np.float16),
         modality=np.zeros((B, cap), np.uint8),
     )
+    if key_meta == "fp16":
+        out["k_min"] = np.zeros((B, H, nw, D), np.float16)
+        out["k_step"] = np.zeros((B, H, nw, D), np.float16)
+    elif key_meta == "mxfp4":
+        out["k_mx"] = np.zeros((B, H, nw, MX_RECORD), np.uint8)
+    else:
+        raise ValueError(key_meta)
     for b in range(B):
         L = int(lens[b])
         out["modality"][b, :L] = modality[b, :L]
         for h in range(H):
-            kq = quantize_keys_fmt(k[b, h], L, signs)
+            if key_meta == "fp16":
+                kq = quantize_keys_fmt(k[b, h], L, signs)
+                nwl = kq["codes"].shape[0] // WINDOW
+                out["k_min"][b, h, :nwl] = kq["m16"]
+                out["k_step"][b, h, :nwl] = kq["step16"]
+            else:
+                kq = quantize_keys_mx_fmt(k[b, h], L, signs)
+                nwl = kq["codes"].shape[0] // WINDOW
+                out["k_mx"][b, h, :nwl] = pack_mx_meta(kq["m_codes"], kq["s_codes"], kq["m_scale"], kq["s_scale"])
             npad = kq["codes"].shape[0]
             out["k_codes"][b, h, :npad] = pack_keys(kq["codes"])
             out["k_norm"][b, h, :npad] = kq["n16"]
-            out["k_min"][b, h, :npad // WINDOW] = kq["m16"]
-            out["k_step"][b, h, :npad // WINDOW] = kq["step16"]
             vq = quantize_values_fmt(v[b, h], modality[b], rot, L)
             vcodes = np.zeros((npad, D), np.uint8)
             vcodes[:L] = vq["codes"]
@@ -50,11 +66,20 @@ def quantize_layer(k, v, modality, lens, signs, rot, capacity=None):
     return out
 
 
+def key_metadata(cache, b, h):
+    """(minimum, step) [n_win][d] of one sequence and KV head: the fp16 fields, or the MXFP4
+    records dequantized (float32, exact)."""
+    if "k_mx" in cache:
+        mc, sc, ms, ss = unpack_mx_meta(cache["k_mx"][b, h])
+        return mx_dequantize(mc, ms).astype(np.float32), mx_dequantize(sc, ss).astype(np.float32)
+    return cache["k_min"][b, h], cache["k_step"][b, h]
+
+
 def unpacked_fields(cache, b, h):
-    """(kc, m16, st16, nk, vc, nv, modality) for one sequence and KV head of a packed cache."""
-    return (unpack_keys(cache["k_codes"][b, h]), cache["k_min"][b, h], cache["k_step"][b, h],
-            cache["k_norm"][b, h], unpack_values(cache["v_codes"][b, h]), cache["v_norm"][b, h],
-            cache["modality"][b])
+    """(kc, m, st, nk, vc, nv, modality) for one sequence and KV head of a packed cache."""
+    m, st = key_metadata(cache, b, h)
+    return (unpack_keys(cache["k_codes"][b, h]), m, st, cache["k_norm"][b, h],
+            unpack_values(cache["v_codes"][b, h]), cache["v_norm"][b, h], cache["modality"][b])
 
 
 def decode_layer(cache, q16, lens, signs, rot, sm_scale, rotated=True, heads=None):

@@ -90,7 +90,8 @@ def window_stats_fmt(z_valid: np.ndarray):
 
 
 def key_codes_fmt(z: np.ndarray, m16: np.ndarray, step16: np.ndarray) -> np.ndarray:
-    """uint8 codes 0..3 for fp32 z [n][d] against one window's fp16 (m16, step16) [d]."""
+    """uint8 codes 0..3 for fp32 z [n][d] against one window's (m16, step16) [d] (fp16, or the
+    fp32 dequantized MXFP4 metadata)."""
     m = m16.astype(F32)
     s = step16.astype(F32)
     with np.errstate(divide="ignore"):
@@ -123,6 +124,41 @@ def quantize_keys_fmt(k16: np.ndarray, length: int, signs: np.ndarray, window: i
         m16[g], st16[g] = window_stats_fmt(z[a:b])
         codes[a:b] = key_codes_fmt(z[a:b], m16[g], st16[g])
     return dict(codes=codes, m16=m16, step16=st16, n16=norms, z=z)
+
+
+def quantize_keys_mx_fmt(k16: np.ndarray, length: int, signs: np.ndarray, window: int = WINDOW):
+    """The key codec with MXFP4 window metadata (readings R16-R19 of ``oracle.mxfp4``).
+
+    Per window: lo = min z + 0, hi = max z + 0, step = fl(fl(hi - lo) / 3) in fp32 as in the fp16
+    variant; the 128-vectors lo and step are stored as MXFP4 (4 blocks of 32 channels each) and
+    the codes are taken against their dequantized values m, s (fp32, exact).
+    Returns codes [n_pad][d], m_codes / s_codes uint8 [n_win][d], m_scale / s_scale uint8
+    [n_win][d / 32], m / s fp32 [n_win][d] (dequantized), n16 [n_pad], z [length][d].
+    """
+    from .mxfp4 import mx_dequantize, mx_quantize
+
+    length = int(length)
+    d = k16.shape[-1]
+    n_win = -(-length // window)
+    n_pad = n_win * window
+    z, n16 = key_direction_fmt(k16[:length], signs)
+    codes = np.zeros((n_pad, d), np.uint8)
+    out = {f: np.zeros((n_win, d), np.uint8) for f in ("m_codes", "s_codes")}
+    out.update({f: np.zeros((n_win, d // 32), np.uint8) for f in ("m_scale", "s_scale")})
+    out.update({f: np.zeros((n_win, d), F32) for f in ("m", "s")})
+    norms = np.zeros(n_pad, np.float16)
+    norms[:length] = n16
+    for g in range(n_win):
+        a, b = g * window, min((g + 1) * window, length)
+        lo = z[a:b].min(axis=0).astype(F32) + F32(0.0)
+        hi = z[a:b].max(axis=0).astype(F32) + F32(0.0)
+        step = (hi - lo) / F32(LEVELS)
+        out["m_codes"][g], out["m_scale"][g] = mx_quantize(lo)
+        out["s_codes"][g], out["s_scale"][g] = mx_quantize(step)
+        out["m"][g] = mx_dequantize(out["m_codes"][g], out["m_scale"][g]).astype(F32)
+        out["s"][g] = mx_dequantize(out["s_codes"][g], out["s_scale"][g]).astype(F32)
+        codes[a:b] = key_codes_fmt(z[a:b], out["m"][g], out["s"][g])
+    return dict(codes=codes, n16=norms, z=z, **out)
 
 
 def quantize_keys_f64(k16: np.ndarray, length: int, signs: np.ndarray, window: int = WINDOW):

@@ -92,6 +92,49 @@ def unpack_values(packed: np.ndarray) -> np.ndarray:
 
 
 # ---------------------------------------------------------------------------------------------
+# MXFP4 key metadata record, one per window: 136 bytes.
+#   bytes 4 q .. 4 q + 1 (little-endian 16 bits): minimum codes of channels 4 q .. 4 q + 3, channel
+#                        4 q + i in bits 4 i .. 4 i + 3 (q = 0 .. 31);
+#   bytes 4 q + 2 .. 4 q + 3: the step codes of the same channels;
+#   byte 128 + 2 b:      E8M0 scale of the minimum block b (channels 32 b .. 32 b + 31, b = 0 .. 3);
+#   byte 129 + 2 b:      E8M0 scale of the step block b.
+# ---------------------------------------------------------------------------------------------
+MX_RECORD = 136
+
+
+def pack_mx_meta(m_codes, s_codes, m_scale, s_scale) -> np.ndarray:
+    """[n_win][128] 4-bit codes and [n_win][4] scale bytes of minimum and step -> [n_win][136]."""
+    m_codes, s_codes = np.asarray(m_codes, np.uint32), np.asarray(s_codes, np.uint32)
+    n = m_codes.shape[0]
+    out = np.zeros((n, MX_RECORD), np.uint8)
+    for q in range(HEAD_DIM // 4):
+        mw = sum(m_codes[:, 4 * q + i] << (4 * i) for i in range(4))
+        sw = sum(s_codes[:, 4 * q + i] << (4 * i) for i in range(4))
+        out[:, 4 * q] = mw & 0xFF
+        out[:, 4 * q + 1] = mw >> 8
+        out[:, 4 * q + 2] = sw & 0xFF
+        out[:, 4 * q + 3] = sw >> 8
+    out[:, 128::2] = m_scale
+    out[:, 129::2] = s_scale
+    return out
+
+
+def unpack_mx_meta(rec: np.ndarray):
+    """[n_win][136] -> (m_codes, s_codes [n_win][128], m_scale, s_scale [n_win][4])."""
+    rec = np.asarray(rec, np.uint8)
+    n = rec.shape[0]
+    m_codes = np.zeros((n, HEAD_DIM), np.uint8)
+    s_codes = np.zeros((n, HEAD_DIM), np.uint8)
+    for q in range(HEAD_DIM // 4):
+        mw = rec[:, 4 * q].astype(np.uint32) | (rec[:, 4 * q + 1].astype(np.uint32) << 8)
+        sw = rec[:, 4 * q + 2].astype(np.uint32) | (rec[:, 4 * q + 3].astype(np.uint32) << 8)
+        for i in range(4):
+            m_codes[:, 4 * q + i] = (mw >> (4 * i)) & 15
+            s_codes[:, 4 * q + i] = (sw >> (4 * i)) & 15
+    return m_codes, s_codes, rec[:, 128:136:2].copy(), rec[:, 129:136:2].copy()
+
+
+# ---------------------------------------------------------------------------------------------
 # Bits per cached element (Tab. 3, "Bits/elem." column). One element = one coordinate of one
 # cached key or value; the column averages keys and values.
 # ---------------------------------------------------------------------------------------------
@@ -120,6 +163,7 @@ def bits_per_element(scheme: str, d: int = HEAD_DIM, group: int = WINDOW) -> flo
     return (k + v) / 2
 
 
-def cache_bytes_per_token_head(d: int = HEAD_DIM, group: int = WINDOW) -> dict:
-    """Bytes this layout stores per cached token per KV head, by field (fp16 metadata)."""
-    return dict(k_codes=d // 4, v_codes=d // 4, k_norm=2, v_norm=2, k_meta=2 * 2 * d / group)
+def cache_bytes_per_token_head(d: int = HEAD_DIM, group: int = WINDOW, key_meta: str = "fp16") -> dict:
+    """Bytes this layout stores per cached token per KV head, by field."""
+    meta = 2 * 2 * d / group if key_meta == "fp16" else MX_RECORD / group
+    return dict(k_codes=d // 4, v_codes=d // 4, k_norm=2, v_norm=2, k_meta=meta)
