@@ -47,6 +47,23 @@
  * Slots of the last window beyond a sequence's length hold code 0 and norm 0.
  * Storage is 84 bytes per token per KV head: 2.625 bits per element, the "FP16 meta." row of
  * the paper's Tab. 3.
+ *
+ * MXFP4 key metadata (dims.key_meta = OKVQ_KEY_META_MXFP4, the paper's default, Sec. 3.1 and
+ * Tab. 3 "Ours (MXFP4 meta.)"): k_min and k_step are replaced by
+ *   k_mx     u8  [B][H][cap/32][136]  one record per window. The window's fp32 minimum vector and
+ *                                      its fp32 step vector (max - min) / 3 are each stored as
+ *                                      MXFP4: 4 blocks of 32 channels, every block one E8M0 scale
+ *                                      2^e (byte e + 127, e = floor(log2(max |x|)) - 2, clamped
+ *                                      to [-127, 127]; -127 for an all-zero block) and 32 FP4
+ *                                      E2M1 elements (nearest value of x / 2^e, ties to even,
+ *                                      saturating at 6; the sign is kept). Bytes 4q..4q+1: the
+ *                                      minimum's elements of channels 4q..4q+3 (channel 4q + i
+ *                                      in bits 4i..4i+3); bytes 4q+2..4q+3: the step's; byte
+ *                                      128 + 2b: the minimum's scale of block b (channels
+ *                                      32b..32b+31); byte 129 + 2b: the step's scale.
+ * Key codes are then computed against the dequantized minimum m and step s (code 0 where s is
+ * zero, else clamp(rint(fl(fl(z - m) * fl(1 / s))), 0, 3)). Storage: 72.25 bytes per token per
+ * KV head, 2.258 bits per element.
  */
 #ifndef OKVQ_H
 #define OKVQ_H
@@ -75,13 +92,19 @@ enum {
   OKVQ_VALUE_EXACT = 1u << 0 /* value rotation as a sequential fp32 dot product (bit-exact codes) */
 };
 
+/* okvq_dims.key_meta: storage of the per-window key minimum and step */
+enum {
+  OKVQ_KEY_META_FP16 = 0, /* fp16 k_min, k_step (84 bytes per token per KV head)           */
+  OKVQ_KEY_META_MXFP4 = 1 /* MXFP4 records in k_mx (72.25 bytes per token per KV head)    */
+};
+
 /* bytes of the prepared rotation tables (okvq_cache.v_rot16, okvq_prepare_rotation) */
 #define OKVQ_ROTATION_TABLE_BYTES 294912
 
 /* which_buffer for okvq_buffer_bytes */
 enum {
   OKVQ_BUF_K_CODES = 0, OKVQ_BUF_V_CODES, OKVQ_BUF_K_NORM, OKVQ_BUF_V_NORM, OKVQ_BUF_K_MIN,
-  OKVQ_BUF_K_STEP, OKVQ_BUF_MODALITY, OKVQ_BUF_K_STAGE, OKVQ_BUF_SEQ_LENS, OKVQ_NUM_BUFFERS
+  OKVQ_BUF_K_STEP, OKVQ_BUF_MODALITY, OKVQ_BUF_K_STAGE, OKVQ_BUF_SEQ_LENS, OKVQ_BUF_K_MX, OKVQ_NUM_BUFFERS
 };
 
 typedef struct {
@@ -91,9 +114,12 @@ typedef struct {
   int32_t head_dim;     /* must be 128                              */
   int32_t window;       /* key group size, must be 32 (Sec. 3.1)    */
   int32_t capacity;     /* token slots per sequence, multiple of 32 */
+  int32_t key_meta;     /* OKVQ_KEY_META_FP16 or OKVQ_KEY_META_MXFP4 */
 } okvq_dims;
 
-typedef struct {               /* all pointers are device memory, laid out as above */
+typedef struct {               /* all pointers are device memory, laid out as above; k_min and
+                                  k_step are used with fp16 metadata (else may be NULL), k_mx
+                                  with MXFP4 metadata (else may be NULL) */
   okvq_dims dims;
   uint8_t* k_codes;
   uint8_t* v_codes;
@@ -110,6 +136,7 @@ typedef struct {               /* all pointers are device memory, laid out as ab
                                   from v_rot: the inverse rotation that decode applies once per
                                   modality (Sec. 2.3), then the forward rotation of append in
                                   the operand layout of its matrix-core kernel              */
+  uint8_t* k_mx;               /* [B][H][cap/32][136] MXFP4 key metadata records            */
 } okvq_cache;
 
 /* Library version (major * 10000 + minor * 100 + patch). */
@@ -118,7 +145,8 @@ int32_t okvq_version(void);
 /* Human-readable name of a status code (static string). */
 const char* okvq_status_string(okvq_status status);
 
-/* Bytes of one cache buffer for `dims` (0 for an unknown buffer or invalid dims). */
+/* Bytes of one cache buffer for `dims` (0 for an unknown buffer, invalid dims, or a buffer the
+ * metadata format of dims does not use: k_min / k_step with MXFP4, k_mx with fp16). */
 size_t okvq_buffer_bytes(const okvq_dims* dims, int32_t which_buffer);
 
 /* Fixed Gaussian codebook of Eq. 3 as used by the kernels: the 4 levels and 3 decision
@@ -134,10 +162,20 @@ okvq_status okvq_codebook(float* levels, float* thresholds);
  *              windows are aligned to token 0; a partial last window takes its min/step over
  *              its valid tokens; its padded slots get code 0 and norm 0. Nothing beyond the
  *              last window of each sequence is written.
- * Bit-exact contract: norms, min, step and codes equal the documented fp32 operation order. */
+ * Bit-exact contract: norms, min, step and codes equal the documented fp32 operation order.
+ * dims->key_meta must be OKVQ_KEY_META_FP16 (else OKVQ_ERR_INVALID_ARGUMENT). */
 okvq_status okvq_quantize_keys(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens,
                                const int32_t* lens_host, const int8_t* key_signs, uint8_t* k_codes,
                                uint16_t* k_min, uint16_t* k_step, uint16_t* k_norm, void* stream);
+
+/* okvq_quantize_keys with MXFP4 window metadata (Sec. 3.1: the paper's default storage of the
+ * Eq. 4 minimum and scale): the same arguments, with k_mx (device u8 [B][H][cap/32][136], the
+ * record layout above) in place of k_min and k_step. dims->key_meta must be
+ * OKVQ_KEY_META_MXFP4. Bit-exact contract: norms, records and codes equal the documented fp32
+ * operation order followed by the MXFP4 conversion. */
+okvq_status okvq_quantize_keys_mx(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens,
+                                  const int32_t* lens_host, const int8_t* key_signs, uint8_t* k_codes,
+                                  uint8_t* k_mx, uint16_t* k_norm, void* stream);
 
 /* Quantize values (Eq. 6 with the codebook of Eq. 3) of a dense block into cache-layout buffers.
  *   v          device f16 [B][H][n_tokens][128]
@@ -161,7 +199,8 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
  * chunking of a sequence yields the same cache bytes as one quantization of the whole sequence.
  * cache->seq_lens[b] is advanced by n_new[b] on the device. Fails with OKVQ_ERR_CAPACITY if
  * lens_host[b] + n_new_host[b] > capacity. The MFMA-mode values read the forward rotation from
- * cache->v_rot16 (okvq_prepare_rotation); OKVQ_VALUE_EXACT reads cache->v_rot. */
+ * cache->v_rot16 (okvq_prepare_rotation); OKVQ_VALUE_EXACT reads cache->v_rot. The key window
+ * metadata is written in the format of cache->dims.key_meta (k_min / k_step, or k_mx). */
 okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
                         const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
                         const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream);
@@ -189,7 +228,8 @@ size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len);
  *   sm_scale   softmax scale, normally 1/sqrt(128)
  *   out        device f32 [B][Hq][128]
  *   workspace  device, at least okvq_decode_workspace_bytes(dims, max(lens_host)) bytes
- * Needs cache->v_rot16 (okvq_prepare_rotation). A sequence of length 0 yields zeros. fp32
+ * Needs cache->v_rot16 (okvq_prepare_rotation); reads the key window metadata in the format of
+ * cache->dims.key_meta. A sequence of length 0 yields zeros. fp32
  * accumulation; the result matches float64 attention over the dequantized cache within 2e-3 of
  * the output norm. */
 okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,

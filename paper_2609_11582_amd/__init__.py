@@ -7,4 +7,5 @@ include/okvq.h); ``okvq`` is its ctypes binding.
 from . import okvq  # noqa: F401
 from .okvq import (KVCache, OkvqError, decode_workspace, make_dims, okvq_append, okvq_buffer_bytes,  # noqa: F401
                    okvq_codebook, okvq_decode_attention, okvq_decode_attention_timed, okvq_decode_workspace_bytes,
-                   okvq_prepare_rotation, okvq_quantize_keys, okvq_quantize_values, okvq_version, status_string)
+                   okvq_prepare_rotation, okvq_quantize_keys, okvq_quantize_keys_mx, okvq_quantize_values, okvq_version,
+                   status_string)

@@ -10,7 +10,7 @@ using namespace okvq;
 
 namespace {
 
-constexpr int32_t kVersion = 100;  // 0.1.0
+constexpr int32_t kVersion = 200;  // 0.2.0: MXFP4 key metadata
 
 // ---- fixed Gaussian codebook (Sec. 2.1, Eq. 3): Lloyd-Max quantizer of N(0, 1), 4 levels ----
 double phi(double x) { return std::isinf(x) ? 0.0 : std::exp(-0.5 * x * x) / std::sqrt(2.0 * M_PI); }
@@ -72,17 +72,22 @@ okvq_status check_dims(const okvq_dims* d) {
   if (d->num_q_heads / d->num_kv_heads > 8) return OKVQ_ERR_UNSUPPORTED;
   if (d->capacity < 32 || d->capacity % 32 != 0) return OKVQ_ERR_INVALID_ARGUMENT;
   if (d->batch > 65535 || d->num_kv_heads > 65535) return OKVQ_ERR_UNSUPPORTED;
+  if (d->key_meta != OKVQ_KEY_META_FP16 && d->key_meta != OKVQ_KEY_META_MXFP4) return OKVQ_ERR_INVALID_ARGUMENT;
   return OKVQ_OK;
 }
+
+bool is_mx(const okvq_dims* d) { return d->key_meta == OKVQ_KEY_META_MXFP4; }
 
 okvq_status check_cache(const okvq_cache* c) {
   if (!c) return OKVQ_ERR_INVALID_ARGUMENT;
   okvq_status st = check_dims(&c->dims);
   if (st != OKVQ_OK) return st;
-  const void* ptrs[] = {c->k_codes, c->v_codes, c->k_norm, c->v_norm, c->k_min, c->k_step,
-                        c->modality, c->k_stage, c->seq_lens, c->key_signs, c->v_rot, c->v_rot16};
+  const void* ptrs[] = {c->k_codes, c->v_codes, c->k_norm,    c->v_norm, c->modality,
+                        c->k_stage, c->seq_lens, c->key_signs, c->v_rot,  c->v_rot16};
   for (const void* p : ptrs)
     if (!aligned16(p)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (is_mx(&c->dims) ? !aligned16(c->k_mx) : (!aligned16(c->k_min) || !aligned16(c->k_step)))
+    return OKVQ_ERR_INVALID_ARGUMENT;
   return OKVQ_OK;
 }
 
@@ -98,6 +103,7 @@ CacheView view(const okvq_cache* c) {
   v.v_norm = c->v_norm;
   v.k_min = c->k_min;
   v.k_step = c->k_step;
+  v.k_mx = is_mx(&c->dims) ? c->k_mx : nullptr;
   v.modality = c->modality;
   v.k_stage = c->k_stage;
   v.seq_lens = c->seq_lens;
@@ -141,8 +147,9 @@ size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
     case OKVQ_BUF_V_CODES: return B * H * cap * (D / 4);
     case OKVQ_BUF_K_NORM: return B * H * cap * 2;
     case OKVQ_BUF_V_NORM: return B * H * cap * 2;
-    case OKVQ_BUF_K_MIN: return B * H * (cap / W) * D * 2;
-    case OKVQ_BUF_K_STEP: return B * H * (cap / W) * D * 2;
+    case OKVQ_BUF_K_MIN: return is_mx(d) ? 0 : B * H * (cap / W) * D * 2;
+    case OKVQ_BUF_K_STEP: return is_mx(d) ? 0 : B * H * (cap / W) * D * 2;
+    case OKVQ_BUF_K_MX: return is_mx(d) ? B * H * (cap / W) * kMxRecord : 0;
     case OKVQ_BUF_MODALITY: return B * cap;
     case OKVQ_BUF_K_STAGE: return B * H * W * D * 2;
     case OKVQ_BUF_SEQ_LENS: return B * 4 + 4;  // the lengths and append's work-group counter
@@ -158,15 +165,10 @@ okvq_status okvq_codebook(float* levels, float* thresholds_out) {
   return OKVQ_OK;
 }
 
-okvq_status okvq_quantize_keys(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens, const int32_t* lens_host,
-                               const int8_t* key_signs, uint8_t* k_codes, uint16_t* k_min, uint16_t* k_step,
-                               uint16_t* k_norm, void* stream) {
-  okvq_status st = check_dims(dims);
-  if (st != OKVQ_OK) return st;
-  if (n_tokens < 0 || !lens_host) return OKVQ_ERR_INVALID_ARGUMENT;
-  if (!aligned16(k) || !aligned16(key_signs) || !aligned16(k_codes) || !aligned16(k_min) || !aligned16(k_step) ||
-      !aligned16(k_norm))
-    return OKVQ_ERR_INVALID_ARGUMENT;
+static okvq_status quantize_keys_impl(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens,
+                                      const int32_t* lens_host, const int8_t* key_signs, uint8_t* k_codes,
+                                      uint16_t* k_min, uint16_t* k_step, uint8_t* k_mx, uint16_t* k_norm,
+                                      void* stream) {
   for (int b = 0; b < dims->batch; ++b) {
     if (lens_host[b] < 0 || lens_host[b] > n_tokens) return OKVQ_ERR_INVALID_ARGUMENT;
     if (lens_host[b] > dims->capacity) return OKVQ_ERR_CAPACITY;
@@ -190,11 +192,35 @@ okvq_status okvq_quantize_keys(const okvq_dims* dims, const uint16_t* k, int32_t
     a.k_codes = k_codes;
     a.k_min = k_min;
     a.k_step = k_step;
+    a.k_mx = k_mx;
     a.k_norm = k_norm;
-    st = hip_status(launch_codec(a, true, false, s));
+    okvq_status st = hip_status(launch_codec(a, true, false, s));
     if (st != OKVQ_OK) return st;
   }
   return OKVQ_OK;
+}
+
+okvq_status okvq_quantize_keys(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens, const int32_t* lens_host,
+                               const int8_t* key_signs, uint8_t* k_codes, uint16_t* k_min, uint16_t* k_step,
+                               uint16_t* k_norm, void* stream) {
+  okvq_status st = check_dims(dims);
+  if (st != OKVQ_OK) return st;
+  if (n_tokens < 0 || !lens_host || is_mx(dims)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(k) || !aligned16(key_signs) || !aligned16(k_codes) || !aligned16(k_min) || !aligned16(k_step) ||
+      !aligned16(k_norm))
+    return OKVQ_ERR_INVALID_ARGUMENT;
+  return quantize_keys_impl(dims, k, n_tokens, lens_host, key_signs, k_codes, k_min, k_step, nullptr, k_norm, stream);
+}
+
+okvq_status okvq_quantize_keys_mx(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens,
+                                  const int32_t* lens_host, const int8_t* key_signs, uint8_t* k_codes, uint8_t* k_mx,
+                                  uint16_t* k_norm, void* stream) {
+  okvq_status st = check_dims(dims);
+  if (st != OKVQ_OK) return st;
+  if (n_tokens < 0 || !lens_host || !is_mx(dims)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(k) || !aligned16(key_signs) || !aligned16(k_codes) || !aligned16(k_mx) || !aligned16(k_norm))
+    return OKVQ_ERR_INVALID_ARGUMENT;
+  return quantize_keys_impl(dims, k, n_tokens, lens_host, key_signs, k_codes, nullptr, nullptr, k_mx, k_norm, stream);
 }
 
 okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const uint8_t* modality, int32_t n_tokens,
@@ -284,6 +310,7 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
     a.k_codes = cache->k_codes;
     a.k_min = cache->k_min;
     a.k_step = cache->k_step;
+    a.k_mx = is_mx(&d) ? cache->k_mx : nullptr;
     a.k_norm = cache->k_norm;
     a.th = thresholds();
     a.v_codes = cache->v_codes;

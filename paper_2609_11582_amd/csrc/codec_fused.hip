@@ -137,6 +137,7 @@ __device__ __forceinline__ void rewrite_stage(const CodecJob& j, const TileCtx& 
   }
 }
 
+template <bool kMx>
 __device__ __forceinline__ void key_role(const CodecArgs& a, int kw, float* lds) {
   const CodecJob& j = a.j;
   int t = blockIdx.x;  // < ntiles: the grid is never larger
@@ -170,9 +171,11 @@ __device__ __forceinline__ void key_role(const CodecArgs& a, int kw, float* lds)
       }
     };
     if (work) {
-      KeyWaveOut out{a.k_codes + c.seq * j.cap * 32, a.k_min + c.seq * (j.cap / kW) * kD,
-                     a.k_step + c.seq * (j.cap / kW) * kD, a.k_norm + c.seq * j.cap};
-      key_quantize_rows(x, n16, tok0, c.len, out, lds, prefetch);
+      const size_t nw = j.cap / kW;
+      KeyWaveOut out{a.k_codes + c.seq * j.cap * 32, kMx ? nullptr : a.k_min + c.seq * nw * kD,
+                     kMx ? nullptr : a.k_step + c.seq * nw * kD, kMx ? a.k_mx + c.seq * nw * kMxRecord : nullptr,
+                     a.k_norm + c.seq * j.cap};
+      key_quantize_rows<kMx>(x, n16, tok0, c.len, out, lds, prefetch);
     } else {
       prefetch();
     }
@@ -460,7 +463,7 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
 }
 
 // ------------------------------------------------------------------------------------------------
-template <bool kKeys, bool kValues>
+template <bool kKeys, bool kValues, bool kMx>
 __global__ __launch_bounds__(256 * (kKeys + kValues), (kKeys && kValues) ? 1 : 2) void k_codec(CodecArgs a) {
   __shared__ __attribute__((aligned(16))) float key_lds[kKeys ? 4 * kKeyWaveLds : 4];
   __shared__ __attribute__((aligned(16))) ValueShared vsh;
@@ -470,7 +473,7 @@ __global__ __launch_bounds__(256 * (kKeys + kValues), (kKeys && kValues) ? 1 : 2
     __syncthreads();  // the only work-group barrier; every wave reaches it
   }
   if (kKeys && wave < 4) {
-    key_role(a, wave, key_lds + wave * kKeyWaveLds);
+    key_role<kMx>(a, wave, key_lds + wave * kKeyWaveLds);
   } else if (kValues) {
     value_role(a, wave - (kKeys ? 4 : 0), vsh);
   }
@@ -526,12 +529,19 @@ hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t 
   // leaves room for two
   const int per_cu = (keys && values) ? 1 : 2;
   const int grid = std::min(a.ntiles, per_cu * cus);
+  const bool mx = a.k_mx != nullptr;
   if (keys && values) {
-    hipLaunchKernelGGL((k_codec<true, true>), dim3(grid), dim3(512), 0, s, a);
+    if (mx)
+      hipLaunchKernelGGL((k_codec<true, true, true>), dim3(grid), dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_codec<true, true, false>), dim3(grid), dim3(512), 0, s, a);
   } else if (keys) {
-    hipLaunchKernelGGL((k_codec<true, false>), dim3(grid), dim3(256), 0, s, a);
+    if (mx)
+      hipLaunchKernelGGL((k_codec<true, false, true>), dim3(grid), dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_codec<true, false, false>), dim3(grid), dim3(256), 0, s, a);
   } else {
-    hipLaunchKernelGGL((k_codec<false, true>), dim3(grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_codec<false, true, false>), dim3(grid), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

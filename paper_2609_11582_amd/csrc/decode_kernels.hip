@@ -52,6 +52,7 @@ struct DecodeArgs {
   const uint16_t* v_norm;
   const uint16_t* k_min;
   const uint16_t* k_step;
+  const uint8_t* k_mx;  // MXFP4 window records (k_decode<true>) instead of k_min / k_step
   const uint8_t* modality;
   const int32_t* seq_lens;
   const int8_t* signs;
@@ -188,6 +189,7 @@ struct PairLoad {
   uint2 nv0, nv1;            // value norms of the same tokens
   uint32_t md0, md1;         // modality ids of the same tokens
   uint2 stp, mnp;            // step / min of channels 32g + 4 (col % 8) .. +3 of the side window
+                             // (MXFP4: stp.x = their record word, stp.y = block g's scale bytes)
 };
 
 struct SeqPtrs {  // uniform per work-group
@@ -197,9 +199,11 @@ struct SeqPtrs {  // uniform per work-group
   const uint16_t* vn;
   const uint16_t* kmin;
   const uint16_t* kstep;
+  const uint8_t* kmx;
   const uint8_t* md;
 };
 
+template <bool kMx>
 __device__ __forceinline__ PairLoad load_pair(const SeqPtrs& sp, int wA, bool hasB, int lane) {
   const int col = lane & 15, g = lane >> 4, r = lane & 15, side = col >> 3;
   const uint32_t wB = hasB ? wA + 1 : wA;
@@ -218,10 +222,30 @@ __device__ __forceinline__ PairLoad load_pair(const SeqPtrs& sp, int wA, bool ha
   d.nv1 = *reinterpret_cast<const uint2*>(sp.vn + t + 16);
   d.md0 = *reinterpret_cast<const uint32_t*>(sp.md + t);
   d.md1 = *reinterpret_cast<const uint32_t*>(sp.md + t + 16);
-  const uint32_t mt = wS * kD + 32u * g + 4u * (col & 7);
-  d.stp = *reinterpret_cast<const uint2*>(sp.kstep + mt);
-  d.mnp = *reinterpret_cast<const uint2*>(sp.kmin + mt);
+  if constexpr (kMx) {
+    const uint8_t* rec = sp.kmx + wS * (uint32_t)kMxRecord;
+    d.stp.x = *reinterpret_cast<const uint32_t*>(rec + 4u * (8u * g + (col & 7)));
+    d.stp.y = *reinterpret_cast<const uint16_t*>(rec + 128u + 2u * g);
+    d.mnp = make_uint2(0u, 0u);
+  } else {
+    const uint32_t mt = wS * kD + 32u * g + 4u * (col & 7);
+    d.stp = *reinterpret_cast<const uint2*>(sp.kstep + mt);
+    d.mnp = *reinterpret_cast<const uint2*>(sp.kmin + mt);
+  }
   return d;
+}
+
+// fp16 minimum / step pairs of 4 channels from their MXFP4 record word and block scale bytes: the
+// gfx950 scaled FP4 -> fp16 conversion multiplies by 2^(X - 127) and rounds to nearest even. A
+// scale byte of 0 (2^-127) is taken as 2^-126: either way the values are below fp16's range and
+// convert to zero.
+__device__ __forceinline__ void mx_to_f16(uint32_t word, uint32_t scales, uint2& mnp, uint2& stp) {
+  const float sm = __builtin_bit_cast(float, max(scales & 0xffu, 1u) << 23);
+  const float ss = __builtin_bit_cast(float, max(scales >> 8, 1u) << 23);
+  mnp.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(word, sm, 0));
+  mnp.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(word, sm, 1));
+  stp.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(word, ss, 2));
+  stp.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(word, ss, 3));
 }
 
 // B operand of the value MFMA for 16-channel block nb: code bytes of tokens 4g..4g+3 and
@@ -235,6 +259,7 @@ __device__ __forceinline__ half8 lut_op(const uint2* vlut, uint4 vc, int nb) {
   return h8(x0.x, x0.y, x1.x, x1.y);
 }
 
+template <bool kMx>
 __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   __shared__ __attribute__((aligned(16))) uint2 vlut[256];
   __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];                     // q' (fp32, padded rows)
@@ -260,8 +285,13 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   const int w_plan = min(w_begin + p.wps, p.cap / kW);  // windows of this split by the plan
   const int wA0 = w_begin + 2 * wave;                    // this wave's pairs: (wA0 + 16 k, +1)
   const size_t nwcap = p.cap / kW;
-  const SeqPtrs sp{p.k_codes + seq * p.cap * 32,       p.v_codes + seq * nwcap * 1024, p.k_norm + seq * p.cap,
-                   p.v_norm + seq * p.cap,             p.k_min + seq * nwcap * kD,     p.k_step + seq * nwcap * kD,
+  const SeqPtrs sp{p.k_codes + seq * p.cap * 32,
+                   p.v_codes + seq * nwcap * 1024,
+                   p.k_norm + seq * p.cap,
+                   p.v_norm + seq * p.cap,
+                   kMx ? nullptr : p.k_min + seq * nwcap * kD,
+                   kMx ? nullptr : p.k_step + seq * nwcap * kD,
+                   kMx ? p.k_mx + seq * nwcap * kMxRecord : nullptr,
                    p.modality + (size_t)b * p.cap};
 
   // ---- every global load of the prologue goes out before any of them is used: the query rows
@@ -275,7 +305,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     qsgn = *reinterpret_cast<const uint32_t*>(p.signs + c4);
   }
   PairLoad bufA, bufB;
-  if (wA0 < w_plan) bufA = load_pair(sp, wA0, wA0 + 1 < w_plan, lane);
+  if (wA0 < w_plan) bufA = load_pair<kMx>(sp, wA0, wA0 + 1 < w_plan, lane);
   const uint32_t touch = reinterpret_cast<const uint32_t*>(p.rot16t)[tid * 48];  // one dword per 192 B
   const int len = min(p.seq_lens[b], p.cap);  // memory-safe if device and host lengths disagree
   const int nwin = (len + kW - 1) / kW;
@@ -336,7 +366,8 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   }
   __syncthreads();
   const float amax = fmaxf(fmaxf(amax_w[0], amax_w[1]), fmaxf(amax_w[2], amax_w[3]));
-  // power-of-two scale k0 keeps |q'_c step_c 2^(k0 - shift)| <= 2^15 (|step| <= 2/3 + rounding)
+  // power-of-two scale k0 keeps |q'_c step_c 2^(k0 - shift)| <= 2^15: |step| <= 2/3 + rounding for
+  // fp16 metadata, and below 1 for MXFP4 (a block's largest step rounds up by at most 3/2)
   const int k0 = (amax > 0.0f) ? min(max(14 - ilogbf(amax), -60), 60) : 0;
   const float kscale = ldexpf(1.0f, 24 - k0);  // undoes 2^(k0 - 24) on the MFMA result
   // Per-lane query operand of the score MFMA, constant over the pairs: for channels
@@ -380,8 +411,10 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     const int wS = wA + side;
 
     // ---- side window metadata through wave-private LDS, natural channel order ----
-    *reinterpret_cast<uint2*>(&mw[16 * g + 2 * c7]) = cur.stp;
-    *reinterpret_cast<uint2*>(&mw[kD / 2 + 16 * g + 2 * c7]) = cur.mnp;
+    uint2 stp = cur.stp, mnp = cur.mnp;
+    if constexpr (kMx) mx_to_f16(cur.stp.x, cur.stp.y, mnp, stp);
+    *reinterpret_cast<uint2*>(&mw[16 * g + 2 * c7]) = stp;
+    *reinterpret_cast<uint2*>(&mw[kD / 2 + 16 * g + 2 * c7]) = mnp;
     wave_lds_sync();
     uint4 mn4[4];
 #pragma unroll
@@ -535,11 +568,11 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   // ---- window pairs, double-buffered loads without register copies ----
   for (int wA = wA0; wA < w_end; wA += 4 * kDecWaves) {
     const int wA2 = wA + 2 * kDecWaves;
-    if (wA2 < w_end) bufB = load_pair(sp, wA2, wA2 + 1 < w_end, lane);
+    if (wA2 < w_end) bufB = load_pair<kMx>(sp, wA2, wA2 + 1 < w_end, lane);
     process(bufA, wA);
     if (wA2 >= w_end) break;
     const int wA3 = wA2 + 2 * kDecWaves;
-    if (wA3 < w_end) bufA = load_pair(sp, wA3, wA3 + 1 < w_end, lane);
+    if (wA3 < w_end) bufA = load_pair<kMx>(sp, wA3, wA3 + 1 < w_end, lane);
     process(bufB, wA2);
   }
 
@@ -784,6 +817,7 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
   a.v_norm = c.v_norm;
   a.k_min = c.k_min;
   a.k_step = c.k_step;
+  a.k_mx = c.k_mx;
   a.modality = c.modality;
   a.seq_lens = c.seq_lens;
   a.signs = c.signs;
@@ -800,11 +834,17 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
   a.cb01 = cb01;
   a.cb23 = cb23;
   hipError_t e;
+  const dim3 grid(plan.nsplit, c.H, c.B), block(64 * kDecWaves);
   if (events) {  // events bound to the two dispatches: start and end of each kernel's execution
-    hipExtLaunchKernelGGL(k_decode, dim3(plan.nsplit, c.H, c.B), dim3(64 * kDecWaves), 0, s, events[0], events[1], 0,
-                          a);
+    if (c.k_mx)
+      hipExtLaunchKernelGGL(k_decode<true>, grid, block, 0, s, events[0], events[1], 0, a);
+    else
+      hipExtLaunchKernelGGL(k_decode<false>, grid, block, 0, s, events[0], events[1], 0, a);
   } else {
-    hipLaunchKernelGGL(k_decode, dim3(plan.nsplit, c.H, c.B), dim3(64 * kDecWaves), 0, s, a);
+    if (c.k_mx)
+      hipLaunchKernelGGL(k_decode<true>, grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL(k_decode<false>, grid, block, 0, s, a);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (events) {

@@ -24,8 +24,9 @@ constexpr int kKeyWaveLds = 64 * kKeyPitch + 2 * kD * 2;  // floats per wave: ti
 
 struct KeyWaveOut {
   uint8_t* codes;  // [cap][32] of this (sequence, head)
-  uint16_t* kmin;  // [cap/32][128]
+  uint16_t* kmin;  // [cap/32][128] fp16 window metadata, or
   uint16_t* kstep; // [cap/32][128]
+  uint8_t* kmx;    // [cap/32][136] MXFP4 window records
   uint16_t* knorm; // [cap]
 };
 
@@ -64,8 +65,9 @@ __device__ __forceinline__ uint32_t key_norm(const float (&x)[kD]) {
 // Phase A, second half, and phases B and C for the 64 tokens [tok0, tok0 + 64) of one wave
 // (lane = token). `len` is the sequence length; the slots of every window that holds a valid
 // token are written (padded slots get code 0 and norm 0). between_bc() runs after phase B (the
-// caller's loads for its next rows go out there, when fewer registers are live).
-template <typename F>
+// caller's loads for its next rows go out there, when fewer registers are live). kMx: the window
+// minimum and step are stored as MXFP4 records and the codes use their dequantized values.
+template <bool kMx, typename F>
 __device__ __forceinline__ void key_quantize_rows(float (&x)[kD], uint32_t n16, int tok0, int len, KeyWaveOut out,
                                                   float* lds, F&& between_bc) {
   const int lane = lane_id();
@@ -139,7 +141,43 @@ __device__ __forceinline__ void key_quantize_rows(float (&x)[kD], uint32_t n16, 
       lo[i] = __builtin_fminf(lo[i], __shfl_xor(lo[i], 16));
       hi[i] = __builtin_fmaxf(hi[i], __shfl_xor(hi[i], 16));
     }
-    if (half == 0 && nvalid > 0) {
+    if constexpr (kMx) {
+      // MXFP4: a block of 32 channels is held by the 8 lanes l with equal l / 8 (channel quads
+      // qd & 7), so the block maxima combine over lane bits 0..2
+      // (lo, hi) become (minimum, step), then (dequantized minimum, 1 / dequantized step), in place
+      float am = 0.0f, as = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        lo[i] = lo[i] + 0.0f;  // canonical +0
+        hi[i] = div_rn((hi[i] + 0.0f) - lo[i], 3.0f);
+        am = fmaxf(am, fabsf(lo[i]));
+        as = fmaxf(as, hi[i]);
+      }
+#pragma unroll
+      for (int lb = 1; lb < 8; lb <<= 1) {
+        am = fmaxf(am, __shfl_xor(am, lb));
+        as = fmaxf(as, __shfl_xor(as, lb));
+      }
+      const int em = mx_exponent(am), es = mx_exponent(as);
+      uint32_t word = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t cm = e2m1_encode(ldexpf(lo[i], -em)), cs = e2m1_encode(ldexpf(hi[i], -es));
+        word |= (cm << (4 * i)) | (cs << (16 + 4 * i));
+        const float sv = e2m1_decode(cs, es);
+        lo[i] = e2m1_decode(cm, em);
+        hi[i] = (sv == 0.0f) ? 0.0f : div_rn(1.0f, sv);
+      }
+      if (half == 0 && nvalid > 0) {
+        uint8_t* rec = out.kmx + (size_t)gwin * kMxRecord;
+        *reinterpret_cast<uint32_t*>(rec + 4 * (16 * q + qd)) = word;
+        if ((qd & 7) == 0)
+          *reinterpret_cast<uint16_t*>(rec + 128 + 2 * (2 * q + (qd >> 3))) = (uint16_t)((em + 127) | ((es + 127) << 8));
+        float4* sp = reinterpret_cast<float4*>(stats + (win * kD + 64 * q + 4 * qd) * 2);
+        sp[0] = make_float4(lo[0], hi[0], lo[1], hi[1]);
+        sp[1] = make_float4(lo[2], hi[2], lo[3], hi[3]);
+      }
+    } else if (half == 0 && nvalid > 0) {
       uint32_t m16[4], s16[4];
       float st[8];
 #pragma unroll

@@ -45,8 +45,9 @@ struct CodecArgs {
   // keys
   const int8_t* signs;
   uint8_t* k_codes;
-  uint16_t* k_min;
+  uint16_t* k_min;   // fp16 window metadata, or
   uint16_t* k_step;
+  uint8_t* k_mx;     // MXFP4 window records (non-null selects this format)
   uint16_t* k_norm;
   // values
   const uint16_t* vsrc;  // value rows, laid out like j.src (the key rows)
@@ -73,6 +74,7 @@ struct CacheView {
   uint16_t* v_norm;
   uint16_t* k_min;
   uint16_t* k_step;
+  uint8_t* k_mx;  // MXFP4 window records, or null for fp16 k_min / k_step
   uint8_t* modality;
   uint16_t* k_stage;
   int32_t* seq_lens;

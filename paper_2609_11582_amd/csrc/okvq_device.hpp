@@ -40,6 +40,33 @@ __device__ __forceinline__ void wave_lds_sync() {
 
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 
+// MXFP4 key window metadata (OCP microscaling format: one E8M0 power-of-two scale per block of 32
+// values, FP4 E2M1 elements). Record of one window: bytes 4q..4q+1 hold the minimum's elements of
+// channels 4q..4q+3 (4 bits each), bytes 4q+2..4q+3 the step's, byte 128 + 2b the minimum's scale
+// byte of channel block b, byte 129 + 2b the step's.
+constexpr int kMxRecord = 136;
+
+// Shared exponent of a block whose largest magnitude is amax: floor(log2(amax)) - 2 (2 is the
+// largest E2M1 exponent), clamped to the E8M0 range; -127 for an all-zero block.
+__device__ __forceinline__ int mx_exponent(float amax) {
+  if (!(amax > 0.0f)) return -127;
+  return min(max(ilogbf(amax) - 2, -127), 127);
+}
+// E2M1 code of t (a block value divided by 2^e, exactly): the nearest of 0, 0.5, 1, 1.5, 2, 3, 4,
+// 6 with ties to the even code, saturating at 6; bit 3 is the sign (t < 0).
+__device__ __forceinline__ uint32_t e2m1_encode(float t) {
+  const float a = fabsf(t);
+  const uint32_t c = (uint32_t)(a > 0.25f) + (uint32_t)(a >= 0.75f) + (uint32_t)(a > 1.25f) +
+                     (uint32_t)(a >= 1.75f) + (uint32_t)(a > 2.5f) + (uint32_t)(a >= 3.5f) + (uint32_t)(a > 5.0f);
+  return c | (t < 0.0f ? 8u : 0u);
+}
+// Value of E2M1 code c times 2^e (exact in fp32: two significant bits, exponent >= -128).
+__device__ __forceinline__ float e2m1_decode(uint32_t c, int e) {
+  const uint32_t E = (c >> 1) & 3u, M = c & 1u;
+  const float v = ldexpf((float)(E ? 2u + M : M), (E ? (int)E : 1) - 2 + e);
+  return (c & 8u) ? -v : v;
+}
+
 // Sequence lengths for the stateless codec calls travel as a kernel argument.
 constexpr int kMaxLenArgs = 256;
 struct LenArgs {

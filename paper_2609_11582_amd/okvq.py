@@ -20,8 +20,13 @@ LIB_PATH = os.path.join(_HERE, "libokvq.so")
 
 OKVQ_OK = 0
 OKVQ_VALUE_EXACT = 1
+OKVQ_KEY_META_FP16 = 0
+OKVQ_KEY_META_MXFP4 = 1
+KEY_META = {"fp16": OKVQ_KEY_META_FP16, "mxfp4": OKVQ_KEY_META_MXFP4}
 ROTATION_TABLE_BYTES = 294912  # OKVQ_ROTATION_TABLE_BYTES
-BUFFERS = ("k_codes", "v_codes", "k_norm", "v_norm", "k_min", "k_step", "modality", "k_stage", "seq_lens")
+MX_RECORD_BYTES = 136  # one MXFP4 key-metadata record per 32-token window
+# buffer ids 0..9 of okvq_buffer_bytes (OKVQ_BUF_*)
+BUFFERS = ("k_codes", "v_codes", "k_norm", "v_norm", "k_min", "k_step", "modality", "k_stage", "seq_lens", "k_mx")
 
 
 class OkvqError(RuntimeError):
@@ -32,12 +37,14 @@ class OkvqError(RuntimeError):
 
 class Dims(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
-                ("head_dim", ctypes.c_int32), ("window", ctypes.c_int32), ("capacity", ctypes.c_int32)]
+                ("head_dim", ctypes.c_int32), ("window", ctypes.c_int32), ("capacity", ctypes.c_int32),
+                ("key_meta", ctypes.c_int32)]
 
 
 class CacheStruct(ctypes.Structure):
-    _fields_ = [("dims", Dims)] + [(n, ctypes.c_void_p) for n in BUFFERS] + [
-        ("key_signs", ctypes.c_void_p), ("v_rot", ctypes.c_void_p), ("v_rot16", ctypes.c_void_p)]
+    _fields_ = [("dims", Dims)] + [(n, ctypes.c_void_p) for n in BUFFERS[:9]] + [
+        ("key_signs", ctypes.c_void_p), ("v_rot", ctypes.c_void_p), ("v_rot16", ctypes.c_void_p),
+        ("k_mx", ctypes.c_void_p)]
 
 
 _lib = None
@@ -60,6 +67,8 @@ def lib() -> ctypes.CDLL:
         L.okvq_codebook.argtypes = [P(ctypes.c_float), P(ctypes.c_float)]
         L.okvq_quantize_keys.restype = i32
         L.okvq_quantize_keys.argtypes = [P(Dims), vp, i32, P(i32), vp, vp, vp, vp, vp, vp]
+        L.okvq_quantize_keys_mx.restype = i32
+        L.okvq_quantize_keys_mx.argtypes = [P(Dims), vp, i32, P(i32), vp, vp, vp, vp, vp]
         L.okvq_quantize_values.restype = i32
         L.okvq_quantize_values.argtypes = [P(Dims), vp, vp, i32, P(i32), vp, u32, vp, vp, vp]
         L.okvq_append.restype = i32
@@ -114,8 +123,8 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def make_dims(batch, num_kv_heads, num_q_heads, capacity, head_dim=128, window=32) -> Dims:
-    return Dims(batch, num_kv_heads, num_q_heads, head_dim, window, capacity)
+def make_dims(batch, num_kv_heads, num_q_heads, capacity, head_dim=128, window=32, key_meta="fp16") -> Dims:
+    return Dims(batch, num_kv_heads, num_q_heads, head_dim, window, capacity, KEY_META[key_meta])
 
 
 def okvq_version() -> int:
@@ -146,6 +155,21 @@ def okvq_quantize_keys(dims, k, n_tokens, lens, key_signs, k_codes, k_min, k_ste
                                   _ptr(k_codes), _ptr(k_min), _ptr(k_step), _ptr(k_norm), _stream(stream))
     if check:
         _check(st, "okvq_quantize_keys")
+    return st
+
+
+def okvq_quantize_keys_mx(dims, k, n_tokens, lens, key_signs, k_codes, k_mx, k_norm, stream=None,
+                          check=True) -> int:
+    B, H = dims.batch, dims.num_kv_heads
+    _need_len(lens, B, "lens")
+    _need(k, B * H * int(n_tokens) * 128 * 2, "k")
+    _need(key_signs, 128, "key_signs")
+    for i, (name, t) in {0: ("k_codes", k_codes), 2: ("k_norm", k_norm), 9: ("k_mx", k_mx)}.items():
+        _need(t, okvq_buffer_bytes(dims, i), name)
+    st = lib().okvq_quantize_keys_mx(ctypes.byref(dims), _ptr(k), int(n_tokens), _i32(lens), _ptr(key_signs),
+                                     _ptr(k_codes), _ptr(k_mx), _ptr(k_norm), _stream(stream))
+    if check:
+        _check(st, "okvq_quantize_keys_mx")
     return st
 
 
@@ -238,30 +262,37 @@ def okvq_decode_attention_timed(cache: "KVCache", lens, q, sm_scale, out, worksp
 
 _DTYPES = dict(k_codes=torch.uint8, v_codes=torch.uint8, k_norm=torch.float16, v_norm=torch.float16,
                k_min=torch.float16, k_step=torch.float16, modality=torch.uint8, k_stage=torch.float16,
-               seq_lens=torch.int32)
+               seq_lens=torch.int32, k_mx=torch.uint8)
 
 
 class KVCache:
     """Device buffers of one layer's packed cache, sized by okvq_buffer_bytes (torch allocations),
-    with the layer's key signs, value rotations and the decode's inverse-rotation table."""
+    with the layer's key signs, value rotations and the decode's inverse-rotation table.
+    key_meta "fp16" keeps the key window minimum and step in k_min / k_step, "mxfp4" in k_mx."""
 
     def __init__(self, batch, num_kv_heads, num_q_heads, capacity, key_signs: torch.Tensor, v_rot: torch.Tensor,
-                 device="cuda"):
-        self.dims = make_dims(batch, num_kv_heads, num_q_heads, capacity)
+                 device="cuda", key_meta="fp16"):
+        self.key_meta = key_meta
+        self.dims = make_dims(batch, num_kv_heads, num_q_heads, capacity, key_meta=key_meta)
         self.key_signs = key_signs.to(device=device, dtype=torch.int8).contiguous()
         self.v_rot = v_rot.to(device=device, dtype=torch.float32).contiguous()
         self.v_rot16 = torch.empty(ROTATION_TABLE_BYTES // 2, dtype=torch.float16, device=device)
         okvq_prepare_rotation(self.v_rot, self.v_rot16)
         self.buffers = {}
+        unused = ("k_mx",) if key_meta == "fp16" else ("k_min", "k_step")
         for i, name in enumerate(BUFFERS):
             nbytes = okvq_buffer_bytes(self.dims, i)
+            if (nbytes == 0) != (name in unused):
+                raise OkvqError(-1, f"okvq_buffer_bytes({name}) = {nbytes}")
             if nbytes == 0:
-                raise OkvqError(-1, f"okvq_buffer_bytes({name})")
+                continue
             dt = _DTYPES[name]
             n = nbytes // torch.tensor([], dtype=dt).element_size()
             self.buffers[name] = torch.zeros(n, dtype=dt, device=device)
-        self.struct = CacheStruct(self.dims, *[self.buffers[n].data_ptr() for n in BUFFERS],
-                                  self.key_signs.data_ptr(), self.v_rot.data_ptr(), self.v_rot16.data_ptr())
+        ptr = {n: (t.data_ptr() if n in self.buffers else None) for n, t in
+               ((n, self.buffers.get(n)) for n in BUFFERS)}
+        self.struct = CacheStruct(self.dims, *[ptr[n] for n in BUFFERS[:9]], self.key_signs.data_ptr(),
+                                  self.v_rot.data_ptr(), self.v_rot16.data_ptr(), ptr["k_mx"])
 
     def __getitem__(self, name):
         return self.buffers[name]
@@ -271,8 +302,12 @@ class KVCache:
         d = self.dims
         B, H, cap = d.batch, d.num_kv_heads, d.capacity
         b = self.buffers
-        return dict(k_codes=b["k_codes"].view(B, H, cap, 32), v_codes=b["v_codes"].view(B, H, cap // 32, 1024),
-                    k_norm=b["k_norm"].view(B, H, cap), v_norm=b["v_norm"].view(B, H, cap),
-                    k_min=b["k_min"].view(B, H, cap // 32, 128), k_step=b["k_step"].view(B, H, cap // 32, 128),
-                    modality=b["modality"].view(B, cap), k_stage=b["k_stage"].view(B, H, 32, 128),
-                    seq_lens=b["seq_lens"][:B])
+        v = dict(k_codes=b["k_codes"].view(B, H, cap, 32), v_codes=b["v_codes"].view(B, H, cap // 32, 1024),
+                 k_norm=b["k_norm"].view(B, H, cap), v_norm=b["v_norm"].view(B, H, cap),
+                 modality=b["modality"].view(B, cap), k_stage=b["k_stage"].view(B, H, 32, 128),
+                 seq_lens=b["seq_lens"][:B])
+        if self.key_meta == "fp16":
+            v.update(k_min=b["k_min"].view(B, H, cap // 32, 128), k_step=b["k_step"].view(B, H, cap // 32, 128))
+        else:
+            v.update(k_mx=b["k_mx"].view(B, H, cap // 32, MX_RECORD_BYTES))
+        return v

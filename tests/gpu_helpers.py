@@ -26,23 +26,30 @@ def host(t, np_dtype=None):
     return a if np_dtype is None else a.view(np_dtype)
 
 
-def quantize_stateless(k, v, modality, lens, signs, rot, capacity, num_q_heads, exact=False):
+def quantize_stateless(k, v, modality, lens, signs, rot, capacity, num_q_heads, exact=False, key_meta="fp16"):
     """Stateless key + value calls on dense blocks -> dict of numpy arrays in cache layout."""
     B, H, N, D = k.shape
-    dims = okvq.make_dims(B, H, num_q_heads, capacity)
+    dims = okvq.make_dims(B, H, num_q_heads, capacity, key_meta=key_meta)
     out = dict(
         k_codes=torch.zeros((B, H, capacity, 32), dtype=torch.uint8, device="cuda"),
         v_codes=torch.zeros((B, H, capacity // 32, 1024), dtype=torch.uint8, device="cuda"),
         k_norm=torch.zeros((B, H, capacity), dtype=torch.float16, device="cuda"),
         v_norm=torch.zeros((B, H, capacity), dtype=torch.float16, device="cuda"),
-        k_min=torch.zeros((B, H, capacity // 32, 128), dtype=torch.float16, device="cuda"),
-        k_step=torch.zeros((B, H, capacity // 32, 128), dtype=torch.float16, device="cuda"),
     )
+    if key_meta == "fp16":
+        out["k_min"] = torch.zeros((B, H, capacity // 32, 128), dtype=torch.float16, device="cuda")
+        out["k_step"] = torch.zeros((B, H, capacity // 32, 128), dtype=torch.float16, device="cuda")
+    else:
+        out["k_mx"] = torch.zeros((B, H, capacity // 32, 136), dtype=torch.uint8, device="cuda")
     kd, vd = f16dev(k), f16dev(v)
     md = dev(np.ascontiguousarray(modality, np.uint8))
     sd = dev(np.ascontiguousarray(signs, np.int8))
     rd = dev(np.ascontiguousarray(rot, np.float32))
-    okvq.okvq_quantize_keys(dims, kd, N, list(lens), sd, out["k_codes"], out["k_min"], out["k_step"], out["k_norm"])
+    if key_meta == "fp16":
+        okvq.okvq_quantize_keys(dims, kd, N, list(lens), sd, out["k_codes"], out["k_min"], out["k_step"],
+                                out["k_norm"])
+    else:
+        okvq.okvq_quantize_keys_mx(dims, kd, N, list(lens), sd, out["k_codes"], out["k_mx"], out["k_norm"])
     okvq.okvq_quantize_values(dims, vd, md, N, list(lens), rd, okvq.okvq.OKVQ_VALUE_EXACT if exact else 0,
                               out["v_codes"], out["v_norm"])
     torch.cuda.synchronize()
@@ -54,9 +61,9 @@ def quantize_stateless(k, v, modality, lens, signs, rot, capacity, num_q_heads, 
     return res
 
 
-def new_cache(B, H, Hq, capacity, signs, rot):
+def new_cache(B, H, Hq, capacity, signs, rot, key_meta="fp16"):
     return okvq.KVCache(B, H, Hq, capacity, torch.from_numpy(np.asarray(signs, np.int8)),
-                        torch.from_numpy(np.asarray(rot, np.float32)))
+                        torch.from_numpy(np.asarray(rot, np.float32)), key_meta=key_meta)
 
 
 def append_chunks(cache, k, v, modality, lens, chunk_plan, exact=False):
@@ -98,7 +105,8 @@ def decode(cache, q, lens, sm_scale=1 / math.sqrt(128)):
 def load_cache(cache, arrays, lens):
     """Copy numpy cache arrays (oracle layout) into a KVCache's device buffers."""
     views = cache.views()
-    for name in ("k_codes", "v_codes", "k_norm", "v_norm", "k_min", "k_step", "modality"):
+    meta = ("k_mx",) if "k_mx" in views else ("k_min", "k_step")
+    for name in ("k_codes", "v_codes", "k_norm", "v_norm", "modality") + meta:
         views[name].copy_(torch.from_numpy(np.ascontiguousarray(arrays[name])).to(views[name].dtype).cuda()
                           if arrays[name].dtype != np.float16 else torch.from_numpy(arrays[name]).cuda())
     views["seq_lens"].copy_(torch.from_numpy(np.asarray(lens, np.int32)).cuda())
@@ -134,16 +142,21 @@ def check_window(arrays, k16, v16, modality, signs, rot, b, h, w, length):
     """One 32-token window of a GPU-written cache against the oracle: key fields bit-exact, value
     norms bit-exact, value codes by the band rule, padded slots zero. ``length`` is the sequence
     length; k16 / v16 / modality are the sequence's full inputs."""
-    from oracle.keys import quantize_keys_fmt
-    from oracle.layout import pack_keys, unpack_values
+    from oracle.keys import quantize_keys_fmt, quantize_keys_mx_fmt
+    from oracle.layout import pack_keys, pack_mx_meta, unpack_values
     from oracle.values import quantize_values_fmt
     a = 32 * w
     n = min(32, length - a)
     assert n > 0
-    kq = quantize_keys_fmt(k16[a:a + n], n, signs)
+    if "k_mx" in arrays:
+        kq = quantize_keys_mx_fmt(k16[a:a + n], n, signs)
+        np.testing.assert_array_equal(arrays["k_mx"][b, h, w],
+                                      pack_mx_meta(kq["m_codes"], kq["s_codes"], kq["m_scale"], kq["s_scale"])[0])
+    else:
+        kq = quantize_keys_fmt(k16[a:a + n], n, signs)
+        np.testing.assert_array_equal(arrays["k_min"][b, h, w].view(np.uint16), kq["m16"][0].view(np.uint16))
+        np.testing.assert_array_equal(arrays["k_step"][b, h, w].view(np.uint16), kq["step16"][0].view(np.uint16))
     np.testing.assert_array_equal(arrays["k_norm"][b, h, a:a + n].view(np.uint16), kq["n16"][:n].view(np.uint16))
-    np.testing.assert_array_equal(arrays["k_min"][b, h, w].view(np.uint16), kq["m16"][0].view(np.uint16))
-    np.testing.assert_array_equal(arrays["k_step"][b, h, w].view(np.uint16), kq["step16"][0].view(np.uint16))
     np.testing.assert_array_equal(arrays["k_codes"][b, h, a:a + n], pack_keys(kq["codes"][:n]))
     vq = quantize_values_fmt(v16[a:a + n], modality[a:a + n], rot, n)
     np.testing.assert_array_equal(arrays["v_norm"][b, h, a:a + n].view(np.uint16), vq["n16"].view(np.uint16))

@@ -107,7 +107,42 @@ def test_invalid_arguments_rejected_before_any_launch():
     assert L.okvq_prepare_rotation(fake, ctypes.c_void_p(4098), None) == -1
 
 
-@pytest.mark.parametrize("which", range(9))
+def test_mxfp4_metadata_buffers_and_validation():
+    """MXFP4 key metadata: 136-byte window records instead of fp16 minimum / step (Tab. 3's 2.258
+    bits per element); each metadata format is accepted only by its own entry points."""
+    okvq = _lib()
+    L = okvq.lib()
+    d = okvq.make_dims(2, 4, 28, 32768, key_meta="mxfp4")
+    names = {0: "k_codes", 1: "v_codes", 2: "k_norm", 3: "v_norm", 9: "k_mx"}
+    total = sum(okvq.okvq_buffer_bytes(d, i) for i in names)
+    elems = 2 * 4 * 32768 * 128 * 2
+    assert total == 2 * 4 * 32768 * 72.25
+    assert abs(total * 8 / elems - bits_per_element("ours_mxfp4_meta")) < 1e-12
+    assert okvq.okvq_buffer_bytes(d, 4) == 0 and okvq.okvq_buffer_bytes(d, 5) == 0
+    assert okvq.okvq_buffer_bytes(d, 9) == 2 * 4 * 1024 * 136
+    assert okvq.okvq_buffer_bytes(okvq.make_dims(2, 4, 28, 32768), 9) == 0
+    fake = ctypes.c_void_p(4096)
+    lens = (ctypes.c_int32 * 2)(10, 10)
+    mx_dims = okvq.make_dims(2, 2, 8, 64, key_meta="mxfp4")
+    fp_dims = okvq.make_dims(2, 2, 8, 64)
+    bad = okvq.make_dims(2, 2, 8, 64)
+    bad.key_meta = 2
+    assert L.okvq_quantize_keys(ctypes.byref(bad), fake, 10, lens, fake, fake, fake, fake, fake, None) == -1
+    assert L.okvq_quantize_keys(ctypes.byref(mx_dims), fake, 10, lens, fake, fake, fake, fake, fake, None) == -1
+    assert L.okvq_quantize_keys_mx(ctypes.byref(fp_dims), fake, 10, lens, fake, fake, fake, fake, None) == -1
+    assert L.okvq_quantize_keys_mx(ctypes.byref(mx_dims), fake, 10, lens, fake, fake, ctypes.c_void_p(4100), fake,
+                                   None) == -1
+    q_lens = (ctypes.c_int32 * 2)(64, 64)
+    # an MXFP4 cache needs k_mx (k_min / k_step may be null); an fp16 cache needs k_min / k_step
+    no_mx = okvq.CacheStruct(mx_dims, *([4096] * 4), 0, 0, *([4096] * 3), 4096, 4096, 4096, 0)
+    assert L.okvq_decode_attention(ctypes.byref(no_mx), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, 1 << 30,
+                                   None) == -1
+    no_min = okvq.CacheStruct(fp_dims, *([4096] * 4), 0, 0, *([4096] * 3), 4096, 4096, 4096, 4096)
+    assert L.okvq_decode_attention(ctypes.byref(no_min), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, 1 << 30,
+                                   None) == -1
+
+
+@pytest.mark.parametrize("which", range(10))
 def test_buffer_bytes_invalid_dims(which):
     okvq = _lib()
     assert okvq.okvq_buffer_bytes(okvq.make_dims(1, 1, 1, 33), which) == 0
