@@ -22,15 +22,17 @@ Reported (one JSON line):
                   update)
   kernels_us      mean duration of each launch, from the same events
   cpu_baseline    the float64 CPU oracle's decode on the same cache, on this host
+  mxfp4           the same workload with MXFP4 key window metadata (72.25 instead of 84 bytes per
+                  token and KV head): append, decode and split-K kernel time, effective GB/s
 
 --profile-pass runs a short fixed sequence for rocprofv3 counter collection: a 256 MiB device
 copy (calibrates FETCH_SIZE / WRITE_SIZE against a known byte count), 8 decode calls on cold
-cache replicas and 2 prefill appends.
+cache replicas and 2 prefill appends, then the same with MXFP4 key metadata.
 
 --shape-scan times decode alone at the other workload shapes (batch 16 with ragged lengths up to
 16384, batch 4 x 65536 with 2 KV heads and 16 query heads, 131072 tokens with 32 query heads, and
-batch 32 x 32768), one JSON line each, on caches filled with random codes and metadata (the
-kernel's work does not depend on the values).
+batch 32 x 32768), with fp16 and with MXFP4 key metadata, one JSON line each, on caches filled with
+random codes and metadata (the kernel's work does not depend on the values).
 """
 
 from __future__ import annotations
@@ -51,6 +53,9 @@ HBM_PEAK_GBPS = 8000.0
 WORKLOAD = "omni7b_32k"
 DECODE_BYTES_PER_WINDOW_HEAD = 2 * 1024 + 2 * 64 + 2 * 256   # codes K, V + norms K, V + min/step
 APPEND_BYTES_PER_TOKEN_HEAD = 2 * 256 + 84                   # read K, V fp16; write the packed cache
+MX_RECORD = 136                                              # MXFP4 min/step record of one window
+DECODE_BYTES_PER_WINDOW_HEAD_MX = 2 * 1024 + 2 * 64 + MX_RECORD
+APPEND_BYTES_PER_TOKEN_HEAD_MX = 2 * 256 + 68 + MX_RECORD / 32
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
 CALIBRATION_COPY_BYTES = 256 << 20
 KERNEL_SOURCES = ("codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "key_quant.hpp", "value_quant.hpp",
@@ -65,16 +70,18 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def decode_algorithmic_bytes(B, H, Hq, lens, with_output=True):
+def decode_algorithmic_bytes(B, H, Hq, lens, with_output=True, key_meta="fp16"):
     nwin = sum(-(-int(L) // 32) for L in lens)
-    return (nwin * H * DECODE_BYTES_PER_WINDOW_HEAD + nwin * 32      # cache + modality map
+    per_win = DECODE_BYTES_PER_WINDOW_HEAD if key_meta == "fp16" else DECODE_BYTES_PER_WINDOW_HEAD_MX
+    return (nwin * H * per_win + nwin * 32                            # cache + modality map
             + B * Hq * 128 * (2 + (4 if with_output else 0))          # q in, out
             + 3 * 128 * 128 * 4)                                      # rotations
 
 
-def append_algorithmic_bytes(B, H, lens):
+def append_algorithmic_bytes(B, H, lens, key_meta="fp16"):
     n = sum(int(L) for L in lens)
-    return n * H * APPEND_BYTES_PER_TOKEN_HEAD + 2 * n + 3 * 128 * 128 * 4 + 128
+    per_tok = APPEND_BYTES_PER_TOKEN_HEAD if key_meta == "fp16" else APPEND_BYTES_PER_TOKEN_HEAD_MX
+    return int(n * H * per_tok) + 2 * n + 3 * 128 * 128 * 4 + 128
 
 
 def measured_traffic(kernel_key):
@@ -109,55 +116,127 @@ def cpu_baseline(cache_np, q, lens, signs, rot, bytes_per_call, min_seconds=10.0
                        f"tokens), float64, {el:.1f} s")
 
 
-def shape_scan(okvq, torch, np, workload, gen_lengths):
-    """Decode alone at larger shapes: per-call time over cycled cache replicas, effective GB/s."""
+def _scan_case(okvq, torch, name, B, lens, H, Hq, key_meta):
+    """Decode alone on random caches of one shape: per-call time over cycled replicas, effective GB/s."""
     dev = torch.device("cuda:0")
     sm = 1 / math.sqrt(128)
+    cap = (max(lens) + 31) // 32 * 32
+    dims = okvq.make_dims(B, H, Hq, cap, key_meta=key_meta)
+    per_cache = sum(okvq.okvq_buffer_bytes(dims, i) for i in range(10))
+    reps = max(2, min(16, int(math.ceil(1.05e9 / per_cache))))
+    g = torch.Generator(device=dev).manual_seed(7)
+    caches = []
+    for r in range(reps):
+        c = okvq.KVCache(B, H, Hq, cap, torch.ones(128, dtype=torch.int8), torch.eye(128).repeat(3, 1, 1), device=dev,
+                         key_meta=key_meta)
+        for n, t in c.buffers.items():
+            if n == "seq_lens":
+                t[:B].copy_(torch.tensor(lens, dtype=torch.int32))
+            elif n == "modality":
+                t.random_(0, 3, generator=g)
+            elif t.dtype == torch.float16:
+                t.copy_((torch.rand(t.shape, device=dev, generator=g) * 0.5 + 0.1).half())
+            elif t.dtype == torch.uint8:
+                t.random_(0, 256, generator=g)
+        if key_meta == "mxfp4":  # block scales of ordinary key statistics (2^-4)
+            c.views()["k_mx"][..., 128:].fill_(123)
+        caches.append(c)
+    q = torch.randn(B, Hq, 128, device=dev, generator=g).half()
+    ws = okvq.decode_workspace(caches[0].dims, max(lens), device=dev)
+    out = torch.empty(B, Hq, 128, device=dev)
+    for i in range(10):
+        okvq.okvq_decode_attention(caches[i % reps], lens, q, sm, out, ws)
+    torch.cuda.synchronize()
+    n = 100
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(n):
+        okvq.okvq_decode_attention(caches[i % reps], lens, q, sm, out, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / n
+    nbytes = decode_algorithmic_bytes(B, H, Hq, lens, key_meta=key_meta)
+    print(json.dumps({"shape_scan": name, "key_meta": key_meta, "batch": B, "kv_heads": H, "q_heads": Hq,
+                      "max_len": max(lens), "decode_us": round(us, 2), "algorithmic_MB": round(nbytes / 1e6, 2),
+                      "GBps": round(nbytes / us / 1e3, 1), "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBPS, 4)}),
+          flush=True)
+
+
+def shape_scan(okvq, torch, workload, gen_lengths):
+    """Decode alone at the other workload shapes, with fp16 and with MXFP4 key metadata."""
     cases = [("omni7b_b16_ragged16k", None), ("omni3b_b4_64k_stream", None), ("omni30b_128k_48layer", None),
              ("omni7b_32k", 32)]
     for name, batch in cases:
         wl = workload(name)
         B = batch or wl.batch
         lens = [int(x) for x in gen_lengths(wl)] if batch is None else [wl.seq_len] * B
-        H, Hq = wl.num_kv_heads, wl.num_q_heads
-        cap = (max(lens) + 31) // 32 * 32
-        dims = okvq.make_dims(B, H, Hq, cap)
-        per_cache = sum(okvq.okvq_buffer_bytes(dims, i) for i in range(9))
-        reps = max(2, min(16, int(math.ceil(1.05e9 / per_cache))))
-        g = torch.Generator(device=dev).manual_seed(7)
-        caches = []
-        for r in range(reps):
-            c = okvq.KVCache(B, H, Hq, cap, torch.ones(128, dtype=torch.int8), torch.eye(128).repeat(3, 1, 1), device=dev)
-            for n, t in c.buffers.items():
-                if n == "seq_lens":
-                    t[:B].copy_(torch.tensor(lens, dtype=torch.int32))
-                elif n == "modality":
-                    t.random_(0, 3, generator=g)
-                elif t.dtype == torch.float16:
-                    t.copy_((torch.rand(t.shape, device=dev, generator=g) * 0.5 + 0.1).half())
-                elif t.dtype == torch.uint8:
-                    t.random_(0, 256, generator=g)
-            caches.append(c)
-        q = torch.randn(B, Hq, 128, device=dev, generator=g).half()
-        ws = okvq.decode_workspace(caches[0].dims, max(lens), device=dev)
-        out = torch.empty(B, Hq, 128, device=dev)
-        for i in range(10):
-            okvq.okvq_decode_attention(caches[i % reps], lens, q, sm, out, ws)
-        torch.cuda.synchronize()
-        n = 100
+        for km in ("fp16", "mxfp4"):
+            _scan_case(okvq, torch, name, B, lens, wl.num_kv_heads, wl.num_q_heads, km)
+
+
+def mx_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream, decode_iters):
+    """The benchmark workload with MXFP4 key window metadata (the paper's default storage): prefill
+    append into an empty cache, decode over >= 1 GB of cold cache replicas, and the split-K kernel's
+    duration from events bound to its dispatch."""
+    B, H, Hq, N = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.seq_len
+    dev = q.device
+    sm = 1 / math.sqrt(128)
+    dims = okvq.make_dims(B, H, Hq, wl.capacity, key_meta="mxfp4")
+    per_cache = sum(okvq.okvq_buffer_bytes(dims, i) for i in range(10))
+    n_cache = max(16, int(math.ceil(1.05e9 / per_cache)))
+    caches = [okvq.KVCache(B, H, Hq, wl.capacity, torch.ones(128, dtype=torch.int8), torch.eye(128).repeat(3, 1, 1),
+                           device=dev, key_meta="mxfp4") for _ in range(n_cache)]
+    okvq.okvq_append(caches[0], [0] * B, k_in[0], v_in[0], m0, lens, n_new_dev, N, stream=stream)
+    torch.cuda.synchronize()
+    for c in caches[1:]:
+        for name in c.buffers:
+            c.buffers[name].copy_(caches[0].buffers[name])
+    ws = okvq.decode_workspace(dims, max(lens), device=dev)
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+    # appends (prefill into an emptied replica, inputs cycled)
+    app = []
+    for i in range(12):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for i in range(n):
-            okvq.okvq_decode_attention(caches[i % reps], lens, q, sm, out, ws)
-        e1.record()
+        c = caches[(i + 1) % n_cache]
+        c.buffers["seq_lens"].zero_()
+        e0.record(stream)
+        okvq.okvq_append(c, [0] * B, k_in[i % len(k_in)], v_in[i % len(v_in)], m0, lens, n_new_dev, N, stream=stream)
+        e1.record(stream)
+        app.append((e0, e1))
+    torch.cuda.synchronize()
+    append_us = float(np.mean([a.elapsed_time(b) for a, b in app[2:]])) * 1e3
+    reps = []
+    for rep in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for i in range(20):
+            okvq.okvq_decode_attention(caches[i % n_cache], lens, q, sm, out, ws, stream=stream)
+        e0.record(stream)
+        for i in range(decode_iters):
+            okvq.okvq_decode_attention(caches[(i * 7 + rep) % n_cache], lens, q, sm, out, ws, stream=stream)
+        e1.record(stream)
         torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) * 1e3 / n
-        nbytes = decode_algorithmic_bytes(B, H, Hq, lens)
-        print(json.dumps({"shape_scan": name, "batch": B, "kv_heads": H, "q_heads": Hq, "max_len": max(lens),
-                          "decode_us": round(us, 2), "algorithmic_MB": round(nbytes / 1e6, 2),
-                          "GBps": round(nbytes / us / 1e3, 1), "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBPS, 4)}),
-              flush=True)
-        del caches
+        reps.append(e0.elapsed_time(e1) * 1e3 / decode_iters)
+    decode_us = float(np.median(reps))
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(decode_iters)]
+    for e4 in evs:
+        for e in e4:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for i in range(decode_iters):
+        okvq.okvq_decode_attention_timed(caches[(i * 7 + 5) % n_cache], lens, q, sm, out, ws, evs[i], stream=stream)
+    torch.cuda.synchronize()
+    split_us = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) * 1e3
+    dbytes = decode_algorithmic_bytes(B, H, Hq, lens, key_meta="mxfp4")
+    sbytes = decode_algorithmic_bytes(B, H, Hq, lens, with_output=False, key_meta="mxfp4")
+    abytes = append_algorithmic_bytes(B, H, lens, key_meta="mxfp4")
+    del caches
+    return {"bytes_per_token_head": 72.25, "decode_us": round(decode_us, 3),
+            "decode_GBps": round(dbytes / decode_us / 1e3, 2),
+            "k_decode_us": round(split_us, 3), "k_decode_GBps": round(sbytes / split_us / 1e3, 2),
+            "k_decode_frac": round(sbytes / split_us / 1e3 / HBM_PEAK_GBPS, 4), "traffic": measured_traffic("k_decode_mx"),
+            "append_us": round(append_us, 3), "append_GBps": round(abytes / append_us / 1e3, 2),
+            "append_frac": round(abytes / append_us / 1e3 / HBM_PEAK_GBPS, 4), "algorithmic_bytes": dbytes,
+            "replicas": n_cache}
 
 
 def main():
@@ -182,7 +261,7 @@ def main():
     from synth import gen_layer, gen_lengths, gen_queries, workload
 
     if args.shape_scan:
-        shape_scan(okvq, torch, np, workload, gen_lengths)
+        shape_scan(okvq, torch, workload, gen_lengths)
         return
 
     wl = workload(WORKLOAD)
@@ -204,7 +283,7 @@ def main():
     n_new_dev = torch.tensor(lens, dtype=torch.int32, device=dev)
 
     # cache replicas (>= 1 GB of packed caches so that decode reads come from HBM)
-    per_cache = sum(okvq.okvq_buffer_bytes(okvq.make_dims(B, H, Hq, wl.capacity), i) for i in range(9))
+    per_cache = sum(okvq.okvq_buffer_bytes(okvq.make_dims(B, H, Hq, wl.capacity), i) for i in range(10))
     n_cache = max(16, int(math.ceil(1.05e9 / per_cache)))
     caches = [okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev) for _ in range(n_cache)]
     okvq.okvq_append(caches[0], [0] * B, k_in[0], v_in[0], m0, lens, n_new_dev, N)
@@ -236,9 +315,26 @@ def main():
         for i in range(2):
             append_into((i + 1) % n_cache, (i + 1) % n_in)
         torch.cuda.synchronize()
+        # the same with MXFP4 key metadata
+        mx = [okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev, key_meta="mxfp4") for _ in range(16)]
+        okvq.okvq_append(mx[0], [0] * B, k_in[0], v_in[0], m0, lens, n_new_dev, N, stream=stream)
+        torch.cuda.synchronize()
+        for c in mx[1:]:
+            for name in c.buffers:
+                c.buffers[name].copy_(mx[0].buffers[name])
+        ws_mx = okvq.decode_workspace(mx[0].dims, max(lens), device=dev)
+        torch.cuda.synchronize()
+        for i in range(8):
+            okvq.okvq_decode_attention(mx[(7 * i + 3) % 16], lens, q, sm, out, ws_mx, stream=stream)
+        torch.cuda.synchronize()
+        for i in range(2):
+            mx[i + 1].buffers["seq_lens"].zero_()
+            okvq.okvq_append(mx[i + 1], [0] * B, k_in[i + 1], v_in[i + 1], m0, lens, n_new_dev, N, stream=stream)
+        torch.cuda.synchronize()
         print(json.dumps({"profile_pass": True, "copy_bytes": CALIBRATION_COPY_BYTES, "decode_calls": 8,
                           "append_calls": 2, "decode_algorithmic_bytes": decode_algorithmic_bytes(B, H, Hq, lens),
-                          "append_algorithmic_bytes": append_algorithmic_bytes(B, H, lens)}), flush=True)
+                          "append_algorithmic_bytes": append_algorithmic_bytes(B, H, lens),
+                          "mxfp4_decode_calls": 8, "mxfp4_append_calls": 2}), flush=True)
         return
 
     # ---- steps: append the prefill into cache replica s, decode a cold replica ----
@@ -341,6 +437,8 @@ def main():
                             "algorithmic_bytes": abytes},
         "cache_replicas": n_cache,
     }
+    line["mxfp4"] = mx_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
+                                   args.decode_iters)
     if not args.no_cpu_baseline:
         cache_np = {n: t.cpu().numpy() for n, t in caches[0].views().items()}
         line["cpu_baseline"] = cpu_baseline(cache_np, q.cpu().numpy(), np.asarray(lens), lay["signs"], lay["rot"],
