@@ -127,7 +127,7 @@ def quantize_keys_fmt(k16: np.ndarray, length: int, signs: np.ndarray, window: i
 
 
 def quantize_keys_mx_fmt(k16: np.ndarray, length: int, signs: np.ndarray, window: int = WINDOW):
-    """The key codec with MXFP4 window metadata (readings R16-R19 of ``oracle.mxfp4``).
+    """The key codec with MXFP4 window metadata (readings R18-R21 of ``oracle.mxfp4``).
 
     Per window: lo = min z + 0, hi = max z + 0, step = fl(fl(hi - lo) / 3) in fp32 as in the fp16
     variant; the 128-vectors lo and step are stored as MXFP4 (4 blocks of 32 channels each) and

@@ -13,14 +13,14 @@ Conversion of a block V (the published MX definition, written out):
   V_i ~ P_i * 2^e
 
 Readings (the paper says only "MXFP4 metadata"):
-* R16 -- a block is 32 consecutive channels of one window's minimum vector (or of its step
+* R18 -- a block is 32 consecutive channels of one window's minimum vector (or of its step
   vector): 4 blocks per window and field, so a window's metadata is final when the window is;
-* R17 -- an all-zero block gets e = -127 and zero elements; a negative value that rounds to
+* R19 -- an all-zero block gets e = -127 and zero elements; a negative value that rounds to
   zero keeps its sign (code 8, -0);
-* R18 -- the key codes are computed against the dequantized minimum and step (what a reader
+* R20 -- the key codes are computed against the dequantized minimum and step (what a reader
   of the cache reconstructs), with the FMT order of the fp16 variant: code = 0 if step == 0,
   else clamp(rint(fl(fl(z - m) * fl(1 / step))), 0, 3);
-* R19 -- the quantity stored is the step (max - min) / 3 in fp32, as in the fp16 variant.
+* R21 -- the quantity stored is the step (max - min) / 3 in fp32, as in the fp16 variant.
 
 Everything here is a plain statement of the definition: the E2M1 value set is built from its
 bit fields and rounding is a brute-force nearest-value search.
