@@ -121,7 +121,8 @@ __device__ __forceinline__ void rewrite_stage(const CodecJob& j, const TileCtx& 
   const int open = (c.len / kW) * kW;
   if (open >= c.len) return;  // (the stage reads of this tile have landed: raw was read from them)
   const int lane = lane_id(), tok = tok0 + lane;
-  const int slot = lane & 31;
+  int slot = lane & 31;
+  __asm__ volatile("" : "+v"(slot));  // keeps the lane's stage-row offset from living across the tile loop
   uint16_t* dst = j.stage + (c.seq * kW + slot) * kD;
   if (open < tok0 + 64) {
     if (tok >= open && tok < c.len) {

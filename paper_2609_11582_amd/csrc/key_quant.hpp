@@ -30,6 +30,17 @@ struct KeyWaveOut {
   uint16_t* knorm; // [cap]
 };
 
+// Lane l <- lane l ^ m for m = 1, 2 (DPP quad permutations) or 4 (LDS-pipe swizzle in xor mode):
+// no address registers, unlike a general shuffle.
+template <int kMask>
+__device__ __forceinline__ float xor_lanes(float v) {
+  const int x = __builtin_bit_cast(int, v);
+  if constexpr (kMask == 1) return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xf, 0xf, false));
+  if constexpr (kMask == 2) return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xf, 0xf, false));
+  static_assert(kMask == 1 || kMask == 2 || kMask == 4, "xor of lane bit 0, 1 or 2");
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(x, (kMask << 10) | 0x1f));
+}
+
 // Sign-flip masks for an fp16 pair (channels c, c+1) from the 32 sign words (4 int8 signs each).
 __device__ __forceinline__ uint32_t sign_pair_mask(const uint32_t (&sw)[32], int c) {
   const uint32_t w = sw[c >> 2];
@@ -153,11 +164,12 @@ __device__ __forceinline__ void key_quantize_rows(float (&x)[kD], uint32_t n16, 
         am = fmaxf(am, fabsf(lo[i]));
         as = fmaxf(as, hi[i]);
       }
-#pragma unroll
-      for (int lb = 1; lb < 8; lb <<= 1) {
-        am = fmaxf(am, __shfl_xor(am, lb));
-        as = fmaxf(as, __shfl_xor(as, lb));
-      }
+      am = fmaxf(am, xor_lanes<1>(am));
+      as = fmaxf(as, xor_lanes<1>(as));
+      am = fmaxf(am, xor_lanes<2>(am));
+      as = fmaxf(as, xor_lanes<2>(as));
+      am = fmaxf(am, xor_lanes<4>(am));
+      as = fmaxf(as, xor_lanes<4>(as));
       const int em = mx_exponent(am), es = mx_exponent(as);
       uint32_t word = 0;
 #pragma unroll
@@ -169,10 +181,16 @@ __device__ __forceinline__ void key_quantize_rows(float (&x)[kD], uint32_t n16, 
         hi[i] = (sv == 0.0f) ? 0.0f : div_rn(1.0f, sv);
       }
       if (half == 0 && nvalid > 0) {
-        uint8_t* rec = out.kmx + (size_t)gwin * kMxRecord;
-        *reinterpret_cast<uint32_t*>(rec + 4 * (16 * q + qd)) = word;
-        if ((qd & 7) == 0)
-          *reinterpret_cast<uint16_t*>(rec + 128 + 2 * (2 * q + (qd >> 3))) = (uint16_t)((em + 127) | ((es + 127) << 8));
+        // 32-bit record offsets, opaque so that their lane parts are not kept live (as 64-bit
+        // values) across the tile loop
+        uint32_t off = (uint32_t)gwin * kMxRecord + 4u * (16 * q + qd);
+        __asm__ volatile("" : "+v"(off));
+        *reinterpret_cast<uint32_t*>(out.kmx + off) = word;
+        if ((qd & 7) == 0) {
+          uint32_t soff = (uint32_t)gwin * kMxRecord + 128u + 2u * (2 * q + (qd >> 3));
+          __asm__ volatile("" : "+v"(soff));
+          *reinterpret_cast<uint16_t*>(out.kmx + soff) = (uint16_t)((em + 127) | ((es + 127) << 8));
+        }
         float4* sp = reinterpret_cast<float4*>(stats + (win * kD + 64 * q + 4 * qd) * 2);
         sp[0] = make_float4(lo[0], hi[0], lo[1], hi[1]);
         sp[1] = make_float4(lo[2], hi[2], lo[3], hi[3]);
@@ -190,7 +208,8 @@ __device__ __forceinline__ void key_quantize_rows(float (&x)[kD], uint32_t n16, 
         st[2 * i] = h2f(m16[i]);
         st[2 * i + 1] = (s16[i] == 0) ? 0.0f : div_rn(1.0f, h2f(s16[i]));
       }
-      const int c = 64 * q + 4 * qd;
+      int c = 64 * q + 4 * qd;
+      __asm__ volatile("" : "+v"(c));  // keeps the lane's channel offset from living across the tile loop
       *reinterpret_cast<uint2*>(out.kmin + gwin * kD + c) = make_uint2(m16[0] | (m16[1] << 16), m16[2] | (m16[3] << 16));
       *reinterpret_cast<uint2*>(out.kstep + gwin * kD + c) = make_uint2(s16[0] | (s16[1] << 16), s16[2] | (s16[3] << 16));
       float4* sp = reinterpret_cast<float4*>(stats + (win * kD + c) * 2);
