@@ -64,6 +64,15 @@
  * Key codes are then computed against the dequantized minimum m and step s (code 0 where s is
  * zero, else clamp(rint(fl(fl(z - m) * fl(1 / s))), 0, 3)). Storage: 72.25 bytes per token per
  * KV head, 2.258 bits per element.
+ *
+ * fp16 residual of the captioning protocol (dims.residual = OKVQ_RESIDUAL_TOKENS, Sec. 3.1: keys
+ * quantized every 128 tokens in groups of 32, values kept in a 128-token fp16 window before they
+ * are quantized). Two more buffers hold the raw rows of the last 128 tokens:
+ *   k_res    f16 [B][H][128][128]     key of token i in row i % 128
+ *   v_res    f16 [B][H][128][128]     value of token i in row i % 128
+ * Append still writes codes for every token (a window's key codes do not depend on when it is
+ * quantized, value codes are per token); decode at length L reads key i quantized if
+ * i < 128 floor(L / 128), else from k_res, and value i quantized if i < L - 128, else from v_res.
  */
 #ifndef OKVQ_H
 #define OKVQ_H
@@ -98,13 +107,18 @@ enum {
   OKVQ_KEY_META_MXFP4 = 1 /* MXFP4 records in k_mx (72.25 bytes per token per KV head)    */
 };
 
+/* okvq_dims.residual: 0 (every token read quantized) or the fp16 window of the captioning
+ * protocol (Sec. 3.1) */
+#define OKVQ_RESIDUAL_TOKENS 128
+
 /* bytes of the prepared rotation tables (okvq_cache.v_rot16, okvq_prepare_rotation) */
 #define OKVQ_ROTATION_TABLE_BYTES 294912
 
 /* which_buffer for okvq_buffer_bytes */
 enum {
   OKVQ_BUF_K_CODES = 0, OKVQ_BUF_V_CODES, OKVQ_BUF_K_NORM, OKVQ_BUF_V_NORM, OKVQ_BUF_K_MIN,
-  OKVQ_BUF_K_STEP, OKVQ_BUF_MODALITY, OKVQ_BUF_K_STAGE, OKVQ_BUF_SEQ_LENS, OKVQ_BUF_K_MX, OKVQ_NUM_BUFFERS
+  OKVQ_BUF_K_STEP, OKVQ_BUF_MODALITY, OKVQ_BUF_K_STAGE, OKVQ_BUF_SEQ_LENS, OKVQ_BUF_K_MX, OKVQ_BUF_K_RES,
+  OKVQ_BUF_V_RES, OKVQ_NUM_BUFFERS
 };
 
 typedef struct {
@@ -115,6 +129,7 @@ typedef struct {
   int32_t window;       /* key group size, must be 32 (Sec. 3.1)    */
   int32_t capacity;     /* token slots per sequence, multiple of 32 */
   int32_t key_meta;     /* OKVQ_KEY_META_FP16 or OKVQ_KEY_META_MXFP4 */
+  int32_t residual;     /* 0 or OKVQ_RESIDUAL_TOKENS (fp16 window)  */
 } okvq_dims;
 
 typedef struct {               /* all pointers are device memory, laid out as above; k_min and
@@ -137,6 +152,9 @@ typedef struct {               /* all pointers are device memory, laid out as ab
                                   modality (Sec. 2.3), then the forward rotation of append in
                                   the operand layout of its matrix-core kernel              */
   uint8_t* k_mx;               /* [B][H][cap/32][136] MXFP4 key metadata records            */
+  uint16_t* k_res;             /* [B][H][128][128] fp16 keys of the last 128 tokens (residual
+                                  mode, else may be NULL)                                     */
+  uint16_t* v_res;             /* [B][H][128][128] fp16 values of the last 128 tokens        */
 } okvq_cache;
 
 /* Library version (major * 10000 + minor * 100 + patch). */
@@ -146,7 +164,8 @@ int32_t okvq_version(void);
 const char* okvq_status_string(okvq_status status);
 
 /* Bytes of one cache buffer for `dims` (0 for an unknown buffer, invalid dims, or a buffer the
- * metadata format of dims does not use: k_min / k_step with MXFP4, k_mx with fp16). */
+ * metadata format of dims does not use: k_min / k_step with MXFP4, k_mx with fp16, k_res / v_res
+ * without the residual). */
 size_t okvq_buffer_bytes(const okvq_dims* dims, int32_t which_buffer);
 
 /* Fixed Gaussian codebook of Eq. 3 as used by the kernels: the 4 levels and 3 decision
@@ -200,7 +219,9 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
  * cache->seq_lens[b] is advanced by n_new[b] on the device. Fails with OKVQ_ERR_CAPACITY if
  * lens_host[b] + n_new_host[b] > capacity. The MFMA-mode values read the forward rotation from
  * cache->v_rot16 (okvq_prepare_rotation); OKVQ_VALUE_EXACT reads cache->v_rot. The key window
- * metadata is written in the format of cache->dims.key_meta (k_min / k_step, or k_mx). */
+ * metadata is written in the format of cache->dims.key_meta (k_min / k_step, or k_mx). With the
+ * residual, the raw key and value rows of the new tokens among the last 128 of each sequence are
+ * also written to k_res and v_res (one more launch, before the codec). */
 okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
                         const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
                         const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream);
@@ -229,7 +250,10 @@ size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len);
  *   out        device f32 [B][Hq][128]
  *   workspace  device, at least okvq_decode_workspace_bytes(dims, max(lens_host)) bytes
  * Needs cache->v_rot16 (okvq_prepare_rotation); reads the key window metadata in the format of
- * cache->dims.key_meta. A sequence of length 0 yields zeros. fp32
+ * cache->dims.key_meta. With the residual (captioning protocol, Sec. 3.1) the split-K launch covers
+ * the tokens below L - 128, and the merge launch also attends the last min(L, 128) tokens -- keys
+ * below 128 floor(L / 128) dequantized, the others and all values in fp16 from k_res / v_res --
+ * and merges them in. A sequence of length 0 yields zeros. fp32
  * accumulation; the result matches float64 attention over the dequantized cache within 2e-3 of
  * the output norm. */
 okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,

@@ -55,3 +55,22 @@ def decode_residual(q16, kc, m, st, nk, vc, nv, modality, k16, v16, length, sign
     if vq:
         vhat[:vq] = dequantize_values(vc[:vq], nv[:vq], modality[:vq], rot)
     return np.stack([softmax_attention(q16[j], khat, vhat, sm_scale) for j in range(group)])
+
+
+def decode_layer_residual(cache, k16, v16, q16, lens, signs, rot, sm_scale, window: int = RESIDUAL):
+    """fp64 outputs [B][Hq][d] of one decode step over a packed cache with the fp16 residual.
+
+    cache: packed buffers (as built by ``oracle.cache.quantize_layer`` or read back from the
+    device); k16, v16 [B][H][>= max(lens)][d]: the fp16 keys and values the cache was built from."""
+    from .cache import unpacked_fields
+    B, Hq, D = q16.shape
+    H = cache["k_codes"].shape[1]
+    G = Hq // H
+    out = np.zeros((B, Hq, D))
+    for b in range(B):
+        for h in range(H):
+            kc, m, st, nk, vc, nv, mod = unpacked_fields(cache, b, h)
+            out[b, h * G:(h + 1) * G] = decode_residual(q16[b, h * G:(h + 1) * G], kc, m, st, nk, vc, nv, mod,
+                                                        k16[b, h], v16[b, h], lens[b], signs, rot, sm_scale, G,
+                                                        window=window)
+    return out

@@ -10,7 +10,7 @@ using namespace okvq;
 
 namespace {
 
-constexpr int32_t kVersion = 200;  // 0.2.0: MXFP4 key metadata
+constexpr int32_t kVersion = 300;  // 0.3.0: fp16 residual of the captioning protocol
 
 // ---- fixed Gaussian codebook (Sec. 2.1, Eq. 3): Lloyd-Max quantizer of N(0, 1), 4 levels ----
 double phi(double x) { return std::isinf(x) ? 0.0 : std::exp(-0.5 * x * x) / std::sqrt(2.0 * M_PI); }
@@ -73,6 +73,7 @@ okvq_status check_dims(const okvq_dims* d) {
   if (d->capacity < 32 || d->capacity % 32 != 0) return OKVQ_ERR_INVALID_ARGUMENT;
   if (d->batch > 65535 || d->num_kv_heads > 65535) return OKVQ_ERR_UNSUPPORTED;
   if (d->key_meta != OKVQ_KEY_META_FP16 && d->key_meta != OKVQ_KEY_META_MXFP4) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (d->residual != 0 && d->residual != OKVQ_RESIDUAL_TOKENS) return OKVQ_ERR_INVALID_ARGUMENT;
   return OKVQ_OK;
 }
 
@@ -88,6 +89,7 @@ okvq_status check_cache(const okvq_cache* c) {
     if (!aligned16(p)) return OKVQ_ERR_INVALID_ARGUMENT;
   if (is_mx(&c->dims) ? !aligned16(c->k_mx) : (!aligned16(c->k_min) || !aligned16(c->k_step)))
     return OKVQ_ERR_INVALID_ARGUMENT;
+  if (c->dims.residual && (!aligned16(c->k_res) || !aligned16(c->v_res))) return OKVQ_ERR_INVALID_ARGUMENT;
   return OKVQ_OK;
 }
 
@@ -110,6 +112,9 @@ CacheView view(const okvq_cache* c) {
   v.signs = c->key_signs;
   v.rot = c->v_rot;
   v.rot16t = c->v_rot16;
+  v.residual = c->dims.residual;
+  v.k_res = c->dims.residual ? c->k_res : nullptr;
+  v.v_res = c->dims.residual ? c->v_res : nullptr;
   return v;
 }
 
@@ -153,6 +158,8 @@ size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
     case OKVQ_BUF_MODALITY: return B * cap;
     case OKVQ_BUF_K_STAGE: return B * H * W * D * 2;
     case OKVQ_BUF_SEQ_LENS: return B * 4 + 4;  // the lengths and append's work-group counter
+    case OKVQ_BUF_K_RES:
+    case OKVQ_BUF_V_RES: return d->residual ? B * H * OKVQ_RESIDUAL_TOKENS * D * 2 : 0;
     default: return 0;
   }
 }
@@ -285,6 +292,12 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool exact = (flags & OKVQ_VALUE_EXACT) != 0;
+  if (d.residual && span > 0) {  // the fp16 rows, before the codec advances the lengths
+    if ((int64_t)d.batch * d.num_kv_heads > INT32_MAX) return OKVQ_ERR_UNSUPPORTED;
+    st = hip_status(launch_residual_store(k_new, v_new, n_max, cache->seq_lens, n_new_dev, d.batch, d.num_kv_heads,
+                                          d.capacity, cache->k_res, cache->v_res, s));
+    if (st != OKVQ_OK) return st;
+  }
   for (int b0 = 0; span > 0 && b0 < d.batch; b0 += kMaxLenArgs) {  // launches of up to 256 sequences
     const int nb = std::min(kMaxLenArgs, d.batch - b0);
     CodecArgs a{};
@@ -368,7 +381,8 @@ static okvq_status decode_impl(const okvq_cache* cache, const int32_t* lens_host
   }
   const size_t need = decode_workspace_bytes(d.batch, d.num_kv_heads, d.num_q_heads, max_len);
   if (!aligned16(workspace) || workspace_bytes < need) return OKVQ_ERR_WORKSPACE;
-  const DecodePlan plan = plan_decode(d.batch, d.num_kv_heads, max_len);
+  // with the fp16 residual the split-K launch covers the tokens below L - 128
+  const DecodePlan plan = plan_decode(d.batch, d.num_kv_heads, std::max(max_len - d.residual, 0));
   const Codebook& cb = codebook();
   const uint32_t cb01 = cb.level16[0] | ((uint32_t)cb.level16[1] << 16);
   const uint32_t cb23 = cb.level16[2] | ((uint32_t)cb.level16[3] << 16);

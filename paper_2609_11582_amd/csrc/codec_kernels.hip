@@ -107,6 +107,43 @@ hipError_t launch_quantize_values_exact(const CodecJob& j, int nb, int max_tiles
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------------------------------------
+// fp16 residual of the captioning protocol (Sec. 3.1): the raw key and value rows of the appended
+// tokens that are among the last 128 of their sequence go to row token % 128 of the ring buffers.
+// One work-group per (sequence, KV head); runs before the codec launch advances the lengths.
+// ------------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_residual_store(const uint16_t* __restrict__ k_new,
+                                                        const uint16_t* __restrict__ v_new, int n_rows,
+                                                        const int32_t* __restrict__ begin_dev,
+                                                        const int32_t* __restrict__ count_dev, int H, int cap,
+                                                        uint16_t* __restrict__ k_res, uint16_t* __restrict__ v_res) {
+  const int seq = blockIdx.x, b = seq / H;
+  const int begin = min(max(begin_dev[b], 0), cap);  // clamped like the codec's device lengths
+  const int end = min(begin + min(max(count_dev[b], 0), n_rows), cap);
+  const int first = max(end - kResidual, begin);
+  const int nrow = end - first;  // <= 128: every ring row is written at most once
+  const uint4* ks = reinterpret_cast<const uint4*>(k_new + (size_t)seq * n_rows * kD);
+  const uint4* vs = reinterpret_cast<const uint4*>(v_new + (size_t)seq * n_rows * kD);
+  uint4* kd = reinterpret_cast<uint4*>(k_res + (size_t)seq * kResidual * kD);
+  uint4* vd = reinterpret_cast<uint4*>(v_res + (size_t)seq * kResidual * kD);
+  for (int idx = threadIdx.x; idx < nrow * 16; idx += 256) {  // 16 uint4 per 128-channel row
+    const int tok = first + (idx >> 4), part = idx & 15;
+    const size_t src = (size_t)(tok - begin) * 16 + part;
+    const int dst = (tok & (kResidual - 1)) * 16 + part;
+    kd[dst] = ks[src];
+    vd[dst] = vs[src];
+  }
+}
+
+hipError_t launch_residual_store(const uint16_t* k_new, const uint16_t* v_new, int n_rows, const int32_t* begin_dev,
+                                 const int32_t* count_dev, int B, int H, int cap, uint16_t* k_res, uint16_t* v_res,
+                                 hipStream_t s) {
+  if (n_rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_residual_store, dim3(B * H), dim3(256), 0, s, k_new, v_new, n_rows, begin_dev, count_dev, H, cap,
+                     k_res, v_res);
+  return hipGetLastError();
+}
+
 // seq_lens[b] += count[b] after an append (stream-ordered after the codec kernels that read them).
 __global__ void k_advance_lengths(int32_t* seq_lens, const int32_t* count, int B) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;

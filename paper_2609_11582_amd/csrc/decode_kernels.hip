@@ -60,6 +60,7 @@ struct DecodeArgs {
   const uint16_t* rot16t;  // [128][3][128] fp16: (c, m, k) -> R_m[k][c]
   float* ws;               // partial records [B][H][nsplit][kRecFloats]
   int H, Hq, G, cap, wps, nsplit;
+  int residual;      // tokens at the end of each sequence left to the merge launch (fp16 residual)
   float qscale;      // sm_scale * log2(e) / sqrt(128)
   uint32_t cb01;     // fp16 codebook levels 0, 1 (low, high half)
   uint32_t cb23;     // fp16 codebook levels 2, 3
@@ -306,7 +307,9 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   }
   PairLoad bufA, bufB;
   if (wA0 < w_plan) bufA = load_pair<kMx>(sp, wA0, wA0 + 1 < w_plan, lane);
-  const int len = min(p.seq_lens[b], p.cap);  // memory-safe if device and host lengths disagree
+  // memory-safe if device and host lengths disagree; with the fp16 residual the last 128 tokens
+  // are the merge launch's
+  const int len = max(min(p.seq_lens[b], p.cap) - p.residual, 0);
   const int nwin = (len + kW - 1) / kW;
   const int w_end = min(w_plan, nwin);
   if (w_begin >= w_end) {  // empty split (ragged batch): a header the merge skips
@@ -700,23 +703,17 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 // ---- merge over splits: o = sum_s 2^(M_s - M) L_s o_s / sum_s 2^(M_s - M) L_s (log-sum-exp) ----
 // One work-group of 256 threads per (query head j, sequence b): thread (split group sg, channel
 // quad q4) sums the splits s = sg (mod 8). Every load is issued before any is used; empty splits
-// carry M = -inf and are skipped (their outputs were never written).
+// carry M = -inf and are skipped (their outputs were never written). A record's L is relative to
+// 2^(M + kLazy) (the split kernel's lazily updated reference).
 constexpr int kMergeThreads = 256;
 constexpr int kMergeUnroll = 8;  // splits per thread held in registers at once
 
-__global__ __launch_bounds__(kMergeThreads) void k_decode_merge(const float* __restrict__ ws, int H, int Hq, int G,
-                                                                int nsplit, float* __restrict__ out) {
-  __shared__ float red[2][kMergeThreads / 64];
-  __shared__ __attribute__((aligned(16))) float4 part[8][32];
-  const int j = blockIdx.x, b = blockIdx.y;
-  const int h = j / G, hd = j % G;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int q4 = tid & 31, sg = tid >> 5;
-  const float* base = ws + ((size_t)b * H + h) * nsplit * kRecFloats;
-
-  float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
-  float M = -__builtin_inff(), L = 0.0f;
-  // running (M, L, o) over this thread's splits: one pass, all loads of a chunk up front
+// running (M, L, o) over the splits s = sg (mod 8) of one (sequence, KV head), query head hd
+__device__ __forceinline__ void merge_splits(const float* base, int nsplit, int hd, int sg, int q4, float& M,
+                                             float& L, float4& o) {
+  o = make_float4(0.f, 0.f, 0.f, 0.f);
+  M = -__builtin_inff();
+  L = 0.0f;
   for (int s0 = sg; s0 < nsplit; s0 += 8 * kMergeUnroll) {
     float ms[kMergeUnroll], ls[kMergeUnroll];
     float4 v[kMergeUnroll];
@@ -750,11 +747,17 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge(const float* __r
     }
     M = mc;
   }
-  // combine the 8 split groups: global max, then rescale
+}
+
+// The 8 split groups combined: every group rescaled to the global max Mt; lanes of tid < 32 end
+// with the summed outputs of channels 4 tid .. 4 tid + 3 in `t` and the summed L in `Lt`.
+__device__ __forceinline__ void combine_groups(float M, float L, float4 o, int tid, float (&red)[2][kMergeThreads / 64],
+                                               float4 (&part)[8][32], float& Mt, float& Lt, float4& t) {
+  const int lane = tid & 63, wave = tid >> 6, q4 = tid & 31, sg = tid >> 5;
   float mw = wave_max(M);
   if (lane == 0) red[0][wave] = mw;
   __syncthreads();
-  float Mt = red[0][0];
+  Mt = red[0][0];
 #pragma unroll
   for (int w = 1; w < kMergeThreads / 64; ++w) Mt = fmaxf(Mt, red[0][w]);
   const float a = (M == -__builtin_inff()) ? 0.0f : exp2f(M - Mt);
@@ -764,11 +767,12 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge(const float* __r
   if (lane == 0) red[1][wave] = lw;
   part[sg][q4] = make_float4(o.x * a, o.y * a, o.z * a, o.w * a);
   __syncthreads();
+  Lt = 0.0f;
+  t = make_float4(0.f, 0.f, 0.f, 0.f);
   if (tid < 32) {
-    float Lt = 0.0f;
 #pragma unroll
     for (int w = 0; w < kMergeThreads / 64; ++w) Lt += red[1][w];
-    float4 t = part[0][tid];
+    t = part[0][tid];
 #pragma unroll
     for (int g = 1; g < 8; ++g) {
       const float4 u = part[g][tid];
@@ -777,9 +781,198 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge(const float* __r
       t.z += u.z;
       t.w += u.w;
     }
+  }
+}
+
+__global__ __launch_bounds__(kMergeThreads) void k_decode_merge(const float* __restrict__ ws, int H, int Hq, int G,
+                                                                int nsplit, float* __restrict__ out) {
+  __shared__ float red[2][kMergeThreads / 64];
+  __shared__ __attribute__((aligned(16))) float4 part[8][32];
+  const int j = blockIdx.x, b = blockIdx.y;
+  const int h = j / G, hd = j % G;
+  const int tid = threadIdx.x;
+  float M, L, Mt, Lt;
+  float4 o, t;
+  merge_splits(ws + ((size_t)b * H + h) * nsplit * kRecFloats, nsplit, hd, tid >> 5, tid & 31, M, L, o);
+  combine_groups(M, L, o, tid, red, part, Mt, Lt, t);
+  if (tid < 32) {
     const float inv = (Lt > 0.0f) ? 1.0f / Lt : 0.0f;
     *reinterpret_cast<float4*>(out + ((size_t)b * Hq + j) * kD + 4 * tid) =
         make_float4(t.x * inv, t.y * inv, t.z * inv, t.w * inv);
+  }
+}
+
+// ---- merge with the fp16 residual of the captioning protocol (Sec. 3.1) ----
+// The split kernel covered the tokens below L - 128. This work-group also attends query head j
+// over the last nt = min(L, 128) tokens [T0, L): key i dequantized from the cache if
+// i < Kq = 128 floor(L / 128) (scored against the rotated query, Sec. 2.3), else read in fp16 from
+// k_res (scored against the query itself; the rotation is orthogonal); every value in fp16 from
+// v_res. Its (max, sum, unnormalized output) joins the splits' log-sum-exp merge. fp32 throughout.
+struct TailArgs {
+  const int32_t* seq_lens;
+  const uint16_t* q;       // [B][Hq][128] fp16
+  const int8_t* signs;     // [128]
+  const uint8_t* k_codes;
+  const uint16_t* k_norm;
+  const uint16_t* k_min;   // fp16 window metadata, or
+  const uint16_t* k_step;
+  const uint8_t* k_mx;     // MXFP4 window records (non-null selects this format)
+  const uint16_t* k_res;   // [B][H][128][128] fp16 rings
+  const uint16_t* v_res;
+  int cap;
+  float qscale;            // sm_scale * log2(e): scores in base 2
+};
+
+__global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const float* __restrict__ ws, int H, int Hq,
+                                                                         int G, int nsplit, float* __restrict__ out,
+                                                                         TailArgs ta) {
+  __shared__ float red[2][kMergeThreads / 64];
+  __shared__ __attribute__((aligned(16))) float4 part[8][32];
+  __shared__ __attribute__((aligned(16))) float qp[kD];   // q sm_scale log2(e)
+  __shared__ __attribute__((aligned(16))) float qr[kD];   // H q sm_scale log2(e) (rotated query)
+  __shared__ float ps[kResidual];                         // tail scores, then weights
+  __shared__ __attribute__((aligned(16))) float ot[4][kD];  // tail output partials, 4 token quarters
+  __shared__ float tred[kMergeThreads / 64];
+  __shared__ __attribute__((aligned(16))) float mst[5][2][kD];  // (minimum, step) of the tail's quantized windows
+  const int j = blockIdx.x, b = blockIdx.y;
+  const int h = j / G, hd = j % G;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const size_t seq = (size_t)b * H + h;
+
+  const int L = min(max(ta.seq_lens[b], 0), ta.cap);
+  const int T0 = max(L - kResidual, 0), nt = L - T0, Kq = L & ~(kResidual - 1);
+
+  // ---- the query, plain and rotated (one wave: butterflies through LDS), and the key window
+  // metadata of the tail's quantized tokens [T0, Kq) as fp32: windows w0 .. w0 + 4 at most ----
+  const int w0 = T0 / kW, nwq = (Kq > T0) ? (Kq - 1) / kW - w0 + 1 : 0;
+  if (tid < kD) {
+    const float x = h2f(ta.q[((size_t)b * Hq + j) * kD + tid]);
+    qp[tid] = x * ta.qscale;
+    qr[tid] = (ta.signs[tid] < 0) ? -x : x;
+  }
+  for (int idx = tid; idx < nwq * kD; idx += kMergeThreads) {
+    const int wi = idx >> 7, c = idx & (kD - 1);
+    const size_t w = seq * (ta.cap / kW) + w0 + wi;
+    float mn, st;
+    if (ta.k_mx) {  // record: channel 4q + i in nibble i of bytes 4q, 4q + 1 (minimum), 4q + 2, 4q + 3 (step)
+      const uint8_t* rec = ta.k_mx + w * kMxRecord;
+      const int q = c >> 2, i = c & 3;
+      const uint32_t cm = (rec[4 * q + (i >> 1)] >> (4 * (i & 1))) & 15u;
+      const uint32_t cs = (rec[4 * q + 2 + (i >> 1)] >> (4 * (i & 1))) & 15u;
+      mn = e2m1_decode(cm, (int)rec[128 + 2 * (c >> 5)] - 127);
+      st = e2m1_decode(cs, (int)rec[129 + 2 * (c >> 5)] - 127);
+    } else {
+      mn = h2f(ta.k_min[w * kD + c]);
+      st = h2f(ta.k_step[w * kD + c]);
+    }
+    mst[wi][0][c] = mn;
+    mst[wi][1][c] = st;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    for (int hh = 1; hh < kD; hh <<= 1) {  // Sylvester order: pairs (i, i + hh) with (i & hh) == 0
+      const int i = (lane / hh) * 2 * hh + (lane % hh);
+      const float a = qr[i], c = qr[i + hh];
+      wave_lds_sync();
+      qr[i] = a + c;
+      qr[i + hh] = a - c;
+      wave_lds_sync();
+    }
+    qr[lane] *= ta.qscale * 0.08838834764831845f;  // 1 / sqrt(128): H is orthonormal
+    qr[lane + 64] *= ta.qscale * 0.08838834764831845f;
+  }
+  __syncthreads();
+
+  // ---- tail scores: two threads per token, 64 channels each ----
+  {
+    const int tt = tid >> 1, half = tid & 1;
+    float sc = -__builtin_inff();
+    if (tt < nt) {
+      const int i = T0 + tt;
+      float acc = 0.0f;
+      if (i < Kq) {  // quantized key: n16 (q' . (m + step code)) over the window's metadata
+        const uint4 cw = *reinterpret_cast<const uint4*>(ta.k_codes + (seq * ta.cap + i) * 32 + 16 * half);
+        const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
+        const float* mrow = mst[i / kW - w0][0];
+        const float* srow = mst[i / kW - w0][1];
+#pragma unroll
+        for (int cc = 0; cc < 64; ++cc) {
+          const int c = 64 * half + cc;
+          const uint32_t code = (words[cc >> 4] >> (16 * (c & 1) + (c & 14))) & 3u;
+          acc = __builtin_fmaf(qr[c], __builtin_fmaf(srow[c], (float)code, mrow[c]), acc);
+        }
+        acc *= h2f(ta.k_norm[seq * ta.cap + i]);
+      } else {  // fp16 key from the ring
+        const uint4* kr = reinterpret_cast<const uint4*>(ta.k_res + (seq * kResidual + (i & (kResidual - 1))) * kD +
+                                                         64 * half);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const uint4 x = kr[u];
+          const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int c = 64 * half + 8 * u + 2 * e;
+            acc = __builtin_fmaf(qp[c], h2f(xs[e] & 0xffffu), acc);
+            acc = __builtin_fmaf(qp[c + 1], h2f(xs[e] >> 16), acc);
+          }
+        }
+      }
+      acc += __shfl_xor(acc, 1);
+      sc = acc;
+    }
+    if (half == 0 && tt < kResidual) ps[tt] = sc;
+    float mw = wave_max(sc);
+    if (lane == 0) tred[wave] = mw;
+  }
+  __syncthreads();
+  float mtail = tred[0];
+#pragma unroll
+  for (int w = 1; w < kMergeThreads / 64; ++w) mtail = fmaxf(mtail, tred[w]);
+  // weights 2^(s - mtail) (mtail = -inf only for an empty tail, which has no tokens)
+  if (tid < nt) ps[tid] = exp2f(ps[tid] - mtail);
+  __syncthreads();
+  // ---- tail output: thread (channel pair cp, token quarter tq) ----
+  {
+    const int cp = tid & 63, tq = tid >> 6;
+    float o0 = 0.0f, o1 = 0.0f;
+    const uint32_t* vr = reinterpret_cast<const uint32_t*>(ta.v_res + seq * kResidual * kD) + cp;
+    for (int tt = tq; tt < nt; tt += 4) {
+      const uint32_t x = vr[((T0 + tt) & (kResidual - 1)) * (kD / 2)];
+      o0 = __builtin_fmaf(ps[tt], h2f(x & 0xffffu), o0);
+      o1 = __builtin_fmaf(ps[tt], h2f(x >> 16), o1);
+    }
+    ot[tq][2 * cp] = o0;
+    ot[tq][2 * cp + 1] = o1;
+  }
+  float ltail = 0.0f;
+  if (wave == 0) {  // sum of the weights
+    float lsum = 0.0f;
+    for (int tt = lane; tt < nt; tt += 64) lsum += ps[tt];
+    lsum = wave_sum(lsum);
+    if (lane == 0) tred[0] = lsum;
+  }
+
+  // ---- the splits, then everything in the frame of the true maximum ----
+  float M, Ls, Mt, Lt;
+  float4 o, t;
+  merge_splits(ws + seq * nsplit * kRecFloats, nsplit, hd, tid >> 5, tid & 31, M, Ls, o);
+  combine_groups(M, Ls, o, tid, red, part, Mt, Lt, t);  // (its barriers also order the tail's LDS writes)
+  ltail = tred[0];
+  if (tid < 32) {
+    const float mref = Mt + kLazy;  // the splits' sums are relative to 2^(Mt + kLazy)
+    const float mf = fmaxf(mref, mtail);
+    const float as = (Mt == -__builtin_inff()) ? 0.0f : exp2f(mref - mf);
+    const float at = (nt == 0) ? 0.0f : exp2f(mtail - mf);
+    const float ltot = Lt * as + ltail * at;
+    const float inv = (ltot > 0.0f) ? 1.0f / ltot : 0.0f;
+    float r[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = 4 * tid + i;
+      const float tv = ot[0][c] + ot[1][c] + ot[2][c] + ot[3][c];
+      r[i] = ((i == 0 ? t.x : i == 1 ? t.y : i == 2 ? t.z : t.w) * as + tv * at) * inv;
+    }
+    *reinterpret_cast<float4*>(out + ((size_t)b * Hq + j) * kD + 4 * tid) = make_float4(r[0], r[1], r[2], r[3]);
   }
 }
 
@@ -830,6 +1023,7 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
   a.cap = c.cap;
   a.wps = plan.wins_per_split;
   a.nsplit = plan.nsplit;
+  a.residual = c.residual;
   a.qscale = sm_scale * 1.4426950408889634f * 0.08838834764831845f;
   a.cb01 = cb01;
   a.cb23 = cb23;
@@ -847,12 +1041,33 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
       hipLaunchKernelGGL(k_decode<false>, grid, block, 0, s, a);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (events) {
-    hipExtLaunchKernelGGL(k_decode_merge, dim3(c.Hq, c.B), dim3(kMergeThreads), 0, s, events[2], events[3], 0,
+  const dim3 mgrid(c.Hq, c.B), mblock(kMergeThreads);
+  if (c.residual) {
+    TailArgs t;
+    t.seq_lens = c.seq_lens;
+    t.q = q;
+    t.signs = c.signs;
+    t.k_codes = c.k_codes;
+    t.k_norm = c.k_norm;
+    t.k_min = c.k_min;
+    t.k_step = c.k_step;
+    t.k_mx = c.k_mx;
+    t.k_res = c.k_res;
+    t.v_res = c.v_res;
+    t.cap = c.cap;
+    t.qscale = sm_scale * 1.4426950408889634f;
+    if (events)
+      hipExtLaunchKernelGGL(k_decode_merge_residual, mgrid, mblock, 0, s, events[2], events[3], 0,
+                            static_cast<const float*>(a.ws), c.H, c.Hq, G, plan.nsplit, out, t);
+    else
+      hipLaunchKernelGGL(k_decode_merge_residual, mgrid, mblock, 0, s, static_cast<const float*>(a.ws), c.H, c.Hq, G,
+                         plan.nsplit, out, t);
+  } else if (events) {
+    hipExtLaunchKernelGGL(k_decode_merge, mgrid, mblock, 0, s, events[2], events[3], 0,
                           static_cast<const float*>(a.ws), c.H, c.Hq, G, plan.nsplit, out);
   } else {
-    hipLaunchKernelGGL(k_decode_merge, dim3(c.Hq, c.B), dim3(kMergeThreads), 0, s, a.ws, c.H, c.Hq, G, plan.nsplit,
-                       out);
+    hipLaunchKernelGGL(k_decode_merge, mgrid, mblock, 0, s, static_cast<const float*>(a.ws), c.H, c.Hq, G,
+                       plan.nsplit, out);
   }
   return hipGetLastError();
 }

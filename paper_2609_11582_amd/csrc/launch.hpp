@@ -65,6 +65,10 @@ struct CodecArgs {
 hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t s);
 hipError_t launch_prepare_fragments(const float* rot, uint4* frag, hipStream_t s);
 hipError_t launch_advance_lengths(int32_t* seq_lens, const int32_t* count, int B, hipStream_t s);
+// Residual rings: rows of the appended tokens among the last 128 of each sequence (device lengths).
+hipError_t launch_residual_store(const uint16_t* k_new, const uint16_t* v_new, int n_rows, const int32_t* begin_dev,
+                                 const int32_t* count_dev, int B, int H, int cap, uint16_t* k_res, uint16_t* v_res,
+                                 hipStream_t s);
 
 struct CacheView {
   int B, H, Hq, cap;
@@ -81,6 +85,9 @@ struct CacheView {
   const int8_t* signs;
   const float* rot;
   const uint16_t* rot16t;  // prepared rotation tables: [128][3][128] fp16 inverse, then forward fragments
+  int residual;            // 0, or kResidual: the last tokens are read in fp16 from k_res / v_res
+  const uint16_t* k_res;   // [B][H][128][128] fp16 rings (token i in row i % 128)
+  const uint16_t* v_res;
 };
 
 struct DecodePlan {

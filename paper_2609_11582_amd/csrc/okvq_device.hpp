@@ -14,6 +14,7 @@ namespace okvq {
 constexpr int kD = 128;      // head dimension
 constexpr int kW = 32;       // key window (tokens per min/step group)
 constexpr int kWave = 64;    // CDNA wavefront size
+constexpr int kResidual = 128;  // fp16 window of the captioning protocol (tokens), a power of two
 
 // fp32(1/sqrt(128)), the normalization of the Sylvester Hadamard matrix of order 128.
 constexpr float kKappa = 0x1.6a09e6p-4f;

@@ -25,8 +25,10 @@ OKVQ_KEY_META_MXFP4 = 1
 KEY_META = {"fp16": OKVQ_KEY_META_FP16, "mxfp4": OKVQ_KEY_META_MXFP4}
 ROTATION_TABLE_BYTES = 294912  # OKVQ_ROTATION_TABLE_BYTES
 MX_RECORD_BYTES = 136  # one MXFP4 key-metadata record per 32-token window
-# buffer ids 0..9 of okvq_buffer_bytes (OKVQ_BUF_*)
-BUFFERS = ("k_codes", "v_codes", "k_norm", "v_norm", "k_min", "k_step", "modality", "k_stage", "seq_lens", "k_mx")
+RESIDUAL_TOKENS = 128  # OKVQ_RESIDUAL_TOKENS: fp16 window of the captioning protocol
+# buffer ids 0..11 of okvq_buffer_bytes (OKVQ_BUF_*)
+BUFFERS = ("k_codes", "v_codes", "k_norm", "v_norm", "k_min", "k_step", "modality", "k_stage", "seq_lens", "k_mx",
+           "k_res", "v_res")
 
 
 class OkvqError(RuntimeError):
@@ -38,13 +40,13 @@ class OkvqError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("window", ctypes.c_int32), ("capacity", ctypes.c_int32),
-                ("key_meta", ctypes.c_int32)]
+                ("key_meta", ctypes.c_int32), ("residual", ctypes.c_int32)]
 
 
 class CacheStruct(ctypes.Structure):
     _fields_ = [("dims", Dims)] + [(n, ctypes.c_void_p) for n in BUFFERS[:9]] + [
         ("key_signs", ctypes.c_void_p), ("v_rot", ctypes.c_void_p), ("v_rot16", ctypes.c_void_p),
-        ("k_mx", ctypes.c_void_p)]
+        ("k_mx", ctypes.c_void_p), ("k_res", ctypes.c_void_p), ("v_res", ctypes.c_void_p)]
 
 
 _lib = None
@@ -123,8 +125,9 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def make_dims(batch, num_kv_heads, num_q_heads, capacity, head_dim=128, window=32, key_meta="fp16") -> Dims:
-    return Dims(batch, num_kv_heads, num_q_heads, head_dim, window, capacity, KEY_META[key_meta])
+def make_dims(batch, num_kv_heads, num_q_heads, capacity, head_dim=128, window=32, key_meta="fp16",
+              residual=0) -> Dims:
+    return Dims(batch, num_kv_heads, num_q_heads, head_dim, window, capacity, KEY_META[key_meta], int(residual))
 
 
 def okvq_version() -> int:
@@ -262,24 +265,28 @@ def okvq_decode_attention_timed(cache: "KVCache", lens, q, sm_scale, out, worksp
 
 _DTYPES = dict(k_codes=torch.uint8, v_codes=torch.uint8, k_norm=torch.float16, v_norm=torch.float16,
                k_min=torch.float16, k_step=torch.float16, modality=torch.uint8, k_stage=torch.float16,
-               seq_lens=torch.int32, k_mx=torch.uint8)
+               seq_lens=torch.int32, k_mx=torch.uint8, k_res=torch.float16, v_res=torch.float16)
 
 
 class KVCache:
     """Device buffers of one layer's packed cache, sized by okvq_buffer_bytes (torch allocations),
     with the layer's key signs, value rotations and the decode's inverse-rotation table.
-    key_meta "fp16" keeps the key window minimum and step in k_min / k_step, "mxfp4" in k_mx."""
+    key_meta "fp16" keeps the key window minimum and step in k_min / k_step, "mxfp4" in k_mx.
+    residual=RESIDUAL_TOKENS adds the fp16 rings of the captioning protocol (k_res, v_res)."""
 
     def __init__(self, batch, num_kv_heads, num_q_heads, capacity, key_signs: torch.Tensor, v_rot: torch.Tensor,
-                 device="cuda", key_meta="fp16"):
+                 device="cuda", key_meta="fp16", residual=0):
         self.key_meta = key_meta
-        self.dims = make_dims(batch, num_kv_heads, num_q_heads, capacity, key_meta=key_meta)
+        self.residual = int(residual)
+        self.dims = make_dims(batch, num_kv_heads, num_q_heads, capacity, key_meta=key_meta, residual=residual)
         self.key_signs = key_signs.to(device=device, dtype=torch.int8).contiguous()
         self.v_rot = v_rot.to(device=device, dtype=torch.float32).contiguous()
         self.v_rot16 = torch.empty(ROTATION_TABLE_BYTES // 2, dtype=torch.float16, device=device)
         okvq_prepare_rotation(self.v_rot, self.v_rot16)
         self.buffers = {}
         unused = ("k_mx",) if key_meta == "fp16" else ("k_min", "k_step")
+        if not self.residual:
+            unused += ("k_res", "v_res")
         for i, name in enumerate(BUFFERS):
             nbytes = okvq_buffer_bytes(self.dims, i)
             if (nbytes == 0) != (name in unused):
@@ -292,7 +299,8 @@ class KVCache:
         ptr = {n: (t.data_ptr() if n in self.buffers else None) for n, t in
                ((n, self.buffers.get(n)) for n in BUFFERS)}
         self.struct = CacheStruct(self.dims, *[ptr[n] for n in BUFFERS[:9]], self.key_signs.data_ptr(),
-                                  self.v_rot.data_ptr(), self.v_rot16.data_ptr(), ptr["k_mx"])
+                                  self.v_rot.data_ptr(), self.v_rot16.data_ptr(), ptr["k_mx"], ptr["k_res"],
+                                  ptr["v_res"])
 
     def __getitem__(self, name):
         return self.buffers[name]
@@ -310,4 +318,6 @@ class KVCache:
             v.update(k_min=b["k_min"].view(B, H, cap // 32, 128), k_step=b["k_step"].view(B, H, cap // 32, 128))
         else:
             v.update(k_mx=b["k_mx"].view(B, H, cap // 32, MX_RECORD_BYTES))
+        if self.residual:
+            v.update(k_res=b["k_res"].view(B, H, RESIDUAL_TOKENS, 128), v_res=b["v_res"].view(B, H, RESIDUAL_TOKENS, 128))
         return v

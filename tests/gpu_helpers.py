@@ -89,6 +89,28 @@ def append_chunks(cache, k, v, modality, lens, chunk_plan, exact=False):
     return cur
 
 
+def append_chunks_from(cache, k, v, modality, cur, n_new, exact=False):
+    """One append of n_new[b] tokens per sequence, continuing from the current lengths cur [B]
+    (the inputs k, v [B][H][N][D], modality [B][N] are the whole sequences). Returns the new lengths."""
+    B, H, N, D = k.shape
+    cur = np.asarray(cur, np.int64)
+    n_new = np.asarray(n_new, np.int64)
+    n_max = max(int(n_new.max()), 1)
+    kn = np.zeros((B, H, n_max, D), np.float16)
+    vn = np.zeros((B, H, n_max, D), np.float16)
+    mn = np.zeros((B, n_max), np.uint8)
+    for b in range(B):
+        a, c = int(cur[b]), int(cur[b] + n_new[b])
+        kn[b, :, :c - a] = k[b, :, a:c]
+        vn[b, :, :c - a] = v[b, :, a:c]
+        mn[b, :c - a] = modality[b, a:c]
+    nd = dev(n_new.astype(np.int32))
+    okvq.okvq_append(cache, cur.astype(np.int32).tolist(), f16dev(kn), f16dev(vn), dev(mn),
+                     n_new.astype(np.int32).tolist(), nd, n_max, okvq.okvq.OKVQ_VALUE_EXACT if exact else 0)
+    torch.cuda.synchronize()
+    return cur + n_new
+
+
 def cache_to_numpy(cache):
     return {n: t.cpu().numpy() for n, t in cache.views().items()}
 

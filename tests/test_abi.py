@@ -142,7 +142,36 @@ def test_mxfp4_metadata_buffers_and_validation():
                                    None) == -1
 
 
-@pytest.mark.parametrize("which", range(10))
+def test_residual_buffers_and_validation():
+    """fp16 residual of the captioning protocol: two 128-token fp16 rings per (sequence, KV head),
+    present only with dims.residual = 128; any other window is rejected, and a residual cache
+    needs both rings."""
+    okvq = _lib()
+    L = okvq.lib()
+    d = okvq.make_dims(2, 4, 28, 4096, residual=128)
+    assert okvq.okvq_buffer_bytes(d, 10) == okvq.okvq_buffer_bytes(d, 11) == 2 * 4 * 128 * 128 * 2
+    assert okvq.okvq_buffer_bytes(okvq.make_dims(2, 4, 28, 4096), 10) == 0
+    assert okvq.okvq_buffer_bytes(okvq.make_dims(2, 4, 28, 4096), 11) == 0
+    # the quantized buffers do not change
+    for i in range(10):
+        assert okvq.okvq_buffer_bytes(d, i) == okvq.okvq_buffer_bytes(okvq.make_dims(2, 4, 28, 4096), i)
+    assert okvq.okvq_buffer_bytes(okvq.make_dims(2, 4, 28, 4096, residual=64), 10) == 0
+    fake = ctypes.c_void_p(4096)
+    q_lens = (ctypes.c_int32 * 2)(64, 64)
+    rd = okvq.make_dims(2, 2, 8, 64, residual=128)
+    ok = okvq.CacheStruct(rd, *([4096] * 9), 4096, 4096, 4096, 0, 4096, 4096)
+    no_ring = okvq.CacheStruct(rd, *([4096] * 9), 4096, 4096, 4096, 0, 4096, 0)
+    odd = okvq.make_dims(2, 2, 8, 64, residual=100)
+    odd_cache = okvq.CacheStruct(odd, *([4096] * 9), 4096, 4096, 4096, 0, 4096, 4096)
+    for cache, want in ((no_ring, -1), (odd_cache, -1), (ok, -4)):  # -4: validation passed up to the workspace
+        assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, 16,
+                                       None) == want
+    n_new = (ctypes.c_int32 * 2)(40, 0)
+    lens_a = (ctypes.c_int32 * 2)(30, 0)
+    assert L.okvq_append(ctypes.byref(no_ring), lens_a, fake, fake, fake, n_new, fake, 40, 0, None) == -1
+
+
+@pytest.mark.parametrize("which", range(12))
 def test_buffer_bytes_invalid_dims(which):
     okvq = _lib()
     assert okvq.okvq_buffer_bytes(okvq.make_dims(1, 1, 1, 33), which) == 0
