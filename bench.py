@@ -24,6 +24,8 @@ Reported (one JSON line):
   cpu_baseline    the float64 CPU oracle's decode on the same cache, on this host
   mxfp4           the same workload with MXFP4 key window metadata (72.25 instead of 84 bytes per
                   token and KV head): append, decode and split-K kernel time, effective GB/s
+  residual        the same workload in the captioning protocol (fp16 rings of the last 128 keys and
+                  values): prefill and one-token append, decode, split-K and merge-with-tail times
 
 --profile-pass runs a short fixed sequence for rocprofv3 counter collection: a 256 MiB device
 copy (calibrates FETCH_SIZE / WRITE_SIZE against a known byte count), 8 decode calls on cold
@@ -82,6 +84,23 @@ def append_algorithmic_bytes(B, H, lens, key_meta="fp16"):
     n = sum(int(L) for L in lens)
     per_tok = APPEND_BYTES_PER_TOKEN_HEAD if key_meta == "fp16" else APPEND_BYTES_PER_TOKEN_HEAD_MX
     return int(n * H * per_tok) + 2 * n + 3 * 128 * 128 * 4 + 128
+
+
+def residual_decode_algorithmic_bytes(B, H, Hq, lens, residual=128):
+    """Decode bytes with the fp16 residual of the captioning protocol: the quantized windows of the
+    tokens below L - 128 (as for plain decode), the tail's quantized keys below 128 floor(L / 128)
+    (codes, norm and their windows' metadata not already counted), its fp16 keys and values
+    (256 B each), the modality map of the quantized part, q, out and R."""
+    total = B * Hq * 128 * (2 + 4) + 3 * 128 * 128 * 4
+    for L in lens:
+        L = int(L)
+        t0, kq = max(L - residual, 0), residual * (L // residual)
+        nwm = -(-t0 // 32)                          # windows read by the split-K kernel
+        nwk = -(-kq // 32)                          # windows holding quantized keys
+        total += nwm * 32 + H * nwm * DECODE_BYTES_PER_WINDOW_HEAD
+        total += H * (max(kq - t0, 0) * 34 + max(nwk - nwm, 0) * 512)
+        total += H * ((L - max(kq, t0)) * 256 + (L - t0) * 256)
+    return total
 
 
 def measured_traffic(kernel_key):
@@ -237,6 +256,86 @@ def mx_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stre
             "append_us": round(append_us, 3), "append_GBps": round(abytes / append_us / 1e3, 2),
             "append_frac": round(abytes / append_us / 1e3 / HBM_PEAK_GBPS, 4), "algorithmic_bytes": dbytes,
             "replicas": n_cache}
+
+
+def residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream, decode_iters):
+    """The benchmark workload in the captioning protocol (Sec. 3.1): fp16 rings of the last 128 keys
+    and values next to the packed cache. Prefill append, one-token append (a generation step), and
+    decode over >= 1 GB of cold cache replicas with the per-launch durations."""
+    B, H, Hq, N = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.seq_len
+    dev = q.device
+    sm = 1 / math.sqrt(128)
+    cap = wl.capacity + 32                                   # room for the generated token
+    dims = okvq.make_dims(B, H, Hq, cap, residual=128)
+    per_cache = sum(okvq.okvq_buffer_bytes(dims, i) for i in range(12))
+    n_cache = max(16, int(math.ceil(1.05e9 / per_cache)))
+    mk = lambda: okvq.KVCache(B, H, Hq, cap, torch.ones(128, dtype=torch.int8), torch.eye(128).repeat(3, 1, 1),
+                              device=dev, residual=128)
+    caches = [mk() for _ in range(n_cache)]
+    okvq.okvq_append(caches[0], [0] * B, k_in[0], v_in[0], m0, lens, n_new_dev, N, stream=stream)
+    torch.cuda.synchronize()
+    for c in caches[1:]:
+        for name in c.buffers:
+            c.buffers[name].copy_(caches[0].buffers[name])
+    ws = okvq.decode_workspace(dims, max(lens), device=dev)
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+    app = []
+    for i in range(12):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c = caches[(i + 1) % n_cache]
+        c.buffers["seq_lens"].zero_()
+        e0.record(stream)
+        okvq.okvq_append(c, [0] * B, k_in[i % len(k_in)], v_in[i % len(v_in)], m0, lens, n_new_dev, N, stream=stream)
+        e1.record(stream)
+        app.append((e0, e1))
+    torch.cuda.synchronize()
+    append_us = float(np.mean([a.elapsed_time(b) for a, b in app[2:]])) * 1e3
+    # one generated token appended at length N (then the length is set back, on the stream)
+    k1 = k_in[0][:, :, :1].contiguous()
+    v1 = v_in[0][:, :, :1].contiguous()
+    m1 = m0[:, :1].contiguous()
+    one = torch.ones(B, dtype=torch.int32, device=dev)
+    back = torch.tensor(lens, dtype=torch.int32, device=dev)
+    app1 = []
+    for i in range(40):
+        c = caches[(3 * i + 2) % n_cache]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        okvq.okvq_append(c, lens, k1, v1, m1, [1] * B, one, 1, stream=stream)
+        e1.record(stream)
+        c.buffers["seq_lens"][:B].copy_(back)
+        app1.append((e0, e1))
+    torch.cuda.synchronize()
+    append1_us = float(np.median([a.elapsed_time(b) for a, b in app1[5:]])) * 1e3
+    reps = []
+    for rep in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for i in range(20):
+            okvq.okvq_decode_attention(caches[i % n_cache], lens, q, sm, out, ws, stream=stream)
+        e0.record(stream)
+        for i in range(decode_iters):
+            okvq.okvq_decode_attention(caches[(i * 7 + rep) % n_cache], lens, q, sm, out, ws, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        reps.append(e0.elapsed_time(e1) * 1e3 / decode_iters)
+    decode_us = float(np.median(reps))
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(decode_iters)]
+    for e4 in evs:
+        for e in e4:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for i in range(decode_iters):
+        okvq.okvq_decode_attention_timed(caches[(i * 7 + 5) % n_cache], lens, q, sm, out, ws, evs[i], stream=stream)
+    torch.cuda.synchronize()
+    split_us = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) * 1e3
+    merge_us = float(np.mean([e[2].elapsed_time(e[3]) for e in evs])) * 1e3
+    dbytes = residual_decode_algorithmic_bytes(B, H, Hq, lens)
+    del caches
+    return {"protocol": "captioning: keys quantized per 128-token block, last 128 values fp16",
+            "decode_us": round(decode_us, 3), "decode_GBps": round(dbytes / decode_us / 1e3, 2),
+            "k_decode_us": round(split_us, 3), "k_decode_merge_residual_us": round(merge_us, 3),
+            "append_prefill_us": round(append_us, 3), "append_one_token_us": round(append1_us, 3),
+            "algorithmic_bytes": dbytes, "replicas": n_cache}
 
 
 def main():
@@ -439,6 +538,8 @@ def main():
     }
     line["mxfp4"] = mx_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                    args.decode_iters)
+    line["residual"] = residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
+                                            args.decode_iters)
     if not args.no_cpu_baseline:
         cache_np = {n: t.cpu().numpy() for n, t in caches[0].views().items()}
         line["cpu_baseline"] = cpu_baseline(cache_np, q.cpu().numpy(), np.asarray(lens), lay["signs"], lay["rot"],

@@ -708,6 +708,49 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 constexpr int kMergeThreads = 256;
 constexpr int kMergeUnroll = 8;  // splits per thread held in registers at once
 
+// Eight split records of one chunk (splits s0, s0 + 8, ..., s0 + 56) for query head hd and channel
+// quad q4; splits beyond nsplit read as empty.
+struct SplitChunk {
+  float ms[kMergeUnroll], ls[kMergeUnroll];
+  float4 v[kMergeUnroll];
+};
+
+__device__ __forceinline__ void load_split_chunk(const float* base, int nsplit, int hd, int q4, int s0, SplitChunk& c) {
+#pragma unroll
+  for (int u = 0; u < kMergeUnroll; ++u) {
+    const int s = s0 + 8 * u;
+    const float* rs = base + (size_t)min(s, nsplit - 1) * kRecFloats;
+    c.ms[u] = (s < nsplit) ? rs[hd] : -__builtin_inff();
+    c.ls[u] = rs[8 + hd];
+    c.v[u] = *reinterpret_cast<const float4*>(rs + kRecHeader + hd * kD + 4 * q4);
+  }
+}
+
+// folds a chunk into the running (M, L, o)
+__device__ __forceinline__ void fold_split_chunk(const SplitChunk& c, float& M, float& L, float4& o) {
+  float mc = M;
+#pragma unroll
+  for (int u = 0; u < kMergeUnroll; ++u) mc = fmaxf(mc, c.ms[u]);
+  if (mc == -__builtin_inff()) return;
+  const float a = exp2f(M - mc);  // M = -inf -> 0
+  L *= a;
+  o.x *= a;
+  o.y *= a;
+  o.z *= a;
+  o.w *= a;
+#pragma unroll
+  for (int u = 0; u < kMergeUnroll; ++u) {
+    if (c.ms[u] == -__builtin_inff()) continue;
+    const float w = exp2f(c.ms[u] - mc) * c.ls[u];
+    L += w;
+    o.x = __builtin_fmaf(w, c.v[u].x, o.x);
+    o.y = __builtin_fmaf(w, c.v[u].y, o.y);
+    o.z = __builtin_fmaf(w, c.v[u].z, o.z);
+    o.w = __builtin_fmaf(w, c.v[u].w, o.w);
+  }
+  M = mc;
+}
+
 // running (M, L, o) over the splits s = sg (mod 8) of one (sequence, KV head), query head hd
 __device__ __forceinline__ void merge_splits(const float* base, int nsplit, int hd, int sg, int q4, float& M,
                                              float& L, float4& o) {
@@ -715,37 +758,9 @@ __device__ __forceinline__ void merge_splits(const float* base, int nsplit, int 
   M = -__builtin_inff();
   L = 0.0f;
   for (int s0 = sg; s0 < nsplit; s0 += 8 * kMergeUnroll) {
-    float ms[kMergeUnroll], ls[kMergeUnroll];
-    float4 v[kMergeUnroll];
-#pragma unroll
-    for (int u = 0; u < kMergeUnroll; ++u) {
-      const int s = s0 + 8 * u;
-      const float* rs = base + (size_t)min(s, nsplit - 1) * kRecFloats;
-      ms[u] = (s < nsplit) ? rs[hd] : -__builtin_inff();
-      ls[u] = rs[8 + hd];
-      v[u] = *reinterpret_cast<const float4*>(rs + kRecHeader + hd * kD + 4 * q4);
-    }
-    float mc = M;
-#pragma unroll
-    for (int u = 0; u < kMergeUnroll; ++u) mc = fmaxf(mc, ms[u]);
-    if (mc == -__builtin_inff()) continue;
-    const float a = exp2f(M - mc);  // M = -inf -> 0
-    L *= a;
-    o.x *= a;
-    o.y *= a;
-    o.z *= a;
-    o.w *= a;
-#pragma unroll
-    for (int u = 0; u < kMergeUnroll; ++u) {
-      if (ms[u] == -__builtin_inff()) continue;
-      const float w = exp2f(ms[u] - mc) * ls[u];
-      L += w;
-      o.x = __builtin_fmaf(w, v[u].x, o.x);
-      o.y = __builtin_fmaf(w, v[u].y, o.y);
-      o.z = __builtin_fmaf(w, v[u].z, o.z);
-      o.w = __builtin_fmaf(w, v[u].w, o.w);
-    }
-    M = mc;
+    SplitChunk c;
+    load_split_chunk(base, nsplit, hd, q4, s0, c);
+    fold_split_chunk(c, M, L, o);
   }
 }
 
@@ -833,40 +848,95 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   __shared__ float ps[kResidual];                         // tail scores, then weights
   __shared__ __attribute__((aligned(16))) float ot[4][kD];  // tail output partials, 4 token quarters
   __shared__ float tred[kMergeThreads / 64];
-  __shared__ __attribute__((aligned(16))) float mst[5][2][kD];  // (minimum, step) of the tail's quantized windows
+  __shared__ __attribute__((aligned(16))) float mst[4][2][kD];  // (minimum, step) of the tail's quantized windows
   const int j = blockIdx.x, b = blockIdx.y;
   const int h = j / G, hd = j % G;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sg = tid >> 5, q4 = tid & 31;
   const size_t seq = (size_t)b * H + h;
+  const float* base = ws + seq * nsplit * kRecFloats;
 
+  // ---- every load goes out before any is used: the first chunk of split records, then (once the
+  // length is known) the query, the metadata of the tail's quantized windows, the tail's keys
+  // (codes and norms, or fp16 rows) and the value rows this thread sums ----
+  SplitChunk ch0;
+  if (sg < nsplit) load_split_chunk(base, nsplit, hd, q4, sg, ch0);
   const int L = min(max(ta.seq_lens[b], 0), ta.cap);
   const int T0 = max(L - kResidual, 0), nt = L - T0, Kq = L & ~(kResidual - 1);
-
-  // ---- the query, plain and rotated (one wave: butterflies through LDS), and the key window
-  // metadata of the tail's quantized tokens [T0, Kq) as fp32: windows w0 .. w0 + 4 at most ----
+  // quantized keys [T0, Kq) lie in windows w0 .. w0 + 3 (Kq - T0 <= 128 and Kq is window aligned)
   const int w0 = T0 / kW, nwq = (Kq > T0) ? (Kq - 1) / kW - w0 + 1 : 0;
+  uint32_t qx = 0;
+  int8_t sgn = 1;
   if (tid < kD) {
-    const float x = h2f(ta.q[((size_t)b * Hq + j) * kD + tid]);
-    qp[tid] = x * ta.qscale;
-    qr[tid] = (ta.signs[tid] < 0) ? -x : x;
+    qx = ta.q[((size_t)b * Hq + j) * kD + tid];
+    sgn = ta.signs[tid];
   }
-  for (int idx = tid; idx < nwq * kD; idx += kMergeThreads) {
-    const int wi = idx >> 7, c = idx & (kD - 1);
-    const size_t w = seq * (ta.cap / kW) + w0 + wi;
-    float mn, st;
-    if (ta.k_mx) {  // record: channel 4q + i in nibble i of bytes 4q, 4q + 1 (minimum), 4q + 2, 4q + 3 (step)
-      const uint8_t* rec = ta.k_mx + w * kMxRecord;
-      const int q = c >> 2, i = c & 3;
-      const uint32_t cm = (rec[4 * q + (i >> 1)] >> (4 * (i & 1))) & 15u;
-      const uint32_t cs = (rec[4 * q + 2 + (i >> 1)] >> (4 * (i & 1))) & 15u;
-      mn = e2m1_decode(cm, (int)rec[128 + 2 * (c >> 5)] - 127);
-      st = e2m1_decode(cs, (int)rec[129 + 2 * (c >> 5)] - 127);
-    } else {
-      mn = h2f(ta.k_min[w * kD + c]);
-      st = h2f(ta.k_step[w * kD + c]);
+  uint32_t mraw[2], sraw[2];  // metadata entries idx = tid, tid + 256 of the (window, channel) table
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int idx = tid + kMergeThreads * r;
+    mraw[r] = sraw[r] = 0;
+    if (idx < nwq * kD) {
+      const int wi = idx >> 7, c = idx & (kD - 1);
+      const size_t w = seq * (ta.cap / kW) + w0 + wi;
+      if (ta.k_mx) {  // record: channel 4q + i in nibble i of bytes 4q, 4q + 1 (minimum), 4q + 2, 4q + 3 (step)
+        const uint8_t* rec = ta.k_mx + w * kMxRecord;
+        const int qq = c >> 2, i = c & 3;
+        mraw[r] = ((rec[4 * qq + (i >> 1)] >> (4 * (i & 1))) & 15u) | ((uint32_t)rec[128 + 2 * (c >> 5)] << 8);
+        sraw[r] = ((rec[4 * qq + 2 + (i >> 1)] >> (4 * (i & 1))) & 15u) | ((uint32_t)rec[129 + 2 * (c >> 5)] << 8);
+      } else {
+        mraw[r] = ta.k_min[w * kD + c];
+        sraw[r] = ta.k_step[w * kD + c];
+      }
     }
-    mst[wi][0][c] = mn;
-    mst[wi][1][c] = st;
+  }
+  // scores: two threads per token tt = tid / 2, channels 64 half .. 64 half + 63
+  const int tt = tid >> 1, half = tid & 1, ti = T0 + tt;
+  const bool tok = tt < nt, quant = tok && ti < Kq;
+  uint4 kr[8];
+  uint32_t knrm = 0;
+  if (quant) {
+    kr[0] = *reinterpret_cast<const uint4*>(ta.k_codes + (seq * ta.cap + ti) * 32 + 16 * half);
+    knrm = ta.k_norm[seq * ta.cap + ti];
+  } else if (tok) {
+    const uint4* row = reinterpret_cast<const uint4*>(ta.k_res + (seq * kResidual + (ti & (kResidual - 1))) * kD +
+                                                      64 * half);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) kr[u] = row[u];
+  }
+  // output: thread (channel pair cp, token quarter tq) sums tokens tq, tq + 4, ...
+  const int cp = tid & 63, tq = tid >> 6;
+  uint32_t vv[kResidual / 4];
+  {
+    const uint32_t* vr = reinterpret_cast<const uint32_t*>(ta.v_res + seq * kResidual * kD) + cp;
+#pragma unroll
+    for (int u = 0; u < kResidual / 4; ++u) {
+      const int t2 = tq + 4 * u;
+      vv[u] = (t2 < nt) ? vr[((T0 + t2) & (kResidual - 1)) * (kD / 2)] : 0u;
+    }
+  }
+
+  // ---- the query, plain and rotated (one wave: butterflies through LDS), the metadata as fp32 ----
+  if (tid < kD) {
+    const float x = h2f(qx);
+    qp[tid] = x * ta.qscale;
+    qr[tid] = (sgn < 0) ? -x : x;
+  }
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int idx = tid + kMergeThreads * r;
+    if (idx < nwq * kD) {
+      float mn, st;
+      if (ta.k_mx) {
+        mn = e2m1_decode(mraw[r] & 15u, (int)(mraw[r] >> 8) - 127);
+        st = e2m1_decode(sraw[r] & 15u, (int)(sraw[r] >> 8) - 127);
+      } else {
+        mn = h2f(mraw[r]);
+        st = h2f(sraw[r]);
+      }
+      mst[idx >> 7][0][idx & (kD - 1)] = mn;
+      mst[idx >> 7][1][idx & (kD - 1)] = st;
+    }
   }
   __syncthreads();
   if (wave == 0) {
@@ -883,32 +953,26 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   }
   __syncthreads();
 
-  // ---- tail scores: two threads per token, 64 channels each ----
+  // ---- tail scores ----
   {
-    const int tt = tid >> 1, half = tid & 1;
     float sc = -__builtin_inff();
-    if (tt < nt) {
-      const int i = T0 + tt;
+    if (tok) {
       float acc = 0.0f;
-      if (i < Kq) {  // quantized key: n16 (q' . (m + step code)) over the window's metadata
-        const uint4 cw = *reinterpret_cast<const uint4*>(ta.k_codes + (seq * ta.cap + i) * 32 + 16 * half);
-        const uint32_t words[4] = {cw.x, cw.y, cw.z, cw.w};
-        const float* mrow = mst[i / kW - w0][0];
-        const float* srow = mst[i / kW - w0][1];
+      if (quant) {  // n16 (q' . (m + step code)) over the window's metadata
+        const uint32_t words[4] = {kr[0].x, kr[0].y, kr[0].z, kr[0].w};
+        const float* mrow = mst[ti / kW - w0][0];
+        const float* srow = mst[ti / kW - w0][1];
 #pragma unroll
         for (int cc = 0; cc < 64; ++cc) {
           const int c = 64 * half + cc;
           const uint32_t code = (words[cc >> 4] >> (16 * (c & 1) + (c & 14))) & 3u;
           acc = __builtin_fmaf(qr[c], __builtin_fmaf(srow[c], (float)code, mrow[c]), acc);
         }
-        acc *= h2f(ta.k_norm[seq * ta.cap + i]);
+        acc *= h2f(knrm);
       } else {  // fp16 key from the ring
-        const uint4* kr = reinterpret_cast<const uint4*>(ta.k_res + (seq * kResidual + (i & (kResidual - 1))) * kD +
-                                                         64 * half);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          const uint4 x = kr[u];
-          const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
+          const uint32_t xs[4] = {kr[u].x, kr[u].y, kr[u].z, kr[u].w};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int c = 64 * half + 8 * u + 2 * e;
@@ -917,10 +981,10 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
           }
         }
       }
-      acc += __shfl_xor(acc, 1);
+      acc += __shfl_xor(acc, 1);  // the token's two threads are both active or both not
       sc = acc;
     }
-    if (half == 0 && tt < kResidual) ps[tt] = sc;
+    if (half == 0) ps[tt] = sc;
     float mw = wave_max(sc);
     if (lane == 0) tred[wave] = mw;
   }
@@ -931,33 +995,36 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   // weights 2^(s - mtail) (mtail = -inf only for an empty tail, which has no tokens)
   if (tid < nt) ps[tid] = exp2f(ps[tid] - mtail);
   __syncthreads();
-  // ---- tail output: thread (channel pair cp, token quarter tq) ----
   {
-    const int cp = tid & 63, tq = tid >> 6;
     float o0 = 0.0f, o1 = 0.0f;
-    const uint32_t* vr = reinterpret_cast<const uint32_t*>(ta.v_res + seq * kResidual * kD) + cp;
-    for (int tt = tq; tt < nt; tt += 4) {
-      const uint32_t x = vr[((T0 + tt) & (kResidual - 1)) * (kD / 2)];
-      o0 = __builtin_fmaf(ps[tt], h2f(x & 0xffffu), o0);
-      o1 = __builtin_fmaf(ps[tt], h2f(x >> 16), o1);
+#pragma unroll
+    for (int u = 0; u < kResidual / 4; ++u) {
+      const int t2 = tq + 4 * u;
+      const float p = (t2 < nt) ? ps[t2] : 0.0f;
+      o0 = __builtin_fmaf(p, h2f(vv[u] & 0xffffu), o0);
+      o1 = __builtin_fmaf(p, h2f(vv[u] >> 16), o1);
     }
     ot[tq][2 * cp] = o0;
     ot[tq][2 * cp + 1] = o1;
   }
-  float ltail = 0.0f;
   if (wave == 0) {  // sum of the weights
     float lsum = 0.0f;
-    for (int tt = lane; tt < nt; tt += 64) lsum += ps[tt];
+    for (int t2 = lane; t2 < nt; t2 += 64) lsum += ps[t2];
     lsum = wave_sum(lsum);
     if (lane == 0) tred[0] = lsum;
   }
 
   // ---- the splits, then everything in the frame of the true maximum ----
-  float M, Ls, Mt, Lt;
-  float4 o, t;
-  merge_splits(ws + seq * nsplit * kRecFloats, nsplit, hd, tid >> 5, tid & 31, M, Ls, o);
+  float M = -__builtin_inff(), Ls = 0.0f, Mt, Lt;
+  float4 o = make_float4(0.f, 0.f, 0.f, 0.f), t;
+  if (sg < nsplit) fold_split_chunk(ch0, M, Ls, o);
+  for (int s0 = sg + 8 * kMergeUnroll; s0 < nsplit; s0 += 8 * kMergeUnroll) {
+    SplitChunk c;
+    load_split_chunk(base, nsplit, hd, q4, s0, c);
+    fold_split_chunk(c, M, Ls, o);
+  }
   combine_groups(M, Ls, o, tid, red, part, Mt, Lt, t);  // (its barriers also order the tail's LDS writes)
-  ltail = tred[0];
+  const float ltail = tred[0];
   if (tid < 32) {
     const float mref = Mt + kLazy;  // the splits' sums are relative to 2^(Mt + kLazy)
     const float mf = fmaxf(mref, mtail);
