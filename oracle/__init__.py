@@ -27,6 +27,9 @@ values     value codec with per-modality rotation R_m (Eq. 6, Eq. 3)
 layout     packed byte layouts and the bits-per-element accounting (Tab. 3)
 attention  decode attention over the quantized cache, two formulations (Eq. 1)
 cache      whole-layer quantization into the packed cache buffers
+residual   decode over the captioning protocol's mixed cache (fp16 residual)
+calibration  modality-aware value-rotation calibration: attention weights, weighted
+           covariance, eigenbasis, R_m = H U_m^T (Eq. 5, Eq. 6)
 
 Parity status: every function is pinned by a ``-m "not gpu"`` test except the
 paper's measured error tables (Tab. 1, Tab. 3 error columns, Tab. 6), which

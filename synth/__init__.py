@@ -10,6 +10,7 @@ can draw from it without sharing any computation.
 from .workloads import (  # noqa: F401
     MOD_AUDIO, MOD_VIDEO, MOD_TEXT, S_SIGN,
     Workload, WORKLOADS, workload, modality_layout, rng_for,
-    gen_keys, gen_values, gen_queries, gen_rotations, gen_signs, gen_lengths,
+    gen_keys, gen_values, gen_queries, gen_rotations, gen_signs, gen_lengths, value_bases,
+    gen_calibration_queries,
     gen_layer, gen_stream_layer, stream_chunk_modalities,
 )

@@ -32,7 +32,7 @@ MOD_AUDIO, MOD_VIDEO, MOD_TEXT = 0, 1, 2
 HEAD_DIM = 128
 
 # stream ids
-S_KEY_NOISE, S_DRIFT, S_OUTLIER, S_VBASIS, S_VCOEF, S_VNOISE, S_ROT, S_SIGN, S_QUERY, S_LEN = range(1, 11)
+S_KEY_NOISE, S_DRIFT, S_OUTLIER, S_VBASIS, S_VCOEF, S_VNOISE, S_ROT, S_SIGN, S_QUERY, S_LEN, S_CALQ = range(1, 12)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -116,6 +116,12 @@ def gen_keys(wid: int, layer: int, b: int, h: int, n: int, d: int = HEAD_DIM) ->
     return k.astype(np.float16)
 
 
+def value_bases(wid: int, layer: int, h: int, d: int = HEAD_DIM, rank: int = 16) -> np.ndarray:
+    """[3][d][rank] the random orthonormal subspace bases of the value generator (audio, video, text)."""
+    g = rng_for(wid, layer, S_VBASIS, 0, h)
+    return np.stack([np.linalg.qr(g.standard_normal((d, rank)))[0] for _ in (MOD_AUDIO, MOD_VIDEO, MOD_TEXT)])
+
+
 def gen_values(wid: int, layer: int, b: int, h: int, modality: np.ndarray, d: int = HEAD_DIM,
                rank: int = 16, noise: float = 0.05) -> np.ndarray:
     """fp16 values [n][d]: B_m c + eps, B_m a random orthonormal d x rank basis per (layer, head, modality)."""
@@ -123,11 +129,10 @@ def gen_values(wid: int, layer: int, b: int, h: int, modality: np.ndarray, d: in
     out = np.empty((n, d))
     coef = rng_for(wid, layer, S_VCOEF, b, h).standard_normal((n, rank))
     eps = noise * rng_for(wid, layer, S_VNOISE, b, h).standard_normal((n, d))
-    g = rng_for(wid, layer, S_VBASIS, 0, h)
+    bases = value_bases(wid, layer, h, d, rank)
     for m in (MOD_AUDIO, MOD_VIDEO, MOD_TEXT):
-        basis, _ = np.linalg.qr(g.standard_normal((d, rank)))
         sel = modality == m
-        out[sel] = coef[sel] @ basis.T
+        out[sel] = coef[sel] @ bases[m].T
     out += eps
     return out.astype(np.float16)
 
@@ -151,6 +156,13 @@ def gen_queries(wid: int, layer: int, batch: int, num_q_heads: int, d: int = HEA
                 step: int = 0) -> np.ndarray:
     """fp16 queries [batch][num_q_heads][d] ~ N(0, 1)."""
     return rng_for(wid, layer, S_QUERY, step, 0).standard_normal((batch, num_q_heads, d)).astype(np.float16)
+
+
+def gen_calibration_queries(wid: int, layer: int, batch: int, num_q_heads: int, n: int,
+                            d: int = HEAD_DIM) -> np.ndarray:
+    """fp16 calibration queries [batch][num_q_heads][n][d] ~ N(0, 1): one per position (the prefill
+    queries whose attention weights Eq. 5 sums)."""
+    return rng_for(wid, layer, S_CALQ).standard_normal((batch, num_q_heads, n, d)).astype(np.float16)
 
 
 def gen_lengths(wl: Workload) -> np.ndarray:
