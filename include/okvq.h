@@ -268,6 +268,57 @@ okvq_status okvq_decode_attention_timed(const okvq_cache* cache, const int32_t* 
                                         float sm_scale, uint32_t flags, float* out, void* workspace,
                                         size_t workspace_bytes, void* stream, void* const* events);
 
+/* ---- Modality-aware value-rotation calibration (Sec. 2.3, Eq. 5 and Eq. 6) ----------------------
+ * Eq. 5 weights every value by how strongly it contributes to the attention output, w_j =
+ * sum_i alpha_{i,j}^2, forms C_m = sum_{j of modality m} w_j v_j^T v_j, and takes U_m from the
+ * eigendecomposition of C_m; Eq. 6 then rotates values by R_m = H U_m^T. The three calls below
+ * produce the okvq_cache.v_rot of a layer from calibration activations: the weights and the
+ * covariance on the device, the eigendecomposition and R_m on the host. Readings: alpha is the
+ * causal softmax attention of every calibration position i over the tokens j <= i, summed over
+ * every query head that reads the KV head; v_j are the raw fp16 values; one C_m per layer (summed
+ * over its sequences and KV heads); H is the layer's randomized Hadamard (the key signs). */
+
+/* Device workspace bytes for okvq_calibration_weights and okvq_value_covariance at n_tokens
+ * positions per sequence (0 for invalid dims). No initial contents are needed. */
+size_t okvq_calibration_workspace_bytes(const okvq_dims* dims, int32_t n_tokens);
+
+/* Attention weights of Eq. 5.
+ *   q          device f16 [B][Hq][n_tokens][128]: the calibration query of every position
+ *   k          device f16 [B][H][n_tokens][128]
+ *   lens_host  host i32 [B], 0 <= lens_host[b] <= n_tokens: positions i < lens_host[b] are queries
+ *              and keys
+ *   sm_scale   softmax scale, normally 1/sqrt(128)
+ *   w          device f32 [B][H][n_tokens] output: w[b][h][t] = sum over the query heads j of KV
+ *              head h (GQA, j / G = h) and the positions i in [t, lens) of alpha_{i,t}^2; zero for
+ *              t >= lens_host[b]
+ * Scores on the matrix cores (fp16 operands, fp32 accumulation), softmax statistics and sums in fp32
+ * (two launches: row statistics, then column sums). */
+okvq_status okvq_calibration_weights(const okvq_dims* dims, const uint16_t* q, const uint16_t* k, int32_t n_tokens,
+                                     const int32_t* lens_host, float sm_scale, float* w, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
+/* Weighted value covariance of Eq. 5.
+ *   v          device f16 [B][H][n_tokens][128]; modality device u8 [B][n_tokens] (0..2)
+ *   w          device f32 [B][H][n_tokens] (okvq_calibration_weights)
+ *   cov        device f32 [3][128][128] output: C_m = sum over sequences, KV heads and tokens
+ *              t < lens_host[b] of modality m of w_t v_t v_t^T (overwritten, not accumulated)
+ * Products on the matrix cores with w v split into fp16 hi + lo parts (about 2^-22 relative per
+ * term), fp32 accumulation; per-chunk partials are summed in a fixed order (deterministic). */
+okvq_status okvq_value_covariance(const okvq_dims* dims, const uint16_t* v, const uint8_t* modality, const float* w,
+                                  int32_t n_tokens, const int32_t* lens_host, float* cov, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* Rotations from the covariances (Eq. 5 eigendecomposition, Eq. 6), on the host, in double
+ * precision (cyclic Jacobi).
+ *   cov          host f32 [3][128][128] (its symmetric part is used)
+ *   signs        host i8 [128], +1 / -1: H = Had diag(s) / sqrt(128), Had the Sylvester matrix
+ *   rot          host f32 [3][128][128] output, R_m = H U_m^T row-major (the okvq_cache.v_rot layout)
+ *   eigenvalues  host f64 [3][128] output in descending order, or NULL
+ * U_m holds the eigenvectors as columns in descending eigenvalue order, each with its largest
+ * component positive (the first one on ties); eigenvectors of equal eigenvalues are not unique. A
+ * modality with C_m = 0 (absent from the calibration data) gets U_m = I, i.e. R_m = H. */
+okvq_status okvq_rotation_from_covariance(const float* cov, const int8_t* signs, float* rot, double* eigenvalues);
+
 #ifdef __cplusplus
 }
 #endif

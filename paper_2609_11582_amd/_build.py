@@ -12,7 +12,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libokvq.so")
-SOURCES = ["api.hip", "codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip"]
+SOURCES = ["api.hip", "codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "calib_kernels.hip"]
 
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",

@@ -1,7 +1,10 @@
 // C ABI of the okvq library: argument validation, launch planning and the fixed codebook.
 // Declarations and contracts: include/okvq.h.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <numeric>
+#include <vector>
 
 #include "okvq.h"
 #include "launch.hpp"
@@ -119,6 +122,52 @@ CacheView view(const okvq_cache* c) {
 }
 
 okvq_status hip_status(hipError_t e) { return e == hipSuccess ? OKVQ_OK : OKVQ_ERR_HIP; }
+
+// ---- host eigensolver of the calibration (Eq. 5): cyclic Jacobi rotations on a symmetric
+// matrix in double precision. Each rotation in the (p, q) plane is chosen to zero a[p][q]; sweeps
+// repeat until the off-diagonal mass is negligible. a (n x n, row-major) is destroyed; the columns of
+// u are the eigenvectors, d the eigenvalues. ----
+void jacobi_eigen(std::vector<double>& a, std::vector<double>& u, std::vector<double>& d, int n) {
+  u.assign((size_t)n * n, 0.0);
+  for (int i = 0; i < n; ++i) u[(size_t)i * n + i] = 1.0;
+  double frob = 0.0;
+  for (double x : a) frob += x * x;
+  for (int sweep = 0; sweep < 100; ++sweep) {
+    double off = 0.0;
+    for (int p = 0; p < n; ++p)
+      for (int q = p + 1; q < n; ++q) off += a[(size_t)p * n + q] * a[(size_t)p * n + q];
+    if (off <= 1e-32 * frob || off == 0.0) break;
+    for (int p = 0; p < n - 1; ++p) {
+      for (int q = p + 1; q < n; ++q) {
+        const double apq = a[(size_t)p * n + q];
+        if (apq == 0.0) continue;
+        const double app = a[(size_t)p * n + p], aqq = a[(size_t)q * n + q];
+        // t = tan(phi) of the rotation that zeroes a[p][q]: the smaller root of t^2 + 2 theta t - 1 = 0
+        const double theta = (aqq - app) / (2.0 * apq);
+        const double t = (theta >= 0.0 ? 1.0 : -1.0) / (std::fabs(theta) + std::sqrt(theta * theta + 1.0));
+        const double c = 1.0 / std::sqrt(t * t + 1.0), s = t * c;
+        for (int k = 0; k < n; ++k) {  // columns p, q
+          const double akp = a[(size_t)k * n + p], akq = a[(size_t)k * n + q];
+          a[(size_t)k * n + p] = c * akp - s * akq;
+          a[(size_t)k * n + q] = s * akp + c * akq;
+        }
+        for (int k = 0; k < n; ++k) {  // rows p, q
+          const double apk = a[(size_t)p * n + k], aqk = a[(size_t)q * n + k];
+          a[(size_t)p * n + k] = c * apk - s * aqk;
+          a[(size_t)q * n + k] = s * apk + c * aqk;
+        }
+        a[(size_t)p * n + q] = a[(size_t)q * n + p] = 0.0;
+        for (int k = 0; k < n; ++k) {
+          const double ukp = u[(size_t)k * n + p], ukq = u[(size_t)k * n + q];
+          u[(size_t)k * n + p] = c * ukp - s * ukq;
+          u[(size_t)k * n + q] = s * ukp + c * ukq;
+        }
+      }
+    }
+  }
+  d.resize(n);
+  for (int i = 0; i < n; ++i) d[i] = a[(size_t)i * n + i];
+}
 
 // Tiles of 256 tokens covering `span` tokens from each sequence's first open window.
 void plan_tiles(CodecArgs& a, int nb, int span) {
@@ -407,6 +456,105 @@ okvq_status okvq_decode_attention_timed(const okvq_cache* cache, const int32_t* 
                                         size_t workspace_bytes, void* stream, void* const* events) {
   if (!events) return OKVQ_ERR_INVALID_ARGUMENT;
   return decode_impl(cache, lens_host, q, sm_scale, flags, out, workspace, workspace_bytes, stream, events);
+}
+
+size_t okvq_calibration_workspace_bytes(const okvq_dims* dims, int32_t n_tokens) {
+  if (check_dims(dims) != OKVQ_OK || n_tokens < 1) return 0;
+  return calib_workspace_bytes(dims->batch, dims->num_kv_heads, dims->num_q_heads, n_tokens);
+}
+
+okvq_status okvq_calibration_weights(const okvq_dims* dims, const uint16_t* q, const uint16_t* k, int32_t n_tokens,
+                                     const int32_t* lens_host, float sm_scale, float* w, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  okvq_status st = check_dims(dims);
+  if (st != OKVQ_OK) return st;
+  if (n_tokens < 1 || !lens_host || !std::isfinite(sm_scale)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(w)) return OKVQ_ERR_INVALID_ARGUMENT;
+  for (int b = 0; b < dims->batch; ++b)
+    if (lens_host[b] < 0 || lens_host[b] > n_tokens) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(workspace) ||
+      workspace_bytes < calib_workspace_bytes(dims->batch, dims->num_kv_heads, dims->num_q_heads, n_tokens))
+    return OKVQ_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
+    const int nb = std::min(kMaxLenArgs, dims->batch - b0);
+    LenArgs la{};
+    for (int i = 0; i < nb; ++i) la.lens[i] = lens_host[b0 + i];
+    st = hip_status(launch_calib_weights(q, k, la, b0, nb, n_tokens, dims->num_kv_heads, dims->num_q_heads, sm_scale,
+                                         w, workspace, s));
+    if (st != OKVQ_OK) return st;
+  }
+  return OKVQ_OK;
+}
+
+okvq_status okvq_value_covariance(const okvq_dims* dims, const uint16_t* v, const uint8_t* modality, const float* w,
+                                  int32_t n_tokens, const int32_t* lens_host, float* cov, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  okvq_status st = check_dims(dims);
+  if (st != OKVQ_OK) return st;
+  if (n_tokens < 1 || !lens_host) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(v) || !aligned16(modality) || !aligned16(w) || !aligned16(cov)) return OKVQ_ERR_INVALID_ARGUMENT;
+  for (int b = 0; b < dims->batch; ++b)
+    if (lens_host[b] < 0 || lens_host[b] > n_tokens) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(workspace) ||
+      workspace_bytes < calib_workspace_bytes(dims->batch, dims->num_kv_heads, dims->num_q_heads, n_tokens))
+    return OKVQ_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int H = dims->num_kv_heads, nchunk = (n_tokens + kCalibChunk - 1) / kCalibChunk;
+  const int nparts = dims->batch * H * nchunk;
+  for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
+    const int nb = std::min(kMaxLenArgs, dims->batch - b0);
+    LenArgs la{};
+    for (int i = 0; i < nb; ++i) la.lens[i] = lens_host[b0 + i];
+    const bool last = b0 + nb >= dims->batch;
+    st = hip_status(launch_calib_covariance(v, modality, w, la, b0, nb, n_tokens, H, static_cast<float*>(workspace),
+                                            b0 * H * nchunk, cov, last, nparts, s));
+    if (st != OKVQ_OK) return st;
+  }
+  return OKVQ_OK;
+}
+
+okvq_status okvq_rotation_from_covariance(const float* cov, const int8_t* signs, float* rot, double* eigenvalues) {
+  if (!cov || !signs || !rot) return OKVQ_ERR_INVALID_ARGUMENT;
+  constexpr int n = 128;
+  for (int i = 0; i < n; ++i)
+    if (signs[i] != 1 && signs[i] != -1) return OKVQ_ERR_INVALID_ARGUMENT;
+  for (int i = 0; i < 3 * n * n; ++i)
+    if (!std::isfinite(cov[i])) return OKVQ_ERR_INVALID_ARGUMENT;
+  const double inv_sqrt_n = 1.0 / std::sqrt((double)n);
+  for (int m = 0; m < 3; ++m) {
+    std::vector<double> a((size_t)n * n), u, d;
+    for (int r = 0; r < n; ++r)  // the symmetric part (the device sums are symmetric up to rounding)
+      for (int c = 0; c < n; ++c)
+        a[(size_t)r * n + c] = 0.5 * ((double)cov[((size_t)m * n + r) * n + c] + (double)cov[((size_t)m * n + c) * n + r]);
+    jacobi_eigen(a, u, d, n);
+    std::vector<int> order(n);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return d[x] > d[y]; });
+    // U_m: eigenvectors as columns in descending eigenvalue order, each with its largest-magnitude
+    // component positive (the first such component on ties)
+    std::vector<double> U((size_t)n * n);
+    for (int k = 0; k < n; ++k) {
+      const int src = order[k];
+      int imax = 0;
+      for (int i = 1; i < n; ++i)
+        if (std::fabs(u[(size_t)i * n + src]) > std::fabs(u[(size_t)imax * n + src])) imax = i;
+      const double sg = u[(size_t)imax * n + src] < 0.0 ? -1.0 : 1.0;
+      for (int i = 0; i < n; ++i) U[(size_t)i * n + k] = sg * u[(size_t)i * n + src];
+      if (eigenvalues) eigenvalues[m * n + k] = d[src];
+    }
+    // R_m = H U_m^T (Eq. 6), H = Had diag(s) / sqrt(128), Had[a][k] = (-1)^popcount(a & k)
+    for (int r = 0; r < n; ++r)
+      for (int c = 0; c < n; ++c) {
+        double acc = 0.0;
+        for (int k = 0; k < n; ++k) {
+          const double h = ((__builtin_popcount(r & k) & 1) ? -1.0 : 1.0) * signs[k];
+          acc += h * U[(size_t)c * n + k];
+        }
+        rot[((size_t)m * n + r) * n + c] = (float)(acc * inv_sqrt_n);
+      }
+  }
+  return OKVQ_OK;
 }
 
 }  // extern "C"

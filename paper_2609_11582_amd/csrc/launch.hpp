@@ -70,6 +70,17 @@ hipError_t launch_residual_store(const uint16_t* k_new, const uint16_t* v_new, i
                                  const int32_t* count_dev, int B, int H, int cap, uint16_t* k_res, uint16_t* v_res,
                                  hipStream_t s);
 
+// Value-rotation calibration (Eq. 5): attention weights of up to 256 sequences per launch (the
+// workspace holds their row statistics), weighted covariance partials per (sequence, head, 64-token
+// chunk) and their reduction.
+size_t calib_workspace_bytes(int B, int H, int Hq, int N);
+hipError_t launch_calib_weights(const uint16_t* q, const uint16_t* k, const LenArgs& lens, int b0, int nb, int N,
+                                int H, int Hq, float sm_scale, float* w, void* ws, hipStream_t s);
+hipError_t launch_calib_covariance(const uint16_t* v, const uint8_t* modality, const float* w, const LenArgs& lens,
+                                   int b0, int nb, int N, int H, float* partial, int part0, float* cov, bool reduce,
+                                   int nparts_total, hipStream_t s);
+constexpr int kCalibChunk = 64;  // tokens per covariance partial
+
 struct CacheView {
   int B, H, Hq, cap;
   uint8_t* k_codes;

@@ -84,6 +84,14 @@ def lib() -> ctypes.CDLL:
         L.okvq_decode_attention_timed.restype = i32
         L.okvq_decode_attention_timed.argtypes = [P(CacheStruct), P(i32), vp, ctypes.c_float, u32, vp, vp, sz, vp,
                                                   P(vp)]
+        L.okvq_calibration_workspace_bytes.restype = sz
+        L.okvq_calibration_workspace_bytes.argtypes = [P(Dims), i32]
+        L.okvq_calibration_weights.restype = i32
+        L.okvq_calibration_weights.argtypes = [P(Dims), vp, vp, i32, P(i32), ctypes.c_float, vp, vp, sz, vp]
+        L.okvq_value_covariance.restype = i32
+        L.okvq_value_covariance.argtypes = [P(Dims), vp, vp, vp, i32, P(i32), vp, vp, sz, vp]
+        L.okvq_rotation_from_covariance.restype = i32
+        L.okvq_rotation_from_covariance.argtypes = [vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -260,6 +268,63 @@ def okvq_decode_attention_timed(cache: "KVCache", lens, q, sm_scale, out, worksp
                                            _ptr(out), _ptr(workspace), int(nbytes), _stream(stream), handles)
     if check:
         _check(st, "okvq_decode_attention_timed")
+    return st
+
+
+def okvq_calibration_workspace_bytes(dims: Dims, n_tokens: int) -> int:
+    return lib().okvq_calibration_workspace_bytes(ctypes.byref(dims), int(n_tokens))
+
+
+def calibration_workspace(dims: Dims, n_tokens: int, device="cuda") -> torch.Tensor:
+    """A calibration workspace of okvq_calibration_workspace_bytes bytes (no contents needed)."""
+    nbytes = max(okvq_calibration_workspace_bytes(dims, n_tokens), 16)
+    return torch.empty((nbytes + 15) // 16 * 4, dtype=torch.float32, device=device)
+
+
+def okvq_calibration_weights(dims, q, k, n_tokens, lens, sm_scale, w, workspace, stream=None, check=True) -> int:
+    B, H, Hq = dims.batch, dims.num_kv_heads, dims.num_q_heads
+    _need_len(lens, B, "lens")
+    _need(q, B * Hq * int(n_tokens) * 128 * 2, "q")
+    _need(k, B * H * int(n_tokens) * 128 * 2, "k")
+    _need(w, B * H * int(n_tokens) * 4, "w")
+    have = workspace.numel() * workspace.element_size()
+    st = lib().okvq_calibration_weights(ctypes.byref(dims), _ptr(q), _ptr(k), int(n_tokens), _i32(lens),
+                                        float(sm_scale), _ptr(w), _ptr(workspace), int(have), _stream(stream))
+    if check:
+        _check(st, "okvq_calibration_weights")
+    return st
+
+
+def okvq_value_covariance(dims, v, modality, w, n_tokens, lens, cov, workspace, stream=None, check=True) -> int:
+    B, H = dims.batch, dims.num_kv_heads
+    _need_len(lens, B, "lens")
+    _need(v, B * H * int(n_tokens) * 128 * 2, "v")
+    _need(modality, B * int(n_tokens), "modality")
+    _need(w, B * H * int(n_tokens) * 4, "w")
+    _need(cov, 3 * 128 * 128 * 4, "cov")
+    have = workspace.numel() * workspace.element_size()
+    st = lib().okvq_value_covariance(ctypes.byref(dims), _ptr(v), _ptr(modality), _ptr(w), int(n_tokens), _i32(lens),
+                                     _ptr(cov), _ptr(workspace), int(have), _stream(stream))
+    if check:
+        _check(st, "okvq_value_covariance")
+    return st
+
+
+def okvq_rotation_from_covariance(cov, signs, rot, eigenvalues=None, check=True) -> int:
+    """Host call: cov float32 [3][128][128], signs int8 [128], rot float32 [3][128][128] (output),
+    eigenvalues float64 [3][128] (output) or None -- C-contiguous numpy arrays."""
+    import numpy as np
+    for name, a, dt, n in (("cov", cov, np.float32, 3 * 128 * 128), ("signs", signs, np.int8, 128),
+                           ("rot", rot, np.float32, 3 * 128 * 128)):
+        if not isinstance(a, np.ndarray) or a.dtype != dt or not a.flags["C_CONTIGUOUS"] or a.size < n:
+            raise ValueError(f"{name}: expected a contiguous {np.dtype(dt).name} numpy array of {n} elements")
+    if eigenvalues is not None and (eigenvalues.dtype != np.float64 or not eigenvalues.flags["C_CONTIGUOUS"]
+                                    or eigenvalues.size < 3 * 128):
+        raise ValueError("eigenvalues: expected a contiguous float64 numpy array of 384 elements")
+    st = lib().okvq_rotation_from_covariance(cov.ctypes.data, signs.ctypes.data, rot.ctypes.data,
+                                             None if eigenvalues is None else eigenvalues.ctypes.data)
+    if check:
+        _check(st, "okvq_rotation_from_covariance")
     return st
 
 

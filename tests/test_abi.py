@@ -185,3 +185,88 @@ def test_package_exports_a_binding_for_every_declared_function():
             continue
         assert hasattr(pkg, n), n
     assert hasattr(pkg, "decode_workspace") and hasattr(pkg, "KVCache")
+
+
+def _gaps(ev):
+    """relative distance of each eigenvalue to its nearest neighbour"""
+    d = np.abs(ev[:, None] - ev[None, :]) + np.eye(len(ev)) * 1e300
+    return d.min(axis=1) / max(abs(ev).max(), 1e-300)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_rotation_from_covariance_matches_oracle(seed):
+    """The library's host eigensolver (cyclic Jacobi, double) against numpy's eigh in the oracle,
+    on the same fp32 covariances: eigenvalues to 1e-12 of the largest, eigenvectors of separated
+    eigenvalues (relative gap > 1e-6) to 1e-9 / gap, every R_m orthogonal."""
+    from oracle.calibration import rotation_from_covariance
+    from synth import gen_signs
+    okvq = _lib()
+    rng = np.random.default_rng(seed)
+    if seed == 0:  # a random eigenbasis with evenly spaced eigenvalues: every eigenvector is unique
+        Q = np.linalg.qr(rng.standard_normal((3, 128, 128)))[0]
+        cov = (Q * np.linspace(10.0, 1.0, 128)) @ Q.transpose(0, 2, 1)
+    else:          # a Wishart-like matrix with a wide spectrum
+        A = rng.standard_normal((3, 128, 128)) * np.geomspace(1.0, 1e-3, 128)
+        cov = A @ A.transpose(0, 2, 1)
+    cov = ((cov + cov.transpose(0, 2, 1)) / 2).astype(np.float32)
+    signs = gen_signs(9, seed)
+    rot = np.zeros((3, 128, 128), np.float32)
+    ev = np.zeros((3, 128), np.float64)
+    okvq.okvq_rotation_from_covariance(cov, signs, rot, ev)
+    R_ref, ev_ref, U_ref = rotation_from_covariance(cov.astype(np.float64), signs)
+    from oracle.hadamard import randomized_hadamard
+    H = randomized_hadamard(signs)
+    for m in range(3):
+        np.testing.assert_allclose(ev[m], ev_ref[m], rtol=0, atol=1e-12 * ev_ref[m].max())
+        U = H.T @ rot[m].astype(np.float64)   # rows: U_m^T
+        g = _gaps(ev_ref[m])
+        sep = g > 1e-6
+        assert sep.sum() >= (128 if seed == 0 else 60)
+        err = np.abs(U - U_ref[m].T).max(axis=1)
+        assert np.all(err[sep] <= 1e-9 / g[sep] + 1e-6), err[sep].max()  # 1e-6: the fp32 output
+        np.testing.assert_allclose(rot[m].astype(np.float64) @ rot[m].T, np.eye(128), atol=1e-6)
+
+
+def test_rotation_from_covariance_special_cases_and_validation():
+    from oracle.hadamard import randomized_hadamard
+    from synth import gen_signs
+    okvq = _lib()
+    signs = gen_signs(3, 0)
+    H = randomized_hadamard(signs)
+    rot = np.zeros((3, 128, 128), np.float32)
+    cov = np.zeros((3, 128, 128), np.float32)
+    cov[1] = np.diag(np.linspace(4.0, 1.0, 128))       # U = I
+    cov[2] = np.diag(np.linspace(1.0, 4.0, 128))       # U = reversal
+    okvq.okvq_rotation_from_covariance(cov, signs, rot)
+    np.testing.assert_allclose(rot[0], H, atol=1e-7)   # an absent modality (C = 0) gets R = H
+    np.testing.assert_allclose(rot[1], H, atol=1e-7)
+    np.testing.assert_allclose(rot[2], H[:, ::-1], atol=1e-7)
+    L = okvq.lib()
+    bad = signs.copy()
+    bad[5] = 0
+    assert okvq.okvq_rotation_from_covariance(cov, bad, rot, check=False) == -1
+    nan = cov.copy()
+    nan[0, 3, 4] = np.nan
+    assert okvq.okvq_rotation_from_covariance(nan, signs, rot, check=False) == -1
+    assert L.okvq_rotation_from_covariance(None, signs.ctypes.data, rot.ctypes.data, None) == -1
+
+
+def test_calibration_validation():
+    okvq = _lib()
+    L = okvq.lib()
+    d = okvq.make_dims(2, 2, 8, 64)
+    assert okvq.okvq_calibration_workspace_bytes(d, 100) > 0
+    assert okvq.okvq_calibration_workspace_bytes(okvq.make_dims(2, 2, 8, 64, head_dim=64), 100) == 0
+    assert okvq.okvq_calibration_workspace_bytes(d, 0) == 0
+    fake = ctypes.c_void_p(4096)
+    lens = (ctypes.c_int32 * 2)(100, 50)
+    big = 1 << 30
+    sm = ctypes.c_float(0.1)
+    assert L.okvq_calibration_weights(ctypes.byref(d), fake, fake, 100, lens, sm, fake, fake, 16, None) == -4
+    assert L.okvq_calibration_weights(ctypes.byref(d), ctypes.c_void_p(4100), fake, 100, lens, sm, fake, fake, big,
+                                      None) == -1
+    over = (ctypes.c_int32 * 2)(101, 50)
+    assert L.okvq_calibration_weights(ctypes.byref(d), fake, fake, 100, over, sm, fake, fake, big, None) == -1
+    assert L.okvq_value_covariance(ctypes.byref(d), fake, fake, fake, 100, lens, fake, fake, 16, None) == -4
+    assert L.okvq_value_covariance(ctypes.byref(d), fake, fake, fake, 100, over, fake, fake, big, None) == -1
+    assert L.okvq_value_covariance(ctypes.byref(d), fake, fake, fake, 0, lens, fake, fake, big, None) == -1
