@@ -26,6 +26,9 @@ Reported (one JSON line):
                   token and KV head): append, decode and split-K kernel time, effective GB/s
   residual        the same workload in the captioning protocol (fp16 rings of the last 128 keys and
                   values): prefill and one-token append, decode, split-K and merge-with-tail times
+  calibration     the value-rotation calibration (Eq. 5) on a 4096-token calibration sequence at the
+                  same head shapes: attention weights (against the fp16 matrix-core peak), weighted
+                  covariance, host eigensolver
 
 --profile-pass runs a short fixed sequence for rocprofv3 counter collection: a 256 MiB device
 copy (calibrates FETCH_SIZE / WRITE_SIZE against a known byte count), 8 decode calls on cold
@@ -61,7 +64,7 @@ APPEND_BYTES_PER_TOKEN_HEAD_MX = 2 * 256 + 68 + MX_RECORD / 32
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
 CALIBRATION_COPY_BYTES = 256 << 20
 KERNEL_SOURCES = ("codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "key_quant.hpp", "value_quant.hpp",
-                  "okvq_device.hpp", "launch.hpp")
+                  "okvq_device.hpp", "launch.hpp", "calib_kernels.hip")
 
 
 def kernel_source_hash() -> str:
@@ -338,6 +341,55 @@ def residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
             "algorithmic_bytes": dbytes, "replicas": n_cache}
 
 
+CALIB_TOKENS = 4096
+
+
+def calibration_measurement(okvq, torch, np, wl, dev):
+    """Value-rotation calibration (Eq. 5, Eq. 6) at the benchmark layer's head shapes on one
+    4096-token calibration sequence: attention weights (row statistics and column sums on the
+    matrix cores), weighted covariance, and the host eigensolver."""
+    from synth import gen_calibration_queries, gen_layer
+    H, Hq, N = wl.num_kv_heads, wl.num_q_heads, CALIB_TOKENS
+    lay = gen_layer(wl, 1, lengths=np.array([N], np.int32), n_tokens=N)
+    q = torch.from_numpy(gen_calibration_queries(wl.wid, 1, 1, Hq, N)).to(dev)
+    k = torch.from_numpy(lay["k"]).to(dev)
+    v = torch.from_numpy(lay["v"]).to(dev)
+    mod = torch.from_numpy(lay["modality"]).to(dev)
+    dims = okvq.make_dims(1, H, Hq, 32)
+    ws = okvq.calibration_workspace(dims, N, device=dev)
+    w = torch.empty((1, H, N), dtype=torch.float32, device=dev)
+    cov = torch.empty((3, 128, 128), dtype=torch.float32, device=dev)
+    sm = 1 / math.sqrt(128)
+    for _ in range(3):
+        okvq.okvq_calibration_weights(dims, q, k, N, [N], sm, w, ws)
+        okvq.okvq_value_covariance(dims, v, mod, w, N, [N], cov, ws)
+    torch.cuda.synchronize()
+    reps = 10
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e[0].record()
+    for _ in range(reps):
+        okvq.okvq_calibration_weights(dims, q, k, N, [N], sm, w, ws)
+    e[1].record()
+    for _ in range(reps):
+        okvq.okvq_value_covariance(dims, v, mod, w, N, [N], cov, ws)
+    e[2].record()
+    torch.cuda.synchronize()
+    weights_us = e[0].elapsed_time(e[1]) * 1e3 / reps
+    cov_us = e[1].elapsed_time(e[2]) * 1e3 / reps
+    c_host = cov.cpu().numpy()
+    rot = np.zeros((3, 128, 128), np.float32)
+    t0 = time.perf_counter()
+    okvq.okvq_rotation_from_covariance(c_host, np.ascontiguousarray(lay["signs"], np.int8), rot)
+    eig_ms = (time.perf_counter() - t0) * 1e3
+    # algorithmic work of the weights: two passes over the causal score triangle of every query head
+    flops = 2 * Hq * (N * (N + 1) // 2) * 128 * 2
+    tflops = flops / weights_us / 1e6
+    return {"tokens": N, "kv_heads": H, "q_heads": Hq, "weights_us": round(weights_us, 2),
+            "weights_roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": 2500.0, "unit": "TFLOP/s",
+                                 "frac": round(tflops / 2500.0, 4), "algorithmic_flops": flops},
+            "covariance_us": round(cov_us, 2), "eigensolver_host_ms": round(eig_ms, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -538,6 +590,7 @@ def main():
     }
     line["mxfp4"] = mx_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                    args.decode_iters)
+    line["calibration"] = calibration_measurement(okvq, torch, np, wl, dev)
     line["residual"] = residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                             args.decode_iters)
     if not args.no_cpu_baseline:

@@ -12,8 +12,9 @@
 //
 //  k_calib_rowstats   (m_i, l_i) of every query row: base-2 running max and sum of 2^(s - m)
 //                     over the causal keys (one wave per 16 queries, keys in blocks of 16);
-//  k_calib_colweights w_j for every key: per wave 16 keys, every later query block of every query
-//                     head of the group, alpha = 2^(s - m_i) / l_i squared and summed;
+//  k_calib_colweights per query head, the sum over its queries of alpha^2 for every key (per wave
+//                     16 keys, every later query tile), alpha = 2^(s - m_i) / l_i;
+//  k_calib_groupsum   w_j = the sum over the query heads of the group;
 //  k_calib_covariance partial C_m of a 64-token chunk on the matrix cores (A = w v split into fp16
 //                     hi + lo parts, B = v), one partial per (chunk, modality);
 //  k_calib_reduce     C_m = the sum of the partials, in a fixed order.
@@ -45,6 +46,23 @@ __device__ __forceinline__ void load_frag(const uint16_t* base, int row, int val
   }
 }
 
+// max over the 16 lanes of a DPP row (lanes 16 g .. 16 g + 15), in every lane: row rotations by
+// 1, 2, 4, 8 on the VALU (no LDS-pipe shuffle)
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x121, 0xf, 0xf, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x122, 0xf, 0xf, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x124, 0xf, 0xf, false)));
+  v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x128, 0xf, 0xf, false)));
+  return v;
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x121, 0xf, 0xf, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x122, 0xf, 0xf, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x124, 0xf, 0xf, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x128, 0xf, 0xf, false));
+  return v;
+}
+
 __device__ __forceinline__ c_floatx4 score_block(const uint4 (&a)[4], const uint4 (&b)[4]) {
   c_floatx4 d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -52,63 +70,95 @@ __device__ __forceinline__ c_floatx4 score_block(const uint4 (&a)[4], const uint
   return d;
 }
 
-// ---- pass 1: row statistics. Grid (query tiles, Hq, sequences of the launch). stats[(bz Hq + j) N + i]
-// = (m_i, l_i) with
-// m in base-2 score units (scores times sm_scale log2 e) and l_i = sum_{t <= i} 2^(s_it - m_i) ----
+// Cooperative tile staging: 64 token rows (fp16 [128]) = 1024 uint4, four per thread of the
+// work-group. Rows at or beyond `valid` read as zero.
+struct TileRegs {
+  uint4 x[4];
+};
+__device__ __forceinline__ void tile_load(const uint16_t* base, int row0, int valid, int tid, TileRegs& r) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int idx = tid + kCalThreads * u, row = row0 + (idx >> 4), part = idx & 15;
+    r.x[u] = (row < valid) ? reinterpret_cast<const uint4*>(base + (size_t)row * kD)[part] : make_uint4(0, 0, 0, 0);
+  }
+}
+// LDS tile [64 rows][128 + 8 halves] (the pad spreads the fragment reads over the banks)
+constexpr int kTilePitch = kD + 8;
+__device__ __forceinline__ void tile_store(_Float16* t, int tid, const TileRegs& r) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int idx = tid + kCalThreads * u;
+    *reinterpret_cast<uint4*>(t + (idx >> 4) * kTilePitch + 8 * (idx & 15)) = r.x[u];
+  }
+}
+// the four k-block fragments of tile row `row` for this lane
+__device__ __forceinline__ void tile_frag(const _Float16* t, int row, int lane, uint4 (&f)[4]) {
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) f[kb] = *reinterpret_cast<const uint4*>(t + row * kTilePitch + 32 * kb + 8 * (lane >> 4));
+}
+
+// ---- pass 1: row statistics. Grid (query tiles of 64, Hq, sequences of the launch); wave w holds
+// queries 16 w .. 16 w + 15 of the tile in registers and walks the causal key tiles of 64 (staged
+// in LDS, the next one loading during the current one's MFMAs). stats[(bz Hq + j) N + i] =
+// (m_i, l_i): m in base-2 score units (scores times sm_scale log2 e), l_i = sum_{t <= i} 2^(s_it - m_i).
+// The running max is shared by the 16 lanes of a row (reduced once per tile), so every lane keeps
+// a partial sum relative to it ----
 __global__ __launch_bounds__(kCalThreads) void k_calib_rowstats(const uint16_t* __restrict__ q,
                                                                 const uint16_t* __restrict__ k, LenArgs lens, int b0,
                                                                 int N, int H, int Hq, float scale2,
                                                                 float2* __restrict__ stats) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ __attribute__((aligned(16))) _Float16 kt[2][kCalTile * kTilePitch];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int j = blockIdx.y, bz = blockIdx.z, b = b0 + bz;
   const int G = Hq / H, h = j / G;
   const int L = min(max(lens.lens[bz], 0), N);
-  const int i0 = blockIdx.x * kCalTile + 16 * wave;  // this wave's 16 queries
-  if (i0 >= L) return;
-  const uint16_t* qb = q + ((size_t)b * Hq + j) * N * kD;
+  const int q0 = blockIdx.x * kCalTile;
+  if (q0 >= L) return;  // (uniform over the work-group)
+  const int i0 = q0 + 16 * wave;
   const uint16_t* kbase = k + ((size_t)b * H + h) * N * kD;
-  uint4 qa[4];
-  load_frag(qb, i0 + (lane & 15), L, lane, qa);
   const int col = lane & 15, g = lane >> 4;
+  uint4 qa[4];
+  load_frag(q + ((size_t)b * Hq + j) * N * kD, i0 + col, L, lane, qa);
   float m[4], l[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     m[i] = -__builtin_inff();
     l[i] = 0.0f;
   }
-  const int t_end = min(i0 + 16, L);  // causal: keys up to the last query of the block
-  uint4 kf[4], kn[4];
-  load_frag(kbase, col, t_end, lane, kf);
-  for (int t0 = 0; t0 < t_end; t0 += 16) {
-    if (t0 + 16 < t_end) load_frag(kbase, t0 + 16 + col, t_end, lane, kn);
-    const c_floatx4 d = score_block(qa, kf);
-    const int t = t0 + col;
+  const int t_end = min(q0 + kCalTile, L);  // keys of the tiles up to the diagonal one
+  TileRegs r;
+  tile_load(kbase, 0, t_end, tid, r);
+  int buf = 0;
+  for (int t0 = 0; t0 < t_end; t0 += kCalTile, buf ^= 1) {
+    tile_store(kt[buf], tid, r);
+    __syncthreads();  // (also: every wave is done with this buffer's previous tile, two tiles ago)
+    if (t0 + kCalTile < t_end) tile_load(kbase, t0 + kCalTile, t_end, tid, r);
+    float s[4][4];  // [key block][row]
+    // a tile whose keys all precede the wave's first query and the length needs no mask
+    const bool open = t0 + kCalTile - 1 <= i0 && t0 + kCalTile <= L;  // (wave-uniform)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int qi = i0 + 4 * g + i;
-      if (t <= qi && t < L) {
-        const float s = d[i] * scale2;
-        const float mn = fmaxf(m[i], s);
-        l[i] = l[i] * exp2f(m[i] - mn) + exp2f(s - mn);  // m = -inf at first: exp2(-inf) = 0
-        m[i] = mn;
+    for (int kb4 = 0; kb4 < 4; ++kb4) {
+      uint4 kf[4];
+      tile_frag(kt[buf], 16 * kb4 + col, lane, kf);
+      const c_floatx4 d = score_block(qa, kf);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = t0 + 16 * kb4 + col, qi = i0 + 4 * g + i;
+        s[kb4][i] = (open || (t <= qi && t < L)) ? d[i] * scale2 : -__builtin_inff();
       }
     }
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) kf[kb] = kn[kb];
-  }
-  // combine the 16 lanes of each row group (lanes 16 g .. 16 g + 15 hold rows 4 g .. 4 g + 3)
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      const float mo = __shfl_xor(m[i], off), lo = __shfl_xor(l[i], off);
-      const float mn = fmaxf(m[i], mo);
-      const float a = (m[i] == -__builtin_inff()) ? 0.0f : l[i] * exp2f(m[i] - mn);
-      const float c = (mo == -__builtin_inff()) ? 0.0f : lo * exp2f(mo - mn);
+    for (int i = 0; i < 4; ++i) {
+      const float tm = row16_max(fmaxf(fmaxf(s[0][i], s[1][i]), fmaxf(s[2][i], s[3][i])));
+      const float mn = fmaxf(m[i], tm);
+      if (mn == -__builtin_inff()) continue;  // nothing visible to this row yet
+      l[i] = l[i] * exp2f(m[i] - mn) + (exp2f(s[0][i] - mn) + exp2f(s[1][i] - mn)) +
+             (exp2f(s[2][i] - mn) + exp2f(s[3][i] - mn));
       m[i] = mn;
-      l[i] = a + c;
     }
   }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) l[i] = row16_sum(l[i]);
   if (col < 4) {  // lane 16 g + i writes row 4 g + i
     const int i = col, qi = i0 + 4 * g + i;
     const float mv = i == 0 ? m[0] : i == 1 ? m[1] : i == 2 ? m[2] : m[3];
@@ -117,60 +167,81 @@ __global__ __launch_bounds__(kCalThreads) void k_calib_rowstats(const uint16_t* 
   }
 }
 
-// ---- pass 2: column weights. Grid (key tiles, H, B). w[(b H + h) N + t] for t < L (zero beyond) ----
+// ---- pass 2: column weights of one query head. Grid (key tiles of 64, Hq, sequences of the
+// launch); wave w holds keys 16 w .. 16 w + 15 of the tile in registers and walks the head's query
+// tiles from the diagonal on (staged in LDS with their statistics as (2 m, 1 / l^2), so that
+// alpha^2 = 2^(2 s - 2 m) / l^2 takes one exp2). wq[(bz Hq + j) N + t]: the head's sum over queries
+// (zero beyond L); k_calib_groupsum adds the heads of each group ----
 __global__ __launch_bounds__(kCalThreads) void k_calib_colweights(const uint16_t* __restrict__ q,
                                                                   const uint16_t* __restrict__ k, LenArgs lens,
                                                                   int b0, int N, int H, int Hq, float scale2,
                                                                   const float2* __restrict__ stats,
-                                                                  float* __restrict__ w) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int h = blockIdx.y, bz = blockIdx.z, b = b0 + bz;
-  const int G = Hq / H;
+                                                                  float* __restrict__ wq) {
+  __shared__ __attribute__((aligned(16))) _Float16 qt[2][kCalTile * kTilePitch];
+  __shared__ __attribute__((aligned(16))) float2 st2[2][kCalTile];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int j = blockIdx.y, bz = blockIdx.z, b = b0 + bz;
+  const int G = Hq / H, h = j / G;
   const int L = min(max(lens.lens[bz], 0), N);
-  const int t0 = blockIdx.x * kCalTile + 16 * wave;  // this wave's 16 keys
+  const int k0 = blockIdx.x * kCalTile;
+  const int t0 = k0 + 16 * wave;  // this wave's 16 keys
   const int col = lane & 15, g = lane >> 4;
-  if (t0 >= N) return;
+  const int t = t0 + col;
   float acc = 0.0f;
-  if (t0 < L) {
+  if (k0 < L) {  // (uniform over the work-group)
     uint4 kf[4];
     load_frag(k + ((size_t)b * H + h) * N * kD, t0 + col, L, lane, kf);
-    const int t = t0 + col;
-    for (int jj = 0; jj < G; ++jj) {
-      const int j = h * G + jj;
-      const uint16_t* qb = q + ((size_t)b * Hq + j) * N * kD;
-      const float2* st = stats + ((size_t)bz * Hq + j) * N;
-      uint4 qa[4], qn[4];
-      float2 sr[4], sn[4];
-      auto load_block = [&](int i0, uint4 (&f)[4], float2 (&s)[4]) {
-        load_frag(qb, i0 + col, L, lane, f);
+    const float scale2x = 2.0f * scale2;
+    const int ntile = (L - k0 + kCalTile - 1) / kCalTile;  // query tiles from the diagonal on
+    const uint16_t* qb = q + ((size_t)b * Hq + j) * N * kD;
+    const float2* sb = stats + ((size_t)bz * Hq + j) * N;
+    auto load = [&](int it, TileRegs& r, float2& sv) {
+      const int qtile = k0 + kCalTile * it;
+      tile_load(qb, qtile, L, tid, r);
+      sv = make_float2(0.f, 0.f);
+      if (tid < kCalTile && qtile + tid < L) sv = sb[qtile + tid];
+    };
+    TileRegs r;
+    float2 sv;
+    load(0, r, sv);
+    for (int it = 0, buf = 0; it < ntile; ++it, buf ^= 1) {
+      tile_store(qt[buf], tid, r);
+      // a query beyond the length gets (2 m, 1 / l^2) = (+inf, 0): its alpha^2 is 2^-inf * 0 = 0
+      if (tid < kCalTile)
+        st2[buf][tid] = (sv.y > 0.0f) ? make_float2(2.0f * sv.x, 1.0f / (sv.y * sv.y)) : make_float2(__builtin_inff(), 0.0f);
+      __syncthreads();
+      if (it + 1 < ntile) load(it + 1, r, sv);
+      const int qtile = k0 + kCalTile * it;
+      const bool diag = it == 0;  // the only query tile that holds queries before the wave's keys
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int qi = i0 + 4 * g + i;
-          s[i] = (qi < L) ? st[qi] : make_float2(0.f, 1.f);
-        }
-      };
-      load_block(t0, qa, sr);  // causal: queries from the wave's first key on
-      for (int i0 = t0; i0 < L; i0 += 16) {
-        if (i0 + 16 < L) load_block(i0 + 16, qn, sn);
+      for (int qb4 = 0; qb4 < 4; ++qb4) {
+        uint4 qa[4];
+        tile_frag(qt[buf], 16 * qb4 + col, lane, qa);
         const c_floatx4 d = score_block(qa, kf);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int qi = i0 + 4 * g + i;
-          if (t <= qi && qi < L && t < L) {
-            const float a = exp2f(d[i] * scale2 - sr[i].x) / sr[i].y;
-            acc = __builtin_fmaf(a, a, acc);
-          }
+          const int ql = 16 * qb4 + 4 * g + i, qi = qtile + ql;
+          const float2 sm = st2[buf][ql];
+          const float a2 = exp2f(__builtin_fmaf(d[i], scale2x, -sm.x)) * sm.y;
+          acc += (!diag || t <= qi) ? a2 : 0.0f;
         }
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) qa[kb] = qn[kb];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) sr[i] = sn[i];
       }
     }
   }
   acc += __shfl_xor(acc, 16);
   acc += __shfl_xor(acc, 32);
-  if (lane < 16 && t0 + lane < N) w[((size_t)b * H + h) * N + t0 + lane] = (t0 + lane < L) ? acc : 0.0f;
+  if (lane < 16 && t0 + lane < N) wq[((size_t)bz * Hq + j) * N + t0 + lane] = (t0 + lane < L) ? acc : 0.0f;
+}
+
+// ---- w[(b H + h) N + t] = sum over the group's query heads, in head order. Grid (N / 256, H, nb) ----
+__global__ __launch_bounds__(256) void k_calib_groupsum(const float* __restrict__ wq, int b0, int N, int H, int Hq,
+                                                        float* __restrict__ w) {
+  const int t = blockIdx.x * 256 + threadIdx.x, h = blockIdx.y, bz = blockIdx.z;
+  if (t >= N) return;
+  const int G = Hq / H;
+  float s = 0.0f;
+  for (int jj = 0; jj < G; ++jj) s += wq[((size_t)bz * Hq + h * G + jj) * N + t];
+  w[((size_t)(b0 + bz) * H + h) * N + t] = s;
 }
 
 // ---- weighted covariance partials. Grid (chunks of 64 tokens, H, B): partial[((bz H + h) nchunk +
@@ -265,17 +336,27 @@ __global__ __launch_bounds__(kCalThreads) void k_calib_covariance(const uint16_t
   }
 }
 
-// ---- C_m[c1][c2] = sum over the partials in index order. Grid (kD kD / 256, 3) ----
+// ---- C_m[c1][c2] = the sum of the partials in a fixed order: eight running sums over p = r (mod
+// 8) (independent load chains), then added in r order. Grid (kD kD / 256, 3) ----
 __global__ __launch_bounds__(256) void k_calib_reduce(const float* __restrict__ partial, int nparts,
                                                       float* __restrict__ cov) {
   const int e = blockIdx.x * 256 + threadIdx.x, m = blockIdx.y;
-  float s = 0.0f;
-  for (int p = 0; p < nparts; ++p) s += partial[((size_t)p * 3 + m) * kD * kD + e];
-  cov[(size_t)m * kD * kD + e] = s;
+  float s[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) s[r] = 0.0f;
+  for (int p0 = 0; p0 < nparts; p0 += 8) {
+    float x[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) x[r] = (p0 + r < nparts) ? partial[((size_t)(p0 + r) * 3 + m) * kD * kD + e] : 0.0f;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) s[r] += x[r];
+  }
+  cov[(size_t)m * kD * kD + e] = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
 }
 
 size_t calib_workspace_bytes(int B, int H, int Hq, int N) {
-  const size_t stats = (size_t)std::min(B, kMaxLenArgs) * Hq * N * sizeof(float2);
+  // row statistics (float2) and the per-head column sums (float) of up to 256 sequences
+  const size_t stats = (size_t)std::min(B, kMaxLenArgs) * Hq * N * (sizeof(float2) + sizeof(float));
   const size_t nchunk = (N + kCovChunk - 1) / kCovChunk;
   const size_t parts = (size_t)B * H * nchunk * 3 * kD * kD * sizeof(float);
   return std::max(stats, parts);
@@ -285,12 +366,16 @@ hipError_t launch_calib_weights(const uint16_t* q, const uint16_t* k, const LenA
                                 int H, int Hq, float sm_scale, float* w, void* ws, hipStream_t s) {
   const float scale2 = sm_scale * 1.4426950408889634f;
   float2* stats = static_cast<float2*>(ws);
-  const dim3 gq((N + kCalTile - 1) / kCalTile, Hq, nb), gk((N + kCalTile - 1) / kCalTile, H, nb);
+  const dim3 gq((N + kCalTile - 1) / kCalTile, Hq, nb);
   hipLaunchKernelGGL(k_calib_rowstats, gq, dim3(kCalThreads), 0, s, q, k, lens, b0, N, H, Hq, scale2, stats);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_calib_colweights, gk, dim3(kCalThreads), 0, s, q, k, lens, b0, N, H, Hq, scale2,
-                     static_cast<const float2*>(stats), w);
+  float* wq = reinterpret_cast<float*>(stats + (size_t)nb * Hq * N);
+  hipLaunchKernelGGL(k_calib_colweights, gq, dim3(kCalThreads), 0, s, q, k, lens, b0, N, H, Hq, scale2,
+                     static_cast<const float2*>(stats), wq);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_calib_groupsum, dim3((N + 255) / 256, H, nb), dim3(256), 0, s, static_cast<const float*>(wq), b0,
+                     N, H, Hq, w);
   return hipGetLastError();
 }
 
