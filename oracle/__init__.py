@@ -30,6 +30,7 @@ cache      whole-layer quantization into the packed cache buffers
 residual   decode over the captioning protocol's mixed cache (fp16 residual)
 calibration  modality-aware value-rotation calibration: attention weights, weighted
            covariance, eigenbasis, R_m = H U_m^T (Eq. 5, Eq. 6)
+turboquant the TurboQuant key codec (Eq. 2, Eq. 3), the paper's baseline, and decode over it
 
 Parity status: every function is pinned by a ``-m "not gpu"`` test except the
 paper's measured error tables (Tab. 1, Tab. 3 error columns, Tab. 6), which

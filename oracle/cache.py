@@ -23,7 +23,8 @@ def quantize_layer(k, v, modality, lens, signs, rot, capacity=None, key_meta="fp
     """Dict of packed buffers (numpy) for k, v [B][H][N][d] fp16, modality [B][N], lens [B].
 
     key_meta "fp16": fp16 window minimum and step (k_min, k_step); "mxfp4": one 136-byte MXFP4
-    record per window (k_mx, layout in ``oracle.layout``).
+    record per window (k_mx, layout in ``oracle.layout``); "turboquant": TurboQuant keys (Gaussian
+    codebook after the Hadamard rotation, no window metadata; ``oracle.turboquant``).
     """
     B, H, N, D = k.shape
     cap = int(capacity or -(-N // WINDOW) * WINDOW)
@@ -40,7 +41,7 @@ def quantize_layer(k, v, modality, lens, signs, rot, capacity=None, key_meta="fp
         out["k_step"] = np.zeros((B, H, nw, D), np.float16)
     elif key_meta == "mxfp4":
         out["k_mx"] = np.zeros((B, H, nw, MX_RECORD), np.uint8)
-    else:
+    elif key_meta != "turboquant":
         raise ValueError(key_meta)
     for b in range(B):
         L = int(lens[b])
@@ -51,6 +52,9 @@ def quantize_layer(k, v, modality, lens, signs, rot, capacity=None, key_meta="fp
                 nwl = kq["codes"].shape[0] // WINDOW
                 out["k_min"][b, h, :nwl] = kq["m16"]
                 out["k_step"][b, h, :nwl] = kq["step16"]
+            elif key_meta == "turboquant":
+                from .turboquant import quantize_keys_tq_fmt
+                kq = quantize_keys_tq_fmt(k[b, h], L, signs)
             else:
                 kq = quantize_keys_mx_fmt(k[b, h], L, signs)
                 nwl = kq["codes"].shape[0] // WINDOW
@@ -83,7 +87,8 @@ def unpacked_fields(cache, b, h):
 
 
 def decode_layer(cache, q16, lens, signs, rot, sm_scale, rotated=True, heads=None):
-    """fp64 outputs [B][Hq][d] of one decode step over a packed cache.
+    """fp64 outputs [B][Hq][d] of one decode step over a packed cache (TurboQuant keys when the
+    cache holds neither window metadata field).
 
     ``heads`` optionally restricts the work to a list of (b, kv head) pairs; other rows are NaN.
     """
@@ -92,9 +97,19 @@ def decode_layer(cache, q16, lens, signs, rot, sm_scale, rotated=True, heads=Non
     G = Hq // H
     out = np.full((B, Hq, D), np.nan)
     fn = decode_rotated if rotated else decode_bruteforce
+    tq = "k_min" not in cache and "k_mx" not in cache
+    if tq:
+        from .turboquant import decode_tq_bruteforce, decode_tq_rotated
+        ftq = decode_tq_rotated if rotated else decode_tq_bruteforce
     for b in range(B):
         for h in range(H):
             if heads is not None and (b, h) not in heads:
+                continue
+            if tq:
+                out[b, h * G:(h + 1) * G] = ftq(q16[b, h * G:(h + 1) * G], unpack_keys(cache["k_codes"][b, h]),
+                                                cache["k_norm"][b, h], unpack_values(cache["v_codes"][b, h]),
+                                                cache["v_norm"][b, h], cache["modality"][b], lens[b], signs, rot,
+                                                sm_scale, G)
                 continue
             kc, m16, st16, nk, vc, nv, mod = unpacked_fields(cache, b, h)
             out[b, h * G:(h + 1) * G] = fn(q16[b, h * G:(h + 1) * G], kc, m16, st16, nk, vc, nv, mod,
