@@ -65,6 +65,14 @@
  * zero, else clamp(rint(fl(fl(z - m) * fl(1 / s))), 0, 3)). Storage: 72.25 bytes per token per
  * KV head, 2.258 bits per element.
  *
+ * TurboQuant keys (dims.key_meta = OKVQ_KEY_META_TURBOQUANT, the paper's baseline, Sec. 2.1 Eq. 2
+ * and Eq. 3): the key direction z (as above: fp16 norm, Hadamard butterflies, z = w fl(kappa / n16))
+ * takes the nearest entry of the same fixed Gaussian codebook as the values, code = #{k : z_c >
+ * tau_k} (a value on a threshold takes the lower code), in the k_codes layout; k_min, k_step and
+ * k_mx are not used. Storage: 68 bytes per token per KV head, 2.125 bits per element (Tab. 3
+ * "TurboQuant (K2/V2)"; with the single global value rotation R_m = H for every modality it is the
+ * whole baseline). Not combined with the fp16 residual.
+ *
  * fp16 residual of the captioning protocol (dims.residual = OKVQ_RESIDUAL_TOKENS, Sec. 3.1: keys
  * quantized every 128 tokens in groups of 32, values kept in a 128-token fp16 window before they
  * are quantized). Two more buffers hold the raw rows of the last 128 tokens:
@@ -103,8 +111,10 @@ enum {
 
 /* okvq_dims.key_meta: storage of the per-window key minimum and step */
 enum {
-  OKVQ_KEY_META_FP16 = 0, /* fp16 k_min, k_step (84 bytes per token per KV head)           */
-  OKVQ_KEY_META_MXFP4 = 1 /* MXFP4 records in k_mx (72.25 bytes per token per KV head)    */
+  OKVQ_KEY_META_FP16 = 0,      /* fp16 k_min, k_step (84 bytes per token per KV head)        */
+  OKVQ_KEY_META_MXFP4 = 1,     /* MXFP4 records in k_mx (72.25 bytes per token per KV head) */
+  OKVQ_KEY_META_TURBOQUANT = 2 /* TurboQuant keys, the paper's baseline: no window metadata
+                                  (68 bytes per token per KV head)                          */
 };
 
 /* okvq_dims.residual: 0 (every token read quantized) or the fp16 window of the captioning
@@ -164,7 +174,7 @@ int32_t okvq_version(void);
 const char* okvq_status_string(okvq_status status);
 
 /* Bytes of one cache buffer for `dims` (0 for an unknown buffer, invalid dims, or a buffer the
- * metadata format of dims does not use: k_min / k_step with MXFP4, k_mx with fp16, k_res / v_res
+ * metadata format of dims does not use: k_min / k_step unless fp16, k_mx unless MXFP4, k_res / v_res
  * without the residual). */
 size_t okvq_buffer_bytes(const okvq_dims* dims, int32_t which_buffer);
 
@@ -195,6 +205,13 @@ okvq_status okvq_quantize_keys(const okvq_dims* dims, const uint16_t* k, int32_t
 okvq_status okvq_quantize_keys_mx(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens,
                                   const int32_t* lens_host, const int8_t* key_signs, uint8_t* k_codes,
                                   uint8_t* k_mx, uint16_t* k_norm, void* stream);
+
+/* okvq_quantize_keys for TurboQuant keys (Eq. 2, Eq. 3; the layout above): the same arguments
+ * without window metadata. dims->key_meta must be OKVQ_KEY_META_TURBOQUANT. Bit-exact contract:
+ * norms and codes equal the documented fp32 order followed by the threshold decisions. */
+okvq_status okvq_quantize_keys_tq(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens,
+                                  const int32_t* lens_host, const int8_t* key_signs, uint8_t* k_codes,
+                                  uint16_t* k_norm, void* stream);
 
 /* Quantize values (Eq. 6 with the codebook of Eq. 3) of a dense block into cache-layout buffers.
  *   v          device f16 [B][H][n_tokens][128]

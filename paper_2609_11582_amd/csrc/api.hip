@@ -13,7 +13,7 @@ using namespace okvq;
 
 namespace {
 
-constexpr int32_t kVersion = 300;  // 0.3.0: fp16 residual of the captioning protocol
+constexpr int32_t kVersion = 400;  // 0.4.0: value-rotation calibration, TurboQuant keys
 
 // ---- fixed Gaussian codebook (Sec. 2.1, Eq. 3): Lloyd-Max quantizer of N(0, 1), 4 levels ----
 double phi(double x) { return std::isinf(x) ? 0.0 : std::exp(-0.5 * x * x) / std::sqrt(2.0 * M_PI); }
@@ -75,12 +75,18 @@ okvq_status check_dims(const okvq_dims* d) {
   if (d->num_q_heads / d->num_kv_heads > 8) return OKVQ_ERR_UNSUPPORTED;
   if (d->capacity < 32 || d->capacity % 32 != 0) return OKVQ_ERR_INVALID_ARGUMENT;
   if (d->batch > 65535 || d->num_kv_heads > 65535) return OKVQ_ERR_UNSUPPORTED;
-  if (d->key_meta != OKVQ_KEY_META_FP16 && d->key_meta != OKVQ_KEY_META_MXFP4) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (d->key_meta != OKVQ_KEY_META_FP16 && d->key_meta != OKVQ_KEY_META_MXFP4 && d->key_meta != OKVQ_KEY_META_TURBOQUANT)
+    return OKVQ_ERR_INVALID_ARGUMENT;
   if (d->residual != 0 && d->residual != OKVQ_RESIDUAL_TOKENS) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (d->residual != 0 && d->key_meta == OKVQ_KEY_META_TURBOQUANT) return OKVQ_ERR_UNSUPPORTED;
   return OKVQ_OK;
 }
 
 bool is_mx(const okvq_dims* d) { return d->key_meta == OKVQ_KEY_META_MXFP4; }
+bool is_fp16(const okvq_dims* d) { return d->key_meta == OKVQ_KEY_META_FP16; }
+int meta_mode(const okvq_dims* d) {
+  return d->key_meta == OKVQ_KEY_META_MXFP4 ? kMetaMx : d->key_meta == OKVQ_KEY_META_TURBOQUANT ? kMetaTq : kMetaFp16;
+}
 
 okvq_status check_cache(const okvq_cache* c) {
   if (!c) return OKVQ_ERR_INVALID_ARGUMENT;
@@ -90,8 +96,8 @@ okvq_status check_cache(const okvq_cache* c) {
                         c->k_stage, c->seq_lens, c->key_signs, c->v_rot,  c->v_rot16};
   for (const void* p : ptrs)
     if (!aligned16(p)) return OKVQ_ERR_INVALID_ARGUMENT;
-  if (is_mx(&c->dims) ? !aligned16(c->k_mx) : (!aligned16(c->k_min) || !aligned16(c->k_step)))
-    return OKVQ_ERR_INVALID_ARGUMENT;
+  if (is_mx(&c->dims) && !aligned16(c->k_mx)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (is_fp16(&c->dims) && (!aligned16(c->k_min) || !aligned16(c->k_step))) return OKVQ_ERR_INVALID_ARGUMENT;
   if (c->dims.residual && (!aligned16(c->k_res) || !aligned16(c->v_res))) return OKVQ_ERR_INVALID_ARGUMENT;
   return OKVQ_OK;
 }
@@ -109,6 +115,7 @@ CacheView view(const okvq_cache* c) {
   v.k_min = c->k_min;
   v.k_step = c->k_step;
   v.k_mx = is_mx(&c->dims) ? c->k_mx : nullptr;
+  v.key_meta = meta_mode(&c->dims);
   v.modality = c->modality;
   v.k_stage = c->k_stage;
   v.seq_lens = c->seq_lens;
@@ -201,8 +208,8 @@ size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
     case OKVQ_BUF_V_CODES: return B * H * cap * (D / 4);
     case OKVQ_BUF_K_NORM: return B * H * cap * 2;
     case OKVQ_BUF_V_NORM: return B * H * cap * 2;
-    case OKVQ_BUF_K_MIN: return is_mx(d) ? 0 : B * H * (cap / W) * D * 2;
-    case OKVQ_BUF_K_STEP: return is_mx(d) ? 0 : B * H * (cap / W) * D * 2;
+    case OKVQ_BUF_K_MIN: return is_fp16(d) ? B * H * (cap / W) * D * 2 : 0;
+    case OKVQ_BUF_K_STEP: return is_fp16(d) ? B * H * (cap / W) * D * 2 : 0;
     case OKVQ_BUF_K_MX: return is_mx(d) ? B * H * (cap / W) * kMxRecord : 0;
     case OKVQ_BUF_MODALITY: return B * cap;
     case OKVQ_BUF_K_STAGE: return B * H * W * D * 2;
@@ -250,6 +257,8 @@ static okvq_status quantize_keys_impl(const okvq_dims* dims, const uint16_t* k, 
     a.k_step = k_step;
     a.k_mx = k_mx;
     a.k_norm = k_norm;
+    a.key_meta = meta_mode(dims);
+    a.th = thresholds();
     okvq_status st = hip_status(launch_codec(a, true, false, s));
     if (st != OKVQ_OK) return st;
   }
@@ -261,7 +270,7 @@ okvq_status okvq_quantize_keys(const okvq_dims* dims, const uint16_t* k, int32_t
                                uint16_t* k_norm, void* stream) {
   okvq_status st = check_dims(dims);
   if (st != OKVQ_OK) return st;
-  if (n_tokens < 0 || !lens_host || is_mx(dims)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (n_tokens < 0 || !lens_host || !is_fp16(dims)) return OKVQ_ERR_INVALID_ARGUMENT;
   if (!aligned16(k) || !aligned16(key_signs) || !aligned16(k_codes) || !aligned16(k_min) || !aligned16(k_step) ||
       !aligned16(k_norm))
     return OKVQ_ERR_INVALID_ARGUMENT;
@@ -277,6 +286,17 @@ okvq_status okvq_quantize_keys_mx(const okvq_dims* dims, const uint16_t* k, int3
   if (!aligned16(k) || !aligned16(key_signs) || !aligned16(k_codes) || !aligned16(k_mx) || !aligned16(k_norm))
     return OKVQ_ERR_INVALID_ARGUMENT;
   return quantize_keys_impl(dims, k, n_tokens, lens_host, key_signs, k_codes, nullptr, nullptr, k_mx, k_norm, stream);
+}
+
+okvq_status okvq_quantize_keys_tq(const okvq_dims* dims, const uint16_t* k, int32_t n_tokens,
+                                  const int32_t* lens_host, const int8_t* key_signs, uint8_t* k_codes,
+                                  uint16_t* k_norm, void* stream) {
+  okvq_status st = check_dims(dims);
+  if (st != OKVQ_OK) return st;
+  if (n_tokens < 0 || !lens_host || dims->key_meta != OKVQ_KEY_META_TURBOQUANT) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(k) || !aligned16(key_signs) || !aligned16(k_codes) || !aligned16(k_norm))
+    return OKVQ_ERR_INVALID_ARGUMENT;
+  return quantize_keys_impl(dims, k, n_tokens, lens_host, key_signs, k_codes, nullptr, nullptr, nullptr, k_norm, stream);
 }
 
 okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const uint8_t* modality, int32_t n_tokens,
@@ -374,6 +394,7 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
     a.k_step = cache->k_step;
     a.k_mx = is_mx(&d) ? cache->k_mx : nullptr;
     a.k_norm = cache->k_norm;
+    a.key_meta = meta_mode(&d);
     a.th = thresholds();
     a.v_codes = cache->v_codes;
     a.v_norm = cache->v_norm;

@@ -138,8 +138,9 @@ __device__ __forceinline__ void rewrite_stage(const CodecJob& j, const TileCtx& 
   }
 }
 
-template <bool kMx>
+template <int kMeta>
 __device__ __forceinline__ void key_role(const CodecArgs& a, int kw, float* lds) {
+  constexpr bool kMx = kMeta == kMetaMx;
   const CodecJob& j = a.j;
   int t = blockIdx.x;  // < ntiles: the grid is never larger
   // The transpose tile of phase B doubles as the row buffer: the next tile's rows are loaded into
@@ -173,10 +174,12 @@ __device__ __forceinline__ void key_role(const CodecArgs& a, int kw, float* lds)
     };
     if (work) {
       const size_t nw = j.cap / kW;
-      KeyWaveOut out{a.k_codes + c.seq * j.cap * 32, kMx ? nullptr : a.k_min + c.seq * nw * kD,
-                     kMx ? nullptr : a.k_step + c.seq * nw * kD, kMx ? a.k_mx + c.seq * nw * kMxRecord : nullptr,
-                     a.k_norm + c.seq * j.cap};
-      key_quantize_rows<kMx>(x, n16, tok0, c.len, out, lds, prefetch);
+      KeyWaveOut out{a.k_codes + c.seq * j.cap * 32,
+                     kMeta == kMetaFp16 ? a.k_min + c.seq * nw * kD : nullptr,
+                     kMeta == kMetaFp16 ? a.k_step + c.seq * nw * kD : nullptr,
+                     kMx ? a.k_mx + c.seq * nw * kMxRecord : nullptr,
+                     a.k_norm + c.seq * j.cap, a.th.t0, a.th.t1, a.th.t2};
+      key_quantize_rows<kMeta>(x, n16, tok0, c.len, out, lds, prefetch);
     } else {
       prefetch();
     }
@@ -464,7 +467,7 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
 }
 
 // ------------------------------------------------------------------------------------------------
-template <bool kKeys, bool kValues, bool kMx>
+template <bool kKeys, bool kValues, int kMeta>
 __global__ __launch_bounds__(256 * (kKeys + kValues), (kKeys && kValues) ? 1 : 2) void k_codec(CodecArgs a) {
   __shared__ __attribute__((aligned(16))) float key_lds[kKeys ? 4 * kKeyWaveLds : 4];
   __shared__ __attribute__((aligned(16))) ValueShared vsh;
@@ -474,7 +477,7 @@ __global__ __launch_bounds__(256 * (kKeys + kValues), (kKeys && kValues) ? 1 : 2
     __syncthreads();  // the only work-group barrier; every wave reaches it
   }
   if (kKeys && wave < 4) {
-    key_role<kMx>(a, wave, key_lds + wave * kKeyWaveLds);
+    key_role<kMeta>(a, wave, key_lds + wave * kKeyWaveLds);
   } else if (kValues) {
     value_role(a, wave - (kKeys ? 4 : 0), vsh);
   }
@@ -530,19 +533,22 @@ hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t 
   // leaves room for two
   const int per_cu = (keys && values) ? 1 : 2;
   const int grid = std::min(a.ntiles, per_cu * cus);
-  const bool mx = a.k_mx != nullptr;
   if (keys && values) {
-    if (mx)
-      hipLaunchKernelGGL((k_codec<true, true, true>), dim3(grid), dim3(512), 0, s, a);
+    if (a.key_meta == kMetaMx)
+      hipLaunchKernelGGL((k_codec<true, true, kMetaMx>), dim3(grid), dim3(512), 0, s, a);
+    else if (a.key_meta == kMetaTq)
+      hipLaunchKernelGGL((k_codec<true, true, kMetaTq>), dim3(grid), dim3(512), 0, s, a);
     else
-      hipLaunchKernelGGL((k_codec<true, true, false>), dim3(grid), dim3(512), 0, s, a);
+      hipLaunchKernelGGL((k_codec<true, true, kMetaFp16>), dim3(grid), dim3(512), 0, s, a);
   } else if (keys) {
-    if (mx)
-      hipLaunchKernelGGL((k_codec<true, false, true>), dim3(grid), dim3(256), 0, s, a);
+    if (a.key_meta == kMetaMx)
+      hipLaunchKernelGGL((k_codec<true, false, kMetaMx>), dim3(grid), dim3(256), 0, s, a);
+    else if (a.key_meta == kMetaTq)
+      hipLaunchKernelGGL((k_codec<true, false, kMetaTq>), dim3(grid), dim3(256), 0, s, a);
     else
-      hipLaunchKernelGGL((k_codec<true, false, false>), dim3(grid), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_codec<true, false, kMetaFp16>), dim3(grid), dim3(256), 0, s, a);
   } else {
-    hipLaunchKernelGGL((k_codec<false, true, false>), dim3(grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_codec<false, true, kMetaFp16>), dim3(grid), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

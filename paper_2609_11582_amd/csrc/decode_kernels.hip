@@ -52,7 +52,7 @@ struct DecodeArgs {
   const uint16_t* v_norm;
   const uint16_t* k_min;
   const uint16_t* k_step;
-  const uint8_t* k_mx;  // MXFP4 window records (k_decode<true>) instead of k_min / k_step
+  const uint8_t* k_mx;  // MXFP4 window records (k_decode<kMetaMx>) instead of k_min / k_step
   const uint8_t* modality;
   const int32_t* seq_lens;
   const int8_t* signs;
@@ -204,8 +204,9 @@ struct SeqPtrs {  // uniform per work-group
   const uint8_t* md;
 };
 
-template <bool kMx>
+template <int kMeta>
 __device__ __forceinline__ PairLoad load_pair(const SeqPtrs& sp, int wA, bool hasB, int lane) {
+  constexpr bool kMx = kMeta == kMetaMx;
   const int col = lane & 15, g = lane >> 4, r = lane & 15, side = col >> 3;
   const uint32_t wB = hasB ? wA + 1 : wA;
   const uint32_t wS = side ? wB : (uint32_t)wA;
@@ -228,10 +229,12 @@ __device__ __forceinline__ PairLoad load_pair(const SeqPtrs& sp, int wA, bool ha
     d.stp.x = *reinterpret_cast<const uint32_t*>(rec + 4u * (8u * g + (col & 7)));
     d.stp.y = *reinterpret_cast<const uint16_t*>(rec + 128u + 2u * g);
     d.mnp = make_uint2(0u, 0u);
-  } else {
+  } else if constexpr (kMeta == kMetaFp16) {
     const uint32_t mt = wS * kD + 32u * g + 4u * (col & 7);
     d.stp = *reinterpret_cast<const uint2*>(sp.kstep + mt);
     d.mnp = *reinterpret_cast<const uint2*>(sp.kmin + mt);
+  } else {  // TurboQuant keys: no window metadata
+    d.stp = d.mnp = make_uint2(0u, 0u);
   }
   return d;
 }
@@ -260,8 +263,22 @@ __device__ __forceinline__ half8 lut_op(const uint2* vlut, uint4 vc, int nb) {
   return h8(x0.x, x0.y, x1.x, x1.y);
 }
 
-template <bool kMx>
+// TurboQuant key operand (k-block kk of the pair): the codebook values of channels 32 g + 8 kk'
+// .. + 7 (kk' = kk & 3) of the lane's token, from the code-byte table: the word's even channels
+// sit in one byte and its odd ones in another, so the operand order is c0, c2, c4, c6, c1, c3, c5,
+// c7 (the query operand uses the same order).
+__device__ __forceinline__ half8 key_a_lut(const uint2* vlut, uint2 w, int kk) {
+  const uint32_t d = (kk & 2) ? w.y : w.x;
+  const int hb = 8 * (kk & 1);
+  const uint2 e = vlut[(d >> hb) & 0xffu];
+  const uint2 o = vlut[(d >> (16 + hb)) & 0xffu];
+  return h8(e.x, e.y, o.x, o.y);
+}
+
+template <int kMeta>
 __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
+  constexpr bool kMx = kMeta == kMetaMx;
+  constexpr bool kTq = kMeta == kMetaTq;
   __shared__ __attribute__((aligned(16))) uint2 vlut[256];
   __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];                     // q' (fp32, padded rows)
   __shared__ float amax_w[kDecWaves];
@@ -290,8 +307,8 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
                    p.v_codes + seq * nwcap * 1024,
                    p.k_norm + seq * p.cap,
                    p.v_norm + seq * p.cap,
-                   kMx ? nullptr : p.k_min + seq * nwcap * kD,
-                   kMx ? nullptr : p.k_step + seq * nwcap * kD,
+                   kMeta == kMetaFp16 ? p.k_min + seq * nwcap * kD : nullptr,
+                   kMeta == kMetaFp16 ? p.k_step + seq * nwcap * kD : nullptr,
                    kMx ? p.k_mx + seq * nwcap * kMxRecord : nullptr,
                    p.modality + (size_t)b * p.cap};
 
@@ -306,7 +323,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     qsgn = *reinterpret_cast<const uint32_t*>(p.signs + c4);
   }
   PairLoad bufA, bufB;
-  if (wA0 < w_plan) bufA = load_pair<kMx>(sp, wA0, wA0 + 1 < w_plan, lane);
+  if (wA0 < w_plan) bufA = load_pair<kMeta>(sp, wA0, wA0 + 1 < w_plan, lane);
   // memory-safe if device and host lengths disagree; with the fp16 residual the last 128 tokens
   // are the merge launch's
   const int len = max(min(p.seq_lens[b], p.cap) - p.residual, 0);
@@ -371,7 +388,9 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   // power-of-two scale k0 keeps |q'_c step_c 2^(k0 - shift)| <= 2^15: |step| <= 2/3 + rounding for
   // fp16 metadata, and below 1 for MXFP4 (a block's largest step rounds up by at most 3/2)
   const int k0 = (amax > 0.0f) ? min(max(14 - ilogbf(amax), -60), 60) : 0;
-  const float kscale = ldexpf(1.0f, 24 - k0);  // undoes 2^(k0 - 24) on the MFMA result
+  // undoes 2^(k0 - 24) on the MFMA result (TurboQuant keys: 2^k0, the codebook values being exact
+  // fp16 operands)
+  const float kscale = ldexpf(1.0f, kTq ? -k0 : 24 - k0);
   // Per-lane query operand of the score MFMA, constant over the pairs: for channels
   // 32g + 8 k4 .. +7, fp16(q'[hd][c] 2^(k0 - shift(c))). The other window's k-blocks multiply it
   // by zero steps (read from `zeros`).
@@ -381,10 +400,18 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     const float4 qa = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 8 * k4]);
     const float4 qb = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 8 * k4 + 4]);
     const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
+    if constexpr (kTq) {  // the key operand's order: c0, c2, c4, c6, c1, c3, c5, c7
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {  // channel pair 4 (k4 & 1) + j of the word
-      const int sh = k0 - code_shift(4 * (k4 & 1) + j);
-      qm[k4][j] = pack2(ldexpf(qv[2 * j], sh), ldexpf(qv[2 * j + 1], sh));
+      for (int j = 0; j < 4; ++j) {
+        const int c0 = (j < 2) ? 4 * j : 4 * (j - 2) + 1;
+        qm[k4][j] = pack2(ldexpf(qv[c0], k0), ldexpf(qv[c0 + 2], k0));
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {  // channel pair 4 (k4 & 1) + j of the word
+        const int sh = k0 - code_shift(4 * (k4 & 1) + j);
+        qm[k4][j] = pack2(ldexpf(qv[2 * j], sh), ldexpf(qv[2 * j + 1], sh));
+      }
     }
   }
   // modality tables of this lane: its own row half (set 1: audio for side 0, video for side 1),
@@ -412,46 +439,56 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     const bool full = hasB && kW * (wA + 2) <= len;  // every token of both windows is valid
     const int wS = wA + side;
 
-    // ---- side window metadata through wave-private LDS, natural channel order ----
-    uint2 stp = cur.stp, mnp = cur.mnp;
-    if constexpr (kMx) mx_to_f16(cur.stp.x, cur.stp.y, mnp, stp);
-    *reinterpret_cast<uint2*>(&mw[16 * g + 2 * c7]) = stp;
-    *reinterpret_cast<uint2*>(&mw[kD / 2 + 16 * g + 2 * c7]) = mnp;
-    wave_lds_sync();
-    uint4 mn4[4];
+    float bias = 0.0f;  // TurboQuant keys: no window minimum
+    if constexpr (!kTq) {
+      // ---- side window metadata through wave-private LDS, natural channel order ----
+      uint2 stp = cur.stp, mnp = cur.mnp;
+      if constexpr (kMx) mx_to_f16(cur.stp.x, cur.stp.y, mnp, stp);
+      *reinterpret_cast<uint2*>(&mw[16 * g + 2 * c7]) = stp;
+      *reinterpret_cast<uint2*>(&mw[kD / 2 + 16 * g + 2 * c7]) = mnp;
+      wave_lds_sync();
+      uint4 mn4[4];
 #pragma unroll
-    for (int k4 = 0; k4 < 4; ++k4) mn4[k4] = *reinterpret_cast<const uint4*>(&mw[kD / 2 + 16 * g + 4 * k4]);
-    // ---- bias q'.m of the side window (fp32): 32 channels per lane, then the 4 lane groups ----
-    float bp[4];  // four independent partial sums (short dependency chains)
+      for (int k4 = 0; k4 < 4; ++k4) mn4[k4] = *reinterpret_cast<const uint4*>(&mw[kD / 2 + 16 * g + 4 * k4]);
+      // ---- bias q'.m of the side window (fp32): 32 channels per lane, then the 4 lane groups ----
+      float bp[4];  // four independent partial sums (short dependency chains)
 #pragma unroll
-    for (int k4 = 0; k4 < 4; ++k4) {
-      const float4 qa = *reinterpret_cast<const float4*>(qrow + 8 * k4);
-      const float4 qb = *reinterpret_cast<const float4*>(qrow + 8 * k4 + 4);
-      const uint4 m = mn4[k4];
-      float b = qa.x * lo_f16(m.x);
-      b = __builtin_fmaf(qa.y, hi_f16(m.x), b);
-      b = __builtin_fmaf(qa.z, lo_f16(m.y), b);
-      b = __builtin_fmaf(qa.w, hi_f16(m.y), b);
-      b = __builtin_fmaf(qb.x, lo_f16(m.z), b);
-      b = __builtin_fmaf(qb.y, hi_f16(m.z), b);
-      b = __builtin_fmaf(qb.z, lo_f16(m.w), b);
-      b = __builtin_fmaf(qb.w, hi_f16(m.w), b);
-      bp[k4] = b;
+      for (int k4 = 0; k4 < 4; ++k4) {
+        const float4 qa = *reinterpret_cast<const float4*>(qrow + 8 * k4);
+        const float4 qb = *reinterpret_cast<const float4*>(qrow + 8 * k4 + 4);
+        const uint4 m = mn4[k4];
+        float b = qa.x * lo_f16(m.x);
+        b = __builtin_fmaf(qa.y, hi_f16(m.x), b);
+        b = __builtin_fmaf(qa.z, lo_f16(m.y), b);
+        b = __builtin_fmaf(qa.w, hi_f16(m.y), b);
+        b = __builtin_fmaf(qb.x, lo_f16(m.z), b);
+        b = __builtin_fmaf(qb.y, hi_f16(m.z), b);
+        b = __builtin_fmaf(qb.z, lo_f16(m.w), b);
+        b = __builtin_fmaf(qb.w, hi_f16(m.w), b);
+        bp[k4] = b;
+      }
+      bias = (bp[0] + bp[1]) + (bp[2] + bp[3]);
+      bias = sum32(sum16(bias));
     }
-    float bias = (bp[0] + bp[1]) + (bp[2] + bp[3]);
-    bias = sum32(sum16(bias));
 
     // ---- scores: two 16-token tiles, each 8 MFMAs block-diagonal over the pair ----
     floatx4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
-      const uint4 sv = *reinterpret_cast<const uint4*>(&(kk < 4 ? stA : stB)[16 * g + 4 * (kk & 3)]);
       const uint32_t* q = qm[kk & 3];
-      const half8 bop = h8(pk_mul(q[0], sv.x), pk_mul(q[1], sv.y), pk_mul(q[2], sv.z), pk_mul(q[3], sv.w));
-      sc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka0 : cur.kb0, kk), bop, sc0, 0, 0, 0);
-      sc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka1 : cur.kb1, kk), bop, sc1, 0, 0, 0);
+      if constexpr (kTq) {  // codebook operands from the table; the other window's k-blocks get a zero query
+        const bool mine = (kk < 4) == (side == 0);
+        const half8 bop = h8(mine ? q[0] : 0u, mine ? q[1] : 0u, mine ? q[2] : 0u, mine ? q[3] : 0u);
+        sc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_lut(vlut, kk < 4 ? cur.ka0 : cur.kb0, kk), bop, sc0, 0, 0, 0);
+        sc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_lut(vlut, kk < 4 ? cur.ka1 : cur.kb1, kk), bop, sc1, 0, 0, 0);
+      } else {
+        const uint4 sv = *reinterpret_cast<const uint4*>(&(kk < 4 ? stA : stB)[16 * g + 4 * (kk & 3)]);
+        const half8 bop = h8(pk_mul(q[0], sv.x), pk_mul(q[1], sv.y), pk_mul(q[2], sv.z), pk_mul(q[3], sv.w));
+        sc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka0 : cur.kb0, kk), bop, sc0, 0, 0, 0);
+        sc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka1 : cur.kb1, kk), bop, sc1, 0, 0, 0);
+      }
     }
-    wave_lds_sync();  // metadata reads done before the next pair overwrites it
+    if constexpr (!kTq) wave_lds_sync();  // metadata reads done before the next pair overwrites it
 
     // ---- online softmax (base 2) over the pair's 64 tokens ----
     const uint32_t nkw[4] = {cur.nk0.x, cur.nk0.y, cur.nk1.x, cur.nk1.y};
@@ -572,11 +609,11 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   // ---- window pairs, double-buffered loads without register copies ----
   for (int wA = wA0; wA < w_end; wA += 4 * kDecWaves) {
     const int wA2 = wA + 2 * kDecWaves;
-    if (wA2 < w_end) bufB = load_pair<kMx>(sp, wA2, wA2 + 1 < w_end, lane);
+    if (wA2 < w_end) bufB = load_pair<kMeta>(sp, wA2, wA2 + 1 < w_end, lane);
     process(bufA, wA);
     if (wA2 >= w_end) break;
     const int wA3 = wA2 + 2 * kDecWaves;
-    if (wA3 < w_end) bufA = load_pair<kMx>(sp, wA3, wA3 + 1 < w_end, lane);
+    if (wA3 < w_end) bufA = load_pair<kMeta>(sp, wA3, wA3 + 1 < w_end, lane);
     process(bufB, wA2);
   }
 
@@ -1096,17 +1133,11 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
   a.cb23 = cb23;
   hipError_t e;
   const dim3 grid(plan.nsplit, c.H, c.B), block(64 * kDecWaves);
-  if (events) {  // events bound to the two dispatches: start and end of each kernel's execution
-    if (c.k_mx)
-      hipExtLaunchKernelGGL(k_decode<true>, grid, block, 0, s, events[0], events[1], 0, a);
-    else
-      hipExtLaunchKernelGGL(k_decode<false>, grid, block, 0, s, events[0], events[1], 0, a);
-  } else {
-    if (c.k_mx)
-      hipLaunchKernelGGL(k_decode<true>, grid, block, 0, s, a);
-    else
-      hipLaunchKernelGGL(k_decode<false>, grid, block, 0, s, a);
-  }
+  auto kern = c.key_meta == kMetaMx ? k_decode<kMetaMx> : c.key_meta == kMetaTq ? k_decode<kMetaTq> : k_decode<kMetaFp16>;
+  if (events)  // events bound to the two dispatches: start and end of each kernel's execution
+    hipExtLaunchKernelGGL(kern, grid, block, 0, s, events[0], events[1], 0, a);
+  else
+    hipLaunchKernelGGL(kern, grid, block, 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const dim3 mgrid(c.Hq, c.B), mblock(kMergeThreads);
   if (c.residual) {

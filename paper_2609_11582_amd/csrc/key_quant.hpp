@@ -28,6 +28,7 @@ struct KeyWaveOut {
   uint16_t* kstep; // [cap/32][128]
   uint8_t* kmx;    // [cap/32][136] MXFP4 window records
   uint16_t* knorm; // [cap]
+  float tau0, tau1, tau2;  // TurboQuant keys: the codebook's decision thresholds (fp32, ascending)
 };
 
 // Lane l <- lane l ^ m for m = 1, 2 (DPP quad permutations) or 4 (LDS-pipe swizzle in xor mode):
@@ -73,14 +74,43 @@ __device__ __forceinline__ uint32_t key_norm(const float (&x)[kD]) {
   return norm_to_f16(sqrt_rn(t[0]));
 }
 
+// TurboQuant phase C (Eq. 3 on the key direction): code = #{k : z > tau_k} per channel (a value
+// on a threshold takes the lower code), packed in the key byte layout; no window metadata.
+__device__ __forceinline__ void key_codes_tq(const float (&x)[kD], uint32_t n16, int tok0, int len, const KeyWaveOut& out) {
+  const int lane = lane_id(), tok = tok0 + lane;
+  const bool valid = tok < len;
+  const int store_slots = min(max(len - tok0 + 31, 0) / 32 * 32, 64);  // slots of valid windows
+  if (lane >= store_slots) return;
+  uint32_t dw[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {  // word u: channels 16u .. 16u + 15, even ones low, odd ones high
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      const float z0 = x[16 * u + 2 * jj], z1 = x[16 * u + 2 * jj + 1];
+      const uint32_t c0 = (uint32_t)(z0 > out.tau0) + (uint32_t)(z0 > out.tau1) + (uint32_t)(z0 > out.tau2);
+      const uint32_t c1 = (uint32_t)(z1 > out.tau0) + (uint32_t)(z1 > out.tau1) + (uint32_t)(z1 > out.tau2);
+      lo |= c0 << (2 * jj);
+      hi |= c1 << (2 * jj);
+    }
+    dw[u] = valid ? (lo | (hi << 16)) : 0u;
+  }
+  uint4* dst = reinterpret_cast<uint4*>(out.codes + (size_t)tok * 32);
+  dst[0] = make_uint4(dw[0], dw[1], dw[2], dw[3]);
+  dst[1] = make_uint4(dw[4], dw[5], dw[6], dw[7]);
+  out.knorm[tok] = valid ? (uint16_t)n16 : (uint16_t)0;
+}
+
 // Phase A, second half, and phases B and C for the 64 tokens [tok0, tok0 + 64) of one wave
 // (lane = token). `len` is the sequence length; the slots of every window that holds a valid
 // token are written (padded slots get code 0 and norm 0). between_bc() runs after phase B (the
-// caller's loads for its next rows go out there, when fewer registers are live). kMx: the window
-// minimum and step are stored as MXFP4 records and the codes use their dequantized values.
-template <bool kMx, typename F>
+// caller's loads for its next rows go out there, when fewer registers are live). kMeta: kMetaMx
+// stores the window minimum and step as MXFP4 records and codes against their dequantized values;
+// kMetaTq codes TurboQuant keys (no phase B).
+template <int kMeta, typename F>
 __device__ __forceinline__ void key_quantize_rows(float (&x)[kD], uint32_t n16, int tok0, int len, KeyWaveOut out,
                                                   float* lds, F&& between_bc) {
+  constexpr bool kMx = kMeta == kMetaMx;
   const int lane = lane_id();
   const int tok = tok0 + lane;
   const bool valid = tok < len;
@@ -101,6 +131,11 @@ __device__ __forceinline__ void key_quantize_rows(float (&x)[kD], uint32_t n16, 
   const float cinv = (n16 == 0) ? 0.0f : div_rn(kKappa, h2f(n16));
 #pragma unroll
   for (int c = 0; c < kD; ++c) x[c] = x[c] * cinv;
+  if constexpr (kMeta == kMetaTq) {
+    between_bc();
+    key_codes_tq(x, n16, tok0, len, out);
+    return;
+  }
 
   // ---- phase B: window min / max through LDS, 64 channels at a time. Lane l reads channel quad
   // l % 16 of rows 16 ((l / 16) % 2) .. +15 of window l / 32; the two row halves are combined with

@@ -47,8 +47,9 @@ struct CodecArgs {
   uint8_t* k_codes;
   uint16_t* k_min;   // fp16 window metadata, or
   uint16_t* k_step;
-  uint8_t* k_mx;     // MXFP4 window records (non-null selects this format)
+  uint8_t* k_mx;     // MXFP4 window records
   uint16_t* k_norm;
+  int key_meta;      // kMetaFp16, kMetaMx or kMetaTq (TurboQuant keys: codes against th, no metadata)
   // values
   const uint16_t* vsrc;  // value rows, laid out like j.src (the key rows)
   const float* rot;      // fp32 R_m (used when rotfrag is null)
@@ -90,6 +91,7 @@ struct CacheView {
   uint16_t* k_min;
   uint16_t* k_step;
   uint8_t* k_mx;  // MXFP4 window records, or null for fp16 k_min / k_step
+  int key_meta;   // kMetaFp16, kMetaMx or kMetaTq
   uint8_t* modality;
   uint16_t* k_stage;
   int32_t* seq_lens;

@@ -47,6 +47,11 @@ __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 // byte of channel block b, byte 129 + 2b the step's.
 constexpr int kMxRecord = 136;
 
+// Key storage modes (template arguments of the key codec and of decode): fp16 window minimum and
+// step, MXFP4 window records, or TurboQuant keys (Gaussian-codebook codes of the Hadamard direction,
+// no window metadata; the paper's baseline, Eq. 2 and Eq. 3).
+constexpr int kMetaFp16 = 0, kMetaMx = 1, kMetaTq = 2;
+
 // Shared exponent of a block whose largest magnitude is amax: floor(log2(amax)) - 2 (2 is the
 // largest E2M1 exponent), clamped to the E8M0 range; -127 for an all-zero block.
 __device__ __forceinline__ int mx_exponent(float amax) {

@@ -22,7 +22,8 @@ OKVQ_OK = 0
 OKVQ_VALUE_EXACT = 1
 OKVQ_KEY_META_FP16 = 0
 OKVQ_KEY_META_MXFP4 = 1
-KEY_META = {"fp16": OKVQ_KEY_META_FP16, "mxfp4": OKVQ_KEY_META_MXFP4}
+OKVQ_KEY_META_TURBOQUANT = 2
+KEY_META = {"fp16": OKVQ_KEY_META_FP16, "mxfp4": OKVQ_KEY_META_MXFP4, "turboquant": OKVQ_KEY_META_TURBOQUANT}
 ROTATION_TABLE_BYTES = 294912  # OKVQ_ROTATION_TABLE_BYTES
 MX_RECORD_BYTES = 136  # one MXFP4 key-metadata record per 32-token window
 RESIDUAL_TOKENS = 128  # OKVQ_RESIDUAL_TOKENS: fp16 window of the captioning protocol
@@ -71,6 +72,8 @@ def lib() -> ctypes.CDLL:
         L.okvq_quantize_keys.argtypes = [P(Dims), vp, i32, P(i32), vp, vp, vp, vp, vp, vp]
         L.okvq_quantize_keys_mx.restype = i32
         L.okvq_quantize_keys_mx.argtypes = [P(Dims), vp, i32, P(i32), vp, vp, vp, vp, vp]
+        L.okvq_quantize_keys_tq.restype = i32
+        L.okvq_quantize_keys_tq.argtypes = [P(Dims), vp, i32, P(i32), vp, vp, vp, vp]
         L.okvq_quantize_values.restype = i32
         L.okvq_quantize_values.argtypes = [P(Dims), vp, vp, i32, P(i32), vp, u32, vp, vp, vp]
         L.okvq_append.restype = i32
@@ -181,6 +184,20 @@ def okvq_quantize_keys_mx(dims, k, n_tokens, lens, key_signs, k_codes, k_mx, k_n
                                      _ptr(k_codes), _ptr(k_mx), _ptr(k_norm), _stream(stream))
     if check:
         _check(st, "okvq_quantize_keys_mx")
+    return st
+
+
+def okvq_quantize_keys_tq(dims, k, n_tokens, lens, key_signs, k_codes, k_norm, stream=None, check=True) -> int:
+    B, H = dims.batch, dims.num_kv_heads
+    _need_len(lens, B, "lens")
+    _need(k, B * H * int(n_tokens) * 128 * 2, "k")
+    _need(key_signs, 128, "key_signs")
+    for i, (name, t) in {0: ("k_codes", k_codes), 2: ("k_norm", k_norm)}.items():
+        _need(t, okvq_buffer_bytes(dims, i), name)
+    st = lib().okvq_quantize_keys_tq(ctypes.byref(dims), _ptr(k), int(n_tokens), _i32(lens), _ptr(key_signs),
+                                     _ptr(k_codes), _ptr(k_norm), _stream(stream))
+    if check:
+        _check(st, "okvq_quantize_keys_tq")
     return st
 
 
@@ -336,7 +353,8 @@ _DTYPES = dict(k_codes=torch.uint8, v_codes=torch.uint8, k_norm=torch.float16, v
 class KVCache:
     """Device buffers of one layer's packed cache, sized by okvq_buffer_bytes (torch allocations),
     with the layer's key signs, value rotations and the decode's inverse-rotation table.
-    key_meta "fp16" keeps the key window minimum and step in k_min / k_step, "mxfp4" in k_mx.
+    key_meta "fp16" keeps the key window minimum and step in k_min / k_step, "mxfp4" in k_mx;
+    "turboquant" stores TurboQuant keys (no window metadata, the paper's baseline).
     residual=RESIDUAL_TOKENS adds the fp16 rings of the captioning protocol (k_res, v_res)."""
 
     def __init__(self, batch, num_kv_heads, num_q_heads, capacity, key_signs: torch.Tensor, v_rot: torch.Tensor,
@@ -349,7 +367,7 @@ class KVCache:
         self.v_rot16 = torch.empty(ROTATION_TABLE_BYTES // 2, dtype=torch.float16, device=device)
         okvq_prepare_rotation(self.v_rot, self.v_rot16)
         self.buffers = {}
-        unused = ("k_mx",) if key_meta == "fp16" else ("k_min", "k_step")
+        unused = {"fp16": ("k_mx",), "mxfp4": ("k_min", "k_step"), "turboquant": ("k_min", "k_step", "k_mx")}[key_meta]
         if not self.residual:
             unused += ("k_res", "v_res")
         for i, name in enumerate(BUFFERS):
@@ -381,7 +399,7 @@ class KVCache:
                  seq_lens=b["seq_lens"][:B])
         if self.key_meta == "fp16":
             v.update(k_min=b["k_min"].view(B, H, cap // 32, 128), k_step=b["k_step"].view(B, H, cap // 32, 128))
-        else:
+        elif self.key_meta == "mxfp4":
             v.update(k_mx=b["k_mx"].view(B, H, cap // 32, MX_RECORD_BYTES))
         if self.residual:
             v.update(k_res=b["k_res"].view(B, H, RESIDUAL_TOKENS, 128), v_res=b["v_res"].view(B, H, RESIDUAL_TOKENS, 128))

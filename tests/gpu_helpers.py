@@ -39,7 +39,7 @@ def quantize_stateless(k, v, modality, lens, signs, rot, capacity, num_q_heads, 
     if key_meta == "fp16":
         out["k_min"] = torch.zeros((B, H, capacity // 32, 128), dtype=torch.float16, device="cuda")
         out["k_step"] = torch.zeros((B, H, capacity // 32, 128), dtype=torch.float16, device="cuda")
-    else:
+    elif key_meta == "mxfp4":
         out["k_mx"] = torch.zeros((B, H, capacity // 32, 136), dtype=torch.uint8, device="cuda")
     kd, vd = f16dev(k), f16dev(v)
     md = dev(np.ascontiguousarray(modality, np.uint8))
@@ -48,8 +48,10 @@ def quantize_stateless(k, v, modality, lens, signs, rot, capacity, num_q_heads, 
     if key_meta == "fp16":
         okvq.okvq_quantize_keys(dims, kd, N, list(lens), sd, out["k_codes"], out["k_min"], out["k_step"],
                                 out["k_norm"])
-    else:
+    elif key_meta == "mxfp4":
         okvq.okvq_quantize_keys_mx(dims, kd, N, list(lens), sd, out["k_codes"], out["k_mx"], out["k_norm"])
+    else:
+        okvq.okvq_quantize_keys_tq(dims, kd, N, list(lens), sd, out["k_codes"], out["k_norm"])
     okvq.okvq_quantize_values(dims, vd, md, N, list(lens), rd, okvq.okvq.OKVQ_VALUE_EXACT if exact else 0,
                               out["v_codes"], out["v_norm"])
     torch.cuda.synchronize()
@@ -127,7 +129,7 @@ def decode(cache, q, lens, sm_scale=1 / math.sqrt(128)):
 def load_cache(cache, arrays, lens):
     """Copy numpy cache arrays (oracle layout) into a KVCache's device buffers."""
     views = cache.views()
-    meta = ("k_mx",) if "k_mx" in views else ("k_min", "k_step")
+    meta = ("k_mx",) if "k_mx" in views else ("k_min", "k_step") if "k_min" in views else ()
     for name in ("k_codes", "v_codes", "k_norm", "v_norm", "modality") + meta:
         views[name].copy_(torch.from_numpy(np.ascontiguousarray(arrays[name])).to(views[name].dtype).cuda()
                           if arrays[name].dtype != np.float16 else torch.from_numpy(arrays[name]).cuda())

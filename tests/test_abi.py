@@ -270,3 +270,33 @@ def test_calibration_validation():
     assert L.okvq_value_covariance(ctypes.byref(d), fake, fake, fake, 100, lens, fake, fake, 16, None) == -4
     assert L.okvq_value_covariance(ctypes.byref(d), fake, fake, fake, 100, over, fake, fake, big, None) == -1
     assert L.okvq_value_covariance(ctypes.byref(d), fake, fake, fake, 0, lens, fake, fake, big, None) == -1
+
+
+def test_turboquant_buffers_and_validation():
+    """TurboQuant keys store no window metadata: 68 bytes per token and KV head with the values,
+    Tab. 3's 2.125 bits per element; each key format is accepted only by its own codec call, and the
+    format does not combine with the fp16 residual."""
+    okvq = _lib()
+    L = okvq.lib()
+    d = okvq.make_dims(2, 4, 28, 4096, key_meta="turboquant")
+    for i in (4, 5, 9):   # k_min, k_step, k_mx
+        assert okvq.okvq_buffer_bytes(d, i) == 0
+    total = sum(okvq.okvq_buffer_bytes(d, i) for i in (0, 1, 2, 3))
+    assert total == 2 * 4 * 4096 * 68
+    assert total * 8 / (2 * 4 * 4096 * 256) == bits_per_element("turboquant_k2v2") == 2.125
+    assert okvq.okvq_buffer_bytes(okvq.make_dims(2, 4, 28, 4096, key_meta="turboquant", residual=128), 0) == 0
+    fake = ctypes.c_void_p(4096)
+    lens = (ctypes.c_int32 * 2)(10, 10)
+    tq = okvq.make_dims(2, 2, 8, 64, key_meta="turboquant")
+    fp = okvq.make_dims(2, 2, 8, 64)
+    assert L.okvq_quantize_keys(ctypes.byref(tq), fake, 10, lens, fake, fake, fake, fake, fake, None) == -1
+    assert L.okvq_quantize_keys_tq(ctypes.byref(fp), fake, 10, lens, fake, fake, fake, None) == -1
+    assert L.okvq_quantize_keys_tq(ctypes.byref(tq), fake, 10, lens, fake, fake, ctypes.c_void_p(4100), None) == -1
+    q_lens = (ctypes.c_int32 * 2)(64, 64)
+    no_meta = okvq.CacheStruct(tq, *([4096] * 4), 0, 0, *([4096] * 3), 4096, 4096, 4096, 0, 0, 0)
+    assert L.okvq_decode_attention(ctypes.byref(no_meta), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, 16,
+                                   None) == -4   # valid up to the workspace size
+    res = okvq.make_dims(2, 2, 8, 64, key_meta="turboquant", residual=128)
+    res_cache = okvq.CacheStruct(res, *([4096] * 9), 4096, 4096, 4096, 0, 4096, 4096)
+    assert L.okvq_decode_attention(ctypes.byref(res_cache), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake,
+                                   1 << 30, None) == -2
