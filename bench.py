@@ -24,6 +24,9 @@ Reported (one JSON line):
   cpu_baseline    the float64 CPU oracle's decode on the same cache, on this host
   mxfp4           the same workload with MXFP4 key window metadata (72.25 instead of 84 bytes per
                   token and KV head): append, decode and split-K kernel time, effective GB/s
+  turboquant      the same workload with TurboQuant keys (Eq. 2: Gaussian codebook after the Hadamard
+                  rotation, no window metadata, 68 bytes per token and KV head) and the single value
+                  rotation R_m = H: the K2/V2 baseline's append and decode
   residual        the same workload in the captioning protocol (fp16 rings of the last 128 keys and
                   values): prefill and one-token append, decode, split-K and merge-with-tail times
   calibration     the value-rotation calibration (Eq. 5) on a 4096-token calibration sequence at the
@@ -32,12 +35,13 @@ Reported (one JSON line):
 
 --profile-pass runs a short fixed sequence for rocprofv3 counter collection: a 256 MiB device
 copy (calibrates FETCH_SIZE / WRITE_SIZE against a known byte count), 8 decode calls on cold
-cache replicas and 2 prefill appends, then the same with MXFP4 key metadata.
+cache replicas and 2 prefill appends, the same with MXFP4 key metadata, 8 decode calls with the
+fp16 residual, and 8 decode calls and 2 appends with TurboQuant keys.
 
 --shape-scan times decode alone at the other workload shapes (batch 16 with ragged lengths up to
 16384, batch 4 x 65536 with 2 KV heads and 16 query heads, 131072 tokens with 32 query heads, and
-batch 32 x 32768), with fp16 and with MXFP4 key metadata, one JSON line each, on caches filled with
-random codes and metadata (the kernel's work does not depend on the values).
+batch 32 x 32768), with fp16 and MXFP4 key metadata and with TurboQuant keys, one JSON line each, on
+caches filled with random codes and metadata (the kernel's work does not depend on the values).
 """
 
 from __future__ import annotations
@@ -61,6 +65,13 @@ APPEND_BYTES_PER_TOKEN_HEAD = 2 * 256 + 84                   # read K, V fp16; w
 MX_RECORD = 136                                              # MXFP4 min/step record of one window
 DECODE_BYTES_PER_WINDOW_HEAD_MX = 2 * 1024 + 2 * 64 + MX_RECORD
 APPEND_BYTES_PER_TOKEN_HEAD_MX = 2 * 256 + 68 + MX_RECORD / 32
+DECODE_BYTES_PER_WINDOW_HEAD_TQ = 2 * 1024 + 2 * 64                # TurboQuant keys: no window metadata
+APPEND_BYTES_PER_TOKEN_HEAD_TQ = 2 * 256 + 68
+DECODE_BYTES_PER_WINDOW = {"fp16": DECODE_BYTES_PER_WINDOW_HEAD, "mxfp4": DECODE_BYTES_PER_WINDOW_HEAD_MX,
+                           "turboquant": DECODE_BYTES_PER_WINDOW_HEAD_TQ}
+APPEND_BYTES_PER_TOKEN = {"fp16": APPEND_BYTES_PER_TOKEN_HEAD, "mxfp4": APPEND_BYTES_PER_TOKEN_HEAD_MX,
+                          "turboquant": APPEND_BYTES_PER_TOKEN_HEAD_TQ}
+CACHE_BYTES_PER_TOKEN_HEAD = {"fp16": 84, "mxfp4": 72.25, "turboquant": 68}
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
 CALIBRATION_COPY_BYTES = 256 << 20
 KERNEL_SOURCES = ("codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "key_quant.hpp", "value_quant.hpp",
@@ -77,7 +88,7 @@ def kernel_source_hash() -> str:
 
 def decode_algorithmic_bytes(B, H, Hq, lens, with_output=True, key_meta="fp16"):
     nwin = sum(-(-int(L) // 32) for L in lens)
-    per_win = DECODE_BYTES_PER_WINDOW_HEAD if key_meta == "fp16" else DECODE_BYTES_PER_WINDOW_HEAD_MX
+    per_win = DECODE_BYTES_PER_WINDOW[key_meta]
     return (nwin * H * per_win + nwin * 32                            # cache + modality map
             + B * Hq * 128 * (2 + (4 if with_output else 0))          # q in, out
             + 3 * 128 * 128 * 4)                                      # rotations
@@ -85,7 +96,7 @@ def decode_algorithmic_bytes(B, H, Hq, lens, with_output=True, key_meta="fp16"):
 
 def append_algorithmic_bytes(B, H, lens, key_meta="fp16"):
     n = sum(int(L) for L in lens)
-    per_tok = APPEND_BYTES_PER_TOKEN_HEAD if key_meta == "fp16" else APPEND_BYTES_PER_TOKEN_HEAD_MX
+    per_tok = APPEND_BYTES_PER_TOKEN[key_meta]
     return int(n * H * per_tok) + 2 * n + 3 * 128 * 128 * 4 + 128
 
 
@@ -185,29 +196,42 @@ def _scan_case(okvq, torch, name, B, lens, H, Hq, key_meta):
 
 
 def shape_scan(okvq, torch, workload, gen_lengths):
-    """Decode alone at the other workload shapes, with fp16 and with MXFP4 key metadata."""
+    """Decode alone at the other workload shapes, with fp16 and MXFP4 key metadata and TurboQuant keys."""
     cases = [("omni7b_b16_ragged16k", None), ("omni3b_b4_64k_stream", None), ("omni30b_128k_48layer", None),
              ("omni7b_32k", 32)]
     for name, batch in cases:
         wl = workload(name)
         B = batch or wl.batch
         lens = [int(x) for x in gen_lengths(wl)] if batch is None else [wl.seq_len] * B
-        for km in ("fp16", "mxfp4"):
+        for km in ("fp16", "mxfp4", "turboquant"):
             _scan_case(okvq, torch, name, B, lens, wl.num_kv_heads, wl.num_q_heads, km)
 
 
-def mx_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream, decode_iters):
-    """The benchmark workload with MXFP4 key window metadata (the paper's default storage): prefill
-    append into an empty cache, decode over >= 1 GB of cold cache replicas, and the split-K kernel's
-    duration from events bound to its dispatch."""
+def sylvester_hadamard(signs):
+    """Orthonormal randomized Hadamard matrix H diag(signs) of order 128 (Sylvester construction):
+    the single value rotation of the TurboQuant baseline."""
+    import numpy as np
+    h = np.ones((1, 1))
+    while h.shape[0] < 128:
+        h = np.block([[h, h], [h, -h]])
+    return (h * np.asarray(signs, np.float64)[None, :] / math.sqrt(128)).astype(np.float32)
+
+
+def key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream, decode_iters,
+                         key_meta, signs=None, rot=None):
+    """The benchmark workload with another key storage: MXFP4 window metadata (the paper's default)
+    or TurboQuant keys (no window metadata). Prefill append into an empty cache, decode over >= 1 GB
+    of cold cache replicas, and the split-K kernel's duration from events bound to its dispatch."""
     B, H, Hq, N = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.seq_len
     dev = q.device
     sm = 1 / math.sqrt(128)
-    dims = okvq.make_dims(B, H, Hq, wl.capacity, key_meta="mxfp4")
+    dims = okvq.make_dims(B, H, Hq, wl.capacity, key_meta=key_meta)
     per_cache = sum(okvq.okvq_buffer_bytes(dims, i) for i in range(10))
     n_cache = max(16, int(math.ceil(1.05e9 / per_cache)))
-    caches = [okvq.KVCache(B, H, Hq, wl.capacity, torch.ones(128, dtype=torch.int8), torch.eye(128).repeat(3, 1, 1),
-                           device=dev, key_meta="mxfp4") for _ in range(n_cache)]
+    signs = torch.ones(128, dtype=torch.int8) if signs is None else signs
+    rot = torch.eye(128).repeat(3, 1, 1) if rot is None else rot
+    caches = [okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev, key_meta=key_meta)
+              for _ in range(n_cache)]
     okvq.okvq_append(caches[0], [0] * B, k_in[0], v_in[0], m0, lens, n_new_dev, N, stream=stream)
     torch.cuda.synchronize()
     for c in caches[1:]:
@@ -248,14 +272,16 @@ def mx_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stre
         okvq.okvq_decode_attention_timed(caches[(i * 7 + 5) % n_cache], lens, q, sm, out, ws, evs[i], stream=stream)
     torch.cuda.synchronize()
     split_us = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) * 1e3
-    dbytes = decode_algorithmic_bytes(B, H, Hq, lens, key_meta="mxfp4")
-    sbytes = decode_algorithmic_bytes(B, H, Hq, lens, with_output=False, key_meta="mxfp4")
-    abytes = append_algorithmic_bytes(B, H, lens, key_meta="mxfp4")
+    dbytes = decode_algorithmic_bytes(B, H, Hq, lens, key_meta=key_meta)
+    sbytes = decode_algorithmic_bytes(B, H, Hq, lens, with_output=False, key_meta=key_meta)
+    abytes = append_algorithmic_bytes(B, H, lens, key_meta=key_meta)
     del caches
-    return {"bytes_per_token_head": 72.25, "decode_us": round(decode_us, 3),
+    tag = {"mxfp4": "mx", "turboquant": "tq"}[key_meta]
+    return {"bytes_per_token_head": CACHE_BYTES_PER_TOKEN_HEAD[key_meta], "decode_us": round(decode_us, 3),
             "decode_GBps": round(dbytes / decode_us / 1e3, 2),
             "k_decode_us": round(split_us, 3), "k_decode_GBps": round(sbytes / split_us / 1e3, 2),
-            "k_decode_frac": round(sbytes / split_us / 1e3 / HBM_PEAK_GBPS, 4), "traffic": measured_traffic("k_decode_mx"),
+            "k_decode_frac": round(sbytes / split_us / 1e3 / HBM_PEAK_GBPS, 4),
+            "traffic": measured_traffic(f"k_decode_{tag}"), "append_traffic": measured_traffic(f"k_codec_{tag}"),
             "append_us": round(append_us, 3), "append_GBps": round(abytes / append_us / 1e3, 2),
             "append_frac": round(abytes / append_us / 1e3 / HBM_PEAK_GBPS, 4), "algorithmic_bytes": dbytes,
             "replicas": n_cache}
@@ -495,10 +521,28 @@ def main():
         for i in range(8):
             okvq.okvq_decode_attention(res[(7 * i + 3) % 16], lens, q, sm, out, ws_res, stream=stream)
         torch.cuda.synchronize()
+        del res
+        # TurboQuant keys (no window metadata)
+        tq = [okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev, key_meta="turboquant") for _ in range(16)]
+        okvq.okvq_append(tq[0], [0] * B, k_in[0], v_in[0], m0, lens, n_new_dev, N, stream=stream)
+        torch.cuda.synchronize()
+        for c in tq[1:]:
+            for name in c.buffers:
+                c.buffers[name].copy_(tq[0].buffers[name])
+        ws_tq = okvq.decode_workspace(tq[0].dims, max(lens), device=dev)
+        torch.cuda.synchronize()
+        for i in range(8):
+            okvq.okvq_decode_attention(tq[(7 * i + 3) % 16], lens, q, sm, out, ws_tq, stream=stream)
+        torch.cuda.synchronize()
+        for i in range(2):
+            tq[i + 1].buffers["seq_lens"].zero_()
+            okvq.okvq_append(tq[i + 1], [0] * B, k_in[i + 1], v_in[i + 1], m0, lens, n_new_dev, N, stream=stream)
+        torch.cuda.synchronize()
         print(json.dumps({"profile_pass": True, "copy_bytes": CALIBRATION_COPY_BYTES, "decode_calls": 8,
                           "append_calls": 2, "decode_algorithmic_bytes": decode_algorithmic_bytes(B, H, Hq, lens),
                           "append_algorithmic_bytes": append_algorithmic_bytes(B, H, lens),
                           "mxfp4_decode_calls": 8, "mxfp4_append_calls": 2, "residual_decode_calls": 8,
+                          "turboquant_decode_calls": 8, "turboquant_append_calls": 2,
                           "residual_decode_algorithmic_bytes": residual_decode_algorithmic_bytes(B, H, Hq, lens)}),
               flush=True)
         return
@@ -603,8 +647,11 @@ def main():
                             "algorithmic_bytes": abytes},
         "cache_replicas": n_cache,
     }
-    line["mxfp4"] = mx_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
-                                   args.decode_iters)
+    line["mxfp4"] = key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
+                                         args.decode_iters, "mxfp4")
+    line["turboquant"] = key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
+                                              args.decode_iters, "turboquant", signs,
+                                              torch.from_numpy(sylvester_hadamard(lay["signs"])).repeat(3, 1, 1))
     line["calibration"] = calibration_measurement(okvq, torch, np, wl, dev)
     line["residual"] = residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                             args.decode_iters)
