@@ -336,6 +336,37 @@ okvq_status okvq_value_covariance(const okvq_dims* dims, const uint16_t* v, cons
  * modality with C_m = 0 (absent from the calibration data) gets U_m = I, i.e. R_m = H. */
 okvq_status okvq_rotation_from_covariance(const float* cov, const int8_t* signs, float* rot, double* eigenvalues);
 
+/* ---- Dense fp16 decode attention: the comparison baseline ------------------------------------
+ * Eq. 1 over an unquantized fp16 KV cache (no codes, norms, rotations or modality map): the
+ * attention that the packed cache replaces, computed the same way (split-K launch, every query head
+ * of a KV head served from one read of K and V, scores and PV on the matrix cores with fp16
+ * operands and fp32 accumulation, a log-sum-exp merge launch). */
+
+/* Device workspace bytes needed by okvq_decode_attention_dense for sequences up to max_seq_len
+ * (0 for invalid dims or a negative length). No initial contents are needed. */
+size_t okvq_dense_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len);
+
+/* One dense decode step.
+ *   dims       batch, num_kv_heads, num_q_heads (G = Hq / H <= 8), head_dim 128, and capacity =
+ *              the token stride of k and v (a multiple of 32); window must be 32, key_meta and
+ *              residual are not used
+ *   k, v       device f16 [B][H][capacity][128]: rows of token i < seq_lens[b] are read
+ *   seq_lens   device i32 [B]: the lengths the kernels use
+ *   lens_host  host i32 [B], 0 <= lens_host[b] <= capacity: plans the launch (equal to seq_lens)
+ *   q          device f16 [B][Hq][128]; query head j reads KV head j / G
+ *   sm_scale   softmax scale, normally 1/sqrt(128)
+ *   out        device f32 [B][Hq][128]; a sequence of length 0 yields zeros
+ *   workspace  device, at least okvq_dense_workspace_bytes(dims, max(lens_host)) bytes
+ *   events     NULL, or four hipEvent_t handles recorded at the start and end of the split-K
+ *              kernel's and of the merge kernel's execution
+ * Every pointer must be 16-byte aligned; arguments are checked on the host before anything is
+ * enqueued. The result matches float64 attention over the same fp16 K and V within 2e-3 of the
+ * output norm. */
+okvq_status okvq_decode_attention_dense(const okvq_dims* dims, const uint16_t* k, const uint16_t* v,
+                                        const int32_t* seq_lens, const int32_t* lens_host, const uint16_t* q,
+                                        float sm_scale, float* out, void* workspace, size_t workspace_bytes,
+                                        void* stream, void* const* events);
+
 #ifdef __cplusplus
 }
 #endif

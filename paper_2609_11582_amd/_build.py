@@ -12,7 +12,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libokvq.so")
-SOURCES = ["api.hip", "codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "calib_kernels.hip"]
+SOURCES = ["api.hip", "codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "calib_kernels.hip",
+           "dense_decode.hip"]
 
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
@@ -33,9 +34,9 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-# per-source additions: the decode kernels never see NaN (finite inputs; -inf is the only special
+# per-source additions: the decode kernels (packed and dense) never see NaN (finite inputs; -inf is the only special
 # value they use), so min / max need no NaN quieting
-EXTRA = {"decode_kernels.hip": ["-fno-honor-nans"]}
+EXTRA = {"decode_kernels.hip": ["-fno-honor-nans"], "dense_decode.hip": ["-fno-honor-nans"]}
 
 
 def build(verbose: bool = False, jobs: int = 4) -> str:

@@ -13,7 +13,7 @@ using namespace okvq;
 
 namespace {
 
-constexpr int32_t kVersion = 400;  // 0.4.0: value-rotation calibration, TurboQuant keys
+constexpr int32_t kVersion = 500;  // 0.5.0: dense fp16 decode baseline
 
 // ---- fixed Gaussian codebook (Sec. 2.1, Eq. 3): Lloyd-Max quantizer of N(0, 1), 4 levels ----
 double phi(double x) { return std::isinf(x) ? 0.0 : std::exp(-0.5 * x * x) / std::sqrt(2.0 * M_PI); }
@@ -477,6 +477,41 @@ okvq_status okvq_decode_attention_timed(const okvq_cache* cache, const int32_t* 
                                         size_t workspace_bytes, void* stream, void* const* events) {
   if (!events) return OKVQ_ERR_INVALID_ARGUMENT;
   return decode_impl(cache, lens_host, q, sm_scale, flags, out, workspace, workspace_bytes, stream, events);
+}
+
+size_t okvq_dense_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len) {
+  if (check_dims(dims) != OKVQ_OK || max_seq_len < 0) return 0;
+  return dense_workspace_bytes(dims->batch, dims->num_kv_heads, max_seq_len);
+}
+
+okvq_status okvq_decode_attention_dense(const okvq_dims* dims, const uint16_t* k, const uint16_t* v,
+                                        const int32_t* seq_lens, const int32_t* lens_host, const uint16_t* q,
+                                        float sm_scale, float* out, void* workspace, size_t workspace_bytes,
+                                        void* stream, void* const* events) {
+  okvq_status st = check_dims(dims);
+  if (st != OKVQ_OK) return st;
+  if (!lens_host || !std::isfinite(sm_scale)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(seq_lens) || !aligned16(q) || !aligned16(out))
+    return OKVQ_ERR_INVALID_ARGUMENT;
+  int max_len = 0;
+  for (int b = 0; b < dims->batch; ++b) {
+    if (lens_host[b] < 0) return OKVQ_ERR_INVALID_ARGUMENT;
+    if (lens_host[b] > dims->capacity) return OKVQ_ERR_CAPACITY;
+    max_len = std::max(max_len, lens_host[b]);
+  }
+  const size_t need = dense_workspace_bytes(dims->batch, dims->num_kv_heads, max_len);
+  if (!aligned16(workspace) || workspace_bytes < need) return OKVQ_ERR_WORKSPACE;
+  hipEvent_t ev[4];
+  if (events) {
+    for (int i = 0; i < 4; ++i) {
+      if (!events[i]) return OKVQ_ERR_INVALID_ARGUMENT;
+      ev[i] = static_cast<hipEvent_t>(events[i]);
+    }
+  }
+  const DensePlan plan = plan_dense(dims->batch, dims->num_kv_heads, max_len);
+  return hip_status(launch_decode_dense(k, v, seq_lens, q, dims->batch, dims->num_kv_heads, dims->num_q_heads,
+                                        dims->capacity, sm_scale, out, workspace, plan,
+                                        static_cast<hipStream_t>(stream), events ? ev : nullptr));
 }
 
 size_t okvq_calibration_workspace_bytes(const okvq_dims* dims, int32_t n_tokens) {

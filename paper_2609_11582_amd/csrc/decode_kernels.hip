@@ -37,12 +37,9 @@ typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kDecWaves = 8;                    // waves per split work-group
-constexpr int kRecHeader = 32;                  // m[8], l[8], pad
-constexpr int kRecFloats = kRecHeader + 8 * kD; // + o[8 heads][128], un-rotated, divided by l
 constexpr int kATile = 3 * kD + 8;              // fp16 row pitch of the un-rotation A tile
 constexpr int kAccPitch = 28;                   // combine tile [channel][24 rows + 4]: conflict-free b128
 constexpr int kMinWps = 2 * kDecWaves;          // fewest windows per split (a pair per wave)
-constexpr int kMaxSplits = 1024;                // most splits per (sequence, KV head)
 constexpr float kLazy = 8.0f;                   // log2 headroom of the lazily updated softmax max
 
 struct DecodeArgs {
@@ -1167,6 +1164,17 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
     hipLaunchKernelGGL(k_decode_merge, mgrid, mblock, 0, s, static_cast<const float*>(a.ws), c.H, c.Hq, G,
                        plan.nsplit, out);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_merge(const float* ws, int B, int H, int Hq, int nsplit, float* out, hipStream_t s,
+                               hipEvent_t const* events) {
+  const dim3 mgrid(Hq, B), mblock(kMergeThreads);
+  const int G = Hq / H;
+  if (events)
+    hipExtLaunchKernelGGL(k_decode_merge, mgrid, mblock, 0, s, events[0], events[1], 0, ws, H, Hq, G, nsplit, out);
+  else
+    hipLaunchKernelGGL(k_decode_merge, mgrid, mblock, 0, s, ws, H, Hq, G, nsplit, out);
   return hipGetLastError();
 }
 

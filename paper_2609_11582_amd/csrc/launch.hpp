@@ -103,6 +103,12 @@ struct CacheView {
   const uint16_t* v_res;
 };
 
+// Split record of the split-K decode launches (read by the log-sum-exp merge): the running max
+// M[8] and sum L[8] of the 8 query-head slots, then o[8][128] divided by L.
+constexpr int kRecHeader = 32;
+constexpr int kRecFloats = kRecHeader + 8 * kD;
+constexpr int kMaxSplits = 1024;  // most splits per (sequence, KV head)
+
 struct DecodePlan {
   int wins_per_split;  // 32-token windows per split-K work-group
   int nsplit;          // splits per (sequence, KV head)
@@ -114,5 +120,22 @@ hipError_t launch_prepare_rotation(const float* rot, uint16_t* rot16t, hipStream
 hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, float* out, void* ws,
                          const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int max_len,
                          hipEvent_t const* events);
+
+// Log-sum-exp merge of split records [B][H][nsplit][kRecFloats] into out [B][Hq][128]; events:
+// nullptr, or two events bound to the launch (start, end).
+hipError_t launch_decode_merge(const float* ws, int B, int H, int Hq, int nsplit, float* out, hipStream_t s,
+                               hipEvent_t const* events);
+
+// Dense fp16 decode attention (the comparison baseline): split-K over 256-token steps, then the
+// same merge. events: nullptr, or four events (split start, end; merge start, end).
+struct DensePlan {
+  int tokens_per_split;
+  int nsplit;
+};
+DensePlan plan_dense(int B, int H, int max_len);
+size_t dense_workspace_bytes(int B, int H, int max_len);
+hipError_t launch_decode_dense(const uint16_t* k, const uint16_t* v, const int32_t* seq_lens, const uint16_t* q, int B,
+                               int H, int Hq, int cap, float sm_scale, float* out, void* ws, const DensePlan& plan,
+                               hipStream_t s, hipEvent_t const* events);
 
 }  // namespace okvq

@@ -95,6 +95,11 @@ def lib() -> ctypes.CDLL:
         L.okvq_value_covariance.argtypes = [P(Dims), vp, vp, vp, i32, P(i32), vp, vp, sz, vp]
         L.okvq_rotation_from_covariance.restype = i32
         L.okvq_rotation_from_covariance.argtypes = [vp, vp, vp, vp]
+        L.okvq_dense_workspace_bytes.restype = sz
+        L.okvq_dense_workspace_bytes.argtypes = [P(Dims), i32]
+        L.okvq_decode_attention_dense.restype = i32
+        L.okvq_decode_attention_dense.argtypes = [P(Dims), vp, vp, vp, P(i32), vp, ctypes.c_float, vp, vp, sz, vp,
+                                                  P(vp)]
         _lib = L
     return _lib
 
@@ -285,6 +290,43 @@ def okvq_decode_attention_timed(cache: "KVCache", lens, q, sm_scale, out, worksp
                                            _ptr(out), _ptr(workspace), int(nbytes), _stream(stream), handles)
     if check:
         _check(st, "okvq_decode_attention_timed")
+    return st
+
+
+def okvq_dense_workspace_bytes(dims: Dims, max_seq_len: int) -> int:
+    return lib().okvq_dense_workspace_bytes(ctypes.byref(dims), int(max_seq_len))
+
+
+def dense_workspace(dims: Dims, max_seq_len: int, device="cuda") -> torch.Tensor:
+    """A workspace of okvq_dense_workspace_bytes bytes for the dense decode (no contents needed)."""
+    nbytes = max(okvq_dense_workspace_bytes(dims, max_seq_len), 16)
+    return torch.empty((nbytes + 15) // 16 * 4, dtype=torch.float32, device=device)
+
+
+def okvq_decode_attention_dense(dims: Dims, k, v, seq_lens, lens, q, sm_scale, out, workspace, events=None,
+                                workspace_bytes=None, stream=None, check=True) -> int:
+    """Dense fp16 decode attention over k, v [B][H][capacity][128] (the comparison baseline);
+    events: None, or four torch.cuda.Event objects (split-K start, end; merge start, end)."""
+    B, H, Hq, cap = dims.batch, dims.num_kv_heads, dims.num_q_heads, dims.capacity
+    _need_len(lens, B, "lens")
+    _need(k, B * H * cap * 128 * 2, "k")
+    _need(v, B * H * cap * 128 * 2, "v")
+    _need(seq_lens, B * 4, "seq_lens")
+    _need(q, B * Hq * 128 * 2, "q")
+    _need(out, B * Hq * 128 * 4, "out")
+    handles = None
+    if events is not None:
+        _need_len(events, 4, "events")
+        handles = (ctypes.c_void_p * 4)(*[ctypes.c_void_p(e.cuda_event) for e in events])
+        if not all(handles):
+            raise ValueError("events: record each torch.cuda.Event once before passing it (torch creates them lazily)")
+    have = workspace.numel() * workspace.element_size()
+    nbytes = have if workspace_bytes is None else min(int(workspace_bytes), have)
+    st = lib().okvq_decode_attention_dense(ctypes.byref(dims), _ptr(k), _ptr(v), _ptr(seq_lens), _i32(lens), _ptr(q),
+                                           float(sm_scale), _ptr(out), _ptr(workspace), int(nbytes), _stream(stream),
+                                           handles)
+    if check:
+        _check(st, "okvq_decode_attention_dense")
     return st
 
 

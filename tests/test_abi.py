@@ -300,3 +300,34 @@ def test_turboquant_buffers_and_validation():
     res_cache = okvq.CacheStruct(res, *([4096] * 9), 4096, 4096, 4096, 0, 4096, 4096)
     assert L.okvq_decode_attention(ctypes.byref(res_cache), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake,
                                    1 << 30, None) == -2
+
+
+def test_dense_decode_validation():
+    """The dense fp16 baseline: workspace sizing and argument checks before any launch."""
+    okvq = _lib()
+    L = okvq.lib()
+    d = okvq.make_dims(2, 2, 8, 64)
+    ws = okvq.okvq_dense_workspace_bytes(d, 64)
+    assert ws == 2 * 2 * 1 * (32 + 8 * 128) * 4        # one 256-token split per (sequence, head)
+    assert okvq.okvq_dense_workspace_bytes(d, 600) == 2 * 2 * 3 * (32 + 8 * 128) * 4
+    assert okvq.okvq_dense_workspace_bytes(d, -1) == 0
+    assert okvq.okvq_dense_workspace_bytes(okvq.make_dims(2, 2, 8, 64, head_dim=64), 64) == 0
+    fake = ctypes.c_void_p(4096)
+    lens = (ctypes.c_int32 * 2)(64, 10)
+    sm = ctypes.c_float(0.1)
+    big = 1 << 30
+    args = lambda dims, lens_, k=fake, wsb=big: (ctypes.byref(dims), k, fake, fake, lens_, fake, sm, fake, fake, wsb,
+                                                 None, None)
+    assert L.okvq_decode_attention_dense(*args(d, lens, wsb=ws - 1)) == -4
+    assert L.okvq_decode_attention_dense(*args(d, lens, k=ctypes.c_void_p(4100))) == -1
+    assert L.okvq_decode_attention_dense(*args(d, (ctypes.c_int32 * 2)(65, 0))) == -3
+    assert L.okvq_decode_attention_dense(*args(d, (ctypes.c_int32 * 2)(-1, 0))) == -1
+    assert L.okvq_decode_attention_dense(*args(okvq.make_dims(2, 1, 16, 64), lens)) == -2
+    assert L.okvq_decode_attention_dense(ctypes.byref(d), fake, fake, fake, None, fake, sm, fake, fake, big, None,
+                                         None) == -1
+    nan = ctypes.c_float(float("nan"))
+    assert L.okvq_decode_attention_dense(ctypes.byref(d), fake, fake, fake, lens, fake, nan, fake, fake, big, None,
+                                         None) == -1
+    bad_events = (ctypes.c_void_p * 4)(4096, 4096, 0, 4096)
+    assert L.okvq_decode_attention_dense(ctypes.byref(d), fake, fake, fake, lens, fake, sm, fake, fake, big, None,
+                                         bad_events) == -1
