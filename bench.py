@@ -29,6 +29,10 @@ Reported (one JSON line):
                   rotation R_m = H: the K2/V2 baseline's append and decode
   residual        the same workload in the captioning protocol (fp16 rings of the last 128 keys and
                   values): prefill and one-token append, decode, split-K and merge-with-tail times
+  omni30b_48layer the 30B-like workload with all 48 layers' caches resident (131072 tokens, 4 KV heads,
+                  32 query heads): one decode step per layer over the packed caches, over packed
+                  caches with the single global value rotation, and with the dense fp16 baseline
+                  kernel over the same fp16 K and V (12.9 GB resident); per-layer append
   calibration     the value-rotation calibration (Eq. 5) on a 4096-token calibration sequence at the
                   same head shapes: attention weights (against the fp16 matrix-core peak), weighted
                   covariance, host eigensolver
@@ -36,7 +40,8 @@ Reported (one JSON line):
 --profile-pass runs a short fixed sequence for rocprofv3 counter collection: a 256 MiB device
 copy (calibrates FETCH_SIZE / WRITE_SIZE against a known byte count), 8 decode calls on cold
 cache replicas and 2 prefill appends, the same with MXFP4 key metadata, 8 decode calls with the
-fp16 residual, and 8 decode calls and 2 appends with TurboQuant keys.
+fp16 residual, 8 decode calls and 2 appends with TurboQuant keys, and 4 dense fp16 decode calls at
+the 30B-like layer shape.
 
 --shape-scan times decode alone at the other workload shapes (batch 16 with ragged lengths up to
 16384, batch 4 x 65536 with 2 KV heads and 16 query heads, 131072 tokens with 32 query heads, and
@@ -75,7 +80,7 @@ CACHE_BYTES_PER_TOKEN_HEAD = {"fp16": 84, "mxfp4": 72.25, "turboquant": 68}
 PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
 CALIBRATION_COPY_BYTES = 256 << 20
 KERNEL_SOURCES = ("codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "key_quant.hpp", "value_quant.hpp",
-                  "okvq_device.hpp", "launch.hpp", "calib_kernels.hip")
+                  "okvq_device.hpp", "launch.hpp", "calib_kernels.hip", "dense_decode.hip")
 
 
 def kernel_source_hash() -> str:
@@ -287,6 +292,130 @@ def key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
             "replicas": n_cache}
 
 
+def dense_decode_bytes(B, H, Hq, lens):
+    """Dense fp16 decode: K and V rows (512 B per token and KV head), q in, out."""
+    return sum(int(L) for L in lens) * H * 512 + B * Hq * 128 * (2 + 4)
+
+
+def layers48_measurement(okvq, torch, np, dev, stream, reps=5):
+    """The 30B-like workload: 48 layers of 131072 tokens resident at once (4 KV heads, 32 query
+    heads), one decode step per layer. Each layer's inputs are generated on the device with its own
+    seed (synth.device) and appended into its own packed cache; the same fp16 K and V stay resident
+    for the dense fp16 baseline (12.9 GB), and a second set of packed caches uses the single global
+    value rotation R_m = H_v (a randomized Hadamard with its own signs) for every modality."""
+    from synth import gen_signs, workload
+    from synth.device import gen_layer_device
+    wl = workload("omni30b_128k_48layer")
+    B, H, Hq, N, nl = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.seq_len, wl.layers
+    sm = 1 / math.sqrt(128)
+    lens = [N] * B
+    n_new = torch.tensor(lens, dtype=torch.int32, device=dev)
+    packed, glob, dk, dv, qs, app = [], [], [], [], [], []
+    for layer in range(nl):
+        lay = gen_layer_device(wl, layer, dev)
+        signs = torch.from_numpy(lay["signs"])
+        hv = torch.from_numpy(sylvester_hadamard(gen_signs(wl.wid, 1000 + layer))).repeat(3, 1, 1)
+        c = okvq.KVCache(B, H, Hq, wl.capacity, signs, torch.from_numpy(lay["rot"]), device=dev)
+        cg = okvq.KVCache(B, H, Hq, wl.capacity, signs, hv, device=dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        okvq.okvq_append(c, [0] * B, lay["k"], lay["v"], lay["modality"], lens, n_new, N, stream=stream)
+        e1.record(stream)
+        okvq.okvq_append(cg, [0] * B, lay["k"], lay["v"], lay["modality"], lens, n_new, N, stream=stream)
+        app.append((e0, e1))
+        packed.append(c)
+        glob.append(cg)
+        dk.append(lay["k"])
+        dv.append(lay["v"])
+        qs.append(torch.from_numpy(lay["q"]).to(dev))
+        torch.cuda.synchronize()
+    append_us = float(np.mean([a.elapsed_time(b) for a, b in app[2:]])) * 1e3
+    ws = okvq.decode_workspace(packed[0].dims, N, device=dev)
+    ddims = okvq.make_dims(B, H, Hq, N)
+    dws = okvq.dense_workspace(ddims, N, device=dev)
+    seq = torch.tensor(lens, dtype=torch.int32, device=dev)
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+
+    def packed_call(layer, caches=packed, events=None):
+        if events is None:
+            okvq.okvq_decode_attention(caches[layer], lens, qs[layer], sm, out, ws, stream=stream)
+        else:
+            okvq.okvq_decode_attention_timed(caches[layer], lens, qs[layer], sm, out, ws, events, stream=stream)
+
+    def dense_call(layer, events=None):
+        okvq.okvq_decode_attention_dense(ddims, dk[layer], dv[layer], seq, lens, qs[layer], sm, out, dws,
+                                         events=events, stream=stream)
+
+    def sweep(fn):
+        """median µs of one decode step over all 48 layers, back to back"""
+        for layer in range(nl):
+            fn(layer)
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for layer in range(nl):
+                fn(layer)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e3)
+        return float(np.median(ts))
+
+    def kernel_us(fn):
+        """mean duration of the split-K kernel and of the merge over one sweep (events bound to them)"""
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(nl)]
+        for e4 in evs:
+            for e in e4:
+                e.record(stream)
+        torch.cuda.synchronize()
+        for layer in range(nl):
+            fn(layer, events=evs[layer])
+        torch.cuda.synchronize()
+        return (float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) * 1e3,
+                float(np.mean([e[2].elapsed_time(e[3]) for e in evs])) * 1e3)
+
+    def latency(fn):
+        lat = []
+        for i in range(20):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn(i % nl)
+            torch.cuda.synchronize()
+            lat.append((time.perf_counter() - t0) * 1e6)
+        return float(np.median(lat))
+
+    pk = decode_algorithmic_bytes(B, H, Hq, lens)
+    pk_split = decode_algorithmic_bytes(B, H, Hq, lens, with_output=False)
+    dn = dense_decode_bytes(B, H, Hq, lens)
+    dn_split = dn - B * Hq * 128 * 4
+    t_packed = sweep(packed_call)
+    t_glob = sweep(lambda layer: packed_call(layer, glob))
+    t_dense = sweep(dense_call)
+    ks, km = kernel_us(packed_call)
+    ds, dm = kernel_us(dense_call)
+    res = {
+        "workload": "omni30b_128k_48layer", "layers": nl, "batch": B, "kv_heads": H, "q_heads": Hq, "seq_len": N,
+        "data": "synthetic, generated on the device per layer (same recipe, torch generator)",
+        "resident_GB": {"packed": round(nl * sum(okvq.okvq_buffer_bytes(packed[0].dims, i) for i in range(10)) / 1e9, 3),
+                        "dense_fp16": round(nl * 2 * B * H * N * 256 / 1e9, 3)},
+        "packed": {"decode_us_all_layers": round(t_packed, 2), "decode_us_per_layer": round(t_packed / nl, 3),
+                   "GBps": round(pk * nl / t_packed / 1e3, 1), "k_decode_us": round(ks, 3),
+                   "k_decode_merge_us": round(km, 3), "k_decode_frac": round(pk_split / ks / 1e3 / HBM_PEAK_GBPS, 4),
+                   "latency_us_per_layer": round(latency(packed_call), 2), "append_us_per_layer": round(append_us, 2),
+                   "algorithmic_bytes_per_layer": pk},
+        "global_rotation": {"decode_us_all_layers": round(t_glob, 2), "decode_us_per_layer": round(t_glob / nl, 3)},
+        "dense_fp16": {"decode_us_all_layers": round(t_dense, 2), "decode_us_per_layer": round(t_dense / nl, 3),
+                       "GBps": round(dn * nl / t_dense / 1e3, 1), "k_decode_dense_us": round(ds, 3),
+                       "merge_us": round(dm, 3), "k_decode_dense_frac": round(dn_split / ds / 1e3 / HBM_PEAK_GBPS, 4),
+                       "latency_us_per_layer": round(latency(dense_call), 2), "algorithmic_bytes_per_layer": dn,
+                       "traffic": measured_traffic("k_decode_dense")},
+        "speedup_packed_vs_dense": round(t_dense / t_packed, 3),
+    }
+    del packed, glob, dk, dv
+    torch.cuda.empty_cache()
+    return res
+
+
 def residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream, decode_iters):
     """The benchmark workload in the captioning protocol (Sec. 3.1): fp16 rings of the last 128 keys
     and values next to the packed cache. Prefill append, one-token append (a generation step), and
@@ -423,6 +552,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--decode-iters", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-layers48", action="store_true", help="skip the 48-layer 131072-token measurement")
     ap.add_argument("--profile-pass", action="store_true", help="short fixed sequence for rocprofv3 --pmc runs")
     ap.add_argument("--shape-scan", action="store_true", help="decode throughput at the other workload shapes")
     args = ap.parse_args()
@@ -538,11 +668,29 @@ def main():
             tq[i + 1].buffers["seq_lens"].zero_()
             okvq.okvq_append(tq[i + 1], [0] * B, k_in[i + 1], v_in[i + 1], m0, lens, n_new_dev, N, stream=stream)
         torch.cuda.synchronize()
+        del tq
+        # the dense fp16 baseline at the 30B-like layer shape: 4 calls alternating over two layers' K
+        # and V (537 MB, beyond the 256 MB Infinity Cache)
+        from synth.device import gen_layer_device
+        w5 = workload("omni30b_128k_48layer")
+        l5 = [gen_layer_device(w5, i, dev) for i in range(2)]
+        d5 = okvq.make_dims(w5.batch, w5.num_kv_heads, w5.num_q_heads, w5.seq_len)
+        lens5 = [w5.seq_len] * w5.batch
+        ws5 = okvq.dense_workspace(d5, w5.seq_len, device=dev)
+        q5 = torch.from_numpy(l5[0]["q"]).to(dev)
+        s5 = torch.tensor(lens5, dtype=torch.int32, device=dev)
+        o5 = torch.empty((w5.batch, w5.num_q_heads, 128), dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+        for i in range(4):
+            okvq.okvq_decode_attention_dense(d5, l5[i % 2]["k"], l5[i % 2]["v"], s5, lens5, q5, sm, o5, ws5,
+                                             stream=stream)
+        torch.cuda.synchronize()
         print(json.dumps({"profile_pass": True, "copy_bytes": CALIBRATION_COPY_BYTES, "decode_calls": 8,
                           "append_calls": 2, "decode_algorithmic_bytes": decode_algorithmic_bytes(B, H, Hq, lens),
                           "append_algorithmic_bytes": append_algorithmic_bytes(B, H, lens),
                           "mxfp4_decode_calls": 8, "mxfp4_append_calls": 2, "residual_decode_calls": 8,
-                          "turboquant_decode_calls": 8, "turboquant_append_calls": 2,
+                          "turboquant_decode_calls": 8, "turboquant_append_calls": 2, "dense_decode_calls": 4,
+                          "dense_decode_algorithmic_bytes": dense_decode_bytes(1, 4, 32, [131072]),
                           "residual_decode_algorithmic_bytes": residual_decode_algorithmic_bytes(B, H, Hq, lens)}),
               flush=True)
         return
@@ -653,6 +801,8 @@ def main():
                                               args.decode_iters, "turboquant", signs,
                                               torch.from_numpy(sylvester_hadamard(lay["signs"])).repeat(3, 1, 1))
     line["calibration"] = calibration_measurement(okvq, torch, np, wl, dev)
+    if not args.no_layers48:
+        line["omni30b_48layer"] = layers48_measurement(okvq, torch, np, dev, stream)
     line["residual"] = residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                             args.decode_iters)
     if not args.no_cpu_baseline:
