@@ -21,7 +21,9 @@ Reported (one JSON line):
                   roofline_append: the whole append call (the fused codec launch and the length
                   update)
   kernels_us      mean duration of each launch, from the same events
-  cpu_baseline    the float64 CPU oracle's decode on the same cache, on this host
+  codec_split     the prefill's keys and values quantized by separate stateless calls
+  cpu_baseline    the CPU oracle on this host: its float64 decode of the same cache on all cores (value)
+                  and single-threaded, and its fp32-order quantization of the prefill
   mxfp4           the same workload with MXFP4 key window metadata (72.25 instead of 84 bytes per
                   token and KV head): append, decode and split-K kernel time, effective GB/s
   turboquant      the same workload with TurboQuant keys (Eq. 2: Gaussian codebook after the Hadamard
@@ -135,23 +137,52 @@ def measured_traffic(kernel_key):
     return None if entry is None else entry.get("bytes_per_launch")
 
 
-def cpu_baseline(cache_np, q, lens, signs, rot, bytes_per_call, min_seconds=10.0):
-    """The float64 oracle's decode (all KV heads of the layer), timed on this host."""
-    from threadpoolctl import threadpool_info
+def cpu_baseline(cache_np, q, lens, signs, rot, bytes_per_call, prefill=None, append_bytes=None,
+                 decode_seconds=8.0, single_seconds=4.0):
+    """The CPU oracle as it stands, timed on this host: the float64 decode of the layer (all KV heads)
+    on every core the BLAS pool uses and single-threaded, and the fp32-order (FMT) quantization of
+    the prefill (all 32768 tokens and KV heads; one KV head single-threaded)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
 
-    from oracle.cache import decode_layer
-    t0 = time.perf_counter()
-    calls = 0
-    while True:
-        decode_layer(cache_np, q, lens, signs, rot, 1 / math.sqrt(128))
-        calls += 1
-        el = time.perf_counter() - t0
-        if el >= min_seconds or calls >= 200:
-            break
+    from oracle.cache import decode_layer, quantize_layer
+
+    def decode_rate(min_seconds):
+        t0 = time.perf_counter()
+        calls = 0
+        while True:
+            decode_layer(cache_np, q, lens, signs, rot, 1 / math.sqrt(128))
+            calls += 1
+            el = time.perf_counter() - t0
+            if el >= min_seconds or calls >= 200:
+                return calls, el
+
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return dict(value=round(bytes_per_call * calls / el / 1e9, 4), unit="GB/s", cores=int(threads), kind="oracle",
-                sample=f"{calls} full decode steps of the {WORKLOAD} layer (4 KV heads, 28 query heads, 32768 "
-                       f"tokens), float64, {el:.1f} s")
+    calls, el = decode_rate(decode_seconds)
+    res = dict(value=round(bytes_per_call * calls / el / 1e9, 4), unit="GB/s", cores=int(threads), kind="oracle",
+               sample=f"{calls} full decode steps of the {WORKLOAD} layer (4 KV heads, 28 query heads, 32768 "
+                      f"tokens), float64, {el:.1f} s")
+    with threadpool_limits(1):
+        c1, e1 = decode_rate(single_seconds)
+    res["single_thread"] = dict(value=round(bytes_per_call * c1 / e1 / 1e9, 4), unit="GB/s", cores=1,
+                                sample=f"{c1} decode steps, {e1:.1f} s")
+    if prefill is not None:
+        k, v, mod = prefill
+        t0 = time.perf_counter()
+        quantize_layer(k, v, mod, lens, signs, rot, k.shape[2])
+        eq = time.perf_counter() - t0
+        with threadpool_limits(1):
+            t0 = time.perf_counter()
+            quantize_layer(k[:, :1], v[:, :1], mod, lens, signs, rot, k.shape[2])
+            eq1 = time.perf_counter() - t0
+        res["quantize"] = dict(value=round(append_bytes / eq / 1e9, 4), unit="GB/s", cores=int(threads),
+                               sample=f"the whole prefill (32768 tokens, 4 KV heads) quantized once, fp32 order, "
+                                      f"{eq:.1f} s",
+                               single_thread=dict(value=round(append_bytes / k.shape[1] / eq1 / 1e9, 4), unit="GB/s",
+                                                  cores=1, sample=f"one KV head of the prefill, {eq1:.1f} s"))
+    res["host"] = dict(cpu_count=os.cpu_count(), affinity=len(os.sched_getaffinity(0)), blas_threads=int(threads),
+                       numpy=np.__version__)
+    return res
 
 
 def _scan_case(okvq, torch, name, B, lens, H, Hq, key_meta):
@@ -290,6 +321,40 @@ def key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
             "append_us": round(append_us, 3), "append_GBps": round(abytes / append_us / 1e3, 2),
             "append_frac": round(abytes / append_us / 1e3 / HBM_PEAK_GBPS, 4), "algorithmic_bytes": dbytes,
             "replicas": n_cache}
+
+
+def codec_split_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, signs, rot, stream, iters=12):
+    """The prefill's keys and values quantized separately by the stateless calls (each its own
+    launch of the codec, one role): okvq_quantize_keys (K rows in; codes, norms, window minimum and
+    step out: 306 B per token and KV head) and okvq_quantize_values (V rows and the modality map in;
+    codes and norms out: 290 B, with R_m read as fp32 rather than as prepared fragments)."""
+    B, H, Hq, N = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.seq_len
+    dev = k_in[0].device
+    c = okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev)
+    vw = c.views()
+    sdev, rdev = c.key_signs, c.v_rot
+    ntok = sum(int(L) for L in lens)
+
+    def timed(fn):
+        ev = []
+        for i in range(iters):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn(i % len(k_in))
+            e1.record(stream)
+            ev.append((e0, e1))
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in ev[2:]])) * 1e3
+
+    ku = timed(lambda i: okvq.okvq_quantize_keys(c.dims, k_in[i], N, lens, sdev, vw["k_codes"], vw["k_min"],
+                                                 vw["k_step"], vw["k_norm"], stream=stream))
+    vu = timed(lambda i: okvq.okvq_quantize_values(c.dims, v_in[i], m0, N, lens, rdev, 0, vw["v_codes"],
+                                                   vw["v_norm"], stream=stream))
+    kb = ntok * H * (256 + 32 + 2 + 16)
+    vb = ntok * H * (256 + 32 + 2) + ntok + 3 * 128 * 128 * 4
+    return {"keys_us": round(ku, 3), "keys_GBps": round(kb / ku / 1e3, 2), "keys_frac": round(kb / ku / 1e3 / HBM_PEAK_GBPS, 4),
+            "values_us": round(vu, 3), "values_GBps": round(vb / vu / 1e3, 2),
+            "values_frac": round(vb / vu / 1e3 / HBM_PEAK_GBPS, 4)}
 
 
 def dense_decode_bytes(B, H, Hq, lens):
@@ -795,6 +860,7 @@ def main():
                             "algorithmic_bytes": abytes},
         "cache_replicas": n_cache,
     }
+    line["codec_split"] = codec_split_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, signs, rot, stream)
     line["mxfp4"] = key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                          args.decode_iters, "mxfp4")
     line["turboquant"] = key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
@@ -808,7 +874,8 @@ def main():
     if not args.no_cpu_baseline:
         cache_np = {n: t.cpu().numpy() for n, t in caches[0].views().items()}
         line["cpu_baseline"] = cpu_baseline(cache_np, q.cpu().numpy(), np.asarray(lens), lay["signs"], lay["rot"],
-                                            dbytes)
+                                            dbytes, prefill=(lay["k"], lay["v"], lay["modality"]),
+                                            append_bytes=abytes)
     print(json.dumps(line), flush=True)
 
 
