@@ -73,6 +73,20 @@
  * "TurboQuant (K2/V2)"; with the single global value rotation R_m = H for every modality it is the
  * whole baseline). Not combined with the fp16 residual.
  *
+ * Bit-width ladder (dims.key_bits, dims.value_bits in 2..4; the K3/V2 row of Tab. 3 and the
+ * K2V2 / K3V3 / K4V4 columns of Tab. 5): keys of the method take the uniform 2^b-level grid of
+ * their window's range (step = (max - min) / (2^b - 1), code = clamp(rint(fl(fl(z - m16)
+ * fl(1 / step16))), 0, 2^b - 1)); TurboQuant keys and all values take the 2^b-level Lloyd-Max
+ * codebook (code = #{k : x > tau_k}). Layout: a token's 128 codes as a little-endian bit stream,
+ * channel c at bits [b c, b c + b) of the token's 16 b bytes:
+ *   k_codes  u8 [B][H][cap][16 key_bits]      v_codes  u8 [B][H][cap][16 value_bits]
+ *   k_norm, v_norm, k_min, k_step (fp16 metadata; absent for TurboQuant keys) and modality as above;
+ *   no k_stage, k_mx or residual rings. okvq_quantize_keys / okvq_quantize_keys_tq /
+ *   okvq_quantize_values fill it (values always in the exact fp32 order; the modality map is the
+ *   caller's copy), okvq_decode_attention reads it, okvq_append returns OKVQ_ERR_UNSUPPORTED.
+ *   Storage per token and KV head: 16 (key_bits + value_bits) + 4 bytes, + 16 with fp16 metadata
+ *   (TurboQuant K3/V2: 84 bytes = 2.625 bits per element).
+ *
  * fp16 residual of the captioning protocol (dims.residual = OKVQ_RESIDUAL_TOKENS, Sec. 3.1: keys
  * quantized every 128 tokens in groups of 32, values kept in a 128-token fp16 window before they
  * are quantized). Two more buffers hold the raw rows of the last 128 tokens:
@@ -138,8 +152,10 @@ typedef struct {
   int32_t head_dim;     /* must be 128                              */
   int32_t window;       /* key group size, must be 32 (Sec. 3.1)    */
   int32_t capacity;     /* token slots per sequence, multiple of 32 */
-  int32_t key_meta;     /* OKVQ_KEY_META_FP16 or OKVQ_KEY_META_MXFP4 */
+  int32_t key_meta;     /* OKVQ_KEY_META_*                          */
   int32_t residual;     /* 0 or OKVQ_RESIDUAL_TOKENS (fp16 window)  */
+  int32_t key_bits;     /* 0: the 2-bit layout above; 2..4: the bit-width ladder layout below */
+  int32_t value_bits;   /* 0, or 2..4 (both 0 or both set)          */
 } okvq_dims;
 
 typedef struct {               /* all pointers are device memory, laid out as above; k_min and
@@ -182,6 +198,11 @@ size_t okvq_buffer_bytes(const okvq_dims* dims, int32_t which_buffer);
  * thresholds of the Lloyd-Max quantizer of N(0, 1/128), computed by the library on the host.
  * levels: host float[4]; thresholds: host float[3]. */
 okvq_status okvq_codebook(float* levels, float* thresholds);
+
+/* The b-bit codebook (b = bits = 2, 3, 4) of the bit-width ladder: the 2^b levels and 2^b - 1
+ * thresholds of the Lloyd-Max quantizer of N(0, 1/128). levels: host float[2^b]; thresholds: host
+ * float[2^b - 1]. OKVQ_ERR_INVALID_ARGUMENT for another width or a NULL pointer. */
+okvq_status okvq_codebook_bits(int32_t bits, float* levels, float* thresholds);
 
 /* Quantize keys (Eq. 2 then Eq. 4) of a dense block into cache-layout buffers.
  *   k          device f16 [B][H][n_tokens][128]; token i of sequence b is valid if i < lens_host[b]

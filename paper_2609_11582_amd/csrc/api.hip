@@ -13,7 +13,7 @@ using namespace okvq;
 
 namespace {
 
-constexpr int32_t kVersion = 500;  // 0.5.0: dense fp16 decode baseline
+constexpr int32_t kVersion = 600;  // 0.6.0: bit-width ladder (b-bit keys and values)
 
 // ---- fixed Gaussian codebook (Sec. 2.1, Eq. 3): Lloyd-Max quantizer of N(0, 1), 4 levels ----
 double phi(double x) { return std::isinf(x) ? 0.0 : std::exp(-0.5 * x * x) / std::sqrt(2.0 * M_PI); }
@@ -23,41 +23,47 @@ double cdf(double x) {
 }
 
 struct Codebook {
-  float level[4];      // levels of N(0, 1/128), fp32
-  float thr[3];        // decision thresholds (midpoints), fp32
-  uint16_t level16[4]; // fp16 levels used by the decode kernel
+  int levels;           // 2^b
+  float level[16];      // levels of N(0, 1/128), fp32
+  float thr[15];        // decision thresholds (midpoints), fp32
+  uint16_t level16[16]; // fp16 levels used by the decode kernels
 };
 
-Codebook make_codebook() {
+Codebook make_codebook(int L) {
   // Lloyd iteration: thresholds are midpoints of neighbouring levels, levels are the centroids
   // of their cells (closed form for a Gaussian density).
-  double c[4] = {-1.5, -0.5, 0.5, 1.5};
+  double c[16];
+  for (int i = 0; i < L; ++i) c[i] = -(L - 1) / 2.0 + i;
   for (int it = 0; it < 100000; ++it) {
-    const double t[3] = {(c[0] + c[1]) / 2, (c[1] + c[2]) / 2, (c[2] + c[3]) / 2};
-    const double e[5] = {-INFINITY, t[0], t[1], t[2], INFINITY};
+    double e[17];
+    e[0] = -INFINITY;
+    e[L] = INFINITY;
+    for (int i = 0; i + 1 < L; ++i) e[i + 1] = (c[i] + c[i + 1]) / 2;
     double delta = 0.0;
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < L; ++i) {
       const double n = (phi(e[i]) - phi(e[i + 1])) / (cdf(e[i + 1]) - cdf(e[i]));
       delta = std::fmax(delta, std::fabs(n - c[i]));
       c[i] = n;
     }
     if (delta < 1e-15) break;
   }
-  double s[4];
-  for (int i = 0; i < 4; ++i) s[i] = (c[i] - c[3 - i]) / 2;  // exact symmetry of the density
+  double s[16];
+  for (int i = 0; i < L; ++i) s[i] = (c[i] - c[L - 1 - i]) / 2;  // exact symmetry of the density
   const double sc = 1.0 / std::sqrt(128.0);
-  Codebook cb;
-  for (int i = 0; i < 4; ++i) {
+  Codebook cb{};
+  cb.levels = L;
+  for (int i = 0; i < L; ++i) {
     cb.level[i] = (float)(s[i] * sc);
     cb.level16[i] = __builtin_bit_cast(uint16_t, (_Float16)(s[i] * sc));
   }
-  for (int i = 0; i < 3; ++i) cb.thr[i] = (float)(((s[i] + s[i + 1]) / 2) * sc);
+  for (int i = 0; i + 1 < L; ++i) cb.thr[i] = (float)(((s[i] + s[i + 1]) / 2) * sc);
   return cb;
 }
 
-const Codebook& codebook() {
-  static const Codebook cb = make_codebook();
-  return cb;
+// the b-bit codebook (b = 2, 3, 4)
+const Codebook& codebook(int bits = 2) {
+  static const Codebook cb2 = make_codebook(4), cb3 = make_codebook(8), cb4 = make_codebook(16);
+  return bits == 3 ? cb3 : bits == 4 ? cb4 : cb2;
 }
 
 Thresholds thresholds() {
@@ -79,8 +85,15 @@ okvq_status check_dims(const okvq_dims* d) {
     return OKVQ_ERR_INVALID_ARGUMENT;
   if (d->residual != 0 && d->residual != OKVQ_RESIDUAL_TOKENS) return OKVQ_ERR_INVALID_ARGUMENT;
   if (d->residual != 0 && d->key_meta == OKVQ_KEY_META_TURBOQUANT) return OKVQ_ERR_UNSUPPORTED;
+  // bit-width ladder: both widths 0 (the 2-bit layout) or both in 2..4 (the bit-stream layout)
+  if (d->key_bits != 0 || d->value_bits != 0) {
+    if (d->key_bits < 2 || d->key_bits > 4 || d->value_bits < 2 || d->value_bits > 4) return OKVQ_ERR_INVALID_ARGUMENT;
+    if (d->key_meta == OKVQ_KEY_META_MXFP4 || d->residual != 0) return OKVQ_ERR_UNSUPPORTED;
+  }
   return OKVQ_OK;
 }
+
+bool is_ladder(const okvq_dims* d) { return d->key_bits != 0; }
 
 bool is_mx(const okvq_dims* d) { return d->key_meta == OKVQ_KEY_META_MXFP4; }
 bool is_fp16(const okvq_dims* d) { return d->key_meta == OKVQ_KEY_META_FP16; }
@@ -92,10 +105,11 @@ okvq_status check_cache(const okvq_cache* c) {
   if (!c) return OKVQ_ERR_INVALID_ARGUMENT;
   okvq_status st = check_dims(&c->dims);
   if (st != OKVQ_OK) return st;
-  const void* ptrs[] = {c->k_codes, c->v_codes, c->k_norm,    c->v_norm, c->modality,
-                        c->k_stage, c->seq_lens, c->key_signs, c->v_rot,  c->v_rot16};
+  const void* ptrs[] = {c->k_codes, c->v_codes, c->k_norm,  c->v_norm, c->modality,
+                        c->seq_lens, c->key_signs, c->v_rot, c->v_rot16};
   for (const void* p : ptrs)
     if (!aligned16(p)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!is_ladder(&c->dims) && !aligned16(c->k_stage)) return OKVQ_ERR_INVALID_ARGUMENT;
   if (is_mx(&c->dims) && !aligned16(c->k_mx)) return OKVQ_ERR_INVALID_ARGUMENT;
   if (is_fp16(&c->dims) && (!aligned16(c->k_min) || !aligned16(c->k_step))) return OKVQ_ERR_INVALID_ARGUMENT;
   if (c->dims.residual && (!aligned16(c->k_res) || !aligned16(c->v_res))) return OKVQ_ERR_INVALID_ARGUMENT;
@@ -125,6 +139,8 @@ CacheView view(const okvq_cache* c) {
   v.residual = c->dims.residual;
   v.k_res = c->dims.residual ? c->k_res : nullptr;
   v.v_res = c->dims.residual ? c->v_res : nullptr;
+  v.key_bits = c->dims.key_bits;
+  v.value_bits = c->dims.value_bits;
   return v;
 }
 
@@ -203,6 +219,19 @@ const char* okvq_status_string(okvq_status s) {
 size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
   if (check_dims(d) != OKVQ_OK) return 0;
   const size_t B = d->batch, H = d->num_kv_heads, cap = d->capacity, D = d->head_dim, W = d->window;
+  if (is_ladder(d)) {  // bit-stream layout: no MXFP4 records, no key stage (no append), no rings
+    switch (which) {
+      case OKVQ_BUF_K_CODES: return B * H * cap * (D * d->key_bits / 8);
+      case OKVQ_BUF_V_CODES: return B * H * cap * (D * d->value_bits / 8);
+      case OKVQ_BUF_K_NORM:
+      case OKVQ_BUF_V_NORM: return B * H * cap * 2;
+      case OKVQ_BUF_K_MIN:
+      case OKVQ_BUF_K_STEP: return is_fp16(d) ? B * H * (cap / W) * D * 2 : 0;
+      case OKVQ_BUF_MODALITY: return B * cap;
+      case OKVQ_BUF_SEQ_LENS: return B * 4 + 4;
+      default: return 0;
+    }
+  }
   switch (which) {
     case OKVQ_BUF_K_CODES: return B * H * cap * (D / 4);
     case OKVQ_BUF_V_CODES: return B * H * cap * (D / 4);
@@ -223,8 +252,16 @@ size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
 okvq_status okvq_codebook(float* levels, float* thresholds_out) {
   if (!levels || !thresholds_out) return OKVQ_ERR_INVALID_ARGUMENT;
   const Codebook& cb = codebook();
-  std::memcpy(levels, cb.level, sizeof(cb.level));
-  std::memcpy(thresholds_out, cb.thr, sizeof(cb.thr));
+  std::memcpy(levels, cb.level, 4 * sizeof(float));
+  std::memcpy(thresholds_out, cb.thr, 3 * sizeof(float));
+  return OKVQ_OK;
+}
+
+okvq_status okvq_codebook_bits(int32_t bits, float* levels, float* thresholds_out) {
+  if (!levels || !thresholds_out || bits < 2 || bits > 4) return OKVQ_ERR_INVALID_ARGUMENT;
+  const Codebook& cb = codebook(bits);
+  std::memcpy(levels, cb.level, cb.levels * sizeof(float));
+  std::memcpy(thresholds_out, cb.thr, (cb.levels - 1) * sizeof(float));
   return OKVQ_OK;
 }
 
@@ -237,6 +274,32 @@ static okvq_status quantize_keys_impl(const okvq_dims* dims, const uint16_t* k, 
     if (lens_host[b] > dims->capacity) return OKVQ_ERR_CAPACITY;
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (is_ladder(dims)) {
+    const Codebook& cb = codebook(dims->key_bits);
+    for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
+      const int nb = std::min(kMaxLenArgs, dims->batch - b0);
+      LadderKeyArgs a{};
+      a.k = k;
+      a.n_rows = n_tokens;
+      a.H = dims->num_kv_heads;
+      a.cap = dims->capacity;
+      a.b0 = b0;
+      int max_len = 0;
+      for (int i = 0; i < nb; ++i) {
+        a.lens.lens[i] = lens_host[b0 + i];
+        max_len = std::max(max_len, lens_host[b0 + i]);
+      }
+      a.signs = key_signs;
+      a.k_codes = k_codes;
+      a.k_min = k_min;
+      a.k_step = k_step;
+      a.k_norm = k_norm;
+      for (int i = 0; i + 1 < cb.levels; ++i) a.tau[i] = cb.thr[i];
+      okvq_status st = hip_status(launch_ladder_keys(a, dims->key_bits, !is_fp16(dims), nb, max_len, s));
+      if (st != OKVQ_OK) return st;
+    }
+    return OKVQ_OK;
+  }
   for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
     const int nb = std::min(kMaxLenArgs, dims->batch - b0);
     CodecArgs a{};
@@ -312,6 +375,31 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
     if (lens_host[b] > dims->capacity) return OKVQ_ERR_CAPACITY;
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (is_ladder(dims)) {  // the exact fp32 order in both modes
+    const Codebook& cb = codebook(dims->value_bits);
+    for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
+      const int nb = std::min(kMaxLenArgs, dims->batch - b0);
+      LadderValueArgs a{};
+      a.v = v;
+      a.modality = modality;
+      a.n_rows = n_tokens;
+      a.H = dims->num_kv_heads;
+      a.cap = dims->capacity;
+      a.b0 = b0;
+      int max_len = 0;
+      for (int i = 0; i < nb; ++i) {
+        a.lens.lens[i] = lens_host[b0 + i];
+        max_len = std::max(max_len, lens_host[b0 + i]);
+      }
+      a.rot = v_rot;
+      a.v_codes = v_codes;
+      a.v_norm = v_norm;
+      for (int i = 0; i + 1 < cb.levels; ++i) a.tau[i] = cb.thr[i];
+      st = hip_status(launch_ladder_values(a, dims->value_bits, nb, max_len, s));
+      if (st != OKVQ_OK) return st;
+    }
+    return OKVQ_OK;
+  }
   const bool exact = (flags & OKVQ_VALUE_EXACT) != 0;
   for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
     const int nb = std::min(kMaxLenArgs, dims->batch - b0);
@@ -348,6 +436,7 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
                         uint32_t flags, void* stream) {
   okvq_status st = check_cache(cache);
   if (st != OKVQ_OK) return st;
+  if (is_ladder(&cache->dims)) return OKVQ_ERR_UNSUPPORTED;  // the ladder layout is filled by the stateless calls
   if (!lens_host || !n_new_host || n_max < 0 || (flags & ~(uint32_t)OKVQ_VALUE_EXACT)) return OKVQ_ERR_INVALID_ARGUMENT;
   if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(mod_new) || !aligned16(n_new_dev))
     return OKVQ_ERR_INVALID_ARGUMENT;
@@ -432,6 +521,7 @@ okvq_status okvq_prepare_rotation(const float* v_rot, uint16_t* v_rot16, void* s
 
 size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len) {
   if (check_dims(dims) != OKVQ_OK || max_seq_len < 0) return 0;
+  if (is_ladder(dims)) return ladder_workspace_bytes(dims->batch, dims->num_kv_heads, max_seq_len);
   return decode_workspace_bytes(dims->batch, dims->num_kv_heads, dims->num_q_heads, max_seq_len);
 }
 
@@ -449,13 +539,9 @@ static okvq_status decode_impl(const okvq_cache* cache, const int32_t* lens_host
     if (lens_host[b] > d.capacity) return OKVQ_ERR_CAPACITY;
     max_len = std::max(max_len, lens_host[b]);
   }
-  const size_t need = decode_workspace_bytes(d.batch, d.num_kv_heads, d.num_q_heads, max_len);
+  const size_t need = is_ladder(&d) ? ladder_workspace_bytes(d.batch, d.num_kv_heads, max_len)
+                                    : decode_workspace_bytes(d.batch, d.num_kv_heads, d.num_q_heads, max_len);
   if (!aligned16(workspace) || workspace_bytes < need) return OKVQ_ERR_WORKSPACE;
-  // with the fp16 residual the split-K launch covers the tokens below L - 128
-  const DecodePlan plan = plan_decode(d.batch, d.num_kv_heads, std::max(max_len - d.residual, 0));
-  const Codebook& cb = codebook();
-  const uint32_t cb01 = cb.level16[0] | ((uint32_t)cb.level16[1] << 16);
-  const uint32_t cb23 = cb.level16[2] | ((uint32_t)cb.level16[3] << 16);
   hipEvent_t ev[4];
   if (events) {
     for (int i = 0; i < 4; ++i) {
@@ -463,6 +549,38 @@ static okvq_status decode_impl(const okvq_cache* cache, const int32_t* lens_host
       ev[i] = static_cast<hipEvent_t>(events[i]);
     }
   }
+  if (is_ladder(&d)) {
+    LadderDecodeArgs a{};
+    a.k_codes = cache->k_codes;
+    a.v_codes = cache->v_codes;
+    a.k_norm = cache->k_norm;
+    a.v_norm = cache->v_norm;
+    a.k_min = is_fp16(&d) ? cache->k_min : nullptr;
+    a.k_step = is_fp16(&d) ? cache->k_step : nullptr;
+    a.modality = cache->modality;
+    a.seq_lens = cache->seq_lens;
+    a.signs = cache->key_signs;
+    a.q = q;
+    a.rot16t = cache->v_rot16;
+    a.ws = static_cast<float*>(workspace);
+    a.H = d.num_kv_heads;
+    a.Hq = d.num_q_heads;
+    a.G = d.num_q_heads / d.num_kv_heads;
+    a.cap = d.capacity;
+    a.qscale = sm_scale * 1.4426950408889634f * 0.08838834764831845f;
+    const Codebook& kc = codebook(d.key_bits);
+    const Codebook& vc = codebook(d.value_bits);
+    for (int i = 0; i < kc.levels; ++i) a.kcb16[i] = kc.level16[i];
+    for (int i = 0; i < vc.levels; ++i) a.vcb16[i] = vc.level16[i];
+    return hip_status(launch_ladder_decode(a, d.key_bits, d.value_bits, !is_fp16(&d), d.batch,
+                                           plan_ladder(d.batch, d.num_kv_heads, max_len), out,
+                                           static_cast<hipStream_t>(stream), events ? ev : nullptr));
+  }
+  // with the fp16 residual the split-K launch covers the tokens below L - 128
+  const DecodePlan plan = plan_decode(d.batch, d.num_kv_heads, std::max(max_len - d.residual, 0));
+  const Codebook& cb = codebook();
+  const uint32_t cb01 = cb.level16[0] | ((uint32_t)cb.level16[1] << 16);
+  const uint32_t cb23 = cb.level16[2] | ((uint32_t)cb.level16[3] << 16);
   return hip_status(launch_decode(view(cache), q, sm_scale, out, workspace, plan, static_cast<hipStream_t>(stream),
                                   cb01, cb23, max_len, events ? ev : nullptr));
 }

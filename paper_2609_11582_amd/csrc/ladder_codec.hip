@@ -1,0 +1,271 @@
+// Codecs of the bit-width ladder: b-bit keys and values, b = 2, 3, 4 (the K3/V2 row of Tab. 3 and
+// the K2V2 / K3V3 / K4V4 columns of Tab. 5), in the token-major bit-stream layout: a token's 128
+// codes form a little-endian bit stream, channel c at bits [b c, b c + b) of the token's 16 b bytes.
+//
+// Keys (one work-group of 128 threads per 128 tokens of a (sequence, KV head)): phase A, thread =
+// token, computes the direction in the key codec's bit-exact order (fp16 norm by the halving tree,
+// butterflies h = 1 .. 64, z = w fl(kappa / n16)); TurboQuant keys then take code = #{k : z_c >
+// tau_k} against the 2^b - 1 thresholds of the b-bit Gaussian codebook (Eq. 2, Eq. 3). The method's
+// keys (Eq. 4) go through an LDS tile: phase B, thread = channel, takes each window's minimum and
+// step (max - min) / (2^b - 1) in fp16 and the codes clamp(rint(fl(fl(z - m16) fl(1 / step16))), 0,
+// 2^b - 1); phase C, thread = token, packs its row.
+//
+// Values (one work-group of 128 threads, thread = output channel, per 32-token window): the
+// exact-mode order of the 2-bit codec -- y_c = sum_j fl(R_cj v_j) left to right in fp32, n16 by the
+// halving tree -- and code = #{k : y_c > fl(n16 tau_k)} against the 2^b - 1 thresholds; then a
+// thread per (token, 32 channels) packs b dwords.
+#include "key_quant.hpp"
+#include "launch.hpp"
+
+namespace okvq {
+namespace {
+
+constexpr int kTileTokens = 128;
+
+// OR the 32 codes of channels 32 part .. 32 part + 31 (one per byte of `codes`) into the b dwords
+// they occupy: bits b (c - 32 part) of the run starting at dword b part.
+template <int kBits>
+__device__ __forceinline__ void pack32(const uint32_t (&cw)[8], uint32_t (&w)[kBits]) {
+#pragma unroll
+  for (int i = 0; i < kBits; ++i) w[i] = 0u;
+#pragma unroll
+  for (int c = 0; c < 32; ++c) {
+    const uint32_t v = (cw[c >> 2] >> (8 * (c & 3))) & 0xffu;
+    const int bit = kBits * c, d = bit >> 5, sh = bit & 31;
+    w[d] |= v << sh;
+    if (sh + kBits > 32) w[d + 1] |= v >> (32 - sh);
+  }
+}
+
+template <int kBits>
+__device__ __forceinline__ void store_run(uint8_t* row, int part, const uint32_t (&w)[kBits]) {
+  uint32_t* p = reinterpret_cast<uint32_t*>(row) + kBits * part;
+#pragma unroll
+  for (int i = 0; i < kBits; ++i) p[i] = w[i];
+}
+
+template <int kBits, bool kTq>
+__global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
+  constexpr int kTop = (1 << kBits) - 1;
+  constexpr int kRowBytes = 16 * kBits;
+  __shared__ float zt[kTileTokens][kD + 1];                              // directions (method keys)
+  __shared__ __attribute__((aligned(16))) uint8_t ct[kTileTokens][kD];  // codes
+  const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz;
+  const int len = a.lens.lens[bz];
+  const int t0 = kTileTokens * blockIdx.x;
+  if (t0 >= len) return;  // uniform over the work-group
+  const int t = threadIdx.x, tok = t0 + t;
+  const bool valid = tok < len;
+  const int npad = (len + kW - 1) / kW * kW;  // slots of every window holding a valid token
+  const size_t seq = (size_t)b * a.H + h;
+
+  // ---- phase A (thread = token): the direction, in registers ----
+  uint32_t sw[32];
+  load_sign_words(a.signs, sw);
+  uint32_t raw[64];
+  if (valid) {
+    load_row_f16(a.k + (seq * a.n_rows + tok) * kD, raw);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 64; ++i) raw[i] = 0u;
+  }
+  float x[kD];
+  key_unpack(raw, sw, x);
+  const uint32_t n16 = key_norm(x);
+#pragma unroll
+  for (int hh = 1; hh < kD; hh <<= 1) {
+#pragma unroll
+    for (int j = 0; j < kD; ++j) {
+      if ((j & hh) == 0) {
+        const float p = x[j], q = x[j + hh];
+        x[j] = p + q;
+        x[j + hh] = p - q;
+      }
+    }
+  }
+  const float cinv = (n16 == 0) ? 0.0f : div_rn(kKappa, h2f(n16));
+#pragma unroll
+  for (int c = 0; c < kD; ++c) x[c] = x[c] * cinv;
+  if (tok < npad) a.k_norm[seq * a.cap + tok] = valid ? (uint16_t)n16 : (uint16_t)0;
+
+  if constexpr (kTq) {
+    // ---- TurboQuant: nearest level of the b-bit codebook, packed straight from registers ----
+    if (tok >= npad) return;
+    uint8_t* row = a.k_codes + (seq * a.cap + tok) * kRowBytes;
+#pragma unroll
+    for (int part = 0; part < 4; ++part) {
+      uint32_t cw[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) cw[i] = 0u;
+#pragma unroll
+      for (int c = 0; c < 32; ++c) {
+        const float z = x[32 * part + c];
+        uint32_t code = 0;
+#pragma unroll
+        for (int k = 0; k < kTop; ++k) code += (uint32_t)(z > a.tau[k]);
+        cw[c >> 2] |= (valid ? code : 0u) << (8 * (c & 3));
+      }
+      uint32_t w[kBits];
+      pack32<kBits>(cw, w);
+      store_run<kBits>(row, part, w);
+    }
+    return;
+  } else {
+#pragma unroll
+    for (int c = 0; c < kD; ++c) zt[t][c] = x[c];
+    __syncthreads();
+
+    // ---- phase B (thread = channel): window minimum and step, then the codes ----
+    const int c = t;
+    const size_t nwcap = a.cap / kW;
+    for (int w = 0; w < kTileTokens / kW; ++w) {
+      const int wt0 = t0 + kW * w;
+      if (wt0 >= len) break;  // uniform
+      const int nv = min(len - wt0, kW);
+      float lo = __builtin_inff(), hi = -__builtin_inff();
+      for (int i = 0; i < nv; ++i) {
+        const float v = zt[kW * w + i][c];
+        lo = fminf(lo, v);
+        hi = fmaxf(hi, v);
+      }
+      lo = lo + 0.0f;  // -0 -> +0
+      hi = hi + 0.0f;
+      const float step = div_rn(hi - lo, (float)kTop);
+      const uint32_t m16 = f2h(lo), s16 = f2h(step);
+      const size_t mi = (seq * nwcap + wt0 / kW) * kD + c;
+      a.k_min[mi] = (uint16_t)m16;
+      a.k_step[mi] = (uint16_t)s16;
+      const float m = h2f(m16), s = h2f(s16);
+      const float inv = (s != 0.0f) ? div_rn(1.0f, s) : 0.0f;
+      for (int i = 0; i < kW; ++i) {
+        uint32_t code = 0;
+        if (i < nv && s != 0.0f) {
+          const float tt = (zt[kW * w + i][c] - m) * inv;
+          code = (uint32_t)fminf(fmaxf(__builtin_rintf(tt), 0.0f), (float)kTop);
+        }
+        ct[kW * w + i][c] = (uint8_t)code;
+      }
+    }
+    __syncthreads();
+
+    // ---- phase C (thread = token): pack the row ----
+    if (tok >= npad) return;
+    uint8_t* row = a.k_codes + (seq * a.cap + tok) * kRowBytes;
+#pragma unroll
+    for (int part = 0; part < 4; ++part) {
+      uint32_t cw[8];
+      const uint4* src = reinterpret_cast<const uint4*>(&ct[t][32 * part]);
+      const uint4 u0 = src[0], u1 = src[1];
+      cw[0] = u0.x; cw[1] = u0.y; cw[2] = u0.z; cw[3] = u0.w;
+      cw[4] = u1.x; cw[5] = u1.y; cw[6] = u1.z; cw[7] = u1.w;
+      uint32_t w[kBits];
+      pack32<kBits>(cw, w);
+      store_run<kBits>(row, part, w);
+    }
+  }
+}
+
+__device__ __forceinline__ float tree_norm_lds(const float* xs) {  // xs: 128 floats (LDS)
+  float tt[64];
+#pragma unroll
+  for (int i = 0; i < 64; ++i) tt[i] = xs[i] * xs[i] + xs[i + 64] * xs[i + 64];
+#pragma unroll
+  for (int n = 32; n >= 1; n >>= 1) {
+#pragma unroll
+    for (int i = 0; i < n; ++i) tt[i] = tt[i] + tt[i + n];
+  }
+  return sqrt_rn(tt[0]);
+}
+
+template <int kBits>
+__global__ __launch_bounds__(128) void k_ladder_values(LadderValueArgs a) {
+  constexpr int kTop = (1 << kBits) - 1;
+  constexpr int kRowBytes = 16 * kBits;
+  __shared__ __attribute__((aligned(16))) float xs[kW][kD];
+  __shared__ float nrm[kW];
+  __shared__ int mods[kW];
+  __shared__ __attribute__((aligned(16))) uint8_t ct[kW][kD];
+  const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz;
+  const int len = a.lens.lens[bz];
+  const int t0 = kW * blockIdx.x;
+  if (t0 >= len) return;
+  const int c = threadIdx.x;
+  const size_t seq = (size_t)b * a.H + h;
+  for (int t = 0; t < kW; ++t) {
+    const int tok = t0 + t;
+    xs[t][c] = (tok < len) ? h2f(a.v[(seq * a.n_rows + tok) * kD + c]) : 0.0f;
+  }
+  if (c < kW) {
+    const int tok = t0 + c;
+    mods[c] = (tok < len) ? (int)a.modality[(size_t)b * a.n_rows + tok] : -1;
+  }
+  __syncthreads();
+  if (c < kW) {
+    const int tok = t0 + c;
+    const uint32_t n16 = (tok < len) ? norm_to_f16(tree_norm_lds(xs[c])) : 0u;
+    nrm[c] = h2f(n16);
+    if (tok < len) a.v_norm[seq * a.cap + tok] = (uint16_t)n16;
+  }
+  __syncthreads();
+  for (int t = 0; t < kW; ++t) {
+    const int m = mods[t];
+    uint32_t code = 0;
+    if (m >= 0 && m <= 2) {  // a valid token of a known modality (others keep code 0)
+      const float* r = a.rot + ((size_t)m * kD + c) * kD;
+      float acc = 0.0f;
+      for (int k = 0; k < kD; ++k) acc = acc + r[k] * xs[t][k];
+      const float nv = nrm[t];
+#pragma unroll
+      for (int k = 0; k < kTop; ++k) code += (uint32_t)(acc > nv * a.tau[k]);
+    }
+    ct[t][c] = (uint8_t)code;
+  }
+  __syncthreads();
+  // packing: thread = (token c / 4, channels 32 (c % 4) .. +31)
+  const int t = c >> 2, part = c & 3, tok = t0 + t;
+  if (tok >= len) return;
+  uint32_t cw[8];
+  const uint4* src = reinterpret_cast<const uint4*>(&ct[t][32 * part]);
+  const uint4 u0 = src[0], u1 = src[1];
+  cw[0] = u0.x; cw[1] = u0.y; cw[2] = u0.z; cw[3] = u0.w;
+  cw[4] = u1.x; cw[5] = u1.y; cw[6] = u1.z; cw[7] = u1.w;
+  uint32_t w[kBits];
+  pack32<kBits>(cw, w);
+  store_run<kBits>(a.v_codes + (seq * a.cap + tok) * kRowBytes, part, w);
+}
+
+template <int kBits>
+hipError_t keys_for_bits(const LadderKeyArgs& a, bool tq, dim3 grid, hipStream_t s) {
+  if (tq)
+    hipLaunchKernelGGL((k_ladder_keys<kBits, true>), grid, dim3(kTileTokens), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_ladder_keys<kBits, false>), grid, dim3(kTileTokens), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ladder_keys(const LadderKeyArgs& a, int bits, bool tq, int nb, int max_len, hipStream_t s) {
+  if (nb <= 0 || max_len <= 0) return hipSuccess;
+  const dim3 grid((max_len + kTileTokens - 1) / kTileTokens, a.H, nb);
+  switch (bits) {
+    case 2: return keys_for_bits<2>(a, tq, grid, s);
+    case 3: return keys_for_bits<3>(a, tq, grid, s);
+    case 4: return keys_for_bits<4>(a, tq, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_ladder_values(const LadderValueArgs& a, int bits, int nb, int max_len, hipStream_t s) {
+  if (nb <= 0 || max_len <= 0) return hipSuccess;
+  const dim3 grid((max_len + kW - 1) / kW, a.H, nb);
+  switch (bits) {
+    case 2: hipLaunchKernelGGL(k_ladder_values<2>, grid, dim3(128), 0, s, a); break;
+    case 3: hipLaunchKernelGGL(k_ladder_values<3>, grid, dim3(128), 0, s, a); break;
+    case 4: hipLaunchKernelGGL(k_ladder_values<4>, grid, dim3(128), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace okvq

@@ -101,6 +101,7 @@ struct CacheView {
   int residual;            // 0, or kResidual: the last tokens are read in fp16 from k_res / v_res
   const uint16_t* k_res;   // [B][H][128][128] fp16 rings (token i in row i % 128)
   const uint16_t* v_res;
+  int key_bits, value_bits;  // 0: the 2-bit layout above; 2..4: the bit-width ladder layout
 };
 
 // Split record of the split-K decode launches (read by the log-sum-exp merge): the running max
@@ -137,5 +138,57 @@ size_t dense_workspace_bytes(int B, int H, int max_len);
 hipError_t launch_decode_dense(const uint16_t* k, const uint16_t* v, const int32_t* seq_lens, const uint16_t* q, int B,
                                int H, int Hq, int cap, float sm_scale, float* out, void* ws, const DensePlan& plan,
                                hipStream_t s, hipEvent_t const* events);
+
+// ---- bit-width ladder: b-bit keys and values (b = 2, 3, 4) in the token-major bit-stream layout ----
+struct LadderKeyArgs {
+  const uint16_t* k;  // [B][H][n_rows][128] fp16
+  int n_rows, H, cap, b0;
+  LenArgs lens;
+  const int8_t* signs;
+  uint8_t* k_codes;   // [B][H][cap][16 b]
+  uint16_t* k_min;    // [B][H][cap/32][128] fp16 (method keys)
+  uint16_t* k_step;
+  uint16_t* k_norm;   // [B][H][cap]
+  float tau[15];      // TurboQuant keys: the 2^b - 1 thresholds (fp32, ascending)
+};
+struct LadderValueArgs {
+  const uint16_t* v;  // [B][H][n_rows][128] fp16
+  const uint8_t* modality;  // [B][n_rows]
+  int n_rows, H, cap, b0;
+  LenArgs lens;
+  const float* rot;   // [3][128][128] fp32
+  uint8_t* v_codes;   // [B][H][cap][16 b]
+  uint16_t* v_norm;
+  float tau[15];
+};
+hipError_t launch_ladder_keys(const LadderKeyArgs& a, int bits, bool tq, int nb, int max_len, hipStream_t s);
+hipError_t launch_ladder_values(const LadderValueArgs& a, int bits, int nb, int max_len, hipStream_t s);
+
+struct LadderDecodeArgs {
+  const uint8_t* k_codes;
+  const uint8_t* v_codes;
+  const uint16_t* k_norm;
+  const uint16_t* v_norm;
+  const uint16_t* k_min;   // null for TurboQuant keys
+  const uint16_t* k_step;
+  const uint8_t* modality;
+  const int32_t* seq_lens;
+  const int8_t* signs;
+  const uint16_t* q;
+  const uint16_t* rot16t;
+  float* ws;
+  int H, Hq, G, cap, tps, nsplit;
+  float qscale;            // sm_scale log2(e) / sqrt(128) (the butterflies are unnormalized)
+  uint16_t kcb16[16];      // fp16 levels of the key codebook (TurboQuant keys)
+  uint16_t vcb16[16];      // fp16 levels of the value codebook
+};
+struct LadderPlan {
+  int tokens_per_split;
+  int nsplit;
+};
+LadderPlan plan_ladder(int B, int H, int max_len);
+size_t ladder_workspace_bytes(int B, int H, int max_len);
+hipError_t launch_ladder_decode(const LadderDecodeArgs& a, int key_bits, int value_bits, bool tq, int B,
+                                const LadderPlan& plan, float* out, hipStream_t s, hipEvent_t const* events);
 
 }  // namespace okvq

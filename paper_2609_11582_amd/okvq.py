@@ -41,7 +41,8 @@ class OkvqError(RuntimeError):
 class Dims(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("window", ctypes.c_int32), ("capacity", ctypes.c_int32),
-                ("key_meta", ctypes.c_int32), ("residual", ctypes.c_int32)]
+                ("key_meta", ctypes.c_int32), ("residual", ctypes.c_int32), ("key_bits", ctypes.c_int32),
+                ("value_bits", ctypes.c_int32)]
 
 
 class CacheStruct(ctypes.Structure):
@@ -68,6 +69,8 @@ def lib() -> ctypes.CDLL:
         L.okvq_buffer_bytes.argtypes = [P(Dims), i32]
         L.okvq_codebook.restype = i32
         L.okvq_codebook.argtypes = [P(ctypes.c_float), P(ctypes.c_float)]
+        L.okvq_codebook_bits.restype = i32
+        L.okvq_codebook_bits.argtypes = [i32, P(ctypes.c_float), P(ctypes.c_float)]
         L.okvq_quantize_keys.restype = i32
         L.okvq_quantize_keys.argtypes = [P(Dims), vp, i32, P(i32), vp, vp, vp, vp, vp, vp]
         L.okvq_quantize_keys_mx.restype = i32
@@ -142,8 +145,10 @@ def _stream(stream) -> Optional[int]:
 
 
 def make_dims(batch, num_kv_heads, num_q_heads, capacity, head_dim=128, window=32, key_meta="fp16",
-              residual=0) -> Dims:
-    return Dims(batch, num_kv_heads, num_q_heads, head_dim, window, capacity, KEY_META[key_meta], int(residual))
+              residual=0, key_bits=0, value_bits=0) -> Dims:
+    """key_bits = value_bits = 0: the 2-bit layout; 2..4 each: the bit-width ladder layout."""
+    return Dims(batch, num_kv_heads, num_q_heads, head_dim, window, capacity, KEY_META[key_meta], int(residual),
+                int(key_bits), int(value_bits))
 
 
 def okvq_version() -> int:
@@ -159,6 +164,15 @@ def okvq_codebook():
     th = (ctypes.c_float * 3)()
     _check(lib().okvq_codebook(lv, th), "okvq_codebook")
     return list(lv), list(th)
+
+
+def okvq_codebook_bits(bits: int):
+    """(levels [2^b], thresholds [2^b - 1]) of the b-bit codebook."""
+    n = 1 << int(bits)
+    lv = (ctypes.c_float * 16)()
+    th = (ctypes.c_float * 15)()
+    _check(lib().okvq_codebook_bits(int(bits), lv, th), "okvq_codebook_bits")
+    return list(lv)[:n], list(th)[:n - 1]
 
 
 def okvq_quantize_keys(dims, k, n_tokens, lens, key_signs, k_codes, k_min, k_step, k_norm, stream=None,
@@ -397,13 +411,17 @@ class KVCache:
     with the layer's key signs, value rotations and the decode's inverse-rotation table.
     key_meta "fp16" keeps the key window minimum and step in k_min / k_step, "mxfp4" in k_mx;
     "turboquant" stores TurboQuant keys (no window metadata, the paper's baseline).
-    residual=RESIDUAL_TOKENS adds the fp16 rings of the captioning protocol (k_res, v_res)."""
+    residual=RESIDUAL_TOKENS adds the fp16 rings of the captioning protocol (k_res, v_res).
+    key_bits, value_bits in 2..4 select the bit-width ladder layout (token-major bit streams; filled
+    by the stateless codec calls, no append)."""
 
     def __init__(self, batch, num_kv_heads, num_q_heads, capacity, key_signs: torch.Tensor, v_rot: torch.Tensor,
-                 device="cuda", key_meta="fp16", residual=0):
+                 device="cuda", key_meta="fp16", residual=0, key_bits=0, value_bits=0):
         self.key_meta = key_meta
         self.residual = int(residual)
-        self.dims = make_dims(batch, num_kv_heads, num_q_heads, capacity, key_meta=key_meta, residual=residual)
+        self.key_bits, self.value_bits = int(key_bits), int(value_bits)
+        self.dims = make_dims(batch, num_kv_heads, num_q_heads, capacity, key_meta=key_meta, residual=residual,
+                              key_bits=key_bits, value_bits=value_bits)
         self.key_signs = key_signs.to(device=device, dtype=torch.int8).contiguous()
         self.v_rot = v_rot.to(device=device, dtype=torch.float32).contiguous()
         self.v_rot16 = torch.empty(ROTATION_TABLE_BYTES // 2, dtype=torch.float16, device=device)
@@ -412,6 +430,8 @@ class KVCache:
         unused = {"fp16": ("k_mx",), "mxfp4": ("k_min", "k_step"), "turboquant": ("k_min", "k_step", "k_mx")}[key_meta]
         if not self.residual:
             unused += ("k_res", "v_res")
+        if self.key_bits:
+            unused += ("k_stage",)
         for i, name in enumerate(BUFFERS):
             nbytes = okvq_buffer_bytes(self.dims, i)
             if (nbytes == 0) != (name in unused):
@@ -435,10 +455,14 @@ class KVCache:
         d = self.dims
         B, H, cap = d.batch, d.num_kv_heads, d.capacity
         b = self.buffers
-        v = dict(k_codes=b["k_codes"].view(B, H, cap, 32), v_codes=b["v_codes"].view(B, H, cap // 32, 1024),
-                 k_norm=b["k_norm"].view(B, H, cap), v_norm=b["v_norm"].view(B, H, cap),
-                 modality=b["modality"].view(B, cap), k_stage=b["k_stage"].view(B, H, 32, 128),
-                 seq_lens=b["seq_lens"][:B])
+        if self.key_bits:  # bit-width ladder: token-major bit streams
+            v = dict(k_codes=b["k_codes"].view(B, H, cap, 16 * self.key_bits),
+                     v_codes=b["v_codes"].view(B, H, cap, 16 * self.value_bits))
+        else:
+            v = dict(k_codes=b["k_codes"].view(B, H, cap, 32), v_codes=b["v_codes"].view(B, H, cap // 32, 1024),
+                     k_stage=b["k_stage"].view(B, H, 32, 128))
+        v.update(k_norm=b["k_norm"].view(B, H, cap), v_norm=b["v_norm"].view(B, H, cap),
+                 modality=b["modality"].view(B, cap), seq_lens=b["seq_lens"][:B])
         if self.key_meta == "fp16":
             v.update(k_min=b["k_min"].view(B, H, cap // 32, 128), k_step=b["k_step"].view(B, H, cap // 32, 128))
         elif self.key_meta == "mxfp4":

@@ -189,3 +189,28 @@ def check_window(arrays, k16, v16, modality, signs, rot, b, h, w, length):
     if n < 32:
         assert not np.any(arrays["k_codes"][b, h, a + n:a + 32])
         assert not np.any(unpack_values(arrays["v_codes"][b, h, w:w + 1])[n:])
+
+
+def ladder_cache(k, v, modality, lens, signs, rot, capacity, num_q_heads, key_bits, value_bits, key_meta="fp16"):
+    """A bit-width-ladder cache filled by the stateless codec calls (keys, values), with the
+    modality map and the device lengths copied in."""
+    B, H, N, D = k.shape
+    cache = okvq.KVCache(B, H, num_q_heads, capacity, torch.from_numpy(np.ascontiguousarray(signs)),
+                         torch.from_numpy(np.ascontiguousarray(rot, np.float32)), key_meta=key_meta,
+                         key_bits=key_bits, value_bits=value_bits)
+    vw = cache.views()
+    kd, vd = f16dev(k), f16dev(v)
+    md = dev(np.ascontiguousarray(modality, np.uint8))
+    if key_meta == "fp16":
+        okvq.okvq_quantize_keys(cache.dims, kd, N, list(lens), cache.key_signs, vw["k_codes"], vw["k_min"],
+                                vw["k_step"], vw["k_norm"])
+    else:
+        okvq.okvq_quantize_keys_tq(cache.dims, kd, N, list(lens), cache.key_signs, vw["k_codes"], vw["k_norm"])
+    okvq.okvq_quantize_values(cache.dims, vd, md, N, list(lens), cache.v_rot, 0, vw["v_codes"], vw["v_norm"])
+    mod = np.zeros((B, capacity), np.uint8)
+    for b in range(B):
+        mod[b, :lens[b]] = modality[b, :lens[b]]
+    vw["modality"].copy_(dev(mod))
+    vw["seq_lens"].copy_(torch.tensor(list(lens), dtype=torch.int32))
+    torch.cuda.synchronize()
+    return cache

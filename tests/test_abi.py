@@ -331,3 +331,53 @@ def test_dense_decode_validation():
     bad_events = (ctypes.c_void_p * 4)(4096, 4096, 0, 4096)
     assert L.okvq_decode_attention_dense(ctypes.byref(d), fake, fake, fake, lens, fake, sm, fake, fake, big, None,
                                          bad_events) == -1
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_ladder_codebooks_match_oracle_bit_for_bit(bits):
+    okvq = _lib()
+    levels, thr = okvq.okvq_codebook_bits(bits)
+    cb, tau = codebook(128, bits)
+    np.testing.assert_array_equal(np.array(levels, np.float32), cb.astype(np.float32))
+    np.testing.assert_array_equal(np.array(thr, np.float32), tau.astype(np.float32))
+
+
+def test_ladder_buffers_and_validation():
+    """The bit-width ladder layout: 16 b bytes of codes per token row, Tab. 3's 2.625 bits for
+    TurboQuant K3/V2; invalid widths and unsupported combinations are rejected before a launch."""
+    from oracle.ladder import bytes_per_token_head
+    okvq = _lib()
+    L = okvq.lib()
+    for kb, vb, meta in ((3, 2, "turboquant"), (3, 3, "fp16"), (4, 4, "fp16"), (2, 4, "turboquant")):
+        d = okvq.make_dims(2, 4, 28, 4096, key_meta=meta, key_bits=kb, value_bits=vb)
+        per = [okvq.okvq_buffer_bytes(d, i) for i in range(12)]
+        assert per[0] == 2 * 4 * 4096 * 16 * kb and per[1] == 2 * 4 * 4096 * 16 * vb
+        assert per[7] == 0 and per[9] == 0 and per[10] == 0 and per[11] == 0   # no stage, MXFP4 or rings
+        total = sum(per[i] for i in (0, 1, 2, 3, 4, 5))
+        assert total == 2 * 4 * 4096 * bytes_per_token_head(kb, vb, meta)
+        assert okvq.okvq_decode_workspace_bytes(d, 4096) > 0
+    tq32 = okvq.make_dims(1, 1, 4, 1024, key_meta="turboquant", key_bits=3, value_bits=2)
+    assert sum(okvq.okvq_buffer_bytes(tq32, i) for i in range(4)) * 8 / (1024 * 256) == 2.625
+    bad = [okvq.make_dims(2, 2, 8, 64, key_bits=3), okvq.make_dims(2, 2, 8, 64, key_bits=5, value_bits=2),
+           okvq.make_dims(2, 2, 8, 64, key_bits=1, value_bits=2)]
+    for d in bad:
+        assert okvq.okvq_buffer_bytes(d, 0) == 0
+    fake = ctypes.c_void_p(4096)
+    lens = (ctypes.c_int32 * 2)(10, 10)
+    assert L.okvq_quantize_keys(ctypes.byref(bad[0]), fake, 10, lens, fake, fake, fake, fake, fake, None) == -1
+    mx = okvq.make_dims(2, 2, 8, 64, key_meta="mxfp4", key_bits=3, value_bits=3)
+    assert L.okvq_quantize_keys_mx(ctypes.byref(mx), fake, 10, lens, fake, fake, fake, fake, None) == -2
+    res = okvq.make_dims(2, 2, 8, 64, residual=128, key_bits=3, value_bits=3)
+    assert L.okvq_quantize_keys(ctypes.byref(res), fake, 10, lens, fake, fake, fake, fake, fake, None) == -2
+    # a ladder cache cannot be appended to; decode checks its own workspace size
+    d = okvq.make_dims(2, 2, 8, 64, key_bits=4, value_bits=4)
+    cache = okvq.CacheStruct(d, *([4096] * 7), 0, 4096, 4096, 4096, 4096, 0, 0, 0)
+    n_new = (ctypes.c_int32 * 2)(4, 0)
+    lens0 = (ctypes.c_int32 * 2)(0, 0)
+    assert L.okvq_append(ctypes.byref(cache), lens0, fake, fake, fake, n_new, fake, 4, 0, None) == -2
+    q_lens = (ctypes.c_int32 * 2)(64, 64)
+    need = okvq.okvq_decode_workspace_bytes(d, 64)
+    assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, need - 1,
+                                   None) == -4
+    assert okvq.okvq_codebook_bits(3)[0][0] < 0 and len(okvq.okvq_codebook_bits(4)[1]) == 15
+    assert L.okvq_codebook_bits(5, (ctypes.c_float * 16)(), (ctypes.c_float * 15)()) == -1

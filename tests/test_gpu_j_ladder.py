@@ -1,0 +1,123 @@
+"""GPU parity of the bit-width ladder (b-bit keys and values, b = 2, 3, 4; Tab. 3 K3/V2, Tab. 5
+K2V2 / K3V3 / K4V4) against oracle.ladder: key codes, window metadata and norms bit-exact (the
+method's keys and TurboQuant keys, every width, ragged and degenerate rows), value codes and norms
+bit-exact (exact fp32 order), and decode within 2e-3 of the output norm -- over the GPU-written
+cache and end to end against the oracle-written one -- for several width pairs, ragged GQA 7 with
+an empty sequence, and the benchmark layer (4 KV heads, 28 query heads, 32768 tokens)."""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle.ladder import decode_layer_bits, quantize_layer_bits
+from synth import gen_layer, gen_queries, workload
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-3
+SM = 1 / math.sqrt(128)
+
+
+def _announce(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+def _arrays(cache):
+    return {n: t.cpu().numpy() for n, t in cache.views().items() if n != "seq_lens"}
+
+
+def _same(a, b, name):
+    if a.dtype == np.float16:
+        a, b = a.view(np.uint16), b.view(np.uint16)
+    mism = np.argwhere(a != b)
+    assert len(mism) == 0, f"{name}: {len(mism)} mismatches, first at {mism[:5].tolist()}"
+
+
+@pytest.mark.parametrize("meta", ["fp16", "turboquant"])
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_ladder_codes_bit_exact(bits, meta):
+    import gpu_helpers as gh
+    lens = [1000, 37, 64, 1, 0, 95]
+    wl = workload("omni7b_32k")
+    lay = gen_layer(wl, 5, lengths=np.asarray(lens, np.int32), n_tokens=max(lens))
+    k, v = lay["k"][:, :2].copy(), lay["v"][:, :2].copy()
+    k[0, 0, 5] = 0                       # zero-norm token
+    k[2, 0, :32, :] = np.float16(60000)  # saturated norm, zero-range window
+    k[3, 1, 0, 7] = np.float16(-0.0)
+    v[0, 1, 9] = 0
+    cap = 1024
+    _announce(f"ladder codes K{bits}V{bits} {meta} lens={lens}")
+    cache = gh.ladder_cache(k, v, lay["modality"], lens, lay["signs"], lay["rot"], cap, 14, bits, bits, meta)
+    got = _arrays(cache)
+    ref = quantize_layer_bits(k, v, lay["modality"], lens, lay["signs"], lay["rot"], cap, bits, bits, meta)
+    for name in ref:
+        _same(got[name], ref[name], name)
+
+
+CASES = [(2, 2, "fp16"), (3, 3, "fp16"), (4, 4, "fp16"), (3, 2, "turboquant"), (4, 4, "turboquant"),
+         (2, 4, "fp16"), (4, 3, "turboquant")]
+
+
+@pytest.mark.parametrize("kb,vb,meta", CASES, ids=[f"K{a}V{b}_{m}" for a, b, m in CASES])
+def test_ladder_decode_ragged_gqa7(kb, vb, meta):
+    import gpu_helpers as gh
+    lens = [1000, 517, 33, 1, 0, 2049, 300]
+    wl = workload("omni7b_32k")
+    lay = gen_layer(wl, 3, lengths=np.asarray(lens, np.int32), n_tokens=max(lens))
+    k, v = lay["k"][:, :2].copy(), lay["v"][:, :2].copy()
+    q = gen_queries(wl.wid, 3, len(lens), 14)
+    cap = -(-max(lens) // 32) * 32
+    _announce(f"ladder decode K{kb}V{vb} {meta} lens={lens}")
+    cache = gh.ladder_cache(k, v, lay["modality"], lens, lay["signs"], lay["rot"], cap, 14, kb, vb, meta)
+    out = gh.decode(cache, q, lens)
+    arrays = _arrays(cache)
+    ref = decode_layer_bits(arrays, q, lens, lay["signs"], lay["rot"], SM, kb, vb)
+    assert np.all(out[4] == 0)
+    live = [b for b, L in enumerate(lens) if L > 0]
+    r = gh.attention_close(out[live], ref[live])
+    print(f"K{kb}V{vb} {meta}: worst err / norm = {r:.2e}", flush=True)
+    assert r <= TOL
+    # the codecs are bit-exact, so the oracle-written cache is the same cache
+    oc = quantize_layer_bits(k, v, lay["modality"], lens, lay["signs"], lay["rot"], cap, kb, vb, meta)
+    for name in oc:
+        _same(arrays[name], oc[name], name)
+
+
+@pytest.mark.parametrize("kb,vb,meta", [(3, 3, "fp16"), (4, 2, "turboquant")], ids=["K3V3_fp16", "K4V2_tq"])
+def test_ladder_decode_several_windows_per_wave(kb, vb, meta):
+    """Lengths long enough that every wave of a split takes several windows (GQA 8)."""
+    import gpu_helpers as gh
+    lens = [20000, 7777]
+    wl = workload("omni3b_b4_64k_stream")
+    lay = gen_layer(wl, 1, lengths=np.asarray(lens, np.int32), n_tokens=max(lens))
+    q = gen_queries(wl.wid, 1, 2, 16)
+    cap = -(-max(lens) // 32) * 32
+    _announce(f"ladder decode K{kb}V{vb} {meta} lens={lens}")
+    cache = gh.ladder_cache(lay["k"], lay["v"], lay["modality"], lens, lay["signs"], lay["rot"], cap, 16, kb, vb, meta)
+    out = gh.decode(cache, q, lens)
+    ref = decode_layer_bits(_arrays(cache), q, lens, lay["signs"], lay["rot"], SM, kb, vb)
+    r = gh.attention_close(out, ref)
+    print(f"K{kb}V{vb} {meta} long: worst err / norm = {r:.2e}", flush=True)
+    assert r <= TOL
+
+
+@pytest.mark.parametrize("kb,vb,meta", [(4, 4, "fp16"), (3, 2, "turboquant")], ids=["K4V4_fp16", "K3V2_tq"])
+def test_ladder_decode_full_size(kb, vb, meta):
+    """The benchmark layer: every query head of two KV heads against the oracle."""
+    import gpu_helpers as gh
+    wl = workload("omni7b_32k")
+    lay = gen_layer(wl, 0)
+    lens = [int(x) for x in lay["lens"]]
+    q = gen_queries(wl.wid, 0, 1, 28)
+    _announce(f"ladder decode omni7b_32k K{kb}V{vb} {meta}")
+    cache = gh.ladder_cache(lay["k"], lay["v"], lay["modality"], lens, lay["signs"], lay["rot"], wl.capacity, 28, kb,
+                            vb, meta)
+    out = gh.decode(cache, q, lens)
+    arrays = _arrays(cache)
+    sub = {n: (a[:, [0, 3]] if a.ndim >= 3 and n != "modality" else a) for n, a in arrays.items()}
+    ref = decode_layer_bits(sub, q[:, list(range(0, 7)) + list(range(21, 28))], lens, lay["signs"], lay["rot"], SM,
+                            kb, vb)
+    rows = list(range(0, 7)) + list(range(21, 28))
+    r = gh.attention_close(out[:, rows], ref)
+    print(f"full size K{kb}V{vb} {meta}: worst err / norm = {r:.2e}", flush=True)
+    assert r <= TOL
