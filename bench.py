@@ -31,6 +31,8 @@ Reported (one JSON line):
                   rotation R_m = H: the K2/V2 baseline's append and decode
   residual        the same workload in the captioning protocol (fp16 rings of the last 128 keys and
                   values): prefill and one-token append, decode, split-K and merge-with-tail times
+  ladder          the same layer at other bit widths (K2V2 .. K4V4, TurboQuant K3V2 / K4V4, Tab. 3 and
+                  Tab. 5) in the bit-stream layout: stateless key and value quantization, decode
   omni30b_48layer the 30B-like workload with all 48 layers' caches resident (131072 tokens, 4 KV heads,
                   32 query heads): one decode step per layer over the packed caches, over packed
                   caches with the single global value rotation, and with the dense fp16 baseline
@@ -356,6 +358,92 @@ def codec_split_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, signs, ro
     return {"keys_us": round(ku, 3), "keys_GBps": round(kb / ku / 1e3, 2), "keys_frac": round(kb / ku / 1e3 / HBM_PEAK_GBPS, 4),
             "values_us": round(vu, 3), "values_GBps": round(vb / vu / 1e3, 2),
             "values_frac": round(vb / vu / 1e3 / HBM_PEAK_GBPS, 4)}
+
+
+LADDER_CASES = ((2, 2, "fp16"), (3, 3, "fp16"), (4, 4, "fp16"), (3, 2, "turboquant"), (4, 4, "turboquant"))
+
+
+def ladder_bytes_per_token_head(kb, vb, meta):
+    return 16 * kb + 16 * vb + 4 + (16 if meta == "fp16" else 0)
+
+
+def ladder_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, q, signs, rot, stream, decode_iters):
+    """The benchmark layer at other bit widths (the bit-width ladder, token-major bit-stream layout):
+    the stateless key and value codecs over the prefill, then decode over >= 1 GB of cold replicas,
+    for the method's keys (fp16 window metadata) and TurboQuant keys."""
+    B, H, Hq, N = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.seq_len
+    dev = q.device
+    sm = 1 / math.sqrt(128)
+    ntok = sum(int(L) for L in lens)
+    res = {}
+    for kb, vb, meta in LADDER_CASES:
+        base = okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev, key_meta=meta, key_bits=kb, value_bits=vb)
+        vw = base.views()
+        ev = []
+        for i in range(8):
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            e0.record(stream)
+            if meta == "fp16":
+                okvq.okvq_quantize_keys(base.dims, k_in[i % len(k_in)], N, lens, base.key_signs, vw["k_codes"],
+                                        vw["k_min"], vw["k_step"], vw["k_norm"], stream=stream)
+            else:
+                okvq.okvq_quantize_keys_tq(base.dims, k_in[i % len(k_in)], N, lens, base.key_signs, vw["k_codes"],
+                                           vw["k_norm"], stream=stream)
+            e1.record(stream)
+            okvq.okvq_quantize_values(base.dims, v_in[i % len(v_in)], m0, N, lens, base.v_rot, 0, vw["v_codes"],
+                                      vw["v_norm"], stream=stream)
+            e2.record(stream)
+            ev.append((e0, e1, e2))
+        vw["modality"].copy_(m0)
+        vw["seq_lens"].copy_(torch.tensor(lens, dtype=torch.int32))
+        torch.cuda.synchronize()
+        keys_us = float(np.mean([a.elapsed_time(b) for a, b, _ in ev[2:]])) * 1e3
+        vals_us = float(np.mean([b.elapsed_time(c) for _, b, c in ev[2:]])) * 1e3
+        per_cache = sum(okvq.okvq_buffer_bytes(base.dims, i) for i in range(12))
+        n_cache = max(16, int(math.ceil(1.05e9 / per_cache)))
+        caches = [base] + [okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev, key_meta=meta, key_bits=kb,
+                                        value_bits=vb) for _ in range(n_cache - 1)]
+        for c in caches[1:]:
+            for name in c.buffers:
+                c.buffers[name].copy_(base.buffers[name])
+        ws = okvq.decode_workspace(base.dims, max(lens), device=dev)
+        out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+        reps = []
+        for rep in range(5):
+            for i in range(10):
+                okvq.okvq_decode_attention(caches[i % n_cache], lens, q, sm, out, ws, stream=stream)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for i in range(decode_iters):
+                okvq.okvq_decode_attention(caches[(i * 7 + rep) % n_cache], lens, q, sm, out, ws, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            reps.append(e0.elapsed_time(e1) * 1e3 / decode_iters)
+        decode_us = float(np.median(reps))
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(decode_iters)]
+        for e4 in evs:
+            for e in e4:
+                e.record(stream)
+        torch.cuda.synchronize()
+        for i in range(decode_iters):
+            okvq.okvq_decode_attention_timed(caches[(i * 7 + 3) % n_cache], lens, q, sm, out, ws, evs[i], stream=stream)
+        torch.cuda.synchronize()
+        split_us = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) * 1e3
+        bpt = ladder_bytes_per_token_head(kb, vb, meta)
+        dbytes = ntok * H * bpt + ntok + B * Hq * 128 * 6 + 3 * 128 * 128 * 2
+        sbytes = dbytes - B * Hq * 128 * 4
+        kbytes = ntok * H * (256 + 16 * kb + 2 + (16 if meta == "fp16" else 0))
+        vbytes = ntok * H * (256 + 16 * vb + 2) + ntok + 3 * 128 * 128 * 4
+        res[f"K{kb}V{vb}_{meta}"] = {
+            "bits_per_element": round(bpt * 8 / 256, 4), "bytes_per_token_head": bpt,
+            "quantize_keys_us": round(keys_us, 2), "quantize_keys_GBps": round(kbytes / keys_us / 1e3, 1),
+            "quantize_values_us": round(vals_us, 2), "quantize_values_GBps": round(vbytes / vals_us / 1e3, 1),
+            "decode_us": round(decode_us, 3), "decode_GBps": round(dbytes / decode_us / 1e3, 1),
+            "k_ladder_decode_us": round(split_us, 3), "k_ladder_decode_frac": round(sbytes / split_us / 1e3 / HBM_PEAK_GBPS, 4),
+            "replicas": n_cache}
+        del caches, base
+        torch.cuda.empty_cache()
+    return res
 
 
 def dense_decode_bytes(B, H, Hq, lens):
@@ -867,6 +955,8 @@ def main():
     line["turboquant"] = key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                               args.decode_iters, "turboquant", signs,
                                               torch.from_numpy(sylvester_hadamard(lay["signs"])).repeat(3, 1, 1))
+    line["ladder"] = ladder_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, q, signs, rot, stream,
+                                        args.decode_iters)
     line["calibration"] = calibration_measurement(okvq, torch, np, wl, dev)
     if not args.no_layers48:
         line["omni30b_48layer"] = layers48_measurement(okvq, torch, np, dev, stream)

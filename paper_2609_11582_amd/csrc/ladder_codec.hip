@@ -12,8 +12,9 @@
 //
 // Values (one work-group of 128 threads, thread = output channel, per 32-token window): the
 // exact-mode order of the 2-bit codec -- y_c = sum_j fl(R_cj v_j) left to right in fp32, n16 by the
-// halving tree -- and code = #{k : y_c > fl(n16 tau_k)} against the 2^b - 1 thresholds; then a
-// thread per (token, 32 channels) packs b dwords.
+// halving tree -- and code = #{k : y_c > fl(n16 tau_k)} against the 2^b - 1 thresholds. A thread
+// holds its row of R_m in registers for each modality present in the window (R is read once per
+// window, not once per token); then a thread per (token, 32 channels) packs b dwords.
 #include "key_quant.hpp"
 #include "launch.hpp"
 
@@ -207,18 +208,41 @@ __global__ __launch_bounds__(128) void k_ladder_values(LadderValueArgs a) {
     if (tok < len) a.v_norm[seq * a.cap + tok] = (uint16_t)n16;
   }
   __syncthreads();
-  for (int t = 0; t < kW; ++t) {
-    const int m = mods[t];
-    uint32_t code = 0;
-    if (m >= 0 && m <= 2) {  // a valid token of a known modality (others keep code 0)
-      const float* r = a.rot + ((size_t)m * kD + c) * kD;
+  // codes default to 0 (padded or out-of-contract tokens); then, per modality present in the window,
+  // this thread's row c of R_m in registers against every token of that modality
+  for (int t = 0; t < kW; ++t) ct[t][c] = 0;
+  for (int m = 0; m < 3; ++m) {
+    bool any = false;
+    for (int t = 0; t < kW; ++t) any |= mods[t] == m;
+    if (!any) continue;  // uniform over the work-group
+    float rr[kD];
+    const float4* rp = reinterpret_cast<const float4*>(a.rot + ((size_t)m * kD + c) * kD);
+#pragma unroll
+    for (int k4 = 0; k4 < kD / 4; ++k4) {
+      const float4 f = rp[k4];
+      rr[4 * k4] = f.x;
+      rr[4 * k4 + 1] = f.y;
+      rr[4 * k4 + 2] = f.z;
+      rr[4 * k4 + 3] = f.w;
+    }
+    for (int t = 0; t < kW; ++t) {
+      if (mods[t] != m) continue;
+      const float4* xr = reinterpret_cast<const float4*>(xs[t]);
       float acc = 0.0f;
-      for (int k = 0; k < kD; ++k) acc = acc + r[k] * xs[t][k];
+#pragma unroll
+      for (int k4 = 0; k4 < kD / 4; ++k4) {  // left to right, no contraction: the exact order
+        const float4 x4 = xr[k4];
+        acc = acc + rr[4 * k4] * x4.x;
+        acc = acc + rr[4 * k4 + 1] * x4.y;
+        acc = acc + rr[4 * k4 + 2] * x4.z;
+        acc = acc + rr[4 * k4 + 3] * x4.w;
+      }
       const float nv = nrm[t];
+      uint32_t code = 0;
 #pragma unroll
       for (int k = 0; k < kTop; ++k) code += (uint32_t)(acc > nv * a.tau[k]);
+      ct[t][c] = (uint8_t)code;
     }
-    ct[t][c] = (uint8_t)code;
   }
   __syncthreads();
   // packing: thread = (token c / 4, channels 32 (c % 4) .. +31)

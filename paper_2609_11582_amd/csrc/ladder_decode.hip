@@ -79,7 +79,6 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];
   __shared__ __attribute__((aligned(16))) uint8_t vt[kLw][kW * kD * 2];    // value tiles
   __shared__ __attribute__((aligned(16))) uint16_t mt[kLw][2][kD];         // window (minimum, step)
-  __shared__ __attribute__((aligned(16))) float tile[kD][24 + 4];          // combined rows [channel][row]
   __shared__ __attribute__((aligned(16))) _Float16 atile[8][kATileL];
   __shared__ float wst[2][8][kLw];
   __shared__ uint32_t wmask[kLw], wnv[kLw];
@@ -418,6 +417,12 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   float nvw = nvmax;
 #pragma unroll
   for (int lb = 1; lb < 64; lb <<= 1) nvw = fmaxf(nvw, __shfl_xor(nvw, lb));
+  __syncthreads();  // every wave is done with its value tile: the tiles hold the waves' rows now
+  float* wacc = reinterpret_cast<float*>(&vt[0][0]);  // [wave][channel][16 rows]: audio 0-7, video 8-15
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb)
+    *reinterpret_cast<float4*>(wacc + ((size_t)wave * kD + 16 * cb + r) * 16 + 4 * g) =
+        make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
   if (lane < 8) {
     wst[0][lane][wave] = started ? m_run : -__builtin_inff();
     wst[1][lane][wave] = l_tot;
@@ -426,7 +431,6 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     wmask[wave] = seen;
     wnv[wave] = __builtin_bit_cast(uint32_t, nvw);
   }
-  for (int i = tid; i < kD * 28; i += 64 * kLw) (&tile[0][0])[i] = 0.0f;
   __syncthreads();
   uint32_t mask = 0;
   float nmax = 0.0f;
@@ -435,8 +439,8 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     mask |= wmask[w];
     nmax = fmaxf(nmax, __builtin_bit_cast(float, wnv[w]));
   }
-  // merged rows divided by L are convex combinations of n_v cb vectors (|cb| < 1): the factor
-  // 2^e / L with e = 13 - ilogb(n_max) keeps the fp16 A tile below 2^14
+  // merged rows divided by L are convex combinations of n_v cb vectors (|cb| < 1/4): the factor
+  // 2^e / L with e = 13 - ilogb(n_max) keeps the fp16 A tile below 2^12
   const int e = (nmax > 0.0f) ? 13 - min(max(ilogbf(nmax), -30), 20) : 0;
   if (tid < 8 * kLw) {
     const int hh = tid >> 3, w = tid & 7;
@@ -455,26 +459,18 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     }
   }
   __syncthreads();
-  // every wave adds its rows, scaled by its factors, in turn (a fixed order)
-  for (int w = 0; w < kLw; ++w) {
-    if (wave == w) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = 4 * g + i, hh = row & 7;
-        const float f = fac[hh][w];
-#pragma unroll
-        for (int cb = 0; cb < 8; ++cb) {
-          tile[16 * cb + r][row] += f * acc[cb][i];
-          if (g < 2) tile[16 * cb + r][16 + row] += f * txw[(16 * cb + r) * 8 + row];
-        }
-      }
-    }
-    __syncthreads();
-  }
-  // A tile [head][128 m + k] (fp16) for the present modalities
+  // A tile [head][128 m + k] (fp16): the waves' rows summed with their factors, in wave order
   for (int idx = tid; idx < 3 * 8 * kD; idx += 64 * kLw) {
     const int m = idx / (8 * kD), hh = (idx / kD) & 7, k = idx & (kD - 1);
-    atile[hh][m * kD + k] = (_Float16)((mask & (1u << m)) ? tile[k][8 * m + hh] : 0.0f);
+    float a = 0.0f;
+    if (mask & (1u << m)) {
+#pragma unroll
+      for (int w = 0; w < kLw; ++w) {
+        const float v = (m < 2) ? wacc[((size_t)w * kD + k) * 16 + 8 * m + hh] : ttx[w][k][hh];
+        a = __builtin_fmaf(fac[hh][w], v, a);
+      }
+    }
+    atile[hh][m * kD + k] = (_Float16)a;
   }
   __syncthreads();
   floatx4 dacc = {0.f, 0.f, 0.f, 0.f};
