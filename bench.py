@@ -50,7 +50,7 @@ the 30B-like layer shape.
 --shape-scan times decode alone at the other workload shapes (batch 16 with ragged lengths up to
 16384, batch 4 x 65536 with 2 KV heads and 16 query heads, 131072 tokens with 32 query heads, and
 batch 32 x 32768), with fp16 and MXFP4 key metadata and with TurboQuant keys, one JSON line each, on
-caches filled with random codes and metadata (the kernel's work does not depend on the values).
+caches filled with random codes and metadata and the workload's modality layout (the kernel's work does not depend on the values).
 """
 
 from __future__ import annotations
@@ -188,8 +188,12 @@ def cpu_baseline(cache_np, q, lens, signs, rot, bytes_per_call, prefill=None, ap
     return res
 
 
-def _scan_case(okvq, torch, name, B, lens, H, Hq, key_meta):
-    """Decode alone on random caches of one shape: per-call time over cycled replicas, effective GB/s."""
+def _scan_case(okvq, torch, name, B, lens, H, Hq, key_meta, wl):
+    """Decode alone on random caches of one shape: per-call time over cycled replicas, effective GB/s.
+    Codes, norms and metadata are random (the kernel's work does not depend on them); the modality
+    map is the workload's token stream (audio-visual chunks, then the text prompt), which does
+    decide the work (a pair with text runs a second value product)."""
+    import numpy as np
     dev = torch.device("cuda:0")
     sm = 1 / math.sqrt(128)
     cap = (max(lens) + 31) // 32 * 32
@@ -197,6 +201,11 @@ def _scan_case(okvq, torch, name, B, lens, H, Hq, key_meta):
     per_cache = sum(okvq.okvq_buffer_bytes(dims, i) for i in range(10))
     reps = max(2, min(16, int(math.ceil(1.05e9 / per_cache))))
     g = torch.Generator(device=dev).manual_seed(7)
+    from synth import modality_layout
+    mm = np.zeros((B, cap), np.uint8)
+    for b, L in enumerate(lens):
+        mm[b, :L] = modality_layout(int(L), wl.video_per_chunk, wl.audio_per_chunk, wl.text_tail)
+    mod_map = torch.from_numpy(mm.reshape(-1)).to(dev)
     caches = []
     for r in range(reps):
         c = okvq.KVCache(B, H, Hq, cap, torch.ones(128, dtype=torch.int8), torch.eye(128).repeat(3, 1, 1), device=dev,
@@ -205,7 +214,7 @@ def _scan_case(okvq, torch, name, B, lens, H, Hq, key_meta):
             if n == "seq_lens":
                 t[:B].copy_(torch.tensor(lens, dtype=torch.int32))
             elif n == "modality":
-                t.random_(0, 3, generator=g)
+                t.copy_(mod_map)
             elif t.dtype == torch.float16:
                 t.copy_((torch.rand(t.shape, device=dev, generator=g) * 0.5 + 0.1).half())
             elif t.dtype == torch.uint8:
@@ -243,7 +252,7 @@ def shape_scan(okvq, torch, workload, gen_lengths):
         B = batch or wl.batch
         lens = [int(x) for x in gen_lengths(wl)] if batch is None else [wl.seq_len] * B
         for km in ("fp16", "mxfp4", "turboquant"):
-            _scan_case(okvq, torch, name, B, lens, wl.num_kv_heads, wl.num_q_heads, km)
+            _scan_case(okvq, torch, name, B, lens, wl.num_kv_heads, wl.num_q_heads, km, wl)
 
 
 def sylvester_hadamard(signs):
