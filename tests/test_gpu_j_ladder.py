@@ -121,3 +121,34 @@ def test_ladder_decode_full_size(kb, vb, meta):
     r = gh.attention_close(out[:, rows], ref)
     print(f"full size K{kb}V{vb} {meta}: worst err / norm = {r:.2e}", flush=True)
     assert r <= TOL
+
+
+def test_ladder_300_sequences_and_exact_flag():
+    """More sequences than one codec launch's length table (256): every sequence's codes bit-exact;
+    the exact-mode flag gives the same value codes (the ladder's value codec is the exact order)."""
+    import torch
+
+    import gpu_helpers as gh
+    import paper_2609_11582_amd as okvq
+    rng = np.random.default_rng(3)
+    B = 300
+    lens = [int(x) for x in rng.integers(0, 65, B)]
+    lens[7] = 64
+    wl = workload("tiny_1k")
+    lay = gen_layer(wl, 2, lengths=np.full(B, 64, np.int32), n_tokens=64)
+    k, v = lay["k"], lay["v"]                              # [300][1][64][128]
+    mod = rng.integers(0, 3, (B, 64)).astype(np.uint8)     # all three rotations in every window
+    _announce(f"ladder K3V3, {B} sequences")
+    cache = gh.ladder_cache(k, v, mod, lens, lay["signs"], lay["rot"], 64, 4, 3, 3, "fp16")
+    got = _arrays(cache)
+    ref = quantize_layer_bits(k, v, mod, lens, lay["signs"], lay["rot"], 64, 3, 3, "fp16")
+    for name in ref:
+        _same(got[name], ref[name], name)
+    vw = cache.views()
+    vc2 = torch.zeros_like(vw["v_codes"])
+    vn2 = torch.zeros_like(vw["v_norm"])
+    okvq.okvq_quantize_values(cache.dims, gh.f16dev(v), gh.dev(np.ascontiguousarray(mod, np.uint8)), 64, lens,
+                              cache.v_rot, okvq.okvq.OKVQ_VALUE_EXACT, vc2, vn2)
+    torch.cuda.synchronize()
+    _same(vc2.cpu().numpy(), ref["v_codes"], "v_codes (exact flag)")
+    _same(vn2.cpu().numpy(), ref["v_norm"], "v_norm (exact flag)")
