@@ -388,19 +388,19 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     wave_lds_sync();  // transposed reads done before the next window overwrites the tile
   };
 
-  LTile<kKB, kVB> ta, tb2;
+  LTile<kKB, kVB> ta, tn;  // the window being computed, and the next one in flight
   int it = 0;
   if (nmine > 0) issue(0, ta);
   for (; it + 2 < nmine; it += 2) {
-    issue(it + 1, tb2);
+    issue(it + 1, tn);
     compute(it, ta);
     issue(it + 2, ta);
-    compute(it + 1, tb2);
+    compute(it + 1, tn);
   }
   if (it + 1 < nmine) {
-    issue(it + 1, tb2);
+    issue(it + 1, tn);
     compute(it, ta);
-    compute(it + 1, tb2);
+    compute(it + 1, tn);
   } else if (it < nmine) {
     compute(it, ta);
   }
