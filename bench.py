@@ -37,6 +37,8 @@ Reported (one JSON line):
                   32 query heads): one decode step per layer over the packed caches, over packed
                   caches with the single global value rotation, and with the dense fp16 baseline
                   kernel over the same fp16 K and V (12.9 GB resident); per-layer append
+  stream          the streaming workload (batch 4 x 65536, 2 KV heads, 16 query heads): 16 steps of a
+                  512-token append per sequence then a decode, each timed
   calibration     the value-rotation calibration (Eq. 5) on a 4096-token calibration sequence at the
                   same head shapes: attention weights (against the fp16 matrix-core peak), weighted
                   covariance, host eigensolver
@@ -452,6 +454,60 @@ def ladder_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, q, signs, rot,
             "replicas": n_cache}
         del caches, base
         torch.cuda.empty_cache()
+    return res
+
+
+def stream_measurement(okvq, torch, np, dev, stream):
+    """The streaming workload (batch 4 x 65536 tokens, 2 KV heads, 16 query heads, video-heavy): a
+    prefill append, then 16 steps of (append 512 audio-visual tokens per sequence, decode). Each
+    append and decode is timed with events; the decode reads the cache the step just wrote (warm in
+    the Infinity Cache, as in the protocol). Inputs generated on the device (synth.device for the
+    prefill; the streamed rows N(0, 1) with the workload's audio-visual pattern -- the append's
+    work does not depend on the values)."""
+    from synth import stream_chunk_modalities, workload
+    from synth.device import gen_layer_device
+    wl = workload("omni3b_b4_64k_stream")
+    B, H, Hq, N, steps, step = wl.batch, wl.num_kv_heads, wl.num_q_heads, wl.seq_len, wl.stream_steps, wl.stream_tokens
+    sm = 1 / math.sqrt(128)
+    lay = gen_layer_device(wl, 0, dev)
+    c = okvq.KVCache(B, H, Hq, wl.capacity, torch.from_numpy(lay["signs"]), torch.from_numpy(lay["rot"]), device=dev)
+    lens = [N] * B
+    okvq.okvq_append(c, [0] * B, lay["k"], lay["v"], lay["modality"], lens, torch.tensor(lens, dtype=torch.int32,
+                                                                                          device=dev), N, stream=stream)
+    g = torch.Generator(device=dev).manual_seed(11)
+    kn = [torch.randn(B, H, step, 128, device=dev, generator=g).half() for _ in range(steps)]
+    vn = [torch.randn(B, H, step, 128, device=dev, generator=g).half() for _ in range(steps)]
+    mods = [torch.from_numpy(np.tile(stream_chunk_modalities(wl, N - wl.text_tail + s * step, step), (B, 1))).to(dev)
+            for s in range(steps)]
+    nn = torch.tensor([step] * B, dtype=torch.int32, device=dev)
+    q = torch.from_numpy(lay["q"]).to(dev)
+    ws = okvq.decode_workspace(c.dims, wl.capacity, device=dev)
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    ev = []
+    for s in range(steps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        cur = N + s * step
+        e[0].record(stream)
+        okvq.okvq_append(c, [cur] * B, kn[s], vn[s], mods[s], [step] * B, nn, step, stream=stream)
+        e[1].record(stream)
+        okvq.okvq_decode_attention(c, [cur + step] * B, q, sm, out, ws, stream=stream)
+        e[2].record(stream)
+        ev.append(e)
+    torch.cuda.synchronize()
+    app = [e[0].elapsed_time(e[1]) * 1e3 for e in ev]
+    dec = [e[1].elapsed_time(e[2]) * 1e3 for e in ev]
+    mean_len = N + step * (steps + 1) / 2
+    abytes = append_algorithmic_bytes(B, H, [step] * B)
+    dbytes = decode_algorithmic_bytes(B, H, Hq, [int(mean_len)] * B)
+    res = {"workload": "omni3b_b4_64k_stream", "batch": B, "kv_heads": H, "q_heads": Hq, "prefill": N,
+           "steps": steps, "tokens_per_step": step,
+           "append_us": round(float(np.mean(app[1:])), 2), "append_GBps": round(abytes / np.mean(app[1:]) / 1e3, 1),
+           "decode_us": round(float(np.mean(dec[1:])), 2), "decode_GBps_warm": round(dbytes / np.mean(dec[1:]) / 1e3, 1),
+           "step_us": round(float(np.mean([a + d for a, d in zip(app[1:], dec[1:])])), 2),
+           "append_algorithmic_bytes": abytes}
+    del c, kn, vn
+    torch.cuda.empty_cache()
     return res
 
 
@@ -969,6 +1025,7 @@ def main():
     line["calibration"] = calibration_measurement(okvq, torch, np, wl, dev)
     if not args.no_layers48:
         line["omni30b_48layer"] = layers48_measurement(okvq, torch, np, dev, stream)
+    line["stream"] = stream_measurement(okvq, torch, np, dev, stream)
     line["residual"] = residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                             args.decode_iters)
     if not args.no_cpu_baseline:
