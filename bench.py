@@ -410,6 +410,16 @@ def ladder_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, q, signs, rot,
         torch.cuda.synchronize()
         keys_us = float(np.mean([a.elapsed_time(b) for a, b, _ in ev[2:]])) * 1e3
         vals_us = float(np.mean([b.elapsed_time(c) for _, b, c in ev[2:]])) * 1e3
+        exact = []
+        for i in range(6):  # the exact fp32 order of the same call
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            okvq.okvq_quantize_values(base.dims, v_in[i % len(v_in)], m0, N, lens, base.v_rot, okvq.okvq.OKVQ_VALUE_EXACT,
+                                      vw["v_codes"], vw["v_norm"], stream=stream)
+            e1.record(stream)
+            exact.append((e0, e1))
+        torch.cuda.synchronize()
+        vals_exact_us = float(np.mean([a.elapsed_time(b) for a, b in exact[2:]])) * 1e3
         per_cache = sum(okvq.okvq_buffer_bytes(base.dims, i) for i in range(12))
         n_cache = max(16, int(math.ceil(1.05e9 / per_cache)))
         caches = [base] + [okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev, key_meta=meta, key_bits=kb,
@@ -449,6 +459,7 @@ def ladder_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, q, signs, rot,
             "bits_per_element": round(bpt * 8 / 256, 4), "bytes_per_token_head": bpt,
             "quantize_keys_us": round(keys_us, 2), "quantize_keys_GBps": round(kbytes / keys_us / 1e3, 1),
             "quantize_values_us": round(vals_us, 2), "quantize_values_GBps": round(vbytes / vals_us / 1e3, 1),
+            "quantize_values_exact_us": round(vals_exact_us, 2),
             "decode_us": round(decode_us, 3), "decode_GBps": round(dbytes / decode_us / 1e3, 1),
             "k_ladder_decode_us": round(split_us, 3), "k_ladder_decode_frac": round(sbytes / split_us / 1e3 / HBM_PEAK_GBPS, 4),
             "replicas": n_cache}

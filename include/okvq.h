@@ -82,8 +82,9 @@
  *   k_codes  u8 [B][H][cap][16 key_bits]      v_codes  u8 [B][H][cap][16 value_bits]
  *   k_norm, v_norm, k_min, k_step (fp16 metadata; absent for TurboQuant keys) and modality as above;
  *   no k_stage, k_mx or residual rings. okvq_quantize_keys / okvq_quantize_keys_tq /
- *   okvq_quantize_values fill it (values always in the exact fp32 order; the modality map is the
- *   caller's copy), okvq_decode_attention reads it, okvq_append returns OKVQ_ERR_UNSUPPORTED.
+ *   okvq_quantize_values fill it (values in either mode; only slots below a length are written;
+ *   the modality map is the caller's copy),
+ *   okvq_decode_attention reads it, okvq_append returns OKVQ_ERR_UNSUPPORTED.
  *   Storage per token and KV head: 16 (key_bits + value_bits) + 4 bytes, + 16 with fp16 metadata
  *   (TurboQuant K3/V2: 84 bytes = 2.625 bits per element).
  *
@@ -241,7 +242,7 @@ okvq_status okvq_quantize_keys_tq(const okvq_dims* dims, const uint16_t* k, int3
  *   flags      OKVQ_VALUE_EXACT: y = R_m v as a sequential fp32 dot product (codes bit-exact with
  *              the documented order); otherwise MFMA with an fp16 hi/lo split of R_m and fp32
  *              accumulation (codes may differ from the exact order only where y lies within a
- *              small band around a decision threshold).
+ *              small band around a decision threshold). Both layouts, both modes.
  *   outputs    device v_codes, v_norm in the cache layout (whole 32-token windows are written;
  *              slots beyond a length get code 0 and norm 0). */
 okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const uint8_t* modality,

@@ -375,7 +375,7 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
     if (lens_host[b] > dims->capacity) return OKVQ_ERR_CAPACITY;
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (is_ladder(dims)) {  // the exact fp32 order in both modes
+  if (is_ladder(dims)) {
     const Codebook& cb = codebook(dims->value_bits);
     for (int b0 = 0; b0 < dims->batch; b0 += kMaxLenArgs) {
       const int nb = std::min(kMaxLenArgs, dims->batch - b0);
@@ -395,7 +395,7 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
       a.v_codes = v_codes;
       a.v_norm = v_norm;
       for (int i = 0; i + 1 < cb.levels; ++i) a.tau[i] = cb.thr[i];
-      st = hip_status(launch_ladder_values(a, dims->value_bits, nb, max_len, s));
+      st = hip_status(launch_ladder_values(a, dims->value_bits, (flags & OKVQ_VALUE_EXACT) != 0, nb, max_len, s));
       if (st != OKVQ_OK) return st;
     }
     return OKVQ_OK;

@@ -10,7 +10,7 @@
 // step (max - min) / (2^b - 1) in fp16 and the codes clamp(rint(fl(fl(z - m16) fl(1 / step16))), 0,
 // 2^b - 1); phase C, thread = token, packs its row.
 //
-// Values (one work-group of 128 threads, thread = output channel, per 32-token window): the
+// Values, exact mode (one work-group of 128 threads, thread = output channel, per 32-token window): the
 // exact-mode order of the 2-bit codec -- y_c = sum_j fl(R_cj v_j) left to right in fp32, n16 by the
 // halving tree -- and code = #{k : y_c > fl(n16 tau_k)} against the 2^b - 1 thresholds. A thread
 // holds its row of R_m in registers for each modality present in the window (R is read once per
@@ -258,6 +258,138 @@ __global__ __launch_bounds__(128) void k_ladder_values(LadderValueArgs a) {
   store_run<kBits>(a.v_codes + (seq * a.cap + tok) * kRowBytes, part, w);
 }
 
+// MFMA mode: one work-group of 256 threads (4 waves) per 128 tokens of a (sequence, KV head). The
+// value rows (fp16, exact) are staged in LDS as MFMA A operands; wave w computes output channels
+// 32 w .. 32 w + 31 of all 128 tokens, per modality present, against its slice of R_m split into
+// fp16 hi + lo parts (B operands, converted once per modality and tile), fp32 accumulation. The
+// codes then equal the exact order's except where y lies within a small band of a threshold (about
+// 2^-22 sum_j |R_cj v_j| of accumulation-order and split error, inside the band the tests allow).
+typedef _Float16 half8v __attribute__((ext_vector_type(8)));
+typedef float floatx4v __attribute__((ext_vector_type(4)));
+constexpr int kVTile = 128;       // tokens per work-group
+constexpr int kVPitch = kD + 8;   // fp16 row pitch of the LDS value tile
+
+__device__ __forceinline__ uint32_t hi_lo_pair(float x0, float x1, bool lo) {
+  const _Float16 h0 = (_Float16)x0, h1 = (_Float16)x1;
+  const _Float16 a = lo ? (_Float16)(x0 - (float)h0) : h0;
+  const _Float16 b = lo ? (_Float16)(x1 - (float)h1) : h1;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+template <int kBits>
+__global__ __launch_bounds__(256) void k_ladder_values_mfma(LadderValueArgs a) {
+  constexpr int kTop = (1 << kBits) - 1;
+  constexpr int kRowBytes = 16 * kBits;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[kVTile][kVPitch];
+  __shared__ float nrm[kVTile];
+  __shared__ int mods[kVTile];
+  __shared__ __attribute__((aligned(16))) uint8_t ct[kVTile][kD];
+  const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz;
+  const int len = a.lens.lens[bz];
+  const int t0 = kVTile * blockIdx.x;
+  if (t0 >= len) return;  // uniform
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, r = lane & 15;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const size_t seq = (size_t)b * a.H + h;
+  // ---- stage the rows (zeros beyond the length), the modalities, the codes' default 0 ----
+  for (int idx = tid; idx < kVTile * (kD / 8); idx += 256) {
+    const int t = idx >> 4, c8 = idx & 15, tok = t0 + t;
+    const uint4 v = (tok < len) ? *reinterpret_cast<const uint4*>(a.v + (seq * a.n_rows + tok) * kD + 8 * c8)
+                                : make_uint4(0u, 0u, 0u, 0u);
+    *reinterpret_cast<uint4*>(&xs[t][8 * c8]) = v;
+    *reinterpret_cast<uint2*>(&ct[t][8 * c8]) = make_uint2(0u, 0u);
+  }
+  if (tid < kVTile) {
+    const int tok = t0 + tid;
+    mods[tid] = (tok < len) ? (int)a.modality[(size_t)b * a.n_rows + tok] : -1;
+  }
+  __syncthreads();
+  if (tid < kVTile) {  // fp16 norm by the halving tree, as the exact mode
+    const int tok = t0 + tid;
+    float tt[64];
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+      const float x0 = h2f(xs[tid][i]), x1 = h2f(xs[tid][i + 64]);
+      tt[i] = x0 * x0 + x1 * x1;
+    }
+#pragma unroll
+    for (int n = 32; n >= 1; n >>= 1) {
+#pragma unroll
+      for (int i = 0; i < n; ++i) tt[i] = tt[i] + tt[i + n];
+    }
+    const uint32_t n16 = (tok < len) ? norm_to_f16(sqrt_rn(tt[0])) : 0u;
+    nrm[tid] = h2f(n16);
+    if (tok < len) a.v_norm[seq * a.cap + tok] = (uint16_t)n16;
+  }
+  __syncthreads();
+  for (int m = 0; m < 3; ++m) {
+    bool any = false;
+    for (int t = 0; t < kVTile; ++t) any |= mods[t] == m;
+    if (!any) continue;  // uniform
+    // B operands: channel c = 32 wave + 16 cb + r, k = 32 kb + 8 g .. + 7 of R_m (hi, lo parts)
+    uint32_t bh[2][4][4], bl[2][4][4];
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+      const float* rrow = a.rot + ((size_t)m * kD + 32 * wave + 16 * cb + r) * kD;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const float4 p0 = *reinterpret_cast<const float4*>(rrow + 32 * kb + 8 * g);
+        const float4 p1 = *reinterpret_cast<const float4*>(rrow + 32 * kb + 8 * g + 4);
+        const float v8[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          bh[cb][kb][j] = hi_lo_pair(v8[2 * j], v8[2 * j + 1], false);
+          bl[cb][kb][j] = hi_lo_pair(v8[2 * j], v8[2 * j + 1], true);
+        }
+      }
+    }
+    for (int rb = 0; rb < kVTile / 16; ++rb) {
+      floatx4v acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const half8v av = *reinterpret_cast<const half8v*>(&xs[16 * rb + r][32 * kb + 8 * g]);
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+          acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+              av, __builtin_bit_cast(half8v, make_uint4(bh[cb][kb][0], bh[cb][kb][1], bh[cb][kb][2], bh[cb][kb][3])),
+              acc[cb], 0, 0, 0);
+          acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+              av, __builtin_bit_cast(half8v, make_uint4(bl[cb][kb][0], bl[cb][kb][1], bl[cb][kb][2], bl[cb][kb][3])),
+              acc[cb], 0, 0, 0);
+        }
+      }
+      // D[token 16 rb + 4 g + i][channel 32 wave + 16 cb + r]
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = 16 * rb + 4 * g + i;
+        if (mods[t] != m) continue;
+        const float nv = nrm[t];
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+          uint32_t code = 0;
+#pragma unroll
+          for (int k = 0; k < kTop; ++k) code += (uint32_t)(acc[cb][i] > nv * a.tau[k]);
+          ct[t][32 * wave + 16 * cb + r] = (uint8_t)code;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // pack: thread = (token, 32 channels), two items each
+  for (int it = tid; it < kVTile * 4; it += 256) {
+    const int t = it >> 2, part = it & 3, tok = t0 + t;
+    if (tok >= len) continue;
+    uint32_t cw[8];
+    const uint4* src = reinterpret_cast<const uint4*>(&ct[t][32 * part]);
+    const uint4 u0 = src[0], u1 = src[1];
+    cw[0] = u0.x; cw[1] = u0.y; cw[2] = u0.z; cw[3] = u0.w;
+    cw[4] = u1.x; cw[5] = u1.y; cw[6] = u1.z; cw[7] = u1.w;
+    uint32_t w[kBits];
+    pack32<kBits>(cw, w);
+    store_run<kBits>(a.v_codes + (seq * a.cap + tok) * kRowBytes, part, w);
+  }
+}
+
 template <int kBits>
 hipError_t keys_for_bits(const LadderKeyArgs& a, bool tq, dim3 grid, hipStream_t s) {
   if (tq)
@@ -280,8 +412,18 @@ hipError_t launch_ladder_keys(const LadderKeyArgs& a, int bits, bool tq, int nb,
   }
 }
 
-hipError_t launch_ladder_values(const LadderValueArgs& a, int bits, int nb, int max_len, hipStream_t s) {
+hipError_t launch_ladder_values(const LadderValueArgs& a, int bits, bool exact, int nb, int max_len, hipStream_t s) {
   if (nb <= 0 || max_len <= 0) return hipSuccess;
+  if (!exact) {
+    const dim3 grid((max_len + kVTile - 1) / kVTile, a.H, nb);
+    switch (bits) {
+      case 2: hipLaunchKernelGGL(k_ladder_values_mfma<2>, grid, dim3(256), 0, s, a); break;
+      case 3: hipLaunchKernelGGL(k_ladder_values_mfma<3>, grid, dim3(256), 0, s, a); break;
+      case 4: hipLaunchKernelGGL(k_ladder_values_mfma<4>, grid, dim3(256), 0, s, a); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   const dim3 grid((max_len + kW - 1) / kW, a.H, nb);
   switch (bits) {
     case 2: hipLaunchKernelGGL(k_ladder_values<2>, grid, dim3(128), 0, s, a); break;

@@ -162,7 +162,8 @@ struct LadderValueArgs {
   float tau[15];
 };
 hipError_t launch_ladder_keys(const LadderKeyArgs& a, int bits, bool tq, int nb, int max_len, hipStream_t s);
-hipError_t launch_ladder_values(const LadderValueArgs& a, int bits, int nb, int max_len, hipStream_t s);
+// exact: the sequential fp32 order (bit-exact codes); else the matrix cores (fp16 hi + lo split of R_m)
+hipError_t launch_ladder_values(const LadderValueArgs& a, int bits, bool exact, int nb, int max_len, hipStream_t s);
 
 struct LadderDecodeArgs {
   const uint8_t* k_codes;

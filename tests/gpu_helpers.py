@@ -191,9 +191,28 @@ def check_window(arrays, k16, v16, modality, signs, rot, b, h, w, length):
         assert not np.any(unpack_values(arrays["v_codes"][b, h, w:w + 1])[n:])
 
 
-def ladder_cache(k, v, modality, lens, signs, rot, capacity, num_q_heads, key_bits, value_bits, key_meta="fp16"):
+def band_compare_bits(gpu_vcodes, v16, modality, rot, length, bits):
+    """b-bit MFMA-mode value codes (one (sequence, head) of the ladder layout, [cap][16 b] bytes)
+    equal the exact order except where y is within the band of a threshold, and never by more than
+    one level. Returns (codes that differ, codes in the band)."""
+    from oracle.ladder import quantize_values_bits_fmt, unpack_bits
+    from oracle.values import rotation_error_bound
+    ref = quantize_values_bits_fmt(v16, modality, rot, length, bits)
+    got = unpack_bits(np.asarray(gpu_vcodes)[:length], bits)
+    eps = rotation_error_bound(v16[:length], modality[:length], rot)
+    dist = np.abs(ref["y"][:, :, None].astype(np.float64) - ref["thr"][:, None, :].astype(np.float64)).min(-1)
+    in_band = dist <= eps
+    diff = got != ref["codes"]
+    assert not np.any(diff & ~in_band), f"{int((diff & ~in_band).sum())} codes differ outside the band"
+    assert np.all(np.abs(got.astype(int) - ref["codes"].astype(int)) <= 1)
+    return int(diff.sum()), int(in_band.sum())
+
+
+def ladder_cache(k, v, modality, lens, signs, rot, capacity, num_q_heads, key_bits, value_bits, key_meta="fp16",
+                 value_flags=None):
     """A bit-width-ladder cache filled by the stateless codec calls (keys, values), with the
-    modality map and the device lengths copied in."""
+    modality map and the device lengths copied in. Values take the exact order unless
+    ``value_flags`` says otherwise (0: the matrix-core mode)."""
     B, H, N, D = k.shape
     cache = okvq.KVCache(B, H, num_q_heads, capacity, torch.from_numpy(np.ascontiguousarray(signs)),
                          torch.from_numpy(np.ascontiguousarray(rot, np.float32)), key_meta=key_meta,
@@ -206,7 +225,8 @@ def ladder_cache(k, v, modality, lens, signs, rot, capacity, num_q_heads, key_bi
                                 vw["k_step"], vw["k_norm"])
     else:
         okvq.okvq_quantize_keys_tq(cache.dims, kd, N, list(lens), cache.key_signs, vw["k_codes"], vw["k_norm"])
-    okvq.okvq_quantize_values(cache.dims, vd, md, N, list(lens), cache.v_rot, 0, vw["v_codes"], vw["v_norm"])
+    flags = okvq.okvq.OKVQ_VALUE_EXACT if value_flags is None else value_flags
+    okvq.okvq_quantize_values(cache.dims, vd, md, N, list(lens), cache.v_rot, flags, vw["v_codes"], vw["v_norm"])
     mod = np.zeros((B, capacity), np.uint8)
     for b in range(B):
         mod[b, :lens[b]] = modality[b, :lens[b]]
