@@ -319,8 +319,14 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     qraw = *reinterpret_cast<const uint2*>(p.q + ((size_t)b * p.Hq + h * p.G + hr) * kD + c4);
     qsgn = *reinterpret_cast<const uint32_t*>(p.signs + c4);
   }
+  // The first pair is loaded unconditionally, its window clamped into the sequence's capacity
+  // (a wave without a pair never uses it): under a branch, the compiler's wait before the barrier
+  // below would have to assume no pair loads in flight and wait for all of them.
   PairLoad bufA, bufB;
-  if (wA0 < w_plan) bufA = load_pair<kMeta>(sp, wA0, wA0 + 1 < w_plan, lane);
+  {
+    const int wAc = max(min(wA0, w_plan - 1), 0);
+    bufA = load_pair<kMeta>(sp, wAc, wAc + 1 < w_plan, lane);
+  }
   // memory-safe if device and host lengths disagree; with the fp16 residual the last 128 tokens
   // are the merge launch's
   const int len = max(min(p.seq_lens[b], p.cap) - p.residual, 0);
