@@ -89,7 +89,16 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, r = lane & 15;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // the length (a scalar load, read before any divergent branch), then the query rows and signs
+  // (waves 0-3), before anything waits
   const int len = min(p.seq_lens[b], p.cap);
+  const int hr = 2 * wave + (lane >> 5), c4 = 4 * (lane & 31);
+  uint2 qr = make_uint2(0u, 0u);
+  uint32_t sg = 0u;
+  if (wave < 4 && hr < p.G) {
+    qr = *reinterpret_cast<const uint2*>(p.q + ((size_t)b * p.Hq + h * p.G + hr) * kD + c4);
+    sg = *reinterpret_cast<const uint32_t*>(p.signs + c4);
+  }
   const int t_begin = split * p.tps, t_end = min(t_begin + p.tps, len);
   const size_t seq = (size_t)b * p.H + h;
   float* rec = p.ws + (seq * p.nsplit + split) * kRecFloats;
@@ -106,22 +115,74 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   const uint16_t* nvbase = p.v_norm + seq * p.cap;
   const uint8_t* mdbase = p.modality + (size_t)b * p.cap;
   const size_t nwcap = p.cap / kW;
+  const int ntile = (t_end - t_begin + kW - 1) / kW;
+  const int nmine = ntile > wave ? (ntile - wave + kLw - 1) / kLw : 0;
+  // key field of k-block kb: byte offset kKB (4 kb + g) of the token row, shift inside its dword
+  auto kfield_dword = [&](int kb) { return (kKB * (4 * kb + g)) >> 2; };
+  const int ksh = 8 * ((kKB * g) & 3);  // the same for every kb (4 kb kKB is a multiple of 4)
+
+  auto issue_tile = [&](int tile, LTile<kKB, kVB>& lt) {
+    const int t0 = t_begin + tile * kW;
+    const int last = t_end - 1;
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      const uint32_t* row = reinterpret_cast<const uint32_t*>(kbase + (size_t)min(t0 + 16 * tb + r, last) * kKRow);
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const int d0 = kfield_dword(kb);
+        lt.kf[tb][kb][0] = row[d0];
+        lt.kf[tb][kb][1] = (kKB == 3) ? row[min(d0 + 1, 4 * kKB - 1)] : 0u;
+      }
+      // norms and modalities of 4 tokens inside the window (slots past the length are masked later)
+      lt.nk[tb] = *reinterpret_cast<const uint2*>(nkbase + t0 + 16 * tb + 4 * g);
+      lt.nv[tb] = *reinterpret_cast<const uint2*>(nvbase + t0 + 16 * tb + 4 * g);
+      lt.md[tb] = *reinterpret_cast<const uint32_t*>(mdbase + t0 + 16 * tb + 4 * g);
+    }
+    {
+      const uint2* vrow = reinterpret_cast<const uint2*>(vbase + (size_t)min(t0 + (lane >> 1), last) * kVRow) +
+                          kVB * (lane & 1);
+#pragma unroll
+      for (int i = 0; i < kVB; ++i) {
+        const uint2 u = vrow[i];
+        lt.vc[2 * i] = u.x;
+        lt.vc[2 * i + 1] = u.y;
+      }
+    }
+    if constexpr (!kTq) {
+      const size_t mrow = (seq * nwcap + t0 / kW) * kD;
+      const uint16_t* src = (lane < 32 ? p.k_min : p.k_step) + mrow + 4 * (lane & 31);
+      lt.meta = *reinterpret_cast<const uint2*>(src);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // the window's loads go out before the work that follows
+  };
+  auto issue = [&](int it, LTile<kKB, kVB>& lt) { issue_tile(wave + kLw * it, lt); };
+  // The first window is loaded before the tables and the query rotation, and unconditionally (a
+  // wave without a window loads the split's last one and never uses it), so that the barrier below
+  // waits for the query loads only.
+  LTile<kKB, kVB> ta, tn;  // the window being computed, and the next one in flight
+  issue_tile(min(wave, ntile - 1), ta);
 
   // ---- tables, and the rotated query: wave w < 4 rotates heads 2w, 2w + 1 (lane: 4 channels) ----
+  // code-pair tables; the codebook levels are picked by selects over constant indices (a dynamic
+  // index into the argument arrays would read them through memory, one more round trip)
+  auto level = [](const uint16_t (&cb)[16], int c, int n) {
+    uint32_t v = (uint32_t)__builtin_amdgcn_readfirstlane((int)cb[0]);
+#pragma unroll
+    for (int j = 1; j < 16; ++j)
+      if (j < n) v = (c == j) ? (uint32_t)__builtin_amdgcn_readfirstlane((int)cb[j]) : v;
+    return v;
+  };
   for (int i = tid; i < (1 << (2 * kKB)); i += 64 * kLw) {
     const int c0 = i & ((1 << kKB) - 1), c1 = i >> kKB;
-    klut[i] = kTq ? (uint32_t)p.kcb16[c0] | ((uint32_t)p.kcb16[c1] << 16) : pk_h2((float)c0, (float)c1);
+    klut[i] = kTq ? level(p.kcb16, c0, 1 << kKB) | (level(p.kcb16, c1, 1 << kKB) << 16) : pk_h2((float)c0, (float)c1);
   }
   for (int i = tid; i < (1 << (2 * kVB)); i += 64 * kLw) {
     const int c0 = i & ((1 << kVB) - 1), c1 = i >> kVB;
-    vlut[i] = (uint32_t)p.vcb16[c0] | ((uint32_t)p.vcb16[c1] << 16);
+    vlut[i] = level(p.vcb16, c0, 1 << kVB) | (level(p.vcb16, c1, 1 << kVB) << 16);
   }
   if (wave < 4) {
-    const int hr = 2 * wave + (lane >> 5), c4 = 4 * (lane & 31);
-    float x[4] = {0.f, 0.f, 0.f, 0.f};
-    if (hr < p.G) {
-      const uint2 qr = *reinterpret_cast<const uint2*>(p.q + ((size_t)b * p.Hq + h * p.G + hr) * kD + c4);
-      const uint32_t sg = *reinterpret_cast<const uint32_t*>(p.signs + c4);
+    float x[4];
+    {  // zero for heads >= G (their loads were skipped)
       const float v[4] = {lo_h(qr.x), hi_h(qr.x), lo_h(qr.y), hi_h(qr.y)};
 #pragma unroll
       for (int i = 0; i < 4; ++i) x[i] = ((sg >> (8 * i + 7)) & 1u) ? -v[i] : v[i];
@@ -172,46 +233,6 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     qop[kb][3] = live ? pk_h2(ldexpf(c.z, k0), ldexpf(c.w, k0)) : 0u;
   }
 
-  const int ntile = (t_end - t_begin + kW - 1) / kW;
-  const int nmine = ntile > wave ? (ntile - wave + kLw - 1) / kLw : 0;
-  // key field of k-block kb: byte offset kKB (4 kb + g) of the token row, shift inside its dword
-  auto kfield_dword = [&](int kb) { return (kKB * (4 * kb + g)) >> 2; };
-  const int ksh = 8 * ((kKB * g) & 3);  // the same for every kb (4 kb kKB is a multiple of 4)
-
-  auto issue = [&](int it, LTile<kKB, kVB>& lt) {
-    const int t0 = t_begin + (wave + kLw * it) * kW;
-    const int last = t_end - 1;
-#pragma unroll
-    for (int tb = 0; tb < 2; ++tb) {
-      const uint32_t* row = reinterpret_cast<const uint32_t*>(kbase + (size_t)min(t0 + 16 * tb + r, last) * kKRow);
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const int d0 = kfield_dword(kb);
-        lt.kf[tb][kb][0] = row[d0];
-        lt.kf[tb][kb][1] = (kKB == 3) ? row[min(d0 + 1, 4 * kKB - 1)] : 0u;
-      }
-      // norms and modalities of 4 tokens inside the window (slots past the length are masked later)
-      lt.nk[tb] = *reinterpret_cast<const uint2*>(nkbase + t0 + 16 * tb + 4 * g);
-      lt.nv[tb] = *reinterpret_cast<const uint2*>(nvbase + t0 + 16 * tb + 4 * g);
-      lt.md[tb] = *reinterpret_cast<const uint32_t*>(mdbase + t0 + 16 * tb + 4 * g);
-    }
-    {
-      const uint2* vrow = reinterpret_cast<const uint2*>(vbase + (size_t)min(t0 + (lane >> 1), last) * kVRow) +
-                          kVB * (lane & 1);
-#pragma unroll
-      for (int i = 0; i < kVB; ++i) {
-        const uint2 u = vrow[i];
-        lt.vc[2 * i] = u.x;
-        lt.vc[2 * i + 1] = u.y;
-      }
-    }
-    if constexpr (!kTq) {
-      const size_t mrow = (seq * nwcap + t0 / kW) * kD;
-      const uint16_t* src = (lane < 32 ? p.k_min : p.k_step) + mrow + 4 * (lane & 31);
-      lt.meta = *reinterpret_cast<const uint2*>(src);
-    }
-    __builtin_amdgcn_sched_barrier(0);  // the window's loads go out before the work that follows
-  };
 
   floatx4 acc[8];  // rows 0-7 audio heads, 8-15 video heads; channel 16 cb + r
 #pragma unroll
@@ -388,9 +409,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     wave_lds_sync();  // transposed reads done before the next window overwrites the tile
   };
 
-  LTile<kKB, kVB> ta, tn;  // the window being computed, and the next one in flight
   int it = 0;
-  if (nmine > 0) issue(0, ta);
   for (; it + 2 < nmine; it += 2) {
     issue(it + 1, tn);
     compute(it, ta);
