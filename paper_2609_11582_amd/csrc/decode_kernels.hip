@@ -760,19 +760,26 @@ __device__ __forceinline__ void load_split_chunk(const float* base, int nsplit, 
   for (int u = 0; u < kMergeUnroll; ++u) {
     const int s = s0 + 8 * u;
     const float* rs = base + (size_t)min(s, nsplit - 1) * kRecFloats;
-    c.ms[u] = (s < nsplit) ? rs[hd] : -__builtin_inff();
+    // loaded unconditionally (the record index is clamped), then selected: a conditional load is
+    // compiled as a branch, after which the wait before the fold covers every load in flight and the
+    // chunk's last loads go out a round trip late
+    const float m = rs[hd];
+    c.ms[u] = (s < nsplit) ? m : -__builtin_inff();
     c.ls[u] = rs[8 + hd];
     c.v[u] = *reinterpret_cast<const float4*>(rs + kRecHeader + hd * kD + 4 * q4);
   }
+  __builtin_amdgcn_sched_barrier(0);  // the whole chunk's loads go out before the fold
 }
 
-// folds a chunk into the running (M, L, o)
+// folds a chunk into the running (M, L, o). Branch-free (selects): with a branch here the compiler
+// sinks the chunk's weight and output loads below it, a second round trip. Empty splits (M = -inf)
+// add nothing; their outputs, never written, are selected away, not multiplied by zero.
 __device__ __forceinline__ void fold_split_chunk(const SplitChunk& c, float& M, float& L, float4& o) {
   float mc = M;
 #pragma unroll
   for (int u = 0; u < kMergeUnroll; ++u) mc = fmaxf(mc, c.ms[u]);
-  if (mc == -__builtin_inff()) return;
-  const float a = exp2f(M - mc);  // M = -inf -> 0
+  const bool any = mc != -__builtin_inff();
+  const float a = any ? exp2f(M - mc) : 1.0f;  // M = -inf -> 0
   L *= a;
   o.x *= a;
   o.y *= a;
@@ -780,15 +787,15 @@ __device__ __forceinline__ void fold_split_chunk(const SplitChunk& c, float& M, 
   o.w *= a;
 #pragma unroll
   for (int u = 0; u < kMergeUnroll; ++u) {
-    if (c.ms[u] == -__builtin_inff()) continue;
-    const float w = exp2f(c.ms[u] - mc) * c.ls[u];
-    L += w;
-    o.x = __builtin_fmaf(w, c.v[u].x, o.x);
-    o.y = __builtin_fmaf(w, c.v[u].y, o.y);
-    o.z = __builtin_fmaf(w, c.v[u].z, o.z);
-    o.w = __builtin_fmaf(w, c.v[u].w, o.w);
+    const bool live = c.ms[u] != -__builtin_inff();
+    const float w = live ? exp2f(c.ms[u] - mc) * c.ls[u] : 0.0f;
+    L = live ? L + w : L;
+    o.x = live ? __builtin_fmaf(w, c.v[u].x, o.x) : o.x;
+    o.y = live ? __builtin_fmaf(w, c.v[u].y, o.y) : o.y;
+    o.z = live ? __builtin_fmaf(w, c.v[u].z, o.z) : o.z;
+    o.w = live ? __builtin_fmaf(w, c.v[u].w, o.w) : o.w;
   }
-  M = mc;
+  M = any ? mc : M;
 }
 
 // running (M, L, o) over the splits s = sg (mod 8) of one (sequence, KV head), query head hd
