@@ -18,13 +18,15 @@
  *   num_q_heads a multiple of num_kv_heads (query head j reads KV head j / G).
  * - Every array argument named "device" is device memory of the current HIP device, caller
  *   owned and 16-byte aligned. fp16 data is passed as uint16_t bit patterns (IEEE binary16).
- * - The library allocates no memory, keeps no state between calls, never synchronizes and
- *   never copies between host and device: each call validates its arguments on the host and
- *   then enqueues kernels on `stream` (a hipStream_t; NULL is the default stream).
+ * - The library allocates no memory, keeps no state between calls and (except okvq_cache_status)
+ *   never synchronizes and never copies between host and device: each call validates its
+ *   arguments on the host and then enqueues kernels on `stream` (a hipStream_t; NULL is the
+ *   default stream).
  * - Argument errors are detected before anything is enqueued: the call returns a negative
  *   status and writes nothing. A failed kernel launch returns OKVQ_ERR_HIP.
  * - Device data contract: inputs are finite and modality ids are 0, 1 or 2. Violations give
- *   unspecified (but memory-safe) results; there is no device-side error channel.
+ *   unspecified (but memory-safe) results. The one device-side error channel is the cache's
+ *   status word (seq_lens[B + 1], read by okvq_cache_status).
  * - Host "lens" arrays plan the launches; the kernels read lengths on the device where noted.
  *   Callers keep the two equal.
  *
@@ -42,8 +44,12 @@
  *   k_step   f16 [B][H][cap/32][128]  per (window, channel) step = (max - min) / 3
  *   modality u8  [B][cap]             0 audio, 1 video, 2 text
  *   k_stage  f16 [B][H][32][128]      raw keys of the open (partial) window, used by append
- *   seq_lens i32 [B + 1]              current lengths (device copy), then one word append uses as
- *                                      a work-group counter (zero initially; append leaves it zero)
+ *   seq_lens i32 [B + 2]              current lengths (device copy), then one word append uses as
+ *                                      a work-group counter (zero initially; append leaves it zero),
+ *                                      then the status word (zero initially; append sets it to 1 if
+ *                                      a wait between the value codec's waves gave up, after which
+ *                                      that append's value codes may be wrong; never cleared by
+ *                                      the library)
  * Slots of the last window beyond a sequence's length hold code 0 and norm 0.
  * Storage is 84 bytes per token per KV head: 2.625 bits per element, the "FP16 meta." row of
  * the paper's Tab. 3.
@@ -264,6 +270,14 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
 okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
                         const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
                         const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream);
+
+/* Status word of a cache (seq_lens[B + 1]): 0, or 1 once an append's value codec stopped waiting for
+ * its partner waves after a bounded number of polls and went on with incomplete tables (that
+ * append's value codes may be wrong; addresses stay in bounds). The one call of the library that
+ * synchronizes: it copies the word to the host after the work already on `stream`.
+ *   status  host i32 output
+ * OKVQ_ERR_HIP if the copy or the synchronization fails. */
+okvq_status okvq_cache_status(const okvq_cache* cache, int32_t* status, void* stream);
 
 /* Rotation tables of a layer, prepared once from v_rot (fp16, round to nearest even):
  *   bytes [0, 98304)       inverse rotation for decode (Sec. 2.3: applied once per modality after

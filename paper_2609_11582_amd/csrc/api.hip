@@ -228,7 +228,7 @@ size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
       case OKVQ_BUF_K_MIN:
       case OKVQ_BUF_K_STEP: return is_fp16(d) ? B * H * (cap / W) * D * 2 : 0;
       case OKVQ_BUF_MODALITY: return B * cap;
-      case OKVQ_BUF_SEQ_LENS: return B * 4 + 4;
+      case OKVQ_BUF_SEQ_LENS: return B * 4 + 8;
       default: return 0;
     }
   }
@@ -242,7 +242,7 @@ size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
     case OKVQ_BUF_K_MX: return is_mx(d) ? B * H * (cap / W) * kMxRecord : 0;
     case OKVQ_BUF_MODALITY: return B * cap;
     case OKVQ_BUF_K_STAGE: return B * H * W * D * 2;
-    case OKVQ_BUF_SEQ_LENS: return B * 4 + 4;  // the lengths and append's work-group counter
+    case OKVQ_BUF_SEQ_LENS: return B * 4 + 8;  // the lengths, append's work-group counter, the status word
     case OKVQ_BUF_K_RES:
     case OKVQ_BUF_V_RES: return d->residual ? B * H * OKVQ_RESIDUAL_TOKENS * D * 2 : 0;
     default: return 0;
@@ -503,10 +503,25 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
       a.rotfrag = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cache->v_rot16) + kRotInverseBytes);
       a.seq_lens_out = cache->seq_lens;
       a.ticket = reinterpret_cast<uint32_t*>(cache->seq_lens + d.batch);
+      a.status = cache->seq_lens + d.batch + 1;
       st = hip_status(launch_codec(a, true, true, s));
     }
     if (st != OKVQ_OK) return st;
   }
+  return OKVQ_OK;
+}
+
+okvq_status okvq_cache_status(const okvq_cache* cache, int32_t* status, void* stream) {
+  okvq_status st = check_cache(cache);
+  if (st != OKVQ_OK) return st;
+  if (!status) return OKVQ_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t word = 0;
+  if (hipMemcpyAsync(&word, cache->seq_lens + cache->dims.batch + 1, sizeof(word), hipMemcpyDeviceToHost, s) !=
+          hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return OKVQ_ERR_HIP;
+  *status = word;
   return OKVQ_OK;
 }
 

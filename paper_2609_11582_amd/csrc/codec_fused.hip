@@ -28,6 +28,7 @@
 // columns = output channels, lane l ends with channel 16 nb + l % 16 of four consecutive tokens:
 // one byte of the value-code layout, at offset 16 l + 8 (rb & 1) + nb of the window block.
 #include <algorithm>
+#include <cstdlib>
 
 #include "key_quant.hpp"
 #include "launch.hpp"
@@ -200,17 +201,30 @@ struct ValueShared {
   uint32_t count;             // arrivals of the value waves at their synchronization points
 };
 
-// The four value waves wait for each other (LDS counter, monotonically increasing).
-__device__ __forceinline__ void value_wave_sync(uint32_t* count, uint32_t target) {
+// The four value waves wait for each other (LDS counter, monotonically increasing). The wait is
+// bounded: after `limit` polls the wave goes on with the tables as they are (its codes may then be
+// wrong, every address stays in bounds) and the wait reports false, which the caller records in
+// the cache's status word.
+__device__ __forceinline__ bool value_wave_sync(uint32_t* count, uint32_t target, int limit) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");  // this wave's table writes are done
   if (lane_id() == 0) __hip_atomic_fetch_add(count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  for (int i = 0; i < kSpinLimit; ++i) {
+  bool arrived = false;
+  for (int i = 0; i < limit; ++i) {
     const uint32_t seen =
         __builtin_amdgcn_readfirstlane(__hip_atomic_load(count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP));
-    if (seen >= target) break;
+    if (seen >= target) {
+      arrived = true;
+      break;
+    }
     __builtin_amdgcn_s_sleep(1);
   }
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  return arrived;
+}
+
+// A value wave that gave up waiting marks the cache's status word (a plain vector store of 1).
+__device__ __forceinline__ void report_wait(const CodecArgs& a, bool arrived) {
+  if (!arrived && a.status && lane_id() == 0) *reinterpret_cast<volatile int32_t*>(a.status) = 1;
 }
 
 // The wave's slice of R_m as B operands: bf[u][kk][part] for output block nb = 2 v + u, k-block kk,
@@ -402,7 +416,7 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
       }
     }
     if (lane == 0) sh.rbm[v] = rbw;
-    value_wave_sync(&sh.count, 4 * ++syncs);
+    report_wait(a, value_wave_sync(&sh.count, 4 * ++syncs, a.spin_limit));
 
     // ---- phase 2: output channels [32 v, 32 v + 32) of all 256 tokens ----
     uint32_t rbmask[3];
@@ -456,7 +470,7 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
       for (int ww = 0; ww < 8; ++ww)
         if ((rbs >> (2 * ww)) & 3u) window(ww);
     }
-    value_wave_sync(&sh.count, 4 * ++syncs);  // the tables are read: the next tile may refill them
+    report_wait(a, value_wave_sync(&sh.count, 4 * ++syncs, a.spin_limit));  // tables read: the next tile may refill them
 
     pend = c;  // stored once the next tile's row loads are out
 #pragma unroll
@@ -522,8 +536,12 @@ hipError_t launch_prepare_fragments(const float* rot, uint4* frag, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t s) {
-  if (a.ntiles <= 0 || (!keys && !values)) return hipSuccess;
+hipError_t launch_codec(const CodecArgs& args, bool keys, bool values, hipStream_t s) {
+  if (args.ntiles <= 0 || (!keys && !values)) return hipSuccess;
+  CodecArgs a = args;
+  a.spin_limit = kSpinLimit;
+  // test hook: a smaller bound for the value waves' wait (0 makes every wait give up at once)
+  if (const char* env = getenv("OKVQ_CODEC_SPIN_LIMIT")) a.spin_limit = std::max(0, atoi(env));
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) {
     int n = 0;

@@ -16,7 +16,11 @@
 //    3 * 0x00010001 << 2j is the channel pair's codes times 2^(2j-24)); the matching power of two
 //    is folded into the B operand q'_c step_gc 2^(k0 - 2j), a packed fp16 product of a per-lane
 //    query register (zero for the other window of the pair) and the window's steps.
-//  * online softmax in base 2 (running max per head, rescaled only when it grows by 2^8);
+//  * online softmax in base 2 (running max per head, rescaled only when it grows by 2^8). The PV
+//    operand p n_v is fp16 with a per-wave power-of-two scale 2^E, E = 15 - (bound exponent of the
+//    largest value norm seen), moved lazily like the max: the largest products sit near 2^15, so
+//    weights down to about 2^-20 of the running max keep full fp16 precision and the rest (down to
+//    about 2^-30) are subnormal with an absolute error below 2^-25 of the scaled unit;
 //  * values stay rotated (Sec. 2.3): the register accumulator has rows 0-7 = audio heads and
 //    8-15 = video heads; text rows (the prompt, a few windows) are accumulated in the wave's slot
 //    of the LDS combine tile. The A operand p n_v is masked per modality with a byte-table lookup
@@ -158,6 +162,17 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// fp16 bit pattern of 2^nvb (nvb in 0..16; 2^16 maps to +inf, which no stored norm reaches).
+__device__ __forceinline__ uint32_t norm_threshold(int nvb) { return (uint32_t)(nvb + 15) << 10; }
+// Smallest nvb in [nvb0, 16] with every lane's norms (two fp16 halves of `nv`, non-negative and
+// finite) below 2^nvb. Wave-uniform; a short scalar loop.
+__device__ __forceinline__ int norm_bound(uint32_t nv, int nvb0) {
+  const uint32_t x = max(nv & 0xffffu, nv >> 16);
+  int nvb = nvb0;
+  while (nvb < 16 && __any(x >= norm_threshold(nvb))) ++nvb;
+  return nvb;
+}
+
 // Scale exponent of the fp16-subnormal code extraction for channel pair j (0..7) of a key word.
 __host__ __device__ constexpr int code_shift(int j) { return j <= 4 ? 2 * j : 2 * j - 10; }
 
@@ -284,6 +299,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   __shared__ __attribute__((aligned(16))) float wst[2][8][kDecWaves];              // [m, l][head][wave]
   __shared__ uint32_t wmask[kDecWaves];
   __shared__ uint32_t wnv[kDecWaves];  // value-norm maxima
+  __shared__ int wexp[kDecWaves];      // operand scale exponents E
   // per wave, column-major accumulator tile for the combine: [channel][row], rows 0-7 audio,
   // 8-15 video, 16-23 text heads
   __shared__ __attribute__((aligned(16))) float wacc[kDecWaves][kD][kAccPitch];
@@ -333,10 +349,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   const int nwin = (len + kW - 1) / kW;
   const int w_end = min(w_plan, nwin);
   if (w_begin >= w_end) {  // empty split (ragged batch): a header the merge skips
-    if (tid < 8) {
-      rec[tid] = -__builtin_inff();
-      rec[8 + tid] = 0.0f;
-    }
+    write_empty_record(rec, tid);
     return;
   }
 
@@ -430,6 +443,10 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   bool started = false;  // a pair has been processed (wave-uniform)
   uint32_t seen = 0;  // modalities seen by this wave
   uint32_t nvm = 0;   // largest value norm seen by this lane (two fp16 halves, non-negative)
+  // Operand scale 2^E of p n_v (wave-uniform): every value norm seen so far is below 2^nvb, so
+  // with p <= 1 the fp16 product p 2^E n_v stays below 2^15 for E = min(15, 15 - nvb). The
+  // accumulators and l_run hold 2^E times the unscaled sums; the combine divides it out.
+  int nvb = 0, E = 15;
   uint32_t* mw = &meta[wave][side][0][0];
   const float* qrow = &qs[hd][32 * g];
   // steps read for the two windows' k-blocks: the lane's own window, zeros for the other one
@@ -520,14 +537,22 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     float wmax = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
     wmax = fmaxf(wmax, fswap8(wmax));
     wmax = max32(max16(wmax));
+    // running maximum of the lane's value norms (fp16 bits), including this pair's
+    nvm = pkmax_u16(nvm, pkmax_u16(pkmax_u16(nvw[0], nvw[1]), pkmax_u16(nvw[2], nvw[3])));
     // lazy rescale: the reference m_run moves only when the max exceeds it by more than 2^8, so
-    // p = 2^(s - m_run - 8) <= 1 and p n_v fits fp16
-    if (!started) {  // first pair: nothing accumulated yet, the reference is just set
+    // p = 2^(s - m_run - 8) <= 1; the scale exponent E moves down only when a value norm reaches
+    // 2^nvb (nvb then gets one binade of headroom above the largest norm seen)
+    if (!started) {  // first pair: nothing accumulated yet, the reference and the scale are just set
       m_run = wmax;
+      nvb = min(norm_bound(nvm, 0) + 1, 16);
+      E = min(15, 15 - nvb);
       started = true;
-    } else if (__any(wmax > m_run + kLazy)) {
+    } else if (__any(wmax > m_run + kLazy) || __any(max(nvm & 0xffffu, nvm >> 16) >= norm_threshold(nvb))) {
       const float m_new = fmaxf(m_run, wmax);
-      const float alpha = fast_exp2(m_run - m_new);
+      const int nb = norm_bound(nvm, nvb);
+      const int nvb_new = nb > nvb ? min(nb + 1, 16) : nvb;
+      const int E_new = min(15, 15 - nvb_new);
+      const float alpha = fast_exp2((m_run - m_new) + (float)(E_new - E));
       l_run *= alpha;
       float arow[4];
 #pragma unroll
@@ -546,18 +571,19 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
         }
       }
       m_run = m_new;
+      nvb = nvb_new;
+      E = E_new;
     }
-    const float mref = m_run + kLazy;
+    const float mref = m_run + kLazy - (float)E;  // pr = p 2^E
     float pr[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       pr[e] = fast_exp2(s[e] - mref);
       l_run += pr[e];
     }
-    uint32_t pv[4];  // p n_v (fp16 pairs), tokens (4g, 4g+1), (4g+2, 4g+3), (16+4g, ..), (16+4g+2, ..)
+    uint32_t pv[4];  // p 2^E n_v (fp16 pairs), tokens (4g, 4g+1), (4g+2, 4g+3), (16+4g, ..), (16+4g+2, ..)
 #pragma unroll
     for (int q = 0; q < 4; ++q) pv[q] = pk_mul(pack_f16(pr[2 * q], pr[2 * q + 1]), nvw[q]);
-    nvm = pkmax_u16(nvm, pkmax_u16(pkmax_u16(nvw[0], nvw[1]), pkmax_u16(nvw[2], nvw[3])));
 
     // ---- modalities present (wave-uniform) and the v_perm selectors of the token pairs ----
     uint32_t pres = __builtin_amdgcn_perm(kTabBits, kTabBits, md[0]) | __builtin_amdgcn_perm(kTabBits, kTabBits, md[1]);
@@ -645,11 +671,12 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   }
   if (lane < 8) {
     wst[0][lane][wave] = m_run;
-    wst[1][lane][wave] = l_run;
+    wst[1][lane][wave] = ldexpf(l_run, -E);  // relative to 2^(m_run + kLazy)
   }
   if (lane == 0) {
     wmask[wave] = seen;
     wnv[wave] = max(nvm & 0xffffu, nvm >> 16);
+    wexp[wave] = E;
   }
 #pragma unroll
   for (int nb = 0; nb < 8; ++nb)  // rows 4g .. 4g + 3 of set 1 (audio, video heads), channel 16 nb + col
@@ -667,7 +694,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   // 2^e / L with e = 15 - ilogb(n_max) keeps the fp16 A tile below 2^13.
   const float nmf = h2f(nmax);
   const int e = (nmf > 0.0f) ? 15 - min(max(ilogbf(nmf), -30), 20) : 0;
-  // factor table fac[head][wave] = 2^(m_w - M) 2^e / L (zero for heads >= G and empty waves):
+  // factor table fac[head][wave] = 2^(m_w - M - E_w) 2^e / L (zero for heads >= G and empty waves):
   // one thread per (head, wave)
   if (tid < 8 * kDecWaves) {
     const int hh = tid >> 3, w = tid & 7;
@@ -684,7 +711,8 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 #pragma unroll
     for (int u = 0; u < kDecWaves; ++u) L += (mv[u] == -__builtin_inff()) ? 0.0f : lv[u] * fast_exp2(mv[u] - M);
     const float sc = (hh < p.G && L > 0.0f) ? ldexpf(1.0f / L, e) : 0.0f;
-    fac[hh][w] = (mv[w] == -__builtin_inff()) ? 0.0f : fast_exp2(mv[w] - M) * sc;
+    // the wave's accumulators carry its operand scale 2^E_w
+    fac[hh][w] = (mv[w] == -__builtin_inff()) ? 0.0f : fast_exp2(mv[w] - M - (float)wexp[w]) * sc;
     if (w == 0) {
       rec[hh] = M;
       rec[8 + hh] = L;
@@ -743,7 +771,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 // ---- merge over splits: o = sum_s 2^(M_s - M) L_s o_s / sum_s 2^(M_s - M) L_s (log-sum-exp) ----
 // One work-group of 256 threads per (query head j, sequence b): thread (split group sg, channel
 // quad q4) sums the splits s = sg (mod 8). Every load is issued before any is used; empty splits
-// carry M = -inf and are skipped (their outputs were never written). A record's L is relative to
+// carry M = -inf and are skipped (their outputs are zeros). A record's L is relative to
 // 2^(M + kLazy) (the split kernel's lazily updated reference).
 constexpr int kMergeThreads = 256;
 constexpr int kMergeUnroll = 8;  // splits per thread held in registers at once
@@ -773,7 +801,8 @@ __device__ __forceinline__ void load_split_chunk(const float* base, int nsplit, 
 
 // folds a chunk into the running (M, L, o). Branch-free (selects): with a branch here the compiler
 // sinks the chunk's weight and output loads below it, a second round trip. Empty splits (M = -inf)
-// add nothing; their outputs, never written, are selected away, not multiplied by zero.
+// add nothing: their weight is selected to zero and their outputs are zeros (records past nsplit,
+// read through the clamped index, are selected away).
 __device__ __forceinline__ void fold_split_chunk(const SplitChunk& c, float& M, float& L, float4& o) {
   float mc = M;
 #pragma unroll

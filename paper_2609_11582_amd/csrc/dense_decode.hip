@@ -75,10 +75,7 @@ __global__ __launch_bounds__(64 * kDnWaves) void k_decode_dense(DenseArgs p) {
   const int t_begin = split * p.tps, t_end = min(t_begin + p.tps, len);
   float* rec = p.ws + (((size_t)b * p.H + h) * p.nsplit + split) * kRecFloats;
   if (t_begin >= t_end) {  // an empty split: the merge skips M = -inf
-    if (tid < 8) {
-      rec[tid] = -__builtin_inff();
-      rec[8 + tid] = 0.0f;
-    }
+    write_empty_record(rec, tid);
     return;
   }
   const size_t seq = (size_t)b * p.H + h;

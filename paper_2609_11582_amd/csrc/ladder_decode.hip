@@ -40,6 +40,14 @@ constexpr int kLStep = kLw * kW;         // tokens per work-group step
 constexpr int kATileL = 3 * kD + 8;      // fp16 row pitch of the un-rotation A tile
 constexpr float kLazyL = 8.0f;           // log2 headroom of the lazily updated softmax reference
 
+// Smallest nvb in [nvb0, 16] with every lane's value norm bound `nv` (finite, below 2^16) under
+// 2^nvb. Wave-uniform; a short scalar loop.
+__device__ __forceinline__ int norm_bound_f(float nv, int nvb0) {
+  int nvb = nvb0;
+  while (nvb < 16 && __any(nv >= ldexpf(1.0f, nvb))) ++nvb;
+  return nvb;
+}
+
 __device__ __forceinline__ half8 h8(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
   return __builtin_bit_cast(half8, make_uint4(a, b, c, d));
 }
@@ -82,6 +90,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   __shared__ __attribute__((aligned(16))) _Float16 atile[8][kATileL];
   __shared__ float wst[2][8][kLw];
   __shared__ uint32_t wmask[kLw], wnv[kLw];
+  __shared__ int wexp[kLw];
   __shared__ __attribute__((aligned(16))) float fac[8][kLw];
   __shared__ __attribute__((aligned(16))) float ttx[kLw][kD][8];  // text rows (heads 0-7) per wave
   __shared__ float amax_w[4];
@@ -103,10 +112,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   const size_t seq = (size_t)b * p.H + h;
   float* rec = p.ws + (seq * p.nsplit + split) * kRecFloats;
   if (t_begin >= t_end) {
-    if (tid < 8) {
-      rec[tid] = -__builtin_inff();
-      rec[8 + tid] = 0.0f;
-    }
+    write_empty_record(rec, tid);
     return;
   }
   const uint8_t* kbase = p.k_codes + seq * p.cap * kKRow;
@@ -245,6 +251,10 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   }
   float m_run = -__builtin_inff(), l_part = 0.0f, nvmax = 0.0f;
   bool started = false;
+  // Operand scale 2^E of p n_v (wave-uniform): every value norm seen is below 2^nvb, so with
+  // p <= 1 the product p 2^E n_v stays below 2^15 for E = min(15, 15 - nvb); l_part and the
+  // accumulators hold 2^E times the unscaled sums (the combine divides it out).
+  int nvb = 0, E = 15;
   uint32_t seen = 0;
   uint8_t* vtw = &vt[wave][0];
   const int trow = 4 * g + (r >> 2), tsub = r & 3;
@@ -322,12 +332,21 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
+    float nvl = 0.0f;  // the lane's largest value norm so far, this window's included
+#pragma unroll
+    for (int e = 0; e < 8; ++e) nvl = fmaxf(nvl, nvf[e]);
+    nvmax = fmaxf(nvmax, nvl);
     if (!started) {
       m_run = mx;
+      nvb = min(norm_bound_f(nvmax, 0) + 1, 16);
+      E = min(15, 15 - nvb);
       started = true;
-    } else if (__any(mx > m_run + kLazyL)) {
+    } else if (__any(mx > m_run + kLazyL) || __any(nvmax >= ldexpf(1.0f, nvb))) {
       const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      const int nb = norm_bound_f(nvmax, nvb);
+      const int nvb_new = nb > nvb ? min(nb + 1, 16) : nvb;
+      const int E_new = min(15, 15 - nvb_new);
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) + (float)(E_new - E));
       l_part *= alpha;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {  // accumulator rows 4 g + i are heads (4 g + i) mod 8
@@ -347,15 +366,16 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
         }
       }
       m_run = m_new;
+      nvb = nvb_new;
+      E = E_new;
     }
-    const float mref = m_run + kLazyL;  // p = 2^(s - mref) <= 1: p n_v fits fp16
+    const float mref = m_run + kLazyL - (float)E;  // pe = p 2^E with p = 2^(s - m_run - 8) <= 1
     float pv[8], pp[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float pe = __builtin_amdgcn_exp2f(x[e] - mref);  // 0 for no token
       l_part += pe;
-      pv[e] = pe * nvf[e];
-      nvmax = fmaxf(nvmax, nvf[e]);
+      pv[e] = pe * nvf[e];  // below 2^15: fits fp16
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) pp[e] = dpp_ror8(pv[e]);  // heads r - 8 for the video rows
@@ -444,11 +464,12 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
         make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
   if (lane < 8) {
     wst[0][lane][wave] = started ? m_run : -__builtin_inff();
-    wst[1][lane][wave] = l_tot;
+    wst[1][lane][wave] = ldexpf(l_tot, -E);  // relative to 2^(m_run + kLazyL)
   }
   if (lane == 0) {
     wmask[wave] = seen;
     wnv[wave] = __builtin_bit_cast(uint32_t, nvw);
+    wexp[wave] = E;
   }
   __syncthreads();
   uint32_t mask = 0;
@@ -471,7 +492,10 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     for (int u = 0; u < kLw; ++u)
       L += (wst[0][hh][u] == -__builtin_inff()) ? 0.0f : wst[1][hh][u] * __builtin_amdgcn_exp2f(wst[0][hh][u] - M);
     const float scl = (hh < p.G && L > 0.0f) ? ldexpf(1.0f / L, e) : 0.0f;
-    fac[hh][w] = (wst[0][hh][w] == -__builtin_inff()) ? 0.0f : __builtin_amdgcn_exp2f(wst[0][hh][w] - M) * scl;
+    // the wave's accumulators carry its operand scale 2^E_w
+    fac[hh][w] = (wst[0][hh][w] == -__builtin_inff())
+                     ? 0.0f
+                     : __builtin_amdgcn_exp2f(wst[0][hh][w] - M - (float)wexp[w]) * scl;
     if (w == 0) {
       rec[hh] = M;
       rec[8 + hh] = L;

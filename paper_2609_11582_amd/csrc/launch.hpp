@@ -62,6 +62,10 @@ struct CodecArgs {
   // sequences; `ticket` counts finished work-groups and is returned to zero
   int32_t* seq_lens_out;
   uint32_t* ticket;
+  // append: status word set to 1 if a value wave stops waiting for the others (kSpinLimit polls,
+  // or the host override below) and goes on with the tables it has; null for the stateless calls
+  int32_t* status;
+  int spin_limit;  // polls of a value-wave wait before it gives up (set by launch_codec)
 };
 hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t s);
 hipError_t launch_prepare_fragments(const float* rot, uint4* frag, hipStream_t s);
@@ -109,6 +113,16 @@ struct CacheView {
 constexpr int kRecHeader = 32;
 constexpr int kRecFloats = kRecHeader + 8 * kD;
 constexpr int kMaxSplits = 1024;  // most splits per (sequence, KV head)
+
+// Record of a split with no tokens (ragged batches): M = -inf, L = 0 and zero outputs, so the
+// merge never reads memory this launch did not write. Threads tid < 256 of the work-group call it.
+__device__ __forceinline__ void write_empty_record(float* rec, int tid) {
+  if (tid < 8) {
+    rec[tid] = -__builtin_inff();
+    rec[8 + tid] = 0.0f;
+  }
+  if (tid < 8 * kD / 4) reinterpret_cast<float4*>(rec + kRecHeader)[tid] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
 
 struct DecodePlan {
   int wins_per_split;  // 32-token windows per split-K work-group

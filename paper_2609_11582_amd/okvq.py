@@ -81,6 +81,8 @@ def lib() -> ctypes.CDLL:
         L.okvq_quantize_values.argtypes = [P(Dims), vp, vp, i32, P(i32), vp, u32, vp, vp, vp]
         L.okvq_append.restype = i32
         L.okvq_append.argtypes = [P(CacheStruct), P(i32), vp, vp, vp, P(i32), vp, i32, u32, vp]
+        L.okvq_cache_status.restype = i32
+        L.okvq_cache_status.argtypes = [P(CacheStruct), P(i32), vp]
         L.okvq_prepare_rotation.restype = i32
         L.okvq_prepare_rotation.argtypes = [vp, vp, vp]
         L.okvq_decode_workspace_bytes.restype = sz
@@ -250,6 +252,15 @@ def okvq_append(cache: "KVCache", lens, k_new, v_new, mod_new, n_new, n_new_dev,
     if check:
         _check(st, "okvq_append")
     return st
+
+
+def okvq_cache_status(cache: "KVCache", stream=None) -> int:
+    """The cache's status word (seq_lens[B + 1]): 0, or 1 once an append's value codec gave up
+    waiting for its partner waves (that append's value codes may be wrong). Synchronizes `stream`."""
+    word = ctypes.c_int32(-1)
+    _check(lib().okvq_cache_status(ctypes.byref(cache.struct), ctypes.byref(word), _stream(stream)),
+           "okvq_cache_status")
+    return int(word.value)
 
 
 def okvq_prepare_rotation(v_rot, v_rot16, stream=None, check=True) -> int:

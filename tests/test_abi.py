@@ -105,6 +105,13 @@ def test_invalid_arguments_rejected_before_any_launch():
     assert L.okvq_decode_attention(ctypes.byref(no_table), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, 1 << 30,
                                    None) == -1
     assert L.okvq_prepare_rotation(fake, ctypes.c_void_p(4098), None) == -1
+    # the status query checks the cache and its output pointer before touching the device
+    word = ctypes.c_int32(7)
+    assert L.okvq_cache_status(ctypes.byref(null_cache), ctypes.byref(word), None) == -1
+    assert L.okvq_cache_status(ctypes.byref(cache), None, None) == -1
+    assert word.value == 7
+    # seq_lens holds the lengths, append's work-group counter and the status word
+    assert okvq.okvq_buffer_bytes(ok_dims, 8) == 4 * ok_dims.batch + 8
 
 
 def test_mxfp4_metadata_buffers_and_validation():

@@ -141,3 +141,29 @@ def test_append_and_decode_beyond_256_sequences():
     dec = decode_layer(got, q, np.asarray(lens), lay["signs"], lay["rot"], 1 / math.sqrt(128),
                        heads={(b, 0) for b in (0, 1, 255, 256, 299)})
     assert gh.attention_close(out, dec) <= 2e-3
+
+
+def test_append_reports_a_value_wait_that_gave_up(monkeypatch):
+    """The value codec's waves wait for each other with a bounded number of polls. Forced from the
+    host to give up at once (OKVQ_CODEC_SPIN_LIMIT=0, no poll), every kernel still ends normally and
+    the append marks the cache's status word; a normal append leaves it at zero."""
+    import torch
+
+    import gpu_helpers as gh
+    import paper_2609_11582_amd as okvq
+    wl = workload("omni7b_32k")
+    lens = [700, 300]
+    lay = gen_layer(wl, 0, lengths=np.asarray(lens, np.int32), n_tokens=max(lens))
+    k, v = lay["k"][:, :2].copy(), lay["v"][:, :2].copy()
+    cache = gh.new_cache(2, 2, 14, 1024, lay["signs"], lay["rot"])
+    print("[gpu-case] append, normal wait", flush=True)
+    gh.append_chunks(cache, k, v, lay["modality"], lens, [[256, 256]])
+    assert okvq.okvq_cache_status(cache) == 0
+    monkeypatch.setenv("OKVQ_CODEC_SPIN_LIMIT", "0")
+    print("[gpu-case] append, wait bound 0", flush=True)
+    cur = gh.append_chunks_from(cache, k, v, lay["modality"], [256, 256], [444, 44])
+    torch.cuda.synchronize()
+    assert list(cur) == lens
+    assert cache.views()["seq_lens"].cpu().tolist() == lens      # the lengths still advanced
+    assert okvq.okvq_cache_status(cache) == 1
+    assert int(cache["seq_lens"][2].item()) == 0                 # the work-group counter is back at zero

@@ -95,12 +95,28 @@ def test_fwht_f32_close_to_f64():
     assert np.all(np.abs(a - b) <= bound)
 
 
-@pytest.mark.parametrize("d", [128])
-def test_fwht_butterfly_order_is_h_ascending(d):
-    # with h ascending the first stage combines neighbours: for x = e_0 + e_1 the output is 2 at
-    # even columns of Had and 0 at odd ones after every stage (Had[:,0] + Had[:,1])
+def test_fwht_butterfly_order_is_h_ascending():
+    """x = e_0 + e_1 + 2^-24 e_2, hand-worked. With h ascending the first stage pairs neighbours:
+    w_0 = 2, w_1 = 0 (exact cancellation), w_2 = w_3 = 2^-24; every later stage adds exact values,
+    so each odd row i ends at Had[i, 2] 2^-24 exactly and each even row at 2 Had[i, 0] (2 + 2^-24
+    rounds back to 2). With h descending, x_0 and x_2 meet first (h = 2): 1 + 2^-24 is a tie and
+    rounds to 1 (even), so the rows where they add lose the 2^-24 before x_1 cancels the 1: those
+    odd rows end at 0, not +-2^-24."""
+    d = 128
     x = np.zeros(d, np.float32)
     x[0] = 1
     x[1] = 1
-    ref = scipy.linalg.hadamard(d)[:, 0] + scipy.linalg.hadamard(d)[:, 1]
-    np.testing.assert_array_equal(fwht_f32(x), ref.astype(np.float32))
+    x[2] = 2.0 ** -24
+    had = scipy.linalg.hadamard(d)
+    want = np.where(np.arange(d) % 2 == 1, had[:, 2] * 2.0 ** -24, 2.0 * had[:, 0]).astype(np.float32)
+    got = fwht_f32(x)
+    np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+    # the same butterflies with h descending give other bits
+    w = x.copy()
+    for h in (64, 32, 16, 8, 4, 2, 1):
+        v = w.reshape(d // (2 * h), 2, h)
+        a, b = v[:, 0, :].copy(), v[:, 1, :].copy()
+        v[:, 0, :], v[:, 1, :] = a + b, a - b
+        w = v.reshape(d)
+    assert not np.array_equal(w.view(np.uint32), got.view(np.uint32))
+    assert np.all(w[1::2][had[1::2, 2] > 0] == 0)
