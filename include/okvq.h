@@ -313,6 +313,19 @@ okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_h
                                   float sm_scale, uint32_t flags, float* out, void* workspace,
                                   size_t workspace_bytes, void* stream);
 
+/* okvq_decode_attention for callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): the same decode, with the split records in a
+ * static device array of OKVQ_NOALLOC_SCRATCH_BYTES on each GPU (held until the process ends)
+ * instead of a caller workspace. No hipMalloc, hipFree or other allocation happens in the call;
+ * its first call on a GPU looks up that GPU's array address once. Every call on a GPU shares the
+ * array: calls that overlap on one GPU (other streams, other threads) race and give wrong results.
+ * The array needs no initial contents.
+ * OKVQ_ERR_WORKSPACE if this call's split records (sequences x KV heads x splits of its plan,
+ * 4224 bytes each; about 256 + B H records by default) exceed the array. */
+#define OKVQ_NOALLOC_SCRATCH_BYTES (4u << 20)
+okvq_status okvq_decode_attention_noalloc(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,
+                                          float sm_scale, uint32_t flags, float* out, void* stream);
+
 /* okvq_decode_attention that also times its two launches: events[0] and events[1] are recorded
  * at the start and end of the split-K kernel's execution, events[2] and events[3] at those of
  * the merge kernel (hipEvent_t handles created by the caller; hipEventElapsedTime of a pair is

@@ -3,6 +3,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <numeric>
 #include <vector>
 
@@ -11,7 +12,32 @@
 
 using namespace okvq;
 
+// Split records of okvq_decode_attention_noalloc: one array per GPU, held until the process ends.
+// In host code `scratch` names a host-side stand-in; its device address on each GPU comes from
+// hipGetSymbolAddress (scratch_address below) and is the only form passed to kernels.
+static __device__ __align__(256) float scratch[OKVQ_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+
+// Device address of `scratch` on the current device, looked up once per device (with that device
+// current) and kept; later calls on the device reuse it.
+okvq_status scratch_address(void** out) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return OKVQ_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return OKVQ_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return OKVQ_ERR_HIP;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return OKVQ_OK;
+}
 
 constexpr int32_t kVersion = 600;  // 0.6.0: bit-width ladder (b-bit keys and values)
 
@@ -540,9 +566,11 @@ size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len) {
   return decode_workspace_bytes(dims->batch, dims->num_kv_heads, dims->num_q_heads, max_seq_len);
 }
 
+// workspace == nullptr with workspace_bytes == 0 selects the static per-GPU scratch array (the
+// allocation-free entry point): the records of this call's plan must fit in it.
 static okvq_status decode_impl(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q, float sm_scale,
                                uint32_t flags, float* out, void* workspace, size_t workspace_bytes, void* stream,
-                               void* const* events) {
+                               void* const* events, bool use_scratch = false) {
   okvq_status st = check_cache(cache);
   if (st != OKVQ_OK) return st;
   if (!lens_host || flags != 0 || !std::isfinite(sm_scale)) return OKVQ_ERR_INVALID_ARGUMENT;
@@ -554,9 +582,18 @@ static okvq_status decode_impl(const okvq_cache* cache, const int32_t* lens_host
     if (lens_host[b] > d.capacity) return OKVQ_ERR_CAPACITY;
     max_len = std::max(max_len, lens_host[b]);
   }
-  const size_t need = is_ladder(&d) ? ladder_workspace_bytes(d.batch, d.num_kv_heads, max_len)
-                                    : decode_workspace_bytes(d.batch, d.num_kv_heads, d.num_q_heads, max_len);
-  if (!aligned16(workspace) || workspace_bytes < need) return OKVQ_ERR_WORKSPACE;
+  if (use_scratch) {  // the records of this call's plan, in the static array
+    const size_t nsplit = is_ladder(&d) ? plan_ladder(d.batch, d.num_kv_heads, max_len).nsplit
+                                        : plan_decode(d.batch, d.num_kv_heads, std::max(max_len - d.residual, 0)).nsplit;
+    if ((size_t)d.batch * d.num_kv_heads * nsplit * kRecFloats * sizeof(float) > OKVQ_NOALLOC_SCRATCH_BYTES)
+      return OKVQ_ERR_WORKSPACE;
+    st = scratch_address(&workspace);
+    if (st != OKVQ_OK) return st;
+  } else {
+    const size_t need = is_ladder(&d) ? ladder_workspace_bytes(d.batch, d.num_kv_heads, max_len)
+                                      : decode_workspace_bytes(d.batch, d.num_kv_heads, d.num_q_heads, max_len);
+    if (!aligned16(workspace) || workspace_bytes < need) return OKVQ_ERR_WORKSPACE;
+  }
   hipEvent_t ev[4];
   if (events) {
     for (int i = 0; i < 4; ++i) {
@@ -603,6 +640,11 @@ static okvq_status decode_impl(const okvq_cache* cache, const int32_t* lens_host
 okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q, float sm_scale,
                                   uint32_t flags, float* out, void* workspace, size_t workspace_bytes, void* stream) {
   return decode_impl(cache, lens_host, q, sm_scale, flags, out, workspace, workspace_bytes, stream, nullptr);
+}
+
+okvq_status okvq_decode_attention_noalloc(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,
+                                          float sm_scale, uint32_t flags, float* out, void* stream) {
+  return decode_impl(cache, lens_host, q, sm_scale, flags, out, nullptr, 0, stream, nullptr, true);
 }
 
 okvq_status okvq_decode_attention_timed(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,

@@ -27,6 +27,7 @@ KEY_META = {"fp16": OKVQ_KEY_META_FP16, "mxfp4": OKVQ_KEY_META_MXFP4, "turboquan
 ROTATION_TABLE_BYTES = 294912  # OKVQ_ROTATION_TABLE_BYTES
 MX_RECORD_BYTES = 136  # one MXFP4 key-metadata record per 32-token window
 RESIDUAL_TOKENS = 128  # OKVQ_RESIDUAL_TOKENS: fp16 window of the captioning protocol
+NOALLOC_SCRATCH_BYTES = 4 << 20  # OKVQ_NOALLOC_SCRATCH_BYTES: split records of the allocation-free decode
 # buffer ids 0..11 of okvq_buffer_bytes (OKVQ_BUF_*)
 BUFFERS = ("k_codes", "v_codes", "k_norm", "v_norm", "k_min", "k_step", "modality", "k_stage", "seq_lens", "k_mx",
            "k_res", "v_res")
@@ -89,6 +90,8 @@ def lib() -> ctypes.CDLL:
         L.okvq_decode_workspace_bytes.argtypes = [P(Dims), i32]
         L.okvq_decode_attention.restype = i32
         L.okvq_decode_attention.argtypes = [P(CacheStruct), P(i32), vp, ctypes.c_float, u32, vp, vp, sz, vp]
+        L.okvq_decode_attention_noalloc.restype = i32
+        L.okvq_decode_attention_noalloc.argtypes = [P(CacheStruct), P(i32), vp, ctypes.c_float, u32, vp, vp]
         L.okvq_decode_attention_timed.restype = i32
         L.okvq_decode_attention_timed.argtypes = [P(CacheStruct), P(i32), vp, ctypes.c_float, u32, vp, vp, sz, vp,
                                                   P(vp)]
@@ -294,6 +297,20 @@ def okvq_decode_attention(cache: "KVCache", lens, q, sm_scale, out, workspace, w
                                      _ptr(out), _ptr(workspace), int(nbytes), _stream(stream))
     if check:
         _check(st, "okvq_decode_attention")
+    return st
+
+
+def okvq_decode_attention_noalloc(cache: "KVCache", lens, q, sm_scale, out, flags=0, stream=None, check=True) -> int:
+    """okvq_decode_attention with the split records in the library's static per-GPU array
+    (NOALLOC_SCRATCH_BYTES): no workspace argument, no allocation in the call."""
+    B, Hq = cache.dims.batch, cache.dims.num_q_heads
+    _need_len(lens, B, "lens")
+    _need(q, B * Hq * 128 * 2, "q")
+    _need(out, B * Hq * 128 * 4, "out")
+    st = lib().okvq_decode_attention_noalloc(ctypes.byref(cache.struct), _i32(lens), _ptr(q), float(sm_scale),
+                                             int(flags), _ptr(out), _stream(stream))
+    if check:
+        _check(st, "okvq_decode_attention_noalloc")
     return st
 
 

@@ -110,6 +110,15 @@ def test_invalid_arguments_rejected_before_any_launch():
     assert L.okvq_cache_status(ctypes.byref(null_cache), ctypes.byref(word), None) == -1
     assert L.okvq_cache_status(ctypes.byref(cache), None, None) == -1
     assert word.value == 7
+    # the allocation-free decode rejects plans whose split records exceed its static array, on the host
+    big = okvq.make_dims(256, 8, 64, 1024)
+    big_cache = okvq.CacheStruct(big, *([4096] * 9), 4096, 4096, 4096)
+    big_lens = (ctypes.c_int32 * 256)(*([1000] * 256))
+    assert 256 * 8 * 4224 > okvq.NOALLOC_SCRATCH_BYTES
+    assert L.okvq_decode_attention_noalloc(ctypes.byref(big_cache), big_lens, fake, ctypes.c_float(0.1), 0, fake,
+                                           None) == -4
+    assert L.okvq_decode_attention_noalloc(ctypes.byref(no_table), q_lens, fake, ctypes.c_float(0.1), 0, fake,
+                                           None) == -1
     # seq_lens holds the lengths, append's work-group counter and the status word
     assert okvq.okvq_buffer_bytes(ok_dims, 8) == 4 * ok_dims.batch + 8
 
