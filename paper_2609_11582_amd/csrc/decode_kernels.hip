@@ -2,31 +2,36 @@
 //
 // Split-K flash decoding in two launches. k_decode: work-group (split, KV head h, sequence b) =
 // 8 waves; wave w takes the split's window pairs (2w + 16k, 2w + 16k + 1) and keeps its own
-// online-softmax state. The waves are combined in LDS, the split's per-modality accumulators are
-// un-rotated on MFMA (the inverse rotation is linear, so applying it per split and then merging
-// equals applying it once per modality after aggregation, Sec. 2.3) and one normalized partial
-// output per split is written. k_decode_merge combines the splits by log-sum-exp.
+// online-softmax state. Each wave streams its pairs through three LDS slots filled by direct
+// memory-to-LDS loads two pairs ahead of the one it computes. The waves are combined in LDS, the
+// split's per-modality accumulators are un-rotated on MFMA (the inverse rotation is linear, so
+// applying it per split and then merging equals applying it once per modality after aggregation,
+// Sec. 2.3) and one normalized partial output per split is written. k_decode_merge combines the
+// splits by log-sum-exp.
 //
 // What one wave does per window pair (all G <= 8 query heads of the KV head from one read):
 //  * scores in the rotated key space (Sec. 2.3): s_i = n_i (q'.m_g + sum_c q'_c step_gc code_ic),
-//    q' = H q sm_scale log2(e) computed once per work-group. The bias q'.m_g is an fp32 dot
-//    product; the code term is an MFMA block-diagonal over the pair: rows = 16 tokens, columns
-//    0-7 = heads for window A and 8-15 = the same heads for window B, K = 256 = the two windows'
-//    128 channels. Codes enter the MFMA unchanged as fp16 subnormals (a key code word masked with
-//    3 * 0x00010001 << 2j is the channel pair's codes times 2^(2j-24)); the matching power of two
-//    is folded into the B operand q'_c step_gc 2^(k0 - 2j), a packed fp16 product of a per-lane
-//    query register (zero for the other window of the pair) and the window's steps.
-//  * online softmax in base 2 (running max per head, rescaled only when it grows by 2^8). The PV
-//    operand p n_v is fp16 with a per-wave power-of-two scale 2^E, E = 15 - (bound exponent of the
-//    largest value norm seen), moved lazily like the max: the largest products sit near 2^15, so
-//    weights down to about 2^-20 of the running max keep full fp16 precision and the rest (down to
-//    about 2^-30) are subnormal with an absolute error below 2^-25 of the scaled unit;
-//  * values stay rotated (Sec. 2.3): the register accumulator has rows 0-7 = audio heads and
-//    8-15 = video heads; text rows (the prompt, a few windows) are accumulated in the wave's slot
-//    of the LDS combine tile. The A operand p n_v is masked per modality with a byte-table lookup
-//    (v_perm) and the two row halves exchange window halves with one DPP row rotation under a
-//    bank mask. B operands come from a 256-entry LDS table mapping a code byte (one channel,
-//    four tokens) to four fp16 codebook values.
+//    q' = H q sm_scale log2(e) computed once per work-group. The bias q'.m_g of both windows is
+//    one MFMA chain (minima as A rows, q' split into fp16 hi and lo columns); the code term is
+//    an MFMA per window and 16-token tile: rows = tokens, columns 0-7 = heads (the side-0 lanes
+//    keep window A's products), 8-15 = the same heads for window B (side-1 lanes), K = the
+//    window's 128 channels. Codes enter the MFMA unchanged as fp16 subnormals (a key code word
+//    masked with 3 * 0x00010001 << 2j is the channel pair's codes times 2^(2j-24)); the
+//    matching power of two is folded into the B operand q'_c step_gc 2^(k0 - 2j), a packed fp16
+//    product of a per-lane query register and the lane's window steps.
+//  * online softmax in base 2 (running max per head, rescaled only when it grows by 2^8; scores
+//    are formed relative to the current reference, so the exponent needs no subtraction). The
+//    PV operand p n_v is fp16 with a per-wave power-of-two scale 2^E, E = 15 - (bound exponent
+//    of the largest value norm seen), moved lazily like the max: the largest products sit near
+//    2^15, so weights down to about 2^-20 of the running max keep full fp16 precision and the
+//    rest (down to about 2^-30) are subnormal with an absolute error below 2^-25 of the scaled
+//    unit;
+//  * values stay rotated (Sec. 2.3): one register accumulator has rows 0-7 = audio heads and
+//    8-15 = video heads, a second one rows 0-7 = text heads (the prompt, a few windows). A pair
+//    of one modality takes its rows straight from p n_v; a mixed pair masks them per token with
+//    a byte-table lookup (v_perm), and the two row halves exchange window halves with one DPP
+//    row rotation under a bank mask. B operands come from a 256-entry LDS table mapping a code
+//    byte (one channel, four tokens) to four fp16 codebook levels.
 #include <hip/hip_ext.h>
 
 #include <algorithm>
@@ -191,19 +196,54 @@ __device__ __forceinline__ half8 key_a_operand(uint2 w, int kk) {
 constexpr uint32_t kTabAudio = 0x000000ffu, kTabVideo = 0x0000ff00u, kTabText = 0x00ff0000u;
 constexpr uint32_t kTabBits = 0x00040201u;  // byte m -> 1 << m (presence bits)
 
-// Loads of one window pair (A = wA, B = wA + 1) for one lane. Lanes 0-7 of every row of 16 score
-// window A, lanes 8-15 window B ("side"); both sides need both windows' key codes (the score MFMA
-// is block-diagonal over the pair) and value codes (one PV MFMA per window). A window beyond the
-// split re-reads window A: its tokens are masked as invalid, so its contents never matter.
-struct PairLoad {
-  uint2 ka0, ka1, kb0, kb1;  // key codes of tokens r and 16 + r of windows A, B (bytes 8g .. 8g+7)
-  uint4 va, vb;              // value codes of windows A, B (the lane's 16 bytes of each block)
-  uint2 nk0, nk1;            // key norms of the side window, tokens 4g .. 4g+3 and 16+4g .. 16+4g+3
-  uint2 nv0, nv1;            // value norms of the same tokens
-  uint32_t md0, md1;         // modality ids of the same tokens
-  uint2 stp, mnp;            // step / min of channels 32g + 4 (col % 8) .. +3 of the side window
-                             // (MXFP4: stp.x = their record word, stp.y = block g's scale bytes)
-};
+// ---- the pair ring: each wave streams its window pairs through three LDS slots, filled by direct
+// memory-to-LDS loads two pairs ahead of the one it computes. No register holds a pair in flight,
+// so the loads of two pairs per wave stay outstanding while the third is computed. The loads are
+// issued from inline assembly: the compiler's wait-count model would otherwise make every read of
+// the ring wait for all of them; the kernel counts its own loads instead (every one of them is a
+// ring load, issued in a fixed number per pair) and waits with explicit vmcnt values. ----
+constexpr int kRingSlots = 3;
+constexpr int kSlotBytes = 6144;
+// byte offsets in a slot: key codes of window A and B (32 tokens x 32 bytes each), value codes of A
+// and B (the window's 1024-byte block), metadata, then norms and modality ids
+constexpr int kChKA = 0, kChKB = 1024, kChVA = 2048, kChVB = 3072, kChMeta = 4096, kChSmall = 5120;
+// the small chunk: key norms of A (64 bytes) and B, value norms of A and B, modality ids of A (32
+// bytes) and B
+constexpr int kSmKn = 0, kSmVn = 128, kSmMd = 256;
+// fp16 steps (window A then B, 256 bytes each) and minima: where the metadata chunk holds them for
+// fp16 metadata, and where decoded MXFP4 records are written (after the records, 272 bytes)
+template <int kMeta> constexpr int kStepOff = kMeta == kMetaMx ? kChMeta + 512 : kChMeta;
+template <int kMeta> constexpr int kMinOff = kMeta == kMetaMx ? kChSmall + 512 : kChMeta + 512;
+// ring loads per pair: four code blocks, the small chunk, and the metadata (one 16-byte load per
+// lane for fp16, two 4-byte loads for the 272 bytes of two MXFP4 records, none for TurboQuant keys)
+template <int kMeta> constexpr int kPairLoads = kMeta == kMetaFp16 ? 6 : kMeta == kMetaMx ? 7 : 5;
+
+// lane's 16 bytes at g go to LDS lds + 16 lane (lds wave-uniform, passed in m0; an LDS load needs
+// one wait state after m0 is written)
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  __asm__ volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds) : "memory");
+}
+// lane's 16 bytes at base + off go to LDS lds + 16 lane (base and lds wave-uniform)
+__device__ __forceinline__ void dma16s(const void* base, uint32_t off, uint32_t lds) {
+  __asm__ volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
+}
+// lane's 4 bytes at g go to LDS lds + 4 lane
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds) {
+  __asm__ volatile("s_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "{m0}"(lds) : "memory");
+}
+// waits until at most n ring loads of this wave are outstanding (n a multiple of the per-pair
+// count, 0..2 pairs)
+template <int kMeta>
+__device__ __forceinline__ void ring_wait(int newer_pairs) {
+  constexpr int c = kPairLoads<kMeta>;
+  if (newer_pairs >= 2) {
+    __asm__ volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * c) : "memory");
+  } else if (newer_pairs == 1) {
+    __asm__ volatile("s_waitcnt vmcnt(%0)" ::"n"(c) : "memory");
+  } else {
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+}
 
 struct SeqPtrs {  // uniform per work-group
   const uint8_t* kc;
@@ -216,39 +256,31 @@ struct SeqPtrs {  // uniform per work-group
   const uint8_t* md;
 };
 
+// Ring loads of window pair (wA, wB) into the slot at LDS address `slot` (wave-uniform arguments;
+// wB = wA when the pair has no second window, whose contents are then never used).
 template <int kMeta>
-__device__ __forceinline__ PairLoad load_pair(const SeqPtrs& sp, int wA, bool hasB, int lane) {
-  constexpr bool kMx = kMeta == kMetaMx;
-  const int col = lane & 15, g = lane >> 4, r = lane & 15, side = col >> 3;
-  const uint32_t wB = hasB ? wA + 1 : wA;
-  const uint32_t wS = side ? wB : (uint32_t)wA;
-  PairLoad d;
-  d.ka0 = *reinterpret_cast<const uint2*>(sp.kc + ((uint32_t)(kW * wA + r) * 32u + 8u * g));
-  d.ka1 = *reinterpret_cast<const uint2*>(sp.kc + ((uint32_t)(kW * wA + 16 + r) * 32u + 8u * g));
-  d.kb0 = *reinterpret_cast<const uint2*>(sp.kc + ((kW * wB + r) * 32u + 8u * g));
-  d.kb1 = *reinterpret_cast<const uint2*>(sp.kc + ((kW * wB + 16 + r) * 32u + 8u * g));
-  d.va = *reinterpret_cast<const uint4*>(sp.vc + ((uint32_t)wA * 1024u + 16u * lane));
-  d.vb = *reinterpret_cast<const uint4*>(sp.vc + (wB * 1024u + 16u * lane));
-  const uint32_t t = kW * wS + 4u * g;
-  d.nk0 = *reinterpret_cast<const uint2*>(sp.kn + t);
-  d.nk1 = *reinterpret_cast<const uint2*>(sp.kn + t + 16);
-  d.nv0 = *reinterpret_cast<const uint2*>(sp.vn + t);
-  d.nv1 = *reinterpret_cast<const uint2*>(sp.vn + t + 16);
-  d.md0 = *reinterpret_cast<const uint32_t*>(sp.md + t);
-  d.md1 = *reinterpret_cast<const uint32_t*>(sp.md + t + 16);
-  if constexpr (kMx) {
-    const uint8_t* rec = sp.kmx + wS * (uint32_t)kMxRecord;
-    d.stp.x = *reinterpret_cast<const uint32_t*>(rec + 4u * (8u * g + (col & 7)));
-    d.stp.y = *reinterpret_cast<const uint16_t*>(rec + 128u + 2u * g);
-    d.mnp = make_uint2(0u, 0u);
-  } else if constexpr (kMeta == kMetaFp16) {
-    const uint32_t mt = wS * kD + 32u * g + 4u * (col & 7);
-    d.stp = *reinterpret_cast<const uint2*>(sp.kstep + mt);
-    d.mnp = *reinterpret_cast<const uint2*>(sp.kmin + mt);
-  } else {  // TurboQuant keys: no window metadata
-    d.stp = d.mnp = make_uint2(0u, 0u);
+__device__ __forceinline__ void issue_pair(const SeqPtrs& sp, uint32_t wA, uint32_t wB, int lane, uint32_t slot) {
+  const uint32_t lo = 16u * lane;
+  dma16s(sp.kc + (size_t)wA * 1024u, lo, slot + kChKA);
+  dma16s(sp.kc + (size_t)wB * 1024u, lo, slot + kChKB);
+  dma16s(sp.vc + (size_t)wA * 1024u, lo, slot + kChVA);
+  dma16s(sp.vc + (size_t)wB * 1024u, lo, slot + kChVB);
+  if constexpr (kMeta == kMetaFp16) {  // lanes 0-15 steps of A, 16-31 of B, 32-47 minima of A, 48-63 of B
+    const uint32_t w = (lane & 16) ? wB : wA;
+    const uint16_t* base = (lane & 32) ? sp.kmin : sp.kstep;
+    dma16(base + w * kD + 8u * (lane & 15), slot + kChMeta);
+  } else if constexpr (kMeta == kMetaMx) {  // 68 record dwords: A's 34, then B's
+    const uint32_t d = (uint32_t)lane;
+    dma4(sp.kmx + (d < 34u ? wA : wB) * (uint32_t)kMxRecord + 4u * (d < 34u ? d : d - 34u), slot + kChMeta);
+    if (lane < 4) dma4(sp.kmx + wB * (uint32_t)kMxRecord + 4u * (30u + lane), slot + kChMeta + 256);
   }
-  return d;
+  if (lane < 20) {  // key norms A, B (lanes 0-7), value norms A, B (8-15), modality ids A, B (16-19)
+    const uint32_t w = (lane < 16 ? (lane & 4) : (lane & 2)) ? wB : wA;
+    const uint8_t* src = lane < 8    ? reinterpret_cast<const uint8_t*>(sp.kn + w * kW) + 16u * (lane & 3)
+                         : lane < 16 ? reinterpret_cast<const uint8_t*>(sp.vn + w * kW) + 16u * (lane & 3)
+                                     : sp.md + w * kW + 16u * (lane & 1);
+    dma16(src, slot + kChSmall);
+  }
 }
 
 // fp16 minimum / step pairs of 4 channels from their MXFP4 record word and block scale bytes: the
@@ -291,20 +323,21 @@ template <int kMeta>
 __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   constexpr bool kMx = kMeta == kMetaMx;
   constexpr bool kTq = kMeta == kMetaTq;
+  // the pair ring (8 waves x 3 slots x 6 KB); after the pair loop the same memory holds the combine
+  // tile (per wave [channel][24 rows + 4]: rows 0-7 audio, 8-15 video, 16-23 text heads) and the
+  // fp16 A tile of the un-rotation
+  __shared__ __attribute__((aligned(16))) uint4 ring_mem[kDecWaves * kRingSlots * kSlotBytes / 16];
   __shared__ __attribute__((aligned(16))) uint2 vlut[256];
   __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];                     // q' (fp32, padded rows)
   __shared__ float amax_w[kDecWaves];
-  __shared__ __attribute__((aligned(16))) uint32_t meta[kDecWaves][2][2][kD / 2];  // [wave][side][step, min]
-  __shared__ __attribute__((aligned(16))) uint32_t zeros[kD / 2];                  // steps of "no window"
   __shared__ __attribute__((aligned(16))) float wst[2][8][kDecWaves];              // [m, l][head][wave]
   __shared__ uint32_t wmask[kDecWaves];
   __shared__ uint32_t wnv[kDecWaves];  // value-norm maxima
   __shared__ int wexp[kDecWaves];      // operand scale exponents E
-  // per wave, column-major accumulator tile for the combine: [channel][row], rows 0-7 audio,
-  // 8-15 video, 16-23 text heads
-  __shared__ __attribute__((aligned(16))) float wacc[kDecWaves][kD][kAccPitch];
-  __shared__ __attribute__((aligned(16))) _Float16 atile[8][kATile];  // merged rows, fp16
   __shared__ __attribute__((aligned(16))) float fac[8][kDecWaves];    // per head and wave: combine factor
+  __shared__ __attribute__((aligned(16))) _Float16 atile[8][kATile];  // merged rows, fp16
+  static_assert(sizeof(float) * kD * kAccPitch <= kRingSlots * kSlotBytes, "a wave's combine rows fit in its ring");
+  uint8_t* const ring = reinterpret_cast<uint8_t*>(ring_mem);
 
   const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = lane_id();
@@ -324,31 +357,41 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
                    kMeta == kMetaFp16 ? p.k_step + seq * nwcap * kD : nullptr,
                    kMx ? p.k_mx + seq * nwcap * kMxRecord : nullptr,
                    p.modality + (size_t)b * p.cap};
+  const uint32_t ring_w = (uint32_t)__builtin_amdgcn_readfirstlane(
+      (int)(uint32_t)(uintptr_t)(ring + (size_t)wave * kRingSlots * kSlotBytes));  // this wave's slots
+  auto slot_lds = [&](int k) { return ring_w + (uint32_t)((k % kRingSlots) * kSlotBytes); };
+  auto slot_ptr = [&](int k) { return ring + (size_t)wave * kRingSlots * kSlotBytes + (k % kRingSlots) * kSlotBytes; };
+  auto pair_w = [&](int k, int w_lim, uint32_t& wA, uint32_t& wB) {
+    wA = (uint32_t)(wA0 + 2 * kDecWaves * k);
+    wB = (int)wA + 1 < w_lim ? wA + 1 : wA;
+  };
 
-  // ---- every global load of the prologue goes out before any of them is used: the query rows
-  // (waves 0-3), the first pair (speculatively: windows within the plan, the length is checked
-  // later) and the sequence length ----
+  // ---- prologue: every load goes out before any is used. Waves 0-3 first load their two query
+  // rows and the signs into slot 2 of their ring (unused until the loop issues a wave's third
+  // pair), then every wave loads its first two pairs of the plan (speculatively: the sequence
+  // length, a scalar load, is checked after) ----
+  // the length first: a scalar load only while no store or ring load precedes it in the kernel
+  const int len_dev = p.seq_lens[b];
   const int hr = 2 * wave + (lane >> 5), c4 = 4 * (lane & 31);
-  uint2 qraw = make_uint2(0, 0);
-  uint32_t qsgn = 0;
-  if (wave < 4 && hr < p.G) {
-    qraw = *reinterpret_cast<const uint2*>(p.q + ((size_t)b * p.Hq + h * p.G + hr) * kD + c4);
-    qsgn = *reinterpret_cast<const uint32_t*>(p.signs + c4);
+  if (wave < 4) {
+    const uint32_t qst = ring_w + 2 * kSlotBytes;
+    if (lane < 32 && 2 * wave + (lane >> 4) < p.G)  // 16 lanes x 16 bytes per query row
+      dma16(p.q + ((size_t)b * p.Hq + h * p.G + 2 * wave) * kD + 8 * lane, qst);
+    if (lane < 8) dma16(p.signs + 16 * lane, qst + 512);
   }
-  // The first pair is loaded unconditionally, its window clamped into the sequence's capacity
-  // (a wave without a pair never uses it): under a branch, the compiler's wait before the barrier
-  // below would have to assume no pair loads in flight and wait for all of them.
-  PairLoad bufA, bufB;
-  {
-    const int wAc = max(min(wA0, w_plan - 1), 0);
-    bufA = load_pair<kMeta>(sp, wAc, wAc + 1 < w_plan, lane);
+  int issued = 0;  // pairs of this wave issued to the ring
+  for (; issued < 2 && wA0 + 2 * kDecWaves * issued < w_plan; ++issued) {
+    uint32_t wA, wB;
+    pair_w(issued, w_plan, wA, wB);
+    issue_pair<kMeta>(sp, wA, wB, lane, slot_lds(issued));
   }
   // memory-safe if device and host lengths disagree; with the fp16 residual the last 128 tokens
   // are the merge launch's
-  const int len = max(min(p.seq_lens[b], p.cap) - p.residual, 0);
+  const int len = max(min(len_dev, p.cap) - p.residual, 0);
   const int nwin = (len + kW - 1) / kW;
   const int w_end = min(w_plan, nwin);
   if (w_begin >= w_end) {  // empty split (ragged batch): a header the merge skips
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // no ring load may land after the exit
     write_empty_record(rec, tid);
     return;
   }
@@ -357,14 +400,13 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     const uint32_t lv[4] = {p.cb01 & 0xffffu, p.cb01 >> 16, p.cb23 & 0xffffu, p.cb23 >> 16};
     vlut[tid] = make_uint2(lv[tid & 3] | (lv[(tid >> 2) & 3] << 16), lv[(tid >> 4) & 3] | (lv[tid >> 6] << 16));
   }
-  if (tid < kD / 2) zeros[tid] = 0u;
-  if (g < 2) {  // text rows of this wave's combine slot start at zero
-#pragma unroll
-    for (int nb = 0; nb < 8; ++nb)
-      *reinterpret_cast<float4*>(&wacc[wave][16 * nb + col][16 + 4 * g]) = make_float4(0.f, 0.f, 0.f, 0.f);
-  }
   // ---- query rotation: wave w < 4 rotates heads 2w, 2w+1; lane holds channels c4 .. c4+3 ----
   if (wave < 4) {
+    ring_wait<kMeta>(issued);  // the query and sign loads (issued first) have landed
+    const uint8_t* qst = slot_ptr(2);
+    uint2 qraw = make_uint2(0, 0);
+    if (hr < p.G) qraw = *reinterpret_cast<const uint2*>(qst + 256 * (lane >> 5) + 2 * c4);
+    const uint32_t qsgn = *reinterpret_cast<const uint32_t*>(qst + 512 + c4);
     float x[4];
     const uint32_t rr[2] = {qraw.x, qraw.y};
 #pragma unroll
@@ -408,8 +450,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   // fp16 operands)
   const float kscale = ldexpf(1.0f, kTq ? -k0 : 24 - k0);
   // Per-lane query operand of the score MFMA, constant over the pairs: for channels
-  // 32g + 8 k4 .. +7, fp16(q'[hd][c] 2^(k0 - shift(c))). The other window's k-blocks multiply it
-  // by zero steps (read from `zeros`).
+  // 32g + 8 k4 .. +7, fp16(q'[hd][c] 2^(k0 - shift(c))).
   uint32_t qm[4][4];
 #pragma unroll
   for (int k4 = 0; k4 < 4; ++k4) {
@@ -430,15 +471,39 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
       }
     }
   }
+  // B operand of the bias MFMA (Eq. 4 linearity: q'.m_g for the pair's two windows): column col
+  // holds fp16(q'[hd] 2^k0) for col < 8 and the rounding residual of the same for col >= 8, so that
+  // a column pair sums to q' 2^k0 to about 2^-22 relative; channel 32 g + 8 kk + i at k-block kk
+  uint32_t qb[4][4];
+  if constexpr (!kTq) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const float4 qa = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 8 * kk]);
+      const float4 qc = *reinterpret_cast<const float4*>(&qs[hd][32 * g + 8 * kk + 4]);
+      const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qc.x, qc.y, qc.z, qc.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float v[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const float x = ldexpf(qv[2 * j + u], k0);
+          const float hi = (float)(_Float16)x;
+          v[u] = side ? x - hi : hi;
+        }
+        qb[kk][j] = pack2(v[0], v[1]);
+      }
+    }
+  }
+  const float bscale = ldexpf(1.0f, -k0);
   // modality tables of this lane: its own row half (set 1: audio for side 0, video for side 1),
   // the partner's, and the text rows (side 0 only)
   const uint32_t tab_own = side ? kTabVideo : kTabAudio;
   const uint32_t tab_oth = side ? kTabAudio : kTabVideo;
   const uint32_t tab_txt0 = side ? 0u : kTabText;
 
-  floatx4 acc1[8];
+  floatx4 acc1[8], acc2[8];  // set 1: audio rows 0-7, video rows 8-15; set 2: text rows 0-7
 #pragma unroll
-  for (int nb = 0; nb < 8; ++nb) acc1[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int nb = 0; nb < 8; ++nb) acc1[nb] = acc2[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -__builtin_inff(), l_run = 0.0f;
   bool started = false;  // a pair has been processed (wave-uniform)
   uint32_t seen = 0;  // modalities seen by this wave
@@ -447,79 +512,90 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   // with p <= 1 the fp16 product p 2^E n_v stays below 2^15 for E = min(15, 15 - nvb). The
   // accumulators and l_run hold 2^E times the unscaled sums; the combine divides it out.
   int nvb = 0, E = 15;
-  uint32_t* mw = &meta[wave][side][0][0];
-  const float* qrow = &qs[hd][32 * g];
-  // steps read for the two windows' k-blocks: the lane's own window, zeros for the other one
-  const uint32_t* stA = side ? zeros : &meta[wave][0][0][0];
-  const uint32_t* stB = side ? &meta[wave][1][0][0] : zeros;
-  float* tacc = &wacc[wave][col][16 + 4 * g];  // text rows of this lane (g < 2), channel 16 nb + col
 
-  auto process = [&](const PairLoad& cur, int wA) {
+  auto process = [&](uint8_t* sl, int wA) {
     const bool hasB = wA + 1 < w_end;
     const bool full = hasB && kW * (wA + 2) <= len;  // every token of both windows is valid
-    const int wS = wA + side;
+    // ---- the pair's data from the slot ----
+    const uint2 ka0 = *reinterpret_cast<const uint2*>(sl + kChKA + 32 * col + 8 * g);
+    const uint2 ka1 = *reinterpret_cast<const uint2*>(sl + kChKA + 32 * (16 + col) + 8 * g);
+    const uint2 kb0 = *reinterpret_cast<const uint2*>(sl + kChKB + 32 * col + 8 * g);
+    const uint2 kb1 = *reinterpret_cast<const uint2*>(sl + kChKB + 32 * (16 + col) + 8 * g);
+    const uint4 va = *reinterpret_cast<const uint4*>(sl + kChVA + 16 * lane);
+    const uint4 vb = *reinterpret_cast<const uint4*>(sl + kChVB + 16 * lane);
+    const uint8_t* sm = sl + kChSmall;
+    const uint2 nk0 = *reinterpret_cast<const uint2*>(sm + kSmKn + 64 * side + 8 * g);
+    const uint2 nk1 = *reinterpret_cast<const uint2*>(sm + kSmKn + 64 * side + 32 + 8 * g);
+    const uint2 nv0 = *reinterpret_cast<const uint2*>(sm + kSmVn + 64 * side + 8 * g);
+    const uint2 nv1 = *reinterpret_cast<const uint2*>(sm + kSmVn + 64 * side + 32 + 8 * g);
+    uint32_t md[2] = {*reinterpret_cast<const uint32_t*>(sm + kSmMd + 32 * side + 4 * g),
+                      *reinterpret_cast<const uint32_t*>(sm + kSmMd + 32 * side + 16 + 4 * g)};
+    // metadata of the lane's window (side): channels 32 g .. 32 g + 31
+    const uint8_t* stp_s = sl + kStepOff<kMeta> + 256 * side + 64 * g;
+    if constexpr (kMx) {  // decode the two records into fp16 steps and minima in the slot
+      const uint8_t* rec_s = sl + kChMeta + kMxRecord * side;
+      const uint32_t word = *reinterpret_cast<const uint32_t*>(rec_s + 4 * (8 * g + c7));
+      const uint32_t scales = *reinterpret_cast<const uint16_t*>(rec_s + 128 + 2 * g);
+      uint2 mnp, stp;
+      mx_to_f16(word, scales, mnp, stp);
+      *reinterpret_cast<uint2*>(sl + kStepOff<kMeta> + 256 * side + 64 * g + 8 * c7) = stp;
+      *reinterpret_cast<uint2*>(sl + kMinOff<kMeta> + 256 * side + 64 * g + 8 * c7) = mnp;
+      wave_lds_sync();
+    }
 
     float bias = 0.0f;  // TurboQuant keys: no window minimum
     if constexpr (!kTq) {
-      // ---- side window metadata through wave-private LDS, natural channel order ----
-      uint2 stp = cur.stp, mnp = cur.mnp;
-      if constexpr (kMx) mx_to_f16(cur.stp.x, cur.stp.y, mnp, stp);
-      *reinterpret_cast<uint2*>(&mw[16 * g + 2 * c7]) = stp;
-      *reinterpret_cast<uint2*>(&mw[kD / 2 + 16 * g + 2 * c7]) = mnp;
-      wave_lds_sync();
-      uint4 mn4[4];
+      // ---- bias q'.m of both windows on the matrix cores: A row r holds the minima of window
+      // r & 1 (so every lane group's rows 4g, 4g + 1 are windows A, B), B the query's hi and lo
+      // parts; a lane adds its column and the partner column (hi + lo) of its side's row ----
+      const uint8_t* min_r = sl + kMinOff<kMeta> + 256 * (col & 1) + 64 * g;
+      floatx4 bacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int k4 = 0; k4 < 4; ++k4) mn4[k4] = *reinterpret_cast<const uint4*>(&mw[kD / 2 + 16 * g + 4 * k4]);
-      // ---- bias q'.m of the side window (fp32): 32 channels per lane, then the 4 lane groups ----
-      float bp[4];  // four independent partial sums (short dependency chains)
-#pragma unroll
-      for (int k4 = 0; k4 < 4; ++k4) {
-        const float4 qa = *reinterpret_cast<const float4*>(qrow + 8 * k4);
-        const float4 qb = *reinterpret_cast<const float4*>(qrow + 8 * k4 + 4);
-        const uint4 m = mn4[k4];
-        float b = qa.x * lo_f16(m.x);
-        b = __builtin_fmaf(qa.y, hi_f16(m.x), b);
-        b = __builtin_fmaf(qa.z, lo_f16(m.y), b);
-        b = __builtin_fmaf(qa.w, hi_f16(m.y), b);
-        b = __builtin_fmaf(qb.x, lo_f16(m.z), b);
-        b = __builtin_fmaf(qb.y, hi_f16(m.z), b);
-        b = __builtin_fmaf(qb.z, lo_f16(m.w), b);
-        b = __builtin_fmaf(qb.w, hi_f16(m.w), b);
-        bp[k4] = b;
+      for (int kk = 0; kk < 4; ++kk) {
+        const uint4 m = *reinterpret_cast<const uint4*>(min_r + 16 * kk);
+        bacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(m.x, m.y, m.z, m.w), h8(qb[kk]), bacc, 0, 0, 0);
       }
-      bias = (bp[0] + bp[1]) + (bp[2] + bp[3]);
-      bias = sum32(sum16(bias));
+      const float bA = bacc[0] + fswap8(bacc[0]), bB = bacc[1] + fswap8(bacc[1]);
+      bias = (side ? bB : bA) * bscale;
     }
 
-    // ---- scores: two 16-token tiles, each 8 MFMAs block-diagonal over the pair ----
-    floatx4 sc0 = {0.f, 0.f, 0.f, 0.f}, sc1 = {0.f, 0.f, 0.f, 0.f};
+    // ---- scores: two 16-token tiles per window, 4 MFMAs each over the window's 128 channels. The
+    // B operand is the lane's own window's q'_c step_c (its column holds that window's head), so the
+    // window-A products are kept by the side-0 lanes and the window-B products by the side-1 lanes ----
+    floatx4 sA0 = {0.f, 0.f, 0.f, 0.f}, sA1 = sA0, sB0 = sA0, sB1 = sA0;
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      const uint32_t* q = qm[kk & 3];
-      if constexpr (kTq) {  // codebook operands from the table; the other window's k-blocks get a zero query
-        const bool mine = (kk < 4) == (side == 0);
-        const half8 bop = h8(mine ? q[0] : 0u, mine ? q[1] : 0u, mine ? q[2] : 0u, mine ? q[3] : 0u);
-        sc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_lut(vlut, kk < 4 ? cur.ka0 : cur.kb0, kk), bop, sc0, 0, 0, 0);
-        sc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_lut(vlut, kk < 4 ? cur.ka1 : cur.kb1, kk), bop, sc1, 0, 0, 0);
+    for (int kk = 0; kk < 4; ++kk) {
+      const uint32_t* q = qm[kk];
+      half8 bop;
+      if constexpr (kTq) {
+        bop = h8(q[0], q[1], q[2], q[3]);
+        sA0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_lut(vlut, ka0, kk), bop, sA0, 0, 0, 0);
+        sA1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_lut(vlut, ka1, kk), bop, sA1, 0, 0, 0);
+        sB0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_lut(vlut, kb0, kk), bop, sB0, 0, 0, 0);
+        sB1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_lut(vlut, kb1, kk), bop, sB1, 0, 0, 0);
       } else {
-        const uint4 sv = *reinterpret_cast<const uint4*>(&(kk < 4 ? stA : stB)[16 * g + 4 * (kk & 3)]);
-        const half8 bop = h8(pk_mul(q[0], sv.x), pk_mul(q[1], sv.y), pk_mul(q[2], sv.z), pk_mul(q[3], sv.w));
-        sc0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka0 : cur.kb0, kk), bop, sc0, 0, 0, 0);
-        sc1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kk < 4 ? cur.ka1 : cur.kb1, kk), bop, sc1, 0, 0, 0);
+        const uint4 sv = *reinterpret_cast<const uint4*>(stp_s + 16 * kk);
+        bop = h8(pk_mul(q[0], sv.x), pk_mul(q[1], sv.y), pk_mul(q[2], sv.z), pk_mul(q[3], sv.w));
+        sA0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(ka0, kk), bop, sA0, 0, 0, 0);
+        sA1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(ka1, kk), bop, sA1, 0, 0, 0);
+        sB0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kb0, kk), bop, sB0, 0, 0, 0);
+        sB1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(key_a_operand(kb1, kk), bop, sB1, 0, 0, 0);
       }
     }
-    if constexpr (!kTq) wave_lds_sync();  // metadata reads done before the next pair overwrites it
+    const floatx4 sc0 = side ? sB0 : sA0, sc1 = side ? sB1 : sA1;
 
-    // ---- online softmax (base 2) over the pair's 64 tokens ----
-    const uint32_t nkw[4] = {cur.nk0.x, cur.nk0.y, cur.nk1.x, cur.nk1.y};
-    const uint32_t nvw[4] = {cur.nv0.x, cur.nv0.y, cur.nv1.x, cur.nv1.y};
-    uint32_t md[2] = {cur.md0, cur.md1};
+    // ---- online softmax (base 2) over the pair's 64 tokens. Scores are formed relative to the
+    // current reference mref = m_run + kLazy - E (p 2^E = 2^(s - mref)), so that the exponent needs no
+    // subtraction; the first pair of the wave and a moved reference shift them once ----
+    const uint32_t nkw[4] = {nk0.x, nk0.y, nk1.x, nk1.y};
+    const uint32_t nvw[4] = {nv0.x, nv0.y, nv1.x, nv1.y};
+    const float mref0 = started ? m_run + kLazy - (float)E : 0.0f;
     float s[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {  // e = 4 t + i: token 16 t + 4 g + i of the side window
       const float raw = (e >> 2) ? sc1[e & 3] : sc0[e & 3];
       const float nkf = (e & 1) ? hi_f16(nkw[e >> 1]) : lo_f16(nkw[e >> 1]);
-      s[e] = nkf * __builtin_fmaf(raw, kscale, bias);
+      s[e] = __builtin_fmaf(nkf, __builtin_fmaf(raw, kscale, bias), -mref0);
     }
     if (!full) {  // partial pair: tokens beyond the length (or a missing window B) do not count
       const bool side_ok = !side || hasB;
@@ -547,8 +623,11 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
       nvb = min(norm_bound(nvm, 0) + 1, 16);
       E = min(15, 15 - nvb);
       started = true;
-    } else if (__any(wmax > m_run + kLazy) || __any(max(nvm & 0xffffu, nvm >> 16) >= norm_threshold(nvb))) {
-      const float m_new = fmaxf(m_run, wmax);
+      const float sh = -(m_run + kLazy - (float)E);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[e] += sh;
+    } else if (__any(wmax > (float)E) || __any(max(nvm & 0xffffu, nvm >> 16) >= norm_threshold(nvb))) {
+      const float m_new = fmaxf(m_run, wmax + mref0);
       const int nb = norm_bound(nvm, nvb);
       const int nvb_new = nb > nvb ? min(nb + 1, 16) : nvb;
       const int E_new = min(15, 15 - nvb_new);
@@ -562,56 +641,74 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc1[nb][i] *= arow[i];
       }
-      if (g < 2) {
+      if (seen & 4u) {  // text rows hold something
 #pragma unroll
         for (int nb = 0; nb < 8; ++nb) {
-          float4* t = reinterpret_cast<float4*>(tacc + 16 * nb * kAccPitch);
-          const float4 v = *t;
-          *t = make_float4(v.x * arow[0], v.y * arow[1], v.z * arow[2], v.w * arow[3]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc2[nb][i] *= arow[i];
         }
       }
       m_run = m_new;
       nvb = nvb_new;
       E = E_new;
+      const float sh = mref0 - (m_run + kLazy - (float)E);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[e] += sh;
     }
-    const float mref = m_run + kLazy - (float)E;  // pr = p 2^E
-    float pr[8];
+    float pr[8];  // p 2^E
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      pr[e] = fast_exp2(s[e] - mref);
+      pr[e] = fast_exp2(s[e]);
       l_run += pr[e];
     }
     uint32_t pv[4];  // p 2^E n_v (fp16 pairs), tokens (4g, 4g+1), (4g+2, 4g+3), (16+4g, ..), (16+4g+2, ..)
 #pragma unroll
     for (int q = 0; q < 4; ++q) pv[q] = pk_mul(pack_f16(pr[2 * q], pr[2 * q + 1]), nvw[q]);
 
-    // ---- modalities present (wave-uniform) and the v_perm selectors of the token pairs ----
-    uint32_t pres = __builtin_amdgcn_perm(kTabBits, kTabBits, md[0]) | __builtin_amdgcn_perm(kTabBits, kTabBits, md[1]);
-    pres |= pres >> 16;
-    pres |= pres >> 8;
-    const bool has_a = __any(pres & 1u), has_v = __any(pres & 2u), has_t = __any(pres & 4u);
-    seen |= (has_a ? 1u : 0u) | (has_v ? 2u : 0u) | (has_t ? 4u : 0u);  // all wave-uniform
-    uint32_t sel[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) sel[q] = __builtin_amdgcn_perm(md[q >> 1], md[q >> 1], (q & 1) ? 0x03030202u : 0x01010000u);
-
-    // ---- values: one PV MFMA per window and 16-channel block. Set 1 (rows 0-7 audio heads from
-    // the side-0 lanes, rows 8-15 video heads from the side-1 lanes) runs for every pair: a branch
-    // around it would give the accumulators two register homes ----
-    {
-      uint32_t opA[4], opB[4];
+    // ---- value operands of set 1 (rows 0-7 audio heads from the side-0 lanes, rows 8-15 video
+    // heads from the side-1 lanes). A pair of one modality (audio or video, every token valid:
+    // tokens past the length carry id 3) takes its rows straight from p n_v; otherwise the
+    // operands are masked per token with v_perm byte tables ----
+    uint32_t opA[4], opB[4], sel[4];
+    bool has_t = false;
+    const bool all_v = __all(md[0] == 0x01010101u && md[1] == 0x01010101u);
+    const bool all_a = __all((md[0] | md[1]) == 0u);
+    if (all_v) {  // window A's video rows come from the side-0 partner, window B's are the lane's own
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
+        opA[q] = take_partner<0xc>(0u, pv[q]);
+        opB[q] = side ? pv[q] : 0u;
+      }
+      seen |= 2u;
+    } else if (all_a) {  // window A's audio rows are the lane's own, window B's come from the side-1 partner
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        opA[q] = side ? 0u : pv[q];
+        opB[q] = take_partner<0x3>(0u, pv[q]);
+      }
+      seen |= 1u;
+    } else {  // modalities present (wave-uniform) and the v_perm selectors of the token pairs
+      uint32_t pres = __builtin_amdgcn_perm(kTabBits, kTabBits, md[0]) | __builtin_amdgcn_perm(kTabBits, kTabBits, md[1]);
+      pres |= pres >> 16;
+      pres |= pres >> 8;
+      const bool has_a = __any(pres & 1u), has_v = __any(pres & 2u);
+      has_t = __any(pres & 4u);
+      seen |= (has_a ? 1u : 0u) | (has_v ? 2u : 0u) | (has_t ? 4u : 0u);  // all wave-uniform
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        sel[q] = __builtin_amdgcn_perm(md[q >> 1], md[q >> 1], (q & 1) ? 0x03030202u : 0x01010000u);
         const uint32_t own = pv[q] & __builtin_amdgcn_perm(tab_own, tab_own, sel[q]);
         const uint32_t oth = pv[q] & __builtin_amdgcn_perm(tab_oth, tab_oth, sel[q]);
         opA[q] = take_partner<0xc>(own, oth);  // window A tokens: video rows from the side-0 partner
         opB[q] = take_partner<0x3>(own, oth);  // window B tokens: audio rows from the side-1 partner
       }
+    }
+    // ---- values: one PV MFMA per window and 16-channel block, set 1 for every pair (a branch
+    // around it would give the accumulators two register homes) ----
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) {
-        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, cur.va, nb), acc1[nb], 0, 0, 0);
-        acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, cur.vb, nb), acc1[nb], 0, 0, 0);
-      }
+    for (int nb = 0; nb < 8; ++nb) {
+      acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, va, nb), acc1[nb], 0, 0, 0);
+      acc1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, vb, nb), acc1[nb], 0, 0, 0);
     }
     if (has_t) {  // set 2: rows 0-7 text heads (side-0 lanes), rows 8-15 zero
       uint32_t opA[4], opB[4];
@@ -623,37 +720,42 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
       }
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
-        floatx4 t = {0.f, 0.f, 0.f, 0.f};
-        t = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, cur.va, nb), t, 0, 0, 0);
-        t = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, cur.vb, nb), t, 0, 0, 0);
-        if (g < 2) {
-          float4* ta = reinterpret_cast<float4*>(tacc + 16 * nb * kAccPitch);
-          const float4 v = *ta;
-          *ta = make_float4(v.x + t[0], v.y + t[1], v.z + t[2], v.w + t[3]);
-        }
+        acc2[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opA), lut_op(vlut, va, nb), acc2[nb], 0, 0, 0);
+        acc2[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(opB), lut_op(vlut, vb, nb), acc2[nb], 0, 0, 0);
       }
     }
   };
 
-  // ---- window pairs, double-buffered loads without register copies ----
-  for (int wA = wA0; wA < w_end; wA += 4 * kDecWaves) {
-    const int wA2 = wA + 2 * kDecWaves;
-    if (wA2 < w_end) bufB = load_pair<kMeta>(sp, wA2, wA2 + 1 < w_end, lane);
-    process(bufA, wA);
-    if (wA2 >= w_end) break;
-    const int wA3 = wA2 + 2 * kDecWaves;
-    if (wA3 < w_end) bufA = load_pair<kMeta>(sp, wA3, wA3 + 1 < w_end, lane);
-    process(bufB, wA2);
+  // ---- window pairs through the ring: issue pair k + 2 (if it has tokens), wait for pair k ----
+  int hi = issued - 1;  // highest pair issued
+  for (int k = 0;; ++k) {
+    const int wA = wA0 + 2 * kDecWaves * k;
+    if (wA >= w_end) break;
+    if (wA + 4 * kDecWaves < w_end) {
+      uint32_t nA, nB;
+      pair_w(k + 2, w_end, nA, nB);
+      issue_pair<kMeta>(sp, nA, nB, lane, slot_lds(k + 2));
+      hi = k + 2;
+    }
+    ring_wait<kMeta>(hi - k);
+    process(slot_ptr(k), wA);
   }
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // speculative loads of the plan beyond the length
 
-  // ---- epilogue. This wave's slice of the inverse-rotation table (output channels 16 wave ..
-  // 16 wave + 15, all 384 (modality, k) rows) as MFMA B operands, loaded first so that the
-  // combine below hides the latency ----
-  uint4 rb[12];
-  {
-    const uint4* rp = reinterpret_cast<const uint4*>(p.rot16t) + (size_t)(16 * wave + (lane & 15)) * 48 + (lane >> 4);
+  // ---- epilogue. Waves 0-3 un-rotate: wave w takes output channels 32 w .. 32 w + 31 (two 16-channel
+  // blocks), so the merged rows are read by four waves instead of eight. Its slice of the
+  // inverse-rotation table (all 384 (modality, k) rows) is loaded first, as MFMA B operands, so
+  // that the combine below hides the latency ----
+  constexpr int kRotWaves = 4;
+  uint4 rb[2][12];
+  if (wave < kRotWaves) {
 #pragma unroll
-    for (int kk = 0; kk < 12; ++kk) rb[kk] = rp[4 * kk];
+    for (int cb = 0; cb < 2; ++cb) {
+      const uint4* rp =
+          reinterpret_cast<const uint4*>(p.rot16t) + (size_t)(32 * wave + 16 * cb + (lane & 15)) * 48 + (lane >> 4);
+#pragma unroll
+      for (int kk = 0; kk < 12; ++kk) rb[cb][kk] = rp[4 * kk];
+    }
   }
 
   // ---- combine the waves of the work-group: every wave writes its raw accumulators and its
@@ -678,10 +780,22 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     wnv[wave] = max(nvm & 0xffffu, nvm >> 16);
     wexp[wave] = E;
   }
+  // the wave's rows go to its own ring slots, free once its last ring load has landed (no other
+  // wave writes there), so no barrier precedes them
+  auto wacc = [&](int w) { return reinterpret_cast<float(*)[kAccPitch]>(ring + (size_t)w * kRingSlots * kSlotBytes); };
+  {
+    float(*mine)[kAccPitch] = wacc(wave);
 #pragma unroll
-  for (int nb = 0; nb < 8; ++nb)  // rows 4g .. 4g + 3 of set 1 (audio, video heads), channel 16 nb + col
-    *reinterpret_cast<float4*>(&wacc[wave][16 * nb + col][4 * g]) =
-        make_float4(acc1[nb][0], acc1[nb][1], acc1[nb][2], acc1[nb][3]);
+    for (int nb = 0; nb < 8; ++nb)  // rows 4g .. 4g + 3 of set 1 (audio, video heads), channel 16 nb + col
+      *reinterpret_cast<float4*>(&mine[16 * nb + col][4 * g]) =
+          make_float4(acc1[nb][0], acc1[nb][1], acc1[nb][2], acc1[nb][3]);
+    if ((seen & 4u) && g < 2) {  // text rows 16 + 4g .. (set 2 rows 0-7), read only for waves that saw text
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb)
+        *reinterpret_cast<float4*>(&mine[16 * nb + col][16 + 4 * g]) =
+            make_float4(acc2[nb][0], acc2[nb][1], acc2[nb][2], acc2[nb][3]);
+    }
+  }
   __syncthreads();
   uint32_t mask = 0, nmax = 0;
 #pragma unroll
@@ -732,7 +846,8 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
       for (int i = 0; i < 4; ++i) f[i] = *reinterpret_cast<const float4*>(&fac[h0 + i][w4]);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const float4 v = *reinterpret_cast<const float4*>(&wacc[w4 + u][k][4 * rq]);
+        if (!(wmask[w4 + u] & (1u << m))) continue;  // that wave saw no token of this modality
+        const float4 v = *reinterpret_cast<const float4*>(&wacc(w4 + u)[k][4 * rq]);
         const float fu[4] = {u == 0 ? f[0].x : u == 1 ? f[0].y : u == 2 ? f[0].z : f[0].w,
                              u == 0 ? f[1].x : u == 1 ? f[1].y : u == 2 ? f[1].z : f[1].w,
                              u == 0 ? f[2].x : u == 1 ? f[2].y : u == 2 ? f[2].z : f[2].w,
@@ -747,10 +862,11 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     for (int i = 0; i < 4; ++i) atile[h0 + i][m * kD + k] = (_Float16)a[i];
   }
   __syncthreads();
-  // ---- inverse rotation on MFMA, once per present modality: wave w computes channels
-  // c = 16 w .. 16 w + 15 of o[head][c] = sum_m sum_k A[head][128 m + k] R_m[k][c]. A rows 8-15
+  // ---- inverse rotation on MFMA, once per present modality: wave w < 4 computes channels
+  // c = 32 w .. 32 w + 31 of o[head][c] = sum_m sum_k A[head][128 m + k] R_m[k][c]. A rows 8-15
   // (lanes whose row is >= 8) only feed output rows that are not stored. ----
-  floatx4 dacc = {0.f, 0.f, 0.f, 0.f};
+  if (wave >= kRotWaves) return;
+  floatx4 dacc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
   for (int m = 0; m < 3; ++m) {
     if (!(mask & (1u << m))) continue;
@@ -758,13 +874,19 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     for (int k4 = 0; k4 < 4; ++k4) {
       const int kk = 4 * m + k4;
       const half8 a = *reinterpret_cast<const half8*>(&atile[lane & 7][32 * kk + 8 * (lane >> 4)]);
-      dacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(half8, rb[kk]), dacc, 0, 0, 0);
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb)
+        dacc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, __builtin_bit_cast(half8, rb[cb][kk]), dacc[cb], 0, 0, 0);
     }
   }
   if (lane < 32) {
     const float sc = ldexpf(1.0f, -e);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) rec[kRecHeader + (4 * (lane >> 4) + i) * kD + 16 * wave + (lane & 15)] = dacc[i] * sc;
+    for (int cb = 0; cb < 2; ++cb) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        rec[kRecHeader + (4 * (lane >> 4) + i) * kD + 32 * wave + 16 * cb + (lane & 15)] = dacc[cb][i] * sc;
+    }
   }
 }
 
