@@ -268,7 +268,7 @@ def sylvester_hadamard(signs):
 
 
 def key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream, decode_iters,
-                         key_meta, signs=None, rot=None):
+                         key_meta, signs=None, rot=None, flags=0):
     """The benchmark workload with another key storage: MXFP4 window metadata (the paper's default)
     or TurboQuant keys (no window metadata). Prefill append into an empty cache, decode over >= 1 GB
     of cold cache replicas, and the split-K kernel's duration from events bound to its dispatch."""
@@ -282,7 +282,7 @@ def key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
     rot = torch.eye(128).repeat(3, 1, 1) if rot is None else rot
     caches = [okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev, key_meta=key_meta)
               for _ in range(n_cache)]
-    okvq.okvq_append(caches[0], [0] * B, k_in[0], v_in[0], m0, lens, n_new_dev, N, stream=stream)
+    okvq.okvq_append(caches[0], [0] * B, k_in[0], v_in[0], m0, lens, n_new_dev, N, flags=flags, stream=stream)
     torch.cuda.synchronize()
     for c in caches[1:]:
         for name in c.buffers:
@@ -296,7 +296,8 @@ def key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
         c = caches[(i + 1) % n_cache]
         c.buffers["seq_lens"].zero_()
         e0.record(stream)
-        okvq.okvq_append(c, [0] * B, k_in[i % len(k_in)], v_in[i % len(v_in)], m0, lens, n_new_dev, N, stream=stream)
+        okvq.okvq_append(c, [0] * B, k_in[i % len(k_in)], v_in[i % len(v_in)], m0, lens, n_new_dev, N, flags=flags,
+                         stream=stream)
         e1.record(stream)
         app.append((e0, e1))
     torch.cuda.synchronize()
@@ -305,21 +306,23 @@ def key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
     for rep in range(5):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         for i in range(20):
-            okvq.okvq_decode_attention(caches[i % n_cache], lens, q, sm, out, ws, stream=stream)
+            okvq.okvq_decode_attention(caches[i % n_cache], lens, q, sm, out, ws, flags=flags, stream=stream)
         e0.record(stream)
         for i in range(decode_iters):
-            okvq.okvq_decode_attention(caches[(i * 7 + rep) % n_cache], lens, q, sm, out, ws, stream=stream)
+            okvq.okvq_decode_attention(caches[(i * 7 + rep) % n_cache], lens, q, sm, out, ws, flags=flags,
+                                       stream=stream)
         e1.record(stream)
         torch.cuda.synchronize()
         reps.append(e0.elapsed_time(e1) * 1e3 / decode_iters)
-    decode_us = float(np.median(reps))
+    decode_us, decode_us_min = float(np.median(reps)), float(np.min(reps))
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(decode_iters)]
     for e4 in evs:
         for e in e4:
             e.record(stream)
     torch.cuda.synchronize()
     for i in range(decode_iters):
-        okvq.okvq_decode_attention_timed(caches[(i * 7 + 5) % n_cache], lens, q, sm, out, ws, evs[i], stream=stream)
+        okvq.okvq_decode_attention_timed(caches[(i * 7 + 5) % n_cache], lens, q, sm, out, ws, evs[i], flags=flags,
+                                         stream=stream)
     torch.cuda.synchronize()
     split_us = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) * 1e3
     dbytes = decode_algorithmic_bytes(B, H, Hq, lens, key_meta=key_meta)
@@ -328,6 +331,7 @@ def key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
     del caches
     tag = {"mxfp4": "mx", "turboquant": "tq"}[key_meta]
     return {"bytes_per_token_head": CACHE_BYTES_PER_TOKEN_HEAD[key_meta], "decode_us": round(decode_us, 3),
+            "decode_us_min": round(decode_us_min, 3),
             "decode_GBps": round(dbytes / decode_us / 1e3, 2),
             "k_decode_us": round(split_us, 3), "k_decode_GBps": round(sbytes / split_us / 1e3, 2),
             "k_decode_frac": round(sbytes / split_us / 1e3 / HBM_PEAK_GBPS, 4),
@@ -440,7 +444,7 @@ def ladder_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, q, signs, rot,
             e1.record(stream)
             torch.cuda.synchronize()
             reps.append(e0.elapsed_time(e1) * 1e3 / decode_iters)
-        decode_us = float(np.median(reps))
+        decode_us, decode_us_min = float(np.median(reps)), float(np.min(reps))
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(decode_iters)]
         for e4 in evs:
             for e in e4:
@@ -460,7 +464,8 @@ def ladder_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, q, signs, rot,
             "quantize_keys_us": round(keys_us, 2), "quantize_keys_GBps": round(kbytes / keys_us / 1e3, 1),
             "quantize_values_us": round(vals_us, 2), "quantize_values_GBps": round(vbytes / vals_us / 1e3, 1),
             "quantize_values_exact_us": round(vals_exact_us, 2),
-            "decode_us": round(decode_us, 3), "decode_GBps": round(dbytes / decode_us / 1e3, 1),
+            "decode_us": round(decode_us, 3), "decode_us_min": round(decode_us_min, 3),
+            "decode_GBps": round(dbytes / decode_us / 1e3, 1),
             "k_ladder_decode_us": round(split_us, 3), "k_ladder_decode_frac": round(sbytes / split_us / 1e3 / HBM_PEAK_GBPS, 4),
             "replicas": n_cache}
         del caches, base
@@ -551,7 +556,8 @@ def layers48_measurement(okvq, torch, np, dev, stream, reps=5):
         e0.record(stream)
         okvq.okvq_append(c, [0] * B, lay["k"], lay["v"], lay["modality"], lens, n_new, N, stream=stream)
         e1.record(stream)
-        okvq.okvq_append(cg, [0] * B, lay["k"], lay["v"], lay["modality"], lens, n_new, N, stream=stream)
+        okvq.okvq_append(cg, [0] * B, lay["k"], lay["v"], lay["modality"], lens, n_new, N,
+                         flags=okvq.okvq.OKVQ_GLOBAL_ROTATION, stream=stream)
         app.append((e0, e1))
         packed.append(c)
         glob.append(cg)
@@ -566,11 +572,15 @@ def layers48_measurement(okvq, torch, np, dev, stream, reps=5):
     seq = torch.tensor(lens, dtype=torch.int32, device=dev)
     out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
 
-    def packed_call(layer, caches=packed, events=None):
+    def packed_call(layer, caches=packed, events=None, flags=0):
         if events is None:
-            okvq.okvq_decode_attention(caches[layer], lens, qs[layer], sm, out, ws, stream=stream)
+            okvq.okvq_decode_attention(caches[layer], lens, qs[layer], sm, out, ws, flags=flags, stream=stream)
         else:
-            okvq.okvq_decode_attention_timed(caches[layer], lens, qs[layer], sm, out, ws, events, stream=stream)
+            okvq.okvq_decode_attention_timed(caches[layer], lens, qs[layer], sm, out, ws, events, flags=flags,
+                                             stream=stream)
+
+    def global_call(layer, events=None):
+        packed_call(layer, glob, events, okvq.okvq.OKVQ_GLOBAL_ROTATION)
 
     def dense_call(layer, events=None):
         okvq.okvq_decode_attention_dense(ddims, dk[layer], dv[layer], seq, lens, qs[layer], sm, out, dws,
@@ -589,7 +599,7 @@ def layers48_measurement(okvq, torch, np, dev, stream, reps=5):
             e1.record(stream)
             torch.cuda.synchronize()
             ts.append(e0.elapsed_time(e1) * 1e3)
-        return float(np.median(ts))
+        return float(np.median(ts)), float(np.min(ts))
 
     def kernel_us(fn):
         """mean duration of the split-K kernel and of the merge over one sweep (events bound to them)"""
@@ -618,23 +628,30 @@ def layers48_measurement(okvq, torch, np, dev, stream, reps=5):
     pk_split = decode_algorithmic_bytes(B, H, Hq, lens, with_output=False)
     dn = dense_decode_bytes(B, H, Hq, lens)
     dn_split = dn - B * Hq * 128 * 4
-    t_packed = sweep(packed_call)
-    t_glob = sweep(lambda layer: packed_call(layer, glob))
-    t_dense = sweep(dense_call)
+    t_packed, t_packed_min = sweep(packed_call)
+    t_glob, t_glob_min = sweep(global_call)
+    t_dense, t_dense_min = sweep(dense_call)
     ks, km = kernel_us(packed_call)
+    gs, gm = kernel_us(global_call)
     ds, dm = kernel_us(dense_call)
     res = {
         "workload": "omni30b_128k_48layer", "layers": nl, "batch": B, "kv_heads": H, "q_heads": Hq, "seq_len": N,
         "data": "synthetic, generated on the device per layer (same recipe, torch generator)",
         "resident_GB": {"packed": round(nl * sum(okvq.okvq_buffer_bytes(packed[0].dims, i) for i in range(10)) / 1e9, 3),
                         "dense_fp16": round(nl * 2 * B * H * N * 256 / 1e9, 3)},
-        "packed": {"decode_us_all_layers": round(t_packed, 2), "decode_us_per_layer": round(t_packed / nl, 3),
+        "packed": {"decode_us_all_layers": round(t_packed, 2), "decode_us_all_layers_min": round(t_packed_min, 2),
+                   "decode_us_per_layer": round(t_packed / nl, 3),
                    "GBps": round(pk * nl / t_packed / 1e3, 1), "k_decode_us": round(ks, 3),
                    "k_decode_merge_us": round(km, 3), "k_decode_frac": round(pk_split / ks / 1e3 / HBM_PEAK_GBPS, 4),
                    "latency_us_per_layer": round(latency(packed_call), 2), "append_us_per_layer": round(append_us, 2),
                    "algorithmic_bytes_per_layer": pk},
-        "global_rotation": {"decode_us_all_layers": round(t_glob, 2), "decode_us_per_layer": round(t_glob / nl, 3)},
-        "dense_fp16": {"decode_us_all_layers": round(t_dense, 2), "decode_us_per_layer": round(t_dense / nl, 3),
+        "global_rotation": {"flag": "OKVQ_GLOBAL_ROTATION", "decode_us_all_layers": round(t_glob, 2),
+                            "decode_us_all_layers_min": round(t_glob_min, 2),
+                            "decode_us_per_layer": round(t_glob / nl, 3), "k_decode_us": round(gs, 3),
+                            "k_decode_merge_us": round(gm, 3),
+                            "k_decode_frac": round(pk_split / gs / 1e3 / HBM_PEAK_GBPS, 4)},
+        "dense_fp16": {"decode_us_all_layers": round(t_dense, 2), "decode_us_all_layers_min": round(t_dense_min, 2),
+                       "decode_us_per_layer": round(t_dense / nl, 3),
                        "GBps": round(dn * nl / t_dense / 1e3, 1), "k_decode_dense_us": round(ds, 3),
                        "merge_us": round(dm, 3), "k_decode_dense_frac": round(dn_split / ds / 1e3 / HBM_PEAK_GBPS, 4),
                        "latency_us_per_layer": round(latency(dense_call), 2), "algorithmic_bytes_per_layer": dn,
@@ -642,6 +659,77 @@ def layers48_measurement(okvq, torch, np, dev, stream, reps=5):
         "speedup_packed_vs_dense": round(t_dense / t_packed, 3),
     }
     del packed, glob, dk, dv
+    torch.cuda.empty_cache()
+    return res
+
+
+def ragged_measurement(okvq, torch, np, dev, stream, decode_iters):
+    """Batch 16 with ragged lengths U[8192, 16384] at the 7B-like head shapes (4 KV heads, 28 query
+    heads): the rows generated on the device from the workload's recipe, each sequence's prefill
+    (its own length, its own modality layout ending in the text prompt) appended into an empty
+    cache, then decode over >= 1 GB of cold cache replicas, and the split-K kernel's duration from
+    events bound to its dispatch."""
+    from synth import gen_lengths, gen_queries, modality_layout, workload
+    from synth.device import gen_layer_device
+    wl = workload("omni7b_b16_ragged16k")
+    B, H, Hq = wl.batch, wl.num_kv_heads, wl.num_q_heads
+    lens = [int(x) for x in gen_lengths(wl)]
+    lay = gen_layer_device(wl, 0, dev)
+    N = lay["k"].shape[2]
+    mod = np.zeros((B, N), np.uint8)
+    for b, L in enumerate(lens):
+        mod[b, :L] = modality_layout(L, wl.video_per_chunk, wl.audio_per_chunk, wl.text_tail)
+    m_in = torch.from_numpy(mod).to(dev)
+    sm = 1 / math.sqrt(128)
+    signs = torch.from_numpy(lay["signs"])
+    rot = torch.from_numpy(lay["rot"])
+    base = okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev)
+    n_new = torch.tensor(lens, dtype=torch.int32, device=dev)
+    okvq.okvq_append(base, [0] * B, lay["k"], lay["v"], m_in, lens, n_new, N, stream=stream)
+    torch.cuda.synchronize()
+    del lay
+    per_cache = sum(okvq.okvq_buffer_bytes(base.dims, i) for i in range(10))
+    n_cache = max(8, int(math.ceil(1.05e9 / per_cache)))
+    caches = [base] + [okvq.KVCache(B, H, Hq, wl.capacity, signs, rot, device=dev) for _ in range(n_cache - 1)]
+    for c in caches[1:]:
+        for name in c.buffers:
+            c.buffers[name].copy_(base.buffers[name])
+    q = torch.from_numpy(gen_queries(wl.wid, 0, B, Hq)).to(dev)
+    ws = okvq.decode_workspace(base.dims, max(lens), device=dev)
+    out = torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
+    reps = []
+    for rep in range(5):
+        for i in range(10):
+            okvq.okvq_decode_attention(caches[i % n_cache], lens, q, sm, out, ws, stream=stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(decode_iters):
+            okvq.okvq_decode_attention(caches[(i * 5 + rep) % n_cache], lens, q, sm, out, ws, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        reps.append(e0.elapsed_time(e1) * 1e3 / decode_iters)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(decode_iters)]
+    for e4 in evs:
+        for e in e4:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for i in range(decode_iters):
+        okvq.okvq_decode_attention_timed(caches[(i * 5 + 3) % n_cache], lens, q, sm, out, ws, evs[i], stream=stream)
+    torch.cuda.synchronize()
+    split_us = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) * 1e3
+    merge_us = float(np.mean([e[2].elapsed_time(e[3]) for e in evs])) * 1e3
+    dbytes = decode_algorithmic_bytes(B, H, Hq, lens)
+    sbytes = decode_algorithmic_bytes(B, H, Hq, lens, with_output=False)
+    decode_us = float(np.median(reps))
+    res = {"workload": wl.name, "batch": B, "kv_heads": H, "q_heads": Hq,
+           "lengths_min_max_mean": [min(lens), max(lens), round(float(np.mean(lens)), 1)],
+           "algorithmic_bytes": dbytes, "decode_us": round(decode_us, 3),
+           "decode_us_min": round(float(np.min(reps)), 3), "decode_GBps": round(dbytes / decode_us / 1e3, 1),
+           "k_decode_us": round(split_us, 3), "k_decode_merge_us": round(merge_us, 3),
+           "k_decode_GBps": round(sbytes / split_us / 1e3, 1),
+           "k_decode_frac": round(sbytes / split_us / 1e3 / HBM_PEAK_GBPS, 4), "replicas": n_cache,
+           "replica_GB": round(n_cache * per_cache / 1e9, 2)}
+    del caches, base
     torch.cuda.empty_cache()
     return res
 
@@ -706,7 +794,7 @@ def residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
         e1.record(stream)
         torch.cuda.synchronize()
         reps.append(e0.elapsed_time(e1) * 1e3 / decode_iters)
-    decode_us = float(np.median(reps))
+    decode_us, decode_us_min = float(np.median(reps)), float(np.min(reps))
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(decode_iters)]
     for e4 in evs:
         for e in e4:
@@ -720,7 +808,8 @@ def residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
     dbytes = residual_decode_algorithmic_bytes(B, H, Hq, lens)
     del caches
     return {"protocol": "captioning: keys quantized per 128-token block, last 128 values fp16",
-            "decode_us": round(decode_us, 3), "decode_GBps": round(dbytes / decode_us / 1e3, 2),
+            "decode_us": round(decode_us, 3), "decode_us_min": round(decode_us_min, 3),
+            "decode_GBps": round(dbytes / decode_us / 1e3, 2),
             "k_decode_us": round(split_us, 3), "k_decode_merge_residual_us": round(merge_us, 3),
             "append_prefill_us": round(append_us, 3), "append_one_token_us": round(append1_us, 3),
             "algorithmic_bytes": dbytes, "replicas": n_cache}
@@ -958,7 +1047,7 @@ def main():
         e1.record(stream)
         torch.cuda.synchronize()
         reps.append(e0.elapsed_time(e1) * 1e3 / args.decode_iters)
-    decode_us = float(np.median(reps))
+    decode_us, decode_us_min = float(np.median(reps)), float(np.min(reps))
 
     # per-launch durations: HIP events bound to the split-K and merge dispatches (start and end of
     # each kernel's execution, as the profiler sees them), over cold replicas
@@ -1008,6 +1097,7 @@ def main():
                    "seq_len": N, "key_window": 32, "bits": 2, "modalities": "150 video + 25 audio per chunk, "
                    "256 text"},
         "decode_us": round(decode_us, 3),
+        "decode_us_min": round(decode_us_min, 3),
         "decode_us_in_step": round(float(np.mean(decode_step_ms)) * 1e3, 3),
         "decode_latency_us": round(float(np.median(lat)), 2),
         "append_us": round(append_us, 3),
@@ -1030,12 +1120,14 @@ def main():
                                          args.decode_iters, "mxfp4")
     line["turboquant"] = key_meta_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                               args.decode_iters, "turboquant", signs,
-                                              torch.from_numpy(sylvester_hadamard(lay["signs"])).repeat(3, 1, 1))
+                                              torch.from_numpy(sylvester_hadamard(lay["signs"])).repeat(3, 1, 1),
+                                              flags=okvq.okvq.OKVQ_GLOBAL_ROTATION)
     line["ladder"] = ladder_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, q, signs, rot, stream,
                                         args.decode_iters)
     line["calibration"] = calibration_measurement(okvq, torch, np, wl, dev)
     if not args.no_layers48:
         line["omni30b_48layer"] = layers48_measurement(okvq, torch, np, dev, stream)
+    line["b16_ragged"] = ragged_measurement(okvq, torch, np, dev, stream, args.decode_iters)
     line["stream"] = stream_measurement(okvq, torch, np, dev, stream)
     line["residual"] = residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q, stream,
                                             args.decode_iters)

@@ -127,7 +127,15 @@ enum { OKVQ_MOD_AUDIO = 0, OKVQ_MOD_VIDEO = 1, OKVQ_MOD_TEXT = 2, OKVQ_NUM_MODAL
 
 /* flags */
 enum {
-  OKVQ_VALUE_EXACT = 1u << 0 /* value rotation as a sequential fp32 dot product (bit-exact codes) */
+  OKVQ_VALUE_EXACT = 1u << 0,    /* value rotation as a sequential fp32 dot product (bit-exact codes) */
+  /* One value rotation for every token: the first table of v_rot (R_0) rotates the values of all
+   * modalities, as in TurboQuant's single randomized rotation (Sec. 2.1, Eq. 2 and Eq. 3; the
+   * TurboQuant rows of Tab. 3), instead of the per-modality R_m of Eq. 6. Accepted by
+   * okvq_quantize_values, okvq_append and the decode calls of the 2-bit layout (the bit-width
+   * ladder returns OKVQ_ERR_UNSUPPORTED). The modality map is still stored. A cache appended with
+   * the flag must be decoded with it (decode then keeps one accumulator and un-rotates once with
+   * R_0); codes and decode equal those of the per-modality path called with v_rot = {R_0, R_0, R_0}. */
+  OKVQ_GLOBAL_ROTATION = 1u << 1
 };
 
 /* okvq_dims.key_meta: storage of the per-window key minimum and step */
@@ -249,6 +257,7 @@ okvq_status okvq_quantize_keys_tq(const okvq_dims* dims, const uint16_t* k, int3
  *              the documented order); otherwise MFMA with an fp16 hi/lo split of R_m and fp32
  *              accumulation (codes may differ from the exact order only where y lies within a
  *              small band around a decision threshold). Both layouts, both modes.
+ *              OKVQ_GLOBAL_ROTATION: R_0 for every token (2-bit layout only).
  *   outputs    device v_codes, v_norm in the cache layout (whole 32-token windows are written;
  *              slots beyond a length get code 0 and norm 0). */
 okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const uint8_t* modality,
@@ -266,7 +275,8 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
  * cache->v_rot16 (okvq_prepare_rotation); OKVQ_VALUE_EXACT reads cache->v_rot. The key window
  * metadata is written in the format of cache->dims.key_meta (k_min / k_step, or k_mx). With the
  * residual, the raw key and value rows of the new tokens among the last 128 of each sequence are
- * also written to k_res and v_res (one more launch, before the codec). */
+ * also written to k_res and v_res (one more launch, before the codec). flags: OKVQ_VALUE_EXACT,
+ * OKVQ_GLOBAL_ROTATION (R_0 for every token). */
 okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
                         const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
                         const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream);
@@ -308,7 +318,8 @@ size_t okvq_decode_workspace_bytes(const okvq_dims* dims, int32_t max_seq_len);
  * below 128 floor(L / 128) dequantized, the others and all values in fp16 from k_res / v_res --
  * and merges them in. A sequence of length 0 yields zeros. fp32
  * accumulation; the result matches float64 attention over the dequantized cache within 2e-3 of
- * the output norm. */
+ * the output norm. flags: 0, or OKVQ_GLOBAL_ROTATION for a cache appended with it (one value
+ * accumulator, one un-rotation with R_0; 2-bit layout only). */
 okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q,
                                   float sm_scale, uint32_t flags, float* out, void* workspace,
                                   size_t workspace_bytes, void* stream);

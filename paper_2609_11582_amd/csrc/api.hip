@@ -393,9 +393,12 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
                                  uint16_t* v_norm, void* stream) {
   okvq_status st = check_dims(dims);
   if (st != OKVQ_OK) return st;
-  if (n_tokens < 0 || !lens_host || (flags & ~(uint32_t)OKVQ_VALUE_EXACT)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (n_tokens < 0 || !lens_host || (flags & ~(uint32_t)(OKVQ_VALUE_EXACT | OKVQ_GLOBAL_ROTATION)))
+    return OKVQ_ERR_INVALID_ARGUMENT;
   if (!aligned16(v) || !aligned16(modality) || !aligned16(v_rot) || !aligned16(v_codes) || !aligned16(v_norm))
     return OKVQ_ERR_INVALID_ARGUMENT;
+  const bool global_rot = (flags & OKVQ_GLOBAL_ROTATION) != 0;
+  if (global_rot && is_ladder(dims)) return OKVQ_ERR_UNSUPPORTED;
   for (int b = 0; b < dims->batch; ++b) {
     if (lens_host[b] < 0 || lens_host[b] > n_tokens) return OKVQ_ERR_INVALID_ARGUMENT;
     if (lens_host[b] > dims->capacity) return OKVQ_ERR_CAPACITY;
@@ -432,6 +435,7 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
     CodecArgs a{};
     a.j.src = v;
     a.j.msrc = modality;
+    a.j.global_rot = global_rot ? 1 : 0;
     a.j.n_rows = n_tokens;
     a.j.b0 = b0;
     a.j.H = dims->num_kv_heads;
@@ -463,7 +467,8 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
   okvq_status st = check_cache(cache);
   if (st != OKVQ_OK) return st;
   if (is_ladder(&cache->dims)) return OKVQ_ERR_UNSUPPORTED;  // the ladder layout is filled by the stateless calls
-  if (!lens_host || !n_new_host || n_max < 0 || (flags & ~(uint32_t)OKVQ_VALUE_EXACT)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!lens_host || !n_new_host || n_max < 0 || (flags & ~(uint32_t)(OKVQ_VALUE_EXACT | OKVQ_GLOBAL_ROTATION)))
+    return OKVQ_ERR_INVALID_ARGUMENT;
   if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(mod_new) || !aligned16(n_new_dev))
     return OKVQ_ERR_INVALID_ARGUMENT;
   const okvq_dims& d = cache->dims;
@@ -487,6 +492,7 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
     CodecArgs a{};
     a.j.src = k_new;
     a.j.msrc = mod_new;
+    a.j.global_rot = (flags & OKVQ_GLOBAL_ROTATION) ? 1 : 0;
     a.j.n_rows = n_max;
     a.j.begin_dev = cache->seq_lens;
     a.j.count_dev = n_new_dev;
@@ -573,9 +579,12 @@ static okvq_status decode_impl(const okvq_cache* cache, const int32_t* lens_host
                                void* const* events, bool use_scratch = false) {
   okvq_status st = check_cache(cache);
   if (st != OKVQ_OK) return st;
-  if (!lens_host || flags != 0 || !std::isfinite(sm_scale)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if (!lens_host || (flags & ~(uint32_t)OKVQ_GLOBAL_ROTATION) || !std::isfinite(sm_scale))
+    return OKVQ_ERR_INVALID_ARGUMENT;
+  const bool global_rot = (flags & OKVQ_GLOBAL_ROTATION) != 0;
   if (!aligned16(q) || !aligned16(out)) return OKVQ_ERR_INVALID_ARGUMENT;
   const okvq_dims& d = cache->dims;
+  if (global_rot && is_ladder(&d)) return OKVQ_ERR_UNSUPPORTED;
   int max_len = 0;
   for (int b = 0; b < d.batch; ++b) {
     if (lens_host[b] < 0) return OKVQ_ERR_INVALID_ARGUMENT;
@@ -634,7 +643,7 @@ static okvq_status decode_impl(const okvq_cache* cache, const int32_t* lens_host
   const uint32_t cb01 = cb.level16[0] | ((uint32_t)cb.level16[1] << 16);
   const uint32_t cb23 = cb.level16[2] | ((uint32_t)cb.level16[3] << 16);
   return hip_status(launch_decode(view(cache), q, sm_scale, out, workspace, plan, static_cast<hipStream_t>(stream),
-                                  cb01, cb23, max_len, events ? ev : nullptr));
+                                  cb01, cb23, max_len, events ? ev : nullptr, global_rot));
 }
 
 okvq_status okvq_decode_attention(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* q, float sm_scale,

@@ -347,7 +347,9 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
     const bool myfresh = mytok >= c.begin && mytok < c.len;
     const int mymod = myfresh ? (int)j.msrc[(size_t)c.b * j.n_rows + min(max(mytok - c.begin, 0), j.n_rows - 1)] : 3;
     uint4 bf[2][4][2];
-    if (a.rotfrag) load_rot_slice(a, 1, v, bf);  // video slice, in flight during phase 1
+    // the first modality's slice (video; R_0 with the global rotation), in flight during phase 1
+    const int m_first = j.global_rot ? 0 : 1;
+    if (a.rotfrag) load_rot_slice(a, m_first, v, bf);
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     uint4 av[4][4];
 #pragma unroll
@@ -398,7 +400,8 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
       for (int e = 0; e < n; ++e) s[e] = s[e] + s[e + n];
     }
     const uint32_t n16 = myfresh ? norm_to_f16(sqrt_rn(s[0])) : 0u;
-    const int mt = (n16 != 0 && (uint32_t)mymod <= 2u) ? mymod : 3;  // 3: no code
+    // 3: no code; with the global rotation every coded token takes R_0
+    const int mt = (n16 != 0 && (uint32_t)mymod <= 2u) ? (j.global_rot ? 0 : mymod) : 3;
     sh.itab[64 * v + lane] = (n16 != 0) ? __builtin_amdgcn_rcpf(h2f(n16) * a.th.t2) : 0.0f;
     if (mytok >= c.begin && mytok < wend) a.v_norm[c.seq * j.cap + mytok] = (uint16_t)n16;
     if (myfresh && a.mod_out && c.h == 0) a.mod_out[(size_t)c.b * j.cap + mytok] = (uint8_t)mymod;
@@ -435,7 +438,7 @@ __device__ __forceinline__ void value_role(const CodecArgs& a, int v, ValueShare
 #pragma unroll
     for (int ww = 0; ww < 8; ++ww) vb[ww] = 0;
     for (int mi = 0; mi < 3; ++mi) {
-      const int m = (mi == 0) ? 1 : (mi == 1 ? 0 : 2);  // video, audio, text
+      const int m = (mi == 0) ? m_first : (mi == 1 ? 1 - m_first : 2);  // video, audio, text (R_0 first if global)
       const uint32_t rbs = rbmask[m];
       if (rbs == 0) continue;
       if (mi > 0 || !a.rotfrag) load_rot_slice(a, m, v, bf);

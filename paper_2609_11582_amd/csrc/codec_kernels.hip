@@ -78,7 +78,7 @@ __global__ __launch_bounds__(128) void k_quantize_values_exact(CodecJob j, const
   for (int t = 0; t < kW; ++t) {
     const int m = mods[t];
     if (m < 0 || m > 2) continue;  // old, padded or out-of-contract token: code 0 here
-    const float* r = rot + ((size_t)m * kD + c) * kD;
+    const float* r = rot + ((size_t)(j.global_rot ? 0 : m) * kD + c) * kD;
     float acc = 0.0f;
     for (int k = 0; k < kD; ++k) acc = acc + r[k] * xs[t][k];
     bytes[t >> 2] |= value_code(acc, nrm[t], th) << (2 * (t & 3));

@@ -319,7 +319,9 @@ __device__ __forceinline__ half8 key_a_lut(const uint2* vlut, uint2 w, int kk) {
   return h8(e.x, e.y, o.x, o.y);
 }
 
-template <int kMeta>
+// kGlobal: every value was rotated by R_0 (the single global rotation): one accumulator set whose
+// rows 0-7 sum window A's tokens and rows 8-15 window B's, no modality masks, one un-rotation
+template <int kMeta, bool kGlobal>
 __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   constexpr bool kMx = kMeta == kMetaMx;
   constexpr bool kTq = kMeta == kMetaTq;
@@ -671,9 +673,16 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
     // operands are masked per token with v_perm byte tables ----
     uint32_t opA[4], opB[4], sel[4];
     bool has_t = false;
-    const bool all_v = __all(md[0] == 0x01010101u && md[1] == 0x01010101u);
-    const bool all_a = __all((md[0] | md[1]) == 0u);
-    if (all_v) {  // window A's video rows come from the side-0 partner, window B's are the lane's own
+    const bool all_v = !kGlobal && __all(md[0] == 0x01010101u && md[1] == 0x01010101u);
+    const bool all_a = !kGlobal && __all((md[0] | md[1]) == 0u);
+    if (kGlobal) {  // rows 0-7 take window A's p n_v (side-0 lanes), rows 8-15 window B's (side-1 lanes)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        opA[q] = side ? 0u : pv[q];
+        opB[q] = side ? pv[q] : 0u;
+      }
+      seen |= 1u;
+    } else if (all_v) {  // window A's video rows come from the side-0 partner, window B's are the lane's own
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         opA[q] = take_partner<0xc>(0u, pv[q]);
@@ -747,6 +756,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   // inverse-rotation table (all 384 (modality, k) rows) is loaded first, as MFMA B operands, so
   // that the combine below hides the latency ----
   constexpr int kRotWaves = 4;
+  constexpr int kRotBlocks = kGlobal ? 4 : 12;  // k-blocks of the table read (R_0's only when global)
   uint4 rb[2][12];
   if (wave < kRotWaves) {
 #pragma unroll
@@ -754,7 +764,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
       const uint4* rp =
           reinterpret_cast<const uint4*>(p.rot16t) + (size_t)(32 * wave + 16 * cb + (lane & 15)) * 48 + (lane >> 4);
 #pragma unroll
-      for (int kk = 0; kk < 12; ++kk) rb[cb][kk] = rp[4 * kk];
+      for (int kk = 0; kk < kRotBlocks; ++kk) rb[cb][kk] = rp[4 * kk];
     }
   }
 
@@ -835,7 +845,8 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   __syncthreads();
   // rows summed over the waves with their factors -> A tile [head][128 m + k] (fp16); thread =
   // (row quad rq, channel k), rows 4 rq .. 4 rq + 3 = heads 4 (rq & 1) .. +3 of modality rq / 2
-  for (int idx = tid; idx < 6 * kD; idx += 64 * kDecWaves) {
+  // (global rotation: two row quads, each the sum of rows 4 rq .. and 8 + 4 rq .., the two windows' parts)
+  for (int idx = tid; idx < (kGlobal ? 2 : 6) * kD; idx += 64 * kDecWaves) {
     const int rq = idx >> 7, k = idx & (kD - 1), m = rq >> 1, h0 = 4 * (rq & 1);
     if (!(mask & (1u << m))) continue;
     float a[4] = {0.f, 0.f, 0.f, 0.f};
@@ -847,7 +858,11 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         if (!(wmask[w4 + u] & (1u << m))) continue;  // that wave saw no token of this modality
-        const float4 v = *reinterpret_cast<const float4*>(&wacc(w4 + u)[k][4 * rq]);
+        float4 v = *reinterpret_cast<const float4*>(&wacc(w4 + u)[k][4 * rq]);
+        if constexpr (kGlobal) {
+          const float4 v2 = *reinterpret_cast<const float4*>(&wacc(w4 + u)[k][8 + 4 * rq]);
+          v = make_float4(v.x + v2.x, v.y + v2.y, v.z + v2.z, v.w + v2.w);
+        }
         const float fu[4] = {u == 0 ? f[0].x : u == 1 ? f[0].y : u == 2 ? f[0].z : f[0].w,
                              u == 0 ? f[1].x : u == 1 ? f[1].y : u == 2 ? f[1].z : f[1].w,
                              u == 0 ? f[2].x : u == 1 ? f[2].y : u == 2 ? f[2].z : f[2].w,
@@ -868,7 +883,7 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode(DecodeArgs p) {
   if (wave >= kRotWaves) return;
   floatx4 dacc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-  for (int m = 0; m < 3; ++m) {
+  for (int m = 0; m < (kGlobal ? 1 : 3); ++m) {
     if (!(mask & (1u << m))) continue;
 #pragma unroll
     for (int k4 = 0; k4 < 4; ++k4) {
@@ -1266,7 +1281,7 @@ size_t decode_workspace_bytes(int B, int H, int /*Hq*/, int max_len) { return re
 
 hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, float* out, void* ws,
                          const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int /*max_len*/,
-                         hipEvent_t const* events) {
+                         hipEvent_t const* events, bool global_rot) {
   const int G = c.Hq / c.H;
   DecodeArgs a;
   a.k_codes = c.k_codes;
@@ -1294,7 +1309,12 @@ hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, 
   a.cb23 = cb23;
   hipError_t e;
   const dim3 grid(plan.nsplit, c.H, c.B), block(64 * kDecWaves);
-  auto kern = c.key_meta == kMetaMx ? k_decode<kMetaMx> : c.key_meta == kMetaTq ? k_decode<kMetaTq> : k_decode<kMetaFp16>;
+  auto kern = global_rot ? (c.key_meta == kMetaMx   ? k_decode<kMetaMx, true>
+                            : c.key_meta == kMetaTq ? k_decode<kMetaTq, true>
+                                                    : k_decode<kMetaFp16, true>)
+                         : (c.key_meta == kMetaMx   ? k_decode<kMetaMx, false>
+                            : c.key_meta == kMetaTq ? k_decode<kMetaTq, false>
+                                                    : k_decode<kMetaFp16, false>);
   if (events)  // events bound to the two dispatches: start and end of each kernel's execution
     hipExtLaunchKernelGGL(kern, grid, block, 0, s, events[0], events[1], 0, a);
   else

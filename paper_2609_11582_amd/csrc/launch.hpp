@@ -24,6 +24,7 @@ struct CodecJob {
   const int32_t* count_dev;  // append: appended tokens (device)
   uint16_t* stage;           // append: [B][H][32][128] raw keys of the open window
   int b0, H, cap;
+  int global_rot;            // values: R_0 rotates every token (the single global rotation)
 };
 
 // Exact-mode values (OKVQ_VALUE_EXACT): one work-group per 32-token window.
@@ -132,9 +133,10 @@ DecodePlan plan_decode(int B, int H, int max_len);
 size_t decode_workspace_bytes(int B, int H, int Hq, int max_len);
 hipError_t launch_prepare_rotation(const float* rot, uint16_t* rot16t, hipStream_t s);
 // events: nullptr, or four events bound to the launches: split-K start, end; merge start, end
+// global_rot: the cache's values were all rotated by R_0 (one accumulator, one un-rotation)
 hipError_t launch_decode(const CacheView& c, const uint16_t* q, float sm_scale, float* out, void* ws,
                          const DecodePlan& plan, hipStream_t s, uint32_t cb01, uint32_t cb23, int max_len,
-                         hipEvent_t const* events);
+                         hipEvent_t const* events, bool global_rot);
 
 // Log-sum-exp merge of split records [B][H][nsplit][kRecFloats] into out [B][Hq][128]; events:
 // nullptr, or two events bound to the launch (start, end).

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libokvq.so")
 
 OKVQ_OK = 0
 OKVQ_VALUE_EXACT = 1
+OKVQ_GLOBAL_ROTATION = 2  # R_0 rotates the values of every modality (the single global rotation)
 OKVQ_KEY_META_FP16 = 0
 OKVQ_KEY_META_MXFP4 = 1
 OKVQ_KEY_META_TURBOQUANT = 2

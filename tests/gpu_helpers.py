@@ -68,8 +68,9 @@ def new_cache(B, H, Hq, capacity, signs, rot, key_meta="fp16"):
                         torch.from_numpy(np.asarray(rot, np.float32)), key_meta=key_meta)
 
 
-def append_chunks(cache, k, v, modality, lens, chunk_plan, exact=False):
-    """Append each sequence in the given chunks. chunk_plan: list of per-step token counts [B]."""
+def append_chunks(cache, k, v, modality, lens, chunk_plan, exact=False, flags=0):
+    """Append each sequence in the given chunks. chunk_plan: list of per-step token counts [B].
+    flags: more append flags (OKVQ_GLOBAL_ROTATION)."""
     B, H, N, D = k.shape
     cur = np.zeros(B, np.int64)
     for step in chunk_plan:
@@ -85,7 +86,8 @@ def append_chunks(cache, k, v, modality, lens, chunk_plan, exact=False):
             mn[b, :c - a] = modality[b, a:c]
         nd = dev(n_new.astype(np.int32))
         okvq.okvq_append(cache, cur.astype(np.int32).tolist(), f16dev(kn), f16dev(vn), dev(mn),
-                         n_new.astype(np.int32).tolist(), nd, n_max, okvq.okvq.OKVQ_VALUE_EXACT if exact else 0)
+                         n_new.astype(np.int32).tolist(), nd, n_max,
+                         (okvq.okvq.OKVQ_VALUE_EXACT if exact else 0) | flags)
         torch.cuda.synchronize()
         cur = cur + n_new
     return cur
@@ -117,11 +119,11 @@ def cache_to_numpy(cache):
     return {n: t.cpu().numpy() for n, t in cache.views().items()}
 
 
-def decode(cache, q, lens, sm_scale=1 / math.sqrt(128)):
+def decode(cache, q, lens, sm_scale=1 / math.sqrt(128), flags=0):
     B, Hq, D = q.shape
     ws = okvq.decode_workspace(cache.dims, int(max(lens)))
     out = torch.full((B, Hq, D), float("nan"), dtype=torch.float32, device="cuda")
-    okvq.okvq_decode_attention(cache, list(lens), f16dev(q), sm_scale, out, ws)
+    okvq.okvq_decode_attention(cache, list(lens), f16dev(q), sm_scale, out, ws, flags=flags)
     torch.cuda.synchronize()
     return out.cpu().numpy().astype(np.float64)
 

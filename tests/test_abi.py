@@ -81,14 +81,17 @@ def test_invalid_arguments_rejected_before_any_launch():
     assert L.okvq_quantize_keys(ctypes.byref(ok_dims), fake, 10, big, fake, fake, fake, fake, fake, None) == -1
     over = (ctypes.c_int32 * 2)(10, 65)
     assert L.okvq_quantize_keys(ctypes.byref(ok_dims), fake, 100, over, fake, fake, fake, fake, fake, None) == -3
-    # unknown flag on values
+    # unknown flags on values and decode (bit 1 is OKVQ_GLOBAL_ROTATION, accepted)
     assert L.okvq_quantize_values(ctypes.byref(ok_dims), fake, fake, 10, lens, fake, 8, fake, fake, None) == -1
+    assert okvq.OKVQ_GLOBAL_ROTATION == 2
     # decode: workspace too small, bad flags, over capacity
     cache = okvq.CacheStruct(ok_dims, *([4096] * 9), 4096, 4096, 4096)
     q_lens = (ctypes.c_int32 * 2)(64, 64)
     assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, 16,
                                    None) == -4
     assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 1, fake, fake, 1 << 30,
+                                   None) == -1
+    assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 4, fake, fake, 1 << 30,
                                    None) == -1
     over_l = (ctypes.c_int32 * 2)(65, 0)
     assert L.okvq_decode_attention(ctypes.byref(cache), over_l, fake, ctypes.c_float(0.1), 0, fake, fake, 1 << 30,
@@ -395,5 +398,10 @@ def test_ladder_buffers_and_validation():
     need = okvq.okvq_decode_workspace_bytes(d, 64)
     assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, need - 1,
                                    None) == -4
+    # the single global rotation is a 2-bit-layout mode: the ladder rejects it before a launch
+    g = okvq.OKVQ_GLOBAL_ROTATION
+    assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), g, fake, fake, 1 << 30,
+                                   None) == -2
+    assert L.okvq_quantize_values(ctypes.byref(d), fake, fake, 10, lens, fake, g, fake, fake, None) == -2
     assert okvq.okvq_codebook_bits(3)[0][0] < 0 and len(okvq.okvq_codebook_bits(4)[1]) == 15
     assert L.okvq_codebook_bits(5, (ctypes.c_float * 16)(), (ctypes.c_float * 15)()) == -1
