@@ -87,10 +87,11 @@
  * channel c at bits [b c, b c + b) of the token's 16 b bytes:
  *   k_codes  u8 [B][H][cap][16 key_bits]      v_codes  u8 [B][H][cap][16 value_bits]
  *   k_norm, v_norm, k_min, k_step (fp16 metadata; absent for TurboQuant keys) and modality as above;
- *   no k_stage, k_mx or residual rings. okvq_quantize_keys / okvq_quantize_keys_tq /
- *   okvq_quantize_values fill it (values in either mode; only slots below a length are written;
- *   the modality map is the caller's copy),
- *   okvq_decode_attention reads it, okvq_append returns OKVQ_ERR_UNSUPPORTED.
+ *   k_stage as above for the method's keys (none for TurboQuant keys, whose codes are per token);
+ *   no k_mx or residual rings. okvq_append fills it (three launches: keys, values, lengths), or
+ *   okvq_quantize_keys / okvq_quantize_keys_tq / okvq_quantize_values do (values in either mode;
+ *   only slots below a length are written; the modality map is the caller's copy; no stage, so a
+ *   cache to be appended to is filled by append from length 0); okvq_decode_attention reads it.
  *   Storage per token and KV head: 16 (key_bits + value_bits) + 4 bytes, + 16 with fp16 metadata
  *   (TurboQuant K3/V2: 84 bytes = 2.625 bits per element).
  *
@@ -276,7 +277,10 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
  * metadata is written in the format of cache->dims.key_meta (k_min / k_step, or k_mx). With the
  * residual, the raw key and value rows of the new tokens among the last 128 of each sequence are
  * also written to k_res and v_res (one more launch, before the codec). flags: OKVQ_VALUE_EXACT,
- * OKVQ_GLOBAL_ROTATION (R_0 for every token). */
+ * OKVQ_GLOBAL_ROTATION (R_0 for every token; the 2-bit layout only). The bit-width ladder layout
+ * (Tab. 5 K3V3 / K4V4, Tab. 3 K3/V2) is appended the same way, with its b-bit codecs: the method's
+ * keys re-quantize the open window from the stage, TurboQuant keys and values code the new tokens;
+ * chunked and one-shot appends give the same bytes there too. */
 okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
                         const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
                         const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream);

@@ -135,7 +135,7 @@ okvq_status check_cache(const okvq_cache* c) {
                         c->seq_lens, c->key_signs, c->v_rot, c->v_rot16};
   for (const void* p : ptrs)
     if (!aligned16(p)) return OKVQ_ERR_INVALID_ARGUMENT;
-  if (!is_ladder(&c->dims) && !aligned16(c->k_stage)) return OKVQ_ERR_INVALID_ARGUMENT;
+  if ((!is_ladder(&c->dims) || is_fp16(&c->dims)) && !aligned16(c->k_stage)) return OKVQ_ERR_INVALID_ARGUMENT;
   if (is_mx(&c->dims) && !aligned16(c->k_mx)) return OKVQ_ERR_INVALID_ARGUMENT;
   if (is_fp16(&c->dims) && (!aligned16(c->k_min) || !aligned16(c->k_step))) return OKVQ_ERR_INVALID_ARGUMENT;
   if (c->dims.residual && (!aligned16(c->k_res) || !aligned16(c->v_res))) return OKVQ_ERR_INVALID_ARGUMENT;
@@ -245,8 +245,9 @@ const char* okvq_status_string(okvq_status s) {
 size_t okvq_buffer_bytes(const okvq_dims* d, int32_t which) {
   if (check_dims(d) != OKVQ_OK) return 0;
   const size_t B = d->batch, H = d->num_kv_heads, cap = d->capacity, D = d->head_dim, W = d->window;
-  if (is_ladder(d)) {  // bit-stream layout: no MXFP4 records, no key stage (no append), no rings
+  if (is_ladder(d)) {  // bit-stream layout: no MXFP4 records or rings; a key stage for the method's keys
     switch (which) {
+      case OKVQ_BUF_K_STAGE: return is_fp16(d) ? B * H * W * D * 2 : 0;
       case OKVQ_BUF_K_CODES: return B * H * cap * (D * d->key_bits / 8);
       case OKVQ_BUF_V_CODES: return B * H * cap * (D * d->value_bits / 8);
       case OKVQ_BUF_K_NORM:
@@ -461,14 +462,72 @@ okvq_status okvq_quantize_values(const okvq_dims* dims, const uint16_t* v, const
   return OKVQ_OK;
 }
 
+// Append to the bit-width ladder layout: the key codec (the method's keys requantize the open
+// window from the stage), the value codec of the new tokens, then the lengths advance.
+static okvq_status ladder_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
+                                 const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
+                                 const int32_t* n_new_dev, int32_t n_max, bool exact, hipStream_t s) {
+  const okvq_dims& d = cache->dims;
+  const bool tq = !is_fp16(&d);
+  const Codebook& kcb = codebook(d.key_bits);
+  const Codebook& vcb = codebook(d.value_bits);
+  for (int b0 = 0; b0 < d.batch; b0 += kMaxLenArgs) {
+    const int nb = std::min(kMaxLenArgs, d.batch - b0);
+    LadderKeyArgs ka{};
+    ka.k = k_new;
+    ka.n_rows = n_max;
+    ka.H = d.num_kv_heads;
+    ka.cap = d.capacity;
+    ka.b0 = b0;
+    ka.begin_dev = cache->seq_lens;
+    ka.count_dev = n_new_dev;
+    ka.stage = tq ? nullptr : cache->k_stage;
+    ka.signs = cache->key_signs;
+    ka.k_codes = cache->k_codes;
+    ka.k_min = tq ? nullptr : cache->k_min;
+    ka.k_step = tq ? nullptr : cache->k_step;
+    ka.k_norm = cache->k_norm;
+    for (int i = 0; i + 1 < kcb.levels; ++i) ka.tau[i] = kcb.thr[i];
+    LadderValueArgs va{};
+    va.v = v_new;
+    va.modality = mod_new;
+    va.n_rows = n_max;
+    va.H = d.num_kv_heads;
+    va.cap = d.capacity;
+    va.b0 = b0;
+    va.begin_dev = cache->seq_lens;
+    va.count_dev = n_new_dev;
+    va.mod_out = cache->modality;
+    va.rot = cache->v_rot;
+    va.v_codes = cache->v_codes;
+    va.v_norm = cache->v_norm;
+    for (int i = 0; i + 1 < vcb.levels; ++i) va.tau[i] = vcb.thr[i];
+    int key_span = 0, most = 0;
+    for (int i = 0; i < nb; ++i) {
+      const int L = lens_host[b0 + i], n = n_new_host[b0 + i];
+      if (n == 0) continue;
+      key_span = std::max(key_span, L + n - (tq ? L : (L / kW) * kW));
+      most = std::max(most, n);
+    }
+    if (most == 0) continue;
+    okvq_status st = hip_status(launch_ladder_keys(ka, d.key_bits, tq, nb, key_span, s));
+    if (st != OKVQ_OK) return st;
+    st = hip_status(launch_ladder_values(va, d.value_bits, exact, nb, most, s));
+    if (st != OKVQ_OK) return st;
+    st = hip_status(launch_advance_lengths(cache->seq_lens + b0, n_new_dev + b0, nb, s));
+    if (st != OKVQ_OK) return st;
+  }
+  return OKVQ_OK;
+}
+
 okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new, const uint16_t* v_new,
                         const uint8_t* mod_new, const int32_t* n_new_host, const int32_t* n_new_dev, int32_t n_max,
                         uint32_t flags, void* stream) {
   okvq_status st = check_cache(cache);
   if (st != OKVQ_OK) return st;
-  if (is_ladder(&cache->dims)) return OKVQ_ERR_UNSUPPORTED;  // the ladder layout is filled by the stateless calls
   if (!lens_host || !n_new_host || n_max < 0 || (flags & ~(uint32_t)(OKVQ_VALUE_EXACT | OKVQ_GLOBAL_ROTATION)))
     return OKVQ_ERR_INVALID_ARGUMENT;
+  if (is_ladder(&cache->dims) && (flags & OKVQ_GLOBAL_ROTATION)) return OKVQ_ERR_UNSUPPORTED;
   if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(mod_new) || !aligned16(n_new_dev))
     return OKVQ_ERR_INVALID_ARGUMENT;
   const okvq_dims& d = cache->dims;
@@ -481,6 +540,9 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool exact = (flags & OKVQ_VALUE_EXACT) != 0;
+  if (is_ladder(&d)) return span > 0 ? ladder_append(cache, lens_host, k_new, v_new, mod_new, n_new_host, n_new_dev, n_max,
+                                                     exact, s)
+                                     : OKVQ_OK;
   if (d.residual && span > 0) {  // the fp16 rows, before the codec advances the lengths
     if ((int64_t)d.batch * d.num_kv_heads > INT32_MAX) return OKVQ_ERR_UNSUPPORTED;
     st = hip_status(launch_residual_store(k_new, v_new, n_max, cache->seq_lens, n_new_dev, d.batch, d.num_kv_heads,

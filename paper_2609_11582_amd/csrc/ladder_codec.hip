@@ -52,8 +52,15 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
   __shared__ float zt[kTileTokens][kD + 1];                              // directions (method keys)
   __shared__ __attribute__((aligned(16))) uint8_t ct[kTileTokens][kD];  // codes
   const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz;
-  const int len = a.lens.lens[bz];
-  const int t0 = kTileTokens * blockIdx.x;
+  int begin = 0, len = a.lens.lens[bz];
+  if (a.begin_dev) {  // append: the device lengths decide, clamped into the buffers
+    begin = min(max(a.begin_dev[b], 0), a.cap);
+    len = min(begin + min(max(a.count_dev[b], 0), a.n_rows), a.cap);
+    if (len <= begin) return;  // uniform
+  }
+  // the method's keys requantize the whole open window, TurboQuant keys only the new tokens
+  const int first = kTq ? begin : (begin / kW) * kW;
+  const int t0 = first + kTileTokens * blockIdx.x;
   if (t0 >= len) return;  // uniform over the work-group
   const int t = threadIdx.x, tok = t0 + t;
   const bool valid = tok < len;
@@ -64,8 +71,9 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
   uint32_t sw[32];
   load_sign_words(a.signs, sw);
   uint32_t raw[64];
-  if (valid) {
-    load_row_f16(a.k + (seq * a.n_rows + tok) * kD, raw);
+  if (valid) {  // older tokens of the open window (append, method keys) from the stage
+    load_row_f16(tok < begin ? a.stage + (seq * kW + (tok - first)) * kD : a.k + (seq * a.n_rows + (tok - begin)) * kD,
+                 raw);
   } else {
 #pragma unroll
     for (int i = 0; i < 64; ++i) raw[i] = 0u;
@@ -115,6 +123,18 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
 #pragma unroll
     for (int c = 0; c < kD; ++c) zt[t][c] = x[c];
     __syncthreads();
+    if (a.stage && blockIdx.x == 0) {
+      // Append: the raw rows of the new open window [open, len) into the stage. Only this
+      // work-group reads the stage (its rows [first, begin) lie in tile 0), and its reads are done;
+      // rows below begin (open == first) are in the stage already.
+      const int open = (len / kW) * kW;
+      for (int idx = t; idx < kW * 16; idx += kTileTokens) {
+        const int slot = idx >> 4, part = idx & 15, st = open + slot;
+        if (st >= begin && st < len)
+          reinterpret_cast<uint4*>(a.stage + (seq * kW + slot) * kD)[part] =
+              reinterpret_cast<const uint4*>(a.k + (seq * a.n_rows + (st - begin)) * kD)[part];
+      }
+    }
 
     // ---- phase B (thread = channel): window minimum and step, then the codes ----
     const int c = t;
@@ -178,6 +198,16 @@ __device__ __forceinline__ float tree_norm_lds(const float* xs) {  // xs: 128 fl
   return sqrt_rn(tt[0]);
 }
 
+// The value tokens [begin, len) of sequence b: stateless [0, lens), append from the device lengths.
+__device__ __forceinline__ void value_span(const LadderValueArgs& a, int bz, int b, int& begin, int& len) {
+  begin = 0;
+  len = a.lens.lens[bz];
+  if (a.begin_dev) {
+    begin = min(max(a.begin_dev[b], 0), a.cap);
+    len = min(begin + min(max(a.count_dev[b], 0), a.n_rows), a.cap);
+  }
+}
+
 template <int kBits>
 __global__ __launch_bounds__(128) void k_ladder_values(LadderValueArgs a) {
   constexpr int kTop = (1 << kBits) - 1;
@@ -187,18 +217,20 @@ __global__ __launch_bounds__(128) void k_ladder_values(LadderValueArgs a) {
   __shared__ int mods[kW];
   __shared__ __attribute__((aligned(16))) uint8_t ct[kW][kD];
   const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz;
-  const int len = a.lens.lens[bz];
-  const int t0 = kW * blockIdx.x;
+  int begin, len;
+  value_span(a, bz, b, begin, len);
+  const int t0 = begin + kW * blockIdx.x;
   if (t0 >= len) return;
   const int c = threadIdx.x;
   const size_t seq = (size_t)b * a.H + h;
   for (int t = 0; t < kW; ++t) {
     const int tok = t0 + t;
-    xs[t][c] = (tok < len) ? h2f(a.v[(seq * a.n_rows + tok) * kD + c]) : 0.0f;
+    xs[t][c] = (tok < len) ? h2f(a.v[(seq * a.n_rows + (tok - begin)) * kD + c]) : 0.0f;
   }
   if (c < kW) {
     const int tok = t0 + c;
-    mods[c] = (tok < len) ? (int)a.modality[(size_t)b * a.n_rows + tok] : -1;
+    mods[c] = (tok < len) ? (int)a.modality[(size_t)b * a.n_rows + (tok - begin)] : -1;
+    if (tok < len && a.mod_out && h == 0) a.mod_out[(size_t)b * a.cap + tok] = (uint8_t)mods[c];
   }
   __syncthreads();
   if (c < kW) {
@@ -285,8 +317,9 @@ __global__ __launch_bounds__(256) void k_ladder_values_mfma(LadderValueArgs a) {
   __shared__ int mods[kVTile];
   __shared__ __attribute__((aligned(16))) uint8_t ct[kVTile][kD];
   const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz;
-  const int len = a.lens.lens[bz];
-  const int t0 = kVTile * blockIdx.x;
+  int begin, len;
+  value_span(a, bz, b, begin, len);
+  const int t0 = begin + kVTile * blockIdx.x;
   if (t0 >= len) return;  // uniform
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, r = lane & 15;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -294,14 +327,15 @@ __global__ __launch_bounds__(256) void k_ladder_values_mfma(LadderValueArgs a) {
   // ---- stage the rows (zeros beyond the length), the modalities, the codes' default 0 ----
   for (int idx = tid; idx < kVTile * (kD / 8); idx += 256) {
     const int t = idx >> 4, c8 = idx & 15, tok = t0 + t;
-    const uint4 v = (tok < len) ? *reinterpret_cast<const uint4*>(a.v + (seq * a.n_rows + tok) * kD + 8 * c8)
+    const uint4 v = (tok < len) ? *reinterpret_cast<const uint4*>(a.v + (seq * a.n_rows + (tok - begin)) * kD + 8 * c8)
                                 : make_uint4(0u, 0u, 0u, 0u);
     *reinterpret_cast<uint4*>(&xs[t][8 * c8]) = v;
     *reinterpret_cast<uint2*>(&ct[t][8 * c8]) = make_uint2(0u, 0u);
   }
   if (tid < kVTile) {
     const int tok = t0 + tid;
-    mods[tid] = (tok < len) ? (int)a.modality[(size_t)b * a.n_rows + tok] : -1;
+    mods[tid] = (tok < len) ? (int)a.modality[(size_t)b * a.n_rows + (tok - begin)] : -1;
+    if (tok < len && a.mod_out && h == 0) a.mod_out[(size_t)b * a.cap + tok] = (uint8_t)mods[tid];
   }
   __syncthreads();
   if (tid < kVTile) {  // fp16 norm by the halving tree, as the exact mode

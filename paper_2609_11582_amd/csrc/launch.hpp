@@ -156,10 +156,18 @@ hipError_t launch_decode_dense(const uint16_t* k, const uint16_t* v, const int32
                                hipStream_t s, hipEvent_t const* events);
 
 // ---- bit-width ladder: b-bit keys and values (b = 2, 3, 4) in the token-major bit-stream layout ----
+// Stateless calls (begin_dev == nullptr): tokens [0, lens[b - b0]) of a dense block. Append:
+// tokens [begin_dev[b], begin_dev[b] + count_dev[b]) whose rows are row (token - begin) of the
+// block; the device lengths decide (clamped into the buffers) and the host's copy only sizes the
+// grid. The method's keys requantize the open window from `first` = 32 floor(begin / 32), its older
+// rows taken from the fp16 stage; TurboQuant keys and values are per token and start at begin.
 struct LadderKeyArgs {
   const uint16_t* k;  // [B][H][n_rows][128] fp16
   int n_rows, H, cap, b0;
   LenArgs lens;
+  const int32_t* begin_dev;  // append: current lengths (device), else null
+  const int32_t* count_dev;  // append: appended tokens (device)
+  uint16_t* stage;           // append, method keys: [B][H][32][128] raw keys of the open window
   const int8_t* signs;
   uint8_t* k_codes;   // [B][H][cap][16 b]
   uint16_t* k_min;    // [B][H][cap/32][128] fp16 (method keys)
@@ -172,11 +180,16 @@ struct LadderValueArgs {
   const uint8_t* modality;  // [B][n_rows]
   int n_rows, H, cap, b0;
   LenArgs lens;
+  const int32_t* begin_dev;  // append: as for the keys
+  const int32_t* count_dev;
+  uint8_t* mod_out;          // append: the cache's modality map (written by KV head 0), else null
   const float* rot;   // [3][128][128] fp32
   uint8_t* v_codes;   // [B][H][cap][16 b]
   uint16_t* v_norm;
   float tau[15];
 };
+// max_len: the longest span of tokens from a tile start to the end (stateless: the longest length;
+// append: for the method's keys the longest length - first, else the most appended tokens)
 hipError_t launch_ladder_keys(const LadderKeyArgs& a, int bits, bool tq, int nb, int max_len, hipStream_t s);
 // exact: the sequential fp32 order (bit-exact codes); else the matrix cores (fp16 hi + lo split of R_m)
 hipError_t launch_ladder_values(const LadderValueArgs& a, int bits, bool exact, int nb, int max_len, hipStream_t s);

@@ -442,7 +442,7 @@ class KVCache:
     "turboquant" stores TurboQuant keys (no window metadata, the paper's baseline).
     residual=RESIDUAL_TOKENS adds the fp16 rings of the captioning protocol (k_res, v_res).
     key_bits, value_bits in 2..4 select the bit-width ladder layout (token-major bit streams; filled
-    by the stateless codec calls, no append)."""
+    by okvq_append or the stateless codec calls)."""
 
     def __init__(self, batch, num_kv_heads, num_q_heads, capacity, key_signs: torch.Tensor, v_rot: torch.Tensor,
                  device="cuda", key_meta="fp16", residual=0, key_bits=0, value_bits=0):
@@ -459,7 +459,7 @@ class KVCache:
         unused = {"fp16": ("k_mx",), "mxfp4": ("k_min", "k_step"), "turboquant": ("k_min", "k_step", "k_mx")}[key_meta]
         if not self.residual:
             unused += ("k_res", "v_res")
-        if self.key_bits:
+        if self.key_bits and key_meta != "fp16":  # ladder: only the method's keys keep a stage
             unused += ("k_stage",)
         for i, name in enumerate(BUFFERS):
             nbytes = okvq_buffer_bytes(self.dims, i)
@@ -487,6 +487,8 @@ class KVCache:
         if self.key_bits:  # bit-width ladder: token-major bit streams
             v = dict(k_codes=b["k_codes"].view(B, H, cap, 16 * self.key_bits),
                      v_codes=b["v_codes"].view(B, H, cap, 16 * self.value_bits))
+            if "k_stage" in b:
+                v.update(k_stage=b["k_stage"].view(B, H, 32, 128))
         else:
             v = dict(k_codes=b["k_codes"].view(B, H, cap, 32), v_codes=b["v_codes"].view(B, H, cap // 32, 1024),
                      k_stage=b["k_stage"].view(B, H, 32, 128))

@@ -371,7 +371,8 @@ def test_ladder_buffers_and_validation():
         d = okvq.make_dims(2, 4, 28, 4096, key_meta=meta, key_bits=kb, value_bits=vb)
         per = [okvq.okvq_buffer_bytes(d, i) for i in range(12)]
         assert per[0] == 2 * 4 * 4096 * 16 * kb and per[1] == 2 * 4 * 4096 * 16 * vb
-        assert per[7] == 0 and per[9] == 0 and per[10] == 0 and per[11] == 0   # no stage, MXFP4 or rings
+        assert per[9] == 0 and per[10] == 0 and per[11] == 0   # no MXFP4 records or rings
+        assert per[7] == (2 * 4 * 32 * 128 * 2 if meta == "fp16" else 0)  # the stage: method keys only
         total = sum(per[i] for i in (0, 1, 2, 3, 4, 5))
         assert total == 2 * 4 * 4096 * bytes_per_token_head(kb, vb, meta)
         assert okvq.okvq_decode_workspace_bytes(d, 4096) > 0
@@ -388,12 +389,18 @@ def test_ladder_buffers_and_validation():
     assert L.okvq_quantize_keys_mx(ctypes.byref(mx), fake, 10, lens, fake, fake, fake, fake, None) == -2
     res = okvq.make_dims(2, 2, 8, 64, residual=128, key_bits=3, value_bits=3)
     assert L.okvq_quantize_keys(ctypes.byref(res), fake, 10, lens, fake, fake, fake, fake, fake, None) == -2
-    # a ladder cache cannot be appended to; decode checks its own workspace size
+    # appending to a ladder cache of the method's keys needs its stage, and the single global
+    # rotation is a 2-bit-layout mode; decode checks its own workspace size
     d = okvq.make_dims(2, 2, 8, 64, key_bits=4, value_bits=4)
-    cache = okvq.CacheStruct(d, *([4096] * 7), 0, 4096, 4096, 4096, 4096, 0, 0, 0)
+    nostage = okvq.CacheStruct(d, *([4096] * 7), 0, 4096, 4096, 4096, 4096, 0, 0, 0)
+    cache = okvq.CacheStruct(d, *([4096] * 9), 4096, 4096, 4096, 0, 0, 0)
     n_new = (ctypes.c_int32 * 2)(4, 0)
     lens0 = (ctypes.c_int32 * 2)(0, 0)
-    assert L.okvq_append(ctypes.byref(cache), lens0, fake, fake, fake, n_new, fake, 4, 0, None) == -2
+    assert L.okvq_append(ctypes.byref(nostage), lens0, fake, fake, fake, n_new, fake, 4, 0, None) == -1
+    assert L.okvq_append(ctypes.byref(cache), lens0, fake, fake, fake, n_new, fake, 4,
+                         okvq.OKVQ_GLOBAL_ROTATION, None) == -2
+    full = (ctypes.c_int32 * 2)(62, 0)
+    assert L.okvq_append(ctypes.byref(cache), full, fake, fake, fake, n_new, fake, 4, 0, None) == -3
     q_lens = (ctypes.c_int32 * 2)(64, 64)
     need = okvq.okvq_decode_workspace_bytes(d, 64)
     assert L.okvq_decode_attention(ctypes.byref(cache), q_lens, fake, ctypes.c_float(0.1), 0, fake, fake, need - 1,

@@ -192,3 +192,76 @@ def test_ladder_values_matrix_core_mode(bits):
     live = [b for b, L in enumerate(lens) if L > 0]
     assert np.all(out[2] == 0)
     assert gh.attention_close(out[live], dref[live]) <= TOL
+
+
+APPEND_CASES = [(2, 2, "fp16"), (3, 3, "fp16"), (4, 4, "fp16"), (2, 4, "fp16"), (3, 2, "turboquant"),
+                (4, 4, "turboquant")]
+APPEND_PLANS = {
+    "one_shot": [[1000, 333, 64, 0]],
+    "ragged_chunks": [[7, 1, 31, 0], [1, 40, 2, 0], [100, 3, 5, 0], [31, 200, 26, 0], [900, 100, 0, 0]],
+    "single_tokens_then_bulk": [[1, 1, 1, 0]] * 40 + [[1000, 1000, 1000, 0]],
+}
+
+
+@pytest.mark.parametrize("plan_name", list(APPEND_PLANS))
+@pytest.mark.parametrize("kb,vb,meta", APPEND_CASES, ids=[f"K{a}V{b}_{m}" for a, b, m in APPEND_CASES])
+def test_ladder_append_chunked_equals_oracle(kb, vb, meta, plan_name):
+    """Appending in any chunking gives the bytes of the one-shot oracle quantization: the method's
+    keys re-quantize the open window from the stage, which then holds the raw keys of the new open
+    window; TurboQuant keys and values are per token. An empty sequence stays empty."""
+    import gpu_helpers as gh
+    import paper_2609_11582_amd as okvq
+    import torch
+    lens = [1000, 333, 64, 0]
+    wl = workload("omni7b_32k")
+    lay = gen_layer(wl, 6, lengths=np.asarray(lens, np.int32), n_tokens=max(lens))
+    k, v = lay["k"][:, :2].copy(), lay["v"][:, :2].copy()
+    k[0, 1, 40] = 0                       # a zero-norm key inside a window
+    k[1, 0, 64:96, :] = np.float16(60000)  # saturated norm, zero-range window
+    cap = 1024
+    cache = okvq.KVCache(len(lens), 2, 14, cap, torch.from_numpy(lay["signs"]),
+                         torch.from_numpy(np.ascontiguousarray(lay["rot"], np.float32)), key_meta=meta,
+                         key_bits=kb, value_bits=vb)
+    _announce(f"ladder append K{kb}V{vb} {meta} plan={plan_name}")
+    done = gh.append_chunks(cache, k, v, lay["modality"], lens, APPEND_PLANS[plan_name], exact=True)
+    assert list(done) == lens
+    got = _arrays(cache)
+    assert np.array_equal(cache.views()["seq_lens"].cpu().numpy(), np.asarray(lens, np.int32))
+    ref = quantize_layer_bits(k, v, lay["modality"], lens, lay["signs"], lay["rot"], cap, kb, vb, meta)
+    for name in ref:
+        _same(got[name], ref[name], name)
+    if meta == "fp16":
+        for b, L in enumerate(lens):
+            o = (L // 32) * 32
+            np.testing.assert_array_equal(got["k_stage"][b, :, :L - o].view(np.uint16), k[b, :, o:L].view(np.uint16))
+
+
+@pytest.mark.parametrize("kb,vb,meta", [(3, 3, "fp16"), (4, 2, "turboquant")], ids=["K3V3_fp16", "K4V2_turboquant"])
+def test_ladder_append_mfma_equals_stateless_then_decode(kb, vb, meta):
+    """Matrix-core values: a chunked append writes the bytes of the stateless matrix-core call
+    (the codes of a token depend on its row alone); decode of the appended cache then matches the
+    oracle, at every step of a streaming append."""
+    import gpu_helpers as gh
+    import paper_2609_11582_amd as okvq
+    import torch
+    lens = [777, 96]
+    wl = workload("omni3b_b4_64k_stream")
+    lay = gen_layer(wl, 1, lengths=np.asarray(lens, np.int32), n_tokens=max(lens))
+    k, v = lay["k"][:, :2].copy(), lay["v"][:, :2].copy()
+    cap = 1024
+    cache = okvq.KVCache(2, 2, 16, cap, torch.from_numpy(lay["signs"]),
+                         torch.from_numpy(np.ascontiguousarray(lay["rot"], np.float32)), key_meta=meta,
+                         key_bits=kb, value_bits=vb)
+    _announce(f"ladder append mfma K{kb}V{vb} {meta}")
+    cur = np.zeros(2, np.int64)
+    for s, step in enumerate([[13, 5], [300, 50], [464, 41]]):
+        cur = gh.append_chunks_from(cache, k, v, lay["modality"], cur, np.minimum(step, np.asarray(lens) - cur))
+        q = gen_queries(wl.wid, 1, 2, 16, step=s + 1)
+        out = gh.decode(cache, q, cur.tolist())
+        ref = decode_layer_bits(_arrays(cache), q, cur.tolist(), lay["signs"], lay["rot"], SM, kb, vb)
+        assert gh.attention_close(out, ref) <= TOL
+    st = gh.ladder_cache(k, v, lay["modality"], lens, lay["signs"], lay["rot"], cap, 16, kb, vb, meta, value_flags=0)
+    got, want = _arrays(cache), _arrays(st)
+    for name in want:
+        if name != "k_stage":
+            _same(got[name], want[name], name)
