@@ -13,7 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libokvq.so")
 SOURCES = ["api.hip", "codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "calib_kernels.hip",
-           "dense_decode.hip", "ladder_codec.hip", "ladder_decode.hip"]
+           "dense_decode.hip", "ladder_codec.hip", "ladder_decode.hip", "append_window.hip"]
 
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
@@ -37,7 +37,10 @@ def hipcc() -> str:
 # per-source additions: the decode kernels (packed and dense) never see NaN (finite inputs; -inf is the only special
 # value they use), so min / max need no NaN quieting
 EXTRA = {"decode_kernels.hip": ["-fno-honor-nans"], "dense_decode.hip": ["-fno-honor-nans"],
-         "ladder_decode.hip": ["-fno-honor-nans"]}
+         "ladder_decode.hip": ["-fno-honor-nans"],
+         # the window append takes window minima and maxima of finite directions (finite inputs are part of the
+         # device data contract)
+         "append_window.hip": ["-fno-honor-nans"]}
 
 
 def build(verbose: bool = False, jobs: int = 4) -> str:

@@ -1,6 +1,7 @@
 // C ABI of the okvq library: argument validation, launch planning and the fixed codebook.
 // Declarations and contracts: include/okvq.h.
 #include <algorithm>
+#include <cstdlib>
 #include <cmath>
 #include <cstring>
 #include <mutex>
@@ -219,6 +220,9 @@ void jacobi_eigen(std::vector<double>& a, std::vector<double>& u, std::vector<do
 }
 
 // Tiles of 256 tokens covering `span` tokens from each sequence's first open window.
+// Appends touching at most this many key windows of a sequence take the window-parallel launch.
+constexpr int kWindowPathMaxWindows = 64;
+
 void plan_tiles(CodecArgs& a, int nb, int span) {
   a.ntx = (span + 255) / 256;
   a.ntiles = a.ntx * a.j.H * nb;
@@ -543,7 +547,20 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
   if (is_ladder(&d)) return span > 0 ? ladder_append(cache, lens_host, k_new, v_new, mod_new, n_new_host, n_new_dev, n_max,
                                                      exact, s)
                                      : OKVQ_OK;
-  if (d.residual && span > 0) {  // the fp16 rows, before the codec advances the lengths
+  // Appends that touch few key windows per sequence take the window-parallel launch (codecs,
+  // residual rings and lengths in one launch); larger ones the tile launch, which streams longer
+  // spans at higher throughput. Both write the same bytes.
+  int nwin = 0;  // key windows from the open window to the new end, largest over sequences
+  for (int b = 0; b < d.batch; ++b) {
+    const int L = lens_host[b], n = n_new_host[b];
+    if (n > 0) nwin = std::max(nwin, (L + n + kW - 1) / kW - L / kW);
+  }
+  bool window_path = !exact && !is_mx(&d) && nwin <= kWindowPathMaxWindows;
+  if (const char* env = getenv("OKVQ_APPEND_PATH")) {  // "window" / "tile": force a path (tests, timing)
+    if (!strcmp(env, "tile")) window_path = false;
+    if (!strcmp(env, "window") && !exact && !is_mx(&d)) window_path = true;
+  }
+  if (d.residual && span > 0 && !window_path) {  // the fp16 rows, before the codec advances the lengths
     if ((int64_t)d.batch * d.num_kv_heads > INT32_MAX) return OKVQ_ERR_UNSUPPORTED;
     st = hip_status(launch_residual_store(k_new, v_new, n_max, cache->seq_lens, n_new_dev, d.batch, d.num_kv_heads,
                                           d.capacity, cache->k_res, cache->v_res, s));
@@ -598,7 +615,18 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
       a.seq_lens_out = cache->seq_lens;
       a.ticket = reinterpret_cast<uint32_t*>(cache->seq_lens + d.batch);
       a.status = cache->seq_lens + d.batch + 1;
-      st = hip_status(launch_codec(a, true, true, s));
+      if (window_path) {
+        a.k_res = d.residual ? cache->k_res : nullptr;
+        a.v_res = d.residual ? cache->v_res : nullptr;
+        int chunk_nwin = 0;
+        for (int i = 0; i < nb; ++i) {
+          const int L = lens_host[b0 + i], n = n_new_host[b0 + i];
+          if (n > 0) chunk_nwin = std::max(chunk_nwin, (L + n + kW - 1) / kW - L / kW);
+        }
+        st = hip_status(launch_append_window(a, chunk_nwin, nb, s));
+      } else {
+        st = hip_status(launch_codec(a, true, true, s));
+      }
     }
     if (st != OKVQ_OK) return st;
   }

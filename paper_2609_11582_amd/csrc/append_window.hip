@@ -1,0 +1,449 @@
+// Window-parallel append: the key and value codecs of one append, the fp16 residual rings and the
+// length update in a single launch, for appends that touch few key windows per (sequence, KV head)
+// -- a generation step, a streamed chunk (Sec. 2.1 Eq. 2 and Sec. 2.3 Eq. 4 for keys; Sec. 2.3
+// Eq. 6 with the codebook of Eq. 3 for values; the residual rings of the captioning protocol, Sec.
+// 3.1). The results are the bytes of the tile codec (codec_fused.hip): the same operations in the
+// same order, spread over more lanes so that the chain from the rows to the codes is short.
+//
+// Work unit: one 32-token key window of one (sequence, KV head), from the open window
+// 32 floor(L / 32) to the new end; a work-group of 512 threads. Thread (t, j) = (tid / 16,
+// tid % 16) holds channels 8j .. 8j + 7 of window token t, for its key and for its value:
+//  * key: sign flip, fp16 norm by the halving tree (levels 64 .. 8 across the 16 lanes of the
+//    token, 4 .. 1 in the lane), butterflies h = 1, 2, 4 in the lane and h = 8 .. 64 across lanes,
+//    z = w fl(kappa / n16); window minimum and maximum per channel over the token groups of a wave,
+//    then over the waves through LDS; codes and their packing in the lane, one key-code dword per
+//    lane pair;
+//  * value: fp16 norm by the same tree; the row goes to an LDS tile of MFMA A operands; wave w then
+//    forms output channels 16w .. 16w + 15 of the window's 32 tokens on the matrix cores (R_m as
+//    fp16 hi + lo B operands, fp32 accumulation, in the tile codec's order), one modality at a time,
+//    and writes their code bytes.
+// Older tokens of the open window come from the key stage; their key codes are rewritten with the
+// window's new minimum and step, their value codes are kept. The work-group of the first window, the
+// only one that reads the stage, rewrites it with the raw rows of the new open window after a
+// barrier that follows its reads. The last work-group to finish advances the lengths.
+#include "launch.hpp"
+
+namespace okvq {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 512;
+static_assert(kMaxLenArgs <= kThreads, "one thread per sequence of the launch for the length update");
+
+// lane l <- lane l ^ m inside the 16-lane rows, all by DPP (no LDS-pipe shuffle): m = 1, 2 by quad
+// permutations, m = 8 by a row rotation by 8, m = 4 by rotations by 12 (lanes 0-3, 8-11 take lane
+// + 4) and by 4 (lanes 4-7, 12-15 take lane - 4) restricted to those banks
+template <int kMask>
+__device__ __forceinline__ float xchg(float v) {
+  static_assert(kMask == 1 || kMask == 2 || kMask == 4 || kMask == 8, "lane mask within a row");
+  const int x = __builtin_bit_cast(int, v);
+  if constexpr (kMask == 1) return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xf, 0xf, true));
+  if constexpr (kMask == 2) return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xf, 0xf, true));
+  if constexpr (kMask == 8) return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, x, 0x128, 0xf, 0xf, true));
+  if constexpr (kMask == 4) {
+    const int up = __builtin_amdgcn_update_dpp(0, x, 0x12C, 0xf, 0x5, true);  // row_ror:12 into banks 0, 2
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(up, x, 0x124, 0xf, 0xA, true));  // row_ror:4, banks 1, 3
+  }
+}
+
+__device__ __forceinline__ uint32_t xchg_u(uint32_t v) {  // lane l ^ 1
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xf, 0xf, true);
+}
+
+// The values of lanes l and l ^ 16 (kRow = 16) or l ^ 32 (kRow = 32) through the VALU row swaps
+// of gfx950: swapping a register with a copy of itself leaves the lane's own value in one result
+// and its partner's in the other (the copy is opaque: given the same value twice, the compiler
+// would fold the two results into one).
+template <int kRow>
+__device__ __forceinline__ void row_pair(float v, float& a, float& b) {
+  uint32_t u = __builtin_bit_cast(uint32_t, v), c = u;
+  __asm__ volatile("" : "+v"(c));
+  if constexpr (kRow == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(u, c, false, false);
+    a = __builtin_bit_cast(float, (uint32_t)r[0]);
+    b = __builtin_bit_cast(float, (uint32_t)r[1]);
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(u, c, false, false);
+    a = __builtin_bit_cast(float, (uint32_t)r[0]);
+    b = __builtin_bit_cast(float, (uint32_t)r[1]);
+  }
+}
+
+// fp16 norm of the token held by a 16-lane group (lane j: channels 8j .. 8j + 7) by the halving
+// tree t <- t[:n/2] + t[n/2:]: the levels 64, 32, 16, 8 pair lane j with lane j ^ 8, 4, 2, 1 (both
+// lanes of a pair form the same sum), the levels 4, 2, 1 stay in the lane. Squares of fp16 values
+// are exact. Every lane of the group ends with the norm.
+__device__ __forceinline__ uint32_t group_norm(const float (&x)[8]) {
+  float t[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float p = xchg<8>(x[e]);
+    t[e] = x[e] * x[e] + p * p;
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) t[e] = t[e] + xchg<4>(t[e]);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) t[e] = t[e] + xchg<2>(t[e]);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) t[e] = t[e] + xchg<1>(t[e]);
+#pragma unroll
+  for (int n = 4; n >= 1; n >>= 1) {
+#pragma unroll
+    for (int e = 0; e < n; ++e) t[e] = t[e] + t[e + n];
+  }
+  return norm_to_f16(sqrt_rn(t[0]));
+}
+
+// Butterfly stage across lanes j and j ^ m of a group: the lower lane takes a + b, the upper one
+// a - b, both as fl(s own + partner) with s = +-1 (an exact product, one rounding).
+template <int kMask>
+__device__ __forceinline__ void cross_stage(float (&x)[8], int j) {
+  const float s = (j & kMask) ? -1.0f : 1.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = __builtin_fmaf(s, x[e], xchg<kMask>(x[e]));
+}
+
+// c ? u : v, component by component (a select of whole vectors becomes one of their addresses)
+__device__ __forceinline__ uint4 select4(bool c, uint4 u, uint4 v) {
+  return make_uint4(c ? u.x : v.x, c ? u.y : v.y, c ? u.z : v.z, c ? u.w : v.w);
+}
+
+// floor(x) as an integer in one instruction (v_cvt_flr_i32_f32)
+__device__ __forceinline__ int floor_to_int(float x) {
+  int r;
+  __asm__("v_cvt_flr_i32_f32 %0, %1" : "=v"(r) : "v"(x));
+  return r;
+}
+
+struct WindowShared {
+  uint4 atile[2][4][64];   // the window's value rows as MFMA A operands: [row block][k-block][lane]
+  float kpart[8][2][kD];   // per wave: the channel minimum and maximum over its 4 tokens
+  float2 kstat[kD];        // per channel: (fp16 minimum, fl(1 / fp16 step)) as fp32
+  float itab[kW];          // per token: fl(1 / T) of the value decision (0: no code)
+  uint32_t tmod[kW];       // per token: the rotation of its value code (3: none)
+  uint32_t last;
+};
+
+// The inputs of thread (t, j) for the window wi of a sequence whose new tokens are [begin, len).
+// The row loads are not predicated per lane: a lane without a row of its own reads the nearest row
+// of its sequence (clamped index, so that lanes spread over distinct rows rather than all meeting on
+// one cache line) and drops what it read; no branch separates the loads from each other. The stage
+// is read only by the first window, and only when it holds older tokens.
+struct WindowInputs {
+  uint4 kraw, vraw;  // key chunk (from the stage below begin), value chunk (new tokens only)
+  uint4 sraw;        // first window, if the new open window starts after it: the key chunk of
+                     // token open + t
+  uint32_t mod;      // modality id of window token t (3: not a new token); lanes 0..31 of every
+  uint32_t wmod;     // wave also read that of window token `lane`, for the modality set
+};
+
+__device__ __forceinline__ WindowInputs window_inputs(const CodecArgs& a, size_t seq, int b, int begin, int len,
+                                                      int wi, int t, int j, int lane) {
+  const CodecJob& J = a.j;
+  WindowInputs in;
+  const int first = (begin / kW) * kW, w0 = first + kW * wi;
+  const size_t mrow = (size_t)b * J.n_rows, srow = seq * J.n_rows;
+  const int last = J.n_rows - 1;
+  const int wtok = w0 + (lane & 31), tok = w0 + t;
+  const bool wfresh = wtok >= begin && wtok < len, fresh = tok >= begin && tok < len;
+  const uint32_t wm = J.msrc[mrow + min(max(wtok - begin, 0), last)];
+  const size_t row = srow + (size_t)min(max(tok - begin, 0), last);
+  const uint32_t tm = J.msrc[mrow + (row - srow)];
+  const uint4 kn = reinterpret_cast<const uint4*>(J.src + row * kD)[j];
+  const uint4 vn = reinterpret_cast<const uint4*>(a.vsrc + row * kD)[j];
+  const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+  in.kraw = select4(fresh, kn, zero);
+  in.vraw = select4(fresh, vn, zero);
+  in.mod = fresh ? tm : 3u;
+  in.wmod = wfresh ? wm : 3u;
+  if (wi == 0 && begin > first) {  // uniform: older tokens of the open window, from the stage
+    const uint4 ks = reinterpret_cast<const uint4*>(J.stage + (seq * kW + min(t, begin - first - 1)) * kD)[j];
+    in.kraw = select4(tok < begin, ks, in.kraw);
+  }
+  in.sraw = zero;
+  const int open = (len / kW) * kW, stok = open + t;
+  if (wi == 0 && open != first && open < len) {  // uniform
+    in.sraw = reinterpret_cast<const uint4*>(J.src + (srow + (size_t)min(max(stok - begin, 0), last)) * kD)[j];
+  }
+  return in;
+}
+
+template <int kMeta>
+__global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
+  static_assert(kMeta == kMetaFp16 || kMeta == kMetaTq, "fp16 window metadata or TurboQuant keys");
+  __shared__ WindowShared sh;
+  const CodecJob& J = a.j;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int t = tid >> 4, j = tid & 15;  // window token, channel chunk
+  const int wi = blockIdx.x, h = blockIdx.y, bz = blockIdx.z, b = J.b0 + bz;
+  const size_t seq = (size_t)b * J.H + h;
+  // the device lengths decide, clamped into the buffers (the host's copy planned the grid)
+  const int begin = min(max(J.begin_dev[b], 0), J.cap);
+  const int len = min(begin + min(max(J.count_dev[b], 0), J.n_rows), J.cap);
+  const int first = (begin / kW) * kW;
+  const int w0 = first + kW * wi;  // the work-group's window
+  if (len > begin && w0 < len) {   // uniform
+    const WindowInputs in = window_inputs(a, seq, b, begin, len, wi, t, j, lane);
+    const int tok = w0 + t;
+    const bool valid = tok < len, fresh = valid && tok >= begin;
+    const uint4 kraw = in.kraw, vraw = in.vraw, sraw = in.sraw;
+    const uint32_t mymod = in.mod;
+    const uint2 sg = *reinterpret_cast<const uint2*>(a.signs + 8 * j);
+    const int open = (len / kW) * kW;
+    const bool restage = J.stage && wi == 0 && open < len;
+    const int stok = open + t;
+    // ---- key direction (thread = token chunk); a wave without a valid token skips the arithmetic ----
+    const bool key_busy = __ballot(valid) != 0, value_busy = __ballot(fresh) != 0;  // wave-uniform
+    float x[8];
+    uint32_t kn16 = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+    if (key_busy) {
+      const uint32_t r4[4] = {kraw.x, kraw.y, kraw.z, kraw.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t w = (i < 2) ? sg.x : sg.y;  // int8 signs of channels 8j + 4 (i / 2) .. + 3
+        const uint32_t m = (i & 1) ? (((w & 0x00800000u) >> 8) | (w & 0x80000000u))
+                                   : (((w & 0x00000080u) << 8) | ((w & 0x00008000u) << 16));
+        const uint32_t r = r4[i] ^ m;
+        x[2 * i] = h2f(r & 0xffffu);
+        x[2 * i + 1] = h2f(r >> 16);
+      }
+      kn16 = group_norm(x);
+#pragma unroll
+      for (int hh = 1; hh < 8; hh <<= 1) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if ((e & hh) == 0) {
+            const float p = x[e], q = x[e + hh];
+            x[e] = p + q;
+            x[e + hh] = p - q;
+          }
+        }
+      }
+      cross_stage<1>(x, j);  // h = 8
+      cross_stage<2>(x, j);  // h = 16
+      cross_stage<4>(x, j);  // h = 32
+      cross_stage<8>(x, j);  // h = 64
+      const float cinv = (kn16 == 0) ? 0.0f : div_rn(kKappa, h2f(kn16));
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = x[e] * cinv;
+    }
+
+    // ---- value norm, A tile, per-token tables ----
+    {
+      const uint32_t r4[4] = {vraw.x, vraw.y, vraw.z, vraw.w};
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[2 * i] = h2f(r4[i] & 0xffffu);
+        v[2 * i + 1] = h2f(r4[i] >> 16);
+      }
+      const uint32_t vn16 = value_busy ? group_norm(v) : 0u;  // 0 for the zero rows of older and padded tokens
+      sh.atile[t >> 4][j >> 2][16 * (j & 3) + (t & 15)] = vraw;
+      if (j == 0) {
+        const uint32_t mt = (vn16 != 0 && mymod <= 2u) ? (J.global_rot ? 0u : mymod) : 3u;
+        sh.itab[t] = (vn16 != 0) ? __builtin_amdgcn_rcpf(h2f(vn16) * a.th.t2) : 0.0f;
+        sh.tmod[t] = mt;
+        if (tok >= begin) a.v_norm[seq * J.cap + tok] = (uint16_t)vn16;  // 0 in the padded slots
+        if (fresh && a.mod_out && h == 0) a.mod_out[(size_t)b * J.cap + tok] = (uint8_t)mymod;
+      }
+    }
+    // residual rings: the raw rows of the new tokens among the last 128
+    if (a.k_res && fresh && tok >= len - kResidual) {
+      const size_t rr = (seq * kResidual + (tok & (kResidual - 1))) * kD;
+      reinterpret_cast<uint4*>(a.k_res + rr)[j] = kraw;
+      reinterpret_cast<uint4*>(a.v_res + rr)[j] = vraw;
+    }
+
+    // ---- window minimum / maximum: the wave's 4 tokens, then the 8 waves through LDS ----
+    if constexpr (kMeta == kMetaFp16) {
+      float lo[8], hi[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        lo[e] = valid ? x[e] : __builtin_inff();
+        hi[e] = valid ? x[e] : -__builtin_inff();
+      }
+      float p, q;
+      if (key_busy) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          row_pair<16>(lo[e], p, q);
+          lo[e] = __builtin_fminf(p, q);
+          row_pair<16>(hi[e], p, q);
+          hi[e] = __builtin_fmaxf(p, q);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          row_pair<32>(lo[e], p, q);
+          lo[e] = __builtin_fminf(p, q);
+          row_pair<32>(hi[e], p, q);
+          hi[e] = __builtin_fmaxf(p, q);
+        }
+      }
+      if (lane < 16) {
+        float4* pl = reinterpret_cast<float4*>(&sh.kpart[wave][0][8 * j]);
+        float4* ph = reinterpret_cast<float4*>(&sh.kpart[wave][1][8 * j]);
+        pl[0] = make_float4(lo[0], lo[1], lo[2], lo[3]);
+        pl[1] = make_float4(lo[4], lo[5], lo[6], lo[7]);
+        ph[0] = make_float4(hi[0], hi[1], hi[2], hi[3]);
+        ph[1] = make_float4(hi[4], hi[5], hi[6], hi[7]);
+      }
+    }
+    // the window's modalities (a superset of those coded) and the B operands of the first of them,
+    // in flight across the barrier and the window statistics
+    uint32_t mset = 0;
+#pragma unroll
+    for (int m = 0; m < 3; ++m)
+      if (__ballot(in.wmod == (uint32_t)m)) mset |= 1u << m;
+    if (J.global_rot) mset = mset ? 1u : 0u;  // R_0 for every token
+    const int m_first = mset ? __builtin_ctz(mset) : 0;
+    uint4 bf[4][2];
+    {
+      const uint4* base = a.rotfrag + (size_t)(m_first * 8 + wave) * 8 * 64 + lane;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int part = 0; part < 2; ++part) bf[kk][part] = base[(kk * 2 + part) * 64];
+    }
+    if (restage) __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stage reads have landed
+    __syncthreads();  // B1: partials, A tile and token tables written; every stage read has landed
+
+    if (restage && stok >= begin && stok < len)  // the new open window's raw keys
+      reinterpret_cast<uint4*>(J.stage + (seq * kW + t) * kD)[j] = select4(open == first, kraw, sraw);
+
+    const size_t nw = J.cap / kW;
+    const int gwin = w0 / kW;
+    if constexpr (kMeta == kMetaFp16) {
+      if (tid < kD) {
+        float l = sh.kpart[0][0][tid], u = sh.kpart[0][1][tid];
+#pragma unroll
+        for (int w = 1; w < 8; ++w) {
+          l = __builtin_fminf(l, sh.kpart[w][0][tid]);
+          u = __builtin_fmaxf(u, sh.kpart[w][1][tid]);
+        }
+        l = l + 0.0f;  // canonical +0
+        u = u + 0.0f;
+        const float step = div_rn(u - l, 3.0f);
+        const uint32_t m16 = f2h(l), s16 = f2h(step);
+        a.k_min[(seq * nw + gwin) * kD + tid] = (uint16_t)m16;
+        a.k_step[(seq * nw + gwin) * kD + tid] = (uint16_t)s16;
+        sh.kstat[tid] = make_float2(h2f(m16), (s16 == 0) ? 0.0f : div_rn(1.0f, h2f(s16)));
+      }
+      __syncthreads();  // B2: window statistics
+    }
+
+    // ---- key codes: 2 bits per channel; word u of a token holds channels 16u .. 16u + 15, the even
+    // ones in its low half; this lane fills bits 8 (j & 1) .. + 7 of both halves of word j / 2 ----
+    uint32_t lo16 = 0, hi16 = 0;
+    if (valid) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int sh2 = 2 * (4 * (j & 1) + i);
+        uint32_t c0, c1;
+        if constexpr (kMeta == kMetaFp16) {
+          const float4 s = *reinterpret_cast<const float4*>(&sh.kstat[8 * j + 2 * i]);
+          constexpr float kRound = 8388608.0f;  // 2^23: rint of the clamped value in the low bits
+          const float t0 = (x[2 * i] - s.x) * s.y;
+          const float t1 = (x[2 * i + 1] - s.z) * s.w;
+          c0 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_fmed3f(t0, 0.0f, 3.0f) + kRound) & 3u;
+          c1 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_fmed3f(t1, 0.0f, 3.0f) + kRound) & 3u;
+        } else {
+          const float z0 = x[2 * i], z1 = x[2 * i + 1];
+          c0 = (uint32_t)(z0 > a.th.t0) + (uint32_t)(z0 > a.th.t1) + (uint32_t)(z0 > a.th.t2);
+          c1 = (uint32_t)(z1 > a.th.t0) + (uint32_t)(z1 > a.th.t1) + (uint32_t)(z1 > a.th.t2);
+        }
+        lo16 |= c0 << sh2;
+        hi16 |= c1 << sh2;
+      }
+    }
+    uint32_t word = lo16 | (hi16 << 16);
+    word |= xchg_u(word);
+    if ((j & 1) == 0) reinterpret_cast<uint32_t*>(a.k_codes + (seq * J.cap + tok) * 32)[j >> 1] = word;
+    if (j == 0) a.k_norm[seq * J.cap + tok] = valid ? (uint16_t)kn16 : (uint16_t)0;
+
+    // ---- value codes: wave w takes output channels 16w .. 16w + 15 of the 32 tokens ----
+    {
+      const int g = lane >> 4;
+      const uint32_t tm = sh.tmod[lane & 31];
+      uint32_t vb[2] = {0u, 0u};
+#pragma unroll 1
+      for (int m = m_first; m < 3; ++m) {
+        const uint32_t mb = (uint32_t)__ballot(tm == (uint32_t)m);  // token bits, lanes 0..31
+        if (mb == 0) continue;
+        if (m != m_first) {
+          const uint4* base = a.rotfrag + (size_t)(m * 8 + wave) * 8 * 64 + lane;
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+            for (int part = 0; part < 2; ++part) bf[kk][part] = base[(kk * 2 + part) * 64];
+        }
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+          floatx4 y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk) {
+            const half8 xa = __builtin_bit_cast(half8, sh.atile[rb][kk][lane]);
+#pragma unroll
+            for (int part = 0; part < 2; ++part)
+              y = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa, __builtin_bit_cast(half8, bf[kk][part]), y, 0, 0, 0);
+          }
+          const float4 it = *reinterpret_cast<const float4*>(&sh.itab[16 * rb + 4 * g]);
+          const float iv[4] = {it.x, it.y, it.z, it.w};
+          uint32_t byte = 0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) byte |= (uint32_t)(min(max(floor_to_int(y[i] * iv[i]), -2), 1) + 2) << (2 * i);
+          const uint32_t b4 = (mb >> (16 * rb + 4 * g)) & 15u;  // the quad's tokens of modality m
+          const uint32_t keep = ((b4 & 1u) | ((b4 & 2u) << 1) | ((b4 & 4u) << 2) | ((b4 & 8u) << 3)) * 3u;
+          vb[rb] |= byte & keep;
+        }
+      }
+      uint8_t* blk = a.v_codes + (seq * nw + gwin) * 1024 + 16 * lane + wave;
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        uint32_t v = vb[rb];
+        const int old = min(max(begin - (w0 + 16 * rb + 4 * g), 0), 4);  // older tokens of the quad keep their bits
+        if (old > 0) {
+          const uint32_t k = (1u << (2 * old)) - 1u;
+          v = ((uint32_t)blk[8 * rb] & k) | (v & ~k);
+        }
+        blk[8 * rb] = (uint8_t)v;
+      }
+    }
+  }
+
+  // The lengths advance once every work-group has read them: each work-group counts itself after
+  // all its threads are done; the last one writes the new lengths and clears the counter.
+  __syncthreads();
+  if (tid == 0) {
+    const uint32_t total = gridDim.x * gridDim.y * gridDim.z;
+    sh.last = (__hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == total - 1) ? 1u : 0u;
+  }
+  __syncthreads();
+  if (sh.last) {
+    // The counts are read only here: vector reads of the lengths' cache line at the start of every
+    // work-group, while the counter's atomics hit that line, made a 4096-work-group launch 4x slower.
+    const int nseq = gridDim.z;
+    if (tid < nseq) a.seq_lens_out[J.b0 + tid] += J.count_dev[J.b0 + tid];
+    if (tid == 0) __hip_atomic_store(a.ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_append_window(const CodecArgs& a, int nwin, int nb, hipStream_t s) {
+  if (nwin <= 0 || nb <= 0) return hipSuccess;
+  const dim3 grid(nwin, a.j.H, nb);
+  if (a.key_meta == kMetaTq)
+    hipLaunchKernelGGL(k_append_window<kMetaTq>, grid, dim3(kThreads), 0, s, a);
+  else if (a.key_meta == kMetaFp16)
+    hipLaunchKernelGGL(k_append_window<kMetaFp16>, grid, dim3(kThreads), 0, s, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace okvq

@@ -146,7 +146,8 @@ def test_append_and_decode_beyond_256_sequences():
 def test_append_reports_a_value_wait_that_gave_up(monkeypatch):
     """The value codec's waves wait for each other with a bounded number of polls. Forced from the
     host to give up at once (OKVQ_CODEC_SPIN_LIMIT=0, no poll), every kernel still ends normally and
-    the append marks the cache's status word; a normal append leaves it at zero."""
+    the append marks the cache's status word; a normal append leaves it at zero. (The tile launch
+    holds the only such wait: the test forces it for these medium-sized appends.)"""
     import torch
 
     import gpu_helpers as gh
@@ -156,6 +157,7 @@ def test_append_reports_a_value_wait_that_gave_up(monkeypatch):
     lay = gen_layer(wl, 0, lengths=np.asarray(lens, np.int32), n_tokens=max(lens))
     k, v = lay["k"][:, :2].copy(), lay["v"][:, :2].copy()
     cache = gh.new_cache(2, 2, 14, 1024, lay["signs"], lay["rot"])
+    monkeypatch.setenv("OKVQ_APPEND_PATH", "tile")
     print("[gpu-case] append, normal wait", flush=True)
     gh.append_chunks(cache, k, v, lay["modality"], lens, [[256, 256]])
     assert okvq.okvq_cache_status(cache) == 0
