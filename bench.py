@@ -513,12 +513,30 @@ def stream_measurement(okvq, torch, np, dev, stream):
     torch.cuda.synchronize()
     app = [e[0].elapsed_time(e[1]) * 1e3 for e in ev]
     dec = [e[1].elapsed_time(e[2]) * 1e3 for e in ev]
+    # device-side append latency: the GPU is kept busy while the host enqueues each timed append, so
+    # that the events bracket the launch alone (the lengths are set back between the calls)
+    L0 = N + (steps - 1) * step  # the last chunk again, from the length before it
+    back = torch.tensor([L0] * B, dtype=torch.int32, device=dev)
+    c.buffers["seq_lens"][:B].copy_(back)
+    dev_app = []
+    for s in range(10):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(200000)
+        e0.record(stream)
+        okvq.okvq_append(c, [L0] * B, kn[steps - 1], vn[steps - 1], mods[steps - 1], [step] * B, nn, step,
+                         stream=stream)
+        e1.record(stream)
+        c.buffers["seq_lens"][:B].copy_(back)
+        dev_app.append((e0, e1))
+    torch.cuda.synchronize()
+    dev_app_us = float(np.median([a.elapsed_time(b) for a, b in dev_app[2:]])) * 1e3
     mean_len = N + step * (steps + 1) / 2
     abytes = append_algorithmic_bytes(B, H, [step] * B)
     dbytes = decode_algorithmic_bytes(B, H, Hq, [int(mean_len)] * B)
     res = {"workload": "omni3b_b4_64k_stream", "batch": B, "kv_heads": H, "q_heads": Hq, "prefill": N,
            "steps": steps, "tokens_per_step": step,
            "append_us": round(float(np.mean(app[1:])), 2), "append_GBps": round(abytes / np.mean(app[1:]) / 1e3, 1),
+           "append_device_us": round(dev_app_us, 2),
            "decode_us": round(float(np.mean(dec[1:])), 2), "decode_GBps_warm": round(dbytes / np.mean(dec[1:]) / 1e3, 1),
            "step_us": round(float(np.mean([a + d for a, d in zip(app[1:], dec[1:])])), 2),
            "append_algorithmic_bytes": abytes}
@@ -783,6 +801,19 @@ def residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
         app1.append((e0, e1))
     torch.cuda.synchronize()
     append1_us = float(np.median([a.elapsed_time(b) for a, b in app1[5:]])) * 1e3
+    # the same with the GPU kept busy while the host enqueues the timed append (device-side latency)
+    app1d = []
+    for i in range(25):
+        c = caches[(3 * i + 2) % n_cache]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(200000)
+        e0.record(stream)
+        okvq.okvq_append(c, lens, k1, v1, m1, [1] * B, one, 1, stream=stream)
+        e1.record(stream)
+        c.buffers["seq_lens"][:B].copy_(back)
+        app1d.append((e0, e1))
+    torch.cuda.synchronize()
+    append1_dev_us = float(np.median([a.elapsed_time(b) for a, b in app1d[5:]])) * 1e3
     reps = []
     for rep in range(5):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -812,6 +843,7 @@ def residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
             "decode_GBps": round(dbytes / decode_us / 1e3, 2),
             "k_decode_us": round(split_us, 3), "k_decode_merge_residual_us": round(merge_us, 3),
             "append_prefill_us": round(append_us, 3), "append_one_token_us": round(append1_us, 3),
+            "append_one_token_device_us": round(append1_dev_us, 3),
             "algorithmic_bytes": dbytes, "replicas": n_cache}
 
 

@@ -220,8 +220,12 @@ void jacobi_eigen(std::vector<double>& a, std::vector<double>& u, std::vector<do
 }
 
 // Tiles of 256 tokens covering `span` tokens from each sequence's first open window.
-// Appends touching at most this many key windows of a sequence take the window-parallel launch.
+// Appends take the window-parallel launch when they touch at most 2 key windows of a sequence (a
+// generation step), or at most 64 windows and 2048 work-groups in all (a streamed chunk); longer
+// spans take the tile launch, whose throughput is higher (32768-token prefill of 4 KV heads:
+// 42 us against 61 us).
 constexpr int kWindowPathMaxWindows = 64;
+constexpr int64_t kWindowPathMaxGroups = 2048;
 
 void plan_tiles(CodecArgs& a, int nb, int span) {
   a.ntx = (span + 255) / 256;
@@ -555,7 +559,8 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
     const int L = lens_host[b], n = n_new_host[b];
     if (n > 0) nwin = std::max(nwin, (L + n + kW - 1) / kW - L / kW);
   }
-  bool window_path = !exact && !is_mx(&d) && nwin <= kWindowPathMaxWindows;
+  const int64_t nwg = (int64_t)nwin * d.num_kv_heads * d.batch;
+  bool window_path = !exact && !is_mx(&d) && (nwin <= 2 || (nwin <= kWindowPathMaxWindows && nwg <= kWindowPathMaxGroups));
   if (const char* env = getenv("OKVQ_APPEND_PATH")) {  // "window" / "tile": force a path (tests, timing)
     if (!strcmp(env, "tile")) window_path = false;
     if (!strcmp(env, "window") && !exact && !is_mx(&d)) window_path = true;
