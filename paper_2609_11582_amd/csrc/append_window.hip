@@ -7,12 +7,13 @@
 //
 // Work unit: one 32-token key window of one (sequence, KV head), from the open window
 // 32 floor(L / 32) to the new end; a work-group of 512 threads. Thread (t, j) = (tid / 16,
-// tid % 16) holds channels 8j .. 8j + 7 of window token t, for its key and for its value:
+// tid % 16) holds channels 8j .. 8j + 7 of the key of window token t and of the value of window
+// token 31 - t (so that in a window holding few new tokens, keys and values are worked on by
+// different waves; a wave without a token of its own skips the arithmetic):
 //  * key: sign flip, fp16 norm by the halving tree (levels 64 .. 8 across the 16 lanes of the
 //    token, 4 .. 1 in the lane), butterflies h = 1, 2, 4 in the lane and h = 8 .. 64 across lanes,
-//    z = w fl(kappa / n16); window minimum and maximum per channel over the token groups of a wave,
-//    then over the waves through LDS; codes and their packing in the lane, one key-code dword per
-//    lane pair;
+//    z = w fl(kappa / n16); window minimum and maximum per channel by LDS atomics; codes and their
+//    packing in the lane, one key-code dword per lane pair;
 //  * value: fp16 norm by the same tree; the row goes to an LDS tile of MFMA A operands; wave w then
 //    forms output channels 16w .. 16w + 15 of the window's 32 tokens on the matrix cores (R_m as
 //    fp16 hi + lo B operands, fp32 accumulation, in the tile codec's order), one modality at a time,
@@ -50,25 +51,6 @@ __device__ __forceinline__ float xchg(float v) {
 
 __device__ __forceinline__ uint32_t xchg_u(uint32_t v) {  // lane l ^ 1
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xf, 0xf, true);
-}
-
-// The values of lanes l and l ^ 16 (kRow = 16) or l ^ 32 (kRow = 32) through the VALU row swaps
-// of gfx950: swapping a register with a copy of itself leaves the lane's own value in one result
-// and its partner's in the other (the copy is opaque: given the same value twice, the compiler
-// would fold the two results into one).
-template <int kRow>
-__device__ __forceinline__ void row_pair(float v, float& a, float& b) {
-  uint32_t u = __builtin_bit_cast(uint32_t, v), c = u;
-  __asm__ volatile("" : "+v"(c));
-  if constexpr (kRow == 16) {
-    const auto r = __builtin_amdgcn_permlane16_swap(u, c, false, false);
-    a = __builtin_bit_cast(float, (uint32_t)r[0]);
-    b = __builtin_bit_cast(float, (uint32_t)r[1]);
-  } else {
-    const auto r = __builtin_amdgcn_permlane32_swap(u, c, false, false);
-    a = __builtin_bit_cast(float, (uint32_t)r[0]);
-    b = __builtin_bit_cast(float, (uint32_t)r[1]);
-  }
 }
 
 // fp16 norm of the token held by a 16-lane group (lane j: channels 8j .. 8j + 7) by the halving
@@ -117,9 +99,12 @@ __device__ __forceinline__ int floor_to_int(float x) {
   return r;
 }
 
+constexpr int kStatSlots = kD + kD / 8;
+
 struct WindowShared {
   uint4 atile[2][4][64];   // the window's value rows as MFMA A operands: [row block][k-block][lane]
-  float kpart[8][2][kD];   // per wave: the channel minimum and maximum over its 4 tokens
+  float kmin[kStatSlots];  // per channel c (slot c + c / 8, spread over the banks): the window
+  float kmax[kStatSlots];  // minimum and maximum, taken by LDS atomics
   float2 kstat[kD];        // per channel: (fp16 minimum, fl(1 / fp16 step)) as fp32
   float itab[kW];          // per token: fl(1 / T) of the value decision (0: no code)
   uint32_t tmod[kW];       // per token: the rotation of its value code (3: none)
@@ -132,11 +117,12 @@ struct WindowShared {
 // one cache line) and drops what it read; no branch separates the loads from each other. The stage
 // is read only by the first window, and only when it holds older tokens.
 struct WindowInputs {
-  uint4 kraw, vraw;  // key chunk (from the stage below begin), value chunk (new tokens only)
+  uint4 kraw;        // key chunk of window token t (from the stage below begin)
+  uint4 vraw;        // value chunk of window token 31 - t (new tokens only)
   uint4 sraw;        // first window, if the new open window starts after it: the key chunk of
                      // token open + t
-  uint32_t mod;      // modality id of window token t (3: not a new token); lanes 0..31 of every
-  uint32_t wmod;     // wave also read that of window token `lane`, for the modality set
+  uint32_t mod;      // modality id of window token 31 - t (3: not a new token); lanes 0..31 of
+  uint32_t wmod;     // every wave also read that of window token `lane`, for the modality set
 };
 
 __device__ __forceinline__ WindowInputs window_inputs(const CodecArgs& a, size_t seq, int b, int begin, int len,
@@ -149,14 +135,17 @@ __device__ __forceinline__ WindowInputs window_inputs(const CodecArgs& a, size_t
   const int wtok = w0 + (lane & 31), tok = w0 + t;
   const bool wfresh = wtok >= begin && wtok < len, fresh = tok >= begin && tok < len;
   const uint32_t wm = J.msrc[mrow + min(max(wtok - begin, 0), last)];
+  const int vtok = w0 + (kW - 1 - t);
+  const bool vfresh = vtok >= begin && vtok < len;
   const size_t row = srow + (size_t)min(max(tok - begin, 0), last);
-  const uint32_t tm = J.msrc[mrow + (row - srow)];
+  const size_t vrow = srow + (size_t)min(max(vtok - begin, 0), last);
+  const uint32_t tm = J.msrc[mrow + (vrow - srow)];
   const uint4 kn = reinterpret_cast<const uint4*>(J.src + row * kD)[j];
-  const uint4 vn = reinterpret_cast<const uint4*>(a.vsrc + row * kD)[j];
+  const uint4 vn = reinterpret_cast<const uint4*>(a.vsrc + vrow * kD)[j];
   const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
   in.kraw = select4(fresh, kn, zero);
-  in.vraw = select4(fresh, vn, zero);
-  in.mod = fresh ? tm : 3u;
+  in.vraw = select4(vfresh, vn, zero);
+  in.mod = vfresh ? tm : 3u;
   in.wmod = wfresh ? wm : 3u;
   if (wi == 0 && begin > first) {  // uniform: older tokens of the open window, from the stage
     const uint4 ks = reinterpret_cast<const uint4*>(J.stage + (seq * kW + min(t, begin - first - 1)) * kD)[j];
@@ -180,9 +169,19 @@ __global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
   const int t = tid >> 4, j = tid & 15;  // window token, channel chunk
   const int wi = blockIdx.x, h = blockIdx.y, bz = blockIdx.z, b = J.b0 + bz;
   const size_t seq = (size_t)b * J.H + h;
-  // the device lengths decide, clamped into the buffers (the host's copy planned the grid)
+  // The device lengths decide, clamped into the buffers (the host's copy planned the grid). (Loading
+  // the rows first with the host's copy gained nothing measurable: the length loads must then be
+  // vector loads, and vector reads of the lengths' cache line in every work-group, while the
+  // counter's atomics hit that line, slow a large launch several times over.)
   const int begin = min(max(J.begin_dev[b], 0), J.cap);
   const int len = min(begin + min(max(J.count_dev[b], 0), J.n_rows), J.cap);
+  if constexpr (kMeta == kMetaFp16) {
+    if (tid < kStatSlots) {
+      sh.kmin[tid] = __builtin_inff();
+      sh.kmax[tid] = -__builtin_inff();
+    }
+    __syncthreads();  // B0 (the waves of a work-group start together)
+  }
   const int first = (begin / kW) * kW;
   const int w0 = first + kW * wi;  // the work-group's window
   if (len > begin && w0 < len) {   // uniform
@@ -196,7 +195,9 @@ __global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
     const bool restage = J.stage && wi == 0 && open < len;
     const int stok = open + t;
     // ---- key direction (thread = token chunk); a wave without a valid token skips the arithmetic ----
-    const bool key_busy = __ballot(valid) != 0, value_busy = __ballot(fresh) != 0;  // wave-uniform
+    const int vt = kW - 1 - t, vtok = w0 + vt;  // the thread's value token
+    const bool vfresh = vtok >= begin && vtok < len;
+    const bool key_busy = __ballot(valid) != 0, value_busy = __ballot(vfresh) != 0;  // wave-uniform
     float x[8];
     uint32_t kn16 = 0;
 #pragma unroll
@@ -243,54 +244,31 @@ __global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
         v[2 * i + 1] = h2f(r4[i] >> 16);
       }
       const uint32_t vn16 = value_busy ? group_norm(v) : 0u;  // 0 for the zero rows of older and padded tokens
-      sh.atile[t >> 4][j >> 2][16 * (j & 3) + (t & 15)] = vraw;
+      sh.atile[vt >> 4][j >> 2][16 * (j & 3) + (vt & 15)] = vraw;
       if (j == 0) {
         const uint32_t mt = (vn16 != 0 && mymod <= 2u) ? (J.global_rot ? 0u : mymod) : 3u;
-        sh.itab[t] = (vn16 != 0) ? __builtin_amdgcn_rcpf(h2f(vn16) * a.th.t2) : 0.0f;
-        sh.tmod[t] = mt;
-        if (tok >= begin) a.v_norm[seq * J.cap + tok] = (uint16_t)vn16;  // 0 in the padded slots
-        if (fresh && a.mod_out && h == 0) a.mod_out[(size_t)b * J.cap + tok] = (uint8_t)mymod;
+        sh.itab[vt] = (vn16 != 0) ? __builtin_amdgcn_rcpf(h2f(vn16) * a.th.t2) : 0.0f;
+        sh.tmod[vt] = mt;
+        if (vtok >= begin) a.v_norm[seq * J.cap + vtok] = (uint16_t)vn16;  // 0 in the padded slots
+        if (vfresh && a.mod_out && h == 0) a.mod_out[(size_t)b * J.cap + vtok] = (uint8_t)mymod;
       }
     }
     // residual rings: the raw rows of the new tokens among the last 128
-    if (a.k_res && fresh && tok >= len - kResidual) {
-      const size_t rr = (seq * kResidual + (tok & (kResidual - 1))) * kD;
-      reinterpret_cast<uint4*>(a.k_res + rr)[j] = kraw;
-      reinterpret_cast<uint4*>(a.v_res + rr)[j] = vraw;
+    if (a.k_res) {
+      if (fresh && tok >= len - kResidual)
+        reinterpret_cast<uint4*>(a.k_res + (seq * kResidual + (tok & (kResidual - 1))) * kD)[j] = kraw;
+      if (vfresh && vtok >= len - kResidual)
+        reinterpret_cast<uint4*>(a.v_res + (seq * kResidual + (vtok & (kResidual - 1))) * kD)[j] = vraw;
     }
 
-    // ---- window minimum / maximum: the wave's 4 tokens, then the 8 waves through LDS ----
+    // ---- window minimum / maximum per channel: LDS atomics of the valid tokens ----
     if constexpr (kMeta == kMetaFp16) {
-      float lo[8], hi[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        lo[e] = valid ? x[e] : __builtin_inff();
-        hi[e] = valid ? x[e] : -__builtin_inff();
-      }
-      float p, q;
-      if (key_busy) {
+      if (valid) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          row_pair<16>(lo[e], p, q);
-          lo[e] = __builtin_fminf(p, q);
-          row_pair<16>(hi[e], p, q);
-          hi[e] = __builtin_fmaxf(p, q);
+          __hip_atomic_fetch_min(&sh.kmin[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          __hip_atomic_fetch_max(&sh.kmax[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          row_pair<32>(lo[e], p, q);
-          lo[e] = __builtin_fminf(p, q);
-          row_pair<32>(hi[e], p, q);
-          hi[e] = __builtin_fmaxf(p, q);
-        }
-      }
-      if (lane < 16) {
-        float4* pl = reinterpret_cast<float4*>(&sh.kpart[wave][0][8 * j]);
-        float4* ph = reinterpret_cast<float4*>(&sh.kpart[wave][1][8 * j]);
-        pl[0] = make_float4(lo[0], lo[1], lo[2], lo[3]);
-        pl[1] = make_float4(lo[4], lo[5], lo[6], lo[7]);
-        ph[0] = make_float4(hi[0], hi[1], hi[2], hi[3]);
-        ph[1] = make_float4(hi[4], hi[5], hi[6], hi[7]);
       }
     }
     // the window's modalities (a superset of those coded) and the B operands of the first of them,
@@ -310,7 +288,7 @@ __global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
         for (int part = 0; part < 2; ++part) bf[kk][part] = base[(kk * 2 + part) * 64];
     }
     if (restage) __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stage reads have landed
-    __syncthreads();  // B1: partials, A tile and token tables written; every stage read has landed
+    __syncthreads();  // B1: window extremes, A tile and token tables written; every stage read has landed
 
     if (restage && stok >= begin && stok < len)  // the new open window's raw keys
       reinterpret_cast<uint4*>(J.stage + (seq * kW + t) * kD)[j] = select4(open == first, kraw, sraw);
@@ -319,14 +297,8 @@ __global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
     const int gwin = w0 / kW;
     if constexpr (kMeta == kMetaFp16) {
       if (tid < kD) {
-        float l = sh.kpart[0][0][tid], u = sh.kpart[0][1][tid];
-#pragma unroll
-        for (int w = 1; w < 8; ++w) {
-          l = __builtin_fminf(l, sh.kpart[w][0][tid]);
-          u = __builtin_fmaxf(u, sh.kpart[w][1][tid]);
-        }
-        l = l + 0.0f;  // canonical +0
-        u = u + 0.0f;
+        const float l = sh.kmin[tid + (tid >> 3)] + 0.0f;  // canonical +0
+        const float u = sh.kmax[tid + (tid >> 3)] + 0.0f;
         const float step = div_rn(u - l, 3.0f);
         const uint32_t m16 = f2h(l), s16 = f2h(step);
         a.k_min[(seq * nw + gwin) * kD + tid] = (uint16_t)m16;
