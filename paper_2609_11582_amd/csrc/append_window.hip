@@ -6,10 +6,9 @@
 // same order, spread over more lanes so that the chain from the rows to the codes is short.
 //
 // Work unit: one 32-token key window of one (sequence, KV head), from the open window
-// 32 floor(L / 32) to the new end; a work-group of 512 threads. Thread (t, j) = (tid / 16,
-// tid % 16) holds channels 8j .. 8j + 7 of the key of window token t and of the value of window
-// token 31 - t (so that in a window holding few new tokens, keys and values are worked on by
-// different waves; a wave without a token of its own skips the arithmetic):
+// 32 floor(L / 32) to the new end, and one of its two roles: a key work-group and a value work-group
+// of 512 threads each. Thread (t, j) = (tid / 16, tid % 16) holds channels 8j .. 8j + 7 of window
+// token t (a wave without a token of its own skips the arithmetic):
 //  * key: sign flip, fp16 norm by the halving tree (levels 64 .. 8 across the 16 lanes of the
 //    token, 4 .. 1 in the lane), butterflies h = 1, 2, 4 in the lane and h = 8 .. 64 across lanes,
 //    z = w fl(kappa / n16); window minimum and maximum per channel by LDS atomics; codes and their
@@ -111,280 +110,290 @@ struct WindowShared {
   uint32_t last;
 };
 
-// The inputs of thread (t, j) for the window wi of a sequence whose new tokens are [begin, len).
-// The row loads are not predicated per lane: a lane without a row of its own reads the nearest row
-// of its sequence (clamped index, so that lanes spread over distinct rows rather than all meeting on
-// one cache line) and drops what it read; no branch separates the loads from each other. The stage
-// is read only by the first window, and only when it holds older tokens.
-struct WindowInputs {
-  uint4 kraw;        // key chunk of window token t (from the stage below begin)
-  uint4 vraw;        // value chunk of window token 31 - t (new tokens only)
-  uint4 sraw;        // first window, if the new open window starts after it: the key chunk of
-                     // token open + t
-  uint32_t mod;      // modality id of window token 31 - t (3: not a new token); lanes 0..31 of
-  uint32_t wmod;     // every wave also read that of window token `lane`, for the modality set
-};
+// The row loads of a work-group are not predicated per lane: a lane without a row of its own reads
+// the nearest row of its sequence (clamped index, so that lanes spread over distinct rows rather than
+// all meeting on one cache line) and drops what it read; no branch separates the loads from each
+// other. The stage is read only by the first window's key work-group, and only when it holds older
+// tokens.
 
-__device__ __forceinline__ WindowInputs window_inputs(const CodecArgs& a, size_t seq, int b, int begin, int len,
-                                                      int wi, int t, int j, int lane) {
+// Key work-group, thread (t, j), window wi of a sequence whose new tokens are [begin, len): the key
+// chunk of window token t (from the stage below begin), and for the first window, if the new open
+// window starts after it, the key chunk of token open + t (sraw).
+__device__ __forceinline__ void key_inputs(const CodecArgs& a, size_t seq, int begin, int len, int wi, int t, int j,
+                                           uint4& kraw, uint4& sraw) {
   const CodecJob& J = a.j;
-  WindowInputs in;
-  const int first = (begin / kW) * kW, w0 = first + kW * wi;
-  const size_t mrow = (size_t)b * J.n_rows, srow = seq * J.n_rows;
-  const int last = J.n_rows - 1;
-  const int wtok = w0 + (lane & 31), tok = w0 + t;
-  const bool wfresh = wtok >= begin && wtok < len, fresh = tok >= begin && tok < len;
-  const uint32_t wm = J.msrc[mrow + min(max(wtok - begin, 0), last)];
-  const int vtok = w0 + (kW - 1 - t);
-  const bool vfresh = vtok >= begin && vtok < len;
-  const size_t row = srow + (size_t)min(max(tok - begin, 0), last);
-  const size_t vrow = srow + (size_t)min(max(vtok - begin, 0), last);
-  const uint32_t tm = J.msrc[mrow + (vrow - srow)];
-  const uint4 kn = reinterpret_cast<const uint4*>(J.src + row * kD)[j];
-  const uint4 vn = reinterpret_cast<const uint4*>(a.vsrc + vrow * kD)[j];
+  const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t, last = J.n_rows - 1;
+  const size_t srow = seq * J.n_rows;
   const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-  in.kraw = select4(fresh, kn, zero);
-  in.vraw = select4(vfresh, vn, zero);
-  in.mod = vfresh ? tm : 3u;
-  in.wmod = wfresh ? wm : 3u;
+  const uint4 kn = reinterpret_cast<const uint4*>(J.src + (srow + (size_t)min(max(tok - begin, 0), last)) * kD)[j];
+  kraw = select4(tok >= begin && tok < len, kn, zero);
   if (wi == 0 && begin > first) {  // uniform: older tokens of the open window, from the stage
     const uint4 ks = reinterpret_cast<const uint4*>(J.stage + (seq * kW + min(t, begin - first - 1)) * kD)[j];
-    in.kraw = select4(tok < begin, ks, in.kraw);
+    kraw = select4(tok < begin, ks, kraw);
   }
-  in.sraw = zero;
+  sraw = zero;
   const int open = (len / kW) * kW, stok = open + t;
-  if (wi == 0 && open != first && open < len) {  // uniform
-    in.sraw = reinterpret_cast<const uint4*>(J.src + (srow + (size_t)min(max(stok - begin, 0), last)) * kD)[j];
-  }
-  return in;
+  if (wi == 0 && open != first && open < len)  // uniform
+    sraw = reinterpret_cast<const uint4*>(J.src + (srow + (size_t)min(max(stok - begin, 0), last)) * kD)[j];
 }
 
+// Value work-group, thread (t, j): the value chunk of window token t (new tokens only), its
+// modality id (3: not a new token), and in lanes 0..31 of every wave the modality id of window token
+// `lane` (wmod), for the window's modality set.
+__device__ __forceinline__ void value_inputs(const CodecArgs& a, size_t seq, int b, int begin, int len, int wi,
+                                             int t, int j, int lane, uint4& vraw, uint32_t& mod, uint32_t& wmod) {
+  const CodecJob& J = a.j;
+  const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t, wtok = w0 + (lane & 31);
+  const int last = J.n_rows - 1;
+  const size_t mrow = (size_t)b * J.n_rows, srow = seq * J.n_rows;
+  const bool fresh = tok >= begin && tok < len, wfresh = wtok >= begin && wtok < len;
+  const int r = min(max(tok - begin, 0), last);
+  const uint4 vn = reinterpret_cast<const uint4*>(a.vsrc + (srow + (size_t)r) * kD)[j];
+  const uint32_t tm = J.msrc[mrow + r];
+  const uint32_t wm = J.msrc[mrow + min(max(wtok - begin, 0), last)];
+  vraw = select4(fresh, vn, make_uint4(0u, 0u, 0u, 0u));
+  mod = fresh ? tm : 3u;
+  wmod = wfresh ? wm : 3u;
+}
+
+// The key work-group of a window: directions, window statistics, codes, norms, the stage and the
+// key ring of the residual.
+template <int kMeta>
+__device__ __forceinline__ void key_window(const CodecArgs& a, WindowShared& sh, size_t seq, int begin, int len,
+                                           int wi, int tid) {
+  const CodecJob& J = a.j;
+  const int t = tid >> 4, j = tid & 15;
+  const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t;
+  const bool valid = tok < len, fresh = valid && tok >= begin;
+  uint4 kraw, sraw;
+  key_inputs(a, seq, begin, len, wi, t, j, kraw, sraw);
+  const uint2 sg = *reinterpret_cast<const uint2*>(a.signs + 8 * j);
+  const int open = (len / kW) * kW, stok = open + t;
+  const bool restage = J.stage && wi == 0 && open < len;
+  // ---- direction (thread = token chunk); a wave without a valid token skips the arithmetic ----
+  const bool busy = __ballot(valid) != 0;  // wave-uniform
+  float x[8];
+  uint32_t kn16 = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+  if (busy) {
+    const uint32_t r4[4] = {kraw.x, kraw.y, kraw.z, kraw.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t w = (i < 2) ? sg.x : sg.y;  // int8 signs of channels 8j + 4 (i / 2) .. + 3
+      const uint32_t m = (i & 1) ? (((w & 0x00800000u) >> 8) | (w & 0x80000000u))
+                                 : (((w & 0x00000080u) << 8) | ((w & 0x00008000u) << 16));
+      const uint32_t r = r4[i] ^ m;
+      x[2 * i] = h2f(r & 0xffffu);
+      x[2 * i + 1] = h2f(r >> 16);
+    }
+    kn16 = group_norm(x);
+#pragma unroll
+    for (int hh = 1; hh < 8; hh <<= 1) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if ((e & hh) == 0) {
+          const float p = x[e], q = x[e + hh];
+          x[e] = p + q;
+          x[e + hh] = p - q;
+        }
+      }
+    }
+    cross_stage<1>(x, j);  // h = 8
+    cross_stage<2>(x, j);  // h = 16
+    cross_stage<4>(x, j);  // h = 32
+    cross_stage<8>(x, j);  // h = 64
+    const float cinv = (kn16 == 0) ? 0.0f : div_rn(kKappa, h2f(kn16));
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = x[e] * cinv;
+  }
+  if (a.k_res && fresh && tok >= len - kResidual)  // the residual ring: raw rows of the last 128 tokens
+    reinterpret_cast<uint4*>(a.k_res + (seq * kResidual + (tok & (kResidual - 1))) * kD)[j] = kraw;
+  // ---- window minimum / maximum per channel: LDS atomics of the valid tokens ----
+  if constexpr (kMeta == kMetaFp16) {
+    if (valid) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        __hip_atomic_fetch_min(&sh.kmin[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __hip_atomic_fetch_max(&sh.kmax[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+    }
+  }
+  if (restage) __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stage reads have landed
+  __syncthreads();  // B1: window extremes written; every stage read has landed
+  if (restage && stok >= begin && stok < len)  // the new open window's raw keys
+    reinterpret_cast<uint4*>(J.stage + (seq * kW + t) * kD)[j] = select4(open == first, kraw, sraw);
+  const size_t nw = J.cap / kW;
+  const int gwin = w0 / kW;
+  if constexpr (kMeta == kMetaFp16) {
+    if (tid < kD) {
+      const float l = sh.kmin[tid + (tid >> 3)] + 0.0f;  // canonical +0
+      const float u = sh.kmax[tid + (tid >> 3)] + 0.0f;
+      const float step = div_rn(u - l, 3.0f);
+      const uint32_t m16 = f2h(l), s16 = f2h(step);
+      a.k_min[(seq * nw + gwin) * kD + tid] = (uint16_t)m16;
+      a.k_step[(seq * nw + gwin) * kD + tid] = (uint16_t)s16;
+      sh.kstat[tid] = make_float2(h2f(m16), (s16 == 0) ? 0.0f : div_rn(1.0f, h2f(s16)));
+    }
+    __syncthreads();  // B2: window statistics
+  }
+  // ---- codes: 2 bits per channel; word u of a token holds channels 16u .. 16u + 15, the even ones
+  // in its low half; this lane fills bits 8 (j & 1) .. + 7 of both halves of word j / 2 ----
+  uint32_t lo16 = 0, hi16 = 0;
+  if (valid) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int sh2 = 2 * (4 * (j & 1) + i);
+      uint32_t c0, c1;
+      if constexpr (kMeta == kMetaFp16) {
+        const float4 st = *reinterpret_cast<const float4*>(&sh.kstat[8 * j + 2 * i]);
+        constexpr float kRound = 8388608.0f;  // 2^23: rint of the clamped value in the low bits
+        const float t0 = (x[2 * i] - st.x) * st.y;
+        const float t1 = (x[2 * i + 1] - st.z) * st.w;
+        c0 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_fmed3f(t0, 0.0f, 3.0f) + kRound) & 3u;
+        c1 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_fmed3f(t1, 0.0f, 3.0f) + kRound) & 3u;
+      } else {
+        const float z0 = x[2 * i], z1 = x[2 * i + 1];
+        c0 = (uint32_t)(z0 > a.th.t0) + (uint32_t)(z0 > a.th.t1) + (uint32_t)(z0 > a.th.t2);
+        c1 = (uint32_t)(z1 > a.th.t0) + (uint32_t)(z1 > a.th.t1) + (uint32_t)(z1 > a.th.t2);
+      }
+      lo16 |= c0 << sh2;
+      hi16 |= c1 << sh2;
+    }
+  }
+  uint32_t word = lo16 | (hi16 << 16);
+  word |= xchg_u(word);
+  if ((j & 1) == 0) reinterpret_cast<uint32_t*>(a.k_codes + (seq * J.cap + tok) * 32)[j >> 1] = word;
+  if (j == 0) a.k_norm[seq * J.cap + tok] = valid ? (uint16_t)kn16 : (uint16_t)0;
+}
+
+// The value work-group of a window: norms, the A tile, then wave w forms output channels 16w ..
+// 16w + 15 of the 32 tokens on the matrix cores, per present modality, and writes their code bytes;
+// also the modality map and the value ring of the residual.
+__device__ __forceinline__ void value_window(const CodecArgs& a, WindowShared& sh, size_t seq, int b, int h,
+                                             int begin, int len, int wi, int tid) {
+  const CodecJob& J = a.j;
+  const int t = tid >> 4, j = tid & 15, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t;
+  const bool fresh = tok >= begin && tok < len;
+  uint4 vraw;
+  uint32_t mymod, wmod;
+  value_inputs(a, seq, b, begin, len, wi, t, j, lane, vraw, mymod, wmod);
+  const bool busy = __ballot(fresh) != 0;  // wave-uniform
+  {
+    const uint32_t r4[4] = {vraw.x, vraw.y, vraw.z, vraw.w};
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = h2f(r4[i] & 0xffffu);
+      v[2 * i + 1] = h2f(r4[i] >> 16);
+    }
+    const uint32_t vn16 = busy ? group_norm(v) : 0u;  // 0 for the zero rows of older and padded tokens
+    sh.atile[t >> 4][j >> 2][16 * (j & 3) + (t & 15)] = vraw;
+    if (j == 0) {
+      const uint32_t mt = (vn16 != 0 && mymod <= 2u) ? (J.global_rot ? 0u : mymod) : 3u;
+      sh.itab[t] = (vn16 != 0) ? __builtin_amdgcn_rcpf(h2f(vn16) * a.th.t2) : 0.0f;
+      sh.tmod[t] = mt;
+      if (tok >= begin) a.v_norm[seq * J.cap + tok] = (uint16_t)vn16;  // 0 in the padded slots
+      if (fresh && a.mod_out && h == 0) a.mod_out[(size_t)b * J.cap + tok] = (uint8_t)mymod;
+    }
+  }
+  if (a.v_res && fresh && tok >= len - kResidual)  // the residual ring: raw rows of the last 128 tokens
+    reinterpret_cast<uint4*>(a.v_res + (seq * kResidual + (tok & (kResidual - 1))) * kD)[j] = vraw;
+  // the window's modalities (a superset of those coded) and the B operands of the first of them,
+  // in flight across the barrier
+  uint32_t mset = 0;
+#pragma unroll
+  for (int m = 0; m < 3; ++m)
+    if (__ballot(wmod == (uint32_t)m)) mset |= 1u << m;
+  if (J.global_rot) mset = mset ? 1u : 0u;  // R_0 for every token
+  const int m_first = mset ? __builtin_ctz(mset) : 0;
+  uint4 bf[4][2];
+  {
+    const uint4* base = a.rotfrag + (size_t)(m_first * 8 + wave) * 8 * 64 + lane;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int part = 0; part < 2; ++part) bf[kk][part] = base[(kk * 2 + part) * 64];
+  }
+  __syncthreads();  // B1: A tile and token tables written
+  const int g = lane >> 4;
+  const uint32_t tm = sh.tmod[lane & 31];
+  uint32_t vb[2] = {0u, 0u};
+#pragma unroll 1
+  for (int m = m_first; m < 3; ++m) {
+    const uint32_t mb = (uint32_t)__ballot(tm == (uint32_t)m);  // token bits, lanes 0..31
+    if (mb == 0) continue;
+    if (m != m_first) {
+      const uint4* base = a.rotfrag + (size_t)(m * 8 + wave) * 8 * 64 + lane;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int part = 0; part < 2; ++part) bf[kk][part] = base[(kk * 2 + part) * 64];
+    }
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      floatx4 y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const half8 xa = __builtin_bit_cast(half8, sh.atile[rb][kk][lane]);
+#pragma unroll
+        for (int part = 0; part < 2; ++part)
+          y = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa, __builtin_bit_cast(half8, bf[kk][part]), y, 0, 0, 0);
+      }
+      const float4 it = *reinterpret_cast<const float4*>(&sh.itab[16 * rb + 4 * g]);
+      const float iv[4] = {it.x, it.y, it.z, it.w};
+      uint32_t byte = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) byte |= (uint32_t)(min(max(floor_to_int(y[i] * iv[i]), -2), 1) + 2) << (2 * i);
+      const uint32_t b4 = (mb >> (16 * rb + 4 * g)) & 15u;  // the quad's tokens of modality m
+      const uint32_t keep = ((b4 & 1u) | ((b4 & 2u) << 1) | ((b4 & 4u) << 2) | ((b4 & 8u) << 3)) * 3u;
+      vb[rb] |= byte & keep;
+    }
+  }
+  const size_t nw = J.cap / kW;
+  uint8_t* blk = a.v_codes + (seq * nw + w0 / kW) * 1024 + 16 * lane + wave;
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+    uint32_t v = vb[rb];
+    const int old = min(max(begin - (w0 + 16 * rb + 4 * g), 0), 4);  // older tokens of the quad keep their bits
+    if (old > 0) {
+      const uint32_t k = (1u << (2 * old)) - 1u;
+      v = ((uint32_t)blk[8 * rb] & k) | (v & ~k);
+    }
+    blk[8 * rb] = (uint8_t)v;
+  }
+}
+
+// Grid: (2 nwin, H, sequences); x < nwin: the key work-group of window x, else the value work-group
+// of window x - nwin.
 template <int kMeta>
 __global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
   static_assert(kMeta == kMetaFp16 || kMeta == kMetaTq, "fp16 window metadata or TurboQuant keys");
   __shared__ WindowShared sh;
   const CodecJob& J = a.j;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int t = tid >> 4, j = tid & 15;  // window token, channel chunk
-  const int wi = blockIdx.x, h = blockIdx.y, bz = blockIdx.z, b = J.b0 + bz;
+  const int tid = threadIdx.x;
+  const int nwin = (int)gridDim.x / 2;
+  const bool values = (int)blockIdx.x >= nwin;  // uniform
+  const int wi = (int)blockIdx.x - (values ? nwin : 0), h = blockIdx.y, bz = blockIdx.z, b = J.b0 + bz;
   const size_t seq = (size_t)b * J.H + h;
-  // The device lengths decide, clamped into the buffers (the host's copy planned the grid). (Loading
-  // the rows first with the host's copy gained nothing measurable: the length loads must then be
-  // vector loads, and vector reads of the lengths' cache line in every work-group, while the
-  // counter's atomics hit that line, slow a large launch several times over.)
+  // the device lengths decide, clamped into the buffers (the host's copy planned the grid)
   const int begin = min(max(J.begin_dev[b], 0), J.cap);
   const int len = min(begin + min(max(J.count_dev[b], 0), J.n_rows), J.cap);
-  if constexpr (kMeta == kMetaFp16) {
+  if (kMeta == kMetaFp16 && !values) {
     if (tid < kStatSlots) {
       sh.kmin[tid] = __builtin_inff();
       sh.kmax[tid] = -__builtin_inff();
     }
     __syncthreads();  // B0 (the waves of a work-group start together)
   }
-  const int first = (begin / kW) * kW;
-  const int w0 = first + kW * wi;  // the work-group's window
-  if (len > begin && w0 < len) {   // uniform
-    const WindowInputs in = window_inputs(a, seq, b, begin, len, wi, t, j, lane);
-    const int tok = w0 + t;
-    const bool valid = tok < len, fresh = valid && tok >= begin;
-    const uint4 kraw = in.kraw, vraw = in.vraw, sraw = in.sraw;
-    const uint32_t mymod = in.mod;
-    const uint2 sg = *reinterpret_cast<const uint2*>(a.signs + 8 * j);
-    const int open = (len / kW) * kW;
-    const bool restage = J.stage && wi == 0 && open < len;
-    const int stok = open + t;
-    // ---- key direction (thread = token chunk); a wave without a valid token skips the arithmetic ----
-    const int vt = kW - 1 - t, vtok = w0 + vt;  // the thread's value token
-    const bool vfresh = vtok >= begin && vtok < len;
-    const bool key_busy = __ballot(valid) != 0, value_busy = __ballot(vfresh) != 0;  // wave-uniform
-    float x[8];
-    uint32_t kn16 = 0;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = 0.0f;
-    if (key_busy) {
-      const uint32_t r4[4] = {kraw.x, kraw.y, kraw.z, kraw.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t w = (i < 2) ? sg.x : sg.y;  // int8 signs of channels 8j + 4 (i / 2) .. + 3
-        const uint32_t m = (i & 1) ? (((w & 0x00800000u) >> 8) | (w & 0x80000000u))
-                                   : (((w & 0x00000080u) << 8) | ((w & 0x00008000u) << 16));
-        const uint32_t r = r4[i] ^ m;
-        x[2 * i] = h2f(r & 0xffffu);
-        x[2 * i + 1] = h2f(r >> 16);
-      }
-      kn16 = group_norm(x);
-#pragma unroll
-      for (int hh = 1; hh < 8; hh <<= 1) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          if ((e & hh) == 0) {
-            const float p = x[e], q = x[e + hh];
-            x[e] = p + q;
-            x[e + hh] = p - q;
-          }
-        }
-      }
-      cross_stage<1>(x, j);  // h = 8
-      cross_stage<2>(x, j);  // h = 16
-      cross_stage<4>(x, j);  // h = 32
-      cross_stage<8>(x, j);  // h = 64
-      const float cinv = (kn16 == 0) ? 0.0f : div_rn(kKappa, h2f(kn16));
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = x[e] * cinv;
-    }
-
-    // ---- value norm, A tile, per-token tables ----
-    {
-      const uint32_t r4[4] = {vraw.x, vraw.y, vraw.z, vraw.w};
-      float v[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        v[2 * i] = h2f(r4[i] & 0xffffu);
-        v[2 * i + 1] = h2f(r4[i] >> 16);
-      }
-      const uint32_t vn16 = value_busy ? group_norm(v) : 0u;  // 0 for the zero rows of older and padded tokens
-      sh.atile[vt >> 4][j >> 2][16 * (j & 3) + (vt & 15)] = vraw;
-      if (j == 0) {
-        const uint32_t mt = (vn16 != 0 && mymod <= 2u) ? (J.global_rot ? 0u : mymod) : 3u;
-        sh.itab[vt] = (vn16 != 0) ? __builtin_amdgcn_rcpf(h2f(vn16) * a.th.t2) : 0.0f;
-        sh.tmod[vt] = mt;
-        if (vtok >= begin) a.v_norm[seq * J.cap + vtok] = (uint16_t)vn16;  // 0 in the padded slots
-        if (vfresh && a.mod_out && h == 0) a.mod_out[(size_t)b * J.cap + vtok] = (uint8_t)mymod;
-      }
-    }
-    // residual rings: the raw rows of the new tokens among the last 128
-    if (a.k_res) {
-      if (fresh && tok >= len - kResidual)
-        reinterpret_cast<uint4*>(a.k_res + (seq * kResidual + (tok & (kResidual - 1))) * kD)[j] = kraw;
-      if (vfresh && vtok >= len - kResidual)
-        reinterpret_cast<uint4*>(a.v_res + (seq * kResidual + (vtok & (kResidual - 1))) * kD)[j] = vraw;
-    }
-
-    // ---- window minimum / maximum per channel: LDS atomics of the valid tokens ----
-    if constexpr (kMeta == kMetaFp16) {
-      if (valid) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          __hip_atomic_fetch_min(&sh.kmin[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-          __hip_atomic_fetch_max(&sh.kmax[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        }
-      }
-    }
-    // the window's modalities (a superset of those coded) and the B operands of the first of them,
-    // in flight across the barrier and the window statistics
-    uint32_t mset = 0;
-#pragma unroll
-    for (int m = 0; m < 3; ++m)
-      if (__ballot(in.wmod == (uint32_t)m)) mset |= 1u << m;
-    if (J.global_rot) mset = mset ? 1u : 0u;  // R_0 for every token
-    const int m_first = mset ? __builtin_ctz(mset) : 0;
-    uint4 bf[4][2];
-    {
-      const uint4* base = a.rotfrag + (size_t)(m_first * 8 + wave) * 8 * 64 + lane;
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-        for (int part = 0; part < 2; ++part) bf[kk][part] = base[(kk * 2 + part) * 64];
-    }
-    if (restage) __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stage reads have landed
-    __syncthreads();  // B1: window extremes, A tile and token tables written; every stage read has landed
-
-    if (restage && stok >= begin && stok < len)  // the new open window's raw keys
-      reinterpret_cast<uint4*>(J.stage + (seq * kW + t) * kD)[j] = select4(open == first, kraw, sraw);
-
-    const size_t nw = J.cap / kW;
-    const int gwin = w0 / kW;
-    if constexpr (kMeta == kMetaFp16) {
-      if (tid < kD) {
-        const float l = sh.kmin[tid + (tid >> 3)] + 0.0f;  // canonical +0
-        const float u = sh.kmax[tid + (tid >> 3)] + 0.0f;
-        const float step = div_rn(u - l, 3.0f);
-        const uint32_t m16 = f2h(l), s16 = f2h(step);
-        a.k_min[(seq * nw + gwin) * kD + tid] = (uint16_t)m16;
-        a.k_step[(seq * nw + gwin) * kD + tid] = (uint16_t)s16;
-        sh.kstat[tid] = make_float2(h2f(m16), (s16 == 0) ? 0.0f : div_rn(1.0f, h2f(s16)));
-      }
-      __syncthreads();  // B2: window statistics
-    }
-
-    // ---- key codes: 2 bits per channel; word u of a token holds channels 16u .. 16u + 15, the even
-    // ones in its low half; this lane fills bits 8 (j & 1) .. + 7 of both halves of word j / 2 ----
-    uint32_t lo16 = 0, hi16 = 0;
-    if (valid) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int sh2 = 2 * (4 * (j & 1) + i);
-        uint32_t c0, c1;
-        if constexpr (kMeta == kMetaFp16) {
-          const float4 s = *reinterpret_cast<const float4*>(&sh.kstat[8 * j + 2 * i]);
-          constexpr float kRound = 8388608.0f;  // 2^23: rint of the clamped value in the low bits
-          const float t0 = (x[2 * i] - s.x) * s.y;
-          const float t1 = (x[2 * i + 1] - s.z) * s.w;
-          c0 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_fmed3f(t0, 0.0f, 3.0f) + kRound) & 3u;
-          c1 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_fmed3f(t1, 0.0f, 3.0f) + kRound) & 3u;
-        } else {
-          const float z0 = x[2 * i], z1 = x[2 * i + 1];
-          c0 = (uint32_t)(z0 > a.th.t0) + (uint32_t)(z0 > a.th.t1) + (uint32_t)(z0 > a.th.t2);
-          c1 = (uint32_t)(z1 > a.th.t0) + (uint32_t)(z1 > a.th.t1) + (uint32_t)(z1 > a.th.t2);
-        }
-        lo16 |= c0 << sh2;
-        hi16 |= c1 << sh2;
-      }
-    }
-    uint32_t word = lo16 | (hi16 << 16);
-    word |= xchg_u(word);
-    if ((j & 1) == 0) reinterpret_cast<uint32_t*>(a.k_codes + (seq * J.cap + tok) * 32)[j >> 1] = word;
-    if (j == 0) a.k_norm[seq * J.cap + tok] = valid ? (uint16_t)kn16 : (uint16_t)0;
-
-    // ---- value codes: wave w takes output channels 16w .. 16w + 15 of the 32 tokens ----
-    {
-      const int g = lane >> 4;
-      const uint32_t tm = sh.tmod[lane & 31];
-      uint32_t vb[2] = {0u, 0u};
-#pragma unroll 1
-      for (int m = m_first; m < 3; ++m) {
-        const uint32_t mb = (uint32_t)__ballot(tm == (uint32_t)m);  // token bits, lanes 0..31
-        if (mb == 0) continue;
-        if (m != m_first) {
-          const uint4* base = a.rotfrag + (size_t)(m * 8 + wave) * 8 * 64 + lane;
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-            for (int part = 0; part < 2; ++part) bf[kk][part] = base[(kk * 2 + part) * 64];
-        }
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-          floatx4 y = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk) {
-            const half8 xa = __builtin_bit_cast(half8, sh.atile[rb][kk][lane]);
-#pragma unroll
-            for (int part = 0; part < 2; ++part)
-              y = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa, __builtin_bit_cast(half8, bf[kk][part]), y, 0, 0, 0);
-          }
-          const float4 it = *reinterpret_cast<const float4*>(&sh.itab[16 * rb + 4 * g]);
-          const float iv[4] = {it.x, it.y, it.z, it.w};
-          uint32_t byte = 0;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) byte |= (uint32_t)(min(max(floor_to_int(y[i] * iv[i]), -2), 1) + 2) << (2 * i);
-          const uint32_t b4 = (mb >> (16 * rb + 4 * g)) & 15u;  // the quad's tokens of modality m
-          const uint32_t keep = ((b4 & 1u) | ((b4 & 2u) << 1) | ((b4 & 4u) << 2) | ((b4 & 8u) << 3)) * 3u;
-          vb[rb] |= byte & keep;
-        }
-      }
-      uint8_t* blk = a.v_codes + (seq * nw + gwin) * 1024 + 16 * lane + wave;
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        uint32_t v = vb[rb];
-        const int old = min(max(begin - (w0 + 16 * rb + 4 * g), 0), 4);  // older tokens of the quad keep their bits
-        if (old > 0) {
-          const uint32_t k = (1u << (2 * old)) - 1u;
-          v = ((uint32_t)blk[8 * rb] & k) | (v & ~k);
-        }
-        blk[8 * rb] = (uint8_t)v;
-      }
-    }
+  const int w0 = (begin / kW) * kW + kW * wi;  // the work-group's window
+  if (len > begin && w0 < len) {               // uniform
+    if (values)
+      value_window(a, sh, seq, b, h, begin, len, wi, tid);
+    else
+      key_window<kMeta>(a, sh, seq, begin, len, wi, tid);
   }
 
   // The lengths advance once every work-group has read them: each work-group counts itself after
@@ -408,7 +417,7 @@ __global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
 
 hipError_t launch_append_window(const CodecArgs& a, int nwin, int nb, hipStream_t s) {
   if (nwin <= 0 || nb <= 0) return hipSuccess;
-  const dim3 grid(nwin, a.j.H, nb);
+  const dim3 grid(2 * nwin, a.j.H, nb);
   if (a.key_meta == kMetaTq)
     hipLaunchKernelGGL(k_append_window<kMetaTq>, grid, dim3(kThreads), 0, s, a);
   else if (a.key_meta == kMetaFp16)
