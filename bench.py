@@ -1036,8 +1036,29 @@ def main():
             okvq.okvq_decode_attention_dense(d5, l5[i % 2]["k"], l5[i % 2]["v"], s5, lens5, q5, sm, o5, ws5,
                                              stream=stream)
         torch.cuda.synchronize()
+        # the prefill's keys and values through the stateless codec calls (one role per launch), twice
+        # each, and 8 one-token appends through the window-parallel launch (lengths set to N - 1 first)
+        c0 = caches[0]
+        v0w = c0.views()
+        for i in range(2):
+            okvq.okvq_quantize_keys(c0.dims, k_in[i], N, lens, c0.key_signs, v0w["k_codes"], v0w["k_min"],
+                                    v0w["k_step"], v0w["k_norm"], stream=stream)
+            okvq.okvq_quantize_values(c0.dims, v_in[i], m0, N, lens, c0.v_rot, 0, v0w["v_codes"], v0w["v_norm"],
+                                      stream=stream)
+        torch.cuda.synchronize()
+        k1 = k_in[0][:, :, :1].contiguous()
+        v1 = v_in[0][:, :, :1].contiguous()
+        m1 = m0[:, :1].contiguous()
+        one = torch.ones(B, dtype=torch.int32, device=dev)
+        short = torch.tensor([L - 1 for L in lens], dtype=torch.int32, device=dev)
+        for i in range(8):
+            c = caches[(5 * i + 1) % n_cache]
+            c.buffers["seq_lens"][:B].copy_(short)
+            okvq.okvq_append(c, [L - 1 for L in lens], k1, v1, m1, [1] * B, one, 1, stream=stream)
+        torch.cuda.synchronize()
         print(json.dumps({"profile_pass": True, "copy_bytes": CALIBRATION_COPY_BYTES, "decode_calls": 8,
-                          "append_calls": 2, "decode_algorithmic_bytes": decode_algorithmic_bytes(B, H, Hq, lens),
+                          "append_calls": 2, "stateless_key_calls": 2, "stateless_value_calls": 2,
+                          "one_token_append_calls": 8, "decode_algorithmic_bytes": decode_algorithmic_bytes(B, H, Hq, lens),
                           "append_algorithmic_bytes": append_algorithmic_bytes(B, H, lens),
                           "mxfp4_decode_calls": 8, "mxfp4_append_calls": 2, "residual_decode_calls": 8,
                           "turboquant_decode_calls": 8, "turboquant_append_calls": 2, "dense_decode_calls": 4,

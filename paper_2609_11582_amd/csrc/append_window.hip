@@ -98,6 +98,32 @@ __device__ __forceinline__ int floor_to_int(float x) {
   return r;
 }
 
+// The launch's arguments: the append fields of the codec arguments without the host's copies of
+// the lengths (the kernel reads the device lengths), about 200 bytes instead of 2.4 KB.
+struct WindowArgs {
+  const uint16_t* src;       // key rows [B][H][n_rows][128] fp16
+  const uint16_t* vsrc;      // value rows, the same layout
+  const uint8_t* msrc;       // [B][n_rows] modality ids
+  const int32_t* begin_dev;  // current lengths (device)
+  const int32_t* count_dev;  // appended tokens (device)
+  uint16_t* stage;           // [B][H][32][128] raw keys of the open window
+  const int8_t* signs;
+  uint8_t* k_codes;
+  uint16_t* k_min;
+  uint16_t* k_step;
+  uint16_t* k_norm;
+  const uint4* rotfrag;      // prepared forward fragments of R_m
+  uint8_t* v_codes;
+  uint16_t* v_norm;
+  uint8_t* mod_out;
+  int32_t* seq_lens_out;
+  uint32_t* ticket;
+  uint16_t* k_res;           // residual rings, or null
+  uint16_t* v_res;
+  Thresholds th;
+  int n_rows, b0, H, cap, global_rot;
+};
+
 constexpr int kStatSlots = kD + kD / 8;
 
 struct WindowShared {
@@ -119,9 +145,9 @@ struct WindowShared {
 // Key work-group, thread (t, j), window wi of a sequence whose new tokens are [begin, len): the key
 // chunk of window token t (from the stage below begin), and for the first window, if the new open
 // window starts after it, the key chunk of token open + t (sraw).
-__device__ __forceinline__ void key_inputs(const CodecArgs& a, size_t seq, int begin, int len, int wi, int t, int j,
+__device__ __forceinline__ void key_inputs(const WindowArgs& a, size_t seq, int begin, int len, int wi, int t, int j,
                                            uint4& kraw, uint4& sraw) {
-  const CodecJob& J = a.j;
+  const WindowArgs& J = a;
   const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t, last = J.n_rows - 1;
   const size_t srow = seq * J.n_rows;
   const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
@@ -140,9 +166,9 @@ __device__ __forceinline__ void key_inputs(const CodecArgs& a, size_t seq, int b
 // Value work-group, thread (t, j): the value chunk of window token t (new tokens only), its
 // modality id (3: not a new token), and in lanes 0..31 of every wave the modality id of window token
 // `lane` (wmod), for the window's modality set.
-__device__ __forceinline__ void value_inputs(const CodecArgs& a, size_t seq, int b, int begin, int len, int wi,
+__device__ __forceinline__ void value_inputs(const WindowArgs& a, size_t seq, int b, int begin, int len, int wi,
                                              int t, int j, int lane, uint4& vraw, uint32_t& mod, uint32_t& wmod) {
-  const CodecJob& J = a.j;
+  const WindowArgs& J = a;
   const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t, wtok = w0 + (lane & 31);
   const int last = J.n_rows - 1;
   const size_t mrow = (size_t)b * J.n_rows, srow = seq * J.n_rows;
@@ -159,9 +185,9 @@ __device__ __forceinline__ void value_inputs(const CodecArgs& a, size_t seq, int
 // The key work-group of a window: directions, window statistics, codes, norms, the stage and the
 // key ring of the residual.
 template <int kMeta>
-__device__ __forceinline__ void key_window(const CodecArgs& a, WindowShared& sh, size_t seq, int begin, int len,
+__device__ __forceinline__ void key_window(const WindowArgs& a, WindowShared& sh, size_t seq, int begin, int len,
                                            int wi, int tid) {
-  const CodecJob& J = a.j;
+  const WindowArgs& J = a;
   const int t = tid >> 4, j = tid & 15;
   const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t;
   const bool valid = tok < len, fresh = valid && tok >= begin;
@@ -270,9 +296,9 @@ __device__ __forceinline__ void key_window(const CodecArgs& a, WindowShared& sh,
 // The value work-group of a window: norms, the A tile, then wave w forms output channels 16w ..
 // 16w + 15 of the 32 tokens on the matrix cores, per present modality, and writes their code bytes;
 // also the modality map and the value ring of the residual.
-__device__ __forceinline__ void value_window(const CodecArgs& a, WindowShared& sh, size_t seq, int b, int h,
+__device__ __forceinline__ void value_window(const WindowArgs& a, WindowShared& sh, size_t seq, int b, int h,
                                              int begin, int len, int wi, int tid) {
-  const CodecJob& J = a.j;
+  const WindowArgs& J = a;
   const int t = tid >> 4, j = tid & 15, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t;
@@ -369,10 +395,10 @@ __device__ __forceinline__ void value_window(const CodecArgs& a, WindowShared& s
 // Grid: (2 nwin, H, sequences); x < nwin: the key work-group of window x, else the value work-group
 // of window x - nwin.
 template <int kMeta>
-__global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
+__global__ __launch_bounds__(kThreads) void k_append_window(WindowArgs a) {
   static_assert(kMeta == kMetaFp16 || kMeta == kMetaTq, "fp16 window metadata or TurboQuant keys");
   __shared__ WindowShared sh;
-  const CodecJob& J = a.j;
+  const WindowArgs& J = a;
   const int tid = threadIdx.x;
   const int nwin = (int)gridDim.x / 2;
   const bool values = (int)blockIdx.x >= nwin;  // uniform
@@ -415,12 +441,39 @@ __global__ __launch_bounds__(kThreads) void k_append_window(CodecArgs a) {
 
 }  // namespace
 
-hipError_t launch_append_window(const CodecArgs& a, int nwin, int nb, hipStream_t s) {
+hipError_t launch_append_window(const CodecArgs& c, int nwin, int nb, hipStream_t s) {
   if (nwin <= 0 || nb <= 0) return hipSuccess;
-  const dim3 grid(2 * nwin, a.j.H, nb);
-  if (a.key_meta == kMetaTq)
+  WindowArgs a;
+  a.src = c.j.src;
+  a.vsrc = c.vsrc;
+  a.msrc = c.j.msrc;
+  a.begin_dev = c.j.begin_dev;
+  a.count_dev = c.j.count_dev;
+  a.stage = c.j.stage;
+  a.signs = c.signs;
+  a.k_codes = c.k_codes;
+  a.k_min = c.k_min;
+  a.k_step = c.k_step;
+  a.k_norm = c.k_norm;
+  a.rotfrag = c.rotfrag;
+  a.v_codes = c.v_codes;
+  a.v_norm = c.v_norm;
+  a.mod_out = c.mod_out;
+  a.seq_lens_out = c.seq_lens_out;
+  a.ticket = c.ticket;
+  a.k_res = c.k_res;
+  a.v_res = c.v_res;
+  a.th = c.th;
+  a.n_rows = c.j.n_rows;
+  a.b0 = c.j.b0;
+  a.H = c.j.H;
+  a.cap = c.j.cap;
+  a.global_rot = c.j.global_rot;
+  const int key_meta = c.key_meta;
+  const dim3 grid(2 * nwin, a.H, nb);
+  if (key_meta == kMetaTq)
     hipLaunchKernelGGL(k_append_window<kMetaTq>, grid, dim3(kThreads), 0, s, a);
-  else if (a.key_meta == kMetaFp16)
+  else if (key_meta == kMetaFp16)
     hipLaunchKernelGGL(k_append_window<kMetaFp16>, grid, dim3(kThreads), 0, s, a);
   else
     return hipErrorInvalidValue;
