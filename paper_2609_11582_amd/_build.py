@@ -38,9 +38,9 @@ def hipcc() -> str:
 # value they use), so min / max need no NaN quieting
 EXTRA = {"decode_kernels.hip": ["-fno-honor-nans"], "dense_decode.hip": ["-fno-honor-nans"],
          "ladder_decode.hip": ["-fno-honor-nans"],
-         # the window append takes window minima and maxima of finite directions (finite inputs are part of the
-         # device data contract)
-         "append_window.hip": ["-fno-honor-nans"]}
+         # the codecs take window minima and maxima of finite directions (finite inputs are part of the device data
+         # contract): no NaN quieting around them
+         "append_window.hip": ["-fno-honor-nans"], "codec_fused.hip": ["-fno-honor-nans"]}
 
 
 def build(verbose: bool = False, jobs: int = 4) -> str:
