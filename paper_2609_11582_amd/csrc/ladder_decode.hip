@@ -4,14 +4,18 @@
 // Work-group (split, KV head h, sequence b) = 8 waves; wave w takes the split's 32-token windows
 // w, w + 8, ... and keeps its own online softmax for the G <= 8 query heads of the KV head.
 //  * scores s_t = n_t (q' . zhat_t), q' = H q sm_scale log2(e). The A operands of the score MFMA
-//    come from each lane's 8 b-bit field of a token row through a small LDS table indexed by a code
-//    pair: the codes as fp16 integers for the method's keys, the b-bit codebook levels for
-//    TurboQuant keys. For the method's keys zhat = m + step code is split as in the 2-bit kernel:
-//    the window term q' . m in fp32 (a per-window bias) and sum_c q'_c step_c code_c on the
-//    matrix cores with B = fp16(q'_c step_c 2^k0) -- rounding the whole of m + step code to fp16
-//    would cost too much where the keys' window means are large (they drift);
-//  * values: each lane dequantizes 64 codes of one token row through a pair table of codebook
-//    levels into the wave's LDS tile (16-byte-chunk XOR swizzle); the PV B operands come back with
+//    come from each lane's 8 b-bit field of a token row: 2- and 4-bit codes of the method's keys
+//    directly, as fp16 subnormals (the field masked per channel pair; the power of two of a
+//    channel's bit position is folded into the query operand), 3-bit codes and TurboQuant levels
+//    through a small LDS table indexed by a code pair. For the method's keys zhat = m + step code
+//    is split as in the 2-bit kernel: the window term q' . m in fp32 (a per-window bias; on the
+//    matrix cores against the query's fp16 hi and lo parts, or in fp32 FMAs for 3-bit keys) and
+//    sum_c q'_c step_c code_c on the matrix cores with B = fp16(q'_c step_c 2^(k0 - shift_c)) --
+//    rounding the whole of m + step code to fp16 would cost too much where the keys' window means
+//    are large (they drift);
+//  * values: each lane dequantizes 64 codes of one token row through a table of codebook levels
+//    (a code byte -> four levels for 2-bit values, a code pair -> two otherwise) into the wave's
+//    LDS tile (16-byte-chunk XOR swizzle); the PV B operands come back with
 //    the transposing LDS read of gfx950 (ds_read_b64_tr_b16), in the token order of the score
 //    tile's rows;
 //  * per-modality PV (values stay rotated): the A operand's rows 0-7 are the audio-masked p n_v of
@@ -68,6 +72,13 @@ __device__ __forceinline__ uint32_t field64(uint32_t lo, uint32_t hi, int sh) {
   return sh == 0 ? lo : __builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh);
 }
 
+// Float offsets of the combine tiles, whose 16-byte slots are XOR-swizzled by the channel so that
+// 16 lanes reading or writing one slot of 16 consecutive channels hit distinct banks: a wave's rows
+// [channel k][16] (slot s = rows 4 s .. 4 s + 3) and its text rows [channel k][8] (slot s = heads
+// 4 s .. 4 s + 3).
+__device__ __forceinline__ int row_ofs(int w, int k, int s) { return ((w * kD + k) << 4) + 4 * (s ^ ((k >> 2) & 3)); }
+__device__ __forceinline__ int text_ofs(int k, int s) { return (k << 3) + 4 * (s ^ ((k >> 3) & 1)); }
+
 // One window's loads for one lane (issued a window ahead of their use).
 template <int kKB, int kVB>
 struct LTile {
@@ -82,8 +93,15 @@ template <int kKB, int kVB, bool kTq>
 __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) {
   constexpr int kKRow = 16 * kKB, kVRow = 16 * kVB;  // bytes per packed token row
   constexpr uint32_t kKMask = (1u << (2 * kKB)) - 1u, kVMask = (1u << (2 * kVB)) - 1u;
-  __shared__ uint32_t klut[1 << (2 * kKB)];  // key code pair -> fp16 pair (integers, or TurboQuant levels)
-  __shared__ uint32_t vlut[1 << (2 * kVB)];  // value code pair -> fp16 codebook levels
+  // 2- and 4-bit codes of the method's keys enter the score MFMA directly as fp16 subnormals (the
+  // field masked per channel pair, the power of two folded into the query operand); 3-bit codes and
+  // TurboQuant levels through a code-pair table
+  constexpr bool kDirect = !kTq && (kKB == 2 || kKB == 4);
+  // 2-bit values: a code byte (4 channels) -> four fp16 codebook levels; else a code pair -> two
+  constexpr bool kVByte = kVB == 2;
+  constexpr bool kBiasMfma = !kTq && kKB != 3;  // q' . m of a window on the matrix cores
+  __shared__ uint32_t klut[kDirect ? 1 : 1 << (2 * kKB)];  // key code pair -> fp16 pair (integers, or TurboQuant levels)
+  __shared__ __attribute__((aligned(8))) uint32_t vlut[kVByte ? 512 : 1 << (2 * kVB)];
   __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];
   __shared__ __attribute__((aligned(16))) uint8_t vt[kLw][kW * kD * 2];    // value tiles
   __shared__ __attribute__((aligned(16))) uint16_t mt[kLw][2][kD];         // window (minimum, step)
@@ -91,8 +109,8 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   __shared__ float wst[2][8][kLw];
   __shared__ uint32_t wmask[kLw], wnv[kLw];
   __shared__ int wexp[kLw];
-  __shared__ __attribute__((aligned(16))) float fac[8][kLw];
-  __shared__ __attribute__((aligned(16))) float ttx[kLw][kD][8];  // text rows (heads 0-7) per wave
+  __shared__ __attribute__((aligned(16))) float fac[kLw][8];      // combine factor per wave and head
+  __shared__ __attribute__((aligned(16))) float ttx[kLw][kD][8];  // text rows (heads 0-7) per wave, swizzled
   __shared__ float amax_w[4];
 
   const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -178,13 +196,22 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
       if (j < n) v = (c == j) ? (uint32_t)__builtin_amdgcn_readfirstlane((int)cb[j]) : v;
     return v;
   };
-  for (int i = tid; i < (1 << (2 * kKB)); i += 64 * kLw) {
-    const int c0 = i & ((1 << kKB) - 1), c1 = i >> kKB;
-    klut[i] = kTq ? level(p.kcb16, c0, 1 << kKB) | (level(p.kcb16, c1, 1 << kKB) << 16) : pk_h2((float)c0, (float)c1);
+  if constexpr (!kDirect) {
+    for (int i = tid; i < (1 << (2 * kKB)); i += 64 * kLw) {
+      const int c0 = i & ((1 << kKB) - 1), c1 = i >> kKB;
+      klut[i] = kTq ? level(p.kcb16, c0, 1 << kKB) | (level(p.kcb16, c1, 1 << kKB) << 16) : pk_h2((float)c0, (float)c1);
+    }
   }
-  for (int i = tid; i < (1 << (2 * kVB)); i += 64 * kLw) {
-    const int c0 = i & ((1 << kVB) - 1), c1 = i >> kVB;
-    vlut[i] = level(p.vcb16, c0, 1 << kVB) | (level(p.vcb16, c1, 1 << kVB) << 16);
+  if constexpr (kVByte) {
+    if (tid < 256) {
+      vlut[2 * tid] = level(p.vcb16, tid & 3, 4) | (level(p.vcb16, (tid >> 2) & 3, 4) << 16);
+      vlut[2 * tid + 1] = level(p.vcb16, (tid >> 4) & 3, 4) | (level(p.vcb16, tid >> 6, 4) << 16);
+    }
+  } else {
+    for (int i = tid; i < (1 << (2 * kVB)); i += 64 * kLw) {
+      const int c0 = i & ((1 << kVB) - 1), c1 = i >> kVB;
+      vlut[i] = level(p.vcb16, c0, 1 << kVB) | (level(p.vcb16, c1, 1 << kVB) << 16);
+    }
   }
   if (wave < 4) {
     float x[4];
@@ -225,19 +252,38 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   // codebook levels below 1/4, so the products stay in range too)
   const float amax = fmaxf(fmaxf(amax_w[0], amax_w[1]), fmaxf(amax_w[2], amax_w[3]));
   const int k0 = (amax > 0.0f) ? min(max(14 - ilogbf(amax), -60), 60) : 0;
-  const float kinv = ldexpf(1.0f, -k0);
+  // direct key codes: channel c of an 8-channel group sits 2 (c & 3) (2-bit) or 4 (c & 1) (4-bit)
+  // bits up in its fp16 half, worth code 2^(shift - 24); the query operand carries 2^-shift
+  auto cshift = [](int c) { return kDirect ? (kKB == 2 ? 2 * (c & 3) : 4 * (c & 1)) : 0; };
+  const float kinv = ldexpf(1.0f, kDirect ? 24 - k0 : -k0);
   // score B operands: channel 32 kb + 8 g + e, head r (zero rows for heads >= G are already zero)
   uint32_t qop[4][4];
+  // bias B operands (method keys): column r < 8 holds fp16(q'[r] 2^k0), column r >= 8 the rounding
+  // residual of the same for head r - 8, so that a column pair sums to q' 2^k0 to about 2^-22
+  uint32_t qbo[4][4];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     const float4 a = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g]);
     const float4 c = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g + 4]);
+    const float qv[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
     const bool live = r < 8;
-    qop[kb][0] = live ? pk_h2(ldexpf(a.x, k0), ldexpf(a.y, k0)) : 0u;
-    qop[kb][1] = live ? pk_h2(ldexpf(a.z, k0), ldexpf(a.w, k0)) : 0u;
-    qop[kb][2] = live ? pk_h2(ldexpf(c.x, k0), ldexpf(c.y, k0)) : 0u;
-    qop[kb][3] = live ? pk_h2(ldexpf(c.z, k0), ldexpf(c.w, k0)) : 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      qop[kb][j] = live ? pk_h2(ldexpf(qv[2 * j], k0 - cshift(2 * j)), ldexpf(qv[2 * j + 1], k0 - cshift(2 * j + 1))) : 0u;
+      if constexpr (kBiasMfma) {
+        float v[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const float x = ldexpf(qv[2 * j + u], k0);
+          const float hi = (float)(_Float16)x;
+          v[u] = live ? hi : x - hi;
+        }
+        qbo[kb][j] = pk_h2(v[0], v[1]);
+      }
+    }
   }
+  const float bscale = ldexpf(1.0f, -k0);
+  const uint32_t ksel = (g & 1) ? 0x03020302u : 0x01000100u;  // 2-bit keys: the lane group's 16-bit field, twice
 
 
   floatx4 acc[8];  // rows 0-7 audio heads, 8-15 video heads; channel 16 cb + r
@@ -247,7 +293,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   if (g < 2) {
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb)
-      *reinterpret_cast<float4*>(txw + (16 * cb + r) * 8 + 4 * g) = make_float4(0.f, 0.f, 0.f, 0.f);
+      *reinterpret_cast<float4*>(txw + text_ofs(16 * cb + r, g)) = make_float4(0.f, 0.f, 0.f, 0.f);
   }
   float m_run = -__builtin_inff(), l_part = 0.0f, nvmax = 0.0f;
   bool started = false;
@@ -272,22 +318,32 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     if constexpr (!kTq) {
       *reinterpret_cast<uint2*>(&mt[wave][lane >> 5][4 * (lane & 31)]) = lt.meta;
       wave_lds_sync();
+      // q' . m: on the matrix cores (every A row holds the window's minima, B the query's hi and lo
+      // columns; a lane adds its column and the partner column r ^ 8), or for 3-bit keys, whose
+      // wider fields leave no registers for the hi / lo operand, in fp32 over the lane group's
+      // channels and summed over the groups
+      floatx4 bacc = {0.f, 0.f, 0.f, 0.f};
       float bp[4];
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
         const uint4 mn4 = *reinterpret_cast<const uint4*>(&mt[wave][0][32 * kb + 8 * g]);
         const uint4 st4 = *reinterpret_cast<const uint4*>(&mt[wave][1][32 * kb + 8 * g]);
-        const float4 qa = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g]);
-        const float4 qc = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g + 4]);
-        float bb = qa.x * lo_h(mn4.x);
-        bb = __builtin_fmaf(qa.y, hi_h(mn4.x), bb);
-        bb = __builtin_fmaf(qa.z, lo_h(mn4.y), bb);
-        bb = __builtin_fmaf(qa.w, hi_h(mn4.y), bb);
-        bb = __builtin_fmaf(qc.x, lo_h(mn4.z), bb);
-        bb = __builtin_fmaf(qc.y, hi_h(mn4.z), bb);
-        bb = __builtin_fmaf(qc.z, lo_h(mn4.w), bb);
-        bb = __builtin_fmaf(qc.w, hi_h(mn4.w), bb);
-        bp[kb] = bb;
+        if constexpr (kBiasMfma) {
+          bacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(mn4.x, mn4.y, mn4.z, mn4.w),
+                                                        h8(qbo[kb][0], qbo[kb][1], qbo[kb][2], qbo[kb][3]), bacc, 0, 0, 0);
+        } else {
+          const float4 qa = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g]);
+          const float4 qc = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g + 4]);
+          float bb = qa.x * lo_h(mn4.x);
+          bb = __builtin_fmaf(qa.y, hi_h(mn4.x), bb);
+          bb = __builtin_fmaf(qa.z, lo_h(mn4.y), bb);
+          bb = __builtin_fmaf(qa.w, hi_h(mn4.y), bb);
+          bb = __builtin_fmaf(qc.x, lo_h(mn4.z), bb);
+          bb = __builtin_fmaf(qc.y, hi_h(mn4.z), bb);
+          bb = __builtin_fmaf(qc.z, lo_h(mn4.w), bb);
+          bb = __builtin_fmaf(qc.w, hi_h(mn4.w), bb);
+          bp[kb] = bb;
+        }
         const uint32_t sv[4] = {st4.x, st4.y, st4.z, st4.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -295,19 +351,35 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
           bq[kb][j] = __builtin_bit_cast(uint32_t, prod);
         }
       }
-      bias = (bp[0] + bp[1]) + (bp[2] + bp[3]);
-      bias += __shfl_xor(bias, 16);
-      bias += __shfl_xor(bias, 32);
+      if constexpr (kBiasMfma) {
+        bias = (bacc[0] + dpp_ror8(bacc[0])) * bscale;
+      } else {
+        bias = (bp[0] + bp[1]) + (bp[2] + bp[3]);
+        bias += __shfl_xor(bias, 16);
+        bias += __shfl_xor(bias, 32);
+      }
     }
     floatx4 sc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
     for (int tb = 0; tb < 2; ++tb) {
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        const uint32_t f = (kKB == 3) ? field64(lt.kf[tb][kb][0], lt.kf[tb][kb][1], ksh) : (lt.kf[tb][kb][0] >> ksh);
         uint32_t a[4];
+        if constexpr (kDirect && kKB == 2) {  // the 16-bit field in both halves, then shifted by 8
+          const uint32_t f = __builtin_amdgcn_perm(lt.kf[tb][kb][0], lt.kf[tb][kb][0], ksel), f8 = f >> 8;
+          a[0] = f & 0x000c0003u;
+          a[1] = f & 0x00c00030u;
+          a[2] = f8 & 0x000c0003u;
+          a[3] = f8 & 0x00c00030u;
+        } else if constexpr (kDirect) {  // 4-bit: byte j of the field holds channels 2j, 2j + 1
+          const uint32_t d = lt.kf[tb][kb][0];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) a[j] = klut[(f >> (2 * kKB * j)) & kKMask];
+          for (int j = 0; j < 4; ++j) a[j] = __builtin_amdgcn_perm(d, d, 0x01010101u * j) & 0x00f0000fu;
+        } else {
+          const uint32_t f = (kKB == 3) ? field64(lt.kf[tb][kb][0], lt.kf[tb][kb][1], ksh) : (lt.kf[tb][kb][0] >> ksh);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) a[j] = klut[(f >> (2 * kKB * j)) & kKMask];
+        }
         sc[tb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(a[0], a[1], a[2], a[3]),
                                                         h8(bq[kb][0], bq[kb][1], bq[kb][2], bq[kb][3]), sc[tb],
                                                         0, 0, 0);
@@ -357,7 +429,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
       if (g < 2) {
 #pragma unroll
         for (int cb = 0; cb < 8; ++cb) {
-          float4* t4 = reinterpret_cast<float4*>(txw + (16 * cb + r) * 8 + 4 * g);
+          float4* t4 = reinterpret_cast<float4*>(txw + text_ofs(16 * cb + r, g));
           const float4 v = *t4;
           float ai[4];
 #pragma unroll
@@ -399,12 +471,22 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) {
       uint32_t dq[4];
+      if constexpr (kVByte) {  // bytes 2 jj, 2 jj + 1 of the row's 16: channels 8 jj .. 8 jj + 7
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int j = 4 * jj + u;
-        const int bit = 2 * kVB * j, d = bit >> 5, sh = bit & 31;
-        const uint32_t f = (sh + 2 * kVB <= 32) ? (lt.vc[d] >> sh) : field64(lt.vc[d], lt.vc[d + 1], sh);
-        dq[u] = vlut[f & kVMask];
+        for (int u = 0; u < 2; ++u) {
+          const int by = 2 * jj + u;
+          const uint2 lv = *reinterpret_cast<const uint2*>(&vlut[2 * ((lt.vc[by >> 2] >> (8 * (by & 3))) & 0xffu)]);
+          dq[2 * u] = lv.x;
+          dq[2 * u + 1] = lv.y;
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int j = 4 * jj + u;
+          const int bit = 2 * kVB * j, d = bit >> 5, sh = bit & 31;
+          const uint32_t f = (sh + 2 * kVB <= 32) ? (lt.vc[d] >> sh) : field64(lt.vc[d], lt.vc[d + 1], sh);
+          dq[u] = vlut[f & kVMask];
+        }
       }
       const int slot = (8 * vhalf + jj) ^ (vrw & 15);
       *reinterpret_cast<uint4*>(vtw + vrw * 256 + 16 * slot) = make_uint4(dq[0], dq[1], dq[2], dq[3]);
@@ -420,7 +502,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
       if (has_t) {  // wave-uniform
         const floatx4 t = __builtin_amdgcn_mfma_f32_16x16x32_f16(a_tx, vb, floatx4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
         if (g < 2) {
-          float4* t4 = reinterpret_cast<float4*>(txw + (16 * cb + r) * 8 + 4 * g);
+          float4* t4 = reinterpret_cast<float4*>(txw + text_ofs(16 * cb + r, g));
           const float4 v = *t4;
           *t4 = make_float4(v.x + t[0], v.y + t[1], v.z + t[2], v.w + t[3]);
         }
@@ -460,7 +542,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   float* wacc = reinterpret_cast<float*>(&vt[0][0]);  // [wave][channel][16 rows]: audio 0-7, video 8-15
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb)
-    *reinterpret_cast<float4*>(wacc + ((size_t)wave * kD + 16 * cb + r) * 16 + 4 * g) =
+    *reinterpret_cast<float4*>(wacc + row_ofs(wave, 16 * cb + r, g)) =
         make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
   if (lane < 8) {
     wst[0][lane][wave] = started ? m_run : -__builtin_inff();
@@ -493,7 +575,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
       L += (wst[0][hh][u] == -__builtin_inff()) ? 0.0f : wst[1][hh][u] * __builtin_amdgcn_exp2f(wst[0][hh][u] - M);
     const float scl = (hh < p.G && L > 0.0f) ? ldexpf(1.0f / L, e) : 0.0f;
     // the wave's accumulators carry its operand scale 2^E_w
-    fac[hh][w] = (wst[0][hh][w] == -__builtin_inff())
+    fac[w][hh] = (wst[0][hh][w] == -__builtin_inff())
                      ? 0.0f
                      : __builtin_amdgcn_exp2f(wst[0][hh][w] - M - (float)wexp[w]) * scl;
     if (w == 0) {
@@ -502,18 +584,25 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     }
   }
   __syncthreads();
-  // A tile [head][128 m + k] (fp16): the waves' rows summed with their factors, in wave order
-  for (int idx = tid; idx < 3 * 8 * kD; idx += 64 * kLw) {
-    const int m = idx / (8 * kD), hh = (idx / kD) & 7, k = idx & (kD - 1);
-    float a = 0.0f;
+  // A tile [head][128 m + k] (fp16): the waves' rows summed with their factors, in wave order;
+  // thread = (row quad rq, channel k), rows 4 rq .. 4 rq + 3 = heads 4 (rq & 1) .. + 3 of modality rq / 2
+  for (int idx = tid; idx < 6 * kD; idx += 64 * kLw) {
+    const int rq = idx >> 7, k = idx & (kD - 1), m = rq >> 1, hq = rq & 1;
+    float a[4] = {0.f, 0.f, 0.f, 0.f};
     if (mask & (1u << m)) {
 #pragma unroll
       for (int w = 0; w < kLw; ++w) {
-        const float v = (m < 2) ? wacc[((size_t)w * kD + k) * 16 + 8 * m + hh] : ttx[w][k][hh];
-        a = __builtin_fmaf(fac[hh][w], v, a);
+        const float4 f = *reinterpret_cast<const float4*>(&fac[w][4 * hq]);
+        const float4 v = (m < 2) ? *reinterpret_cast<const float4*>(wacc + row_ofs(w, k, rq))
+                                 : *reinterpret_cast<const float4*>(&ttx[w][0][0] + text_ofs(k, hq));
+        a[0] = __builtin_fmaf(f.x, v.x, a[0]);
+        a[1] = __builtin_fmaf(f.y, v.y, a[1]);
+        a[2] = __builtin_fmaf(f.z, v.z, a[2]);
+        a[3] = __builtin_fmaf(f.w, v.w, a[3]);
       }
     }
-    atile[hh][m * kD + k] = (_Float16)a;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) atile[4 * hq + i][m * kD + k] = (_Float16)a[i];
   }
   __syncthreads();
   floatx4 dacc = {0.f, 0.f, 0.f, 0.f};
