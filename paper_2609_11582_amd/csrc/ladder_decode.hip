@@ -4,12 +4,13 @@
 // Work-group (split, KV head h, sequence b) = 8 waves; wave w takes the split's 32-token windows
 // w, w + 8, ... and keeps its own online softmax for the G <= 8 query heads of the KV head.
 //  * scores s_t = n_t (q' . zhat_t), q' = H q sm_scale log2(e). The A operands of the score MFMA
-//    come from each lane's 8 b-bit field of a token row: 2- and 4-bit codes of the method's keys
+//    come from one contiguous run of each lane's token row (channels 32 g .. 32 g + 31; k-block kb
+//    takes channels 32 g + 8 kb .. + 7 in both operands): 2- and 4-bit codes of the method's keys
 //    directly, as fp16 subnormals (the field masked per channel pair; the power of two of a
 //    channel's bit position is folded into the query operand), 3-bit codes and TurboQuant levels
 //    through a small LDS table indexed by a code pair. For the method's keys zhat = m + step code
-//    is split as in the 2-bit kernel: the window term q' . m in fp32 (a per-window bias; on the
-//    matrix cores against the query's fp16 hi and lo parts, or in fp32 FMAs for 3-bit keys) and
+//    is split as in the 2-bit kernel: the window term q' . m in fp32 (a per-window bias, on the
+//    matrix cores against the query's fp16 hi and lo parts) and
 //    sum_c q'_c step_c code_c on the matrix cores with B = fp16(q'_c step_c 2^(k0 - shift_c)) --
 //    rounding the whole of m + step code to fp16 would cost too much where the keys' window means
 //    are large (they drift);
@@ -82,7 +83,7 @@ __device__ __forceinline__ int text_ofs(int k, int s) { return (k << 3) + 4 * (s
 // One window's loads for one lane (issued a window ahead of their use).
 template <int kKB, int kVB>
 struct LTile {
-  uint32_t kf[2][4][2];  // key fields: tile tb, k-block kb: the dword holding the field and the next
+  uint32_t kw[2][kKB];   // key codes of channels 32 g .. 32 g + 31 of token 16 tb + r (4 kKB bytes)
   uint32_t vc[2 * kVB];  // 64 value codes of row lane / 2, channels 64 (lane % 2) .. + 63
   uint2 nk[2], nv[2];    // norms of tokens 16 tb + 4 g .. + 3
   uint32_t md[2];        // their modality bytes
@@ -99,7 +100,6 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   constexpr bool kDirect = !kTq && (kKB == 2 || kKB == 4);
   // 2-bit values: a code byte (4 channels) -> four fp16 codebook levels; else a code pair -> two
   constexpr bool kVByte = kVB == 2;
-  constexpr bool kBiasMfma = !kTq && kKB != 3;  // q' . m of a window on the matrix cores
   __shared__ uint32_t klut[kDirect ? 1 : 1 << (2 * kKB)];  // key code pair -> fp16 pair (integers, or TurboQuant levels)
   __shared__ __attribute__((aligned(8))) uint32_t vlut[kVByte ? 512 : 1 << (2 * kVB)];
   __shared__ __attribute__((aligned(16))) float qs[8][kD + 4];
@@ -141,21 +141,30 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   const size_t nwcap = p.cap / kW;
   const int ntile = (t_end - t_begin + kW - 1) / kW;
   const int nmine = ntile > wave ? (ntile - wave + kLw - 1) / kLw : 0;
-  // key field of k-block kb: byte offset kKB (4 kb + g) of the token row, shift inside its dword
-  auto kfield_dword = [&](int kb) { return (kKB * (4 * kb + g)) >> 2; };
-  const int ksh = 8 * ((kKB * g) & 3);  // the same for every kb (4 kb kKB is a multiple of 4)
+  // The score MFMA's k-block kb takes channels 32 g + 8 kb .. + 7 in lane group g (the A and B
+  // operands agree on it, and the contraction covers every channel once), so a lane's four blocks
+  // are one contiguous run of 4 kKB bytes of the token row.
 
   auto issue_tile = [&](int tile, LTile<kKB, kVB>& lt) {
     const int t0 = t_begin + tile * kW;
     const int last = t_end - 1;
 #pragma unroll
     for (int tb = 0; tb < 2; ++tb) {
-      const uint32_t* row = reinterpret_cast<const uint32_t*>(kbase + (size_t)min(t0 + 16 * tb + r, last) * kKRow);
+      const uint8_t* row = kbase + (size_t)min(t0 + 16 * tb + r, last) * kKRow + 4 * kKB * g;
+      if constexpr (kKB == 2) {
+        const uint2 u = *reinterpret_cast<const uint2*>(row);
+        lt.kw[tb][0] = u.x;
+        lt.kw[tb][1] = u.y;
+      } else if constexpr (kKB == 4) {
+        const uint4 u = *reinterpret_cast<const uint4*>(row);
+        lt.kw[tb][0] = u.x;
+        lt.kw[tb][1] = u.y;
+        lt.kw[tb][2] = u.z;
+        lt.kw[tb][3] = u.w;
+      } else {
+        const uint32_t* w = reinterpret_cast<const uint32_t*>(row);
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const int d0 = kfield_dword(kb);
-        lt.kf[tb][kb][0] = row[d0];
-        lt.kf[tb][kb][1] = (kKB == 3) ? row[min(d0 + 1, 4 * kKB - 1)] : 0u;
+        for (int i = 0; i < kKB; ++i) lt.kw[tb][i] = w[i];
       }
       // norms and modalities of 4 tokens inside the window (slots past the length are masked later)
       lt.nk[tb] = *reinterpret_cast<const uint2*>(nkbase + t0 + 16 * tb + 4 * g);
@@ -163,13 +172,23 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
       lt.md[tb] = *reinterpret_cast<const uint32_t*>(mdbase + t0 + 16 * tb + 4 * g);
     }
     {
-      const uint2* vrow = reinterpret_cast<const uint2*>(vbase + (size_t)min(t0 + (lane >> 1), last) * kVRow) +
-                          kVB * (lane & 1);
+      const uint8_t* vrow = vbase + (size_t)min(t0 + (lane >> 1), last) * kVRow + 8 * kVB * (lane & 1);
+      if constexpr (kVB % 2 == 0) {  // 16-byte aligned halves
 #pragma unroll
-      for (int i = 0; i < kVB; ++i) {
-        const uint2 u = vrow[i];
-        lt.vc[2 * i] = u.x;
-        lt.vc[2 * i + 1] = u.y;
+        for (int i = 0; i < kVB / 2; ++i) {
+          const uint4 u = reinterpret_cast<const uint4*>(vrow)[i];
+          lt.vc[4 * i] = u.x;
+          lt.vc[4 * i + 1] = u.y;
+          lt.vc[4 * i + 2] = u.z;
+          lt.vc[4 * i + 3] = u.w;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < kVB; ++i) {
+          const uint2 u = reinterpret_cast<const uint2*>(vrow)[i];
+          lt.vc[2 * i] = u.x;
+          lt.vc[2 * i + 1] = u.y;
+        }
       }
     }
     if constexpr (!kTq) {
@@ -263,14 +282,14 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   uint32_t qbo[4][4];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
-    const float4 a = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g]);
-    const float4 c = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g + 4]);
+    const float4 a = *reinterpret_cast<const float4*>(&qs[r & 7][32 * g + 8 * kb]);
+    const float4 c = *reinterpret_cast<const float4*>(&qs[r & 7][32 * g + 8 * kb + 4]);
     const float qv[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
     const bool live = r < 8;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       qop[kb][j] = live ? pk_h2(ldexpf(qv[2 * j], k0 - cshift(2 * j)), ldexpf(qv[2 * j + 1], k0 - cshift(2 * j + 1))) : 0u;
-      if constexpr (kBiasMfma) {
+      if constexpr (!kTq) {
         float v[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
@@ -283,7 +302,6 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     }
   }
   const float bscale = ldexpf(1.0f, -k0);
-  const uint32_t ksel = (g & 1) ? 0x03020302u : 0x01000100u;  // 2-bit keys: the lane group's 16-bit field, twice
 
 
   floatx4 acc[8];  // rows 0-7 audio heads, 8-15 video heads; channel 16 cb + r
@@ -318,32 +336,15 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
     if constexpr (!kTq) {
       *reinterpret_cast<uint2*>(&mt[wave][lane >> 5][4 * (lane & 31)]) = lt.meta;
       wave_lds_sync();
-      // q' . m: on the matrix cores (every A row holds the window's minima, B the query's hi and lo
-      // columns; a lane adds its column and the partner column r ^ 8), or for 3-bit keys, whose
-      // wider fields leave no registers for the hi / lo operand, in fp32 over the lane group's
-      // channels and summed over the groups
+      // q' . m on the matrix cores: every A row holds the window's minima, B the query's hi and lo
+      // columns; a lane adds its column and the partner column r ^ 8
       floatx4 bacc = {0.f, 0.f, 0.f, 0.f};
-      float bp[4];
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        const uint4 mn4 = *reinterpret_cast<const uint4*>(&mt[wave][0][32 * kb + 8 * g]);
-        const uint4 st4 = *reinterpret_cast<const uint4*>(&mt[wave][1][32 * kb + 8 * g]);
-        if constexpr (kBiasMfma) {
-          bacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(mn4.x, mn4.y, mn4.z, mn4.w),
-                                                        h8(qbo[kb][0], qbo[kb][1], qbo[kb][2], qbo[kb][3]), bacc, 0, 0, 0);
-        } else {
-          const float4 qa = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g]);
-          const float4 qc = *reinterpret_cast<const float4*>(&qs[r & 7][32 * kb + 8 * g + 4]);
-          float bb = qa.x * lo_h(mn4.x);
-          bb = __builtin_fmaf(qa.y, hi_h(mn4.x), bb);
-          bb = __builtin_fmaf(qa.z, lo_h(mn4.y), bb);
-          bb = __builtin_fmaf(qa.w, hi_h(mn4.y), bb);
-          bb = __builtin_fmaf(qc.x, lo_h(mn4.z), bb);
-          bb = __builtin_fmaf(qc.y, hi_h(mn4.z), bb);
-          bb = __builtin_fmaf(qc.z, lo_h(mn4.w), bb);
-          bb = __builtin_fmaf(qc.w, hi_h(mn4.w), bb);
-          bp[kb] = bb;
-        }
+        const uint4 mn4 = *reinterpret_cast<const uint4*>(&mt[wave][0][32 * g + 8 * kb]);
+        const uint4 st4 = *reinterpret_cast<const uint4*>(&mt[wave][1][32 * g + 8 * kb]);
+        bacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(mn4.x, mn4.y, mn4.z, mn4.w),
+                                                      h8(qbo[kb][0], qbo[kb][1], qbo[kb][2], qbo[kb][3]), bacc, 0, 0, 0);
         const uint32_t sv[4] = {st4.x, st4.y, st4.z, st4.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -351,13 +352,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
           bq[kb][j] = __builtin_bit_cast(uint32_t, prod);
         }
       }
-      if constexpr (kBiasMfma) {
-        bias = (bacc[0] + dpp_ror8(bacc[0])) * bscale;
-      } else {
-        bias = (bp[0] + bp[1]) + (bp[2] + bp[3]);
-        bias += __shfl_xor(bias, 16);
-        bias += __shfl_xor(bias, 32);
-      }
+      bias = (bacc[0] + dpp_ror8(bacc[0])) * bscale;
     }
     floatx4 sc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
@@ -366,17 +361,21 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
       for (int kb = 0; kb < 4; ++kb) {
         uint32_t a[4];
         if constexpr (kDirect && kKB == 2) {  // the 16-bit field in both halves, then shifted by 8
-          const uint32_t f = __builtin_amdgcn_perm(lt.kf[tb][kb][0], lt.kf[tb][kb][0], ksel), f8 = f >> 8;
+          const uint32_t d = lt.kw[tb][kb >> 1];
+          const uint32_t f = __builtin_amdgcn_perm(d, d, (kb & 1) ? 0x03020302u : 0x01000100u), f8 = f >> 8;
           a[0] = f & 0x000c0003u;
           a[1] = f & 0x00c00030u;
           a[2] = f8 & 0x000c0003u;
           a[3] = f8 & 0x00c00030u;
         } else if constexpr (kDirect) {  // 4-bit: byte j of the field holds channels 2j, 2j + 1
-          const uint32_t d = lt.kf[tb][kb][0];
+          const uint32_t d = lt.kw[tb][kb];
 #pragma unroll
           for (int j = 0; j < 4; ++j) a[j] = __builtin_amdgcn_perm(d, d, 0x01010101u * j) & 0x00f0000fu;
         } else {
-          const uint32_t f = (kKB == 3) ? field64(lt.kf[tb][kb][0], lt.kf[tb][kb][1], ksh) : (lt.kf[tb][kb][0] >> ksh);
+          // the block's field: bits 8 kKB kb .. + 8 kKB - 1 of the lane's run
+          constexpr int kFieldBits = 8 * kKB;
+          const int bit = kFieldBits * kb, dw = bit >> 5, sh = bit & 31;
+          const uint32_t f = (sh + kFieldBits <= 32) ? (lt.kw[tb][dw] >> sh) : field64(lt.kw[tb][dw], lt.kw[tb][dw + 1], sh);
 #pragma unroll
           for (int j = 0; j < 4; ++j) a[j] = klut[(f >> (2 * kKB * j)) & kKMask];
         }
