@@ -530,13 +530,25 @@ def stream_measurement(okvq, torch, np, dev, stream):
         dev_app.append((e0, e1))
     torch.cuda.synchronize()
     dev_app_us = float(np.median([a.elapsed_time(b) for a, b in dev_app[2:]])) * 1e3
+    # the append kernel alone: events bound to its dispatch (okvq_append_timed)
+    kern = []
+    for s in range(10):
+        e2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for e in e2:
+            e.record(stream)
+        okvq.okvq_append_timed(c, [L0] * B, kn[steps - 1], vn[steps - 1], mods[steps - 1], [step] * B, nn, step, e2,
+                               stream=stream)
+        c.buffers["seq_lens"][:B].copy_(back)
+        kern.append(e2)
+    torch.cuda.synchronize()
+    kern_us = float(np.median([a.elapsed_time(b) for a, b in kern[2:]])) * 1e3
     mean_len = N + step * (steps + 1) / 2
     abytes = append_algorithmic_bytes(B, H, [step] * B)
     dbytes = decode_algorithmic_bytes(B, H, Hq, [int(mean_len)] * B)
     res = {"workload": "omni3b_b4_64k_stream", "batch": B, "kv_heads": H, "q_heads": Hq, "prefill": N,
            "steps": steps, "tokens_per_step": step,
            "append_us": round(float(np.mean(app[1:])), 2), "append_GBps": round(abytes / np.mean(app[1:]) / 1e3, 1),
-           "append_device_us": round(dev_app_us, 2),
+           "append_device_us": round(dev_app_us, 2), "append_kernel_us": round(kern_us, 2),
            "decode_us": round(float(np.mean(dec[1:])), 2), "decode_GBps_warm": round(dbytes / np.mean(dec[1:]) / 1e3, 1),
            "step_us": round(float(np.mean([a + d for a, d in zip(app[1:], dec[1:])])), 2),
            "append_algorithmic_bytes": abytes}
@@ -814,6 +826,17 @@ def residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
         app1d.append((e0, e1))
     torch.cuda.synchronize()
     append1_dev_us = float(np.median([a.elapsed_time(b) for a, b in app1d[5:]])) * 1e3
+    app1k = []  # the append kernel alone: events bound to its dispatch (okvq_append_timed)
+    for i in range(25):
+        c = caches[(3 * i + 2) % n_cache]
+        e2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for e in e2:
+            e.record(stream)
+        okvq.okvq_append_timed(c, lens, k1, v1, m1, [1] * B, one, 1, e2, stream=stream)
+        c.buffers["seq_lens"][:B].copy_(back)
+        app1k.append(e2)
+    torch.cuda.synchronize()
+    append1_kern_us = float(np.median([a.elapsed_time(b) for a, b in app1k[5:]])) * 1e3
     reps = []
     for rep in range(5):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -844,6 +867,7 @@ def residual_measurement(okvq, torch, np, wl, lens, k_in, v_in, m0, n_new_dev, q
             "k_decode_us": round(split_us, 3), "k_decode_merge_residual_us": round(merge_us, 3),
             "append_prefill_us": round(append_us, 3), "append_one_token_us": round(append1_us, 3),
             "append_one_token_device_us": round(append1_dev_us, 3),
+            "append_one_token_kernel_us": round(append1_kern_us, 3),
             "algorithmic_bytes": dbytes, "replicas": n_cache}
 
 

@@ -285,6 +285,19 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
                         const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
                         const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream);
 
+/* okvq_append that also times its codec: events[0] and events[1] (hipEvent_t handles created by the
+ * caller) are recorded at the start and end of the execution of the one launch that codes the keys
+ * and values (the window-parallel launch of a small append, or the fused codec launch), so that
+ * hipEventElapsedTime of the pair is that kernel's duration without the host's submission. The cache
+ * bytes are those of okvq_append. OKVQ_ERR_INVALID_ARGUMENT for a null events array or handle;
+ * OKVQ_ERR_UNSUPPORTED where the append takes other launches too or none (the bit-width ladder,
+ * OKVQ_VALUE_EXACT, the fp16 residual on the fused-codec path, more than 256 sequences, no new
+ * token), before anything is launched. */
+okvq_status okvq_append_timed(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
+                              const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
+                              const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream,
+                              void* const* events);
+
 /* Status word of a cache (seq_lens[B + 1]): 0, or 1 once an append's value codec stopped waiting for
  * its partner waves after a bounded number of polls and went on with incomplete tables (that
  * append's value codes may be wrong; addresses stay in bounds). The one call of the library that

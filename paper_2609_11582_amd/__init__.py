@@ -6,7 +6,7 @@ include/okvq.h); ``okvq`` is its ctypes binding.
 
 from . import okvq  # noqa: F401
 from .okvq import (KVCache, OkvqError, calibration_workspace, decode_workspace, dense_workspace,  # noqa: F401
-                   make_dims, okvq_append, okvq_buffer_bytes, okvq_calibration_weights,
+                   make_dims, okvq_append, okvq_append_timed, okvq_buffer_bytes, okvq_calibration_weights,
                    okvq_calibration_workspace_bytes, okvq_codebook, okvq_codebook_bits, okvq_decode_attention,
                    okvq_decode_attention_dense, okvq_decode_attention_noalloc, okvq_decode_attention_timed, okvq_decode_workspace_bytes,
                    okvq_dense_workspace_bytes, okvq_cache_status, okvq_prepare_rotation, okvq_quantize_keys,

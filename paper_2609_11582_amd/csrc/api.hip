@@ -528,9 +528,11 @@ static okvq_status ladder_append(const okvq_cache* cache, const int32_t* lens_ho
   return OKVQ_OK;
 }
 
-okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new, const uint16_t* v_new,
-                        const uint8_t* mod_new, const int32_t* n_new_host, const int32_t* n_new_dev, int32_t n_max,
-                        uint32_t flags, void* stream) {
+// events (okvq_append_timed): two events bound to the one launch that codes keys and values
+static okvq_status append_impl(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
+                               const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
+                               const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream,
+                               void* const* events) {
   okvq_status st = check_cache(cache);
   if (st != OKVQ_OK) return st;
   if (!lens_host || !n_new_host || n_max < 0 || (flags & ~(uint32_t)(OKVQ_VALUE_EXACT | OKVQ_GLOBAL_ROTATION)))
@@ -548,6 +550,13 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool exact = (flags & OKVQ_VALUE_EXACT) != 0;
+  hipEvent_t ev[2];
+  if (events) {  // one codec launch to bind the events to
+    if (!events[0] || !events[1]) return OKVQ_ERR_INVALID_ARGUMENT;
+    if (is_ladder(&d) || exact || d.batch > kMaxLenArgs || span == 0) return OKVQ_ERR_UNSUPPORTED;
+    ev[0] = static_cast<hipEvent_t>(events[0]);
+    ev[1] = static_cast<hipEvent_t>(events[1]);
+  }
   if (is_ladder(&d)) return span > 0 ? ladder_append(cache, lens_host, k_new, v_new, mod_new, n_new_host, n_new_dev, n_max,
                                                      exact, s)
                                      : OKVQ_OK;
@@ -565,6 +574,7 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
     if (!strcmp(env, "tile")) window_path = false;
     if (!strcmp(env, "window") && !exact && !is_mx(&d)) window_path = true;
   }
+  if (events && d.residual && !window_path) return OKVQ_ERR_UNSUPPORTED;  // a second launch
   if (d.residual && span > 0 && !window_path) {  // the fp16 rows, before the codec advances the lengths
     if ((int64_t)d.batch * d.num_kv_heads > INT32_MAX) return OKVQ_ERR_UNSUPPORTED;
     st = hip_status(launch_residual_store(k_new, v_new, n_max, cache->seq_lens, n_new_dev, d.batch, d.num_kv_heads,
@@ -628,14 +638,28 @@ okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const
           const int L = lens_host[b0 + i], n = n_new_host[b0 + i];
           if (n > 0) chunk_nwin = std::max(chunk_nwin, (L + n + kW - 1) / kW - L / kW);
         }
-        st = hip_status(launch_append_window(a, chunk_nwin, nb, s));
+        st = hip_status(launch_append_window(a, chunk_nwin, nb, s, events ? ev : nullptr));
       } else {
-        st = hip_status(launch_codec(a, true, true, s));
+        st = hip_status(launch_codec(a, true, true, s, events ? ev : nullptr));
       }
     }
     if (st != OKVQ_OK) return st;
   }
   return OKVQ_OK;
+}
+
+okvq_status okvq_append(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new, const uint16_t* v_new,
+                        const uint8_t* mod_new, const int32_t* n_new_host, const int32_t* n_new_dev, int32_t n_max,
+                        uint32_t flags, void* stream) {
+  return append_impl(cache, lens_host, k_new, v_new, mod_new, n_new_host, n_new_dev, n_max, flags, stream, nullptr);
+}
+
+okvq_status okvq_append_timed(const okvq_cache* cache, const int32_t* lens_host, const uint16_t* k_new,
+                              const uint16_t* v_new, const uint8_t* mod_new, const int32_t* n_new_host,
+                              const int32_t* n_new_dev, int32_t n_max, uint32_t flags, void* stream,
+                              void* const* events) {
+  if (!events) return OKVQ_ERR_INVALID_ARGUMENT;
+  return append_impl(cache, lens_host, k_new, v_new, mod_new, n_new_host, n_new_dev, n_max, flags, stream, events);
 }
 
 okvq_status okvq_cache_status(const okvq_cache* cache, int32_t* status, void* stream) {

@@ -21,6 +21,8 @@
 // window's new minimum and step, their value codes are kept. The work-group of the first window, the
 // only one that reads the stage, rewrites it with the raw rows of the new open window after a
 // barrier that follows its reads. The last work-group to finish advances the lengths.
+#include <hip/hip_ext.h>
+
 #include "launch.hpp"
 
 namespace okvq {
@@ -441,7 +443,7 @@ __global__ __launch_bounds__(kThreads) void k_append_window(WindowArgs a) {
 
 }  // namespace
 
-hipError_t launch_append_window(const CodecArgs& c, int nwin, int nb, hipStream_t s) {
+hipError_t launch_append_window(const CodecArgs& c, int nwin, int nb, hipStream_t s, hipEvent_t const* events) {
   if (nwin <= 0 || nb <= 0) return hipSuccess;
   WindowArgs a;
   a.src = c.j.src;
@@ -471,12 +473,12 @@ hipError_t launch_append_window(const CodecArgs& c, int nwin, int nb, hipStream_
   a.global_rot = c.j.global_rot;
   const int key_meta = c.key_meta;
   const dim3 grid(2 * nwin, a.H, nb);
-  if (key_meta == kMetaTq)
-    hipLaunchKernelGGL(k_append_window<kMetaTq>, grid, dim3(kThreads), 0, s, a);
-  else if (key_meta == kMetaFp16)
-    hipLaunchKernelGGL(k_append_window<kMetaFp16>, grid, dim3(kThreads), 0, s, a);
+  if (key_meta != kMetaTq && key_meta != kMetaFp16) return hipErrorInvalidValue;
+  void (*fn)(WindowArgs) = key_meta == kMetaTq ? k_append_window<kMetaTq> : k_append_window<kMetaFp16>;
+  if (events)
+    hipExtLaunchKernelGGL(fn, grid, dim3(kThreads), 0, s, events[0], events[1], 0, a);
   else
-    return hipErrorInvalidValue;
+    hipLaunchKernelGGL(fn, grid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -27,6 +27,8 @@
 // B[8 (l / 16) + e][l % 16], and D[4 (l / 16) + i][l % 16], i = 0..3. With rows = tokens and
 // columns = output channels, lane l ends with channel 16 nb + l % 16 of four consecutive tokens:
 // one byte of the value-code layout, at offset 16 l + 8 (rb & 1) + nb of the window block.
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 #include <cstdlib>
 
@@ -539,7 +541,16 @@ hipError_t launch_prepare_fragments(const float* rot, uint4* frag, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_codec(const CodecArgs& args, bool keys, bool values, hipStream_t s) {
+// one launch, bound to the two events when given
+template <typename Kernel>
+void launch_one(Kernel fn, int grid, int block, hipStream_t s, hipEvent_t const* events, const CodecArgs& a) {
+  if (events)
+    hipExtLaunchKernelGGL(fn, dim3(grid), dim3(block), 0, s, events[0], events[1], 0, a);
+  else
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(block), 0, s, a);
+}
+
+hipError_t launch_codec(const CodecArgs& args, bool keys, bool values, hipStream_t s, hipEvent_t const* events) {
   if (args.ntiles <= 0 || (!keys && !values)) return hipSuccess;
   CodecArgs a = args;
   a.spin_limit = kSpinLimit;
@@ -556,20 +567,20 @@ hipError_t launch_codec(const CodecArgs& args, bool keys, bool values, hipStream
   const int grid = std::min(a.ntiles, per_cu * cus);
   if (keys && values) {
     if (a.key_meta == kMetaMx)
-      hipLaunchKernelGGL((k_codec<true, true, kMetaMx>), dim3(grid), dim3(512), 0, s, a);
+      launch_one(k_codec<true, true, kMetaMx>, grid, 512, s, events, a);
     else if (a.key_meta == kMetaTq)
-      hipLaunchKernelGGL((k_codec<true, true, kMetaTq>), dim3(grid), dim3(512), 0, s, a);
+      launch_one(k_codec<true, true, kMetaTq>, grid, 512, s, events, a);
     else
-      hipLaunchKernelGGL((k_codec<true, true, kMetaFp16>), dim3(grid), dim3(512), 0, s, a);
+      launch_one(k_codec<true, true, kMetaFp16>, grid, 512, s, events, a);
   } else if (keys) {
     if (a.key_meta == kMetaMx)
-      hipLaunchKernelGGL((k_codec<true, false, kMetaMx>), dim3(grid), dim3(256), 0, s, a);
+      launch_one(k_codec<true, false, kMetaMx>, grid, 256, s, events, a);
     else if (a.key_meta == kMetaTq)
-      hipLaunchKernelGGL((k_codec<true, false, kMetaTq>), dim3(grid), dim3(256), 0, s, a);
+      launch_one(k_codec<true, false, kMetaTq>, grid, 256, s, events, a);
     else
-      hipLaunchKernelGGL((k_codec<true, false, kMetaFp16>), dim3(grid), dim3(256), 0, s, a);
+      launch_one(k_codec<true, false, kMetaFp16>, grid, 256, s, events, a);
   } else {
-    hipLaunchKernelGGL((k_codec<false, true, kMetaFp16>), dim3(grid), dim3(256), 0, s, a);
+    launch_one(k_codec<false, true, kMetaFp16>, grid, 256, s, events, a);
   }
   return hipGetLastError();
 }

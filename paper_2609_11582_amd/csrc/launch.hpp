@@ -71,11 +71,12 @@ struct CodecArgs {
   uint16_t* k_res;
   uint16_t* v_res;
 };
-hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t s);
+// events (optional): two events recorded at the start and end of the launch's execution
+hipError_t launch_codec(const CodecArgs& a, bool keys, bool values, hipStream_t s, hipEvent_t const* events = nullptr);
 // Window-parallel append (MFMA-mode values; fp16 window metadata or TurboQuant keys): one launch
 // over nwin key windows per sequence from each open window, with the residual rings and the length
 // update (seq_lens_out, ticket as for the tile launch). Writes the tile codec's bytes.
-hipError_t launch_append_window(const CodecArgs& a, int nwin, int nb, hipStream_t s);
+hipError_t launch_append_window(const CodecArgs& a, int nwin, int nb, hipStream_t s, hipEvent_t const* events = nullptr);
 hipError_t launch_prepare_fragments(const float* rot, uint4* frag, hipStream_t s);
 hipError_t launch_advance_lengths(int32_t* seq_lens, const int32_t* count, int B, hipStream_t s);
 // Residual rings: rows of the appended tokens among the last 128 of each sequence (device lengths).

@@ -83,6 +83,8 @@ def lib() -> ctypes.CDLL:
         L.okvq_quantize_values.argtypes = [P(Dims), vp, vp, i32, P(i32), vp, u32, vp, vp, vp]
         L.okvq_append.restype = i32
         L.okvq_append.argtypes = [P(CacheStruct), P(i32), vp, vp, vp, P(i32), vp, i32, u32, vp]
+        L.okvq_append_timed.restype = i32
+        L.okvq_append_timed.argtypes = [P(CacheStruct), P(i32), vp, vp, vp, P(i32), vp, i32, u32, vp, P(vp)]
         L.okvq_cache_status.restype = i32
         L.okvq_cache_status.argtypes = [P(CacheStruct), P(i32), vp]
         L.okvq_prepare_rotation.restype = i32
@@ -255,6 +257,28 @@ def okvq_append(cache: "KVCache", lens, k_new, v_new, mod_new, n_new, n_new_dev,
                            _i32(n_new), _ptr(n_new_dev), int(n_max), int(flags), _stream(stream))
     if check:
         _check(st, "okvq_append")
+    return st
+
+
+def okvq_append_timed(cache: "KVCache", lens, k_new, v_new, mod_new, n_new, n_new_dev, n_max, events, flags=0,
+                      stream=None, check=True) -> int:
+    """okvq_append that records two torch.cuda.Event objects at the start and end of its codec
+    launch (the window-parallel launch, or the fused codec launch)."""
+    B, H = cache.dims.batch, cache.dims.num_kv_heads
+    _need_len(lens, B, "lens")
+    _need_len(n_new, B, "n_new")
+    _need(k_new, B * H * int(n_max) * 128 * 2, "k_new")
+    _need(v_new, B * H * int(n_max) * 128 * 2, "v_new")
+    _need(mod_new, B * int(n_max), "mod_new")
+    _need(n_new_dev, B * 4, "n_new_dev")
+    _need_len(events, 2, "events")
+    handles = (ctypes.c_void_p * 2)(*[ctypes.c_void_p(e.cuda_event) for e in events])
+    if not all(handles):
+        raise ValueError("events: record each torch.cuda.Event once before passing it (torch creates them lazily)")
+    st = lib().okvq_append_timed(ctypes.byref(cache.struct), _i32(lens), _ptr(k_new), _ptr(v_new), _ptr(mod_new),
+                                 _i32(n_new), _ptr(n_new_dev), int(n_max), int(flags), _stream(stream), handles)
+    if check:
+        _check(st, "okvq_append_timed")
     return st
 
 

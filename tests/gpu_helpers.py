@@ -68,9 +68,10 @@ def new_cache(B, H, Hq, capacity, signs, rot, key_meta="fp16"):
                         torch.from_numpy(np.asarray(rot, np.float32)), key_meta=key_meta)
 
 
-def append_chunks(cache, k, v, modality, lens, chunk_plan, exact=False, flags=0):
+def append_chunks(cache, k, v, modality, lens, chunk_plan, exact=False, flags=0, timed=None):
     """Append each sequence in the given chunks. chunk_plan: list of per-step token counts [B].
-    flags: more append flags (OKVQ_GLOBAL_ROTATION)."""
+    flags: more append flags (OKVQ_GLOBAL_ROTATION). timed: a list that receives the codec launch's
+    duration (ms) of every step, through okvq_append_timed."""
     B, H, N, D = k.shape
     cur = np.zeros(B, np.int64)
     for step in chunk_plan:
@@ -85,9 +86,19 @@ def append_chunks(cache, k, v, modality, lens, chunk_plan, exact=False, flags=0)
             vn[b, :, :c - a] = v[b, :, a:c]
             mn[b, :c - a] = modality[b, a:c]
         nd = dev(n_new.astype(np.int32))
-        okvq.okvq_append(cache, cur.astype(np.int32).tolist(), f16dev(kn), f16dev(vn), dev(mn),
-                         n_new.astype(np.int32).tolist(), nd, n_max,
-                         (okvq.okvq.OKVQ_VALUE_EXACT if exact else 0) | flags)
+        fl = (okvq.okvq.OKVQ_VALUE_EXACT if exact else 0) | flags
+        if timed is not None and n_new.sum() > 0:
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            for e in ev:
+                e.record()
+            torch.cuda.synchronize()
+            okvq.okvq_append_timed(cache, cur.astype(np.int32).tolist(), f16dev(kn), f16dev(vn), dev(mn),
+                                   n_new.astype(np.int32).tolist(), nd, n_max, ev, fl)
+            torch.cuda.synchronize()
+            timed.append(ev[0].elapsed_time(ev[1]))
+        else:
+            okvq.okvq_append(cache, cur.astype(np.int32).tolist(), f16dev(kn), f16dev(vn), dev(mn),
+                             n_new.astype(np.int32).tolist(), nd, n_max, fl)
         torch.cuda.synchronize()
         cur = cur + n_new
     return cur

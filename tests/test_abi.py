@@ -412,3 +412,27 @@ def test_ladder_buffers_and_validation():
     assert L.okvq_quantize_values(ctypes.byref(d), fake, fake, 10, lens, fake, g, fake, fake, None) == -2
     assert okvq.okvq_codebook_bits(3)[0][0] < 0 and len(okvq.okvq_codebook_bits(4)[1]) == 15
     assert L.okvq_codebook_bits(5, (ctypes.c_float * 16)(), (ctypes.c_float * 15)()) == -1
+
+
+def test_timed_append_rejects_before_launching():
+    """okvq_append_timed binds its events to the one codec launch: it refuses a null events array or
+    handle, and appends that take other launches too (the ladder layout, the exact value order) or
+    none, before anything is launched (fake pointers, never dereferenced)."""
+    okvq = _lib()
+    L = okvq.lib()
+    fake = ctypes.c_void_p(4096)
+    ev = (ctypes.c_void_p * 2)(4096, 8192)
+    ev_null = (ctypes.c_void_p * 2)(4096, 0)
+    d2 = okvq.make_dims(2, 2, 8, 64)
+    c2 = okvq.CacheStruct(d2, *([4096] * 9), 4096, 4096, 4096)
+    lens0 = (ctypes.c_int32 * 2)(0, 0)
+    n_new = (ctypes.c_int32 * 2)(4, 0)
+    none = (ctypes.c_int32 * 2)(0, 0)
+    args = (lens0, fake, fake, fake, n_new, fake, 4)
+    assert L.okvq_append_timed(ctypes.byref(c2), *args, 0, None, None) == -1
+    assert L.okvq_append_timed(ctypes.byref(c2), *args, 0, None, ev_null) == -1
+    assert L.okvq_append_timed(ctypes.byref(c2), *args, okvq.OKVQ_VALUE_EXACT, None, ev) == -2
+    assert L.okvq_append_timed(ctypes.byref(c2), lens0, fake, fake, fake, none, fake, 4, 0, None, ev) == -2
+    dl = okvq.make_dims(2, 2, 8, 64, key_bits=4, value_bits=4)
+    cl = okvq.CacheStruct(dl, *([4096] * 9), 4096, 4096, 4096, 0, 0, 0)
+    assert L.okvq_append_timed(ctypes.byref(cl), *args, 0, None, ev) == -2

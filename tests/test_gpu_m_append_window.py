@@ -36,7 +36,7 @@ def _layer(seed):
     return k, v, mod, lay["signs"], lay["rot"]
 
 
-def _appended(monkeypatch, path, meta, plan, residual=0, flags=0, seed=2):
+def _appended(monkeypatch, path, meta, plan, residual=0, flags=0, seed=2, timed=None):
     import gpu_helpers as gh
     import paper_2609_11582_amd as okvq
     import torch
@@ -44,7 +44,7 @@ def _appended(monkeypatch, path, meta, plan, residual=0, flags=0, seed=2):
     monkeypatch.setenv("OKVQ_APPEND_PATH", path)
     cache = okvq.KVCache(len(LENS), 2, 16, 1024, torch.from_numpy(np.asarray(signs, np.int8)),
                          torch.from_numpy(np.asarray(rot, np.float32)), key_meta=meta, residual=residual)
-    done = gh.append_chunks(cache, k, v, mod, LENS, plan, flags=flags)
+    done = gh.append_chunks(cache, k, v, mod, LENS, plan, flags=flags, timed=timed)
     assert list(done) == LENS
     out = gh.cache_to_numpy(cache)
     out["ticket"] = int(cache.buffers["seq_lens"][len(LENS)].item())
@@ -95,3 +95,16 @@ def test_window_path_global_rotation(monkeypatch):
     tile, _ = _appended(monkeypatch, "tile", "fp16", PLANS["ragged_chunks"], flags=g, seed=6)
     for name in tile:
         _same(win[name], tile[name], name)
+
+
+@pytest.mark.parametrize("path,plan_name", [("window", "ragged_chunks"), ("tile", "stream_512")])
+def test_timed_append_writes_the_same_bytes(path, plan_name, monkeypatch):
+    """okvq_append_timed (events bound to the codec launch) writes the bytes of okvq_append and
+    gives one positive duration per step."""
+    _announce(f"timed append {path} plan={plan_name}")
+    ms = []
+    timed, _ = _appended(monkeypatch, path, "fp16", PLANS[plan_name], seed=8, timed=ms)
+    plain, _ = _appended(monkeypatch, path, "fp16", PLANS[plan_name], seed=8)
+    for name in plain:
+        _same(timed[name], plain[name], name)
+    assert len(ms) > 0 and all(0.0 < x < 100.0 for x in ms), ms
