@@ -914,10 +914,11 @@ constexpr int kMergeThreads = 256;
 constexpr int kMergeUnroll = 8;  // splits per thread held in registers at once
 
 // Eight split records of one chunk (splits s0, s0 + 8, ..., s0 + 56) for query head hd and channel
-// quad q4; splits beyond nsplit read as empty.
+// quad q4, as loaded; the fold treats splits beyond nsplit (read through a clamped index) as empty.
 struct SplitChunk {
   float ms[kMergeUnroll], ls[kMergeUnroll];
   float4 v[kMergeUnroll];
+  int s0, nsplit;
 };
 
 __device__ __forceinline__ void load_split_chunk(const float* base, int nsplit, int hd, int q4, int s0, SplitChunk& c) {
@@ -925,14 +926,16 @@ __device__ __forceinline__ void load_split_chunk(const float* base, int nsplit, 
   for (int u = 0; u < kMergeUnroll; ++u) {
     const int s = s0 + 8 * u;
     const float* rs = base + (size_t)min(s, nsplit - 1) * kRecFloats;
-    // loaded unconditionally (the record index is clamped), then selected: a conditional load is
-    // compiled as a branch, after which the wait before the fold covers every load in flight and the
-    // chunk's last loads go out a round trip late
-    const float m = rs[hd];
-    c.ms[u] = (s < nsplit) ? m : -__builtin_inff();
+    // loaded unconditionally (the record index is clamped) and selected in the fold: a conditional
+    // load is compiled as a branch, after which the wait before the fold covers every load in flight
+    // and the chunk's last loads go out a round trip late; a select here would wait for the load
+    // before any later load of the caller goes out
+    c.ms[u] = rs[hd];
     c.ls[u] = rs[8 + hd];
     c.v[u] = *reinterpret_cast<const float4*>(rs + kRecHeader + hd * kD + 4 * q4);
   }
+  c.s0 = s0;
+  c.nsplit = nsplit;
   __builtin_amdgcn_sched_barrier(0);  // the whole chunk's loads go out before the fold
 }
 
@@ -941,9 +944,12 @@ __device__ __forceinline__ void load_split_chunk(const float* base, int nsplit, 
 // add nothing: their weight is selected to zero and their outputs are zeros (records past nsplit,
 // read through the clamped index, are selected away).
 __device__ __forceinline__ void fold_split_chunk(const SplitChunk& c, float& M, float& L, float4& o) {
+  float ms[kMergeUnroll];
+#pragma unroll
+  for (int u = 0; u < kMergeUnroll; ++u) ms[u] = (c.s0 + 8 * u < c.nsplit) ? c.ms[u] : -__builtin_inff();
   float mc = M;
 #pragma unroll
-  for (int u = 0; u < kMergeUnroll; ++u) mc = fmaxf(mc, c.ms[u]);
+  for (int u = 0; u < kMergeUnroll; ++u) mc = fmaxf(mc, ms[u]);
   const bool any = mc != -__builtin_inff();
   const float a = any ? exp2f(M - mc) : 1.0f;  // M = -inf -> 0
   L *= a;
@@ -953,8 +959,8 @@ __device__ __forceinline__ void fold_split_chunk(const SplitChunk& c, float& M, 
   o.w *= a;
 #pragma unroll
   for (int u = 0; u < kMergeUnroll; ++u) {
-    const bool live = c.ms[u] != -__builtin_inff();
-    const float w = live ? exp2f(c.ms[u] - mc) * c.ls[u] : 0.0f;
+    const bool live = ms[u] != -__builtin_inff();
+    const float w = live ? exp2f(ms[u] - mc) * c.ls[u] : 0.0f;
     L = live ? L + w : L;
     o.x = live ? __builtin_fmaf(w, c.v[u].x, o.x) : o.x;
     o.y = live ? __builtin_fmaf(w, c.v[u].y, o.y) : o.y;
@@ -1059,7 +1065,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   __shared__ __attribute__((aligned(16))) float qp[kD];   // q sm_scale log2(e)
   __shared__ __attribute__((aligned(16))) float qr[kD];   // H q sm_scale log2(e) (rotated query)
   __shared__ float ps[kResidual];                         // tail scores, then weights
-  __shared__ __attribute__((aligned(16))) float ot[4][kD];  // tail output partials, 4 token quarters
+  __shared__ __attribute__((aligned(16))) float ot[16][kD];  // tail output partials, 16 token groups
   __shared__ float tred[kMergeThreads / 64];
   __shared__ __attribute__((aligned(16))) float mst[4][2][kD];  // (minimum, step) of the tail's quantized windows
   const int j = blockIdx.x, b = blockIdx.y;
@@ -1072,62 +1078,67 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   // ---- every load goes out before any is used: the first chunk of split records, then (once the
   // length is known) the query, the metadata of the tail's quantized windows, the tail's keys
   // (codes and norms, or fp16 rows) and the value rows this thread sums ----
+  const int len_dev = ta.seq_lens[b];  // first, a scalar load in flight while the records' loads go out
   SplitChunk ch0;
   if (sg < nsplit) load_split_chunk(base, nsplit, hd, q4, sg, ch0);
-  const int L = min(max(ta.seq_lens[b], 0), ta.cap);
+  const int L = min(max(len_dev, 0), ta.cap);
   const int T0 = max(L - kResidual, 0), nt = L - T0, Kq = L & ~(kResidual - 1);
   // quantized keys [T0, Kq) lie in windows w0 .. w0 + 3 (Kq - T0 <= 128 and Kq is window aligned)
   const int w0 = T0 / kW, nwq = (Kq > T0) ? (Kq - 1) / kW - w0 + 1 : 0;
-  uint32_t qx = 0;
-  int8_t sgn = 1;
-  if (tid < kD) {
-    qx = ta.q[((size_t)b * Hq + j) * kD + tid];
-    sgn = ta.signs[tid];
-  }
-  uint32_t mraw[2], sraw[2];  // metadata entries idx = tid, tid + 256 of the (window, channel) table
+  // loaded by every thread (channel tid mod 128) and used after the barrier: a load inside a branch
+  // gets its use pulled in behind it, and the wait there holds back every later load
+  const uint32_t qx = ta.q[((size_t)b * Hq + j) * kD + (tid & (kD - 1))];
+  const int8_t sgn = ta.signs[tid & (kD - 1)];
+  // metadata entries idx = tid, tid + 256 of the (window, channel) table, as loaded (entries past the
+  // tail's windows read window w0's, never used): fp16 minimum and step, or the MXFP4 record's
+  // nibble bytes and block scales (channel 4q + i in nibble i of bytes 4q, 4q + 1 (minimum), 4q + 2,
+  // 4q + 3 (step); scales at 128 + 2 (c / 32), + 1)
+  uint32_t mraw[2], sraw[2], mscl[2], sscl[2];
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
     const int idx = tid + kMergeThreads * r;
-    mraw[r] = sraw[r] = 0;
-    if (idx < nwq * kD) {
-      const int wi = idx >> 7, c = idx & (kD - 1);
-      const size_t w = seq * (ta.cap / kW) + w0 + wi;
-      if (ta.k_mx) {  // record: channel 4q + i in nibble i of bytes 4q, 4q + 1 (minimum), 4q + 2, 4q + 3 (step)
-        const uint8_t* rec = ta.k_mx + w * kMxRecord;
-        const int qq = c >> 2, i = c & 3;
-        mraw[r] = ((rec[4 * qq + (i >> 1)] >> (4 * (i & 1))) & 15u) | ((uint32_t)rec[128 + 2 * (c >> 5)] << 8);
-        sraw[r] = ((rec[4 * qq + 2 + (i >> 1)] >> (4 * (i & 1))) & 15u) | ((uint32_t)rec[129 + 2 * (c >> 5)] << 8);
-      } else {
-        mraw[r] = ta.k_min[w * kD + c];
-        sraw[r] = ta.k_step[w * kD + c];
-      }
+    const int ic = (idx < nwq * kD) ? idx : (idx & (kD - 1));
+    const int wi = ic >> 7, c = ic & (kD - 1);
+    const size_t w = seq * (ta.cap / kW) + w0 + wi;
+    if (ta.k_mx) {  // uniform
+      const uint8_t* rec = ta.k_mx + w * kMxRecord;
+      const int qq = c >> 2, i = c & 3;
+      mraw[r] = rec[4 * qq + (i >> 1)];
+      sraw[r] = rec[4 * qq + 2 + (i >> 1)];
+      mscl[r] = rec[128 + 2 * (c >> 5)];
+      sscl[r] = rec[129 + 2 * (c >> 5)];
+    } else {
+      mraw[r] = ta.k_min[w * kD + c];
+      sraw[r] = ta.k_step[w * kD + c];
+      mscl[r] = sscl[r] = 0;
     }
   }
   // scores: two threads per token tt = tid / 2, channels 64 half .. 64 half + 63
   const int tt = tid >> 1, half = tid & 1, ti = T0 + tt;
   const bool tok = tt < nt, quant = tok && ti < Kq;
+  // both forms of the token's key, loaded by every thread (clamped indices, branch-free): a load in
+  // a branch makes later loads wait behind it (the two branches share registers)
+  const int tc = min(ti, ta.cap - 1);
+  const uint4 kq = *reinterpret_cast<const uint4*>(ta.k_codes + (seq * ta.cap + tc) * 32 + 16 * half);
+  const uint32_t knrm = ta.k_norm[seq * ta.cap + tc];
   uint4 kr[8];
-  uint32_t knrm = 0;
-  if (quant) {
-    kr[0] = *reinterpret_cast<const uint4*>(ta.k_codes + (seq * ta.cap + ti) * 32 + 16 * half);
-    knrm = ta.k_norm[seq * ta.cap + ti];
-  } else if (tok) {
+  {
     const uint4* row = reinterpret_cast<const uint4*>(ta.k_res + (seq * kResidual + (ti & (kResidual - 1))) * kD +
                                                       64 * half);
 #pragma unroll
     for (int u = 0; u < 8; ++u) kr[u] = row[u];
   }
-  // output: thread (channel pair cp, token quarter tq) sums tokens tq, tq + 4, ...
-  const int cp = tid & 63, tq = tid >> 6;
-  uint32_t vv[kResidual / 4];
+  // output: thread (channel octet c8, token group tg) sums tokens tg, tg + 16, ..., tg + 112 (16-byte
+  // loads: a wave keeps fewer than 64 loads in flight, the most its counter tracks)
+  const int c8 = tid & 15, tg = tid >> 4;
+  uint4 vv[kResidual / 16];
   {
-    const uint32_t* vr = reinterpret_cast<const uint32_t*>(ta.v_res + seq * kResidual * kD) + cp;
+    const uint4* vr = reinterpret_cast<const uint4*>(ta.v_res + seq * kResidual * kD) + c8;
 #pragma unroll
-    for (int u = 0; u < kResidual / 4; ++u) {
-      const int t2 = tq + 4 * u;
-      vv[u] = (t2 < nt) ? vr[((T0 + t2) & (kResidual - 1)) * (kD / 2)] : 0u;
-    }
+    for (int u = 0; u < kResidual / 16; ++u)  // every ring row (finite); rows past the tail get weight 0
+      vv[u] = vr[((T0 + tg + 16 * u) & (kResidual - 1)) * (kD / 8)];
   }
+  __builtin_amdgcn_sched_barrier(0);  // every load above goes out before the first use
 
   // ---- the query, plain and rotated (one wave: butterflies through LDS), the metadata as fp32 ----
   if (tid < kD) {
@@ -1141,8 +1152,9 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
     if (idx < nwq * kD) {
       float mn, st;
       if (ta.k_mx) {
-        mn = e2m1_decode(mraw[r] & 15u, (int)(mraw[r] >> 8) - 127);
-        st = e2m1_decode(sraw[r] & 15u, (int)(sraw[r] >> 8) - 127);
+        const int i = idx & 3;
+        mn = e2m1_decode((mraw[r] >> (4 * (i & 1))) & 15u, (int)mscl[r] - 127);
+        st = e2m1_decode((sraw[r] >> (4 * (i & 1))) & 15u, (int)sscl[r] - 127);
       } else {
         mn = h2f(mraw[r]);
         st = h2f(sraw[r]);
@@ -1172,7 +1184,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
     if (tok) {
       float acc = 0.0f;
       if (quant) {  // n16 (q' . (m + step code)) over the window's metadata
-        const uint32_t words[4] = {kr[0].x, kr[0].y, kr[0].z, kr[0].w};
+        const uint32_t words[4] = {kq.x, kq.y, kq.z, kq.w};
         const float* mrow = mst[ti / kW - w0][0];
         const float* srow = mst[ti / kW - w0][1];
 #pragma unroll
@@ -1209,16 +1221,20 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   if (tid < nt) ps[tid] = exp2f(ps[tid] - mtail);
   __syncthreads();
   {
-    float o0 = 0.0f, o1 = 0.0f;
+    float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int u = 0; u < kResidual / 4; ++u) {
-      const int t2 = tq + 4 * u;
+    for (int u = 0; u < kResidual / 16; ++u) {
+      const int t2 = tg + 16 * u;
       const float p = (t2 < nt) ? ps[t2] : 0.0f;
-      o0 = __builtin_fmaf(p, h2f(vv[u] & 0xffffu), o0);
-      o1 = __builtin_fmaf(p, h2f(vv[u] >> 16), o1);
+      const uint32_t w4[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        o[2 * e] = __builtin_fmaf(p, h2f(w4[e] & 0xffffu), o[2 * e]);
+        o[2 * e + 1] = __builtin_fmaf(p, h2f(w4[e] >> 16), o[2 * e + 1]);
+      }
     }
-    ot[tq][2 * cp] = o0;
-    ot[tq][2 * cp + 1] = o1;
+    *reinterpret_cast<float4*>(&ot[tg][8 * c8]) = make_float4(o[0], o[1], o[2], o[3]);
+    *reinterpret_cast<float4*>(&ot[tg][8 * c8 + 4]) = make_float4(o[4], o[5], o[6], o[7]);
   }
   if (wave == 0) {  // sum of the weights
     float lsum = 0.0f;
@@ -1245,13 +1261,14 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
     const float at = (nt == 0) ? 0.0f : exp2f(mtail - mf);
     const float ltot = Lt * as + ltail * at;
     const float inv = (ltot > 0.0f) ? 1.0f / ltot : 0.0f;
-    float r[4];
+    float4 tv = *reinterpret_cast<const float4*>(&ot[0][4 * tid]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = 4 * tid + i;
-      const float tv = ot[0][c] + ot[1][c] + ot[2][c] + ot[3][c];
-      r[i] = ((i == 0 ? t.x : i == 1 ? t.y : i == 2 ? t.z : t.w) * as + tv * at) * inv;
+    for (int g2 = 1; g2 < 16; ++g2) {
+      const float4 u = *reinterpret_cast<const float4*>(&ot[g2][4 * tid]);
+      tv = make_float4(tv.x + u.x, tv.y + u.y, tv.z + u.z, tv.w + u.w);
     }
+    const float r[4] = {(t.x * as + tv.x * at) * inv, (t.y * as + tv.y * at) * inv, (t.z * as + tv.z * at) * inv,
+                        (t.w * as + tv.w * at) * inv};
     *reinterpret_cast<float4*>(out + ((size_t)b * Hq + j) * kD + 4 * tid) = make_float4(r[0], r[1], r[2], r[3]);
   }
 }
