@@ -153,16 +153,18 @@ __device__ __forceinline__ void key_inputs(const WindowArgs& a, size_t seq, int 
   const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t, last = J.n_rows - 1;
   const size_t srow = seq * J.n_rows;
   const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-  const uint4 kn = reinterpret_cast<const uint4*>(J.src + (srow + (size_t)min(max(tok - begin, 0), last)) * kD)[j];
-  kraw = select4(tok >= begin && tok < len, kn, zero);
-  if (wi == 0 && begin > first) {  // uniform: older tokens of the open window, from the stage
-    const uint4 ks = reinterpret_cast<const uint4*>(J.stage + (seq * kW + min(t, begin - first - 1)) * kD)[j];
-    kraw = select4(tok < begin, ks, kraw);
-  }
-  sraw = zero;
   const int open = (len / kW) * kW, stok = open + t;
+  const bool staged = wi == 0 && begin > first;  // uniform: older tokens of the open window, from the stage
+  // every load goes out before the selects (a select right behind its load waits for it and holds
+  // back the loads after it)
+  const uint4 kn = reinterpret_cast<const uint4*>(J.src + (srow + (size_t)min(max(tok - begin, 0), last)) * kD)[j];
+  uint4 ks = zero;
+  sraw = zero;
+  if (staged) ks = reinterpret_cast<const uint4*>(J.stage + (seq * kW + min(t, begin - first - 1)) * kD)[j];
   if (wi == 0 && open != first && open < len)  // uniform
     sraw = reinterpret_cast<const uint4*>(J.src + (srow + (size_t)min(max(stok - begin, 0), last)) * kD)[j];
+  kraw = select4(tok >= begin && tok < len, kn, zero);
+  if (staged) kraw = select4(tok < begin, ks, kraw);
 }
 
 // Value work-group, thread (t, j): the value chunk of window token t (new tokens only), its
@@ -193,9 +195,9 @@ __device__ __forceinline__ void key_window(const WindowArgs& a, WindowShared& sh
   const int t = tid >> 4, j = tid & 15;
   const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t;
   const bool valid = tok < len, fresh = valid && tok >= begin;
+  const uint2 sg = *reinterpret_cast<const uint2*>(a.signs + 8 * j);
   uint4 kraw, sraw;
   key_inputs(a, seq, begin, len, wi, t, j, kraw, sraw);
-  const uint2 sg = *reinterpret_cast<const uint2*>(a.signs + 8 * j);
   const int open = (len / kW) * kW, stok = open + t;
   const bool restage = J.stage && wi == 0 && open < len;
   // ---- direction (thread = token chunk); a wave without a valid token skips the arithmetic ----
@@ -308,6 +310,22 @@ __device__ __forceinline__ void value_window(const WindowArgs& a, WindowShared& 
   uint4 vraw;
   uint32_t mymod, wmod;
   value_inputs(a, seq, b, begin, len, wi, t, j, lane, vraw, mymod, wmod);
+  // the window's modalities (a superset of those coded) and the B operands of the first of them,
+  // loaded first: in flight while the norms, tables and stores below are formed, and across the barrier
+  uint32_t mset = 0;
+#pragma unroll
+  for (int m = 0; m < 3; ++m)
+    if (__ballot(wmod == (uint32_t)m)) mset |= 1u << m;
+  if (J.global_rot) mset = mset ? 1u : 0u;  // R_0 for every token
+  const int m_first = mset ? __builtin_ctz(mset) : 0;
+  uint4 bf[4][2];
+  {
+    const uint4* base = a.rotfrag + (size_t)(m_first * 8 + wave) * 8 * 64 + lane;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int part = 0; part < 2; ++part) bf[kk][part] = base[(kk * 2 + part) * 64];
+  }
   const bool busy = __ballot(fresh) != 0;  // wave-uniform
   {
     const uint32_t r4[4] = {vraw.x, vraw.y, vraw.z, vraw.w};
@@ -329,22 +347,6 @@ __device__ __forceinline__ void value_window(const WindowArgs& a, WindowShared& 
   }
   if (a.v_res && fresh && tok >= len - kResidual)  // the residual ring: raw rows of the last 128 tokens
     reinterpret_cast<uint4*>(a.v_res + (seq * kResidual + (tok & (kResidual - 1))) * kD)[j] = vraw;
-  // the window's modalities (a superset of those coded) and the B operands of the first of them,
-  // in flight across the barrier
-  uint32_t mset = 0;
-#pragma unroll
-  for (int m = 0; m < 3; ++m)
-    if (__ballot(wmod == (uint32_t)m)) mset |= 1u << m;
-  if (J.global_rot) mset = mset ? 1u : 0u;  // R_0 for every token
-  const int m_first = mset ? __builtin_ctz(mset) : 0;
-  uint4 bf[4][2];
-  {
-    const uint4* base = a.rotfrag + (size_t)(m_first * 8 + wave) * 8 * 64 + lane;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-      for (int part = 0; part < 2; ++part) bf[kk][part] = base[(kk * 2 + part) * 64];
-  }
   __syncthreads();  // B1: A tile and token tables written
   const int g = lane >> 4;
   const uint32_t tm = sh.tmod[lane & 31];
