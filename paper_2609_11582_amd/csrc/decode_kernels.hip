@@ -1093,24 +1093,30 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   // tail's windows read window w0's, never used): fp16 minimum and step, or the MXFP4 record's
   // nibble bytes and block scales (channel 4q + i in nibble i of bytes 4q, 4q + 1 (minimum), 4q + 2,
   // 4q + 3 (step); scales at 128 + 2 (c / 32), + 1)
-  uint32_t mraw[2], sraw[2], mscl[2], sscl[2];
+  uint32_t mraw[2], sraw[2], mnib[2], snib[2], scl[2];
+  {
+    // both formats' loads on every path (no branch: a branch between loads makes later ones wait
+    // behind earlier ones), from valid addresses: with MXFP4 records the fp16 loads read record bytes,
+    // and without them the record loads read the same window's fp16 minima (a record's bytes lie within
+    // its window's 256-byte row); the format picks which to decode
+    const bool mx = ta.k_mx != nullptr;
+    const uint16_t* kmin = mx ? reinterpret_cast<const uint16_t*>(ta.k_mx) : ta.k_min;
+    const uint16_t* kstep = mx ? reinterpret_cast<const uint16_t*>(ta.k_mx) : ta.k_step;
+    const uint8_t* kmx = mx ? ta.k_mx : reinterpret_cast<const uint8_t*>(ta.k_min);
+    const size_t mxstride = mx ? kMxRecord : 2 * kD;
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int idx = tid + kMergeThreads * r;
-    const int ic = (idx < nwq * kD) ? idx : (idx & (kD - 1));
-    const int wi = ic >> 7, c = ic & (kD - 1);
-    const size_t w = seq * (ta.cap / kW) + w0 + wi;
-    if (ta.k_mx) {  // uniform
-      const uint8_t* rec = ta.k_mx + w * kMxRecord;
+    for (int r = 0; r < 2; ++r) {
+      const int idx = tid + kMergeThreads * r;
+      const int ic = (idx < nwq * kD) ? idx : (idx & (kD - 1));
+      const int wi = ic >> 7, c = ic & (kD - 1);
+      const size_t w = seq * (ta.cap / kW) + w0 + wi;
+      mraw[r] = kmin[mx ? 0 : w * kD + c];
+      sraw[r] = kstep[mx ? 0 : w * kD + c];
+      const uint8_t* rec = kmx + w * mxstride;
       const int qq = c >> 2, i = c & 3;
-      mraw[r] = rec[4 * qq + (i >> 1)];
-      sraw[r] = rec[4 * qq + 2 + (i >> 1)];
-      mscl[r] = rec[128 + 2 * (c >> 5)];
-      sscl[r] = rec[129 + 2 * (c >> 5)];
-    } else {
-      mraw[r] = ta.k_min[w * kD + c];
-      sraw[r] = ta.k_step[w * kD + c];
-      mscl[r] = sscl[r] = 0;
+      mnib[r] = rec[4 * qq + (i >> 1)];
+      snib[r] = rec[4 * qq + 2 + (i >> 1)];
+      scl[r] = *reinterpret_cast<const uint16_t*>(rec + 128 + 2 * (c >> 5));  // minimum's scale, step's scale
     }
   }
   // scores: two threads per token tt = tid / 2, channels 64 half .. 64 half + 63
@@ -1122,9 +1128,9 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   const uint4 kq = *reinterpret_cast<const uint4*>(ta.k_codes + (seq * ta.cap + tc) * 32 + 16 * half);
   const uint32_t knrm = ta.k_norm[seq * ta.cap + tc];
   uint4 kr[8];
-  {
-    const uint4* row = reinterpret_cast<const uint4*>(ta.k_res + (seq * kResidual + (ti & (kResidual - 1))) * kD +
-                                                      64 * half);
+  {  // the token's ring row, or ring row 0 for a quantized key (one shared line, never used)
+    const int rr = quant ? 0 : (ti & (kResidual - 1));
+    const uint4* row = reinterpret_cast<const uint4*>(ta.k_res + (seq * kResidual + rr) * kD + 64 * half);
 #pragma unroll
     for (int u = 0; u < 8; ++u) kr[u] = row[u];
   }
@@ -1153,8 +1159,8 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
       float mn, st;
       if (ta.k_mx) {
         const int i = idx & 3;
-        mn = e2m1_decode((mraw[r] >> (4 * (i & 1))) & 15u, (int)mscl[r] - 127);
-        st = e2m1_decode((sraw[r] >> (4 * (i & 1))) & 15u, (int)sscl[r] - 127);
+        mn = e2m1_decode((mnib[r] >> (4 * (i & 1))) & 15u, (int)(scl[r] & 0xffu) - 127);
+        st = e2m1_decode((snib[r] >> (4 * (i & 1))) & 15u, (int)(scl[r] >> 8) - 127);
       } else {
         mn = h2f(mraw[r]);
         st = h2f(sraw[r]);
