@@ -1088,7 +1088,9 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   // loaded by every thread (channel tid mod 128) and used after the barrier: a load inside a branch
   // gets its use pulled in behind it, and the wait there holds back every later load
   const uint32_t qx = ta.q[((size_t)b * Hq + j) * kD + (tid & (kD - 1))];
-  const int8_t sgn = ta.signs[tid & (kD - 1)];
+  // and, for the rotation in wave 0, channels 4 l .. 4 l + 3 of lane l (mod 32) with their signs
+  const uint2 qrow4 = *reinterpret_cast<const uint2*>(ta.q + ((size_t)b * Hq + j) * kD + 4 * (lane & 31));
+  const uint32_t s4 = *reinterpret_cast<const uint32_t*>(ta.signs + 4 * (lane & 31));
   // metadata entries idx = tid, tid + 256 of the (window, channel) table, as loaded (entries past the
   // tail's windows read window w0's, never used): fp16 minimum and step, or the MXFP4 record's
   // nibble bytes and block scales (channel 4q + i in nibble i of bytes 4q, 4q + 1 (minimum), 4q + 2,
@@ -1146,11 +1148,34 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
   }
   __builtin_amdgcn_sched_barrier(0);  // every load above goes out before the first use
 
-  // ---- the query, plain and rotated (one wave: butterflies through LDS), the metadata as fp32 ----
-  if (tid < kD) {
-    const float x = h2f(qx);
-    qp[tid] = x * ta.qscale;
-    qr[tid] = (sgn < 0) ? -x : x;
+  // ---- the query, plain and rotated (wave 0: the butterflies in registers), the metadata as fp32 ----
+  if (tid < kD) qp[tid] = h2f(qx) * ta.qscale;
+  if (wave == 0) {  // Sylvester order, h ascending: channel bits 0, 1 in the lane, bits 2..6 = lane bits 0..4
+    const uint32_t qw[2] = {qrow4.x, qrow4.y};
+    float x[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float v = h2f((qw[i >> 1] >> (16 * (i & 1))) & 0xffffu);
+      x[i] = ((s4 >> (8 * i + 7)) & 1u) ? -v : v;
+    }
+    {
+      const float a = x[0] + x[1], c = x[0] - x[1], d = x[2] + x[3], e = x[2] - x[3];
+      x[0] = a + d;
+      x[2] = a - d;
+      x[1] = c + e;
+      x[3] = c - e;
+    }
+#pragma unroll
+    for (int lb = 1; lb < 32; lb <<= 1) {
+      const bool hi = (lane & lb) != 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float o = __shfl_xor(x[i], lb);
+        x[i] = hi ? o - x[i] : x[i] + o;
+      }
+    }
+    const float sc = ta.qscale * 0.08838834764831845f;  // 1 / sqrt(128): H is orthonormal
+    if (lane < 32) *reinterpret_cast<float4*>(&qr[4 * lane]) = make_float4(x[0] * sc, x[1] * sc, x[2] * sc, x[3] * sc);
   }
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
@@ -1168,19 +1193,6 @@ __global__ __launch_bounds__(kMergeThreads) void k_decode_merge_residual(const f
       mst[idx >> 7][0][idx & (kD - 1)] = mn;
       mst[idx >> 7][1][idx & (kD - 1)] = st;
     }
-  }
-  __syncthreads();
-  if (wave == 0) {
-    for (int hh = 1; hh < kD; hh <<= 1) {  // Sylvester order: pairs (i, i + hh) with (i & hh) == 0
-      const int i = (lane / hh) * 2 * hh + (lane % hh);
-      const float a = qr[i], c = qr[i + hh];
-      wave_lds_sync();
-      qr[i] = a + c;
-      qr[i + hh] = a - c;
-      wave_lds_sync();
-    }
-    qr[lane] *= ta.qscale * 0.08838834764831845f;  // 1 / sqrt(128): H is orthonormal
-    qr[lane + 64] *= ta.qscale * 0.08838834764831845f;
   }
   __syncthreads();
 
