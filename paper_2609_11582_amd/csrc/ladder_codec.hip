@@ -144,10 +144,11 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
       if (wt0 >= len) break;  // uniform
       const int nv = min(len - wt0, kW);
       float lo = __builtin_inff(), hi = -__builtin_inff();
-      for (int i = 0; i < nv; ++i) {
+#pragma unroll
+      for (int i = 0; i < kW; ++i) {  // all 32 reads in flight at once; slots past the length skipped
         const float v = zt[kW * w + i][c];
-        lo = fminf(lo, v);
-        hi = fmaxf(hi, v);
+        lo = (i < nv) ? fminf(lo, v) : lo;
+        hi = (i < nv) ? fmaxf(hi, v) : hi;
       }
       lo = lo + 0.0f;  // -0 -> +0
       hi = hi + 0.0f;
@@ -158,13 +159,11 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
       a.k_step[mi] = (uint16_t)s16;
       const float m = h2f(m16), s = h2f(s16);
       const float inv = (s != 0.0f) ? div_rn(1.0f, s) : 0.0f;
-      for (int i = 0; i < kW; ++i) {
-        uint32_t code = 0;
-        if (i < nv && s != 0.0f) {
-          const float tt = (zt[kW * w + i][c] - m) * inv;
-          code = (uint32_t)fminf(fmaxf(__builtin_rintf(tt), 0.0f), (float)kTop);
-        }
-        ct[kW * w + i][c] = (uint8_t)code;
+#pragma unroll
+      for (int i = 0; i < kW; ++i) {  // branch-free: the reads go out together
+        const float tt = (zt[kW * w + i][c] - m) * inv;
+        const uint32_t code = (uint32_t)fminf(fmaxf(__builtin_rintf(tt), 0.0f), (float)kTop);
+        ct[kW * w + i][c] = (uint8_t)((i < nv && s != 0.0f) ? code : 0u);
       }
     }
     __syncthreads();
