@@ -275,7 +275,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   // bits up in its fp16 half, worth code 2^(shift - 24); the query operand carries 2^-shift
   auto cshift = [](int c) { return kDirect ? (kKB == 2 ? 2 * (c & 3) : 4 * (c & 1)) : 0; };
   const float kinv = ldexpf(1.0f, kDirect ? 24 - k0 : -k0);
-  // score B operands: channel 32 kb + 8 g + e, head r (zero rows for heads >= G are already zero)
+  // score B operands: channel 32 g + 8 kb + e, head r (zero rows for heads >= G are already zero)
   uint32_t qop[4][4];
   // bias B operands (method keys): column r < 8 holds fp16(q'[r] 2^k0), column r >= 8 the rounding
   // residual of the same for head r - 8, so that a column pair sums to q' 2^k0 to about 2^-22
