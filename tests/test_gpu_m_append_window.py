@@ -97,14 +97,15 @@ def test_window_path_global_rotation(monkeypatch):
         _same(win[name], tile[name], name)
 
 
-@pytest.mark.parametrize("path,plan_name", [("window", "ragged_chunks"), ("tile", "stream_512")])
-def test_timed_append_writes_the_same_bytes(path, plan_name, monkeypatch):
+@pytest.mark.parametrize("path,plan_name,meta", [("window", "ragged_chunks", "fp16"), ("tile", "stream_512", "fp16"),
+                                                ("window", "window_crossing", "turboquant")])
+def test_timed_append_writes_the_same_bytes(path, plan_name, meta, monkeypatch):
     """okvq_append_timed (events bound to the codec launch) writes the bytes of okvq_append and
     gives one positive duration per step."""
-    _announce(f"timed append {path} plan={plan_name}")
+    _announce(f"timed append {path} {meta} plan={plan_name}")
     ms = []
-    timed, _ = _appended(monkeypatch, path, "fp16", PLANS[plan_name], seed=8, timed=ms)
-    plain, _ = _appended(monkeypatch, path, "fp16", PLANS[plan_name], seed=8)
+    timed, _ = _appended(monkeypatch, path, meta, PLANS[plan_name], seed=8, timed=ms)
+    plain, _ = _appended(monkeypatch, path, meta, PLANS[plan_name], seed=8)
     for name in plain:
         _same(timed[name], plain[name], name)
     assert len(ms) > 0 and all(0.0 < x < 100.0 for x in ms), ms
