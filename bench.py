@@ -87,7 +87,7 @@ PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
 CALIBRATION_COPY_BYTES = 256 << 20
 KERNEL_SOURCES = ("codec_kernels.hip", "codec_fused.hip", "decode_kernels.hip", "key_quant.hpp", "value_quant.hpp",
                   "okvq_device.hpp", "launch.hpp", "calib_kernels.hip", "dense_decode.hip", "ladder_codec.hip",
-                  "ladder_decode.hip", "append_window.hip")
+                  "ladder_decode.hip", "append_window.hip", "lane_quant.hpp")
 
 
 def kernel_source_hash() -> str:

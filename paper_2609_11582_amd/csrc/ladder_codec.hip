@@ -16,6 +16,7 @@
 // holds its row of R_m in registers for each modality present in the window (R is read once per
 // window, not once per token); then a thread per (token, 32 channels) packs b dwords.
 #include "key_quant.hpp"
+#include "lane_quant.hpp"
 #include "launch.hpp"
 
 namespace okvq {
@@ -182,6 +183,106 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
       pack32<kBits>(cw, w);
       store_run<kBits>(row, part, w);
     }
+  }
+}
+
+// The method's keys, one work-group of 512 threads per 32-token key window (the window-parallel
+// form; TurboQuant keys keep the token-per-thread kernel above, which needs no window statistics):
+// thread (t, j) holds channels 8j .. 8j + 7 of window token t. The direction runs in the key codec's
+// order across the 16 lanes of the token (lane_direction); the window minimum and maximum of each
+// channel are LDS float atomics over the valid tokens (exact, order-free); 128 threads form the fp16
+// minimum, step = (max - min) / (2^b - 1) and fl(1 / step16); then every thread codes its 8 channels,
+// clamp(rint(fl(fl(z - m16) fl(1 / step16))), 0, 2^b - 1), and writes their b bytes of the token's
+// bit stream (channel 8j + e at bits b e of bytes b j .. b j + b - 1).
+constexpr int kWinThreads = 512;
+constexpr int kWinStatSlots = kD + kD / 8;  // channel c in slot c + c / 8 (spread over the banks)
+
+template <int kBits>
+__global__ __launch_bounds__(kWinThreads) void k_ladder_keys_win(LadderKeyArgs a) {
+  constexpr int kTop = (1 << kBits) - 1;
+  constexpr int kRowBytes = 16 * kBits;
+  __shared__ float kmin[kWinStatSlots], kmax[kWinStatSlots];
+  __shared__ __attribute__((aligned(8))) float2 kstat[kD];  // (fp16 minimum, fl(1 / fp16 step)) as fp32
+  const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz, wi = blockIdx.x;
+  const int tid = threadIdx.x, t = tid >> 4, j = tid & 15;
+  int begin = 0, len = a.lens.lens[bz];
+  if (a.begin_dev) {  // append: the device lengths decide, clamped into the buffers
+    begin = min(max(a.begin_dev[b], 0), a.cap);
+    len = min(begin + min(max(a.count_dev[b], 0), a.n_rows), a.cap);
+  }
+  const int first = (begin / kW) * kW, w0 = first + kW * wi, tok = w0 + t;
+  if (len <= begin || w0 >= len) return;  // uniform over the work-group
+  const size_t seq = (size_t)b * a.H + h;
+  const int npad = (len + kW - 1) / kW * kW;
+  const int open = (len / kW) * kW, stok = open + t, last = a.n_rows - 1;
+  const bool valid = tok < len;
+  const bool staged = a.begin_dev && wi == 0 && begin > first;          // older tokens from the stage
+  const bool restage = a.stage && a.begin_dev && wi == 0 && open < len;  // the new open window's rows
+  if (tid < kWinStatSlots) {
+    kmin[tid] = __builtin_inff();
+    kmax[tid] = -__builtin_inff();
+  }
+  // every load before any use: the signs, the token's row (or its staged row), the open window's row
+  const uint2 sg = *reinterpret_cast<const uint2*>(a.signs + 8 * j);
+  const size_t srow = seq * a.n_rows;
+  const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+  const uint4 kn = reinterpret_cast<const uint4*>(a.k + (srow + (size_t)min(max(tok - begin, 0), last)) * kD)[j];
+  uint4 ks = zero, sraw = zero;
+  if (staged) ks = reinterpret_cast<const uint4*>(a.stage + (seq * kW + min(t, begin - first - 1)) * kD)[j];
+  if (restage && open != first)
+    sraw = reinterpret_cast<const uint4*>(a.k + (srow + (size_t)min(max(stok - begin, 0), last)) * kD)[j];
+  uint4 kraw = make_uint4(valid && tok >= begin ? kn.x : 0u, valid && tok >= begin ? kn.y : 0u,
+                          valid && tok >= begin ? kn.z : 0u, valid && tok >= begin ? kn.w : 0u);
+  if (staged && tok < begin) kraw = ks;
+  __syncthreads();  // the statistics slots are initialized
+  float x[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+  uint32_t n16 = 0;
+  if (__ballot(valid) != 0) n16 = lane_direction(kraw, sg, j, x);  // wave-uniform
+  if (j == 0 && tok < npad) a.k_norm[seq * a.cap + tok] = valid ? (uint16_t)n16 : (uint16_t)0;
+  if (valid) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      __hip_atomic_fetch_min(&kmin[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      __hip_atomic_fetch_max(&kmax[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+  }
+  if (restage) __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stage reads have landed
+  __syncthreads();  // window extremes complete; every stage read of the work-group has landed
+  if (restage && stok >= begin && stok < len)
+    reinterpret_cast<uint4*>(a.stage + (seq * kW + t) * kD)[j] = (open == first) ? kraw : sraw;
+  if (tid < kD) {
+    const float lo = kmin[tid + (tid >> 3)] + 0.0f;  // -0 -> +0
+    const float hi = kmax[tid + (tid >> 3)] + 0.0f;
+    const float step = div_rn(hi - lo, (float)kTop);
+    const uint32_t m16 = f2h(lo), s16 = f2h(step);
+    const size_t mi = (seq * (a.cap / kW) + w0 / kW) * kD + tid;
+    a.k_min[mi] = (uint16_t)m16;
+    a.k_step[mi] = (uint16_t)s16;
+    const float sv = h2f(s16);
+    kstat[tid] = make_float2(h2f(m16), (sv != 0.0f) ? div_rn(1.0f, sv) : 0.0f);
+  }
+  __syncthreads();  // the window's statistics
+  if (tok >= npad) return;
+  uint32_t bits = 0;
+  if (valid) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float2 st = kstat[8 * j + e];
+      const float tt = (x[e] - st.x) * st.y;
+      const uint32_t code = (uint32_t)fminf(fmaxf(__builtin_rintf(tt), 0.0f), (float)kTop);
+      bits |= code << (kBits * e);
+    }
+  }
+  uint8_t* row = a.k_codes + (seq * a.cap + tok) * kRowBytes + kBits * j;
+  if constexpr (kBits == 2) {
+    *reinterpret_cast<uint16_t*>(row) = (uint16_t)bits;
+  } else if constexpr (kBits == 4) {
+    *reinterpret_cast<uint32_t*>(row) = bits;
+  } else {
+#pragma unroll
+    for (int i = 0; i < kBits; ++i) row[i] = (uint8_t)(bits >> (8 * i));
   }
 }
 
@@ -424,11 +525,14 @@ __global__ __launch_bounds__(256) void k_ladder_values_mfma(LadderValueArgs a) {
 }
 
 template <int kBits>
-hipError_t keys_for_bits(const LadderKeyArgs& a, bool tq, dim3 grid, hipStream_t s) {
-  if (tq)
+hipError_t keys_for_bits(const LadderKeyArgs& a, bool tq, int nb, int max_len, hipStream_t s) {
+  if (tq) {
+    const dim3 grid((max_len + kTileTokens - 1) / kTileTokens, a.H, nb);
     hipLaunchKernelGGL((k_ladder_keys<kBits, true>), grid, dim3(kTileTokens), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_ladder_keys<kBits, false>), grid, dim3(kTileTokens), 0, s, a);
+  } else {
+    const dim3 grid((max_len + kW - 1) / kW, a.H, nb);  // one work-group per key window of the span
+    hipLaunchKernelGGL(k_ladder_keys_win<kBits>, grid, dim3(kWinThreads), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -436,11 +540,10 @@ hipError_t keys_for_bits(const LadderKeyArgs& a, bool tq, dim3 grid, hipStream_t
 
 hipError_t launch_ladder_keys(const LadderKeyArgs& a, int bits, bool tq, int nb, int max_len, hipStream_t s) {
   if (nb <= 0 || max_len <= 0) return hipSuccess;
-  const dim3 grid((max_len + kTileTokens - 1) / kTileTokens, a.H, nb);
   switch (bits) {
-    case 2: return keys_for_bits<2>(a, tq, grid, s);
-    case 3: return keys_for_bits<3>(a, tq, grid, s);
-    case 4: return keys_for_bits<4>(a, tq, grid, s);
+    case 2: return keys_for_bits<2>(a, tq, nb, max_len, s);
+    case 3: return keys_for_bits<3>(a, tq, nb, max_len, s);
+    case 4: return keys_for_bits<4>(a, tq, nb, max_len, s);
     default: return hipErrorInvalidValue;
   }
 }
