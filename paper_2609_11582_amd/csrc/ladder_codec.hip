@@ -189,19 +189,20 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
 // The method's keys, one work-group of 512 threads per 32-token key window (the window-parallel
 // form; TurboQuant keys keep the token-per-thread kernel above, which needs no window statistics):
 // thread (t, j) holds channels 8j .. 8j + 7 of window token t. The direction runs in the key codec's
-// order across the 16 lanes of the token (lane_direction); the window minimum and maximum of each
-// channel are LDS float atomics over the valid tokens (exact, order-free); 128 threads form the fp16
-// minimum, step = (max - min) / (2^b - 1) and fl(1 / step16); then every thread codes its 8 channels,
+// order across the 16 lanes of the token (lane_direction) and goes to an LDS tile; 128 threads, one
+// per channel, take the window minimum and maximum over the valid tokens (exact in any order; LDS
+// atomics would serialize the 32 tokens of a channel on one address) and form the fp16 minimum,
+// step = (max - min) / (2^b - 1) and fl(1 / step16); then every thread codes its 8 channels,
 // clamp(rint(fl(fl(z - m16) fl(1 / step16))), 0, 2^b - 1), and writes their b bytes of the token's
 // bit stream (channel 8j + e at bits b e of bytes b j .. b j + b - 1).
 constexpr int kWinThreads = 512;
-constexpr int kWinStatSlots = kD + kD / 8;  // channel c in slot c + c / 8 (spread over the banks)
+constexpr int kWinPitch = kD + 4;  // floats per token row of the direction tile
 
 template <int kBits>
 __global__ __launch_bounds__(kWinThreads) void k_ladder_keys_win(LadderKeyArgs a) {
   constexpr int kTop = (1 << kBits) - 1;
   constexpr int kRowBytes = 16 * kBits;
-  __shared__ float kmin[kWinStatSlots], kmax[kWinStatSlots];
+  __shared__ __attribute__((aligned(16))) float zt[kW][kWinPitch];  // the window's directions
   __shared__ __attribute__((aligned(8))) float2 kstat[kD];  // (fp16 minimum, fl(1 / fp16 step)) as fp32
   const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz, wi = blockIdx.x;
   const int tid = threadIdx.x, t = tid >> 4, j = tid & 15;
@@ -218,10 +219,6 @@ __global__ __launch_bounds__(kWinThreads) void k_ladder_keys_win(LadderKeyArgs a
   const bool valid = tok < len;
   const bool staged = a.begin_dev && wi == 0 && begin > first;          // older tokens from the stage
   const bool restage = a.stage && a.begin_dev && wi == 0 && open < len;  // the new open window's rows
-  if (tid < kWinStatSlots) {
-    kmin[tid] = __builtin_inff();
-    kmax[tid] = -__builtin_inff();
-  }
   // every load before any use: the signs, the token's row (or its staged row), the open window's row
   const uint2 sg = *reinterpret_cast<const uint2*>(a.signs + 8 * j);
   const size_t srow = seq * a.n_rows;
@@ -234,27 +231,29 @@ __global__ __launch_bounds__(kWinThreads) void k_ladder_keys_win(LadderKeyArgs a
   uint4 kraw = make_uint4(valid && tok >= begin ? kn.x : 0u, valid && tok >= begin ? kn.y : 0u,
                           valid && tok >= begin ? kn.z : 0u, valid && tok >= begin ? kn.w : 0u);
   if (staged && tok < begin) kraw = ks;
-  __syncthreads();  // the statistics slots are initialized
   float x[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) x[e] = 0.0f;
   uint32_t n16 = 0;
   if (__ballot(valid) != 0) n16 = lane_direction(kraw, sg, j, x);  // wave-uniform
   if (j == 0 && tok < npad) a.k_norm[seq * a.cap + tok] = valid ? (uint16_t)n16 : (uint16_t)0;
-  if (valid) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      __hip_atomic_fetch_min(&kmin[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-      __hip_atomic_fetch_max(&kmax[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    }
-  }
+  *reinterpret_cast<float4*>(&zt[t][8 * j]) = make_float4(x[0], x[1], x[2], x[3]);
+  *reinterpret_cast<float4*>(&zt[t][8 * j + 4]) = make_float4(x[4], x[5], x[6], x[7]);
   if (restage) __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stage reads have landed
-  __syncthreads();  // window extremes complete; every stage read of the work-group has landed
+  __syncthreads();  // the direction tile is complete; every stage read of the work-group has landed
   if (restage && stok >= begin && stok < len)
     reinterpret_cast<uint4*>(a.stage + (seq * kW + t) * kD)[j] = (open == first) ? kraw : sraw;
   if (tid < kD) {
-    const float lo = kmin[tid + (tid >> 3)] + 0.0f;  // -0 -> +0
-    const float hi = kmax[tid + (tid >> 3)] + 0.0f;
+    const int nv = min(len - w0, kW);
+    float lo = __builtin_inff(), hi = -__builtin_inff();
+#pragma unroll
+    for (int i = 0; i < kW; ++i) {  // all 32 reads in flight at once; slots past the length skipped
+      const float v = zt[i][tid];
+      lo = (i < nv) ? fminf(lo, v) : lo;
+      hi = (i < nv) ? fmaxf(hi, v) : hi;
+    }
+    lo = lo + 0.0f;  // -0 -> +0
+    hi = hi + 0.0f;
     const float step = div_rn(hi - lo, (float)kTop);
     const uint32_t m16 = f2h(lo), s16 = f2h(step);
     const size_t mi = (seq * (a.cap / kW) + w0 / kW) * kD + tid;

@@ -68,6 +68,10 @@ __device__ __forceinline__ short4v lds_tr(const uint8_t* p) {
 __device__ __forceinline__ float dpp_ror8(float v) {  // lane l <- lane (l + 8) mod 16 of its row
   return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x128, 0xf, 0xf, false));
 }
+template <int kN>
+__device__ __forceinline__ float dpp_ror(float v) {  // a rotation by kN lanes inside each 16-lane row
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x120 + kN, 0xf, 0xf, false));
+}
 // bits [sh, sh + n) of the 64-bit word hi:lo (sh < 32)
 __device__ __forceinline__ uint32_t field64(uint32_t lo, uint32_t hi, int sh) {
   return sh == 0 ? lo : __builtin_amdgcn_alignbit(hi, lo, (uint32_t)sh);
@@ -107,7 +111,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   __shared__ __attribute__((aligned(16))) uint16_t mt[kLw][2][kD];         // window (minimum, step)
   __shared__ __attribute__((aligned(16))) _Float16 atile[8][kATileL];
   __shared__ float wst[2][8][kLw];
-  __shared__ uint32_t wmask[kLw], wnv[kLw];
+  __shared__ uint32_t wmask[kLw], nv_all;  // nv_all: the largest value norm (fp32 bits, non-negative)
   __shared__ int wexp[kLw];
   __shared__ __attribute__((aligned(16))) float fac[kLw][8];      // combine factor per wave and head
   __shared__ __attribute__((aligned(16))) float ttx[kLw][kD][8];  // text rows (heads 0-7) per wave, swizzled
@@ -264,6 +268,7 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
 #pragma unroll
     for (int lb = 1; lb < 64; lb <<= 1) am = fmaxf(am, __shfl_xor(am, lb));
     if (lane == 0) amax_w[wave] = am;
+    if (tid == 0) nv_all = 0u;
     *reinterpret_cast<float4*>(&qs[hr][c4]) = make_float4(x[0], x[1], x[2], x[3]);
   }
   __syncthreads();
@@ -401,19 +406,23 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
       if (!ok) mdv[tb] |= 0x03u << (8 * i);  // modality 3: no token
       mx = fmaxf(mx, x[e]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    // mx is the lane's maximum; a head's maximum over its four lane groups is needed only where the
+    // reference moves (a lane above m_run + kLazyL puts its head above it too)
+    auto head_max = [](float v) {
+      v = fmaxf(v, __shfl_xor(v, 16));
+      return fmaxf(v, __shfl_xor(v, 32));
+    };
     float nvl = 0.0f;  // the lane's largest value norm so far, this window's included
 #pragma unroll
     for (int e = 0; e < 8; ++e) nvl = fmaxf(nvl, nvf[e]);
     nvmax = fmaxf(nvmax, nvl);
     if (!started) {
-      m_run = mx;
+      m_run = head_max(mx);
       nvb = min(norm_bound_f(nvmax, 0) + 1, 16);
       E = min(15, 15 - nvb);
       started = true;
     } else if (__any(mx > m_run + kLazyL) || __any(nvmax >= ldexpf(1.0f, nvb))) {
-      const float m_new = fmaxf(m_run, mx);
+      const float m_new = fmaxf(m_run, head_max(mx));
       const int nb = norm_bound_f(nvmax, nvb);
       const int nvb_new = nb > nvb ? min(nb + 1, 16) : nvb;
       const int E_new = min(15, 15 - nvb_new);
@@ -534,11 +543,17 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   }
   float l_tot = l_part + __shfl_xor(l_part, 16);
   l_tot += __shfl_xor(l_tot, 32);
-  float nvw = nvmax;
-#pragma unroll
-  for (int lb = 1; lb < 64; lb <<= 1) nvw = fmaxf(nvw, __shfl_xor(nvw, lb));
-  __syncthreads();  // every wave is done with its value tile: the tiles hold the waves' rows now
-  float* wacc = reinterpret_cast<float*>(&vt[0][0]);  // [wave][channel][16 rows]: audio 0-7, video 8-15
+  // the largest value norm: a maximum over each 16-lane row by DPP rotations, then one LDS atomic per
+  // row (non-negative floats order as their bit patterns)
+  float nvr = nvmax;
+  nvr = fmaxf(nvr, dpp_ror8(nvr));
+  nvr = fmaxf(nvr, dpp_ror<4>(nvr));
+  nvr = fmaxf(nvr, dpp_ror<2>(nvr));
+  nvr = fmaxf(nvr, dpp_ror<1>(nvr));
+  if (r == 0) __hip_atomic_fetch_max(&nv_all, __builtin_bit_cast(uint32_t, nvr), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  // [wave][channel][16 rows]: audio 0-7, video 8-15; wave w's rows fill exactly its own value tile,
+  // which it no longer reads, so no barrier is needed before the writes
+  float* wacc = reinterpret_cast<float*>(&vt[0][0]);
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb)
     *reinterpret_cast<float4*>(wacc + row_ofs(wave, 16 * cb + r, g)) =
@@ -549,17 +564,13 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
   }
   if (lane == 0) {
     wmask[wave] = seen;
-    wnv[wave] = __builtin_bit_cast(uint32_t, nvw);
     wexp[wave] = E;
   }
   __syncthreads();
   uint32_t mask = 0;
-  float nmax = 0.0f;
+  const float nmax = __builtin_bit_cast(float, nv_all);
 #pragma unroll
-  for (int w = 0; w < kLw; ++w) {
-    mask |= wmask[w];
-    nmax = fmaxf(nmax, __builtin_bit_cast(float, wnv[w]));
-  }
+  for (int w = 0; w < kLw; ++w) mask |= wmask[w];
   // merged rows divided by L are convex combinations of n_v cb vectors (|cb| < 1/4): the factor
   // 2^e / L with e = 13 - ilogb(n_max) keeps the fp16 A tile below 2^12
   const int e = (nmax > 0.0f) ? 13 - min(max(ilogbf(nmax), -30), 20) : 0;
