@@ -11,9 +11,8 @@
 // token t (a wave without a token of its own skips the arithmetic):
 //  * key: sign flip, fp16 norm by the halving tree (levels 64 .. 8 across the 16 lanes of the
 //    token, 4 .. 1 in the lane), butterflies h = 1, 2, 4 in the lane and h = 8 .. 64 across lanes,
-//    z = w fl(kappa / n16); the directions go to an LDS tile, and 128 threads take the window
-//    minimum and maximum per channel; codes and their packing in the lane, one key-code dword per
-//    lane pair;
+//    z = w fl(kappa / n16); window minimum and maximum per channel by LDS atomics; codes and their
+//    packing in the lane, one key-code dword per lane pair;
 //  * value: fp16 norm by the same tree; the row goes to an LDS tile of MFMA A operands; wave w then
 //    forms output channels 16w .. 16w + 15 of the window's 32 tokens on the matrix cores (R_m as
 //    fp16 hi + lo B operands, fp32 accumulation, in the tile codec's order), one modality at a time,
@@ -74,13 +73,12 @@ struct WindowArgs {
   int n_rows, b0, H, cap, global_rot;
 };
 
-constexpr int kDirPitch = kD + 4;  // floats per token row of the key direction tile
+constexpr int kStatSlots = kD + kD / 8;
 
 struct WindowShared {
-  union {
-    uint4 atile[2][4][64];      // value work-group: the window's value rows as MFMA A operands
-    float zt[kW][kDirPitch];    // key work-group: the window's directions [token][channel]
-  };
+  uint4 atile[2][4][64];   // the window's value rows as MFMA A operands: [row block][k-block][lane]
+  float kmin[kStatSlots];  // per channel c (slot c + c / 8, spread over the banks): the window
+  float kmax[kStatSlots];  // minimum and maximum, taken by LDS atomics
   float2 kstat[kD];        // per channel: (fp16 minimum, fl(1 / fp16 step)) as fp32
   float itab[kW];          // per token: fl(1 / T) of the value decision (0: no code)
   uint32_t tmod[kW];       // per token: the rotation of its value code (3: none)
@@ -158,30 +156,26 @@ __device__ __forceinline__ void key_window(const WindowArgs& a, WindowShared& sh
   if (busy) kn16 = lane_direction(kraw, sg, j, x);
   if (a.k_res && fresh && tok >= len - kResidual)  // the residual ring: raw rows of the last 128 tokens
     reinterpret_cast<uint4*>(a.k_res + (seq * kResidual + (tok & (kResidual - 1))) * kD)[j] = kraw;
-  // ---- the directions into the LDS tile, for the per-channel window minimum / maximum (LDS atomics
-  // would serialize the tokens of a channel on one address) ----
+  // ---- window minimum / maximum per channel: LDS atomics of the valid tokens ----
   if constexpr (kMeta == kMetaFp16) {
-    *reinterpret_cast<float4*>(&sh.zt[t][8 * j]) = make_float4(x[0], x[1], x[2], x[3]);
-    *reinterpret_cast<float4*>(&sh.zt[t][8 * j + 4]) = make_float4(x[4], x[5], x[6], x[7]);
+    if (valid) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        __hip_atomic_fetch_min(&sh.kmin[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        __hip_atomic_fetch_max(&sh.kmax[9 * j + e], x[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+    }
   }
   if (restage) __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stage reads have landed
-  __syncthreads();  // B1: the direction tile is complete; every stage read has landed
+  __syncthreads();  // B1: window extremes written; every stage read has landed
   if (restage && stok >= begin && stok < len)  // the new open window's raw keys
     reinterpret_cast<uint4*>(J.stage + (seq * kW + t) * kD)[j] = select4(open == first, kraw, sraw);
   const size_t nw = J.cap / kW;
   const int gwin = w0 / kW;
   if constexpr (kMeta == kMetaFp16) {
     if (tid < kD) {
-      const int nv = min(len - w0, kW);
-      float l = __builtin_inff(), u = -__builtin_inff();
-#pragma unroll
-      for (int i = 0; i < kW; ++i) {  // all 32 reads in flight at once; slots past the length skipped
-        const float v = sh.zt[i][tid];
-        l = (i < nv) ? fminf(l, v) : l;
-        u = (i < nv) ? fmaxf(u, v) : u;
-      }
-      l = l + 0.0f;  // canonical +0
-      u = u + 0.0f;
+      const float l = sh.kmin[tid + (tid >> 3)] + 0.0f;  // canonical +0
+      const float u = sh.kmax[tid + (tid >> 3)] + 0.0f;
       const float step = div_rn(u - l, 3.0f);
       const uint32_t m16 = f2h(l), s16 = f2h(step);
       a.k_min[(seq * nw + gwin) * kD + tid] = (uint16_t)m16;
@@ -334,6 +328,13 @@ __global__ __launch_bounds__(kThreads) void k_append_window(WindowArgs a) {
   // the device lengths decide, clamped into the buffers (the host's copy planned the grid)
   const int begin = min(max(J.begin_dev[b], 0), J.cap);
   const int len = min(begin + min(max(J.count_dev[b], 0), J.n_rows), J.cap);
+  if (kMeta == kMetaFp16 && !values) {
+    if (tid < kStatSlots) {
+      sh.kmin[tid] = __builtin_inff();
+      sh.kmax[tid] = -__builtin_inff();
+    }
+    __syncthreads();  // B0 (the waves of a work-group start together)
+  }
   const int w0 = (begin / kW) * kW + kW * wi;  // the work-group's window
   if (len > begin && w0 < len) {               // uniform
     if (values)

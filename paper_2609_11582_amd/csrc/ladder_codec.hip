@@ -245,15 +245,20 @@ __global__ __launch_bounds__(kWinThreads) void k_ladder_keys_win(LadderKeyArgs a
     reinterpret_cast<uint4*>(a.stage + (seq * kW + t) * kD)[j] = (open == first) ? kraw : sraw;
   if (tid < kD) {
     const int nv = min(len - w0, kW);
-    float lo = __builtin_inff(), hi = -__builtin_inff();
+    float lo4[4], hi4[4];  // four independent chains (the minimum and maximum are exact in any order)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      lo4[u] = __builtin_inff();
+      hi4[u] = -__builtin_inff();
+    }
 #pragma unroll
     for (int i = 0; i < kW; ++i) {  // all 32 reads in flight at once; slots past the length skipped
       const float v = zt[i][tid];
-      lo = (i < nv) ? fminf(lo, v) : lo;
-      hi = (i < nv) ? fmaxf(hi, v) : hi;
+      lo4[i & 3] = (i < nv) ? fminf(lo4[i & 3], v) : lo4[i & 3];
+      hi4[i & 3] = (i < nv) ? fmaxf(hi4[i & 3], v) : hi4[i & 3];
     }
-    lo = lo + 0.0f;  // -0 -> +0
-    hi = hi + 0.0f;
+    const float lo = fminf(fminf(lo4[0], lo4[1]), fminf(lo4[2], lo4[3])) + 0.0f;  // -0 -> +0
+    const float hi = fmaxf(fmaxf(hi4[0], hi4[1]), fmaxf(hi4[2], hi4[3])) + 0.0f;
     const float step = div_rn(hi - lo, (float)kTop);
     const uint32_t m16 = f2h(lo), s16 = f2h(step);
     const size_t mi = (seq * (a.cap / kW) + w0 / kW) * kD + tid;
