@@ -396,7 +396,8 @@ __global__ __launch_bounds__(128) void k_ladder_values(LadderValueArgs a) {
 
 // MFMA mode: one work-group of 256 threads (4 waves) per 128 tokens of a (sequence, KV head). The
 // value rows (fp16, exact) are staged in LDS as MFMA A operands; wave w computes output channels
-// 32 w .. 32 w + 31 of all 128 tokens, per modality present, against its slice of R_m split into
+// 32 w .. 32 w + 31, per modality, of the 16-token row blocks holding a token of it (ballots of the
+// norm step mark them), against its slice of R_m split into
 // fp16 hi + lo parts (B operands, converted once per modality and tile), fp32 accumulation. The
 // codes then equal the exact order's except where y lies within a small band of a threshold (about
 // 2^-22 sum_j |R_cj v_j| of accumulation-order and split error, inside the band the tests allow).
@@ -419,6 +420,7 @@ __global__ __launch_bounds__(256) void k_ladder_values_mfma(LadderValueArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t xs[kVTile][kVPitch];
   __shared__ float nrm[kVTile];
   __shared__ int mods[kVTile];
+  __shared__ uint32_t wpres[kVTile / 64];  // bit 8 m + row block: modality m present in those 16 rows
   __shared__ __attribute__((aligned(16))) uint8_t ct[kVTile][kD];
   const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz;
   int begin, len;
@@ -442,14 +444,22 @@ __global__ __launch_bounds__(256) void k_ladder_values_mfma(LadderValueArgs a) {
     if (tok < len && a.mod_out && h == 0) a.mod_out[(size_t)b * a.cap + tok] = (uint8_t)mods[tid];
   }
   __syncthreads();
-  if (tid < kVTile) {  // fp16 norm by the halving tree, as the exact mode
+  if (tid < kVTile) {  // fp16 norm by the halving tree, as the exact mode; the row in 16-byte reads
     const int tok = t0 + tid;
+    float x[kD];
+#pragma unroll
+    for (int c8 = 0; c8 < kD / 8; ++c8) {
+      const uint4 v = *reinterpret_cast<const uint4*>(&xs[tid][8 * c8]);
+      const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        x[8 * c8 + 2 * i] = h2f(w4[i] & 0xffffu);
+        x[8 * c8 + 2 * i + 1] = h2f(w4[i] >> 16);
+      }
+    }
     float tt[64];
 #pragma unroll
-    for (int i = 0; i < 64; ++i) {
-      const float x0 = h2f(xs[tid][i]), x1 = h2f(xs[tid][i + 64]);
-      tt[i] = x0 * x0 + x1 * x1;
-    }
+    for (int i = 0; i < 64; ++i) tt[i] = x[i] * x[i] + x[i + 64] * x[i + 64];
 #pragma unroll
     for (int n = 32; n >= 1; n >>= 1) {
 #pragma unroll
@@ -458,12 +468,23 @@ __global__ __launch_bounds__(256) void k_ladder_values_mfma(LadderValueArgs a) {
     const uint32_t n16 = (tok < len) ? norm_to_f16(sqrt_rn(tt[0])) : 0u;
     nrm[tid] = h2f(n16);
     if (tok < len) a.v_norm[seq * a.cap + tok] = (uint16_t)n16;
+    const int mo = mods[tid];  // -1 past the length
+    uint32_t pres = 0;
+#pragma unroll
+    for (int m = 0; m < 3; ++m) {
+      const uint64_t bm = __ballot(mo == m);  // this wave's tokens: row blocks 4 wave .. 4 wave + 3
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if ((bm >> (16 * i)) & 0xffffu) pres |= 1u << (8 * m + 4 * wave + i);
+    }
+    if (lane == 0) wpres[wave] = pres;
   }
   __syncthreads();
+  uint32_t present = 0;
+#pragma unroll
+  for (int w = 0; w < kVTile / 64; ++w) present |= wpres[w];
   for (int m = 0; m < 3; ++m) {
-    bool any = false;
-    for (int t = 0; t < kVTile; ++t) any |= mods[t] == m;
-    if (!any) continue;  // uniform
+    if (!((present >> (8 * m)) & 0xffu)) continue;  // uniform
     // B operands: channel c = 32 wave + 16 cb + r, k = 32 kb + 8 g .. + 7 of R_m (hi, lo parts)
     uint32_t bh[2][4][4], bl[2][4][4];
 #pragma unroll
@@ -482,6 +503,7 @@ __global__ __launch_bounds__(256) void k_ladder_values_mfma(LadderValueArgs a) {
       }
     }
     for (int rb = 0; rb < kVTile / 16; ++rb) {
+      if (!((present >> (8 * m + rb)) & 1u)) continue;  // no token of modality m in these rows (uniform)
       floatx4v acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
