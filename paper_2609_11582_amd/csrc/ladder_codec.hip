@@ -186,26 +186,37 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
   }
 }
 
-// The method's keys, one work-group of 512 threads per 32-token key window (the window-parallel
-// form; TurboQuant keys keep the token-per-thread kernel above, which needs no window statistics):
-// thread (t, j) holds channels 8j .. 8j + 7 of window token t. The direction runs in the key codec's
-// order across the 16 lanes of the token (lane_direction) and goes to an LDS tile; 128 threads, one
-// per channel, take the window minimum and maximum over the valid tokens (exact in any order; LDS
-// atomics would serialize the 32 tokens of a channel on one address) and form the fp16 minimum,
-// step = (max - min) / (2^b - 1) and fl(1 / step16); then every thread codes its 8 channels,
-// clamp(rint(fl(fl(z - m16) fl(1 / step16))), 0, 2^b - 1), and writes their b bytes of the token's
-// bit stream (channel 8j + e at bits b e of bytes b j .. b j + b - 1).
-constexpr int kWinThreads = 512;
+// The method's keys, one work-group of 128 threads per 32-token key window: thread (t, q) holds
+// channels 32q .. 32q + 31 of window token t, so that a token spans the 4 lanes of a DPP quad. The
+// norm tree and the butterflies run in the key codec's bit-exact order: the tree's levels 64 and 32
+// pair lane q with q ^ 2 and q ^ 1 (both lanes of a pair form the same exact-order sum), the levels
+// 16 .. 1 and the butterfly stages h = 1 .. 16 stay in the lane, and the stages h = 32, 64 cross to
+// lane q ^ 1, q ^ 2 as fl(+-own + partner); z = w fl(kappa / n16). The directions go to an LDS tile;
+// thread c then takes channel c's window minimum and maximum over the valid tokens (exact in any
+// order) and forms the fp16 minimum, step = (max - min) / (2^b - 1) and fl(1 / step16); every thread
+// codes its 32 channels, clamp(rint(fl(fl(z - m16) fl(1 / step16))), 0, 2^b - 1), which fill b
+// dwords of the token's bit stream (the run at dword b q). TurboQuant keys keep the token-per-thread
+// kernel above, which needs no window statistics.
+constexpr int kQuadThreads = 128;
 constexpr int kWinPitch = kD + 4;  // floats per token row of the direction tile
 
+// Butterfly stage across lanes q and q ^ kMask of a quad: the lower lane takes a + b, the upper one
+// a - b, both as fl(s own + partner) with s = +-1 (an exact product, one rounding).
+template <int kMask, int kN>
+__device__ __forceinline__ void quad_stage(float (&x)[kN], int q) {
+  const float s = (q & kMask) ? -1.0f : 1.0f;
+#pragma unroll
+  for (int e = 0; e < kN; ++e) x[e] = __builtin_fmaf(s, x[e], xchg<kMask>(x[e]));
+}
+
 template <int kBits>
-__global__ __launch_bounds__(kWinThreads) void k_ladder_keys_win(LadderKeyArgs a) {
+__global__ __launch_bounds__(kQuadThreads) void k_ladder_keys_quad(LadderKeyArgs a) {
   constexpr int kTop = (1 << kBits) - 1;
   constexpr int kRowBytes = 16 * kBits;
   __shared__ __attribute__((aligned(16))) float zt[kW][kWinPitch];  // the window's directions
   __shared__ __attribute__((aligned(8))) float2 kstat[kD];  // (fp16 minimum, fl(1 / fp16 step)) as fp32
   const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz, wi = blockIdx.x;
-  const int tid = threadIdx.x, t = tid >> 4, j = tid & 15;
+  const int tid = threadIdx.x, t = tid >> 2, q = tid & 3;
   int begin = 0, len = a.lens.lens[bz];
   if (a.begin_dev) {  // append: the device lengths decide, clamped into the buffers
     begin = min(max(a.begin_dev[b], 0), a.cap);
@@ -219,31 +230,99 @@ __global__ __launch_bounds__(kWinThreads) void k_ladder_keys_win(LadderKeyArgs a
   const bool valid = tok < len;
   const bool staged = a.begin_dev && wi == 0 && begin > first;          // older tokens from the stage
   const bool restage = a.stage && a.begin_dev && wi == 0 && open < len;  // the new open window's rows
-  // every load before any use: the signs, the token's row (or its staged row), the open window's row
-  const uint2 sg = *reinterpret_cast<const uint2*>(a.signs + 8 * j);
+  // every load before any use: the signs, the token's 64-byte chunk (or its staged one), the open
+  // window's chunk
+  const uint4* sp = reinterpret_cast<const uint4*>(a.signs + 32 * q);
+  const uint4 sg0 = sp[0], sg1 = sp[1];
   const size_t srow = seq * a.n_rows;
   const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-  const uint4 kn = reinterpret_cast<const uint4*>(a.k + (srow + (size_t)min(max(tok - begin, 0), last)) * kD)[j];
-  uint4 ks = zero, sraw = zero;
-  if (staged) ks = reinterpret_cast<const uint4*>(a.stage + (seq * kW + min(t, begin - first - 1)) * kD)[j];
-  if (restage && open != first)
-    sraw = reinterpret_cast<const uint4*>(a.k + (srow + (size_t)min(max(stok - begin, 0), last)) * kD)[j];
-  uint4 kraw = make_uint4(valid && tok >= begin ? kn.x : 0u, valid && tok >= begin ? kn.y : 0u,
-                          valid && tok >= begin ? kn.z : 0u, valid && tok >= begin ? kn.w : 0u);
-  if (staged && tok < begin) kraw = ks;
-  float x[8];
+  const uint4* kp = reinterpret_cast<const uint4*>(a.k + (srow + (size_t)min(max(tok - begin, 0), last)) * kD + 32 * q);
+  const uint4* stp = reinterpret_cast<const uint4*>(a.stage + (seq * kW + max(min(t, begin - first - 1), 0)) * kD + 32 * q);
+  const uint4* ssp = reinterpret_cast<const uint4*>(a.k + (srow + (size_t)min(max(stok - begin, 0), last)) * kD + 32 * q);
+  const bool fresh = valid && tok >= begin, old = staged && tok < begin;
+  // kraw: the token's 32 keys (from the stage below begin, zero past the length); sraw: those of
+  // token open + t, for the stage
+  uint32_t kraw[16], sraw[16];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) x[e] = 0.0f;
-  uint32_t n16 = 0;
-  if (__ballot(valid) != 0) n16 = lane_direction(kraw, sg, j, x);  // wave-uniform
-  if (j == 0 && tok < npad) a.k_norm[seq * a.cap + tok] = valid ? (uint16_t)n16 : (uint16_t)0;
-  *reinterpret_cast<float4*>(&zt[t][8 * j]) = make_float4(x[0], x[1], x[2], x[3]);
-  *reinterpret_cast<float4*>(&zt[t][8 * j + 4]) = make_float4(x[4], x[5], x[6], x[7]);
+  for (int i = 0; i < 4; ++i) {
+    const uint4 n = kp[i];
+    uint4 o = zero, r = zero;
+    if (staged) o = stp[i];
+    if (restage && open != first) r = ssp[i];
+    const uint4 f = fresh ? n : zero;
+    const uint4 k = old ? o : f;
+    kraw[4 * i] = k.x;
+    kraw[4 * i + 1] = k.y;
+    kraw[4 * i + 2] = k.z;
+    kraw[4 * i + 3] = k.w;
+    sraw[4 * i] = r.x;
+    sraw[4 * i + 1] = r.y;
+    sraw[4 * i + 2] = r.z;
+    sraw[4 * i + 3] = r.w;
+  }
+  // ---- direction: signs applied (the fp16 sign bits flipped), channel 32q + 8i + e in x[8i + e] ----
+  float x[32];
+  const uint32_t sw[8] = {sg0.x, sg0.y, sg0.z, sg0.w, sg1.x, sg1.y, sg1.z, sg1.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t r4[4] = {kraw[4 * i], kraw[4 * i + 1], kraw[4 * i + 2], kraw[4 * i + 3]};
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const uint32_t w = sw[2 * i + (d >> 1)];  // int8 signs of channels 8i + 4 (d / 2) .. + 3
+      const uint32_t m = (d & 1) ? (((w & 0x00800000u) >> 8) | (w & 0x80000000u))
+                                 : (((w & 0x00000080u) << 8) | ((w & 0x00008000u) << 16));
+      const uint32_t rr = r4[d] ^ m;
+      x[8 * i + 2 * d] = h2f(rr & 0xffffu);
+      x[8 * i + 2 * d + 1] = h2f(rr >> 16);
+    }
+  }
+  // fp16 norm: levels 64 and 32 across the quad, 16 .. 1 in the lane
+  float tt[32];
+#pragma unroll
+  for (int e = 0; e < 32; ++e) {
+    const float p = xchg<2>(x[e]);
+    tt[e] = x[e] * x[e] + p * p;
+  }
+#pragma unroll
+  for (int e = 0; e < 32; ++e) tt[e] = tt[e] + xchg<1>(tt[e]);
+#pragma unroll
+  for (int n = 16; n >= 1; n >>= 1) {
+#pragma unroll
+    for (int e = 0; e < n; ++e) tt[e] = tt[e] + tt[e + n];
+  }
+  const uint32_t n16 = norm_to_f16(sqrt_rn(tt[0]));
+#pragma unroll
+  for (int hh = 1; hh < 32; hh <<= 1) {
+#pragma unroll
+    for (int e = 0; e < 32; ++e) {
+      if ((e & hh) == 0) {
+        const float p = x[e], r = x[e + hh];
+        x[e] = p + r;
+        x[e + hh] = p - r;
+      }
+    }
+  }
+  quad_stage<1>(x, q);  // h = 32
+  quad_stage<2>(x, q);  // h = 64
+  const float cinv = (n16 == 0) ? 0.0f : div_rn(kKappa, h2f(n16));
+#pragma unroll
+  for (int e = 0; e < 32; ++e) x[e] = x[e] * cinv;
+  if (q == 0 && tok < npad) a.k_norm[seq * a.cap + tok] = valid ? (uint16_t)n16 : (uint16_t)0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    *reinterpret_cast<float4*>(&zt[t][32 * q + 4 * i]) = make_float4(x[4 * i], x[4 * i + 1], x[4 * i + 2], x[4 * i + 3]);
   if (restage) __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this thread's stage reads have landed
   __syncthreads();  // the direction tile is complete; every stage read of the work-group has landed
-  if (restage && stok >= begin && stok < len)
-    reinterpret_cast<uint4*>(a.stage + (seq * kW + t) * kD)[j] = (open == first) ? kraw : sraw;
-  if (tid < kD) {
+  if (restage && stok >= begin && stok < len) {
+    uint4* p = reinterpret_cast<uint4*>(a.stage + (seq * kW + t) * kD + 32 * q);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t* v = (open == first) ? &kraw[4 * i] : &sraw[4 * i];
+      p[i] = make_uint4(v[0], v[1], v[2], v[3]);
+    }
+  }
+  {  // thread = channel
+    const int c = tid;
     const int nv = min(len - w0, kW);
     float lo4[4], hi4[4];  // four independent chains (the minimum and maximum are exact in any order)
 #pragma unroll
@@ -253,7 +332,7 @@ __global__ __launch_bounds__(kWinThreads) void k_ladder_keys_win(LadderKeyArgs a
     }
 #pragma unroll
     for (int i = 0; i < kW; ++i) {  // all 32 reads in flight at once; slots past the length skipped
-      const float v = zt[i][tid];
+      const float v = zt[i][c];
       lo4[i & 3] = (i < nv) ? fminf(lo4[i & 3], v) : lo4[i & 3];
       hi4[i & 3] = (i < nv) ? fmaxf(hi4[i & 3], v) : hi4[i & 3];
     }
@@ -261,33 +340,29 @@ __global__ __launch_bounds__(kWinThreads) void k_ladder_keys_win(LadderKeyArgs a
     const float hi = fmaxf(fmaxf(hi4[0], hi4[1]), fmaxf(hi4[2], hi4[3])) + 0.0f;
     const float step = div_rn(hi - lo, (float)kTop);
     const uint32_t m16 = f2h(lo), s16 = f2h(step);
-    const size_t mi = (seq * (a.cap / kW) + w0 / kW) * kD + tid;
+    const size_t mi = (seq * (a.cap / kW) + w0 / kW) * kD + c;
     a.k_min[mi] = (uint16_t)m16;
     a.k_step[mi] = (uint16_t)s16;
     const float sv = h2f(s16);
-    kstat[tid] = make_float2(h2f(m16), (sv != 0.0f) ? div_rn(1.0f, sv) : 0.0f);
+    kstat[c] = make_float2(h2f(m16), (sv != 0.0f) ? div_rn(1.0f, sv) : 0.0f);
   }
   __syncthreads();  // the window's statistics
   if (tok >= npad) return;
-  uint32_t bits = 0;
+  uint32_t cw[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) cw[i] = 0u;
   if (valid) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float2 st = kstat[8 * j + e];
-      const float tt = (x[e] - st.x) * st.y;
-      const uint32_t code = (uint32_t)fminf(fmaxf(__builtin_rintf(tt), 0.0f), (float)kTop);
-      bits |= code << (kBits * e);
+    for (int e = 0; e < 32; ++e) {
+      const float2 st = kstat[32 * q + e];
+      const float tq = (x[e] - st.x) * st.y;
+      const uint32_t code = (uint32_t)fminf(fmaxf(__builtin_rintf(tq), 0.0f), (float)kTop);
+      cw[e >> 2] |= code << (8 * (e & 3));
     }
   }
-  uint8_t* row = a.k_codes + (seq * a.cap + tok) * kRowBytes + kBits * j;
-  if constexpr (kBits == 2) {
-    *reinterpret_cast<uint16_t*>(row) = (uint16_t)bits;
-  } else if constexpr (kBits == 4) {
-    *reinterpret_cast<uint32_t*>(row) = bits;
-  } else {
-#pragma unroll
-    for (int i = 0; i < kBits; ++i) row[i] = (uint8_t)(bits >> (8 * i));
-  }
+  uint32_t w[kBits];
+  pack32<kBits>(cw, w);
+  store_run<kBits>(a.k_codes + (seq * a.cap + tok) * kRowBytes, q, w);
 }
 
 __device__ __forceinline__ float tree_norm_lds(const float* xs) {  // xs: 128 floats (LDS)
@@ -557,7 +632,7 @@ hipError_t keys_for_bits(const LadderKeyArgs& a, bool tq, int nb, int max_len, h
     hipLaunchKernelGGL((k_ladder_keys<kBits, true>), grid, dim3(kTileTokens), 0, s, a);
   } else {
     const dim3 grid((max_len + kW - 1) / kW, a.H, nb);  // one work-group per key window of the span
-    hipLaunchKernelGGL(k_ladder_keys_win<kBits>, grid, dim3(kWinThreads), 0, s, a);
+    hipLaunchKernelGGL(k_ladder_keys_quad<kBits>, grid, dim3(kQuadThreads), 0, s, a);
   }
   return hipGetLastError();
 }
