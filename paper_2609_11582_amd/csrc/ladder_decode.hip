@@ -401,8 +401,13 @@ __global__ __launch_bounds__(64 * kLw) void k_ladder_decode(LadderDecodeArgs p) 
       const uint32_t nkw = (i < 2) ? lt.nk[tb].x : lt.nk[tb].y;
       const uint32_t nvw = (i < 2) ? lt.nv[tb].x : lt.nv[tb].y;
       const float nk = (i & 1) ? hi_h(nkw) : lo_h(nkw);
-      nvf[e] = ok ? ((i & 1) ? hi_h(nvw) : lo_h(nvw)) : 0.0f;
-      x[e] = ok ? nk * __builtin_fmaf(sc[tb][i], kinv, bias) : -__builtin_inff();
+      // computed for every slot and then selected (slots past the length hold whatever the norms'
+      // memory holds there): kept out of a branch per slot, which the compiler would otherwise form
+      float nvv = (i & 1) ? hi_h(nvw) : lo_h(nvw);
+      float xv = nk * __builtin_fmaf(sc[tb][i], kinv, bias);
+      __asm__ volatile("" : "+v"(nvv), "+v"(xv));
+      nvf[e] = ok ? nvv : 0.0f;
+      x[e] = ok ? xv : -__builtin_inff();
       if (!ok) mdv[tb] |= 0x03u << (8 * i);  // modality 3: no token
       mx = fmaxf(mx, x[e]);
     }
