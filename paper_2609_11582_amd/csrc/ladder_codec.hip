@@ -2,13 +2,13 @@
 // the K2V2 / K3V3 / K4V4 columns of Tab. 5), in the token-major bit-stream layout: a token's 128
 // codes form a little-endian bit stream, channel c at bits [b c, b c + b) of the token's 16 b bytes.
 //
-// Keys (one work-group of 128 threads per 128 tokens of a (sequence, KV head)): phase A, thread =
-// token, computes the direction in the key codec's bit-exact order (fp16 norm by the halving tree,
-// butterflies h = 1 .. 64, z = w fl(kappa / n16)); TurboQuant keys then take code = #{k : z_c >
-// tau_k} against the 2^b - 1 thresholds of the b-bit Gaussian codebook (Eq. 2, Eq. 3). The method's
-// keys (Eq. 4) go through an LDS tile: phase B, thread = channel, takes each window's minimum and
-// step (max - min) / (2^b - 1) in fp16 and the codes clamp(rint(fl(fl(z - m16) fl(1 / step16))), 0,
-// 2^b - 1); phase C, thread = token, packs its row.
+// Keys: the direction in the key codec's bit-exact order (fp16 norm by the halving tree,
+// butterflies h = 1 .. 64, z = w fl(kappa / n16)). TurboQuant keys (one work-group of 128 threads
+// per 128 tokens, thread = token) take code = #{k : z_c > tau_k} against the 2^b - 1 thresholds of
+// the b-bit Gaussian codebook (Eq. 2, Eq. 3), straight from registers. The method's keys (Eq. 4;
+// one work-group of 128 threads per 32-token window, four lanes per token) take each window's
+// minimum and step (max - min) / (2^b - 1) in fp16 through an LDS tile and the codes
+// clamp(rint(fl(fl(z - m16) fl(1 / step16))), 0, 2^b - 1).
 //
 // Values, exact mode (one work-group of 128 threads, thread = output channel, per 32-token window): the
 // exact-mode order of the 2-bit codec -- y_c = sum_j fl(R_cj v_j) left to right in fp32, n16 by the
@@ -46,12 +46,10 @@ __device__ __forceinline__ void store_run(uint8_t* row, int part, const uint32_t
   for (int i = 0; i < kBits; ++i) p[i] = w[i];
 }
 
-template <int kBits, bool kTq>
-__global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
+template <int kBits>
+__global__ __launch_bounds__(kTileTokens) void k_ladder_keys_tq(LadderKeyArgs a) {
   constexpr int kTop = (1 << kBits) - 1;
   constexpr int kRowBytes = 16 * kBits;
-  __shared__ float zt[kTileTokens][kD + 1];                              // directions (method keys)
-  __shared__ __attribute__((aligned(16))) uint8_t ct[kTileTokens][kD];  // codes
   const int h = blockIdx.y, bz = blockIdx.z, b = a.b0 + bz;
   int begin = 0, len = a.lens.lens[bz];
   if (a.begin_dev) {  // append: the device lengths decide, clamped into the buffers
@@ -59,22 +57,20 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
     len = min(begin + min(max(a.count_dev[b], 0), a.n_rows), a.cap);
     if (len <= begin) return;  // uniform
   }
-  // the method's keys requantize the whole open window, TurboQuant keys only the new tokens
-  const int first = kTq ? begin : (begin / kW) * kW;
-  const int t0 = first + kTileTokens * blockIdx.x;
+  // TurboQuant keys are per token: only the new tokens are coded
+  const int t0 = begin + kTileTokens * blockIdx.x;
   if (t0 >= len) return;  // uniform over the work-group
   const int t = threadIdx.x, tok = t0 + t;
   const bool valid = tok < len;
   const int npad = (len + kW - 1) / kW * kW;  // slots of every window holding a valid token
   const size_t seq = (size_t)b * a.H + h;
 
-  // ---- phase A (thread = token): the direction, in registers ----
+  // ---- the direction, in registers (thread = token) ----
   uint32_t sw[32];
   load_sign_words(a.signs, sw);
   uint32_t raw[64];
-  if (valid) {  // older tokens of the open window (append, method keys) from the stage
-    load_row_f16(tok < begin ? a.stage + (seq * kW + (tok - first)) * kD : a.k + (seq * a.n_rows + (tok - begin)) * kD,
-                 raw);
+  if (valid) {
+    load_row_f16(a.k + (seq * a.n_rows + (tok - begin)) * kD, raw);
   } else {
 #pragma unroll
     for (int i = 0; i < 64; ++i) raw[i] = 0u;
@@ -98,91 +94,25 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
   for (int c = 0; c < kD; ++c) x[c] = x[c] * cinv;
   if (tok < npad) a.k_norm[seq * a.cap + tok] = valid ? (uint16_t)n16 : (uint16_t)0;
 
-  if constexpr (kTq) {
-    // ---- TurboQuant: nearest level of the b-bit codebook, packed straight from registers ----
-    if (tok >= npad) return;
-    uint8_t* row = a.k_codes + (seq * a.cap + tok) * kRowBytes;
+  // ---- nearest level of the b-bit codebook, packed straight from registers ----
+  if (tok >= npad) return;
+  uint8_t* row = a.k_codes + (seq * a.cap + tok) * kRowBytes;
 #pragma unroll
-    for (int part = 0; part < 4; ++part) {
-      uint32_t cw[8];
+  for (int part = 0; part < 4; ++part) {
+    uint32_t cw[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) cw[i] = 0u;
+    for (int i = 0; i < 8; ++i) cw[i] = 0u;
 #pragma unroll
-      for (int c = 0; c < 32; ++c) {
-        const float z = x[32 * part + c];
-        uint32_t code = 0;
+    for (int c = 0; c < 32; ++c) {
+      const float z = x[32 * part + c];
+      uint32_t code = 0;
 #pragma unroll
-        for (int k = 0; k < kTop; ++k) code += (uint32_t)(z > a.tau[k]);
-        cw[c >> 2] |= (valid ? code : 0u) << (8 * (c & 3));
-      }
-      uint32_t w[kBits];
-      pack32<kBits>(cw, w);
-      store_run<kBits>(row, part, w);
+      for (int k = 0; k < kTop; ++k) code += (uint32_t)(z > a.tau[k]);
+      cw[c >> 2] |= (valid ? code : 0u) << (8 * (c & 3));
     }
-    return;
-  } else {
-#pragma unroll
-    for (int c = 0; c < kD; ++c) zt[t][c] = x[c];
-    __syncthreads();
-    if (a.stage && blockIdx.x == 0) {
-      // Append: the raw rows of the new open window [open, len) into the stage. Only this
-      // work-group reads the stage (its rows [first, begin) lie in tile 0), and its reads are done;
-      // rows below begin (open == first) are in the stage already.
-      const int open = (len / kW) * kW;
-      for (int idx = t; idx < kW * 16; idx += kTileTokens) {
-        const int slot = idx >> 4, part = idx & 15, st = open + slot;
-        if (st >= begin && st < len)
-          reinterpret_cast<uint4*>(a.stage + (seq * kW + slot) * kD)[part] =
-              reinterpret_cast<const uint4*>(a.k + (seq * a.n_rows + (st - begin)) * kD)[part];
-      }
-    }
-
-    // ---- phase B (thread = channel): window minimum and step, then the codes ----
-    const int c = t;
-    const size_t nwcap = a.cap / kW;
-    for (int w = 0; w < kTileTokens / kW; ++w) {
-      const int wt0 = t0 + kW * w;
-      if (wt0 >= len) break;  // uniform
-      const int nv = min(len - wt0, kW);
-      float lo = __builtin_inff(), hi = -__builtin_inff();
-#pragma unroll
-      for (int i = 0; i < kW; ++i) {  // all 32 reads in flight at once; slots past the length skipped
-        const float v = zt[kW * w + i][c];
-        lo = (i < nv) ? fminf(lo, v) : lo;
-        hi = (i < nv) ? fmaxf(hi, v) : hi;
-      }
-      lo = lo + 0.0f;  // -0 -> +0
-      hi = hi + 0.0f;
-      const float step = div_rn(hi - lo, (float)kTop);
-      const uint32_t m16 = f2h(lo), s16 = f2h(step);
-      const size_t mi = (seq * nwcap + wt0 / kW) * kD + c;
-      a.k_min[mi] = (uint16_t)m16;
-      a.k_step[mi] = (uint16_t)s16;
-      const float m = h2f(m16), s = h2f(s16);
-      const float inv = (s != 0.0f) ? div_rn(1.0f, s) : 0.0f;
-#pragma unroll
-      for (int i = 0; i < kW; ++i) {  // branch-free: the reads go out together
-        const float tt = (zt[kW * w + i][c] - m) * inv;
-        const uint32_t code = (uint32_t)fminf(fmaxf(__builtin_rintf(tt), 0.0f), (float)kTop);
-        ct[kW * w + i][c] = (uint8_t)((i < nv && s != 0.0f) ? code : 0u);
-      }
-    }
-    __syncthreads();
-
-    // ---- phase C (thread = token): pack the row ----
-    if (tok >= npad) return;
-    uint8_t* row = a.k_codes + (seq * a.cap + tok) * kRowBytes;
-#pragma unroll
-    for (int part = 0; part < 4; ++part) {
-      uint32_t cw[8];
-      const uint4* src = reinterpret_cast<const uint4*>(&ct[t][32 * part]);
-      const uint4 u0 = src[0], u1 = src[1];
-      cw[0] = u0.x; cw[1] = u0.y; cw[2] = u0.z; cw[3] = u0.w;
-      cw[4] = u1.x; cw[5] = u1.y; cw[6] = u1.z; cw[7] = u1.w;
-      uint32_t w[kBits];
-      pack32<kBits>(cw, w);
-      store_run<kBits>(row, part, w);
-    }
+    uint32_t w[kBits];
+    pack32<kBits>(cw, w);
+    store_run<kBits>(row, part, w);
   }
 }
 
@@ -195,7 +125,7 @@ __global__ __launch_bounds__(kTileTokens) void k_ladder_keys(LadderKeyArgs a) {
 // thread c then takes channel c's window minimum and maximum over the valid tokens (exact in any
 // order) and forms the fp16 minimum, step = (max - min) / (2^b - 1) and fl(1 / step16); every thread
 // codes its 32 channels, clamp(rint(fl(fl(z - m16) fl(1 / step16))), 0, 2^b - 1), which fill b
-// dwords of the token's bit stream (the run at dword b q). TurboQuant keys keep the token-per-thread
+// dwords of the token's bit stream (the run at dword b q). TurboQuant keys take the token-per-thread
 // kernel above, which needs no window statistics.
 constexpr int kQuadThreads = 128;
 constexpr int kWinPitch = kD + 4;  // floats per token row of the direction tile
@@ -629,7 +559,7 @@ template <int kBits>
 hipError_t keys_for_bits(const LadderKeyArgs& a, bool tq, int nb, int max_len, hipStream_t s) {
   if (tq) {
     const dim3 grid((max_len + kTileTokens - 1) / kTileTokens, a.H, nb);
-    hipLaunchKernelGGL((k_ladder_keys<kBits, true>), grid, dim3(kTileTokens), 0, s, a);
+    hipLaunchKernelGGL(k_ladder_keys_tq<kBits>, grid, dim3(kTileTokens), 0, s, a);
   } else {
     const dim3 grid((max_len + kW - 1) / kW, a.H, nb);  // one work-group per key window of the span
     hipLaunchKernelGGL(k_ladder_keys_quad<kBits>, grid, dim3(kQuadThreads), 0, s, a);

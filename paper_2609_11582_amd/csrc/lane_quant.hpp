@@ -1,8 +1,8 @@
 // Key directions with a token spread over the 16 lanes of a DPP row: lane j holds channels 8j ..
 // 8j + 7. The norm, the butterflies and the scaling run in the key codec's bit-exact order (the
 // halving tree, stages h = 1 .. 64, z = w fl(kappa / n16)); the levels and stages that pair a
-// channel with one 8 or more apart cross lanes by DPP. Shared by the window-parallel append and
-// the window-parallel key codec of the bit-width ladder.
+// channel with one 8 or more apart cross lanes by DPP. Used by the window-parallel append; the
+// bit-width ladder's key codec (four lanes per token) uses its DPP exchanges.
 #pragma once
 
 #include "key_quant.hpp"
