@@ -167,8 +167,13 @@ __global__ __launch_bounds__(kQuadThreads) void k_ladder_keys_quad(LadderKeyArgs
   const size_t srow = seq * a.n_rows;
   const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
   const uint4* kp = reinterpret_cast<const uint4*>(a.k + (srow + (size_t)min(max(tok - begin, 0), last)) * kD + 32 * q);
-  const uint4* stp = reinterpret_cast<const uint4*>(a.stage + (seq * kW + max(min(t, begin - first - 1), 0)) * kD + 32 * q);
-  const uint4* ssp = reinterpret_cast<const uint4*>(a.k + (srow + (size_t)min(max(stok - begin, 0), last)) * kD + 32 * q);
+  // the stage (only where it holds older tokens: the stage may be absent otherwise) and the open
+  // window's rows (only where the new open window starts after this one)
+  const uint4* stp = staged ? reinterpret_cast<const uint4*>(a.stage + (seq * kW + min(t, begin - first - 1)) * kD + 32 * q)
+                            : kp;
+  const uint4* ssp = (restage && open != first)
+                         ? reinterpret_cast<const uint4*>(a.k + (srow + (size_t)min(max(stok - begin, 0), last)) * kD + 32 * q)
+                         : kp;
   const bool fresh = valid && tok >= begin, old = staged && tok < begin;
   // kraw: the token's 32 keys (from the stage below begin, zero past the length); sraw: those of
   // token open + t, for the stage
