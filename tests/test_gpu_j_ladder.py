@@ -1,6 +1,7 @@
 """GPU parity of the bit-width ladder (b-bit keys and values, b = 2, 3, 4; Tab. 3 K3/V2, Tab. 5
 K2V2 / K3V3 / K4V4) against oracle.ladder: key codes, window metadata and norms bit-exact (the
-method's keys and TurboQuant keys, every width, ragged and degenerate rows), value codes and norms
+method's keys and TurboQuant keys, every width, ragged and degenerate rows, and the benchmark layer
+at full size), value codes and norms
 bit-exact in the exact fp32 order and within the rotation band in the matrix-core mode, and decode within 2e-3 of the output norm -- over the GPU-written
 cache and end to end against the oracle-written one -- for several width pairs, ragged GQA 7 with
 an empty sequence, and the benchmark layer (4 KV heads, 28 query heads, 32768 tokens)."""
@@ -52,6 +53,46 @@ def test_ladder_codes_bit_exact(bits, meta):
     ref = quantize_layer_bits(k, v, lay["modality"], lens, lay["signs"], lay["rot"], cap, bits, bits, meta)
     for name in ref:
         _same(got[name], ref[name], name)
+
+
+@pytest.mark.parametrize("bits,meta", [(2, "fp16"), (3, "fp16"), (4, "fp16"), (3, "turboquant"), (4, "turboquant")],
+                         ids=["K2_fp16", "K3_fp16", "K4_fp16", "K3_tq", "K4_tq"])
+def test_ladder_keys_full_size_bit_exact(bits, meta):
+    """The benchmark layer (32768 tokens, 4 KV heads) through the stateless key call the benchmark
+    times: codes, window minimum / step and norms of KV heads 0 and 3 equal the oracle's bytes."""
+    import gpu_helpers as gh
+    import paper_2609_11582_amd as okvq
+    import torch
+    from oracle.ladder import pack_bits, quantize_keys_bits_fmt, quantize_keys_tq_bits_fmt
+    wl = workload("omni7b_32k")
+    lay = gen_layer(wl, 0)
+    lens = [int(x) for x in lay["lens"]]
+    B, H, N, _ = lay["k"].shape
+    _announce(f"ladder keys full size K{bits} {meta} lens={lens}")
+    cache = okvq.KVCache(B, H, 28, wl.capacity, torch.from_numpy(lay["signs"]),
+                         torch.from_numpy(np.ascontiguousarray(lay["rot"], np.float32)), key_meta=meta,
+                         key_bits=bits, value_bits=bits)
+    vw = cache.views()
+    kd = gh.f16dev(lay["k"])
+    if meta == "fp16":
+        okvq.okvq_quantize_keys(cache.dims, kd, N, lens, cache.key_signs, vw["k_codes"], vw["k_min"], vw["k_step"],
+                                vw["k_norm"])
+    else:
+        okvq.okvq_quantize_keys_tq(cache.dims, kd, N, lens, cache.key_signs, vw["k_codes"], vw["k_norm"])
+    torch.cuda.synchronize()
+    got = _arrays(cache)
+    for b, L in enumerate(lens):
+        for h in (0, 3):
+            if meta == "fp16":
+                kq = quantize_keys_bits_fmt(lay["k"][b, h], L, lay["signs"], bits)
+                nwl = kq["codes"].shape[0] // 32
+                _same(got["k_min"][b, h, :nwl], kq["m16"], f"k_min[{b},{h}]")
+                _same(got["k_step"][b, h, :nwl], kq["step16"], f"k_step[{b},{h}]")
+            else:
+                kq = quantize_keys_tq_bits_fmt(lay["k"][b, h], L, lay["signs"], bits)
+            npad = kq["codes"].shape[0]
+            _same(got["k_codes"][b, h, :npad], pack_bits(kq["codes"], bits), f"k_codes[{b},{h}]")
+            _same(got["k_norm"][b, h, :npad], kq["n16"], f"k_norm[{b},{h}]")
 
 
 CASES = [(2, 2, "fp16"), (3, 3, "fp16"), (4, 4, "fp16"), (3, 2, "turboquant"), (4, 4, "turboquant"),
