@@ -95,6 +95,34 @@ def test_ladder_keys_full_size_bit_exact(bits, meta):
             _same(got["k_norm"][b, h, :npad], kq["n16"], f"k_norm[{b},{h}]")
 
 
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_ladder_values_full_size_matrix_core(bits):
+    """The benchmark layer (32768 tokens) through the stateless value call in the matrix-core mode the
+    benchmark times: KV head 3's norms bit-exact and its codes within the band rule of the exact
+    order (the modality map of the workload, audio runs inside video chunks and the text tail)."""
+    import gpu_helpers as gh
+    import paper_2609_11582_amd as okvq
+    import torch
+    from oracle.ladder import quantize_values_bits_fmt
+    wl = workload("omni7b_32k")
+    lay = gen_layer(wl, 0)
+    lens = [int(x) for x in lay["lens"]]
+    B, H, N, _ = lay["v"].shape
+    _announce(f"ladder values full size V{bits} lens={lens}")
+    cache = okvq.KVCache(B, H, 28, wl.capacity, torch.from_numpy(lay["signs"]),
+                         torch.from_numpy(np.ascontiguousarray(lay["rot"], np.float32)), key_bits=bits, value_bits=bits)
+    vw = cache.views()
+    okvq.okvq_quantize_values(cache.dims, gh.f16dev(lay["v"]), gh.dev(np.ascontiguousarray(lay["modality"], np.uint8)), N,
+                              lens, cache.v_rot, 0, vw["v_codes"], vw["v_norm"])
+    torch.cuda.synchronize()
+    got = _arrays(cache)
+    b, h, L = 0, 3, lens[0]
+    ref = quantize_values_bits_fmt(lay["v"][b, h], lay["modality"][b], lay["rot"], L, bits)
+    _same(got["v_norm"][b, h, :L], ref["n16"], "v_norm")
+    diff, band = gh.band_compare_bits(got["v_codes"][b, h], lay["v"][b, h], lay["modality"][b], lay["rot"], L, bits)
+    print(f"V{bits} full size: {diff} codes differ, {band} in the band", flush=True)
+
+
 CASES = [(2, 2, "fp16"), (3, 3, "fp16"), (4, 4, "fp16"), (3, 2, "turboquant"), (4, 4, "turboquant"),
          (2, 4, "fp16"), (4, 3, "turboquant")]
 
