@@ -170,7 +170,8 @@ def test_ladder_decode_several_windows_per_wave(kb, vb, meta):
     assert r <= TOL
 
 
-@pytest.mark.parametrize("kb,vb,meta", [(4, 4, "fp16"), (3, 2, "turboquant")], ids=["K4V4_fp16", "K3V2_tq"])
+@pytest.mark.parametrize("kb,vb,meta", [(2, 2, "fp16"), (4, 4, "fp16"), (3, 2, "turboquant")],
+                         ids=["K2V2_fp16", "K4V4_fp16", "K3V2_tq"])
 def test_ladder_decode_full_size(kb, vb, meta):
     """The benchmark layer: every query head of two KV heads against the oracle."""
     import gpu_helpers as gh
